@@ -1,0 +1,391 @@
+/*
+ * nopfs_ref.c -- CPU oracle for the clairvoyant planning path of NoPFS
+ * (Dryden, Boehringer, Ben-Nun, Hoefler, "Clairvoyant Prefetching for
+ * Distributed Machine Learning I/O", SC'21).
+ *
+ * TEST INFRASTRUCTURE ONLY. Plain, slow, single-threaded C. It is called by
+ * the test suite, the smoke check and the benchmark's CPU-baseline leg, and by
+ * nothing in the product path. It shares no source with the GPU library.
+ *
+ * Every stage is written as the plain definition, in the paper's order:
+ *   keys   -> one 32-bit Philox-4x32-10 word per (epoch, sample)
+ *   perm   -> samples sorted by (key, id)        (Background: one shuffle per
+ *             epoch, every sample exactly once, reproducible from the seed)
+ *   shard  -> worker i reads global positions p = i (mod N) of each epoch, in
+ *             order, giving its access stream R (Performance Modeling: the
+ *             batches B^h, the worker batches B^{h,i} and the stream R)
+ *   stats  -> per (worker, sample): number of reads and first read position
+ *             (Distribution of Accesses: the access frequency X / r_k)
+ *   next   -> per stream position: the next position reading the same sample
+ *             (I/O Access Patterns: Belady's rule needs the next use)
+ *   plan   -> per worker, samples ranked by frequency, then poured into the
+ *             storage classes fastest first until full (Design, last steps)
+ *
+ * Readings where the paper is silent (each is stated where it is used):
+ *   - keys are Philox-4x32-10 words: counter (k/4, e, 0, 0), key (seed lo,
+ *     seed hi), word k%4; equal keys are ordered by the smaller sample id;
+ *   - ids, epochs and positions are 0-based;
+ *   - B is the per-worker batch; the global batch is N*B;
+ *   - worker i takes global positions p with p % N == i (strided split);
+ *   - drop_last=1 issues the first T*N*B positions of each epoch; with
+ *     drop_last=0 every position is issued and rows are padded with -1;
+ *   - "first" and "next" are positions in the worker's own stream, -1 = never;
+ *   - the plan ranks by (count desc, first asc with never = +inf, id asc),
+ *     fills tier 0, then tier 1, ..., stopping each tier at its first misfit;
+ *     samples never read by a worker are ranked last, by id, and still placed.
+ */
+#include "nopfs_ref.h"
+
+#include <stdlib.h>
+#include <string.h>
+
+#define REF_EINVAL (-1)
+#define REF_ERANGE (-2)
+#define REF_ENOMEM (-3)
+
+/* ------------------------------------------------------------------------ */
+/* Philox-4x32-10, from the description in Salmon et al., SC'11:             */
+/* each round multiplies words 0 and 2 by two fixed 32-bit constants, takes  */
+/* the high halves, XORs them with the other two words and the round key,    */
+/* and the round key is bumped by two Weyl constants between rounds.         */
+/* ------------------------------------------------------------------------ */
+#define PHILOX_M0 0xD2511F53u
+#define PHILOX_M1 0xCD9E8D57u
+#define PHILOX_W0 0x9E3779B9u
+#define PHILOX_W1 0xBB67AE85u
+
+void nopfs_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
+                             uint32_t out[4]) {
+  uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    uint64_t p0 = (uint64_t)PHILOX_M0 * x0;
+    uint64_t p1 = (uint64_t)PHILOX_M1 * x2;
+    uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    uint32_t y0 = hi1 ^ x1 ^ k0;
+    uint32_t y1 = lo1;
+    uint32_t y2 = hi0 ^ x3 ^ k1;
+    uint32_t y3 = lo0;
+    x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+    k0 += PHILOX_W0;
+    k1 += PHILOX_W1;
+  }
+  out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Shape (Performance Modeling: T iterations per epoch, floor or ceil of    */
+/* F over the global batch; worker batches partition each global batch).    */
+/* ------------------------------------------------------------------------ */
+static int check_job(const nopfs_ref_job* job) {
+  if (!job) return REF_EINVAL;
+  if (job->F < 1 || job->E < 1 || job->N < 1 || job->B < 1) return REF_EINVAL;
+  if (job->drop_last != 0 && job->drop_last != 1) return REF_EINVAL;
+  if (job->F >= ((int64_t)1 << 31) || job->E > 255) return REF_ERANGE;
+  return 0;
+}
+
+/* Length of worker i's stream in one epoch. */
+static int64_t epoch_len(const nopfs_ref_job* job, int64_t i) {
+  int64_t F = job->F, N = job->N, B = job->B;
+  if (job->drop_last) {
+    int64_t T = F / (N * B);
+    return T * B;
+  }
+  if (i >= F) return 0;
+  return (F - i + N - 1) / N; /* positions p < F with p % N == i */
+}
+
+/* Number of positions of each epoch that are actually read. */
+static int64_t issued(const nopfs_ref_job* job) {
+  int64_t F = job->F, N = job->N, B = job->B;
+  if (job->drop_last) return (F / (N * B)) * N * B;
+  return F;
+}
+
+int nopfs_ref_stream_shape(const nopfs_ref_job* job, int64_t* T, int64_t* M_max,
+                           int64_t* M_per_worker) {
+  int rc = check_job(job);
+  if (rc) return rc;
+  int64_t F = job->F, N = job->N, B = job->B, E = job->E;
+  int64_t t = job->drop_last ? F / (N * B) : (F + N * B - 1) / (N * B);
+  int64_t mmax = 0;
+  for (int64_t i = 0; i < N; ++i) {
+    int64_t m = E * epoch_len(job, i);
+    if (m > mmax) mmax = m;
+    if (M_per_worker) M_per_worker[i] = m;
+  }
+  if (mmax >= ((int64_t)1 << 31)) return REF_ERANGE;
+  if (T) *T = t;
+  if (M_max) *M_max = mmax;
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Keys and the epoch permutation (Background: each epoch is a random       */
+/* shuffle of all sample indices, and knowing the seed reproduces it).      */
+/* ------------------------------------------------------------------------ */
+int nopfs_ref_epoch_keys(const nopfs_ref_job* job, int32_t e, uint32_t* keys) {
+  int rc = check_job(job);
+  if (rc) return rc;
+  if (!keys || e < 0 || e >= job->E) return REF_EINVAL;
+  uint32_t key[2] = {(uint32_t)job->seed, (uint32_t)(job->seed >> 32)};
+  for (int64_t k = 0; k < job->F; ++k) {
+    uint32_t ctr[4] = {(uint32_t)(k >> 2), (uint32_t)e, 0u, 0u};
+    uint32_t out[4];
+    nopfs_ref_philox4x32_10(ctr, key, out);
+    keys[k] = out[k & 3];
+  }
+  return 0;
+}
+
+typedef struct { uint32_t key; int32_t id; } keyed_t;
+
+static int cmp_keyed(const void* a, const void* b) {
+  const keyed_t* x = (const keyed_t*)a;
+  const keyed_t* y = (const keyed_t*)b;
+  if (x->key != y->key) return x->key < y->key ? -1 : 1;
+  if (x->id != y->id) return x->id < y->id ? -1 : 1;
+  return 0;
+}
+
+int nopfs_ref_epoch_perm(const nopfs_ref_job* job, int32_t e, int32_t* perm) {
+  int rc = check_job(job);
+  if (rc) return rc;
+  if (!perm || e < 0 || e >= job->E) return REF_EINVAL;
+  int64_t F = job->F;
+  uint32_t* keys = (uint32_t*)malloc((size_t)F * sizeof(uint32_t));
+  keyed_t* rec = (keyed_t*)malloc((size_t)F * sizeof(keyed_t));
+  if (!keys || !rec) { free(keys); free(rec); return REF_ENOMEM; }
+  nopfs_ref_epoch_keys(job, e, keys);
+  for (int64_t k = 0; k < F; ++k) { rec[k].key = keys[k]; rec[k].id = (int32_t)k; }
+  qsort(rec, (size_t)F, sizeof(keyed_t), cmp_keyed);
+  for (int64_t p = 0; p < F; ++p) perm[p] = rec[p].id;
+  free(keys);
+  free(rec);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Shard (Performance Modeling: B^{h,1..N} partition B^h, and worker i's    */
+/* stream R is the concatenation of its local batches in iteration order).  */
+/* With the strided split, the j-th read of worker i in epoch e is global    */
+/* position p = j*N + i, and it lands at stream position e*L_i + j.          */
+/* ------------------------------------------------------------------------ */
+static void shard_epoch(const nopfs_ref_job* job, int32_t e, const int32_t* perm,
+                        int64_t M_max, int32_t* R) {
+  int64_t N = job->N, P = issued(job);
+  for (int64_t p = 0; p < P; ++p) {
+    int64_t i = p % N, j = p / N;
+    int64_t L = epoch_len(job, i);
+    R[i * M_max + (int64_t)e * L + j] = perm[p];
+  }
+}
+
+static void pad_rows(const nopfs_ref_job* job, int64_t M_max, int32_t* R) {
+  for (int64_t i = 0; i < job->N; ++i) {
+    int64_t M = (int64_t)job->E * epoch_len(job, i);
+    for (int64_t f = M; f < M_max; ++f) R[i * M_max + f] = -1;
+  }
+}
+
+int nopfs_ref_streams_from_perms(const nopfs_ref_job* job, const int32_t* perms,
+                                 int32_t* R) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!perms || !R) return REF_EINVAL;
+  pad_rows(job, M_max, R);
+  for (int32_t e = 0; e < job->E; ++e)
+    shard_epoch(job, e, perms + (int64_t)e * job->F, M_max, R);
+  return 0;
+}
+
+int nopfs_ref_access_streams(const nopfs_ref_job* job, int32_t* R) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!R) return REF_EINVAL;
+  int32_t* perm = (int32_t*)malloc((size_t)job->F * sizeof(int32_t));
+  if (!perm) return REF_ENOMEM;
+  pad_rows(job, M_max, R);
+  for (int32_t e = 0; e < job->E; ++e) {
+    rc = nopfs_ref_epoch_perm(job, e, perm);
+    if (rc) break;
+    shard_epoch(job, e, perm, M_max, R);
+  }
+  free(perm);
+  return rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Access statistics (Distribution of Accesses: the number of times a       */
+/* worker reads a sample over all E epochs; the first read time is kept so  */
+/* the plan can order equally frequent samples).                            */
+/* ------------------------------------------------------------------------ */
+int nopfs_ref_access_stats(const nopfs_ref_job* job, const int32_t* R,
+                           uint8_t* count, int32_t* first) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!R || !count || !first) return REF_EINVAL;
+  int64_t F = job->F;
+  for (int64_t i = 0; i < job->N; ++i) {
+    uint8_t* c = count + i * F;
+    int32_t* fi = first + i * F;
+    for (int64_t k = 0; k < F; ++k) { c[k] = 0; fi[k] = -1; }
+    int64_t M = (int64_t)job->E * epoch_len(job, i);
+    for (int64_t f = 0; f < M; ++f) {
+      int32_t k = R[i * M_max + f];
+      if (k < 0 || k >= F) return REF_EINVAL;
+      if (c[k] == 0) fi[k] = (int32_t)f;
+      c[k] += 1;
+    }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Next use (I/O Access Patterns: the optimal replacement discards the      */
+/* sample whose next use is furthest; the next use is found by walking the  */
+/* stream backwards and remembering the last position seen per sample).     */
+/* ------------------------------------------------------------------------ */
+int nopfs_ref_reuse_next(const nopfs_ref_job* job, const int32_t* R,
+                         int32_t* next) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!R || !next) return REF_EINVAL;
+  int64_t F = job->F;
+  int32_t* last = (int32_t*)malloc((size_t)F * sizeof(int32_t));
+  if (!last) return REF_ENOMEM;
+  for (int64_t i = 0; i < job->N; ++i) {
+    for (int64_t k = 0; k < F; ++k) last[k] = -1;
+    int64_t M = (int64_t)job->E * epoch_len(job, i);
+    for (int64_t f = M; f < M_max; ++f) next[i * M_max + f] = -1;
+    for (int64_t f = M - 1; f >= 0; --f) {
+      int32_t k = R[i * M_max + f];
+      if (k < 0 || k >= F) { free(last); return REF_EINVAL; }
+      next[i * M_max + f] = last[k];
+      last[k] = (int32_t)f;
+    }
+  }
+  free(last);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Tier plan (Design: a worker caches the samples with the largest access    */
+/* frequency r_k in its fastest storage class, then the next class, and so  */
+/* on, until the dataset is cached or local storage is full).               */
+/* ------------------------------------------------------------------------ */
+typedef struct { int32_t count; int64_t first; int32_t id; } ranked_t;
+
+static int cmp_ranked(const void* a, const void* b) {
+  const ranked_t* x = (const ranked_t*)a;
+  const ranked_t* y = (const ranked_t*)b;
+  if (x->count != y->count) return x->count > y->count ? -1 : 1;  /* desc */
+  if (x->first != y->first) return x->first < y->first ? -1 : 1;  /* asc  */
+  if (x->id != y->id) return x->id < y->id ? -1 : 1;              /* asc  */
+  return 0;
+}
+
+int nopfs_ref_tier_plan(const nopfs_ref_job* job, const uint8_t* count,
+                        const int32_t* first, const int64_t* sizes,
+                        const int64_t* caps, int32_t J, int8_t* tier,
+                        int64_t* used) {
+  int rc = check_job(job);
+  if (rc) return rc;
+  if (!count || !first || !sizes || !caps || !tier || !used) return REF_EINVAL;
+  if (J < 1) return REF_EINVAL;
+  if (J > 127) return REF_ERANGE;
+  for (int32_t j = 0; j < J; ++j)
+    if (caps[j] < 0) return REF_EINVAL;
+  int64_t F = job->F;
+  ranked_t* order = (ranked_t*)malloc((size_t)F * sizeof(ranked_t));
+  if (!order) return REF_ENOMEM;
+  for (int64_t i = 0; i < job->N; ++i) {
+    for (int64_t k = 0; k < F; ++k) {
+      order[k].count = count[i * F + k];
+      order[k].first = first[i * F + k] >= 0 ? first[i * F + k] : INT64_MAX;
+      order[k].id = (int32_t)k;
+    }
+    qsort(order, (size_t)F, sizeof(ranked_t), cmp_ranked);
+    int64_t pos = 0;
+    for (int32_t j = 0; j < J; ++j) {
+      int64_t u = 0;
+      while (pos < F && u + sizes[order[pos].id] <= caps[j]) {
+        tier[i * F + order[pos].id] = (int8_t)j;
+        u += sizes[order[pos].id];
+        pos++;
+      }
+      used[i * J + j] = u;
+    }
+    for (int64_t q = pos; q < F; ++q) tier[i * F + order[q].id] = -1;
+  }
+  free(order);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sampled columns. The position of sample s in epoch e is, by definition   */
+/* of the sorted order, the number of samples whose (key, id) is smaller.   */
+/* Everything else for s follows from its positions in the E epochs.        */
+/* ------------------------------------------------------------------------ */
+int nopfs_ref_sample_columns(const nopfs_ref_job* job, const int32_t* samples,
+                             int64_t S, int64_t* pos, int32_t* occ_worker,
+                             int32_t* occ_f, int32_t* occ_next,
+                             uint8_t* col_count, int32_t* col_first) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!samples || S < 0 || !pos || !occ_worker || !occ_f || !occ_next ||
+      !col_count || !col_first)
+    return REF_EINVAL;
+  int64_t F = job->F, N = job->N, E = job->E, P = issued(job);
+  for (int64_t s = 0; s < S; ++s)
+    if (samples[s] < 0 || samples[s] >= F) return REF_EINVAL;
+  uint32_t* keys = (uint32_t*)malloc((size_t)F * sizeof(uint32_t));
+  if (!keys) return REF_ENOMEM;
+  for (int32_t e = 0; e < E; ++e) {
+    nopfs_ref_epoch_keys(job, e, keys);
+    for (int64_t s = 0; s < S; ++s) {
+      int64_t ks = samples[s];
+      uint32_t key_s = keys[ks];
+      int64_t smaller = 0;
+      for (int64_t k = 0; k < F; ++k)
+        smaller += (keys[k] < key_s) | ((keys[k] == key_s) & (k < ks));
+      pos[e * S + s] = smaller;
+    }
+  }
+  free(keys);
+  for (int64_t i = 0; i < N; ++i)
+    for (int64_t s = 0; s < S; ++s) {
+      col_count[i * S + s] = 0;
+      col_first[i * S + s] = -1;
+    }
+  for (int32_t e = 0; e < E; ++e)
+    for (int64_t s = 0; s < S; ++s) {
+      int64_t p = pos[e * S + s];
+      if (p >= P) { occ_worker[e * S + s] = -1; occ_f[e * S + s] = -1; continue; }
+      int64_t i = p % N, j = p / N;
+      int64_t f = (int64_t)e * epoch_len(job, i) + j;
+      occ_worker[e * S + s] = (int32_t)i;
+      occ_f[e * S + s] = (int32_t)f;
+      if (col_count[i * S + s] == 0) col_first[i * S + s] = (int32_t)f;
+      col_count[i * S + s] += 1;
+    }
+  for (int32_t e = 0; e < E; ++e)
+    for (int64_t s = 0; s < S; ++s) {
+      int32_t nx = -1;
+      if (occ_worker[e * S + s] >= 0)
+        for (int32_t e2 = e + 1; e2 < E; ++e2)
+          if (occ_worker[e2 * S + s] == occ_worker[e * S + s]) {
+            nx = occ_f[e2 * S + s];
+            break;
+          }
+      occ_next[e * S + s] = nx;
+    }
+  return 0;
+}

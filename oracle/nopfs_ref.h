@@ -1,0 +1,85 @@
+/*
+ * nopfs_ref.h -- the CPU oracle for clairvoyant access planning.
+ *
+ * TEST INFRASTRUCTURE. This library is a plain, slow, single-threaded
+ * reference implementation used only by the test suite, the smoke check and
+ * the benchmark's CPU-baseline leg. The GPU library never includes, links or
+ * calls it, and it includes nothing from the GPU library: the job struct below
+ * is declared here on its own, with the same field order and widths as the
+ * GPU library's, so that one Python-side description can fill both.
+ *
+ * All array arguments are HOST pointers. Every function returns 0 on success
+ * and a negative code on invalid arguments (-1 invalid, -2 out of range,
+ * -3 out of memory).
+ */
+#ifndef NOPFS_REF_H
+#define NOPFS_REF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct nopfs_ref_job {
+  int64_t  F;          /* samples in the dataset (paper notation F)          */
+  int32_t  E;          /* epochs                                             */
+  int32_t  N;          /* data-parallel workers                              */
+  int32_t  B;          /* per-worker mini-batch size                         */
+  int32_t  drop_last;  /* 1: drop the last, partial iteration of each epoch  */
+  uint64_t seed;       /* shuffle seed (Philox key)                          */
+} nopfs_ref_job;
+
+/* Philox-4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11). */
+void nopfs_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
+                             uint32_t out[4]);
+
+/* Iterations per epoch T, longest stream M_max, per-worker stream lengths. */
+int nopfs_ref_stream_shape(const nopfs_ref_job* job, int64_t* T, int64_t* M_max,
+                           int64_t* M_per_worker /* [N] or NULL */);
+
+/* Shuffle key of every sample in epoch e: keys[k], k in [0, F). */
+int nopfs_ref_epoch_keys(const nopfs_ref_job* job, int32_t e, uint32_t* keys);
+
+/* Epoch permutation: perm[p] = sample at global position p of epoch e. */
+int nopfs_ref_epoch_perm(const nopfs_ref_job* job, int32_t e, int32_t* perm);
+
+/* Shard the given epoch permutations perms[E][F] into R[N][M_max]. */
+int nopfs_ref_streams_from_perms(const nopfs_ref_job* job, const int32_t* perms,
+                                 int32_t* R);
+
+/* Every worker's access stream R[N][M_max] (rows padded with -1). */
+int nopfs_ref_access_streams(const nopfs_ref_job* job, int32_t* R);
+
+/* count[N][F] and first[N][F] from R. */
+int nopfs_ref_access_stats(const nopfs_ref_job* job, const int32_t* R,
+                           uint8_t* count, int32_t* first);
+
+/* next[N][M_max] from R. */
+int nopfs_ref_reuse_next(const nopfs_ref_job* job, const int32_t* R,
+                         int32_t* next);
+
+/* tier[N][F] and used[N][J] from count, first, sizes[F] and caps[J]. Only
+ * job->F, job->E and job->N (the number of rows) are read. */
+int nopfs_ref_tier_plan(const nopfs_ref_job* job, const uint8_t* count,
+                        const int32_t* first, const int64_t* sizes,
+                        const int64_t* caps, int32_t J, int8_t* tier,
+                        int64_t* used);
+
+/* Per-sample columns for S chosen samples, computed one sample at a time
+ * from the definition of the shuffle (for checks at sizes where the full
+ * oracle is too slow):
+ *   pos[e][s]       global position of samples[s] in epoch e's order
+ *   occ_worker[e][s] worker that reads it in epoch e (-1: dropped tail)
+ *   occ_f[e][s]     stream position of that read (-1: dropped)
+ *   occ_next[e][s]  next read of the same sample by the same worker (-1: none)
+ *   col_count[i][s], col_first[i][s]  count / first column for worker i     */
+int nopfs_ref_sample_columns(const nopfs_ref_job* job, const int32_t* samples,
+                             int64_t S, int64_t* pos, int32_t* occ_worker,
+                             int32_t* occ_f, int32_t* occ_next,
+                             uint8_t* col_count, int32_t* col_first);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NOPFS_REF_H */

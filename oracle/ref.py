@@ -1,0 +1,197 @@
+"""ctypes wrapper of the CPU oracle (``oracle/liboracle.so``).
+
+TEST INFRASTRUCTURE: only the tests, ``__graft_entry__.smoke()`` and the
+benchmark's CPU-baseline leg may import this module. The product path (the
+``paper_2101_08734_amd`` package) never imports it.
+
+All arrays are numpy arrays on the host. Functions raise ``OracleError`` on a
+negative return code.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "nopfs_ref.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+GCC_CMD = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
+           "-o", _LIB, _SRC]
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+class RefJob(ctypes.Structure):
+    _fields_ = [("F", ctypes.c_int64), ("E", ctypes.c_int32),
+                ("N", ctypes.c_int32), ("B", ctypes.c_int32),
+                ("drop_last", ctypes.c_int32), ("seed", ctypes.c_uint64)]
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (plain C, no GPU code)."""
+    if force or not os.path.exists(_LIB) or \
+            os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        subprocess.run(GCC_CMD, check=True)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        jp = ctypes.POINTER(RefJob)
+        L.nopfs_ref_philox4x32_10.argtypes = [P, P, P]
+        L.nopfs_ref_philox4x32_10.restype = None
+        L.nopfs_ref_stream_shape.argtypes = [jp, P, P, P]
+        L.nopfs_ref_epoch_keys.argtypes = [jp, ctypes.c_int32, P]
+        L.nopfs_ref_epoch_perm.argtypes = [jp, ctypes.c_int32, P]
+        L.nopfs_ref_streams_from_perms.argtypes = [jp, P, P]
+        L.nopfs_ref_access_streams.argtypes = [jp, P]
+        L.nopfs_ref_access_stats.argtypes = [jp, P, P, P]
+        L.nopfs_ref_reuse_next.argtypes = [jp, P, P]
+        L.nopfs_ref_tier_plan.argtypes = [jp, P, P, P, P, ctypes.c_int32, P, P]
+        L.nopfs_ref_sample_columns.argtypes = [jp, P, ctypes.c_int64, P, P, P,
+                                               P, P, P]
+        for name in ("nopfs_ref_stream_shape", "nopfs_ref_epoch_keys",
+                     "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms",
+                     "nopfs_ref_access_streams", "nopfs_ref_access_stats",
+                     "nopfs_ref_reuse_next", "nopfs_ref_tier_plan",
+                     "nopfs_ref_sample_columns"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def make_job(F, E, N, B, drop_last=1, seed=42) -> RefJob:
+    return RefJob(int(F), int(E), int(N), int(B), int(drop_last), int(seed))
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise OracleError(f"{what} returned {rc}")
+
+
+def philox4x32_10(ctr, key):
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().nopfs_ref_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def stream_shape(job: RefJob):
+    T = np.zeros(1, np.int64)
+    Mmax = np.zeros(1, np.int64)
+    Mw = np.zeros(job.N, np.int64)
+    _check(lib().nopfs_ref_stream_shape(ctypes.byref(job), _ptr(T), _ptr(Mmax),
+                                        _ptr(Mw)), "stream_shape")
+    return int(T[0]), int(Mmax[0]), Mw
+
+
+def epoch_keys(job: RefJob, e: int) -> np.ndarray:
+    keys = np.empty(job.F, np.uint32)
+    _check(lib().nopfs_ref_epoch_keys(ctypes.byref(job), e, _ptr(keys)),
+           "epoch_keys")
+    return keys
+
+
+def epoch_perm(job: RefJob, e: int) -> np.ndarray:
+    perm = np.empty(job.F, np.int32)
+    _check(lib().nopfs_ref_epoch_perm(ctypes.byref(job), e, _ptr(perm)),
+           "epoch_perm")
+    return perm
+
+
+def streams_from_perms(job: RefJob, perms: np.ndarray) -> np.ndarray:
+    _, Mmax, _ = stream_shape(job)
+    perms = np.ascontiguousarray(perms, dtype=np.int32)
+    assert perms.shape == (job.E, job.F)
+    R = np.empty((job.N, Mmax), np.int32)
+    _check(lib().nopfs_ref_streams_from_perms(ctypes.byref(job), _ptr(perms),
+                                              _ptr(R)), "streams_from_perms")
+    return R
+
+
+def access_streams(job: RefJob) -> np.ndarray:
+    _, Mmax, _ = stream_shape(job)
+    R = np.empty((job.N, Mmax), np.int32)
+    _check(lib().nopfs_ref_access_streams(ctypes.byref(job), _ptr(R)),
+           "access_streams")
+    return R
+
+
+def access_stats(job: RefJob, R: np.ndarray):
+    R = np.ascontiguousarray(R, dtype=np.int32)
+    count = np.empty((job.N, job.F), np.uint8)
+    first = np.empty((job.N, job.F), np.int32)
+    _check(lib().nopfs_ref_access_stats(ctypes.byref(job), _ptr(R),
+                                        _ptr(count), _ptr(first)),
+           "access_stats")
+    return count, first
+
+
+def reuse_next(job: RefJob, R: np.ndarray) -> np.ndarray:
+    R = np.ascontiguousarray(R, dtype=np.int32)
+    nxt = np.empty_like(R)
+    _check(lib().nopfs_ref_reuse_next(ctypes.byref(job), _ptr(R), _ptr(nxt)),
+           "reuse_next")
+    return nxt
+
+
+def tier_plan(job: RefJob, count, first, sizes, caps):
+    count = np.ascontiguousarray(count, dtype=np.uint8)
+    first = np.ascontiguousarray(first, dtype=np.int32)
+    sizes = np.ascontiguousarray(sizes, dtype=np.int64)
+    caps = np.ascontiguousarray(caps, dtype=np.int64)
+    rows = count.shape[0]
+    sub = RefJob(job.F, job.E, rows, job.B, job.drop_last, job.seed)
+    tier = np.empty((rows, job.F), np.int8)
+    used = np.empty((rows, len(caps)), np.int64)
+    _check(lib().nopfs_ref_tier_plan(ctypes.byref(sub), _ptr(count),
+                                     _ptr(first), _ptr(sizes), _ptr(caps),
+                                     len(caps), _ptr(tier), _ptr(used)),
+           "tier_plan")
+    return tier, used
+
+
+def sample_columns(job: RefJob, samples):
+    samples = np.ascontiguousarray(samples, dtype=np.int32)
+    S = len(samples)
+    E, N = job.E, job.N
+    pos = np.empty((E, S), np.int64)
+    occ_worker = np.empty((E, S), np.int32)
+    occ_f = np.empty((E, S), np.int32)
+    occ_next = np.empty((E, S), np.int32)
+    col_count = np.empty((N, S), np.uint8)
+    col_first = np.empty((N, S), np.int32)
+    _check(lib().nopfs_ref_sample_columns(
+        ctypes.byref(job), _ptr(samples), S, _ptr(pos), _ptr(occ_worker),
+        _ptr(occ_f), _ptr(occ_next), _ptr(col_count), _ptr(col_first)),
+        "sample_columns")
+    return dict(pos=pos, occ_worker=occ_worker, occ_f=occ_f,
+                occ_next=occ_next, col_count=col_count, col_first=col_first)
+
+
+def full_pipeline(job: RefJob, sizes, caps):
+    """All four stages, in order, on the host."""
+    R = access_streams(job)
+    count, first = access_stats(job, R)
+    nxt = reuse_next(job, R)
+    tier, used = tier_plan(job, count, first, sizes, caps)
+    return dict(R=R, count=count, first=first, next=nxt, tier=tier, used=used)
