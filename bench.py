@@ -1,0 +1,233 @@
+"""Benchmark of the clairvoyant planning path on one MI355X.
+
+One step = the whole path on one job: access streams -> access stats ->
+next reuse -> tier plan, with inputs (sizes) resident in HBM and outputs
+preallocated. The metric is planned sample-accesses per second: the number of
+reads the job issues (A = N * E * L) over the device time of one step.
+
+Prints ONE JSON line. Per-kernel durations come from HIP events recorded by
+the library around each of its launches, on the stream it launches on, over
+the timed steps. The dominant kernel's roofline uses the algorithmic bytes of
+its stage (the bytes the stage must read and write given the C ABI's dense
+layouts), and the HBM traffic measured by rocprofv3 counters (summary under
+profiles/) when that summary matches the current kernel sources.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "planned sample-accesses/sec (E×F×stats+plan) and % of HBM peak, 1 MI355X"
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+DEFAULT_WORKLOAD = "imagenet22k"
+
+
+def algorithmic_bytes(job, M_w):
+    """Bytes each stage must move given the dense C-ABI layouts, per launch
+    of the kernel that produces that stage's output."""
+    A = int(sum(M_w))
+    NF = job.N * job.F
+    return {
+        # streams: write R (4 B per read)
+        "stream_sort": 4 * A,
+        # stats: read R, write count (1 B) and first (4 B) for every cell
+        "stats_tile": 4 * A + 5 * NF,
+        # next: read R, write next
+        "next_unpartition": 8 * A,
+        # plan: read count and first, read sizes, write tier
+        "plan_write": 5 * NF + 8 * job.F + NF,
+        "plan_hist": 5 * NF + 8 * job.F,
+        "seg_partition": 8 * A,
+        "next_tile": 8 * A,
+        "stream_scatter": 8 * job.E * job.F,
+    }, A
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2101_08734_amd", "csrc", "*"))):
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary, or None if absent or taken on different kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("{"):
+            d = json.loads(line)
+            if d.get("source_hash") != kernel_source_hash():
+                return None
+            k = d.get("kernels", {}).get(kernel)
+            return None if k is None else k.get("hbm_bytes_per_launch")
+    return None
+
+
+def cpu_baseline(w, sizes, caps, epochs=2, workers=2):
+    """The oracle on a bounded sample of the same workload: `epochs` of the E
+    epochs sorted and sharded for all workers, and stats, next use and plan
+    for `workers` of the N workers on those streams; each stage's time is
+    scaled linearly to the full job (streams by E/epochs, per-worker stages
+    by N/workers)."""
+    import numpy as np
+    from oracle import ref
+    ref.build()
+    job = ref.make_job(w.F, epochs, w.N, w.B, w.drop_last, w.seed)
+    full = ref.make_job(*w.job_tuple())
+    _, _, Mw = ref.stream_shape(full)
+    A = int(Mw.sum())
+    t0 = time.perf_counter()
+    R = ref.access_streams(job)
+    t1 = time.perf_counter()
+    count, first = ref.access_stats_rows(job, R[:workers], 0)
+    t2 = time.perf_counter()
+    ref.reuse_next_rows(job, R[:workers], 0)
+    t3 = time.perf_counter()
+    ref.tier_plan(full, count, first, sizes, np.asarray(caps, np.int64))
+    t4 = time.perf_counter()
+    est = (t1 - t0) * (w.E / epochs) + (t4 - t1) * (w.N / workers)
+    return {
+        "value": A / est,
+        "unit": "accesses/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{w.name}: {epochs} of {w.E} epochs sorted+sharded for all {w.N} workers "
+                   f"({t1 - t0:.1f}s), stats {t2 - t1:.2f}s + next {t3 - t2:.2f}s + plan "
+                   f"{t4 - t3:.1f}s for {workers} of {w.N} workers; scaled x{w.E // epochs} "
+                   f"(streams) and x{w.N // workers} (per-worker stages) to {est:.0f}s for the "
+                   f"full job; single-threaded, {os.cpu_count()} host cores present"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-bytes", type=int, default=1 << 30,
+                    help="size of the calibration copy run after the timed steps")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py plans all N workers of a job on one GPU; runs on more than one "
+              "GPU are not part of this build (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2101_08734_amd import nopfs
+    from paper_2101_08734_amd import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    job = nopfs.Job(*w.job_tuple())
+    T, M, M_w = nopfs.stream_shape(job)
+    sizes_h = wl.sizes(w)
+    caps = [int(c) for c in wl.caps(w)]
+    dev = torch.device("cuda:0")
+    sizes = torch.from_numpy(sizes_h).to(dev)
+    R = torch.empty((job.N, M), dtype=torch.int32, device=dev)
+    count = torch.empty((job.N, job.F), dtype=torch.uint8, device=dev)
+    first = torch.empty((job.N, job.F), dtype=torch.int32, device=dev)
+    nxt = torch.empty((job.N, M), dtype=torch.int32, device=dev)
+    tier = torch.empty((job.N, job.F), dtype=torch.int8, device=dev)
+    used = torch.empty((job.N, len(caps)), dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        nopfs.access_streams(job, R, stream=stream)
+        nopfs.access_stats(job, R, count, first, stream=stream)
+        nopfs.reuse_next(job, R, nxt, stream=stream)
+        nopfs.tier_plan(job, count, first, sizes, caps, tier, used, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] {w.name}: warmup done", file=sys.stderr, flush=True)
+
+    nopfs.profile_enable(True)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    nopfs.profile_enable(False)
+    kernels = nopfs.profile_results()
+    dev_ms = ev0.elapsed_time(ev1)
+    ms_per_step = dev_ms / args.steps
+    print(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall:.2f}s)",
+          file=sys.stderr, flush=True)
+
+    # calibration copy (known traffic) for the counter runs
+    if args.calibrate_bytes > 0:
+        a = torch.empty(args.calibrate_bytes, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        nopfs.calibration_copy(a, b, args.calibrate_bytes, stream=stream)
+        torch.cuda.synchronize()
+        del a, b
+
+    alg, A = algorithmic_bytes(job, M_w)
+    per_kernel = {k: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps,
+                      "avg_ms": ms / n} for k, (n, ms) in kernels.items()}
+    dominant = max(per_kernel, key=lambda k: per_kernel[k]["ms_per_step"])
+    dom = per_kernel[dominant]
+    roofline = None
+    if dominant in alg:
+        achieved = alg[dominant] / (dom["avg_ms"] * 1e-3) / 1e9
+        traffic = committed_traffic(w.name, dominant)
+        roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": traffic, "algorithmic_bytes": alg[dominant],
+                    "avg_ms": round(dom["avg_ms"], 4)}
+    for k, v in per_kernel.items():
+        if k in alg:
+            v["alg_GBps"] = round(alg[k] / (v["avg_ms"] * 1e-3) / 1e9, 1)
+    print("[bench] kernels: " + json.dumps(per_kernel), file=sys.stderr, flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on a bounded sample ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, sizes_h, caps)
+
+    line = {
+        "metric": METRIC,
+        "value": A / (ms_per_step * 1e-3),
+        "unit": "accesses/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "F": w.F, "E": w.E, "N": w.N, "B": w.B,
+                   "drop_last": w.drop_last, "seed": w.seed, "accesses": A,
+                   "tier_caps_bytes": caps, "parallelism": "none (all N workers on one GPU)"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

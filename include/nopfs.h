@@ -1,0 +1,176 @@
+/*
+ * nopfs.h -- C ABI of the MI355X (gfx950) clairvoyant access planner.
+ *
+ * Given the shuffle seed of a data-parallel training job, the library expands
+ * it into every worker's exact sample-access stream for all epochs, and from
+ * those streams derives per-(worker, sample) access frequencies and first
+ * reads, next-reuse positions, and a frequency-ordered placement of samples
+ * into capacity-limited storage tiers. This is the clairvoyant planning of
+ * NoPFS (Dryden et al., SC'21): section 2 (reproducible shuffles), section 3
+ * (access patterns, Belady's next use, the access-frequency distribution),
+ * section 4 (batches, worker batches and the stream R) and section 5.1 (the
+ * placement rule).
+ *
+ * CONVENTIONS (all entry points)
+ *  - Array arguments are DEVICE pointers owned by the caller, except where
+ *    marked "host". Outputs are preallocated by the caller; the library writes
+ *    every element of every output (no zeroing needed) and keeps no pointer
+ *    after the enqueued work completes.
+ *  - `hip_stream` is a hipStream_t (NULL = the null stream). GPU calls only
+ *    enqueue work on it and return; the caller keeps the buffers alive until
+ *    the stream has completed. Internal scratch is allocated and freed in
+ *    stream order on the same stream.
+ *  - Return 0 on success, a negative NOPFS_E* code otherwise. Argument errors
+ *    are detected on the host before anything is enqueued. No C++ exception
+ *    crosses this boundary. nopfs_last_error() gives a thread-local detail.
+ *  - An array with no elements (R and next when M_max == 0) may be NULL.
+ *  - Layouts are row-major; [N][F] tables are indexed i*F + k with 64-bit
+ *    arithmetic (N*F may exceed 2^31).
+ *  - Entry points are stateless and reentrant: several jobs (say a training
+ *    and a validation job) can be planned concurrently on different streams.
+ *  - Every result is exact integer work and deterministic: the output is a
+ *    pure function of the inputs.
+ *
+ * READINGS of points the paper leaves open (binding for every entry point):
+ *  - Shuffle: epoch e orders samples by a 32-bit key, word (k mod 4) of
+ *    Philox-4x32-10 (Salmon et al., SC'11) at counter (k div 4, e, 0, 0) with
+ *    key (seed low 32 bits, seed high 32 bits); equal keys go by smaller id.
+ *  - Ids, epochs and stream positions are 0-based.
+ *  - B is the per-worker batch; the global batch is N*B. Worker i reads the
+ *    global positions p of each epoch with p mod N == i, in order.
+ *  - drop_last=1: T = F div (N*B) iterations, every worker reads L = T*B
+ *    samples per epoch, positions p >= T*N*B are not read. drop_last=0:
+ *    T = ceil(F / (N*B)), worker i reads L_i = ceil((F - i) / N) samples per
+ *    epoch (0 when i >= F); rows shorter than M_max are padded with -1.
+ *  - Stream positions f index a worker's own stream R_i: f = e*L_i + j for
+ *    its j-th read in epoch e. "Never" is -1.
+ */
+#ifndef NOPFS_H
+#define NOPFS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define NOPFS_OK        0
+#define NOPFS_EINVAL  (-1) /* null pointer, F<1, E<1, N<1, B<1, drop_last not
+                              0/1, J<1, a negative capacity                  */
+#define NOPFS_ERANGE  (-2) /* F >= 2^31, E > 255, M_max >= 2^31, J > 127     */
+#define NOPFS_ENOMEM  (-3) /* internal scratch could not be allocated        */
+#define NOPFS_EDEVICE (-4) /* HIP runtime or launch error (see last_error)   */
+
+/* A training job as the paper states it (section 4 and the Python Job of
+ * section 5.2.1): F samples, E epochs, N data-parallel workers, per-worker
+ * mini-batch B, whether the last partial iteration is dropped, and the seed. */
+typedef struct nopfs_job {
+  int64_t  F;          /* samples, 1 <= F < 2^31                            */
+  int32_t  E;          /* epochs, 1 <= E <= 255 (counts are uint8)          */
+  int32_t  N;          /* workers, >= 1                                     */
+  int32_t  B;          /* per-worker batch, >= 1                            */
+  int32_t  drop_last;  /* 0 or 1                                            */
+  uint64_t seed;       /* shuffle seed                                      */
+} nopfs_job;
+
+/* Host only, no GPU. Iterations per epoch *T, the longest stream *M_max
+ * (= E * max_i L_i), and if M_per_worker != NULL (host, [N]) each worker's
+ * stream length M_i = E * L_i. Section 4: T is floor (or ceil when the last
+ * small iteration is kept) of F over the global batch. Any output pointer may
+ * be NULL. Errors: EINVAL, ERANGE. */
+int nopfs_stream_shape(const nopfs_job* job, int64_t* T, int64_t* M_max,
+                       int64_t* M_per_worker);
+
+/* Access streams (section 2: the seed reproduces every epoch's shuffle;
+ * section 4: worker batches partition each global batch and R is the
+ * concatenation of a worker's batches).
+ *   R: int32 [N][M_max], R[i][f] = sample read by worker i at position f,
+ *      -1 in padding (drop_last=0 only).
+ * Errors: EINVAL, ERANGE, ENOMEM, EDEVICE. */
+int nopfs_access_streams(const nopfs_job* job, int32_t* R, void* hip_stream);
+
+/* Access frequencies and first reads (section 3.1: worker i's access
+ * frequency X of sample k over all E epochs; section 5.1 names it r_k).
+ *   R:     int32 [N][M_max], as written by nopfs_access_streams for this job
+ *          (precondition; other contents give unspecified but in-bounds
+ *          results as long as every entry is in [0, F) or padding).
+ *   count: uint8 [N][F], number of reads of k in R_i.
+ *   first: int32 [N][F], smallest f with R_i[f] == k, or -1.
+ * Errors: EINVAL, ERANGE, ENOMEM, EDEVICE. */
+int nopfs_access_stats(const nopfs_job* job, const int32_t* R, uint8_t* count,
+                       int32_t* first, void* hip_stream);
+
+/* Next reuse (section 3: Belady's replacement evicts the sample whose next
+ * use is furthest; the four rules of Cao et al. need it).
+ *   R:    int32 [N][M_max], as for nopfs_access_stats.
+ *   next: int32 [N][M_max], smallest f' > f with R_i[f'] == R_i[f], or -1
+ *         (also -1 in padding). The reuse distance is next - f; every reuse
+ *         lies in a later epoch.
+ * Errors: EINVAL, ERANGE, ENOMEM, EDEVICE. */
+int nopfs_reuse_next(const nopfs_job* job, const int32_t* R, int32_t* next,
+                     void* hip_stream);
+
+/* Tier placement (section 5.1: a worker caches the samples with the largest
+ * access frequency in its fastest storage class, then the next, until the
+ * dataset is cached or its storage is full).
+ * Per worker i, samples are ranked by (count desc, first asc with -1 last,
+ * id asc); tier 0 takes samples along the ranking while they fit in caps[0],
+ * the first sample that does not fit starts tier 1, and so on; what remains
+ * after tier J-1 is uncached. Samples a worker never reads are ranked last
+ * and are still placed (they can serve other workers). Tiers are independent
+ * per worker. The staging buffer (storage class 0 of section 4) is not a
+ * placement tier: pass only cache classes, fastest first.
+ *   count, first: as written by nopfs_access_stats for this job.
+ *   sizes: int64 [F] sample sizes in bytes, each >= 1 (precondition; other
+ *          values give unspecified but in-bounds results).
+ *   caps:  HOST int64 [J] per-worker tier capacities in bytes, >= 0.
+ *   tier:  int8 [N][F], tier index of k on worker i, or -1 (uncached).
+ *   used:  int64 [N][J], bytes placed in each tier.
+ * Errors: EINVAL, ERANGE (J > 127), ENOMEM, EDEVICE. */
+int nopfs_tier_plan(const nopfs_job* job, const uint8_t* count,
+                    const int32_t* first, const int64_t* sizes,
+                    const int64_t* caps, int32_t J, int8_t* tier,
+                    int64_t* used, void* hip_stream);
+
+/* Static description of a status code. Never NULL. */
+const char* nopfs_strerror(int code);
+
+/* Thread-local detail of the last failing call on this thread ("" if none). */
+const char* nopfs_last_error(void);
+
+/* ---- Measurement aids ------------------------------------------------- */
+
+/* Per-kernel timing with HIP events recorded on the caller's stream around
+ * every kernel the library launches. enable=1 starts (and clears) the
+ * record, enable=0 stops. Timing is off by default. */
+int nopfs_profile_enable(int enable);
+
+/* Synchronises on the recorded events and reports, for the idx-th kernel
+ * name seen since profiling was enabled, its name (static string), number of
+ * launches and total milliseconds. Returns NOPFS_EINVAL when idx is past the
+ * end. */
+int nopfs_profile_query(int idx, const char** name, int64_t* launches,
+                        double* total_ms);
+
+/* A plain device-to-device copy of `bytes` bytes (multiple of 16, 16-byte
+ * aligned pointers) with a kernel of known traffic, used to calibrate HBM
+ * byte counters. */
+int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes,
+                           void* hip_stream);
+
+/* ---- Test hooks ------------------------------------------------------- */
+
+/* Overrides internal capacities so tests can drive the slow paths on small
+ * inputs (0 restores the default):
+ *   which=1  largest bucket the stream sort keeps in LDS (elements)
+ *   which=2  candidate records per worker in the tier plan's fast path, and
+ *            reads per window in the next-use fast path
+ *   which=3  fail the next internal scratch allocation (value 1)
+ * Not thread-safe; meant for tests only. */
+int nopfs_debug_set(int which, int64_t value);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NOPFS_H */

@@ -224,20 +224,22 @@ int nopfs_ref_access_streams(const nopfs_ref_job* job, int32_t* R) {
 /* worker reads a sample over all E epochs; the first read time is kept so  */
 /* the plan can order equally frequent samples).                            */
 /* ------------------------------------------------------------------------ */
-int nopfs_ref_access_stats(const nopfs_ref_job* job, const int32_t* R,
-                           uint8_t* count, int32_t* first) {
+int nopfs_ref_access_stats_rows(const nopfs_ref_job* job, const int32_t* R,
+                                int64_t i0, int64_t i1, uint8_t* count,
+                                int32_t* first) {
   int64_t M_max;
   int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
   if (rc) return rc;
-  if (!R || !count || !first) return REF_EINVAL;
+  if (!R || !count || !first || i0 < 0 || i1 > job->N || i0 > i1) return REF_EINVAL;
   int64_t F = job->F;
-  for (int64_t i = 0; i < job->N; ++i) {
-    uint8_t* c = count + i * F;
-    int32_t* fi = first + i * F;
+  for (int64_t i = i0; i < i1; ++i) {
+    uint8_t* c = count + (i - i0) * F;
+    int32_t* fi = first + (i - i0) * F;
+    const int32_t* row = R + (i - i0) * M_max;
     for (int64_t k = 0; k < F; ++k) { c[k] = 0; fi[k] = -1; }
     int64_t M = (int64_t)job->E * epoch_len(job, i);
     for (int64_t f = 0; f < M; ++f) {
-      int32_t k = R[i * M_max + f];
+      int32_t k = row[f];
       if (k < 0 || k >= F) return REF_EINVAL;
       if (c[k] == 0) fi[k] = (int32_t)f;
       c[k] += 1;
@@ -246,33 +248,49 @@ int nopfs_ref_access_stats(const nopfs_ref_job* job, const int32_t* R,
   return 0;
 }
 
+int nopfs_ref_access_stats(const nopfs_ref_job* job, const int32_t* R,
+                           uint8_t* count, int32_t* first) {
+  int rc = check_job(job);
+  if (rc) return rc;
+  return nopfs_ref_access_stats_rows(job, R, 0, job->N, count, first);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Next use (I/O Access Patterns: the optimal replacement discards the      */
 /* sample whose next use is furthest; the next use is found by walking the  */
 /* stream backwards and remembering the last position seen per sample).     */
 /* ------------------------------------------------------------------------ */
-int nopfs_ref_reuse_next(const nopfs_ref_job* job, const int32_t* R,
-                         int32_t* next) {
+int nopfs_ref_reuse_next_rows(const nopfs_ref_job* job, const int32_t* R,
+                              int64_t i0, int64_t i1, int32_t* next) {
   int64_t M_max;
   int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
   if (rc) return rc;
-  if (!R || !next) return REF_EINVAL;
+  if (!R || !next || i0 < 0 || i1 > job->N || i0 > i1) return REF_EINVAL;
   int64_t F = job->F;
   int32_t* last = (int32_t*)malloc((size_t)F * sizeof(int32_t));
   if (!last) return REF_ENOMEM;
-  for (int64_t i = 0; i < job->N; ++i) {
+  for (int64_t i = i0; i < i1; ++i) {
+    const int32_t* row = R + (i - i0) * M_max;
+    int32_t* nrow = next + (i - i0) * M_max;
     for (int64_t k = 0; k < F; ++k) last[k] = -1;
     int64_t M = (int64_t)job->E * epoch_len(job, i);
-    for (int64_t f = M; f < M_max; ++f) next[i * M_max + f] = -1;
+    for (int64_t f = M; f < M_max; ++f) nrow[f] = -1;
     for (int64_t f = M - 1; f >= 0; --f) {
-      int32_t k = R[i * M_max + f];
+      int32_t k = row[f];
       if (k < 0 || k >= F) { free(last); return REF_EINVAL; }
-      next[i * M_max + f] = last[k];
+      nrow[f] = last[k];
       last[k] = (int32_t)f;
     }
   }
   free(last);
   return 0;
+}
+
+int nopfs_ref_reuse_next(const nopfs_ref_job* job, const int32_t* R,
+                         int32_t* next) {
+  int rc = check_job(job);
+  if (rc) return rc;
+  return nopfs_ref_reuse_next_rows(job, R, 0, job->N, next);
 }
 
 /* ------------------------------------------------------------------------ */

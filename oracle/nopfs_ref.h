@@ -55,9 +55,18 @@ int nopfs_ref_access_streams(const nopfs_ref_job* job, int32_t* R);
 int nopfs_ref_access_stats(const nopfs_ref_job* job, const int32_t* R,
                            uint8_t* count, int32_t* first);
 
+/* The same for workers [i0, i1) only: R, count and first point at row i0. */
+int nopfs_ref_access_stats_rows(const nopfs_ref_job* job, const int32_t* R,
+                                int64_t i0, int64_t i1, uint8_t* count,
+                                int32_t* first);
+
 /* next[N][M_max] from R. */
 int nopfs_ref_reuse_next(const nopfs_ref_job* job, const int32_t* R,
                          int32_t* next);
+
+/* The same for workers [i0, i1) only: R and next point at row i0. */
+int nopfs_ref_reuse_next_rows(const nopfs_ref_job* job, const int32_t* R,
+                              int64_t i0, int64_t i1, int32_t* next);
 
 /* tier[N][F] and used[N][J] from count, first, sizes[F] and caps[J]. Only
  * job->F, job->E and job->N (the number of rows) are read. */

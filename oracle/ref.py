@@ -60,6 +60,8 @@ def lib():
         L.nopfs_ref_access_streams.argtypes = [jp, P]
         L.nopfs_ref_access_stats.argtypes = [jp, P, P, P]
         L.nopfs_ref_reuse_next.argtypes = [jp, P, P]
+        L.nopfs_ref_access_stats_rows.argtypes = [jp, P, ctypes.c_int64, ctypes.c_int64, P, P]
+        L.nopfs_ref_reuse_next_rows.argtypes = [jp, P, ctypes.c_int64, ctypes.c_int64, P]
         L.nopfs_ref_tier_plan.argtypes = [jp, P, P, P, P, ctypes.c_int32, P, P]
         L.nopfs_ref_sample_columns.argtypes = [jp, P, ctypes.c_int64, P, P, P,
                                                P, P, P]
@@ -67,7 +69,8 @@ def lib():
                      "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms",
                      "nopfs_ref_access_streams", "nopfs_ref_access_stats",
                      "nopfs_ref_reuse_next", "nopfs_ref_tier_plan",
-                     "nopfs_ref_sample_columns"):
+                     "nopfs_ref_sample_columns", "nopfs_ref_access_stats_rows",
+                     "nopfs_ref_reuse_next_rows"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -144,6 +147,25 @@ def access_stats(job: RefJob, R: np.ndarray):
                                         _ptr(count), _ptr(first)),
            "access_stats")
     return count, first
+
+
+def access_stats_rows(job: RefJob, R_rows: np.ndarray, i0: int):
+    """Stats of workers [i0, i0 + len(R_rows)) only."""
+    R_rows = np.ascontiguousarray(R_rows, dtype=np.int32)
+    n = R_rows.shape[0]
+    count = np.empty((n, job.F), np.uint8)
+    first = np.empty((n, job.F), np.int32)
+    _check(lib().nopfs_ref_access_stats_rows(ctypes.byref(job), _ptr(R_rows), i0, i0 + n,
+                                             _ptr(count), _ptr(first)), "access_stats_rows")
+    return count, first
+
+
+def reuse_next_rows(job: RefJob, R_rows: np.ndarray, i0: int) -> np.ndarray:
+    R_rows = np.ascontiguousarray(R_rows, dtype=np.int32)
+    nxt = np.empty_like(R_rows)
+    _check(lib().nopfs_ref_reuse_next_rows(ctypes.byref(job), _ptr(R_rows), i0,
+                                           i0 + R_rows.shape[0], _ptr(nxt)), "reuse_next_rows")
+    return nxt
 
 
 def reuse_next(job: RefJob, R: np.ndarray) -> np.ndarray:

@@ -1,0 +1,226 @@
+// Host-side plumbing of the planner library: argument validation and shape
+// arithmetic, error reporting, stream-ordered scratch, per-kernel event
+// timing, and the calibration copy kernel.
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+
+namespace nopfs {
+
+static thread_local std::string g_last_error;
+
+void set_last_error(const std::string& msg) { g_last_error = msg; }
+
+int fail(int code, const std::string& msg) {
+  set_last_error(msg);
+  return code;
+}
+
+int hip_fail(hipError_t err, const char* what) {
+  set_last_error(std::string(what) + ": " + hipGetErrorString(err));
+  return NOPFS_EDEVICE;
+}
+
+int make_shape(const nopfs_job* job, Shape* s) {
+  if (!job) return fail(NOPFS_EINVAL, "job is NULL");
+  if (job->F < 1 || job->E < 1 || job->N < 1 || job->B < 1)
+    return fail(NOPFS_EINVAL, "F, E, N and B must be >= 1");
+  if (job->drop_last != 0 && job->drop_last != 1)
+    return fail(NOPFS_EINVAL, "drop_last must be 0 or 1");
+  if (job->F >= (int64_t(1) << 31)) return fail(NOPFS_ERANGE, "F must be < 2^31");
+  if (job->E > 255) return fail(NOPFS_ERANGE, "E must be <= 255 (uint8 counts)");
+  s->F = job->F;
+  s->E = job->E;
+  s->N = job->N;
+  s->B = job->B;
+  s->drop_last = job->drop_last;
+  s->seed = job->seed;
+  const int64_t G = s->N * s->B;
+  s->T = s->drop_last ? s->F / G : (s->F + G - 1) / G;
+  s->L = epoch_len(s->F, s->N, s->B, s->drop_last, 0);
+  s->M_max = s->E * s->L;
+  s->P = s->drop_last ? s->T * G : s->F;
+  if (s->M_max >= (int64_t(1) << 31)) return fail(NOPFS_ERANGE, "M_max must be < 2^31");
+  return NOPFS_OK;
+}
+
+// ---------------------------------------------------------------- scratch --
+static int64_t g_debug[4] = {0, 0, 0, 0};
+
+int64_t debug_value(int which) { return (which >= 0 && which < 4) ? g_debug[which] : 0; }
+
+bool take_alloc_failure() {
+  if (g_debug[3]) {
+    g_debug[3] = 0;
+    return true;
+  }
+  return false;
+}
+
+Scratch::~Scratch() {
+  for (int i = n_ - 1; i >= 0; --i) (void)hipFreeAsync(ptrs_[i], stream_);
+}
+
+int Scratch::alloc(void** p, size_t bytes) {
+  *p = nullptr;
+  if (n_ >= 32) return fail(NOPFS_ENOMEM, "too many scratch buffers");
+  if (take_alloc_failure()) return fail(NOPFS_ENOMEM, "scratch allocation failed (test hook)");
+  bytes = (bytes + 255) & ~size_t(255);
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMallocAsync(p, bytes, stream_);
+  if (e != hipSuccess || !*p) {
+    (void)hipGetLastError();
+    *p = nullptr;
+    return fail(NOPFS_ENOMEM, std::string("scratch allocation of ") +
+                                  std::to_string(bytes) + " bytes failed");
+  }
+  ptrs_[n_++] = *p;
+  return NOPFS_OK;
+}
+
+// -------------------------------------------------------------- profiling --
+namespace {
+struct ProfRec {
+  const char* name;
+  hipEvent_t start, stop;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;
+thread_local size_t t_open_idx = 0;
+}  // namespace
+
+void prof_begin(const char* name, hipStream_t s) {
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  if (!g_prof_on) return;
+  ProfRec r{name, nullptr, nullptr};
+  if (hipEventCreate(&r.start) != hipSuccess || hipEventCreate(&r.stop) != hipSuccess) {
+    (void)hipGetLastError();
+    return;
+  }
+  (void)hipEventRecord(r.start, s);
+  g_prof.push_back(r);
+  t_open_idx = g_prof.size();
+}
+
+void prof_end(hipStream_t s) {
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  if (!g_prof_on || t_open_idx == 0 || t_open_idx > g_prof.size()) return;
+  (void)hipEventRecord(g_prof[t_open_idx - 1].stop, s);
+  t_open_idx = 0;
+}
+
+static void prof_clear() {
+  for (auto& r : g_prof) {
+    if (r.start) (void)hipEventDestroy(r.start);
+    if (r.stop) (void)hipEventDestroy(r.stop);
+  }
+  g_prof.clear();
+}
+
+// -------------------------------------------------------- calibration copy --
+__global__ void __launch_bounds__(256) calibration_copy_kernel(const uint4* __restrict__ src,
+                                                               uint4* __restrict__ dst,
+                                                               int64_t n) {
+  int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (; i < n; i += stride) dst[i] = src[i];
+}
+
+}  // namespace nopfs
+
+using namespace nopfs;
+
+extern "C" {
+
+int nopfs_stream_shape(const nopfs_job* job, int64_t* T, int64_t* M_max,
+                       int64_t* M_per_worker) {
+  try {
+    Shape s;
+    int rc = make_shape(job, &s);
+    if (rc) return rc;
+    if (T) *T = s.T;
+    if (M_max) *M_max = s.M_max;
+    if (M_per_worker)
+      for (int64_t i = 0; i < s.N; ++i)
+        M_per_worker[i] = s.E * epoch_len(s.F, s.N, s.B, s.drop_last, i);
+    return NOPFS_OK;
+  } catch (...) {
+    return fail(NOPFS_EINVAL, "unexpected host exception");
+  }
+}
+
+const char* nopfs_strerror(int code) {
+  switch (code) {
+    case NOPFS_OK: return "ok";
+    case NOPFS_EINVAL: return "invalid argument";
+    case NOPFS_ERANGE: return "argument out of supported range";
+    case NOPFS_ENOMEM: return "scratch allocation failed";
+    case NOPFS_EDEVICE: return "HIP runtime or launch error";
+    default: return "unknown status code";
+  }
+}
+
+const char* nopfs_last_error(void) { return g_last_error.c_str(); }
+
+int nopfs_profile_enable(int enable) {
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  if (enable) {
+    prof_clear();
+    g_prof_on = true;
+  } else {
+    g_prof_on = false;
+  }
+  return NOPFS_OK;
+}
+
+int nopfs_profile_query(int idx, const char** name, int64_t* launches,
+                        double* total_ms) {
+  std::lock_guard<std::mutex> g(g_prof_mu);
+  std::vector<const char*> names;
+  for (auto& r : g_prof) {
+    bool seen = false;
+    for (auto* n : names) seen |= (std::string(n) == r.name);
+    if (!seen) names.push_back(r.name);
+  }
+  if (idx < 0 || idx >= int(names.size())) return NOPFS_EINVAL;
+  double ms = 0;
+  int64_t cnt = 0;
+  for (auto& r : g_prof) {
+    if (std::string(r.name) != names[idx]) continue;
+    if (hipEventSynchronize(r.stop) != hipSuccess) return hip_fail(hipGetLastError(), "event sync");
+    float t = 0;
+    if (hipEventElapsedTime(&t, r.start, r.stop) != hipSuccess)
+      return hip_fail(hipGetLastError(), "event elapsed");
+    ms += t;
+    cnt++;
+  }
+  if (name) *name = names[idx];
+  if (launches) *launches = cnt;
+  if (total_ms) *total_ms = ms;
+  return NOPFS_OK;
+}
+
+int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes, void* hip_stream) {
+  if (!src || !dst || bytes < 0 || (bytes & 15) ||
+      (reinterpret_cast<uintptr_t>(src) & 15) || (reinterpret_cast<uintptr_t>(dst) & 15))
+    return fail(NOPFS_EINVAL, "calibration copy needs 16-byte aligned, 16-byte multiple buffers");
+  const int64_t n = bytes / 16;
+  if (n == 0) return NOPFS_OK;
+  int64_t blocks = ceil_div(n, 256 * 8);
+  if (blocks > 65536) blocks = 65536;
+  return launch("calibration_copy", calibration_copy_kernel, dim3(uint32_t(blocks)), dim3(256), 0,
+                static_cast<hipStream_t>(hip_stream), static_cast<const uint4*>(src),
+                static_cast<uint4*>(dst), n);
+}
+
+int nopfs_debug_set(int which, int64_t value) {
+  if (which < 1 || which > 3 || value < 0) return NOPFS_EINVAL;
+  g_debug[which] = value;
+  return NOPFS_OK;
+}
+
+}  // extern "C"

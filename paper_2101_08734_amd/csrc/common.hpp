@@ -1,0 +1,175 @@
+// Shared host and device helpers of the planner library (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "nopfs.h"
+
+namespace nopfs {
+
+// ---------------------------------------------------------------- errors --
+struct Status {
+  int code = NOPFS_OK;
+  bool ok() const { return code == NOPFS_OK; }
+};
+
+void set_last_error(const std::string& msg);
+int fail(int code, const std::string& msg);  // records msg, returns code
+int hip_fail(hipError_t err, const char* what);
+
+#define NOPFS_HIP(call)                                   \
+  do {                                                    \
+    hipError_t _e = (call);                               \
+    if (_e != hipSuccess) return ::nopfs::hip_fail(_e, #call); \
+  } while (0)
+
+// ----------------------------------------------------------------- shape --
+struct Shape {
+  int64_t F, E, N, B;
+  int drop_last;
+  int64_t T;       // iterations per epoch
+  int64_t L;       // per-epoch reads of worker 0 (the longest row)
+  int64_t M_max;   // E * L
+  int64_t P;       // issued positions per epoch
+  uint64_t seed;
+};
+
+// Validates the job and fills the shape. Returns a NOPFS_* code.
+int make_shape(const nopfs_job* job, Shape* s);
+
+// Per-epoch reads of worker i (same rule as the public header).
+__host__ __device__ inline int64_t epoch_len(int64_t F, int64_t N, int64_t B,
+                                             int drop_last, int64_t i) {
+  if (drop_last) return (F / (N * B)) * B;
+  if (i >= F) return 0;
+  return (F - i + N - 1) / N;
+}
+
+// --------------------------------------------------------------- scratch --
+// Stream-ordered device scratch (hipMallocAsync / hipFreeAsync).
+class Scratch {
+ public:
+  explicit Scratch(hipStream_t s) : stream_(s) {}
+  ~Scratch();
+  // Allocates `bytes` (rounded up to 256) and returns NOPFS_OK or ENOMEM.
+  int alloc(void** p, size_t bytes);
+  template <typename T>
+  int alloc_n(T** p, size_t n) { return alloc(reinterpret_cast<void**>(p), n * sizeof(T)); }
+
+ private:
+  hipStream_t stream_;
+  void* ptrs_[32] = {};
+  int n_ = 0;
+};
+
+// ---------------------------------------------------------------- launch --
+// Records HIP events around a launch when profiling is on.
+void prof_begin(const char* name, hipStream_t s);
+void prof_end(hipStream_t s);
+
+template <typename Kernel, typename... Args>
+int launch(const char* name, Kernel k, dim3 grid, dim3 block, size_t shmem,
+           hipStream_t s, Args... args) {
+  if (grid.x == 0 || grid.y == 0 || grid.z == 0) return NOPFS_OK;
+  prof_begin(name, s);
+  hipLaunchKernelGGL(k, grid, block, shmem, s, args...);
+  hipError_t e = hipGetLastError();
+  prof_end(s);
+  if (e != hipSuccess) return hip_fail(e, name);
+  return NOPFS_OK;
+}
+
+// Debug overrides (nopfs_debug_set).
+int64_t debug_value(int which);
+bool take_alloc_failure();
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------------- device --
+// Workgroups are dispatched round-robin over the 8 XCDs (WG i -> XCD i % 8),
+// and each XCD has its own L2. Remapping the flat block id so that XCD x
+// receives a contiguous range of logical tiles keeps neighbouring tiles
+// (which touch neighbouring cache lines) inside one L2. `padded` is the grid
+// size rounded up to a multiple of 8; callers drop logical ids >= real count.
+__device__ inline uint32_t xcd_logical(uint32_t bid, uint32_t padded) {
+  const uint32_t per = padded >> 3;
+  return (bid & 7u) * per + (bid >> 3);
+}
+
+inline uint32_t xcd_padded(uint32_t n) { return (n + 7u) & ~7u; }
+
+__device__ inline uint64_t lanemask_lt() {
+  const uint32_t lane = __lane_id();
+  return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+// Inclusive scan of a 32-bit value across the 64 lanes of a wave.
+__device__ inline uint32_t wave_inclusive_scan(uint32_t v) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint32_t o = __shfl_up(v, d, 64);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+__device__ inline uint64_t wave_inclusive_scan64(uint64_t v) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint64_t o = __shfl_up(v, d, 64);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+// Exclusive scan over the whole workgroup (blockDim.x a multiple of 64, at
+// most 1024). `tmp` holds one slot per wave plus one. Returns the exclusive
+// prefix of v; *total receives the sum over the block.
+__device__ inline uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp,
+                                                uint32_t* total) {
+  const int lane = __lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  uint32_t inc = wave_inclusive_scan(v);
+  if (lane == 63) tmp[wave] = inc;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    uint32_t w = threadIdx.x < (unsigned)nwaves ? tmp[threadIdx.x] : 0u;
+    uint32_t wi = wave_inclusive_scan(w);
+    if (threadIdx.x < (unsigned)nwaves) tmp[threadIdx.x] = wi - w;
+    if (threadIdx.x == 63) tmp[64] = wi;
+  }
+  __syncthreads();
+  uint32_t r = tmp[wave] + inc - v;
+  *total = tmp[64];
+  __syncthreads();
+  return r;
+}
+
+__device__ inline uint64_t block_exclusive_scan64(uint64_t v, uint64_t* tmp,
+                                                  uint64_t* total) {
+  const int lane = __lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  uint64_t inc = wave_inclusive_scan64(v);
+  if (lane == 63) tmp[wave] = inc;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    uint64_t w = threadIdx.x < (unsigned)nwaves ? tmp[threadIdx.x] : 0ull;
+    uint64_t wi = wave_inclusive_scan64(w);
+    if (threadIdx.x < (unsigned)nwaves) tmp[threadIdx.x] = wi - w;
+    if (threadIdx.x == 63) tmp[64] = wi;
+  }
+  __syncthreads();
+  uint64_t r = tmp[wave] + inc - v;
+  *total = tmp[64];
+  __syncthreads();
+  return r;
+}
+
+}  // namespace nopfs

@@ -1,0 +1,526 @@
+// nopfs_tier_plan: frequency-ordered, capacity-limited placement (section 5.1:
+// the largest access frequencies go to the fastest storage class, then the
+// next class, until the dataset is cached or local storage is full).
+//
+// Per worker the ranking is (count desc, first asc, id asc), which is the
+// order of the 40-bit key  (E - count) << 32 | (count ? first : id)  because
+// first reads are distinct stream positions. Tier j ends at the first sample
+// that no longer fits ("first misfit"), so the plan is fixed by J cut points
+// along the ranking. They are found without sorting the N*F cells:
+//
+//   plan_hist    -- weighted histogram of sizes over rank-ordered bins of the
+//                   key (LDS-privatised). Bins of class count>=1 split the
+//                   first-read range; their number per class follows the
+//                   expected Binomial(E, L/F) population so crowded classes
+//                   get fine bins. Class 0 is binned by id, 256 ids a bin.
+//   plan_cut     -- per worker: prefix sums over bins, then for each tier the
+//                   range of bins that can contain its cut (interval
+//                   arithmetic: the cut of tier j depends on where tier j-1
+//                   ended, known only up to one bin at this point).
+//   plan_write   -- every cell's tier from its bin; cells in a candidate bin
+//                   get a placeholder and are appended to a per-worker list.
+//   plan_resolve -- per worker: the candidates sorted by key in LDS and the
+//                   greedy fill replayed over them exactly; writes their
+//                   tiers and the bytes used per tier.
+//   plan_exact   -- per worker whose candidate list overflowed: an exact
+//                   weighted radix select over the full row for every cut,
+//                   then a full rewrite of the row (slow, rarely taken).
+#include <limits.h>
+#include <math.h>
+
+#include <new>
+#include <vector>
+
+#include "common.hpp"
+
+namespace nopfs {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTileCells = 8192;          // samples per (worker, tile)
+constexpr int kClass0Shift = 8;           // 256 ids per class-0 bin
+constexpr uint32_t kBins1Budget = 4096;   // bins for classes count >= 1
+constexpr int kCandMax = 4096;            // candidate records per worker (LDS sort)
+constexpr int kResolveThreads = 1024;
+
+struct PlanArgs {
+  int64_t F, N, M_max;
+  int32_t E, J;
+  uint32_t nbin1, nb0, nbin;
+  int32_t cmax;
+  uint16_t nbc[256];   // bins of class c (1 <= c <= E)
+  int64_t caps[128];
+};
+
+struct ClassTable {
+  uint32_t base[256];
+  float scale[256];
+};
+
+__device__ void build_class_table(const PlanArgs& a, ClassTable& t) {
+  if (threadIdx.x == 0) {
+    uint32_t b = 0;
+    for (int c = a.E; c >= 1; --c) {
+      t.base[c] = b;
+      t.scale[c] = float(a.nbc[c]) / float(a.M_max > 0 ? a.M_max : 1);
+      b += a.nbc[c];
+    }
+    t.base[0] = b;
+    t.scale[0] = 0.f;
+  }
+  __syncthreads();
+}
+
+// Rank-ordered bin of a cell; identical in every kernel that uses it.
+__device__ __forceinline__ uint32_t bin_of(const PlanArgs& a, const ClassTable& t, uint32_t c,
+                                           int32_t f, int64_t k) {
+  if (c == 0) return a.nbin1 + uint32_t(k >> kClass0Shift);
+  if (c > uint32_t(a.E)) c = uint32_t(a.E);
+  float x = f > 0 ? float(f) * t.scale[c] : 0.f;
+  uint32_t xi = uint32_t(x);
+  const uint32_t top = a.nbc[c] - 1u;
+  if (xi > top) xi = top;
+  return t.base[c] + xi;
+}
+
+__device__ __forceinline__ uint64_t rank_key(const PlanArgs& a, uint32_t c, int32_t f, int64_t k) {
+  if (c > uint32_t(a.E)) c = uint32_t(a.E);
+  const uint64_t hi = uint64_t(uint32_t(a.E) - c) << 32;
+  return hi | (c ? uint64_t(uint32_t(f)) : uint64_t(k));
+}
+
+__global__ void fill_u64(uint64_t* p, int64_t n) {
+  int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (; i < n; i += stride) p[i] = 0;
+}
+
+__global__ void fill_i32(int32_t* p, int64_t n) {
+  int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (; i < n; i += stride) p[i] = 0;
+}
+
+// -- histogram -----------------------------------------------------------------
+__global__ void __launch_bounds__(kThreads)
+plan_hist(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restrict__ first,
+          const int64_t* __restrict__ sizes, uint64_t* __restrict__ H, uint32_t ntiles) {
+  extern __shared__ uint64_t h1[];  // nbin1 weighted bins
+  __shared__ ClassTable ct;
+  __shared__ uint64_t h0[kTileCells >> kClass0Shift];
+  const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
+  if (t >= ntiles) return;
+  const int64_t kt = t / a.N, i = t - kt * a.N;
+  build_class_table(a, ct);
+  for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads) h1[b] = 0;
+  for (uint32_t b = threadIdx.x; b < (kTileCells >> kClass0Shift); b += kThreads) h0[b] = 0;
+  __syncthreads();
+  const int64_t k0 = kt * kTileCells;
+  const int64_t kn = (a.F - k0) < kTileCells ? (a.F - k0) : kTileCells;
+  const uint8_t* crow = count + i * a.F + k0;
+  const int32_t* frow = first + i * a.F + k0;
+  for (int64_t x = threadIdx.x; x < kn; x += kThreads) {
+    const uint32_t c = crow[x];
+    const uint64_t sz = uint64_t(sizes[k0 + x]);
+    if (c == 0) {
+      atomicAdd(reinterpret_cast<unsigned long long*>(&h0[x >> kClass0Shift]),
+                static_cast<unsigned long long>(sz));
+    } else {
+      const uint32_t b = bin_of(a, ct, c, frow[x], k0 + x);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&h1[b]), static_cast<unsigned long long>(sz));
+    }
+  }
+  __syncthreads();
+  uint64_t* Hi = H + i * int64_t(a.nbin + 1);
+  for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads)
+    if (h1[b]) atomicAdd(reinterpret_cast<unsigned long long*>(&Hi[b]),
+                         static_cast<unsigned long long>(h1[b]));
+  const uint32_t nb0_tile = uint32_t((kn + (1 << kClass0Shift) - 1) >> kClass0Shift);
+  for (uint32_t b = threadIdx.x; b < nb0_tile; b += kThreads)
+    Hi[a.nbin1 + uint32_t(k0 >> kClass0Shift) + b] = h0[b];
+}
+
+// -- cut ranges ------------------------------------------------------------------
+// H[i] becomes cum_before (nbin + 1 entries, the last is the row total).
+__global__ void __launch_bounds__(1024)
+plan_cut(PlanArgs a, uint64_t* __restrict__ H, int32_t* __restrict__ ranges) {
+  __shared__ uint64_t tmp[65];
+  const int64_t i = blockIdx.x;
+  uint64_t* Hi = H + i * int64_t(a.nbin + 1);
+  uint64_t carry = 0;
+  for (uint32_t b0 = 0; b0 < a.nbin; b0 += 1024) {
+    const uint32_t b = b0 + threadIdx.x;
+    const uint64_t v = b < a.nbin ? Hi[b] : 0ull;
+    uint64_t total;
+    const uint64_t ex = block_exclusive_scan64(v, tmp, &total);
+    if (b < a.nbin) Hi[b] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0) Hi[a.nbin] = carry;
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  const uint64_t total = carry;
+  const int32_t nbin = int32_t(a.nbin);
+  uint64_t s_lo = 0, s_hi = 0;
+  int32_t* rg = ranges + i * 2 * a.J;
+  for (int j = 0; j < a.J; ++j) {
+    const uint64_t cap = uint64_t(a.caps[j]);
+    const uint64_t t_lo = s_lo + cap < s_lo ? ~0ull : s_lo + cap;
+    const uint64_t t_hi = s_hi + cap < s_hi ? ~0ull : s_hi + cap;
+    if (t_lo >= total) {
+      for (int jj = j; jj < a.J; ++jj) {
+        rg[2 * jj] = nbin;
+        rg[2 * jj + 1] = nbin;
+      }
+      return;
+    }
+    // lo: first bin b with cum_after(b) = Hi[b+1] > t_lo
+    int32_t lo = 1, hi = nbin;  // search x in [1, nbin] for the first Hi[x] > t_lo
+    while (lo < hi) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (Hi[mid] > t_lo) hi = mid; else lo = mid + 1;
+    }
+    const int32_t blo = lo - 1;
+    // hi: last bin b < nbin with cum_before(b) = Hi[b] <= t_hi
+    lo = 0;
+    hi = nbin - 1;
+    while (lo < hi) {
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if (Hi[mid] <= t_hi) lo = mid; else hi = mid - 1;
+    }
+    const int32_t bhi = lo;
+    rg[2 * j] = blo;
+    rg[2 * j + 1] = bhi;
+    s_lo = Hi[blo];
+    s_hi = t_hi < total ? t_hi : total;
+  }
+}
+
+// -- tier write with candidate capture ----------------------------------------------
+struct CandRec {
+  uint64_t key;
+  uint32_t k;
+  uint32_t pad;
+};
+
+__global__ void __launch_bounds__(kThreads)
+plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restrict__ first,
+           const int32_t* __restrict__ ranges, int8_t* __restrict__ tier,
+           CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t ntiles) {
+  __shared__ ClassTable ct;
+  __shared__ int32_t rg[256];
+  const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
+  if (t >= ntiles) return;
+  const int64_t kt = t / a.N, i = t - kt * a.N;
+  build_class_table(a, ct);
+  for (int x = threadIdx.x; x < 2 * a.J; x += kThreads) rg[x] = ranges[i * 2 * a.J + x];
+  __syncthreads();
+  const int64_t k0 = kt * kTileCells;
+  const int64_t kn = (a.F - k0) < kTileCells ? (a.F - k0) : kTileCells;
+  const uint8_t* crow = count + i * a.F + k0;
+  const int32_t* frow = first + i * a.F + k0;
+  int8_t* trow = tier + i * a.F + k0;
+  CandRec* ci = cand + i * int64_t(a.cmax);
+  const uint64_t lt = lanemask_lt();
+  for (int64_t x0 = 0; x0 < kn; x0 += kThreads) {
+    const int64_t x = x0 + threadIdx.x;
+    bool is_cand = false;
+    uint64_t key = 0;
+    if (x < kn) {
+      const uint32_t c = crow[x];
+      const int32_t f = c ? frow[x] : -1;
+      const uint32_t b = bin_of(a, ct, c, f, k0 + x);
+      int tv = 0;
+      for (int j = 0; j < a.J; ++j) {
+        if (int32_t(b) >= rg[2 * j] && int32_t(b) <= rg[2 * j + 1]) is_cand = true;
+        tv += int32_t(b) > rg[2 * j + 1];
+      }
+      trow[x] = is_cand ? int8_t(0) : (tv >= a.J ? int8_t(-1) : int8_t(tv));
+      key = (uint64_t(b) << 32) | (c ? uint64_t(uint32_t(f)) : uint64_t(k0 + x));
+    }
+    const uint64_t m = __ballot(is_cand);
+    if (m) {
+      int32_t basev = 0;
+      const int leader = __ffsll((long long)m) - 1;
+      if (int(__lane_id()) == leader) basev = atomicAdd(&ccount[i], __popcll(m));
+      basev = __shfl(basev, leader, 64);
+      if (is_cand) {
+        const int32_t slot = basev + __popcll(m & lt);
+        if (slot < a.cmax) ci[slot] = CandRec{key, uint32_t(k0 + x), 0u};
+      }
+    }
+  }
+}
+
+// -- exact resolution of the candidates --------------------------------------------------
+struct ResolveSmem {
+  uint64_t key[kCandMax];
+  uint32_t k[kCandMax];
+};
+
+__global__ void __launch_bounds__(kResolveThreads)
+plan_resolve(PlanArgs a, const uint64_t* __restrict__ H, const CandRec* __restrict__ cand,
+             const int32_t* __restrict__ ccount, const int64_t* __restrict__ sizes,
+             int8_t* __restrict__ tier, int64_t* __restrict__ used, int32_t* __restrict__ overflow) {
+  __shared__ ResolveSmem s;
+  const int64_t i = blockIdx.x;
+  const int32_t n = ccount[i];
+  if (threadIdx.x == 0) overflow[i] = n > a.cmax ? 1 : 0;
+  if (n > a.cmax) return;
+  const uint64_t* Hi = H + i * int64_t(a.nbin + 1);
+  const CandRec* ci = cand + i * int64_t(a.cmax);
+  int32_t P2 = 1;
+  while (P2 < n) P2 <<= 1;
+  for (int32_t x = threadIdx.x; x < P2; x += kResolveThreads) {
+    if (x < n) {
+      s.key[x] = ci[x].key;
+      s.k[x] = ci[x].k;
+    } else {
+      s.key[x] = ~0ull;
+      s.k[x] = 0xFFFFFFFFu;
+    }
+  }
+  __syncthreads();
+  // bitonic sort by key (keys are unique)
+  for (int32_t kk = 2; kk <= P2; kk <<= 1) {
+    for (int32_t j = kk >> 1; j > 0; j >>= 1) {
+      for (int32_t x = threadIdx.x; x < P2; x += kResolveThreads) {
+        const int32_t y = x ^ j;
+        if (y > x) {
+          const bool up = (x & kk) == 0;
+          const uint64_t kx = s.key[x], ky = s.key[y];
+          if ((kx > ky) == up) {
+            s.key[x] = ky; s.key[y] = kx;
+            const uint32_t t = s.k[x]; s.k[x] = s.k[y]; s.k[y] = t;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  if (threadIdx.x != 0) return;
+  // replay the greedy fill: definite bins between candidates are added whole
+  int64_t* ui = used + i * a.J;
+  int8_t* trow = tier + i * a.F;
+  int j = 0;
+  uint64_t u = 0;
+  int64_t last_bin = -1;
+  for (int32_t x = 0; x < n; ++x) {
+    const int64_t b = int64_t(s.key[x] >> 32);
+    if (b != last_bin) {
+      const uint64_t gap_start = last_bin < 0 ? 0ull : Hi[last_bin + 1];
+      u += Hi[b] - gap_start;
+      last_bin = b;
+    }
+    const uint64_t sz = uint64_t(sizes[s.k[x]]);
+    while (j < a.J && u + sz > uint64_t(a.caps[j])) {
+      ui[j] = int64_t(u);
+      ++j;
+      u = 0;
+    }
+    if (j < a.J) {
+      trow[s.k[x]] = int8_t(j);
+      u += sz;
+    } else {
+      trow[s.k[x]] = int8_t(-1);
+    }
+  }
+  if (j < a.J) {
+    const uint64_t gap_start = last_bin < 0 ? 0ull : Hi[last_bin + 1];
+    u += Hi[a.nbin] - gap_start;
+    ui[j] = int64_t(u);
+    for (int jj = j + 1; jj < a.J; ++jj) ui[jj] = 0;
+  }
+}
+
+// -- exact fallback: weighted radix select over the whole row ------------------------------
+__global__ void __launch_bounds__(1024)
+plan_exact(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restrict__ first,
+           const int64_t* __restrict__ sizes, const int32_t* __restrict__ overflow,
+           int8_t* __restrict__ tier, int64_t* __restrict__ used) {
+  __shared__ uint64_t hist[256];
+  __shared__ uint64_t cuts[128];
+  __shared__ uint64_t sh_prefix, sh_acc, sh_total;
+  const int64_t i = blockIdx.x;
+  if (!overflow[i]) return;
+  const uint8_t* crow = count + i * a.F;
+  const int32_t* frow = first + i * a.F;
+  int8_t* trow = tier + i * a.F;
+  uint64_t base = 0;        // bytes ranked before the start of tier j
+  uint64_t total = 0;
+  bool at_end = false;
+  for (int j = 0; j < a.J; ++j) {
+    if (at_end) {
+      if (threadIdx.x == 0) {
+        cuts[j] = ~0ull;
+        used[i * a.J + j] = 0;
+      }
+      continue;
+    }
+    const uint64_t target = base + uint64_t(a.caps[j]) < base ? ~0ull : base + uint64_t(a.caps[j]);
+    uint64_t prefix = 0, acc = 0;
+    // 40-bit key, five 8-bit digits from the top
+    for (int level = 0; level < 5; ++level) {
+      const int shift = 32 - 8 * level;
+      for (int d = threadIdx.x; d < 256; d += blockDim.x) hist[d] = 0;
+      __syncthreads();
+      for (int64_t k = threadIdx.x; k < a.F; k += blockDim.x) {
+        const uint32_t c = crow[k];
+        const uint64_t key = rank_key(a, c, c ? frow[k] : -1, k);
+        if (level > 0 && (key >> (shift + 8)) != prefix) continue;
+        atomicAdd(reinterpret_cast<unsigned long long*>(&hist[(key >> shift) & 0xFF]),
+                  static_cast<unsigned long long>(sizes[k]));
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        if (level == 0) {
+          uint64_t t = 0;
+          for (int d = 0; d < 256; ++d) t += hist[d];
+          sh_total = t;
+        }
+        uint64_t run = acc;
+        int d = 0;
+        for (; d < 256; ++d) {
+          if (run + hist[d] > target) break;
+          run += hist[d];
+        }
+        sh_prefix = (prefix << 8) | uint64_t(d < 256 ? d : 255);
+        sh_acc = run;
+      }
+      __syncthreads();
+      if (level == 0) total = sh_total;
+      if (total <= target) break;  // everything left fits
+      prefix = sh_prefix;
+      acc = sh_acc;
+      __syncthreads();
+    }
+    if (total <= target) {
+      if (threadIdx.x == 0) {
+        cuts[j] = ~0ull;
+        used[i * a.J + j] = int64_t(total - base);
+      }
+      at_end = true;
+    } else {
+      if (threadIdx.x == 0) {
+        cuts[j] = prefix;
+        used[i * a.J + j] = int64_t(acc - base);
+      }
+      base = acc;
+    }
+    __syncthreads();
+  }
+  __syncthreads();
+  for (int64_t k = threadIdx.x; k < a.F; k += blockDim.x) {
+    const uint32_t c = crow[k];
+    const uint64_t key = rank_key(a, c, c ? frow[k] : -1, k);
+    int tv = 0;
+    for (int j = 0; j < a.J; ++j) tv += key >= cuts[j];
+    trow[k] = tv >= a.J ? int8_t(-1) : int8_t(tv);
+  }
+}
+
+// Bins per class c >= 1, in proportion to the expected number of cells of
+// class c (a worker reads a sample in each epoch with probability L/F, so
+// counts follow Binomial(E, L/F)); at least one bin per class.
+void class_bins(int64_t F, int64_t E, int64_t L, uint16_t* nbc, uint32_t* nbin1) {
+  const double p = F > 0 ? double(L) / double(F) : 0.0;
+  std::vector<double> pmf(size_t(E) + 1, 0.0);
+  double acc = 0;
+  for (int64_t c = 1; c <= E; ++c) {
+    double lp = lgamma(double(E) + 1) - lgamma(double(c) + 1) - lgamma(double(E - c) + 1);
+    lp += (p > 0 ? double(c) * log(p) : -INFINITY);
+    lp += (p < 1 ? double(E - c) * log1p(-p) : (E - c == 0 ? 0.0 : -INFINITY));
+    pmf[size_t(c)] = exp(lp);
+    acc += pmf[size_t(c)];
+  }
+  uint32_t total = 0;
+  for (int64_t c = 0; c < 256; ++c) nbc[c] = 0;
+  for (int64_t c = 1; c <= E; ++c) {
+    double share = acc > 0 ? pmf[size_t(c)] / acc : 1.0 / double(E);
+    double want = floor(share * double(kBins1Budget));
+    if (!(want >= 1.0)) want = 1.0;
+    if (want > 4096.0) want = 4096.0;
+    nbc[c] = uint16_t(want);
+    total += nbc[c];
+  }
+  *nbin1 = total;
+}
+
+}  // namespace
+
+int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
+              const int64_t* sizes, const int64_t* caps, int32_t J, int8_t* tier, int64_t* used,
+              hipStream_t st) {
+  Shape s;
+  int rc = make_shape(job, &s);
+  if (rc) return rc;
+  if (!count || !first || !sizes || !caps || !tier || !used)
+    return fail(NOPFS_EINVAL, "count, first, sizes, caps, tier and used must be non-NULL");
+  if (J < 1) return fail(NOPFS_EINVAL, "J must be >= 1");
+  if (J > 127) return fail(NOPFS_ERANGE, "J must be <= 127");
+  for (int j = 0; j < J; ++j)
+    if (caps[j] < 0) return fail(NOPFS_EINVAL, "capacities must be >= 0");
+
+  PlanArgs a;
+  a.F = s.F;
+  a.N = s.N;
+  a.M_max = s.M_max;
+  a.E = int32_t(s.E);
+  a.J = J;
+  class_bins(s.F, s.E, s.L, a.nbc, &a.nbin1);
+  a.nb0 = uint32_t(ceil_div(s.F, int64_t(1) << kClass0Shift));
+  a.nbin = a.nbin1 + a.nb0;
+  a.cmax = kCandMax;
+  if (debug_value(2) > 0 && debug_value(2) < kCandMax) a.cmax = int32_t(debug_value(2));
+  for (int j = 0; j < 128; ++j) a.caps[j] = j < J ? caps[j] : 0;
+
+  Scratch scr(st);
+  uint64_t* H;
+  int32_t *ranges, *ccount, *overflow;
+  CandRec* cand;
+  const int64_t hn = s.N * int64_t(a.nbin + 1);
+  if ((rc = scr.alloc_n(&H, size_t(hn)))) return rc;
+  if ((rc = scr.alloc_n(&ranges, size_t(s.N * 2 * J)))) return rc;
+  if ((rc = scr.alloc_n(&ccount, size_t(s.N)))) return rc;
+  if ((rc = scr.alloc_n(&overflow, size_t(s.N)))) return rc;
+  if ((rc = scr.alloc_n(&cand, size_t(s.N * a.cmax)))) return rc;
+
+  int64_t fb = ceil_div(hn, 1024);
+  if (fb > 65536) fb = 65536;
+  if ((rc = launch("fill_u64", fill_u64, dim3(uint32_t(fb)), dim3(256), 0, st, H, hn))) return rc;
+  if ((rc = launch("fill_i32", fill_i32, dim3(uint32_t(ceil_div(s.N, 256))), dim3(256), 0, st, ccount,
+                   s.N)))
+    return rc;
+  const uint32_t ntiles = uint32_t(s.N * ceil_div(s.F, kTileCells));
+  if ((rc = launch("plan_hist", plan_hist, dim3(xcd_padded(ntiles)), dim3(kThreads),
+                   size_t(a.nbin1) * 8, st, a, count, first, sizes, H, ntiles)))
+    return rc;
+  if ((rc = launch("plan_cut", plan_cut, dim3(uint32_t(s.N)), dim3(1024), 0, st, a, H, ranges)))
+    return rc;
+  if ((rc = launch("plan_write", plan_write, dim3(xcd_padded(ntiles)), dim3(kThreads), 0, st, a,
+                   count, first, (const int32_t*)ranges, tier, cand, ccount, ntiles)))
+    return rc;
+  if ((rc = launch("plan_resolve", plan_resolve, dim3(uint32_t(s.N)), dim3(kResolveThreads), 0, st,
+                   a, (const uint64_t*)H, (const CandRec*)cand, (const int32_t*)ccount, sizes, tier,
+                   used, overflow)))
+    return rc;
+  if ((rc = launch("plan_exact", plan_exact, dim3(uint32_t(s.N)), dim3(1024), 0, st, a, count, first,
+                   sizes, (const int32_t*)overflow, tier, used)))
+    return rc;
+  return NOPFS_OK;
+}
+
+}  // namespace nopfs
+
+extern "C" int nopfs_tier_plan(const nopfs_job* job, const uint8_t* count, const int32_t* first,
+                               const int64_t* sizes, const int64_t* caps, int32_t J, int8_t* tier,
+                               int64_t* used, void* hip_stream) {
+  try {
+    return nopfs::plan_impl(job, count, first, sizes, caps, J, tier, used,
+                            static_cast<hipStream_t>(hip_stream));
+  } catch (const std::bad_alloc&) {
+    return nopfs::fail(NOPFS_ENOMEM, "host allocation failed");
+  } catch (...) {
+    return nopfs::fail(NOPFS_EDEVICE, "unexpected host exception");
+  }
+}

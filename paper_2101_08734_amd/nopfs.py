@@ -1,0 +1,230 @@
+"""Python binding of libnopfs.so (argument marshalling only).
+
+Every computation runs in the library's HIP kernels; this module only turns
+torch tensors (device memory) and torch's current stream into the C ABI's
+pointers. It raises ``NopfsError`` for a non-zero status and ``RuntimeError``
+if the compiled library is missing: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch  # loads the HIP runtime before the library does
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnopfs.so")
+
+NOPFS_OK, NOPFS_EINVAL, NOPFS_ERANGE, NOPFS_ENOMEM, NOPFS_EDEVICE = 0, -1, -2, -3, -4
+
+
+class NopfsError(RuntimeError):
+    def __init__(self, code: int, what: str, detail: str):
+        super().__init__(f"{what}: status {code} ({detail})")
+        self.code = code
+
+
+class _Job(ctypes.Structure):
+    _fields_ = [("F", ctypes.c_int64), ("E", ctypes.c_int32),
+                ("N", ctypes.c_int32), ("B", ctypes.c_int32),
+                ("drop_last", ctypes.c_int32), ("seed", ctypes.c_uint64)]
+
+
+@dataclass(frozen=True)
+class Job:
+    """A training job as the paper states it: F samples, E epochs, N workers,
+    per-worker batch B, drop_last, shuffle seed."""
+    F: int
+    E: int
+    N: int
+    B: int
+    drop_last: int = 1
+    seed: int = 42
+
+    def c(self) -> _Job:
+        return _Job(int(self.F), int(self.E), int(self.N), int(self.B),
+                    int(self.drop_last), int(self.seed) & ((1 << 64) - 1))
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Loads the compiled library (fails loudly if it was not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python paper_2101_08734_amd/build.py` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        jp = ctypes.POINTER(_Job)
+        sig = {
+            "nopfs_stream_shape": [jp, P, P, P],
+            "nopfs_access_streams": [jp, P, P],
+            "nopfs_access_stats": [jp, P, P, P, P],
+            "nopfs_reuse_next": [jp, P, P, P],
+            "nopfs_tier_plan": [jp, P, P, P, P, I32, P, P, P],
+            "nopfs_profile_enable": [ctypes.c_int],
+            "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
+                                    ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)],
+            "nopfs_calibration_copy": [P, P, I64, P],
+            "nopfs_debug_set": [ctypes.c_int, I64],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        L.nopfs_strerror.argtypes = [ctypes.c_int]
+        L.nopfs_strerror.restype = ctypes.c_char_p
+        L.nopfs_last_error.argtypes = []
+        L.nopfs_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_stats",
+            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_strerror",
+            "nopfs_last_error", "nopfs_profile_enable", "nopfs_profile_query",
+            "nopfs_calibration_copy", "nopfs_debug_set")
+
+
+def _check(rc: int, what: str):
+    if rc != NOPFS_OK:
+        L = lib()
+        detail = L.nopfs_last_error().decode() or L.nopfs_strerror(rc).decode()
+        raise NopfsError(rc, what, detail)
+
+
+def _ptr(t) -> ctypes.c_void_p:
+    if t is None:
+        return ctypes.c_void_p(0)
+    if isinstance(t, int):
+        return ctypes.c_void_p(t)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _device_tensor(t, dtype, shape, name):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)}")
+    return t
+
+
+def stream_shape(job: Job):
+    """(T, M_max, [M_i]) on the host; no GPU needed."""
+    T = ctypes.c_int64()
+    M = ctypes.c_int64()
+    Mw = (ctypes.c_int64 * int(job.N))()
+    j = job.c()
+    _check(lib().nopfs_stream_shape(ctypes.byref(j), ctypes.byref(T), ctypes.byref(M), Mw),
+           "nopfs_stream_shape")
+    return T.value, M.value, list(Mw)
+
+
+def access_streams(job: Job, R=None, stream=None):
+    _, M, _ = stream_shape(job)
+    if R is None:
+        R = torch.empty((job.N, M), dtype=torch.int32, device="cuda")
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    j = job.c()
+    _check(lib().nopfs_access_streams(ctypes.byref(j), _ptr(R), _stream(stream)),
+           "nopfs_access_streams")
+    return R
+
+
+def access_stats(job: Job, R, count=None, first=None, stream=None):
+    _, M, _ = stream_shape(job)
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    if count is None:
+        count = torch.empty((job.N, job.F), dtype=torch.uint8, device="cuda")
+    if first is None:
+        first = torch.empty((job.N, job.F), dtype=torch.int32, device="cuda")
+    _device_tensor(count, torch.uint8, (job.N, job.F), "count")
+    _device_tensor(first, torch.int32, (job.N, job.F), "first")
+    j = job.c()
+    _check(lib().nopfs_access_stats(ctypes.byref(j), _ptr(R), _ptr(count), _ptr(first),
+                                    _stream(stream)), "nopfs_access_stats")
+    return count, first
+
+
+def reuse_next(job: Job, R, next=None, stream=None):
+    _, M, _ = stream_shape(job)
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    if next is None:
+        next = torch.empty((job.N, M), dtype=torch.int32, device="cuda")
+    _device_tensor(next, torch.int32, (job.N, M), "next")
+    j = job.c()
+    _check(lib().nopfs_reuse_next(ctypes.byref(j), _ptr(R), _ptr(next), _stream(stream)),
+           "nopfs_reuse_next")
+    return next
+
+
+def tier_plan(job: Job, count, first, sizes, caps, tier=None, used=None, stream=None):
+    """caps: host sequence of per-worker tier capacities (bytes), fastest first."""
+    _device_tensor(count, torch.uint8, (job.N, job.F), "count")
+    _device_tensor(first, torch.int32, (job.N, job.F), "first")
+    _device_tensor(sizes, torch.int64, (job.F,), "sizes")
+    caps_list = [int(c) for c in caps]
+    J = len(caps_list)
+    caps_host = (ctypes.c_int64 * max(J, 1))(*caps_list)
+    if tier is None:
+        tier = torch.empty((job.N, job.F), dtype=torch.int8, device="cuda")
+    if used is None:
+        used = torch.empty((job.N, max(J, 1)), dtype=torch.int64, device="cuda")
+    _device_tensor(tier, torch.int8, (job.N, job.F), "tier")
+    _device_tensor(used, torch.int64, (job.N, max(J, 1)), "used")
+    j = job.c()
+    _check(lib().nopfs_tier_plan(ctypes.byref(j), _ptr(count), _ptr(first), _ptr(sizes),
+                                 ctypes.cast(caps_host, ctypes.c_void_p), J, _ptr(tier),
+                                 _ptr(used), _stream(stream)), "nopfs_tier_plan")
+    return tier, used
+
+
+def plan(job: Job, sizes, caps, stream=None):
+    """The whole path: streams, stats, next use, tier plan (all on device)."""
+    R = access_streams(job, stream=stream)
+    count, first = access_stats(job, R, stream=stream)
+    nxt = reuse_next(job, R, stream=stream)
+    tier, used = tier_plan(job, count, first, sizes, caps, stream=stream)
+    return dict(R=R, count=count, first=first, next=nxt, tier=tier, used=used)
+
+
+# -- measurement aids -----------------------------------------------------------
+def profile_enable(on: bool):
+    _check(lib().nopfs_profile_enable(1 if on else 0), "nopfs_profile_enable")
+
+
+def profile_results():
+    """{kernel name: (launches, total ms)} for kernels since profile_enable(True)."""
+    out = {}
+    idx = 0
+    while True:
+        name = ctypes.c_char_p()
+        n = ctypes.c_int64()
+        ms = ctypes.c_double()
+        rc = lib().nopfs_profile_query(idx, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms))
+        if rc == NOPFS_EINVAL:
+            break
+        _check(rc, "nopfs_profile_query")
+        out[name.value.decode()] = (n.value, ms.value)
+        idx += 1
+    return out
+
+
+def calibration_copy(src, dst, nbytes: int, stream=None):
+    _check(lib().nopfs_calibration_copy(_ptr(src), _ptr(dst), int(nbytes), _stream(stream)),
+           "nopfs_calibration_copy")
+
+
+def debug_set(which: int, value: int):
+    _check(lib().nopfs_debug_set(int(which), int(value)), "nopfs_debug_set")

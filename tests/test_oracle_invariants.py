@@ -69,3 +69,14 @@ def test_sample_columns_agree(oracle, F, E, N, B, d, seed):
                 continue
             assert R[i, f] == k
             assert nxt[i, f] == cols["occ_next"][e, s_idx]
+
+
+def test_row_variants_agree(oracle):
+    job = oracle.make_job(3_001, 5, 7, 4, 0, 23)
+    R = oracle.access_streams(job)
+    count, first = oracle.access_stats(job, R)
+    nxt = oracle.reuse_next(job, R)
+    c2, f2 = oracle.access_stats_rows(job, R[3:6], 3)
+    np.testing.assert_array_equal(c2, count[3:6])
+    np.testing.assert_array_equal(f2, first[3:6])
+    np.testing.assert_array_equal(oracle.reuse_next_rows(job, R[2:7], 2), nxt[2:7])
