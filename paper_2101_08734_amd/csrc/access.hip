@@ -37,11 +37,32 @@ constexpr int kScShift = 14;
 constexpr int kSC = 1 << kScShift;  // reads per sub-chunk
 constexpr uint32_t kJMask = kSC - 1;
 constexpr uint32_t kMaxWindows = 8192;  // sample windows per worker
-constexpr int kThreads = 256;
-constexpr int kStatsWin = 16384;        // samples held in LDS by stats_tile
-constexpr int kNextWin = 4096;          // samples per next_tile window (fast path)
-constexpr int kNextEnt = 4096;          // reads per next_tile window (fast path)
-constexpr int kSlowWin = 16384;         // samples per pass of the epoch-serial path
+// Tuning knobs (measured on MI355X; see the benchmark notes). Every value
+// gives identical results; only speed changes.
+#ifndef NOPFS_STATS_THREADS
+#define NOPFS_STATS_THREADS 512
+#endif
+#ifndef NOPFS_STATS_WS
+#define NOPFS_STATS_WS 13
+#endif
+#ifndef NOPFS_NEXT_THREADS
+#define NOPFS_NEXT_THREADS 256
+#endif
+#ifndef NOPFS_NEXT_ENT
+#define NOPFS_NEXT_ENT 2048
+#endif
+#ifndef NOPFS_NEXT_WSMAX
+#define NOPFS_NEXT_WSMAX 13
+#endif
+
+constexpr int kThreads = 256;  // partition / unpartition workgroups
+constexpr int kStatsThreads = NOPFS_STATS_THREADS;
+constexpr int kNextThreads = NOPFS_NEXT_THREADS;
+static_assert(kNextThreads >= 256 && kNextThreads % 64 == 0, "next_tile needs one thread per bucket");
+static_assert(kStatsThreads >= 64 && kStatsThreads % 64 == 0, "stats_tile block size");
+constexpr int kStatsWin = 1 << NOPFS_STATS_WS;  // samples held in LDS by stats_tile
+constexpr int kNextEnt = NOPFS_NEXT_ENT;   // reads per next_tile window (fast path)
+constexpr int kSlowWin = 8192;          // samples per pass of the epoch-serial path
 
 struct SegParams {
   int64_t F, N, B, L, M_max;
@@ -122,59 +143,129 @@ seg_partition(SegParams p, const int32_t* __restrict__ R, uint32_t* __restrict__
   for (uint32_t q = threadIdx.x; q < len; q += kThreads) Pk[base + q] = stage[q];
 }
 
-// Iterates over every read of window kb of worker i, in batches of runs (one
-// run = the window's slice of one sub-chunk). fn(pos_in_row, f_base, v)
-// receives the read's position in the partitioned row, the stream position
-// of its sub-chunk start, and the packed read.
+// Iterates over every read of window kb of worker i whose epoch lies in
+// [e_lo, e_hi), in batches of runs (one run = the window's slice of one
+// sub-chunk). fn(pos, f_base, v, idx) receives the read's position in the
+// partitioned row, the stream position of its sub-chunk start, the packed
+// read, and its index in the order (epoch, sub-chunk, position in run).
+// Loads are issued four per thread before any is consumed, so the latency
+// of the dependent (offsets -> reads) chain is paid once per batch.
+template <int NT>
 struct RunTable {
-  uint32_t pref[kThreads + 1];
-  int64_t start[kThreads];  // position in the row of the run's first read
-  int64_t fbase[kThreads];  // stream position of the sub-chunk start
+  uint32_t pref[NT + 1];
+  int32_t start[NT];  // position in the row of the run's first read
+  int32_t fbase[NT];  // stream position of the sub-chunk start
   uint32_t tmp[65];
 };
 
-template <typename Fn>
-__device__ __forceinline__ void for_each_read(const SegParams& p, int64_t i, uint32_t kb,
-                                              const uint16_t* __restrict__ O, RunTable& rt,
-                                              int64_t e_lo, int64_t e_hi, Fn fn) {
+// Loads the run table of runs [r0, r0 + NT) of epochs [e_lo, e_hi)
+// and returns the number of reads they hold. Leaves rt ready for lookups.
+template <int NT>
+__device__ __forceinline__ uint32_t load_runs(const SegParams& p, int64_t i, uint32_t kb,
+                                              const uint16_t* __restrict__ OT, RunTable<NT>& rt,
+                                              int64_t e_lo, int64_t runs, int64_t r0) {
   const int64_t Li = seg_len(p, i);
-  const int64_t runs = (e_hi - e_lo) * p.nsc;
-  for (int64_t r0 = 0; r0 < runs; r0 += kThreads) {
-    const int64_t r = r0 + threadIdx.x;
-    uint32_t len = 0;
-    if (r < runs) {
-      const int64_t e = e_lo + r / p.nsc, sc = r % p.nsc;
-      const uint16_t* o = O + orow(p, i, e, sc);
-      const uint32_t a = o[kb], b = o[kb + 1];
-      len = b - a;
-      rt.fbase[threadIdx.x] = e * Li + sc * kSC;
-      rt.start[threadIdx.x] = e * Li + sc * kSC + a;
-    }
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan(len, rt.tmp, &total);
-    rt.pref[threadIdx.x] = ex;
-    if (threadIdx.x == 0) rt.pref[kThreads] = total;
-    __syncthreads();
-    const int nr = int(runs - r0 < kThreads ? runs - r0 : kThreads);
-    for (uint32_t t = threadIdx.x; t < total; t += kThreads) {
-      int lo = 0, hi = nr - 1;  // last run with pref <= t
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (rt.pref[mid] <= t) lo = mid; else hi = mid - 1;
+  const int64_t R = int64_t(p.E) * p.nsc;
+  const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * R;  // window kb: run starts
+  const uint16_t* ob = oa + R;                            // window kb+1: run ends
+  const int64_t r = r0 + threadIdx.x;
+  uint32_t len = 0;
+  if (r < runs) {
+    const int64_t run = e_lo * p.nsc + r;
+    const int64_t e = run / p.nsc, sc = run % p.nsc;
+    const uint32_t a = oa[run], b = ob[run];
+    len = b - a;
+    rt.fbase[threadIdx.x] = int32_t(e * Li + sc * kSC);
+    rt.start[threadIdx.x] = int32_t(e * Li + sc * kSC + a);
+  }
+  uint32_t total;
+  const uint32_t ex = block_exclusive_scan(len, rt.tmp, &total);
+  rt.pref[threadIdx.x] = ex;
+  __syncthreads();
+  return total;
+}
+
+// Window-major copy of the partition offsets: OT[i][b][run] = O[i][run][b],
+// so a tile reads the starts and ends of all its runs contiguously.
+__global__ void __launch_bounds__(256)
+offsets_transpose(SegParams p, const uint16_t* __restrict__ O, uint16_t* __restrict__ OT) {
+  __shared__ uint16_t tile[64][65];
+  const int64_t R = int64_t(p.E) * p.nsc;
+  const int64_t C = int64_t(p.nbk) + 1;
+  const int64_t i = blockIdx.z;
+  const int64_t r0 = int64_t(blockIdx.x) * 64, c0 = int64_t(blockIdx.y) * 64;
+  const uint16_t* src = O + i * R * C;
+  uint16_t* dst = OT + i * R * C;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t r = r0 + y, c = c0 + tx;
+    if (r < R && c < C) tile[y][tx] = src[r * C + c];
+  }
+  __syncthreads();
+  for (int y = ty; y < 64; y += 4) {
+    const int64_t c = c0 + y, r = r0 + tx;
+    if (r < R && c < C) dst[c * R + r] = tile[tx][y];
+  }
+}
+
+// Calls fn(pos, f_base, v, idx) for the `total` reads of the loaded runs:
+// pos is the read's position in the partitioned row, f_base the stream
+// position of its sub-chunk start, v the packed read and idx its running
+// index in (epoch, sub-chunk, position) order. Four loads per thread are in
+// flight before any is consumed.
+template <int NT, typename Fn>
+__device__ __forceinline__ void consume_runs(const RunTable<NT>& rt, int nr, uint32_t total,
+                                             const uint32_t* __restrict__ prow, uint32_t done,
+                                             Fn fn) {
+  for (uint32_t t0 = threadIdx.x; t0 < total; t0 += 4 * NT) {
+    int64_t pos[4], fb[4];
+    uint32_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t t = t0 + u * NT;
+      pos[u] = -1;
+      fb[u] = 0;
+      if (t < total) {
+        int lo = 0, hi = nr - 1;  // last run with pref <= t
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (rt.pref[mid] <= t) lo = mid; else hi = mid - 1;
+        }
+        pos[u] = rt.start[lo] + (t - rt.pref[lo]);
+        fb[u] = rt.fbase[lo];
       }
-      const int64_t pos = rt.start[lo] + (t - rt.pref[lo]);
-      fn(pos, rt.fbase[lo], t + 0u);
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = pos[u] >= 0 ? prow[pos[u]] : 0u;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (pos[u] >= 0) fn(pos[u], fb[u], v[u], done + t0 + u * NT);
+  }
+}
+
+template <int NT, typename Fn>
+__device__ __forceinline__ void for_each_read(const SegParams& p, int64_t i, uint32_t kb,
+                                              const uint16_t* __restrict__ O,
+                                              const uint32_t* __restrict__ prow, RunTable<NT>& rt,
+                                              int64_t e_lo, int64_t e_hi, Fn fn) {
+  const int64_t runs = (e_hi - e_lo) * p.nsc;
+  uint32_t done = 0;
+  for (int64_t r0 = 0; r0 < runs; r0 += NT) {
+    const uint32_t total = load_runs(p, i, kb, O, rt, e_lo, runs, r0);
+    const int nr = int(runs - r0 < NT ? runs - r0 : NT);
+    consume_runs(rt, nr, total, prow, done, fn);
+    done += total;
     __syncthreads();
   }
 }
 
 // -- stats --------------------------------------------------------------------
-__global__ void __launch_bounds__(kThreads)
-stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ O,
+template <bool kVec>
+__global__ void __launch_bounds__(kStatsThreads)
+stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
            uint8_t* __restrict__ count, int32_t* __restrict__ first, uint32_t ntiles) {
   extern __shared__ uint32_t sm[];
-  __shared__ RunTable rt;
+  __shared__ RunTable<kStatsThreads> rt;
   uint32_t* cw = sm;                                   // kStatsWin / 4 words of byte counters
   int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsWin / 4);
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
@@ -187,12 +278,11 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   const uint32_t* prow = Pk + i * p.M_max;
   for (int64_t w0 = k0; w0 < kend; w0 += kStatsWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kStatsWin ? kend - w0 : kStatsWin);
-    for (uint32_t x = threadIdx.x; x < (wlen + 3) / 4; x += kThreads) cw[x] = 0;
-    for (uint32_t x = threadIdx.x; x < wlen; x += kThreads) fi[x] = INT_MAX;
+    for (uint32_t x = threadIdx.x; x < (wlen + 3) / 4; x += kStatsThreads) cw[x] = 0;
+    for (uint32_t x = threadIdx.x; x < wlen; x += kStatsThreads) fi[x] = INT_MAX;
     __syncthreads();
     const uint32_t xoff = uint32_t(w0 - k0);
-    for_each_read(p, i, kb, O, rt, 0, p.E, [&](int64_t pos, int64_t fbase, uint32_t) {
-      const uint32_t v = prow[pos];
+    for_each_read(p, i, kb, OT, prow, rt, 0, p.E, [&](int64_t, int64_t fbase, uint32_t v, uint32_t) {
       const uint32_t x = (v >> kScShift) - xoff;
       if (x < wlen) {
         atomicAdd(&cw[x >> 2], 1u << ((x & 3u) * 8u));
@@ -202,19 +292,43 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     __syncthreads();
     uint8_t* crow = count + i * p.F + w0;
     int32_t* frow = first + i * p.F + w0;
-    for (uint32_t x = threadIdx.x; x < wlen; x += kThreads) {
-      const uint32_t c = (cw[x >> 2] >> ((x & 3u) * 8u)) & 0xFFu;
+    auto cnt_at = [&](uint32_t x) { return (cw[x >> 2] >> ((x & 3u) * 8u)) & 0xFFu; };
+    // cells up to the first flat index divisible by 4 and after the last
+    // group of 4 go one per thread; the rest as 4-cell groups per lane
+    uint32_t head = kVec ? uint32_t((4 - ((i * p.F + w0) & 3)) & 3) : wlen;
+    if (head > wlen) head = wlen;
+    const uint32_t nunits = (wlen - head) >> 2;
+    const uint32_t tail0 = head + 4 * nunits;
+    for (uint32_t x = threadIdx.x; x < head; x += kStatsThreads) {
+      const uint32_t c = cnt_at(x);
       crow[x] = uint8_t(c);
       frow[x] = c ? fi[x] : -1;
+    }
+    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kStatsThreads) {
+      const uint32_t c = cnt_at(x);
+      crow[x] = uint8_t(c);
+      frow[x] = c ? fi[x] : -1;
+    }
+    for (uint32_t u = threadIdx.x; u < nunits; u += kStatsThreads) {
+      const uint32_t x = head + 4 * u;
+      const uint32_t c0 = cnt_at(x), c1 = cnt_at(x + 1), c2 = cnt_at(x + 2), c3 = cnt_at(x + 3);
+      *reinterpret_cast<uint32_t*>(crow + x) = c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
+      *reinterpret_cast<int4*>(frow + x) =
+          make_int4(c0 ? fi[x] : -1, c1 ? fi[x + 1] : -1, c2 ? fi[x + 2] : -1, c3 ? fi[x + 3] : -1);
     }
     __syncthreads();
   }
 }
 
 // -- next ---------------------------------------------------------------------
+// Fast path: the window's reads are gathered into LDS in (epoch, sub-chunk)
+// order, counting-sorted by the top 8 bits of their sample offset, and each
+// of the 256 buckets (about a dozen reads) is insertion-sorted by (sample,
+// position). In that order the read that follows a read of the same sample
+// is its next use.
 struct NextSmem {
-  uint32_t start[kNextWin];
-  uint32_t cur[kNextWin];
+  uint32_t hist[256];
+  uint32_t cur[256];
   int32_t f[kNextEnt];
   int32_t pos[kNextEnt];
   uint16_t kl[kNextEnt];
@@ -222,35 +336,35 @@ struct NextSmem {
 };
 
 __device__ void next_tile_slow(const SegParams& p, int64_t i, uint32_t kb, const uint32_t* prow,
-                               const uint16_t* O, int32_t* nrow, RunTable& rt, int32_t* last) {
+                               const uint16_t* O, int32_t* nrow, RunTable<kNextThreads>& rt, int32_t* last) {
   const int64_t W = int64_t(1) << p.ws;
   const int64_t k0 = int64_t(kb) * W;
   const int64_t kend = k0 + W < p.F ? k0 + W : p.F;
   for (int64_t w0 = k0; w0 < kend; w0 += kSlowWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kSlowWin ? kend - w0 : kSlowWin);
     const uint32_t xoff = uint32_t(w0 - k0);
-    for (uint32_t x = threadIdx.x; x < wlen; x += kThreads) last[x] = -1;
+    for (uint32_t x = threadIdx.x; x < wlen; x += kNextThreads) last[x] = -1;
     __syncthreads();
     for (int64_t e = p.E - 1; e >= 0; --e) {
       // reads of one epoch are distinct samples: no two threads share a slot
-      for_each_read(p, i, kb, O, rt, e, e + 1, [&](int64_t pos, int64_t fbase, uint32_t) {
-        const uint32_t v = prow[pos];
-        const uint32_t x = (v >> kScShift) - xoff;
-        if (x < wlen) {
-          nrow[pos] = last[x];
-          last[x] = int32_t(fbase + (v & kJMask));
-        }
-      });
+      for_each_read(p, i, kb, O, prow, rt, e, e + 1,
+                    [&](int64_t pos, int64_t fbase, uint32_t v, uint32_t) {
+                      const uint32_t x = (v >> kScShift) - xoff;
+                      if (x < wlen) {
+                        nrow[pos] = last[x];
+                        last[x] = int32_t(fbase + (v & kJMask));
+                      }
+                    });
       __syncthreads();
     }
   }
 }
 
-__global__ void __launch_bounds__(kThreads)
-next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ O,
+__global__ void __launch_bounds__(kNextThreads)
+next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
           int32_t* __restrict__ nextP, uint32_t ntiles) {
   extern __shared__ uint32_t sm[];
-  __shared__ RunTable rt;
+  __shared__ RunTable<kNextThreads> rt;
   __shared__ uint32_t s_total;
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
@@ -258,110 +372,89 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
   const uint32_t kb = tile - uint32_t(i) * p.nbk;
   const uint32_t* prow = Pk + i * p.M_max;
   int32_t* nrow = nextP + i * p.M_max;
-  const uint32_t W = 1u << p.ws;
+  const int64_t runs = int64_t(p.E) * p.nsc;
 
-  // number of reads in the window
-  if (threadIdx.x == 0) s_total = 0;
-  __syncthreads();
-  {
+  // number of reads in the window; with at most kNextThreads runs the run
+  // table loaded here is reused for the gather below
+  uint32_t total;
+  if (runs <= kNextThreads) {
+    total = load_runs(p, i, kb, OT, rt, 0, runs, 0);
+  } else {
+    if (threadIdx.x == 0) s_total = 0;
+    __syncthreads();
+    const int64_t R = runs;
+    const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * R;
     uint32_t mine = 0;
-    const int64_t runs = int64_t(p.E) * p.nsc;
-    for (int64_t r = threadIdx.x; r < runs; r += kThreads) {
-      const uint16_t* o = O + orow(p, i, r / p.nsc, r % p.nsc);
-      mine += uint32_t(o[kb + 1] - o[kb]);
-    }
+    for (int64_t r = threadIdx.x; r < runs; r += kNextThreads) mine += uint32_t(oa[R + r] - oa[r]);
     atomicAdd(&s_total, mine);
+    __syncthreads();
+    total = s_total;
   }
-  __syncthreads();
-  const uint32_t total = s_total;
   if (total == 0) return;
-  if (W > uint32_t(kNextWin) || total > uint32_t(p.ent_cap)) {
-    next_tile_slow(p, i, kb, prow, O, nrow, rt, reinterpret_cast<int32_t*>(sm));
+  if (p.ws > 16 || total > uint32_t(p.ent_cap)) {
+    __syncthreads();
+    next_tile_slow(p, i, kb, prow, OT, nrow, rt, reinterpret_cast<int32_t*>(sm));
     return;
   }
   NextSmem& s = *reinterpret_cast<NextSmem*>(sm);
-  for (uint32_t x = threadIdx.x; x < W; x += kThreads) s.start[x] = 0;
+  const int dshift = p.ws > 8 ? p.ws - 8 : 0;
+  if (threadIdx.x < 256) s.hist[threadIdx.x] = 0;
   __syncthreads();
-  // gather the window's reads; the flat index runs over (epoch, sub-chunk)
-  uint32_t base = 0;
-  {
-    const int64_t runs = int64_t(p.E) * p.nsc;
-    const int64_t Li = seg_len(p, i);
-    for (int64_t r0 = 0; r0 < runs; r0 += kThreads) {
-      const int64_t r = r0 + threadIdx.x;
-      uint32_t len = 0;
-      if (r < runs) {
-        const int64_t e = r / p.nsc, sc = r % p.nsc;
-        const uint16_t* o = O + orow(p, i, e, sc);
-        const uint32_t a = o[kb], b = o[kb + 1];
-        len = b - a;
-        rt.fbase[threadIdx.x] = e * Li + sc * kSC;
-        rt.start[threadIdx.x] = e * Li + sc * kSC + a;
-      }
-      uint32_t tot;
-      const uint32_t ex = block_exclusive_scan(len, rt.tmp, &tot);
-      rt.pref[threadIdx.x] = ex;
-      __syncthreads();
-      const int nr = int(runs - r0 < kThreads ? runs - r0 : kThreads);
-      for (uint32_t t = threadIdx.x; t < tot; t += kThreads) {
-        int lo = 0, hi = nr - 1;
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if (rt.pref[mid] <= t) lo = mid; else hi = mid - 1;
-        }
-        const int64_t pos = rt.start[lo] + (t - rt.pref[lo]);
-        const uint32_t v = prow[pos];
-        const uint32_t idx = base + t;
-        const uint32_t x = v >> kScShift;
-        s.kl[idx] = uint16_t(x);
-        s.f[idx] = int32_t(rt.fbase[lo] + (v & kJMask));
-        s.pos[idx] = int32_t(pos);
-        atomicAdd(&s.start[x], 1u);
-      }
-      base += tot;
-      __syncthreads();
-    }
+  auto gather = [&](int64_t pos, int64_t fbase, uint32_t v, uint32_t idx) {
+    const uint32_t x = v >> kScShift;
+    s.kl[idx] = uint16_t(x);
+    s.f[idx] = int32_t(fbase + (v & kJMask));
+    s.pos[idx] = int32_t(pos);
+    atomicAdd(&s.hist[x >> dshift], 1u);
+  };
+  if (runs <= kNextThreads) {
+    consume_runs(rt, int(runs), total, prow, 0u, gather);
+    __syncthreads();
+  } else {
+    for_each_read(p, i, kb, OT, prow, rt, 0, p.E, gather);
   }
-  // bucket starts
   {
-    uint32_t carry = 0;
-    for (uint32_t x0 = 0; x0 < W; x0 += kThreads) {
-      const uint32_t x = x0 + threadIdx.x;
-      const uint32_t v = x < W ? s.start[x] : 0u;
-      uint32_t tot;
-      const uint32_t ex = block_exclusive_scan(v, rt.tmp, &tot);
-      if (x < W) {
-        s.start[x] = carry + ex;
-        s.cur[x] = carry + ex;
-      }
-      carry += tot;
+    const uint32_t c = threadIdx.x < 256 ? s.hist[threadIdx.x] : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_scan(c, rt.tmp, &tot);
+    if (threadIdx.x < 256) {
+      s.hist[threadIdx.x] = ex;
+      s.cur[threadIdx.x] = ex;
     }
   }
   __syncthreads();
-  for (uint32_t idx = threadIdx.x; idx < total; idx += kThreads) {
-    const uint32_t slot = atomicAdd(&s.cur[s.kl[idx]], 1u);
+  for (uint32_t idx = threadIdx.x; idx < total; idx += kNextThreads) {
+    const uint32_t slot = atomicAdd(&s.cur[s.kl[idx] >> dshift], 1u);
     s.ord[slot] = uint16_t(idx);
   }
   __syncthreads();
-  // order each bucket by stream position (buckets are short)
-  for (uint32_t x = threadIdx.x; x < W; x += kThreads) {
-    const uint32_t a = s.start[x], b = s.cur[x];
+  if (threadIdx.x < 256) {
+    // bucket d = threadIdx.x: order by (sample offset, stream position)
+    const uint32_t a = s.hist[threadIdx.x], b = s.cur[threadIdx.x];
     for (uint32_t u = a + 1; u < b; ++u) {
       const uint16_t v = s.ord[u];
+      const uint32_t kv = s.kl[v];
       const int32_t fv = s.f[v];
       uint32_t c = u;
-      while (c > a && s.f[s.ord[c - 1]] > fv) {
-        s.ord[c] = s.ord[c - 1];
+      while (c > a) {
+        const uint16_t w = s.ord[c - 1];
+        const uint32_t kw = s.kl[w];
+        if (kw < kv || (kw == kv && s.f[w] < fv)) break;
+        s.ord[c] = w;
         --c;
       }
       s.ord[c] = v;
     }
   }
   __syncthreads();
-  for (uint32_t u = threadIdx.x; u < total; u += kThreads) {
+  for (uint32_t u = threadIdx.x; u < total; u += kNextThreads) {
     const uint32_t idx = s.ord[u];
-    const uint32_t end = s.cur[s.kl[idx]];
-    nrow[s.pos[idx]] = (u + 1 < end) ? s.f[s.ord[u + 1]] : -1;
+    int32_t nx = -1;
+    if (u + 1 < total) {
+      const uint32_t nidx = s.ord[u + 1];
+      if (s.kl[nidx] == s.kl[idx]) nx = s.f[nidx];
+    }
+    nrow[s.pos[idx]] = nx;
   }
 }
 
@@ -425,13 +518,21 @@ size_t partition_smem(const SegParams& p) {
 }
 
 int run_partition(const SegParams& p, const int32_t* R, Scratch& scr, uint32_t** Pk,
-                  uint16_t** O, hipStream_t st) {
+                  uint16_t** OT, hipStream_t st) {
   int rc;
+  uint16_t* O;
+  const size_t on = size_t(p.N * p.E * p.nsc) * (p.nbk + 1);
   if ((rc = scr.alloc_n(Pk, size_t(p.N * p.M_max)))) return rc;
-  if ((rc = scr.alloc_n(O, size_t(p.N * p.E * p.nsc) * (p.nbk + 1)))) return rc;
+  if ((rc = scr.alloc_n(&O, on))) return rc;
+  if ((rc = scr.alloc_n(OT, on))) return rc;
   const int64_t wgs = p.N * p.E * p.nsc;
-  return launch("seg_partition", seg_partition, dim3(uint32_t(wgs)), dim3(kThreads),
-                partition_smem(p), st, p, R, *Pk, *O);
+  if ((rc = launch("seg_partition", seg_partition, dim3(uint32_t(wgs)), dim3(kThreads),
+                   partition_smem(p), st, p, R, *Pk, O)))
+    return rc;
+  const int64_t runs = int64_t(p.E) * p.nsc;
+  return launch("offsets_transpose", offsets_transpose,
+                dim3(uint32_t(ceil_div(runs, 64)), uint32_t(ceil_div(p.nbk + 1, 64)), uint32_t(p.N)),
+                dim3(256), 0, st, p, (const uint16_t*)O, *OT);
 }
 
 }  // namespace
@@ -450,15 +551,21 @@ int stats_impl(const nopfs_job* job, const int32_t* R, uint8_t* count, int32_t* 
     return launch("fill_stats_empty", fill_stats_empty, dim3(uint32_t(blocks)), dim3(256), 0, st, n,
                   count, first);
   }
-  SegParams p = seg_params(s, 14);
+  SegParams p = seg_params(s, NOPFS_STATS_WS);
   Scratch scr(st);
   uint32_t* Pk;
-  uint16_t* O;
-  if ((rc = run_partition(p, R, scr, &Pk, &O, st))) return rc;
+  uint16_t* OT;
+  if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
   const uint32_t ntiles = uint32_t(s.N * p.nbk);
   const size_t smem = size_t(kStatsWin / 4 + kStatsWin) * 4;
-  return launch("stats_tile", stats_tile, dim3(xcd_padded(ntiles)), dim3(kThreads), smem, st, p,
-                (const uint32_t*)Pk, (const uint16_t*)O, count, first, ntiles);
+  // vector stores need 4-byte aligned count rows and 16-byte aligned first rows
+  const bool vec = (reinterpret_cast<uintptr_t>(count) & 3) == 0 &&
+                   (reinterpret_cast<uintptr_t>(first) & 15) == 0;
+  if (vec)
+    return launch("stats_tile", stats_tile<true>, dim3(xcd_padded(ntiles)), dim3(kStatsThreads), smem,
+                  st, p, (const uint32_t*)Pk, (const uint16_t*)OT, count, first, ntiles);
+  return launch("stats_tile", stats_tile<false>, dim3(xcd_padded(ntiles)), dim3(kStatsThreads), smem,
+                st, p, (const uint32_t*)Pk, (const uint16_t*)OT, count, first, ntiles);
 }
 
 int next_impl(const nopfs_job* job, const int32_t* R, int32_t* next, hipStream_t st) {
@@ -467,23 +574,24 @@ int next_impl(const nopfs_job* job, const int32_t* R, int32_t* next, hipStream_t
   if (rc) return rc;
   if (s.M_max == 0) return NOPFS_OK;  // R and next have no elements and may be NULL
   if (!R || !next) return fail(NOPFS_EINVAL, "R and next must be non-NULL");
-  // window width: about half the fast-path capacity of reads per window
+  // window width: about three quarters of the fast-path capacity of reads
   const double reads_per_sample = double(s.M_max) / double(s.F);
   int ws = 0;
-  while (ws < 12 && double(int64_t(1) << (ws + 1)) * reads_per_sample <= kNextEnt / 2) ++ws;
+  while (ws < NOPFS_NEXT_WSMAX && double(int64_t(1) << (ws + 1)) * reads_per_sample <= kNextEnt * 3 / 4)
+    ++ws;
   SegParams p = seg_params(s, ws);
   if (debug_value(2) > 0 && debug_value(2) < kNextEnt) p.ent_cap = int32_t(debug_value(2));
   Scratch scr(st);
   uint32_t* Pk;
-  uint16_t* O;
+  uint16_t* OT;
   int32_t* nextP;
-  if ((rc = run_partition(p, R, scr, &Pk, &O, st))) return rc;
+  if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
   if ((rc = scr.alloc_n(&nextP, size_t(s.N * s.M_max)))) return rc;
   const uint32_t ntiles = uint32_t(s.N * p.nbk);
   size_t smem = sizeof(NextSmem);
   if (smem < size_t(kSlowWin) * 4) smem = size_t(kSlowWin) * 4;
-  if ((rc = launch("next_tile", next_tile, dim3(xcd_padded(ntiles)), dim3(kThreads), smem, st, p,
-                   (const uint32_t*)Pk, (const uint16_t*)O, nextP, ntiles)))
+  if ((rc = launch("next_tile", next_tile, dim3(xcd_padded(ntiles)), dim3(kNextThreads), smem, st, p,
+                   (const uint32_t*)Pk, (const uint16_t*)OT, nextP, ntiles)))
     return rc;
   const int64_t wgs = s.N * s.E * p.nsc;
   if ((rc = launch("next_unpartition", next_unpartition, dim3(uint32_t(wgs)), dim3(kThreads), 0, st, p,

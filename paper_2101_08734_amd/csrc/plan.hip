@@ -8,11 +8,16 @@
 // that no longer fits ("first misfit"), so the plan is fixed by J cut points
 // along the ranking. They are found without sorting the N*F cells:
 //
+//   plan_binsum  -- bytes of every run of 256 consecutive ids.
 //   plan_hist    -- weighted histogram of sizes over rank-ordered bins of the
-//                   key (LDS-privatised). Bins of class count>=1 split the
-//                   first-read range; their number per class follows the
+//                   key, LDS-privatised per (worker, slice of 2^19 samples)
+//                   and flushed once per slice. Bins of class count>=1 split
+//                   the first-read range; their number per class follows the
 //                   expected Binomial(E, L/F) population so crowded classes
-//                   get fine bins. Class 0 is binned by id, 256 ids a bin.
+//                   get fine bins. Class 0 is binned by id, 256 ids a bin,
+//                   and its bytes are the bin's total minus the bytes read.
+//   Both passes over the [N][F] tables read four cells per lane with one
+//   32-bit load of counts and one 128-bit load of first reads.
 //   plan_cut     -- per worker: prefix sums over bins, then for each tier the
 //                   range of bins that can contain its cut (interval
 //                   arithmetic: the cut of tier j depends on where tier j-1
@@ -36,9 +41,10 @@
 namespace nopfs {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kTileCells = 8192;          // samples per (worker, tile)
+constexpr int kThreads = 512;
+constexpr int64_t kSliceCells = int64_t(1) << 19;  // samples per (worker, slice) tile
 constexpr int kClass0Shift = 8;           // 256 ids per class-0 bin
+constexpr int kSliceBins0 = int(kSliceCells >> kClass0Shift);
 constexpr uint32_t kBins1Budget = 4096;   // bins for classes count >= 1
 constexpr int kCandMax = 4096;            // candidate records per worker (LDS sort)
 constexpr int kResolveThreads = 1024;
@@ -102,32 +108,94 @@ __global__ void fill_i32(int32_t* p, int64_t n) {
 }
 
 // -- histogram -----------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+plan_binsum(int64_t F, uint32_t nb0, const int64_t* __restrict__ sizes, uint64_t* __restrict__ binsum) {
+  const uint32_t b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= nb0) return;
+  const int64_t k0 = int64_t(b) << kClass0Shift;
+  uint64_t v = 0;
+  for (int x = __lane_id(); x < (1 << kClass0Shift); x += 64)
+    if (k0 + x < F) v += uint64_t(sizes[k0 + x]);
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  if (__lane_id() == 0) binsum[b] = v;
+}
+
+// Cells of row i in [ks, ke): cells before the first flat index that is a
+// multiple of 4 ("head") and after the last whole group of 4 ("tail") go
+// one per thread; the groups in between go one group per lane. kVec=false
+// (unaligned caller buffers) visits every cell one per thread.
+struct RowSplit {
+  int64_t body0, nunits, tail0;
+};
+
+__device__ __forceinline__ RowSplit split_row(int64_t flat0, int64_t ks, int64_t ke, bool vec) {
+  RowSplit r;
+  if (!vec) {
+    r.body0 = ke; r.nunits = 0; r.tail0 = ke;
+    return r;
+  }
+  int64_t head = (4 - (flat0 & 3)) & 3;
+  if (head > ke - ks) head = ke - ks;
+  r.body0 = ks + head;
+  r.nunits = (ke - r.body0) >> 2;
+  r.tail0 = r.body0 + 4 * r.nunits;
+  return r;
+}
+
+template <bool kVec>
 __global__ void __launch_bounds__(kThreads)
 plan_hist(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restrict__ first,
-          const int64_t* __restrict__ sizes, uint64_t* __restrict__ H, uint32_t ntiles) {
-  extern __shared__ uint64_t h1[];  // nbin1 weighted bins
+          const int64_t* __restrict__ sizes, const uint64_t* __restrict__ binsum,
+          uint64_t* __restrict__ H, uint32_t nslices) {
+  extern __shared__ uint64_t sm[];
+  uint64_t* h1 = sm;                 // nbin1 weighted bins
+  uint64_t* h0 = sm + a.nbin1;       // bytes read, per class-0 bin of the slice
   __shared__ ClassTable ct;
-  __shared__ uint64_t h0[kTileCells >> kClass0Shift];
   const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
-  if (t >= ntiles) return;
-  const int64_t kt = t / a.N, i = t - kt * a.N;
+  if (t >= uint32_t(a.N) * nslices) return;
+  const int64_t sl = t / a.N, i = t - sl * a.N;
   build_class_table(a, ct);
   for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads) h1[b] = 0;
-  for (uint32_t b = threadIdx.x; b < (kTileCells >> kClass0Shift); b += kThreads) h0[b] = 0;
+  for (uint32_t b = threadIdx.x; b < uint32_t(kSliceBins0); b += kThreads) h0[b] = 0;
   __syncthreads();
-  const int64_t k0 = kt * kTileCells;
-  const int64_t kn = (a.F - k0) < kTileCells ? (a.F - k0) : kTileCells;
-  const uint8_t* crow = count + i * a.F + k0;
-  const int32_t* frow = first + i * a.F + k0;
-  for (int64_t x = threadIdx.x; x < kn; x += kThreads) {
-    const uint32_t c = crow[x];
-    const uint64_t sz = uint64_t(sizes[k0 + x]);
-    if (c == 0) {
-      atomicAdd(reinterpret_cast<unsigned long long*>(&h0[x >> kClass0Shift]),
-                static_cast<unsigned long long>(sz));
-    } else {
-      const uint32_t b = bin_of(a, ct, c, frow[x], k0 + x);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&h1[b]), static_cast<unsigned long long>(sz));
+  const int64_t ks = sl * kSliceCells;
+  const int64_t ke = ks + kSliceCells < a.F ? ks + kSliceCells : a.F;
+  const uint8_t* crow = count + i * a.F;
+  const int32_t* frow = first + i * a.F;
+  auto cell = [&](int64_t k, uint32_t c, int32_t f) {
+    if (c != 0) {
+      const unsigned long long sz = static_cast<unsigned long long>(sizes[k]);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_of(a, ct, c, f, k)]), sz);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&h0[(k - ks) >> kClass0Shift]), sz);
+    }
+  };
+  const RowSplit rs = split_row(i * a.F + ks, ks, ke, kVec);
+  for (int64_t k = ks + threadIdx.x; k < rs.body0; k += kThreads) cell(k, crow[k], frow[k]);
+  for (int64_t k = rs.tail0 + threadIdx.x; k < ke; k += kThreads) cell(k, crow[k], frow[k]);
+  constexpr int kU = 4;
+  for (int64_t u0 = 0; u0 < rs.nunits; u0 += kU * kThreads) {
+    uint32_t cw[kU];
+    int4 fw[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int64_t u = u0 + j * kThreads + threadIdx.x;
+      const int64_t k = rs.body0 + 4 * u;
+      if (u < rs.nunits) {
+        cw[j] = *reinterpret_cast<const uint32_t*>(crow + k);
+        fw[j] = *reinterpret_cast<const int4*>(frow + k);
+      } else {
+        cw[j] = 0;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      if (cw[j] == 0) continue;
+      const int64_t k = rs.body0 + 4 * (u0 + j * kThreads + threadIdx.x);
+      cell(k + 0, cw[j] & 0xFFu, fw[j].x);
+      cell(k + 1, (cw[j] >> 8) & 0xFFu, fw[j].y);
+      cell(k + 2, (cw[j] >> 16) & 0xFFu, fw[j].z);
+      cell(k + 3, cw[j] >> 24, fw[j].w);
     }
   }
   __syncthreads();
@@ -135,9 +203,11 @@ plan_hist(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restri
   for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads)
     if (h1[b]) atomicAdd(reinterpret_cast<unsigned long long*>(&Hi[b]),
                          static_cast<unsigned long long>(h1[b]));
-  const uint32_t nb0_tile = uint32_t((kn + (1 << kClass0Shift) - 1) >> kClass0Shift);
-  for (uint32_t b = threadIdx.x; b < nb0_tile; b += kThreads)
-    Hi[a.nbin1 + uint32_t(k0 >> kClass0Shift) + b] = h0[b];
+  // class 0: all bytes of the bin minus the bytes of samples read
+  const uint32_t b0 = uint32_t(ks >> kClass0Shift);
+  const uint32_t nb = uint32_t((ke - ks + (1 << kClass0Shift) - 1) >> kClass0Shift);
+  for (uint32_t b = threadIdx.x; b < nb; b += kThreads)
+    Hi[a.nbin1 + b0 + b] = binsum[b0 + b] - h0[b];
 }
 
 // -- cut ranges ------------------------------------------------------------------
@@ -203,50 +273,99 @@ struct CandRec {
   uint32_t pad;
 };
 
+template <bool kVec>
 __global__ void __launch_bounds__(kThreads)
 plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restrict__ first,
            const int32_t* __restrict__ ranges, int8_t* __restrict__ tier,
-           CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t ntiles) {
+           CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t nslices) {
   __shared__ ClassTable ct;
   __shared__ int32_t rg[256];
   const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
-  if (t >= ntiles) return;
-  const int64_t kt = t / a.N, i = t - kt * a.N;
+  if (t >= uint32_t(a.N) * nslices) return;
+  const int64_t sl = t / a.N, i = t - sl * a.N;
   build_class_table(a, ct);
   for (int x = threadIdx.x; x < 2 * a.J; x += kThreads) rg[x] = ranges[i * 2 * a.J + x];
   __syncthreads();
-  const int64_t k0 = kt * kTileCells;
-  const int64_t kn = (a.F - k0) < kTileCells ? (a.F - k0) : kTileCells;
-  const uint8_t* crow = count + i * a.F + k0;
-  const int32_t* frow = first + i * a.F + k0;
-  int8_t* trow = tier + i * a.F + k0;
+  const int64_t ks = sl * kSliceCells;
+  const int64_t ke = ks + kSliceCells < a.F ? ks + kSliceCells : a.F;
+  const uint8_t* crow = count + i * a.F;
+  const int32_t* frow = first + i * a.F;
+  int8_t* trow = tier + i * a.F;
   CandRec* ci = cand + i * int64_t(a.cmax);
-  const uint64_t lt = lanemask_lt();
-  for (int64_t x0 = 0; x0 < kn; x0 += kThreads) {
-    const int64_t x = x0 + threadIdx.x;
+  // tier of one cell; *key receives its candidate record key when it is one
+  auto classify = [&](int64_t k, uint32_t c, int32_t f, uint64_t* key) -> int {
+    if (c == 0) f = -1;
+    const uint32_t b = bin_of(a, ct, c, f, k);
     bool is_cand = false;
-    uint64_t key = 0;
-    if (x < kn) {
-      const uint32_t c = crow[x];
-      const int32_t f = c ? frow[x] : -1;
-      const uint32_t b = bin_of(a, ct, c, f, k0 + x);
-      int tv = 0;
-      for (int j = 0; j < a.J; ++j) {
-        if (int32_t(b) >= rg[2 * j] && int32_t(b) <= rg[2 * j + 1]) is_cand = true;
-        tv += int32_t(b) > rg[2 * j + 1];
-      }
-      trow[x] = is_cand ? int8_t(0) : (tv >= a.J ? int8_t(-1) : int8_t(tv));
-      key = (uint64_t(b) << 32) | (c ? uint64_t(uint32_t(f)) : uint64_t(k0 + x));
+    int tv = 0;
+    for (int j = 0; j < a.J; ++j) {
+      is_cand |= int32_t(b) >= rg[2 * j] && int32_t(b) <= rg[2 * j + 1];
+      tv += int32_t(b) > rg[2 * j + 1];
     }
-    const uint64_t m = __ballot(is_cand);
-    if (m) {
-      int32_t basev = 0;
-      const int leader = __ffsll((long long)m) - 1;
-      if (int(__lane_id()) == leader) basev = atomicAdd(&ccount[i], __popcll(m));
-      basev = __shfl(basev, leader, 64);
-      if (is_cand) {
-        const int32_t slot = basev + __popcll(m & lt);
-        if (slot < a.cmax) ci[slot] = CandRec{key, uint32_t(k0 + x), 0u};
+    if (is_cand) {
+      *key = (uint64_t(b) << 32) | (c ? uint64_t(uint32_t(f)) : uint64_t(k));
+      return 256;  // marker: candidate (placeholder tier 0)
+    }
+    return tv >= a.J ? -1 : tv;
+  };
+  auto single = [&](int64_t k) {
+    uint64_t key = 0;
+    const int tv = classify(k, crow[k], frow[k], &key);
+    trow[k] = tv == 256 ? int8_t(0) : int8_t(tv);
+    if (tv == 256) {
+      const int32_t slot = atomicAdd(&ccount[i], 1);
+      if (slot < a.cmax) ci[slot] = CandRec{key, uint32_t(k), 0u};
+    }
+  };
+  const RowSplit rs = split_row(i * a.F + ks, ks, ke, kVec);
+  for (int64_t k = ks + threadIdx.x; k < rs.body0; k += kThreads) single(k);
+  for (int64_t k = rs.tail0 + threadIdx.x; k < ke; k += kThreads) single(k);
+  constexpr int kU = 4;
+  for (int64_t u0 = 0; u0 < rs.nunits; u0 += kU * kThreads) {
+    uint32_t cw[kU];
+    int4 fw[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int64_t u = u0 + j * kThreads + threadIdx.x;
+      const int64_t k = rs.body0 + 4 * u;
+      if (u < rs.nunits) {
+        cw[j] = *reinterpret_cast<const uint32_t*>(crow + k);
+        fw[j] = *reinterpret_cast<const int4*>(frow + k);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int64_t u = u0 + j * kThreads + threadIdx.x;
+      const int64_t k = rs.body0 + 4 * u;
+      const bool ok = u < rs.nunits;
+      uint64_t key[4] = {0, 0, 0, 0};
+      int tv[4] = {0, 0, 0, 0};
+      int nc = 0;
+      if (ok) {
+        const int32_t fv[4] = {fw[j].x, fw[j].y, fw[j].z, fw[j].w};
+        uint32_t packed = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          tv[q] = classify(k + q, (cw[j] >> (8 * q)) & 0xFFu, fv[q], &key[q]);
+          nc += tv[q] == 256;
+          packed |= uint32_t(uint8_t(int8_t(tv[q] == 256 ? 0 : tv[q]))) << (8 * q);
+        }
+        *reinterpret_cast<uint32_t*>(trow + k) = packed;
+      }
+      if (__ballot(nc > 0)) {
+        const uint32_t inc = wave_inclusive_scan(uint32_t(nc));
+        const uint32_t tot = __shfl(inc, 63, 64);
+        int32_t basev = 0;
+        if (__lane_id() == 63) basev = atomicAdd(&ccount[i], int32_t(tot));
+        basev = __shfl(basev, 63, 64);
+        int32_t slot = basev + int32_t(inc) - nc;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (tv[q] == 256) {
+            if (slot < a.cmax) ci[slot] = CandRec{key[q], uint32_t(k + q), 0u};
+            ++slot;
+          }
+        }
       }
     }
   }
@@ -475,11 +594,12 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
   for (int j = 0; j < 128; ++j) a.caps[j] = j < J ? caps[j] : 0;
 
   Scratch scr(st);
-  uint64_t* H;
+  uint64_t *H, *binsum;
   int32_t *ranges, *ccount, *overflow;
   CandRec* cand;
   const int64_t hn = s.N * int64_t(a.nbin + 1);
   if ((rc = scr.alloc_n(&H, size_t(hn)))) return rc;
+  if ((rc = scr.alloc_n(&binsum, size_t(a.nb0)))) return rc;
   if ((rc = scr.alloc_n(&ranges, size_t(s.N * 2 * J)))) return rc;
   if ((rc = scr.alloc_n(&ccount, size_t(s.N)))) return rc;
   if ((rc = scr.alloc_n(&overflow, size_t(s.N)))) return rc;
@@ -491,14 +611,27 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
   if ((rc = launch("fill_i32", fill_i32, dim3(uint32_t(ceil_div(s.N, 256))), dim3(256), 0, st, ccount,
                    s.N)))
     return rc;
-  const uint32_t ntiles = uint32_t(s.N * ceil_div(s.F, kTileCells));
-  if ((rc = launch("plan_hist", plan_hist, dim3(xcd_padded(ntiles)), dim3(kThreads),
-                   size_t(a.nbin1) * 8, st, a, count, first, sizes, H, ntiles)))
+  if ((rc = launch("plan_binsum", plan_binsum, dim3(uint32_t(ceil_div(a.nb0, 4))), dim3(256), 0, st,
+                   s.F, a.nb0, sizes, binsum)))
+    return rc;
+  // vector loads need 4-byte aligned count/tier rows and 16-byte aligned first rows
+  const bool vec = (reinterpret_cast<uintptr_t>(count) & 3) == 0 &&
+                   (reinterpret_cast<uintptr_t>(tier) & 3) == 0 &&
+                   (reinterpret_cast<uintptr_t>(first) & 15) == 0;
+  const uint32_t nslices = uint32_t(ceil_div(s.F, kSliceCells));
+  const uint32_t ntiles = uint32_t(s.N) * nslices;
+  const size_t hsmem = size_t(a.nbin1 + kSliceBins0) * 8;
+  if ((rc = vec ? launch("plan_hist", plan_hist<true>, dim3(xcd_padded(ntiles)), dim3(kThreads), hsmem,
+                         st, a, count, first, sizes, (const uint64_t*)binsum, H, nslices)
+                : launch("plan_hist", plan_hist<false>, dim3(xcd_padded(ntiles)), dim3(kThreads), hsmem,
+                         st, a, count, first, sizes, (const uint64_t*)binsum, H, nslices)))
     return rc;
   if ((rc = launch("plan_cut", plan_cut, dim3(uint32_t(s.N)), dim3(1024), 0, st, a, H, ranges)))
     return rc;
-  if ((rc = launch("plan_write", plan_write, dim3(xcd_padded(ntiles)), dim3(kThreads), 0, st, a,
-                   count, first, (const int32_t*)ranges, tier, cand, ccount, ntiles)))
+  if ((rc = vec ? launch("plan_write", plan_write<true>, dim3(xcd_padded(ntiles)), dim3(kThreads), 0,
+                         st, a, count, first, (const int32_t*)ranges, tier, cand, ccount, nslices)
+                : launch("plan_write", plan_write<false>, dim3(xcd_padded(ntiles)), dim3(kThreads), 0,
+                         st, a, count, first, (const int32_t*)ranges, tier, cand, ccount, nslices)))
     return rc;
   if ((rc = launch("plan_resolve", plan_resolve, dim3(uint32_t(s.N)), dim3(kResolveThreads), 0, st,
                    a, (const uint64_t*)H, (const CandRec*)cand, (const int32_t*)ccount, sizes, tier,

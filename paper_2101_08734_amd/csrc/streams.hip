@@ -5,19 +5,25 @@
 // the N workers and a worker's stream R is the concatenation of its batches.
 //
 // Epoch e orders the samples by (key_e(k), k), key_e(k) a Philox-4x32-10
-// word. The order is built as a two-level radix sort over all epochs of a
-// batch at once:
-//   1. stream_count   -- Philox keys in registers, histogram of the bucket
-//                        umulhi(key, nb) per epoch (LDS-privatised).
-//   2. stream_scan    -- bucket start positions per epoch.
-//   3. stream_scatter -- keys regenerated, (key, id) pairs written into their
-//                        bucket (order inside a bucket is arbitrary).
-//   4. stream_sort    -- one workgroup per bucket: LSD radix sort of the
-//                        bucket in LDS, ranked with wavefront ballots (8-bit
-//                        digits), equal keys put back in id order, and the
-//                        sorted positions p sharded straight into R:
-//                        R[p mod N][e*L_i + p div N]. The write goes through
-//                        an LDS transpose so each worker row gets a run.
+// word. The order is built as a bucket sort over all epochs of a batch at
+// once. Fine bucket b = umulhi(key, nb) holds a few thousand keys; coarse
+// bucket c = umulhi(key, nb1) (nb = nb1 * nf) groups nf consecutive fine ones.
+//   1. stream_count   -- Philox keys in registers; per (epoch, chunk of 64K
+//                        ids) histogram of the fine buckets.
+//   2. stream_offsets -- per (epoch, fine bucket) running sum over chunks.
+//   3. stream_scan    -- fine bucket start positions per epoch.
+//   4. stream_scatter -- keys regenerated and (key, id) pairs written into
+//                        their coarse bucket (at most 64 per epoch, so each
+//                        workgroup's open cache lines fit in L2 and every
+//                        line is completed there before it is written back).
+//   5. stream_split   -- each coarse bucket read back in 16K-pair pieces and
+//                        split into its nf fine buckets (skipped when nf = 1).
+//   6. stream_sort    -- one workgroup per fine bucket: counting sort in LDS
+//                        by the top 11 bits of the key inside the bucket,
+//                        each (tiny) group insertion-sorted by (key, id), and
+//                        the sorted positions p sharded straight into R:
+//                        R[p mod N][e*L_i + p div N], through an LDS
+//                        transpose so each worker row gets a run.
 // Buckets larger than the LDS capacity (not expected for uniform keys, but
 // possible in principle) are sorted in place in global memory by a bitonic
 // network inside the same workgroup.
@@ -29,36 +35,33 @@
 namespace nopfs {
 namespace {
 
-constexpr int kChunkThreads = 256;
+constexpr int kChunkThreads = 1024;
 constexpr int kBlocksPerThread = 16;                                   // Philox blocks
-constexpr int64_t kChunkIds = int64_t(kChunkThreads) * kBlocksPerThread * 4;  // 16384
+constexpr int64_t kChunkIds = int64_t(kChunkThreads) * kBlocksPerThread * 4;  // 65536
 constexpr uint32_t kMaxBuckets = 8192;
 
 constexpr int kSortThreads = 512;
-constexpr int kSortWaves = kSortThreads / 64;
 constexpr int kItems = 16;
 constexpr int kSortCap = kSortThreads * kItems;  // 8192 (key, id) pairs in LDS
-constexpr int kDigits = 256;
+constexpr int kDigitBits = 11;
+constexpr int kDigits = 1 << kDigitBits;
 
 struct StreamParams {
   int64_t F, N, B, P, L, M_max;
   int32_t drop_last;
   uint32_t seed_lo, seed_hi;
-  uint32_t nb;        // buckets per epoch
+  uint32_t nb;        // fine buckets per epoch
+  uint32_t nb1;       // coarse buckets per epoch
+  uint32_t nf;        // fine buckets per coarse bucket (nb = nb1 * nf)
   int32_t e0;         // first epoch of the batch
   int32_t sort_bits;  // significant bits of a key inside its bucket
   int32_t cap;        // largest bucket sorted in LDS
 };
 
-__global__ void fill_u32(uint32_t* p, int64_t n, uint32_t v) {
-  int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-  for (; i < n; i += stride) p[i] = v;
-}
-
-// -- 1. histogram of buckets ------------------------------------------------
+// -- 1. histogram of buckets per chunk ----------------------------------------
+// cnt layout: [epoch][chunk][bucket]
 __global__ void __launch_bounds__(kChunkThreads)
-stream_count(StreamParams p, uint32_t* __restrict__ tot) {
+stream_count(StreamParams p, uint32_t nchunks, uint32_t* __restrict__ cnt) {
   extern __shared__ uint32_t hist[];
   const uint32_t nb = p.nb;
   for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) hist[b] = 0;
@@ -78,12 +81,40 @@ stream_count(StreamParams p, uint32_t* __restrict__ tot) {
     }
   }
   __syncthreads();
-  uint32_t* t = tot + int64_t(blockIdx.y) * nb;
-  for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x)
-    if (hist[b]) atomicAdd(&t[b], hist[b]);
+  uint32_t* out = cnt + (int64_t(blockIdx.y) * nchunks + blockIdx.x) * nb;
+  for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) out[b] = hist[b];
 }
 
-// -- 2. bucket starts --------------------------------------------------------
+// -- 2. chunk offsets inside each bucket --------------------------------------
+// In place: cnt[e][c][b] becomes the number of bucket-b keys of epoch e in
+// chunks before c; tot[e][b] receives the bucket size.
+__global__ void __launch_bounds__(256)
+stream_offsets(uint32_t nb, uint32_t nchunks, uint32_t* __restrict__ cnt,
+               uint32_t* __restrict__ tot) {
+  const uint32_t b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= nb) return;
+  uint32_t* col = cnt + int64_t(blockIdx.y) * nchunks * nb + b;
+  uint32_t run = 0;
+  uint32_t c = 0;
+  for (; c + 8 <= nchunks; c += 8) {
+    uint32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = col[int64_t(c + u) * nb];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      col[int64_t(c + u) * nb] = run;
+      run += v[u];
+    }
+  }
+  for (; c < nchunks; ++c) {
+    const uint32_t v = col[int64_t(c) * nb];
+    col[int64_t(c) * nb] = run;
+    run += v;
+  }
+  tot[int64_t(blockIdx.y) * nb + b] = run;
+}
+
+// -- 3. bucket starts --------------------------------------------------------
 __global__ void __launch_bounds__(1024)
 stream_scan(uint32_t nb, const uint32_t* __restrict__ tot, uint32_t* __restrict__ start,
             uint32_t* __restrict__ cursor) {
@@ -106,55 +137,48 @@ stream_scan(uint32_t nb, const uint32_t* __restrict__ tot, uint32_t* __restrict_
   if (threadIdx.x == 0) st[nb] = carry;
 }
 
-// -- 3. scatter into buckets -------------------------------------------------
+// -- 4. scatter into coarse buckets ------------------------------------------
+// Target bucket t = umulhi(key, nt): the fine bucket when nf = 1 (nt = nb),
+// else the coarse bucket (nt = nb1). A chunk's share of coarse bucket c
+// starts at the bucket's first fine start plus the chunk's offsets in each
+// of its fine buckets.
 __global__ void __launch_bounds__(kChunkThreads)
-stream_scatter(StreamParams p, uint32_t nchunks, uint32_t* __restrict__ cursor,
-               uint32_t* __restrict__ keys, int32_t* __restrict__ ids) {
+stream_scatter(StreamParams p, uint32_t nchunks, const uint32_t* __restrict__ cnt,
+               const uint32_t* __restrict__ start, uint32_t* __restrict__ keys,
+               int32_t* __restrict__ ids) {
   extern __shared__ uint32_t smem[];
-  const uint32_t nb = p.nb;
-  uint32_t* cnt = smem;
-  uint32_t* base = smem + nb;
+  const uint32_t nb = p.nb, nf = p.nf;
+  const uint32_t nt = nf == 1 ? nb : p.nb1;
+  uint32_t* slot = smem;
+  uint32_t* base = smem + nt;
   const uint32_t chunk = xcd_logical(blockIdx.x, gridDim.x);
   if (chunk >= nchunks) return;
-  for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) cnt[b] = 0;
+  const uint32_t* off = cnt + (int64_t(blockIdx.y) * nchunks + chunk) * nb;
+  const uint32_t* st = start + int64_t(blockIdx.y) * (nb + 1);
+  for (uint32_t b = threadIdx.x; b < nt; b += blockDim.x) {
+    uint32_t o = 0;
+    for (uint32_t f = b * nf; f < (b + 1) * nf; ++f) o += off[f];
+    slot[b] = 0;
+    base[b] = st[b * nf] + o;
+  }
   __syncthreads();
   const uint32_t e = uint32_t(p.e0) + blockIdx.y;
   const int64_t blk0 = int64_t(chunk) * (kChunkIds / 4);
-  uint32_t kr[kBlocksPerThread][4];
-#pragma unroll
+  uint32_t* ko = keys + int64_t(blockIdx.y) * p.F;
+  int32_t* io = ids + int64_t(blockIdx.y) * p.F;
+#pragma unroll 2
   for (int it = 0; it < kBlocksPerThread; ++it) {
     const int64_t blk = blk0 + it * kChunkThreads + threadIdx.x;
     const int64_t id0 = blk * 4;
     if (id0 < p.F) {
       const Philox4 r = philox_block(uint32_t(blk), e, p.seed_lo, p.seed_hi);
-      kr[it][0] = r.x; kr[it][1] = r.y; kr[it][2] = r.z; kr[it][3] = r.w;
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (id0 + c < p.F) atomicAdd(&cnt[__umulhi(kr[it][c], nb)], 1u);
-    }
-  }
-  __syncthreads();
-  uint32_t* cur = cursor + int64_t(blockIdx.y) * nb;
-  for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) {
-    const uint32_t c = cnt[b];
-    if (c) base[b] = atomicAdd(&cur[b], c);
-    cnt[b] = 0;
-  }
-  __syncthreads();
-  uint32_t* ko = keys + int64_t(blockIdx.y) * p.F;
-  int32_t* io = ids + int64_t(blockIdx.y) * p.F;
-#pragma unroll
-  for (int it = 0; it < kBlocksPerThread; ++it) {
-    const int64_t blk = blk0 + it * kChunkThreads + threadIdx.x;
-    const int64_t id0 = blk * 4;
-    if (id0 < p.F) {
+      const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         if (id0 + c < p.F) {
-          const uint32_t key = kr[it][c];
-          const uint32_t b = __umulhi(key, nb);
-          const uint32_t dst = base[b] + atomicAdd(&cnt[b], 1u);
-          ko[dst] = key;
+          const uint32_t b = __umulhi(w[c], nt);
+          const uint32_t dst = base[b] + atomicAdd(&slot[b], 1u);
+          ko[dst] = w[c];
           io[dst] = int32_t(id0 + c);
         }
       }
@@ -162,76 +186,62 @@ stream_scatter(StreamParams p, uint32_t nchunks, uint32_t* __restrict__ cursor,
   }
 }
 
-// -- 4. per-bucket sort and shard --------------------------------------------
+// -- 5. split coarse buckets into fine buckets ---------------------------------
+constexpr int kSplitThreads = 1024;
+constexpr int kSplitItems = 16;
+constexpr uint32_t kSplitPiece = kSplitThreads * kSplitItems;
+
+__global__ void __launch_bounds__(kSplitThreads)
+stream_split(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __restrict__ cursor,
+             const uint32_t* __restrict__ keys1, const int32_t* __restrict__ ids1,
+             uint32_t* __restrict__ keys, int32_t* __restrict__ ids) {
+  extern __shared__ uint32_t smem[];
+  const uint32_t nb = p.nb, nf = p.nf;
+  uint32_t* cnt = smem;
+  uint32_t* base = smem + nf;
+  const uint32_t c = blockIdx.y;
+  const int64_t eoff = int64_t(blockIdx.z) * p.F;
+  const uint32_t* st = start + int64_t(blockIdx.z) * (nb + 1);
+  uint32_t* cur = cursor + int64_t(blockIdx.z) * nb;
+  const uint32_t r0 = st[c * nf], r1 = st[(c + 1) * nf];
+  for (uint32_t q0 = r0 + blockIdx.x * kSplitPiece; q0 < r1; q0 += gridDim.x * kSplitPiece) {
+    for (uint32_t f = threadIdx.x; f < nf; f += kSplitThreads) cnt[f] = 0;
+    __syncthreads();
+    uint32_t k[kSplitItems], sl[kSplitItems];
+    int32_t id[kSplitItems];
+#pragma unroll
+    for (int r = 0; r < kSplitItems; ++r) {
+      const uint32_t q = q0 + r * kSplitThreads + threadIdx.x;
+      if (q < r1) {
+        k[r] = keys1[eoff + q];
+        id[r] = ids1[eoff + q];
+        sl[r] = atomicAdd(&cnt[__umulhi(k[r], nb) - c * nf], 1u);
+      }
+    }
+    __syncthreads();
+    for (uint32_t f = threadIdx.x; f < nf; f += kSplitThreads)
+      if (cnt[f]) base[f] = atomicAdd(&cur[c * nf + f], cnt[f]);
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSplitItems; ++r) {
+      const uint32_t q = q0 + r * kSplitThreads + threadIdx.x;
+      if (q < r1) {
+        const uint32_t dst = base[__umulhi(k[r], nb) - c * nf] + sl[r];
+        keys[eoff + dst] = k[r];
+        ids[eoff + dst] = id[r];
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// -- 6. per-bucket sort and shard --------------------------------------------
 struct SortSmem {
   uint32_t keys[kSortCap];
   int32_t ids[kSortCap];
-  uint32_t cnt[kDigits * kSortWaves];
+  uint32_t hist[kDigits];
   uint32_t tmp[65];
 };
-
-// One stable counting-sort pass over an 8-bit digit. Items live in registers
-// in wave-striped order: item r of lane l in wave w has local index
-// (w*kItems + r)*64 + l, which is also the stability order. Within a wave,
-// lanes holding the same digit are found with 8 ballots; per-wave running
-// counters in LDS give each item its rank among equal digits of its wave.
-__device__ __forceinline__ void rank_pass(uint32_t (&k)[kItems], int32_t (&id)[kItems], int shift,
-                                          SortSmem& s) {
-  const int lane = __lane_id();
-  const int wave = threadIdx.x >> 6;
-  for (int i = threadIdx.x; i < kDigits * kSortWaves; i += kSortThreads) s.cnt[i] = 0;
-  __syncthreads();
-  const uint64_t lt = lanemask_lt();
-  uint32_t rank[kItems];
-#pragma unroll
-  for (int r = 0; r < kItems; ++r) {
-    const uint32_t d = (k[r] >> shift) & 0xFFu;
-    uint64_t m = ~0ull;
-#pragma unroll
-    for (int bit = 0; bit < 8; ++bit) {
-      const bool set = (d >> bit) & 1u;
-      const uint64_t bb = __ballot(set);
-      m &= set ? bb : ~bb;
-    }
-    uint32_t* c = &s.cnt[d * kSortWaves + wave];
-    const uint32_t before = *c;
-    rank[r] = before + uint32_t(__popcll(m & lt));
-    if ((m >> lane) == 1ull) *c = before + uint32_t(__popcll(m));
-  }
-  __syncthreads();
-  // exclusive scan of the counters in (digit, wave) order
-  constexpr int kPer = kDigits * kSortWaves / kSortThreads;
-  uint32_t v[kPer];
-  uint32_t sum = 0;
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    v[j] = s.cnt[threadIdx.x * kPer + j];
-    sum += v[j];
-  }
-  uint32_t total;
-  uint32_t ex = block_exclusive_scan(sum, s.tmp, &total);
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    s.cnt[threadIdx.x * kPer + j] = ex;
-    ex += v[j];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < kItems; ++r) {
-    const uint32_t d = (k[r] >> shift) & 0xFFu;
-    const uint32_t dst = s.cnt[d * kSortWaves + wave] + rank[r];
-    s.keys[dst] = k[r];
-    s.ids[dst] = id[r];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < kItems; ++r) {
-    const int q = (wave * kItems + r) * 64 + lane;
-    k[r] = s.keys[q];
-    id[r] = s.ids[q];
-  }
-  __syncthreads();
-}
 
 __device__ __forceinline__ bool pair_greater(uint32_t ka, int32_t ia, uint32_t kb, int32_t ib) {
   return ka > kb || (ka == kb && ia > ib);
@@ -303,37 +313,70 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
   }
 
   const uint32_t key_lo = uint32_t(((uint64_t(b) << 32) + nb - 1) / nb);
-  const int lane = __lane_id();
-  const int wave = threadIdx.x >> 6;
-  uint32_t k[kItems];
+  const int db = p.sort_bits < kDigitBits ? p.sort_bits : kDigitBits;
+  const int dshift = p.sort_bits - db;
+  for (int x = threadIdx.x; x < kDigits; x += kSortThreads) s.hist[x] = 0;
+  __syncthreads();
+  // counting sort by the top bits of the key inside the bucket
+  uint32_t k[kItems], slot[kItems];
   int32_t id[kItems];
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t((wave * kItems + r) * 64 + lane);
+    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
     if (q < n) {
       k[r] = gk[q] - key_lo;
       id[r] = gi[q];
-    } else {
-      k[r] = 0xFFFFFFFFu;  // padding sorts last (it starts last and passes are stable)
-      id[r] = INT_MAX;
     }
   }
-  for (int shift = 0; shift < p.sort_bits; shift += 8) rank_pass(k, id, shift, s);
-
-  // equal keys: restore ascending id order inside each run of ties
-  for (uint32_t q = threadIdx.x; q + 1 < n; q += kSortThreads) {
-    if (s.keys[q] == s.keys[q + 1] && (q == 0 || s.keys[q - 1] != s.keys[q])) {
-      uint32_t end = q + 2;
-      while (end < n && s.keys[end] == s.keys[q]) ++end;
-      for (uint32_t a = q + 1; a < end; ++a) {
-        const int32_t v = s.ids[a];
-        uint32_t c = a;
-        while (c > q && s.ids[c - 1] > v) {
-          s.ids[c] = s.ids[c - 1];
-          --c;
-        }
-        s.ids[c] = v;
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
+    if (q < n) slot[r] = atomicAdd(&s.hist[k[r] >> dshift], 1u);
+  }
+  __syncthreads();
+  {
+    constexpr int kPer = kDigits / kSortThreads;
+    uint32_t v[kPer];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      v[j] = s.hist[threadIdx.x * kPer + j];
+      sum += v[j];
+    }
+    uint32_t total;
+    uint32_t ex = block_exclusive_scan(sum, s.tmp, &total);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      s.hist[threadIdx.x * kPer + j] = ex;
+      ex += v[j];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
+    if (q < n) {
+      const uint32_t dst = s.hist[k[r] >> dshift] + slot[r];
+      s.keys[dst] = k[r];
+      s.ids[dst] = id[r];
+    }
+  }
+  __syncthreads();
+  // each digit group (a few pairs each) in (key, id) order
+  for (int d = threadIdx.x; d < kDigits; d += kSortThreads) {
+    const uint32_t a0 = s.hist[d];
+    const uint32_t a1 = d + 1 < kDigits ? s.hist[d + 1] : n;
+    for (uint32_t u = a0 + 1; u < a1; ++u) {
+      const uint32_t kv = s.keys[u];
+      const int32_t iv = s.ids[u];
+      uint32_t c = u;
+      while (c > a0 && pair_greater(s.keys[c - 1], s.ids[c - 1], kv, iv)) {
+        s.keys[c] = s.keys[c - 1];
+        s.ids[c] = s.ids[c - 1];
+        --c;
       }
+      s.keys[c] = kv;
+      s.ids[c] = iv;
     }
   }
   __syncthreads();
@@ -387,7 +430,10 @@ int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st) {
   int64_t nb64 = ceil_div(s.F, cap * 3 / 4 > 0 ? cap * 3 / 4 : 1);
   if (nb64 < 1) nb64 = 1;
   if (nb64 > int64_t(kMaxBuckets)) nb64 = kMaxBuckets;
-  const uint32_t nb = uint32_t(nb64);
+  // coarse buckets: at most 64 per epoch, nf fine buckets each
+  const uint32_t nb1 = uint32_t(nb64 < 64 ? nb64 : 64);
+  const uint32_t nf = uint32_t(ceil_div(nb64, nb1));
+  const uint32_t nb = nb1 * nf;
   const uint64_t width = ((uint64_t(1) << 32) + nb - 1) / nb;
   int bits = 0;
   while ((uint64_t(1) << bits) < width) ++bits;
@@ -398,41 +444,59 @@ int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st) {
   p.seed_lo = uint32_t(s.seed);
   p.seed_hi = uint32_t(s.seed >> 32);
   p.nb = nb;
+  p.nb1 = nb1;
+  p.nf = nf;
   p.sort_bits = bits;
   p.cap = int32_t(cap);
 
-  // epochs per batch: keys + ids of a batch stay under ~6 GB of scratch
-  const int64_t budget = int64_t(6) << 30;
-  int64_t EB = budget / (8 * s.F);
+  // epochs per batch: the pair arrays of a batch stay under ~16 GB of scratch
+  const int64_t budget = int64_t(16) << 30;
+  int64_t EB = budget / ((nf > 1 ? 16 : 8) * s.F);
   if (EB < 1) EB = 1;
   if (EB > s.E) EB = s.E;
 
+  const uint32_t nchunks = uint32_t(ceil_div(s.F, kChunkIds));
   Scratch scr(st);
-  uint32_t *keys, *tot, *start, *cursor;
-  int32_t* ids;
+  uint32_t *keys, *keys1 = nullptr, *cnt, *tot, *start, *cursor;
+  int32_t *ids, *ids1 = nullptr;
   if ((rc = scr.alloc_n(&keys, size_t(EB * s.F)))) return rc;
   if ((rc = scr.alloc_n(&ids, size_t(EB * s.F)))) return rc;
+  if (nf > 1) {
+    if ((rc = scr.alloc_n(&keys1, size_t(EB * s.F)))) return rc;
+    if ((rc = scr.alloc_n(&ids1, size_t(EB * s.F)))) return rc;
+  }
+  if ((rc = scr.alloc_n(&cnt, size_t(EB) * nchunks * nb))) return rc;
   if ((rc = scr.alloc_n(&tot, size_t(EB * nb)))) return rc;
   if ((rc = scr.alloc_n(&start, size_t(EB * (nb + 1))))) return rc;
   if ((rc = scr.alloc_n(&cursor, size_t(EB * nb)))) return rc;
+  const uint32_t nt = nf == 1 ? nb : nb1;
+  // pieces per coarse bucket for the split: about 1.25x the mean size
+  const uint32_t pieces = uint32_t(ceil_div(ceil_div(s.F, nb1) * 5 / 4, kSplitPiece));
 
-  const uint32_t nchunks = uint32_t(ceil_div(s.F, kChunkIds));
   for (int64_t e0 = 0; e0 < s.E; e0 += EB) {
     const uint32_t eb = uint32_t(e0 + EB <= s.E ? EB : s.E - e0);
     p.e0 = int32_t(e0);
-    if ((rc = launch("fill_u32", fill_u32, dim3(uint32_t(ceil_div(eb * nb, 256))), dim3(256), 0, st,
-                     tot, int64_t(eb) * nb, 0u)))
-      return rc;
     if ((rc = launch("stream_count", stream_count, dim3(nchunks, eb), dim3(kChunkThreads),
-                     size_t(nb) * 4, st, p, tot)))
+                     size_t(nb) * 4, st, p, nchunks, cnt)))
       return rc;
-    if ((rc = launch("stream_scan", stream_scan, dim3(eb), dim3(1024), 0, st, nb, tot, start, cursor)))
+    if ((rc = launch("stream_offsets", stream_offsets, dim3(uint32_t(ceil_div(nb, 256)), eb),
+                     dim3(256), 0, st, nb, nchunks, cnt, tot)))
+      return rc;
+    if ((rc = launch("stream_scan", stream_scan, dim3(eb), dim3(1024), 0, st, nb,
+                     (const uint32_t*)tot, start, cursor)))
       return rc;
     if ((rc = launch("stream_scatter", stream_scatter, dim3(xcd_padded(nchunks), eb),
-                     dim3(kChunkThreads), size_t(nb) * 8, st, p, nchunks, cursor, keys, ids)))
+                     dim3(kChunkThreads), size_t(nt) * 8, st, p, nchunks, (const uint32_t*)cnt,
+                     (const uint32_t*)start, nf > 1 ? keys1 : keys, nf > 1 ? ids1 : ids)))
       return rc;
+    if (nf > 1) {
+      if ((rc = launch("stream_split", stream_split, dim3(pieces, nb1, eb), dim3(kSplitThreads),
+                       size_t(nf) * 8, st, p, (const uint32_t*)start, cursor,
+                       (const uint32_t*)keys1, (const int32_t*)ids1, keys, ids)))
+        return rc;
+    }
     if ((rc = launch("stream_sort", stream_sort, dim3(xcd_padded(nb), eb), dim3(kSortThreads), 0, st,
-                     p, start, keys, ids, R)))
+                     p, (const uint32_t*)start, keys, ids, R)))
       return rc;
   }
   if (!s.drop_last && s.F % s.N != 0) {
