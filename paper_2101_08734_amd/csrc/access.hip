@@ -58,7 +58,7 @@ constexpr uint32_t kMaxWindows = 8192;  // sample windows per worker
 constexpr int kThreads = 256;  // partition / unpartition workgroups
 constexpr int kStatsThreads = NOPFS_STATS_THREADS;
 constexpr int kNextThreads = NOPFS_NEXT_THREADS;
-static_assert(kNextThreads >= 256 && kNextThreads % 64 == 0, "next_tile needs one thread per bucket");
+static_assert(kNextThreads >= 64 && kNextThreads % 64 == 0, "next_tile block size");
 static_assert(kStatsThreads >= 64 && kStatsThreads % 64 == 0, "stats_tile block size");
 constexpr int kStatsWin = 1 << NOPFS_STATS_WS;  // samples held in LDS by stats_tile
 constexpr int kNextEnt = NOPFS_NEXT_ENT;   // reads per next_tile window (fast path)
@@ -82,7 +82,9 @@ __device__ __forceinline__ int64_t orow(const SegParams& p, int64_t i, int64_t e
 }
 
 // -- partition ----------------------------------------------------------------
-__global__ void __launch_bounds__(kThreads)
+constexpr int kPartThreads = 512;
+
+__global__ void __launch_bounds__(kPartThreads)
 seg_partition(SegParams p, const int32_t* __restrict__ R, uint32_t* __restrict__ Pk,
               uint16_t* __restrict__ O) {
   extern __shared__ uint32_t sm[];
@@ -90,72 +92,63 @@ seg_partition(SegParams p, const int32_t* __restrict__ R, uint32_t* __restrict__
   const uint32_t nbk = p.nbk;
   uint32_t* hist = sm;
   uint32_t* stage = sm + ((nbk + 4) & ~3u);
-  const int64_t wg = blockIdx.x;
-  const int64_t per_worker = int64_t(p.E) * p.nsc;
-  const int64_t i = wg / per_worker;
-  const int64_t rem = wg - i * per_worker;
-  const int64_t e = rem / p.nsc, sc = rem - e * p.nsc;
+  const uint32_t wg = blockIdx.x;
+  const uint32_t per_worker = uint32_t(p.E) * uint32_t(p.nsc);
+  const uint32_t i = wg / per_worker;
+  const uint32_t rem = wg - i * per_worker;
+  const uint32_t e = rem / uint32_t(p.nsc), sc = rem - e * uint32_t(p.nsc);
   const int64_t Li = seg_len(p, i);
-  int64_t len64 = Li - sc * kSC;
+  int64_t len64 = Li - int64_t(sc) * kSC;
   len64 = len64 < 0 ? 0 : (len64 > kSC ? kSC : len64);
   const uint32_t len = uint32_t(len64);
-  const int64_t base = i * p.M_max + e * Li + sc * kSC;
+  const int64_t base = int64_t(i) * p.M_max + int64_t(e) * Li + int64_t(sc) * kSC;
   const uint32_t W = 1u << p.ws;
+  const uint32_t F = uint32_t(p.F);
 
-  for (uint32_t b = threadIdx.x; b <= nbk; b += kThreads) hist[b] = 0;
+  for (uint32_t b = threadIdx.x; b <= nbk; b += kPartThreads) hist[b] = 0;
   __syncthreads();
-  constexpr int kPer = kSC / kThreads;
-  int32_t kk[kPer];
+  constexpr int kPer = kSC / kPartThreads;
+  uint32_t kk[kPer];
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
-    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
-    kk[r] = q < len ? R[base + q] : -1;
+    const uint32_t q = uint32_t(r * kPartThreads) + threadIdx.x;
     // entries outside [0, F) break the precondition; keep them in bounds
-    if (q < len && uint64_t(uint32_t(kk[r])) >= uint64_t(p.F)) kk[r] = 0;
-    if (q < len) atomicAdd(&hist[uint32_t(kk[r]) >> p.ws], 1u);
+    uint32_t k = q < len ? uint32_t(R[base + q]) : 0u;
+    kk[r] = k < F ? k : 0u;
   }
-  __syncthreads();
-  uint16_t* o = O + orow(p, i, e, sc);
-  uint32_t carry = 0;
-  for (uint32_t b0 = 0; b0 < nbk; b0 += kThreads) {
-    const uint32_t b = b0 + threadIdx.x;
-    const uint32_t v = b < nbk ? hist[b] : 0u;
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan(v, tmp, &total);
-    if (b < nbk) {
-      hist[b] = carry + ex;
-      o[b] = uint16_t(carry + ex);
-    }
-    carry += total;
-  }
-  if (threadIdx.x == 0) o[nbk] = uint16_t(len);
-  __syncthreads();
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
-    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
+    const uint32_t q = uint32_t(r * kPartThreads) + threadIdx.x;
+    if (q < len) atomicAdd(&hist[kk[r] >> p.ws], 1u);
+  }
+  __syncthreads();
+  block_scan_array(hist, nbk, tmp);
+  uint16_t* o = O + orow(p, i, e, sc);
+  for (uint32_t b = threadIdx.x; b < nbk; b += kPartThreads) o[b] = uint16_t(hist[b]);
+  if (threadIdx.x == 0) o[nbk] = uint16_t(len);
+  __syncthreads();  // the offsets are read above before they become cursors below
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const uint32_t q = uint32_t(r * kPartThreads) + threadIdx.x;
     if (q < len) {
-      const uint32_t k = uint32_t(kk[r]);
+      const uint32_t k = kk[r];
       const uint32_t slot = atomicAdd(&hist[k >> p.ws], 1u);
       stage[slot] = ((k & (W - 1)) << kScShift) | q;
     }
   }
   __syncthreads();
-  for (uint32_t q = threadIdx.x; q < len; q += kThreads) Pk[base + q] = stage[q];
+  for (uint32_t q = threadIdx.x; q < len; q += kPartThreads) Pk[base + q] = stage[q];
 }
 
-// Iterates over every read of window kb of worker i whose epoch lies in
-// [e_lo, e_hi), in batches of runs (one run = the window's slice of one
-// sub-chunk). fn(pos, f_base, v, idx) receives the read's position in the
-// partitioned row, the stream position of its sub-chunk start, the packed
-// read, and its index in the order (epoch, sub-chunk, position in run).
-// Loads are issued four per thread before any is consumed, so the latency
-// of the dependent (offsets -> reads) chain is paid once per batch.
+constexpr uint32_t kRunMap = 2048;  // reads whose run index is kept in LDS
+
 template <int NT>
 struct RunTable {
   uint32_t pref[NT + 1];
   int32_t start[NT];  // position in the row of the run's first read
   int32_t fbase[NT];  // stream position of the sub-chunk start
   uint32_t tmp[65];
+  uint16_t run_of[kRunMap];  // run index of each read (when total <= kRunMap)
 };
 
 // Loads the run table of runs [r0, r0 + NT) of epochs [e_lo, e_hi)
@@ -172,7 +165,7 @@ __device__ __forceinline__ uint32_t load_runs(const SegParams& p, int64_t i, uin
   uint32_t len = 0;
   if (r < runs) {
     const int64_t run = e_lo * p.nsc + r;
-    const int64_t e = run / p.nsc, sc = run % p.nsc;
+    const uint32_t e = uint32_t(run) / uint32_t(p.nsc), sc = uint32_t(run) - e * uint32_t(p.nsc);
     const uint32_t a = oa[run], b = ob[run];
     len = b - a;
     rt.fbase[threadIdx.x] = int32_t(e * Li + sc * kSC);
@@ -181,6 +174,8 @@ __device__ __forceinline__ uint32_t load_runs(const SegParams& p, int64_t i, uin
   uint32_t total;
   const uint32_t ex = block_exclusive_scan(len, rt.tmp, &total);
   rt.pref[threadIdx.x] = ex;
+  if (total <= kRunMap)
+    for (uint32_t q = 0; q < len; ++q) rt.run_of[ex + q] = uint16_t(threadIdx.x);
   __syncthreads();
   return total;
 }
@@ -226,10 +221,16 @@ __device__ __forceinline__ void consume_runs(const RunTable<NT>& rt, int nr, uin
       pos[u] = -1;
       fb[u] = 0;
       if (t < total) {
-        int lo = 0, hi = nr - 1;  // last run with pref <= t
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if (rt.pref[mid] <= t) lo = mid; else hi = mid - 1;
+        int lo;
+        if (total <= kRunMap) {
+          lo = rt.run_of[t];
+        } else {
+          lo = 0;  // last run with pref <= t
+          int hi = nr - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (rt.pref[mid] <= t) lo = mid; else hi = mid - 1;
+          }
         }
         pos[u] = rt.start[lo] + (t - rt.pref[lo]);
         fb[u] = rt.fbase[lo];
@@ -322,13 +323,16 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
 
 // -- next ---------------------------------------------------------------------
 // Fast path: the window's reads are gathered into LDS in (epoch, sub-chunk)
-// order, counting-sorted by the top 8 bits of their sample offset, and each
-// of the 256 buckets (about a dozen reads) is insertion-sorted by (sample,
+// order, counting-sorted by the top 10 bits of their sample offset, and each
+// of the 1024 buckets (one or two reads) is insertion-sorted by (sample,
 // position). In that order the read that follows a read of the same sample
 // is its next use.
+constexpr int kNextBucketBits = 10;
+constexpr int kNextBuckets = 1 << kNextBucketBits;
+
 struct NextSmem {
-  uint32_t hist[256];
-  uint32_t cur[256];
+  uint32_t hist[kNextBuckets];
+  uint32_t cur[kNextBuckets];
   int32_t f[kNextEnt];
   int32_t pos[kNextEnt];
   uint16_t kl[kNextEnt];
@@ -397,8 +401,8 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
     return;
   }
   NextSmem& s = *reinterpret_cast<NextSmem*>(sm);
-  const int dshift = p.ws > 8 ? p.ws - 8 : 0;
-  if (threadIdx.x < 256) s.hist[threadIdx.x] = 0;
+  const int dshift = p.ws > kNextBucketBits ? p.ws - kNextBucketBits : 0;
+  for (int d = threadIdx.x; d < kNextBuckets; d += kNextThreads) s.hist[d] = 0;
   __syncthreads();
   auto gather = [&](int64_t pos, int64_t fbase, uint32_t v, uint32_t idx) {
     const uint32_t x = v >> kScShift;
@@ -413,24 +417,17 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
   } else {
     for_each_read(p, i, kb, OT, prow, rt, 0, p.E, gather);
   }
-  {
-    const uint32_t c = threadIdx.x < 256 ? s.hist[threadIdx.x] : 0u;
-    uint32_t tot;
-    const uint32_t ex = block_exclusive_scan(c, rt.tmp, &tot);
-    if (threadIdx.x < 256) {
-      s.hist[threadIdx.x] = ex;
-      s.cur[threadIdx.x] = ex;
-    }
-  }
+  block_scan_array(s.hist, kNextBuckets, rt.tmp);
+  for (int d = threadIdx.x; d < kNextBuckets; d += kNextThreads) s.cur[d] = s.hist[d];
   __syncthreads();
   for (uint32_t idx = threadIdx.x; idx < total; idx += kNextThreads) {
     const uint32_t slot = atomicAdd(&s.cur[s.kl[idx] >> dshift], 1u);
     s.ord[slot] = uint16_t(idx);
   }
   __syncthreads();
-  if (threadIdx.x < 256) {
-    // bucket d = threadIdx.x: order by (sample offset, stream position)
-    const uint32_t a = s.hist[threadIdx.x], b = s.cur[threadIdx.x];
+  for (int d = threadIdx.x; d < kNextBuckets; d += kNextThreads) {
+    // bucket d: order by (sample offset, stream position)
+    const uint32_t a = s.hist[d], b = s.cur[d];
     for (uint32_t u = a + 1; u < b; ++u) {
       const uint16_t v = s.ord[u];
       const uint32_t kv = s.kl[v];
@@ -526,7 +523,7 @@ int run_partition(const SegParams& p, const int32_t* R, Scratch& scr, uint32_t**
   if ((rc = scr.alloc_n(&O, on))) return rc;
   if ((rc = scr.alloc_n(OT, on))) return rc;
   const int64_t wgs = p.N * p.E * p.nsc;
-  if ((rc = launch("seg_partition", seg_partition, dim3(uint32_t(wgs)), dim3(kThreads),
+  if ((rc = launch("seg_partition", seg_partition, dim3(uint32_t(wgs)), dim3(kPartThreads),
                    partition_smem(p), st, p, R, *Pk, O)))
     return rc;
   const int64_t runs = int64_t(p.E) * p.nsc;

@@ -172,4 +172,25 @@ __device__ inline uint64_t block_exclusive_scan64(uint64_t v, uint64_t* tmp,
   return r;
 }
 
+// In-place exclusive scan of the n-entry LDS array a by the whole workgroup:
+// each thread sums a contiguous segment, one block scan combines the
+// segments, and each thread writes its segment's prefixes. Returns the total.
+// Ends with a barrier.
+__device__ inline uint32_t block_scan_array(uint32_t* a, uint32_t n, uint32_t* tmp) {
+  const uint32_t per = (n + blockDim.x - 1) / blockDim.x;
+  const uint32_t b0 = threadIdx.x * per;
+  const uint32_t b1 = b0 + per < n ? b0 + per : n;
+  uint32_t sum = 0;
+  for (uint32_t b = b0; b < b1; ++b) sum += a[b];
+  uint32_t total;
+  uint32_t run = block_exclusive_scan(sum, tmp, &total);
+  for (uint32_t b = b0; b < b1; ++b) {
+    const uint32_t v = a[b];
+    a[b] = run;
+    run += v;
+  }
+  __syncthreads();
+  return total;
+}
+
 }  // namespace nopfs

@@ -60,6 +60,7 @@ struct PlanArgs {
 
 struct ClassTable {
   uint32_t base[256];
+  uint32_t top[256];   // nbc[c] - 1
   float scale[256];
 };
 
@@ -68,10 +69,12 @@ __device__ void build_class_table(const PlanArgs& a, ClassTable& t) {
     uint32_t b = 0;
     for (int c = a.E; c >= 1; --c) {
       t.base[c] = b;
+      t.top[c] = a.nbc[c] - 1u;
       t.scale[c] = float(a.nbc[c]) / float(a.M_max > 0 ? a.M_max : 1);
       b += a.nbc[c];
     }
     t.base[0] = b;
+    t.top[0] = 0;
     t.scale[0] = 0.f;
   }
   __syncthreads();
@@ -84,7 +87,7 @@ __device__ __forceinline__ uint32_t bin_of(const PlanArgs& a, const ClassTable& 
   if (c > uint32_t(a.E)) c = uint32_t(a.E);
   float x = f > 0 ? float(f) * t.scale[c] : 0.f;
   uint32_t xi = uint32_t(x);
-  const uint32_t top = a.nbc[c] - 1u;
+  const uint32_t top = t.top[c];
   if (xi > top) xi = top;
   return t.base[c] + xi;
 }
@@ -280,6 +283,10 @@ plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
            CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t nslices) {
   __shared__ ClassTable ct;
   __shared__ int32_t rg[256];
+  // tier of every bin this workgroup can meet (all bins of classes >= 1,
+  // then this slice's class-0 bins); kCand marks candidate bins
+  __shared__ int8_t btier[kBins1Budget + 256 + kSliceBins0];
+  constexpr int kCand = 127;
   const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
   if (t >= uint32_t(a.N) * nslices) return;
   const int64_t sl = t / a.N, i = t - sl * a.N;
@@ -288,25 +295,33 @@ plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
   __syncthreads();
   const int64_t ks = sl * kSliceCells;
   const int64_t ke = ks + kSliceCells < a.F ? ks + kSliceCells : a.F;
+  const uint32_t b0_slice = a.nbin1 + uint32_t(ks >> kClass0Shift);
+  const uint32_t nb_slice = uint32_t((ke - ks + (1 << kClass0Shift) - 1) >> kClass0Shift);
+  for (uint32_t x = threadIdx.x; x < a.nbin1 + nb_slice; x += kThreads) {
+    const int32_t b = int32_t(x < a.nbin1 ? x : b0_slice + (x - a.nbin1));
+    bool cand = false;
+    int tv = 0;
+    for (int j = 0; j < a.J; ++j) {
+      cand |= b >= rg[2 * j] && b <= rg[2 * j + 1];
+      tv += rg[2 * j + 1] < b;
+    }
+    btier[x] = cand ? int8_t(kCand) : (tv >= a.J ? int8_t(-1) : int8_t(tv));
+  }
+  __syncthreads();
   const uint8_t* crow = count + i * a.F;
   const int32_t* frow = first + i * a.F;
   int8_t* trow = tier + i * a.F;
   CandRec* ci = cand + i * int64_t(a.cmax);
-  // tier of one cell; *key receives its candidate record key when it is one
+  // tier of one cell, or 256 for a candidate (its record key in *key)
   auto classify = [&](int64_t k, uint32_t c, int32_t f, uint64_t* key) -> int {
     if (c == 0) f = -1;
     const uint32_t b = bin_of(a, ct, c, f, k);
-    bool is_cand = false;
-    int tv = 0;
-    for (int j = 0; j < a.J; ++j) {
-      is_cand |= int32_t(b) >= rg[2 * j] && int32_t(b) <= rg[2 * j + 1];
-      tv += int32_t(b) > rg[2 * j + 1];
-    }
-    if (is_cand) {
+    const int tv = btier[b < a.nbin1 ? b : a.nbin1 + (b - b0_slice)];
+    if (tv == kCand) {
       *key = (uint64_t(b) << 32) | (c ? uint64_t(uint32_t(f)) : uint64_t(k));
-      return 256;  // marker: candidate (placeholder tier 0)
+      return 256;
     }
-    return tv >= a.J ? -1 : tv;
+    return tv;
   };
   auto single = [&](int64_t k) {
     uint64_t key = 0;

@@ -386,24 +386,43 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
   const uint32_t j0 = lo / N, j1 = (pend - 1) / N;
   const uint32_t nj = j1 - j0 + 1;
   const uint32_t Np = (N & 1u) ? N : N + 1u;  // odd row pitch: conflict-free columns
+  // (j, i) of position lo + threadIdx.x, stepped by kSortThreads positions
+  // per iteration without dividing
+  const uint32_t step_i = kSortThreads % N, step_j = kSortThreads / N;
+  uint32_t ci = (lo + threadIdx.x) % N, cj = (lo + threadIdx.x) / N;
   if (uint64_t(nj) * Np <= uint64_t(kSortCap)) {
     uint32_t* stage = s.keys;
     for (uint32_t q = threadIdx.x; lo + q < pend; q += kSortThreads) {
-      const uint32_t pp = lo + q;
-      stage[(pp / N - j0) * Np + pp % N] = uint32_t(s.ids[q]);
+      stage[(cj - j0) * Np + ci] = uint32_t(s.ids[q]);
+      ci += step_i;
+      cj += step_j;
+      if (ci >= N) {
+        ci -= N;
+        ++cj;
+      }
     }
     __syncthreads();
+    // t -> (row i, column jj) with consecutive t on consecutive columns of a
+    // row; t < 2^13, so the float reciprocal gives t / nj up to one step
     const uint32_t total = nj * N;
+    const float inv_nj = 1.0f / float(nj);
     for (uint32_t t = threadIdx.x; t < total; t += kSortThreads) {
-      const uint32_t i = t / nj, jj = t - i * nj;
+      uint32_t i = uint32_t(float(t) * inv_nj);
+      if (i * nj > t) --i;
+      else if ((i + 1) * nj <= t) ++i;
+      const uint32_t jj = t - i * nj;
       const uint32_t pp = (j0 + jj) * N + i;
       if (pp >= lo && pp < pend) R[row_offset(p, i, e) + j0 + jj] = int32_t(stage[jj * Np + i]);
     }
   } else {
     for (uint32_t q = threadIdx.x; lo + q < pend; q += kSortThreads) {
-      const uint32_t pp = lo + q;
-      const uint32_t i = pp % N, j = pp / N;
-      R[row_offset(p, i, e) + j] = s.ids[q];
+      R[row_offset(p, ci, e) + cj] = s.ids[q];
+      ci += step_i;
+      cj += step_j;
+      if (ci >= N) {
+        ci -= N;
+        ++cj;
+      }
     }
   }
 }
