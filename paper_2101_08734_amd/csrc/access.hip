@@ -322,21 +322,19 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
 }
 
 // -- next ---------------------------------------------------------------------
-// Fast path: the window's reads are gathered into LDS in (epoch, sub-chunk)
-// order, counting-sorted by the top 10 bits of their sample offset, and each
-// of the 1024 buckets (one or two reads) is insertion-sorted by (sample,
-// position). In that order the read that follows a read of the same sample
-// is its next use.
-constexpr int kNextBucketBits = 10;
-constexpr int kNextBuckets = 1 << kNextBucketBits;
+// Fast path: the window's reads are gathered into LDS and pushed onto short
+// chains, one per hash slot of their sample offset (atomic exchange on the
+// slot head). A read's next use is then the smallest later stream position
+// among the reads of the same sample on its chain; chains hold about one
+// read on average, so no sort is needed.
+constexpr int kNextSlots = 4096;  // hash slots per window (power of two)
+constexpr uint32_t kNoLink = 0xFFFFu;
 
 struct NextSmem {
-  uint32_t hist[kNextBuckets];
-  uint32_t cur[kNextBuckets];
+  uint32_t head[kNextSlots];
   int32_t f[kNextEnt];
-  int32_t pos[kNextEnt];
   uint16_t kl[kNextEnt];
-  uint16_t ord[kNextEnt];
+  uint16_t link[kNextEnt];
 };
 
 __device__ void next_tile_slow(const SegParams& p, int64_t i, uint32_t kb, const uint32_t* prow,
@@ -401,78 +399,82 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
     return;
   }
   NextSmem& s = *reinterpret_cast<NextSmem*>(sm);
-  const int dshift = p.ws > kNextBucketBits ? p.ws - kNextBucketBits : 0;
-  for (int d = threadIdx.x; d < kNextBuckets; d += kNextThreads) s.hist[d] = 0;
+  for (int d = threadIdx.x; d < kNextSlots; d += kNextThreads) s.head[d] = kNoLink;
   __syncthreads();
-  auto gather = [&](int64_t pos, int64_t fbase, uint32_t v, uint32_t idx) {
+  auto gather = [&](int64_t, int64_t fbase, uint32_t v, uint32_t idx) {
     const uint32_t x = v >> kScShift;
     s.kl[idx] = uint16_t(x);
     s.f[idx] = int32_t(fbase + (v & kJMask));
-    s.pos[idx] = int32_t(pos);
-    atomicAdd(&s.hist[x >> dshift], 1u);
+    s.link[idx] = uint16_t(atomicExch(&s.head[x & (kNextSlots - 1)], idx));
   };
   if (runs <= kNextThreads) {
     consume_runs(rt, int(runs), total, prow, 0u, gather);
-    __syncthreads();
   } else {
     for_each_read(p, i, kb, OT, prow, rt, 0, p.E, gather);
   }
-  block_scan_array(s.hist, kNextBuckets, rt.tmp);
-  for (int d = threadIdx.x; d < kNextBuckets; d += kNextThreads) s.cur[d] = s.hist[d];
   __syncthreads();
-  for (uint32_t idx = threadIdx.x; idx < total; idx += kNextThreads) {
-    const uint32_t slot = atomicAdd(&s.cur[s.kl[idx] >> dshift], 1u);
-    s.ord[slot] = uint16_t(idx);
-  }
-  __syncthreads();
-  for (int d = threadIdx.x; d < kNextBuckets; d += kNextThreads) {
-    // bucket d: order by (sample offset, stream position)
-    const uint32_t a = s.hist[d], b = s.cur[d];
-    for (uint32_t u = a + 1; u < b; ++u) {
-      const uint16_t v = s.ord[u];
-      const uint32_t kv = s.kl[v];
-      const int32_t fv = s.f[v];
-      uint32_t c = u;
-      while (c > a) {
-        const uint16_t w = s.ord[c - 1];
-        const uint32_t kw = s.kl[w];
-        if (kw < kv || (kw == kv && s.f[w] < fv)) break;
-        s.ord[c] = w;
-        --c;
+  // each read: smallest later position of the same sample on its chain
+  constexpr int kPerThread = (kNextEnt + kNextThreads - 1) / kNextThreads;
+  int32_t res[kPerThread];
+#pragma unroll
+  for (int q = 0; q < kPerThread; ++q) {
+    const uint32_t idx = threadIdx.x + q * kNextThreads;
+    res[q] = -1;
+    if (idx < total) {
+      const uint32_t x = s.kl[idx];
+      const int32_t f = s.f[idx];
+      int32_t best = INT_MAX;
+      for (uint32_t w = s.head[x & (kNextSlots - 1)]; w != kNoLink; w = s.link[w]) {
+        const int32_t fw = s.f[w];
+        if (s.kl[w] == x && fw > f && fw < best) best = fw;
       }
-      s.ord[c] = v;
+      res[q] = best == INT_MAX ? -1 : best;
     }
   }
-  __syncthreads();
-  for (uint32_t u = threadIdx.x; u < total; u += kNextThreads) {
-    const uint32_t idx = s.ord[u];
-    int32_t nx = -1;
-    if (u + 1 < total) {
-      const uint32_t nidx = s.ord[u + 1];
-      if (s.kl[nidx] == s.kl[idx]) nx = s.f[nidx];
+  if (runs <= kNextThreads && total <= kRunMap) {
+    // output position from the read's index through the run table
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+      const uint32_t idx = threadIdx.x + q * kNextThreads;
+      if (idx < total) {
+        const int r = rt.run_of[idx];
+        nrow[rt.start[r] + (idx - rt.pref[r])] = res[q];
+      }
     }
-    nrow[s.pos[idx]] = nx;
+  } else {
+    __syncthreads();  // every chain walk is done before f is overwritten
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+      const uint32_t idx = threadIdx.x + q * kNextThreads;
+      if (idx < total) s.f[idx] = res[q];
+    }
+    __syncthreads();
+    for_each_read(p, i, kb, OT, prow, rt, 0, p.E,
+                  [&](int64_t pos, int64_t, uint32_t, uint32_t idx) { nrow[pos] = s.f[idx]; });
   }
 }
 
-__global__ void __launch_bounds__(kThreads)
+constexpr int kUnpartThreads = 1024;
+
+__global__ void __launch_bounds__(kUnpartThreads)
 next_unpartition(SegParams p, const uint32_t* __restrict__ Pk, const int32_t* __restrict__ nextP,
                  int32_t* __restrict__ next) {
   __shared__ int32_t stage[kSC];
-  const int64_t wg = blockIdx.x;
-  const int64_t per_worker = int64_t(p.E) * p.nsc;
-  const int64_t i = wg / per_worker;
-  const int64_t rem = wg - i * per_worker;
-  const int64_t e = rem / p.nsc, sc = rem - e * p.nsc;
+  const uint32_t wg = blockIdx.x;
+  const uint32_t per_worker = uint32_t(p.E) * uint32_t(p.nsc);
+  const uint32_t i = wg / per_worker;
+  const uint32_t rem = wg - i * per_worker;
+  const uint32_t e = rem / uint32_t(p.nsc), sc = rem - e * uint32_t(p.nsc);
   const int64_t Li = seg_len(p, i);
-  int64_t len64 = Li - sc * kSC;
+  int64_t len64 = Li - int64_t(sc) * kSC;
   len64 = len64 < 0 ? 0 : (len64 > kSC ? kSC : len64);
   const uint32_t len = uint32_t(len64);
   if (len == 0) return;
-  const int64_t base = i * p.M_max + e * Li + sc * kSC;
-  for (uint32_t q = threadIdx.x; q < len; q += kThreads) stage[Pk[base + q] & kJMask] = nextP[base + q];
+  const int64_t base = int64_t(i) * p.M_max + int64_t(e) * Li + int64_t(sc) * kSC;
+  for (uint32_t q = threadIdx.x; q < len; q += kUnpartThreads)
+    stage[Pk[base + q] & kJMask] = nextP[base + q];
   __syncthreads();
-  for (uint32_t q = threadIdx.x; q < len; q += kThreads) next[base + q] = stage[q];
+  for (uint32_t q = threadIdx.x; q < len; q += kUnpartThreads) next[base + q] = stage[q];
 }
 
 __global__ void pad_rows(SegParams p, int32_t* __restrict__ out) {
@@ -591,7 +593,8 @@ int next_impl(const nopfs_job* job, const int32_t* R, int32_t* next, hipStream_t
                    (const uint32_t*)Pk, (const uint16_t*)OT, nextP, ntiles)))
     return rc;
   const int64_t wgs = s.N * s.E * p.nsc;
-  if ((rc = launch("next_unpartition", next_unpartition, dim3(uint32_t(wgs)), dim3(kThreads), 0, st, p,
+  if ((rc = launch("next_unpartition", next_unpartition, dim3(uint32_t(wgs)), dim3(kUnpartThreads), 0,
+                   st, p,
                    (const uint32_t*)Pk, (const int32_t*)nextP, next)))
     return rc;
   if (!s.drop_last && s.F % s.N != 0)
