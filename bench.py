@@ -77,6 +77,62 @@ def committed_traffic(workload, kernel):
     return None
 
 
+def _kernel_short_name(full):
+    """'ns::(anonymous namespace)::plan_hist<true>(args...)' -> 'plan_hist'."""
+    import re
+    m = re.findall(r"(\w+)(?:<[^>()]*>)?\(", full)
+    return m[-1] if m else full
+
+
+def rocprof_summary(d, workload):
+    """Summarises rocprofv3 output under d (kt/ kernel trace with --stats,
+    fetch/ and write/ counter runs of FETCH_SIZE and WRITE_SIZE), all made by
+    this script's benchmark command. Counters are scaled by what they read
+    for the calibration copy (1 GiB read + 1 GiB written). Prints a Markdown
+    report ending with one JSON line that the benchmark reads back."""
+    import collections
+    import csv
+    stats = {}
+    for path in glob.glob(os.path.join(d, "kt", "*kernel_stats.csv")):
+        for r in csv.DictReader(open(path)):
+            stats[_kernel_short_name(r["Name"])] = (int(r["Calls"]), float(r["AverageNs"]) / 1e6,
+                                                    float(r["Percentage"]))
+    ctr = collections.defaultdict(lambda: collections.defaultdict(list))
+    for sub in ("fetch", "write"):
+        for path in glob.glob(os.path.join(d, sub, "*counter_collection.csv")):
+            for r in csv.DictReader(open(path)):
+                ctr[_kernel_short_name(r["Kernel_Name"])][r["Counter_Name"]].append(
+                    float(r["Counter_Value"]))
+    cal = ctr.get("calibration_copy_kernel", {})
+    gib_kib = float(1 << 20)
+    ff = gib_kib / (sum(cal["FETCH_SIZE"]) / len(cal["FETCH_SIZE"])) if cal.get("FETCH_SIZE") else None
+    wf = gib_kib / (sum(cal["WRITE_SIZE"]) / len(cal["WRITE_SIZE"])) if cal.get("WRITE_SIZE") else None
+    out = {"source_hash": kernel_source_hash(), "workload": workload,
+           "fetch_factor": ff, "write_factor": wf, "kernels": {}}
+    lines = [f"| kernel | calls | avg ms | % time | HBM read GB/launch | HBM write GB/launch | GB/s |",
+             "|---|---|---|---|---|---|---|"]
+    for k, (calls, avg_ms, pct) in sorted(stats.items(), key=lambda x: -x[1][2]):
+        c = ctr.get(k, {})
+        rd = wr = None
+        if c.get("FETCH_SIZE") and ff:
+            rd = sum(c["FETCH_SIZE"]) / len(c["FETCH_SIZE"]) * 1024 * ff
+        if c.get("WRITE_SIZE") and wf:
+            wr = sum(c["WRITE_SIZE"]) / len(c["WRITE_SIZE"]) * 1024 * wf
+        tot = (rd or 0) + (wr or 0)
+        out["kernels"][k] = {"calls": calls, "avg_ms": round(avg_ms, 5),
+                             "hbm_read_bytes_per_launch": rd, "hbm_write_bytes_per_launch": wr,
+                             "hbm_bytes_per_launch": tot if rd is not None and wr is not None else None}
+        gbs = f"{tot / (avg_ms * 1e-3) / 1e9:.0f}" if avg_ms > 0 and tot else ""
+        lines.append(f"| {k} | {calls} | {avg_ms:.4f} | {pct:.2f} | "
+                     f"{'' if rd is None else f'{rd / 1e9:.3f}'} | "
+                     f"{'' if wr is None else f'{wr / 1e9:.3f}'} | {gbs} |")
+    print("\n".join(lines))
+    print()
+    print(f"Counter scaling from the calibration copy: FETCH_SIZE x {ff}, WRITE_SIZE x {wf}.")
+    print()
+    print(json.dumps(out))
+
+
 def cpu_baseline(w, sizes, caps, epochs=2, workers=2):
     """The oracle on a bounded sample of the same workload: `epochs` of the E
     epochs sorted and sharded for all workers, and stats, next use and plan
@@ -122,7 +178,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-bytes", type=int, default=1 << 30,
                     help="size of the calibration copy run after the timed steps")
+    ap.add_argument("--rocprof-summary", metavar="DIR",
+                    help="summarise rocprofv3 output of this benchmark (no GPU needed)")
     args = ap.parse_args()
+    if args.rocprof_summary:
+        rocprof_summary(args.rocprof_summary, args.workload)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py plans all N workers of a job on one GPU; runs on more than one "
               "GPU are not part of this build (use --gpus 1).", file=sys.stderr)
