@@ -40,8 +40,8 @@ constexpr int kBlocksPerThread = 16;                                   // Philox
 constexpr int64_t kChunkIds = int64_t(kChunkThreads) * kBlocksPerThread * 4;  // 65536
 constexpr uint32_t kMaxBuckets = 8192;
 
-constexpr int kSortThreads = 512;
-constexpr int kItems = 16;
+constexpr int kSortThreads = 1024;
+constexpr int kItems = 8;
 constexpr int kSortCap = kSortThreads * kItems;  // 8192 (key, id) pairs in LDS
 constexpr int kDigitBits = 11;
 constexpr int kDigits = 1 << kDigitBits;
@@ -139,18 +139,30 @@ stream_scan(uint32_t nb, const uint32_t* __restrict__ tot, uint32_t* __restrict_
 
 // -- 4. scatter into coarse buckets ------------------------------------------
 // Target bucket t = umulhi(key, nt): the fine bucket when nf = 1 (nt = nb),
-// else the coarse bucket (nt = nb1). A chunk's share of coarse bucket c
-// starts at the bucket's first fine start plus the chunk's offsets in each
-// of its fine buckets.
+// else the coarse bucket (nt = nb1); nt <= 64 either way. A chunk's share of
+// bucket t starts at the bucket's first fine start plus the chunk's offsets
+// in each of its fine buckets. The chunk is processed in rounds of 8K ids:
+// each round is counting-sorted by bucket in LDS and every bucket's part of
+// the round is written as one contiguous run after the previous rounds'.
+constexpr int kRoundIds = 8192;
+constexpr int kRoundBlocks = kRoundIds / 4 / kChunkThreads;  // Philox blocks per thread
+constexpr int kMaxTargets = 64;
+
+struct ScatterSmem {
+  uint32_t key[kRoundIds];
+  int32_t id[kRoundIds];
+  uint32_t cnt[kMaxTargets];
+  uint32_t off[kMaxTargets];   // start of each bucket's run in the round
+  uint32_t base[kMaxTargets];  // next free position of each bucket (global)
+};
+
 __global__ void __launch_bounds__(kChunkThreads)
 stream_scatter(StreamParams p, uint32_t nchunks, const uint32_t* __restrict__ cnt,
                const uint32_t* __restrict__ start, uint32_t* __restrict__ keys,
                int32_t* __restrict__ ids) {
-  extern __shared__ uint32_t smem[];
+  __shared__ ScatterSmem s;
   const uint32_t nb = p.nb, nf = p.nf;
   const uint32_t nt = nf == 1 ? nb : p.nb1;
-  uint32_t* slot = smem;
-  uint32_t* base = smem + nt;
   const uint32_t chunk = xcd_logical(blockIdx.x, gridDim.x);
   if (chunk >= nchunks) return;
   const uint32_t* off = cnt + (int64_t(blockIdx.y) * nchunks + chunk) * nb;
@@ -158,54 +170,91 @@ stream_scatter(StreamParams p, uint32_t nchunks, const uint32_t* __restrict__ cn
   for (uint32_t b = threadIdx.x; b < nt; b += blockDim.x) {
     uint32_t o = 0;
     for (uint32_t f = b * nf; f < (b + 1) * nf; ++f) o += off[f];
-    slot[b] = 0;
-    base[b] = st[b * nf] + o;
+    s.base[b] = st[b * nf] + o;
   }
-  __syncthreads();
   const uint32_t e = uint32_t(p.e0) + blockIdx.y;
-  const int64_t blk0 = int64_t(chunk) * (kChunkIds / 4);
   uint32_t* ko = keys + int64_t(blockIdx.y) * p.F;
   int32_t* io = ids + int64_t(blockIdx.y) * p.F;
-#pragma unroll 2
-  for (int it = 0; it < kBlocksPerThread; ++it) {
-    const int64_t blk = blk0 + it * kChunkThreads + threadIdx.x;
-    const int64_t id0 = blk * 4;
-    if (id0 < p.F) {
+  const int64_t id_chunk = int64_t(chunk) * kChunkIds;
+  for (int64_t r0 = id_chunk; r0 < id_chunk + kChunkIds && r0 < p.F; r0 += kRoundIds) {
+    if (threadIdx.x < nt) s.cnt[threadIdx.x] = 0;
+    __syncthreads();
+    uint32_t w[kRoundBlocks][4], slot[kRoundBlocks][4];
+#pragma unroll
+    for (int it = 0; it < kRoundBlocks; ++it) {
+      const int64_t blk = r0 / 4 + it * kChunkThreads + threadIdx.x;
+      const int64_t id0 = blk * 4;
       const Philox4 r = philox_block(uint32_t(blk), e, p.seed_lo, p.seed_hi);
-      const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+      w[it][0] = r.x; w[it][1] = r.y; w[it][2] = r.z; w[it][3] = r.w;
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (id0 + c < p.F) slot[it][c] = atomicAdd(&s.cnt[__umulhi(w[it][c], nt)], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const uint32_t v = threadIdx.x < nt ? s.cnt[threadIdx.x] : 0u;
+      const uint32_t inc = wave_inclusive_scan(v);
+      if (threadIdx.x < nt) s.off[threadIdx.x] = inc - v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int it = 0; it < kRoundBlocks; ++it) {
+      const int64_t blk = r0 / 4 + it * kChunkThreads + threadIdx.x;
+      const int64_t id0 = blk * 4;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         if (id0 + c < p.F) {
-          const uint32_t b = __umulhi(w[c], nt);
-          const uint32_t dst = base[b] + atomicAdd(&slot[b], 1u);
-          ko[dst] = w[c];
-          io[dst] = int32_t(id0 + c);
+          const uint32_t q = s.off[__umulhi(w[it][c], nt)] + slot[it][c];
+          s.key[q] = w[it][c];
+          s.id[q] = int32_t(id0 + c);
         }
       }
     }
+    __syncthreads();
+    const uint32_t n = uint32_t(p.F - r0 < kRoundIds ? p.F - r0 : kRoundIds);
+    for (uint32_t q = threadIdx.x; q < n; q += kChunkThreads) {
+      const uint32_t k = s.key[q];
+      const uint32_t b = __umulhi(k, nt);
+      const uint32_t dst = s.base[b] + (q - s.off[b]);
+      ko[dst] = k;
+      io[dst] = s.id[q];
+    }
+    __syncthreads();
+    if (threadIdx.x < nt) s.base[threadIdx.x] += s.cnt[threadIdx.x];
   }
 }
 
 // -- 5. split coarse buckets into fine buckets ---------------------------------
+// A piece of 8K pairs of coarse bucket c per round: counting sort by fine
+// bucket in LDS, then one contiguous run per fine bucket at a position taken
+// from the bucket's cursor.
 constexpr int kSplitThreads = 1024;
-constexpr int kSplitItems = 16;
+constexpr int kSplitItems = 8;
 constexpr uint32_t kSplitPiece = kSplitThreads * kSplitItems;
+constexpr uint32_t kMaxFine = 256;
+
+struct SplitSmem {
+  uint32_t key[kSplitPiece];
+  int32_t id[kSplitPiece];
+  uint32_t cnt[kMaxFine];
+  uint32_t off[kMaxFine];
+  uint32_t base[kMaxFine];
+  uint32_t tmp[65];
+};
 
 __global__ void __launch_bounds__(kSplitThreads)
 stream_split(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __restrict__ cursor,
              const uint32_t* __restrict__ keys1, const int32_t* __restrict__ ids1,
              uint32_t* __restrict__ keys, int32_t* __restrict__ ids) {
-  extern __shared__ uint32_t smem[];
+  __shared__ SplitSmem s;
   const uint32_t nb = p.nb, nf = p.nf;
-  uint32_t* cnt = smem;
-  uint32_t* base = smem + nf;
   const uint32_t c = blockIdx.y;
   const int64_t eoff = int64_t(blockIdx.z) * p.F;
   const uint32_t* st = start + int64_t(blockIdx.z) * (nb + 1);
   uint32_t* cur = cursor + int64_t(blockIdx.z) * nb;
   const uint32_t r0 = st[c * nf], r1 = st[(c + 1) * nf];
   for (uint32_t q0 = r0 + blockIdx.x * kSplitPiece; q0 < r1; q0 += gridDim.x * kSplitPiece) {
-    for (uint32_t f = threadIdx.x; f < nf; f += kSplitThreads) cnt[f] = 0;
+    for (uint32_t f = threadIdx.x; f < nf; f += kSplitThreads) s.cnt[f] = 0;
     __syncthreads();
     uint32_t k[kSplitItems], sl[kSplitItems];
     int32_t id[kSplitItems];
@@ -215,21 +264,38 @@ stream_split(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __res
       if (q < r1) {
         k[r] = keys1[eoff + q];
         id[r] = ids1[eoff + q];
-        sl[r] = atomicAdd(&cnt[__umulhi(k[r], nb) - c * nf], 1u);
+        sl[r] = atomicAdd(&s.cnt[__umulhi(k[r], nb) - c * nf], 1u);
       }
     }
     __syncthreads();
-    for (uint32_t f = threadIdx.x; f < nf; f += kSplitThreads)
-      if (cnt[f]) base[f] = atomicAdd(&cur[c * nf + f], cnt[f]);
+    {
+      const uint32_t f = threadIdx.x;
+      const uint32_t v = f < nf ? s.cnt[f] : 0u;
+      uint32_t tot;
+      const uint32_t ex = block_exclusive_scan(v, s.tmp, &tot);
+      if (f < nf) {
+        s.off[f] = ex;
+        if (v) s.base[f] = atomicAdd(&cur[c * nf + f], v);
+      }
+    }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kSplitItems; ++r) {
       const uint32_t q = q0 + r * kSplitThreads + threadIdx.x;
       if (q < r1) {
-        const uint32_t dst = base[__umulhi(k[r], nb) - c * nf] + sl[r];
-        keys[eoff + dst] = k[r];
-        ids[eoff + dst] = id[r];
+        const uint32_t d = s.off[__umulhi(k[r], nb) - c * nf] + sl[r];
+        s.key[d] = k[r];
+        s.id[d] = id[r];
       }
+    }
+    __syncthreads();
+    const uint32_t n = r1 - q0 < kSplitPiece ? r1 - q0 : kSplitPiece;
+    for (uint32_t q = threadIdx.x; q < n; q += kSplitThreads) {
+      const uint32_t kk = s.key[q];
+      const uint32_t f = __umulhi(kk, nb) - c * nf;
+      const uint32_t dst = s.base[f] + (q - s.off[f]);
+      keys[eoff + dst] = kk;
+      ids[eoff + dst] = s.id[q];
     }
     __syncthreads();
   }
@@ -488,7 +554,6 @@ int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st) {
   if ((rc = scr.alloc_n(&tot, size_t(EB * nb)))) return rc;
   if ((rc = scr.alloc_n(&start, size_t(EB * (nb + 1))))) return rc;
   if ((rc = scr.alloc_n(&cursor, size_t(EB * nb)))) return rc;
-  const uint32_t nt = nf == 1 ? nb : nb1;
   // pieces per coarse bucket for the split: about 1.25x the mean size
   const uint32_t pieces = uint32_t(ceil_div(ceil_div(s.F, nb1) * 5 / 4, kSplitPiece));
 
@@ -505,12 +570,12 @@ int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st) {
                      (const uint32_t*)tot, start, cursor)))
       return rc;
     if ((rc = launch("stream_scatter", stream_scatter, dim3(xcd_padded(nchunks), eb),
-                     dim3(kChunkThreads), size_t(nt) * 8, st, p, nchunks, (const uint32_t*)cnt,
+                     dim3(kChunkThreads), 0, st, p, nchunks, (const uint32_t*)cnt,
                      (const uint32_t*)start, nf > 1 ? keys1 : keys, nf > 1 ? ids1 : ids)))
       return rc;
     if (nf > 1) {
       if ((rc = launch("stream_split", stream_split, dim3(pieces, nb1, eb), dim3(kSplitThreads),
-                       size_t(nf) * 8, st, p, (const uint32_t*)start, cursor,
+                       0, st, p, (const uint32_t*)start, cursor,
                        (const uint32_t*)keys1, (const int32_t*)ids1, keys, ids)))
         return rc;
     }
