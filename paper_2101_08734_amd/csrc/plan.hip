@@ -14,8 +14,10 @@
 //                   and flushed once per slice. Bins of class count>=1 split
 //                   the first-read range; their number per class follows the
 //                   expected Binomial(E, L/F) population so crowded classes
-//                   get fine bins. Class 0 is binned by id, 256 ids a bin,
-//                   and its bytes are the bin's total minus the bytes read.
+//                   get fine bins. Class 0 is binned by id, 256 ids a bin;
+//                   the bytes read per class-0 bin are summed per wave and
+//                   added to a global array, and plan_cut takes the bin's
+//                   total minus those bytes.
 //   Both passes over the [N][F] tables read four cells per lane with one
 //   32-bit load of counts and one 128-bit load of first reads.
 //   plan_cut     -- per worker: prefix sums over bins, then for each tier the
@@ -149,56 +151,95 @@ __device__ __forceinline__ RowSplit split_row(int64_t flat0, int64_t ks, int64_t
 template <bool kVec>
 __global__ void __launch_bounds__(kThreads)
 plan_hist(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restrict__ first,
-          const int64_t* __restrict__ sizes, const uint64_t* __restrict__ binsum,
+          const int64_t* __restrict__ sizes, uint64_t* __restrict__ Z,
           uint64_t* __restrict__ H, uint32_t nslices) {
   extern __shared__ uint64_t sm[];
   uint64_t* h1 = sm;                 // nbin1 weighted bins
-  uint64_t* h0 = sm + a.nbin1;       // bytes read, per class-0 bin of the slice
   __shared__ ClassTable ct;
   const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
   if (t >= uint32_t(a.N) * nslices) return;
   const int64_t sl = t / a.N, i = t - sl * a.N;
   build_class_table(a, ct);
   for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads) h1[b] = 0;
-  for (uint32_t b = threadIdx.x; b < uint32_t(kSliceBins0); b += kThreads) h0[b] = 0;
   __syncthreads();
   const int64_t ks = sl * kSliceCells;
   const int64_t ke = ks + kSliceCells < a.F ? ks + kSliceCells : a.F;
   const uint8_t* crow = count + i * a.F;
   const int32_t* frow = first + i * a.F;
+  unsigned long long* Zi = reinterpret_cast<unsigned long long*>(Z + i * int64_t(a.nb0));
   auto cell = [&](int64_t k, uint32_t c, int32_t f) {
     if (c != 0) {
       const unsigned long long sz = static_cast<unsigned long long>(sizes[k]);
       atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_of(a, ct, c, f, k)]), sz);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&h0[(k - ks) >> kClass0Shift]), sz);
+      atomicAdd(&Zi[k >> kClass0Shift], sz);
     }
   };
   const RowSplit rs = split_row(i * a.F + ks, ks, ke, kVec);
   for (int64_t k = ks + threadIdx.x; k < rs.body0; k += kThreads) cell(k, crow[k], frow[k]);
   for (int64_t k = rs.tail0 + threadIdx.x; k < ke; k += kThreads) cell(k, crow[k], frow[k]);
+  // Body: 4 cells per lane, kU lanes' worth of units per thread per
+  // iteration. The next iteration's count and first words are requested
+  // before this one's sizes, so one memory round trip overlaps the other.
   constexpr int kU = 4;
-  for (int64_t u0 = 0; u0 < rs.nunits; u0 += kU * kThreads) {
-    uint32_t cw[kU];
-    int4 fw[kU];
+  uint32_t cw[kU];
+  int4 fw[kU];
+  auto load = [&](int64_t u0) {
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
       const int64_t u = u0 + j * kThreads + threadIdx.x;
       const int64_t k = rs.body0 + 4 * u;
+      cw[j] = 0;
       if (u < rs.nunits) {
         cw[j] = *reinterpret_cast<const uint32_t*>(crow + k);
         fw[j] = *reinterpret_cast<const int4*>(frow + k);
-      } else {
-        cw[j] = 0;
       }
+    }
+  };
+  if (rs.nunits > 0) load(0);
+  for (int64_t u0 = 0; u0 < rs.nunits; u0 += kU * kThreads) {
+    uint32_t c[kU];
+    int4 f[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      c[j] = cw[j];
+      f[j] = fw[j];
+    }
+    if (u0 + kU * kThreads < rs.nunits) load(u0 + kU * kThreads);
+    uint64_t sz[kU][4];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int64_t k = rs.body0 + 4 * (u0 + j * kThreads + threadIdx.x);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        sz[j][q] = ((c[j] >> (8 * q)) & 0xFFu) ? uint64_t(sizes[k + q]) : 0ull;
     }
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
-      if (cw[j] == 0) continue;
       const int64_t k = rs.body0 + 4 * (u0 + j * kThreads + threadIdx.x);
-      cell(k + 0, cw[j] & 0xFFu, fw[j].x);
-      cell(k + 1, (cw[j] >> 8) & 0xFFu, fw[j].y);
-      cell(k + 2, (cw[j] >> 16) & 0xFFu, fw[j].z);
-      cell(k + 3, cw[j] >> 24, fw[j].w);
+      const int32_t fv[4] = {f[j].x, f[j].y, f[j].z, f[j].w};
+      // bytes read, split at the class-0 bin boundary inside this wave's
+      // 256 consecutive cells, reduced over the wave
+      const int64_t kw = rs.body0 + 4 * (u0 + j * kThreads + (threadIdx.x & ~63u));
+      const int64_t kcut = ((kw >> kClass0Shift) + 1) << kClass0Shift;
+      uint64_t lo = 0, hi = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t cq = (c[j] >> (8 * q)) & 0xFFu;
+        if (cq != 0) {
+          atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_of(a, ct, cq, fv[q], k + q)]),
+                    static_cast<unsigned long long>(sz[j][q]));
+          if (k + q < kcut) lo += sz[j][q]; else hi += sz[j][q];
+        }
+      }
+#pragma unroll
+      for (int d = 32; d >= 1; d >>= 1) {
+        lo += __shfl_xor(lo, d, 64);
+        hi += __shfl_xor(hi, d, 64);
+      }
+      if (__lane_id() == 0 && kw < ke) {
+        if (lo) atomicAdd(&Zi[kw >> kClass0Shift], static_cast<unsigned long long>(lo));
+        if (hi) atomicAdd(&Zi[kcut >> kClass0Shift], static_cast<unsigned long long>(hi));
+      }
     }
   }
   __syncthreads();
@@ -206,24 +247,25 @@ plan_hist(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restri
   for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads)
     if (h1[b]) atomicAdd(reinterpret_cast<unsigned long long*>(&Hi[b]),
                          static_cast<unsigned long long>(h1[b]));
-  // class 0: all bytes of the bin minus the bytes of samples read
-  const uint32_t b0 = uint32_t(ks >> kClass0Shift);
-  const uint32_t nb = uint32_t((ke - ks + (1 << kClass0Shift) - 1) >> kClass0Shift);
-  for (uint32_t b = threadIdx.x; b < nb; b += kThreads)
-    Hi[a.nbin1 + b0 + b] = binsum[b0 + b] - h0[b];
 }
 
 // -- cut ranges ------------------------------------------------------------------
 // H[i] becomes cum_before (nbin + 1 entries, the last is the row total).
+// Class-0 bin b holds every byte of its 256 ids (binsum) minus the bytes of
+// the ids this worker reads (Z).
 __global__ void __launch_bounds__(1024)
-plan_cut(PlanArgs a, uint64_t* __restrict__ H, int32_t* __restrict__ ranges) {
+plan_cut(PlanArgs a, const uint64_t* __restrict__ binsum, const uint64_t* __restrict__ Z,
+         uint64_t* __restrict__ H, int32_t* __restrict__ ranges) {
   __shared__ uint64_t tmp[65];
   const int64_t i = blockIdx.x;
   uint64_t* Hi = H + i * int64_t(a.nbin + 1);
+  const uint64_t* Zi = Z + i * int64_t(a.nb0);
   uint64_t carry = 0;
   for (uint32_t b0 = 0; b0 < a.nbin; b0 += 1024) {
     const uint32_t b = b0 + threadIdx.x;
-    const uint64_t v = b < a.nbin ? Hi[b] : 0ull;
+    uint64_t v = 0;
+    if (b < a.nbin1) v = Hi[b];
+    else if (b < a.nbin) v = binsum[b - a.nbin1] - Zi[b - a.nbin1];
     uint64_t total;
     const uint64_t ex = block_exclusive_scan64(v, tmp, &total);
     if (b < a.nbin) Hi[b] = carry + ex;
@@ -336,9 +378,9 @@ plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
   for (int64_t k = ks + threadIdx.x; k < rs.body0; k += kThreads) single(k);
   for (int64_t k = rs.tail0 + threadIdx.x; k < ke; k += kThreads) single(k);
   constexpr int kU = 4;
-  for (int64_t u0 = 0; u0 < rs.nunits; u0 += kU * kThreads) {
-    uint32_t cw[kU];
-    int4 fw[kU];
+  uint32_t cw[kU];
+  int4 fw[kU];
+  auto load = [&](int64_t u0) {
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
       const int64_t u = u0 + j * kThreads + threadIdx.x;
@@ -348,6 +390,18 @@ plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
         fw[j] = *reinterpret_cast<const int4*>(frow + k);
       }
     }
+  };
+  if (rs.nunits > 0) load(0);
+  for (int64_t u0 = 0; u0 < rs.nunits; u0 += kU * kThreads) {
+    uint32_t cc[kU];
+    int4 ff[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      cc[j] = cw[j];
+      ff[j] = fw[j];
+    }
+    // the next iteration's words are in flight while this one is classified
+    if (u0 + kU * kThreads < rs.nunits) load(u0 + kU * kThreads);
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
       const int64_t u = u0 + j * kThreads + threadIdx.x;
@@ -357,11 +411,11 @@ plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
       int tv[4] = {0, 0, 0, 0};
       int nc = 0;
       if (ok) {
-        const int32_t fv[4] = {fw[j].x, fw[j].y, fw[j].z, fw[j].w};
+        const int32_t fv[4] = {ff[j].x, ff[j].y, ff[j].z, ff[j].w};
         uint32_t packed = 0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          tv[q] = classify(k + q, (cw[j] >> (8 * q)) & 0xFFu, fv[q], &key[q]);
+          tv[q] = classify(k + q, (cc[j] >> (8 * q)) & 0xFFu, fv[q], &key[q]);
           nc += tv[q] == 256;
           packed |= uint32_t(uint8_t(int8_t(tv[q] == 256 ? 0 : tv[q]))) << (8 * q);
         }
@@ -609,12 +663,13 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
   for (int j = 0; j < 128; ++j) a.caps[j] = j < J ? caps[j] : 0;
 
   Scratch scr(st);
-  uint64_t *H, *binsum;
+  uint64_t *H, *binsum, *Z;
   int32_t *ranges, *ccount, *overflow;
   CandRec* cand;
   const int64_t hn = s.N * int64_t(a.nbin + 1);
   if ((rc = scr.alloc_n(&H, size_t(hn)))) return rc;
   if ((rc = scr.alloc_n(&binsum, size_t(a.nb0)))) return rc;
+  if ((rc = scr.alloc_n(&Z, size_t(s.N) * a.nb0))) return rc;
   if ((rc = scr.alloc_n(&ranges, size_t(s.N * 2 * J)))) return rc;
   if ((rc = scr.alloc_n(&ccount, size_t(s.N)))) return rc;
   if ((rc = scr.alloc_n(&overflow, size_t(s.N)))) return rc;
@@ -623,6 +678,10 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
   int64_t fb = ceil_div(hn, 1024);
   if (fb > 65536) fb = 65536;
   if ((rc = launch("fill_u64", fill_u64, dim3(uint32_t(fb)), dim3(256), 0, st, H, hn))) return rc;
+  const int64_t zn = s.N * int64_t(a.nb0);
+  int64_t zb = ceil_div(zn, 1024);
+  if (zb > 65536) zb = 65536;
+  if ((rc = launch("fill_u64", fill_u64, dim3(uint32_t(zb)), dim3(256), 0, st, Z, zn))) return rc;
   if ((rc = launch("fill_i32", fill_i32, dim3(uint32_t(ceil_div(s.N, 256))), dim3(256), 0, st, ccount,
                    s.N)))
     return rc;
@@ -635,13 +694,14 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
                    (reinterpret_cast<uintptr_t>(first) & 15) == 0;
   const uint32_t nslices = uint32_t(ceil_div(s.F, kSliceCells));
   const uint32_t ntiles = uint32_t(s.N) * nslices;
-  const size_t hsmem = size_t(a.nbin1 + kSliceBins0) * 8;
+  const size_t hsmem = size_t(a.nbin1) * 8;
   if ((rc = vec ? launch("plan_hist", plan_hist<true>, dim3(xcd_padded(ntiles)), dim3(kThreads), hsmem,
-                         st, a, count, first, sizes, (const uint64_t*)binsum, H, nslices)
+                         st, a, count, first, sizes, Z, H, nslices)
                 : launch("plan_hist", plan_hist<false>, dim3(xcd_padded(ntiles)), dim3(kThreads), hsmem,
-                         st, a, count, first, sizes, (const uint64_t*)binsum, H, nslices)))
+                         st, a, count, first, sizes, Z, H, nslices)))
     return rc;
-  if ((rc = launch("plan_cut", plan_cut, dim3(uint32_t(s.N)), dim3(1024), 0, st, a, H, ranges)))
+  if ((rc = launch("plan_cut", plan_cut, dim3(uint32_t(s.N)), dim3(1024), 0, st, a,
+                   (const uint64_t*)binsum, (const uint64_t*)Z, H, ranges)))
     return rc;
   if ((rc = vec ? launch("plan_write", plan_write<true>, dim3(xcd_padded(ntiles)), dim3(kThreads), 0,
                          st, a, count, first, (const int32_t*)ranges, tier, cand, ccount, nslices)

@@ -40,8 +40,15 @@ constexpr int kBlocksPerThread = 16;                                   // Philox
 constexpr int64_t kChunkIds = int64_t(kChunkThreads) * kBlocksPerThread * 4;  // 65536
 constexpr uint32_t kMaxBuckets = 8192;
 
-constexpr int kSortThreads = 1024;
-constexpr int kItems = 8;
+// Tuning knobs: bucket capacity = threads x items (identical results).
+#ifndef NOPFS_SORT_THREADS
+#define NOPFS_SORT_THREADS 1024
+#endif
+#ifndef NOPFS_SORT_ITEMS
+#define NOPFS_SORT_ITEMS 8
+#endif
+constexpr int kSortThreads = NOPFS_SORT_THREADS;
+constexpr int kItems = NOPFS_SORT_ITEMS;
 constexpr int kSortCap = kSortThreads * kItems;  // 8192 (key, id) pairs in LDS
 constexpr int kDigitBits = 11;
 constexpr int kDigits = 1 << kDigitBits;
