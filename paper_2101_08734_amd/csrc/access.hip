@@ -55,7 +55,6 @@ constexpr uint32_t kMaxWindows = 8192;  // sample windows per worker
 #define NOPFS_NEXT_WSMAX 13
 #endif
 
-constexpr int kThreads = 256;  // partition / unpartition workgroups
 constexpr int kStatsThreads = NOPFS_STATS_THREADS;
 constexpr int kNextThreads = NOPFS_NEXT_THREADS;
 static_assert(kNextThreads >= 64 && kNextThreads % 64 == 0, "next_tile block size");

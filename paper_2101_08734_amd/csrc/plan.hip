@@ -50,6 +50,17 @@ constexpr int kSliceBins0 = int(kSliceCells >> kClass0Shift);
 constexpr uint32_t kBins1Budget = 4096;   // bins for classes count >= 1
 constexpr int kCandMax = 4096;            // candidate records per worker (LDS sort)
 constexpr int kResolveThreads = 1024;
+// Tuning knobs of the histogram pass (every value gives identical results).
+#ifndef NOPFS_HIST_UNITS
+#define NOPFS_HIST_UNITS 4
+#endif
+#ifndef NOPFS_HIST_SIZES_AHEAD
+#define NOPFS_HIST_SIZES_AHEAD 1
+#endif
+constexpr int kHistU = NOPFS_HIST_UNITS;        // 4-cell units per thread per iteration
+constexpr bool kHistSizesAhead = NOPFS_HIST_SIZES_AHEAD != 0;
+
+typedef long long I64x2 __attribute__((ext_vector_type(2)));
 
 struct PlanArgs {
   int64_t F, N, M_max;
@@ -60,38 +71,42 @@ struct PlanArgs {
   int64_t caps[128];
 };
 
+// One 8-byte LDS record per count class: the bin scale and, packed, the
+// first bin of the class (high 16 bits) and its last bin offset (low 16).
 struct ClassTable {
-  uint32_t base[256];
-  uint32_t top[256];   // nbc[c] - 1
-  float scale[256];
+  float2 e[256];  // x = scale, y = bits of (base << 16 | top)
 };
 
 __device__ void build_class_table(const PlanArgs& a, ClassTable& t) {
   if (threadIdx.x == 0) {
     uint32_t b = 0;
     for (int c = a.E; c >= 1; --c) {
-      t.base[c] = b;
-      t.top[c] = a.nbc[c] - 1u;
-      t.scale[c] = float(a.nbc[c]) / float(a.M_max > 0 ? a.M_max : 1);
+      const float scale = float(a.nbc[c]) / float(a.M_max > 0 ? a.M_max : 1);
+      t.e[c] = make_float2(scale, __uint_as_float((b << 16) | (a.nbc[c] - 1u)));
       b += a.nbc[c];
     }
-    t.base[0] = b;
-    t.top[0] = 0;
-    t.scale[0] = 0.f;
+    t.e[0] = make_float2(0.f, __uint_as_float(b << 16));
+    // counts above E break the precondition; they bin like class E
+    for (int c = a.E + 1; c < 256; ++c) t.e[c] = t.e[a.E];
   }
   __syncthreads();
+}
+
+// Bin of a read cell (class c in [1, 255], first read f >= 0).
+__device__ __forceinline__ uint32_t bin_read(const ClassTable& t, uint32_t c, int32_t f) {
+  const float2 r = t.e[c];
+  const uint32_t bt = __float_as_uint(r.y);
+  // a negative f (not a first read) lands in the class's first bin
+  const uint32_t xi0 = uint32_t(fmaxf(float(f) * r.x, 0.f));
+  const uint32_t top = bt & 0xFFFFu;
+  return (bt >> 16) + (xi0 < top ? xi0 : top);
 }
 
 // Rank-ordered bin of a cell; identical in every kernel that uses it.
 __device__ __forceinline__ uint32_t bin_of(const PlanArgs& a, const ClassTable& t, uint32_t c,
                                            int32_t f, int64_t k) {
   if (c == 0) return a.nbin1 + uint32_t(k >> kClass0Shift);
-  if (c > uint32_t(a.E)) c = uint32_t(a.E);
-  float x = f > 0 ? float(f) * t.scale[c] : 0.f;
-  uint32_t xi = uint32_t(x);
-  const uint32_t top = t.top[c];
-  if (xi > top) xi = top;
-  return t.base[c] + xi;
+  return bin_read(t, c, f);
 }
 
 __device__ __forceinline__ uint64_t rank_key(const PlanArgs& a, uint32_t c, int32_t f, int64_t k) {
@@ -154,35 +169,43 @@ plan_hist(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restri
           const int64_t* __restrict__ sizes, uint64_t* __restrict__ Z,
           uint64_t* __restrict__ H, uint32_t nslices) {
   extern __shared__ uint64_t sm[];
-  uint64_t* h1 = sm;                 // nbin1 weighted bins
+  uint64_t* h1 = sm;                              // nbin1 weighted bins
+  unsigned long long* zs =                        // read bytes of this slice's class-0 bins
+      reinterpret_cast<unsigned long long*>(sm + a.nbin1);
   __shared__ ClassTable ct;
   const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
   if (t >= uint32_t(a.N) * nslices) return;
   const int64_t sl = t / a.N, i = t - sl * a.N;
   build_class_table(a, ct);
-  for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads) h1[b] = 0;
-  __syncthreads();
   const int64_t ks = sl * kSliceCells;
   const int64_t ke = ks + kSliceCells < a.F ? ks + kSliceCells : a.F;
+  const uint32_t zb0 = uint32_t(ks >> kClass0Shift);
+  const uint32_t nz = uint32_t((ke - ks + (1 << kClass0Shift) - 1) >> kClass0Shift);
+  for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads) h1[b] = 0;
+  for (uint32_t b = threadIdx.x; b < nz; b += kThreads) zs[b] = 0;
+  __syncthreads();
   const uint8_t* crow = count + i * a.F;
   const int32_t* frow = first + i * a.F;
-  unsigned long long* Zi = reinterpret_cast<unsigned long long*>(Z + i * int64_t(a.nb0));
   auto cell = [&](int64_t k, uint32_t c, int32_t f) {
     if (c != 0) {
       const unsigned long long sz = static_cast<unsigned long long>(sizes[k]);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_of(a, ct, c, f, k)]), sz);
-      atomicAdd(&Zi[k >> kClass0Shift], sz);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_read(ct, c, f)]), sz);
+      atomicAdd(&zs[uint32_t(k >> kClass0Shift) - zb0], sz);
     }
   };
   const RowSplit rs = split_row(i * a.F + ks, ks, ke, kVec);
   for (int64_t k = ks + threadIdx.x; k < rs.body0; k += kThreads) cell(k, crow[k], frow[k]);
   for (int64_t k = rs.tail0 + threadIdx.x; k < ke; k += kThreads) cell(k, crow[k], frow[k]);
-  // Body: 4 cells per lane, kU lanes' worth of units per thread per
-  // iteration. The next iteration's count and first words are requested
-  // before this one's sizes, so one memory round trip overlaps the other.
-  constexpr int kU = 4;
+  // Body: 4 cells per lane, kHistU units per thread per iteration. The next
+  // iteration's count, first and size words are requested before this
+  // iteration's are used, so their memory round trip overlaps the work.
+  // Sizes are fetched for every cell (two 16-byte loads per unit): a line of
+  // sizes almost always holds some read cell, and waiting for the counts
+  // before asking for sizes would put a second round trip on the path.
+  constexpr int kU = kHistU;
   uint32_t cw[kU];
   int4 fw[kU];
+  I64x2 sw[kU][2];
   auto load = [&](int64_t u0) {
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
@@ -192,6 +215,10 @@ plan_hist(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restri
       if (u < rs.nunits) {
         cw[j] = *reinterpret_cast<const uint32_t*>(crow + k);
         fw[j] = *reinterpret_cast<const int4*>(frow + k);
+        if (kHistSizesAhead) {
+          __builtin_memcpy(&sw[j][0], sizes + k, 16);
+          __builtin_memcpy(&sw[j][1], sizes + k + 2, 16);
+        }
       }
     }
   };
@@ -199,50 +226,55 @@ plan_hist(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restri
   for (int64_t u0 = 0; u0 < rs.nunits; u0 += kU * kThreads) {
     uint32_t c[kU];
     int4 f[kU];
+    uint64_t sz[kU][4];
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
       c[j] = cw[j];
       f[j] = fw[j];
+      if (kHistSizesAhead) {
+        sz[j][0] = uint64_t(sw[j][0].x);
+        sz[j][1] = uint64_t(sw[j][0].y);
+        sz[j][2] = uint64_t(sw[j][1].x);
+        sz[j][3] = uint64_t(sw[j][1].y);
+      }
     }
     if (u0 + kU * kThreads < rs.nunits) load(u0 + kU * kThreads);
-    uint64_t sz[kU][4];
+    if (!kHistSizesAhead) {
 #pragma unroll
-    for (int j = 0; j < kU; ++j) {
-      const int64_t k = rs.body0 + 4 * (u0 + j * kThreads + threadIdx.x);
+      for (int j = 0; j < kU; ++j) {
+        const int64_t k = rs.body0 + 4 * (u0 + j * kThreads + threadIdx.x);
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        sz[j][q] = ((c[j] >> (8 * q)) & 0xFFu) ? uint64_t(sizes[k + q]) : 0ull;
+        for (int q = 0; q < 4; ++q)
+          sz[j][q] = ((c[j] >> (8 * q)) & 0xFFu) ? uint64_t(sizes[k + q]) : 0ull;
+      }
     }
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
       const int64_t k = rs.body0 + 4 * (u0 + j * kThreads + threadIdx.x);
+      if (c[j] == 0) continue;
       const int32_t fv[4] = {f[j].x, f[j].y, f[j].z, f[j].w};
-      // bytes read, split at the class-0 bin boundary inside this wave's
-      // 256 consecutive cells, reduced over the wave
-      const int64_t kw = rs.body0 + 4 * (u0 + j * kThreads + (threadIdx.x & ~63u));
-      const int64_t kcut = ((kw >> kClass0Shift) + 1) << kClass0Shift;
+      // the unit's read bytes, split where its 4 cells cross into the
+      // next class-0 bin (at most once)
+      const uint32_t z = uint32_t(k >> kClass0Shift) - zb0;
+      const uint32_t qcut = uint32_t(((k >> kClass0Shift) + 1) << kClass0Shift) - uint32_t(k);
       uint64_t lo = 0, hi = 0;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const uint32_t cq = (c[j] >> (8 * q)) & 0xFFu;
         if (cq != 0) {
-          atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_of(a, ct, cq, fv[q], k + q)]),
+          atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_read(ct, cq, fv[q])]),
                     static_cast<unsigned long long>(sz[j][q]));
-          if (k + q < kcut) lo += sz[j][q]; else hi += sz[j][q];
+          if (uint32_t(q) < qcut) lo += sz[j][q]; else hi += sz[j][q];
         }
       }
-#pragma unroll
-      for (int d = 32; d >= 1; d >>= 1) {
-        lo += __shfl_xor(lo, d, 64);
-        hi += __shfl_xor(hi, d, 64);
-      }
-      if (__lane_id() == 0 && kw < ke) {
-        if (lo) atomicAdd(&Zi[kw >> kClass0Shift], static_cast<unsigned long long>(lo));
-        if (hi) atomicAdd(&Zi[kcut >> kClass0Shift], static_cast<unsigned long long>(hi));
-      }
+      if (lo) atomicAdd(&zs[z], static_cast<unsigned long long>(lo));
+      if (hi) atomicAdd(&zs[z + 1], static_cast<unsigned long long>(hi));
     }
   }
   __syncthreads();
+  // every class-0 bin lies in exactly one slice (slices are whole bins)
+  uint64_t* Zi = Z + i * int64_t(a.nb0) + zb0;
+  for (uint32_t b = threadIdx.x; b < nz; b += kThreads) Zi[b] = zs[b];
   uint64_t* Hi = H + i * int64_t(a.nbin + 1);
   for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads)
     if (h1[b]) atomicAdd(reinterpret_cast<unsigned long long*>(&Hi[b]),
@@ -678,10 +710,6 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
   int64_t fb = ceil_div(hn, 1024);
   if (fb > 65536) fb = 65536;
   if ((rc = launch("fill_u64", fill_u64, dim3(uint32_t(fb)), dim3(256), 0, st, H, hn))) return rc;
-  const int64_t zn = s.N * int64_t(a.nb0);
-  int64_t zb = ceil_div(zn, 1024);
-  if (zb > 65536) zb = 65536;
-  if ((rc = launch("fill_u64", fill_u64, dim3(uint32_t(zb)), dim3(256), 0, st, Z, zn))) return rc;
   if ((rc = launch("fill_i32", fill_i32, dim3(uint32_t(ceil_div(s.N, 256))), dim3(256), 0, st, ccount,
                    s.N)))
     return rc;
@@ -694,7 +722,7 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
                    (reinterpret_cast<uintptr_t>(first) & 15) == 0;
   const uint32_t nslices = uint32_t(ceil_div(s.F, kSliceCells));
   const uint32_t ntiles = uint32_t(s.N) * nslices;
-  const size_t hsmem = size_t(a.nbin1) * 8;
+  const size_t hsmem = (size_t(a.nbin1) + kSliceBins0) * 8;
   if ((rc = vec ? launch("plan_hist", plan_hist<true>, dim3(xcd_padded(ntiles)), dim3(kThreads), hsmem,
                          st, a, count, first, sizes, Z, H, nslices)
                 : launch("plan_hist", plan_hist<false>, dim3(xcd_padded(ntiles)), dim3(kThreads), hsmem,

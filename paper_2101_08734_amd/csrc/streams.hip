@@ -20,7 +20,8 @@
 //                        split into its nf fine buckets (skipped when nf = 1).
 //   6. stream_sort    -- one workgroup per fine bucket: counting sort in LDS
 //                        by the top 11 bits of the key inside the bucket,
-//                        each (tiny) group insertion-sorted by (key, id), and
+//                        each pair then placed inside its (tiny) digit group
+//                        by its rank in (key, id) order, and
 //                        the sorted positions p sharded straight into R:
 //                        R[p mod N][e*L_i + p div N], through an LDS
 //                        transpose so each worker row gets a run.
@@ -310,8 +311,7 @@ stream_split(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __res
 
 // -- 6. per-bucket sort and shard --------------------------------------------
 struct SortSmem {
-  uint32_t keys[kSortCap];
-  int32_t ids[kSortCap];
+  uint2 kv[kSortCap];  // (key, id) pairs; later the sorted ids and the shard stage
   uint32_t hist[kDigits];
   uint32_t tmp[65];
 };
@@ -425,32 +425,40 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
     }
   }
   __syncthreads();
+  uint32_t dst[kItems];
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
     if (q < n) {
-      const uint32_t dst = s.hist[k[r] >> dshift] + slot[r];
-      s.keys[dst] = k[r];
-      s.ids[dst] = id[r];
+      dst[r] = s.hist[k[r] >> dshift] + slot[r];
+      s.kv[dst[r]] = make_uint2(k[r], uint32_t(id[r]));
     }
   }
   __syncthreads();
-  // each digit group (a few pairs each) in (key, id) order
-  for (int d = threadIdx.x; d < kDigits; d += kSortThreads) {
-    const uint32_t a0 = s.hist[d];
-    const uint32_t a1 = d + 1 < kDigits ? s.hist[d + 1] : n;
-    for (uint32_t u = a0 + 1; u < a1; ++u) {
-      const uint32_t kv = s.keys[u];
-      const int32_t iv = s.ids[u];
-      uint32_t c = u;
-      while (c > a0 && pair_greater(s.keys[c - 1], s.ids[c - 1], kv, iv)) {
-        s.keys[c] = s.keys[c - 1];
-        s.ids[c] = s.ids[c - 1];
-        --c;
+  // Inside its digit group (a few pairs), every pair's final position is
+  // the group start plus the number of group pairs ordered before it by
+  // (key, id); the loads of one pair's scan do not depend on each other.
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
+    if (q < n) {
+      const uint32_t d = k[r] >> dshift;
+      const uint32_t a0 = s.hist[d];
+      const uint32_t a1 = d + 1 < uint32_t(kDigits) ? s.hist[d + 1] : n;
+      uint32_t rank = 0;
+      for (uint32_t v = a0; v < a1; ++v) {
+        const uint2 o = s.kv[v];
+        rank += pair_greater(k[r], id[r], o.x, int32_t(o.y));
       }
-      s.keys[c] = kv;
-      s.ids[c] = iv;
+      dst[r] = a0 + rank;
     }
+  }
+  __syncthreads();
+  int32_t* sorted = reinterpret_cast<int32_t*>(s.kv);  // ids in (key, id) order
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
+    if (q < n) sorted[dst[r]] = id[r];
   }
   __syncthreads();
 
@@ -464,9 +472,9 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
   const uint32_t step_i = kSortThreads % N, step_j = kSortThreads / N;
   uint32_t ci = (lo + threadIdx.x) % N, cj = (lo + threadIdx.x) / N;
   if (uint64_t(nj) * Np <= uint64_t(kSortCap)) {
-    uint32_t* stage = s.keys;
+    uint32_t* stage = reinterpret_cast<uint32_t*>(s.kv) + kSortCap;
     for (uint32_t q = threadIdx.x; lo + q < pend; q += kSortThreads) {
-      stage[(cj - j0) * Np + ci] = uint32_t(s.ids[q]);
+      stage[(cj - j0) * Np + ci] = uint32_t(sorted[q]);
       ci += step_i;
       cj += step_j;
       if (ci >= N) {
@@ -489,7 +497,7 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
     }
   } else {
     for (uint32_t q = threadIdx.x; lo + q < pend; q += kSortThreads) {
-      R[row_offset(p, ci, e) + cj] = s.ids[q];
+      R[row_offset(p, ci, e) + cj] = sorted[q];
       ci += step_i;
       cj += step_j;
       if (ci >= N) {
