@@ -260,12 +260,17 @@ __device__ __forceinline__ void for_each_read(const SegParams& p, int64_t i, uin
 }
 
 // -- stats --------------------------------------------------------------------
+// Every thread takes whole runs (one run = the window's reads inside one
+// sub-chunk, a few reads for uniform shuffles): it loads the run's bounds and
+// then up to kRunLoads of its reads at once, so a tile needs one dependent
+// pair of loads and no workgroup-wide scan before the LDS updates.
+constexpr int kRunLoads = 8;
+
 template <bool kVec>
 __global__ void __launch_bounds__(kStatsThreads)
 stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
            uint8_t* __restrict__ count, int32_t* __restrict__ first, uint32_t ntiles) {
   extern __shared__ uint32_t sm[];
-  __shared__ RunTable<kStatsThreads> rt;
   uint32_t* cw = sm;                                   // kStatsWin / 4 words of byte counters
   int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsWin / 4);
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
@@ -276,19 +281,45 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   const int64_t k0 = int64_t(kb) * W;
   const int64_t kend = k0 + W < p.F ? k0 + W : p.F;
   const uint32_t* prow = Pk + i * p.M_max;
+  const int64_t Li = seg_len(p, i);
+  const int64_t runs = int64_t(p.E) * p.nsc;
+  const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;  // run starts in window kb
+  const uint16_t* ob = oa + runs;                            // run ends
+  const uint32_t nsc = uint32_t(p.nsc);
   for (int64_t w0 = k0; w0 < kend; w0 += kStatsWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kStatsWin ? kend - w0 : kStatsWin);
+    const uint32_t xoff = uint32_t(w0 - k0);
+    // bounds of this thread's first run, requested before the LDS is cleared
+    uint32_t ra = 0, rb = 0;
+    if (threadIdx.x < runs) {
+      ra = oa[threadIdx.x];
+      rb = ob[threadIdx.x];
+    }
     for (uint32_t x = threadIdx.x; x < (wlen + 3) / 4; x += kStatsThreads) cw[x] = 0;
     for (uint32_t x = threadIdx.x; x < wlen; x += kStatsThreads) fi[x] = INT_MAX;
     __syncthreads();
-    const uint32_t xoff = uint32_t(w0 - k0);
-    for_each_read(p, i, kb, OT, prow, rt, 0, p.E, [&](int64_t, int64_t fbase, uint32_t v, uint32_t) {
-      const uint32_t x = (v >> kScShift) - xoff;
-      if (x < wlen) {
-        atomicAdd(&cw[x >> 2], 1u << ((x & 3u) * 8u));
-        atomicMin(&fi[x], int32_t(fbase + (v & kJMask)));
+    for (int64_t r = threadIdx.x; r < runs; r += kStatsThreads) {
+      if (r != threadIdx.x) {
+        ra = oa[r];
+        rb = ob[r];
       }
-    });
+      const uint32_t e = uint32_t(r) / nsc, sc = uint32_t(r) - e * nsc;
+      const int64_t fb = int64_t(e) * Li + int64_t(sc) * kSC;
+      const uint32_t* src = prow + fb;
+      for (uint32_t q = ra; q < rb; q += kRunLoads) {
+        uint32_t v[kRunLoads];
+#pragma unroll
+        for (int u = 0; u < kRunLoads; ++u) v[u] = q + u < rb ? src[q + u] : 0u;
+#pragma unroll
+        for (int u = 0; u < kRunLoads; ++u) {
+          const uint32_t x = (v[u] >> kScShift) - xoff;
+          if (q + u < rb && x < wlen) {
+            atomicAdd(&cw[x >> 2], 1u << ((x & 3u) * 8u));
+            atomicMin(&fi[x], int32_t(fb + (v[u] & kJMask)));
+          }
+        }
+      }
+    }
     __syncthreads();
     uint8_t* crow = count + i * p.F + w0;
     int32_t* frow = first + i * p.F + w0;
