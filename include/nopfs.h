@@ -133,6 +133,24 @@ int nopfs_tier_plan(const nopfs_job* job, const uint8_t* count,
                     const int64_t* caps, int32_t J, int8_t* tier,
                     int64_t* used, void* hip_stream);
 
+/* The whole planning path in one call: the shuffle seed expanded into every
+ * worker's streams (sections 2 and 4), access frequencies, first reads and
+ * next uses (section 3), and the tier placement (section 5.1), i.e. the
+ * preparation a worker does once before training starts.
+ * Outputs are exactly those of nopfs_access_streams, nopfs_access_stats,
+ * nopfs_reuse_next and nopfs_tier_plan called in that order with the same
+ * arguments (same layouts, same readings); every pointer is as documented
+ * there. R and next may be NULL when M_max == 0. Fewer passes over memory:
+ * the counting and next-use passes share their partition of R where they
+ * can, and the tier plan reads a compact list of the read cells produced by
+ * the counting pass (scratch of about 8 bytes per read, freed in stream
+ * order when the enqueued work ends).
+ * Errors: EINVAL, ERANGE, ENOMEM, EDEVICE, all detected before any launch
+ * except ENOMEM/EDEVICE from a later stage (outputs are then unspecified). */
+int nopfs_plan_job(const nopfs_job* job, const int64_t* sizes, const int64_t* caps,
+                   int32_t J, int32_t* R, uint8_t* count, int32_t* first, int32_t* next,
+                   int8_t* tier, int64_t* used, void* hip_stream);
+
 /* Static description of a status code. Never NULL. */
 const char* nopfs_strerror(int code);
 

@@ -28,7 +28,7 @@
 
 #include <new>
 
-#include "common.hpp"
+#include "pipeline.hpp"
 
 namespace nopfs {
 namespace {
@@ -40,10 +40,10 @@ constexpr uint32_t kMaxWindows = 8192;  // sample windows per worker
 // Tuning knobs (measured on MI355X; see the benchmark notes). Every value
 // gives identical results; only speed changes.
 #ifndef NOPFS_STATS_THREADS
-#define NOPFS_STATS_THREADS 512
+#define NOPFS_STATS_THREADS 256
 #endif
 #ifndef NOPFS_STATS_WS
-#define NOPFS_STATS_WS 13
+#define NOPFS_STATS_WS 12
 #endif
 #ifndef NOPFS_NEXT_THREADS
 #define NOPFS_NEXT_THREADS 256
@@ -59,6 +59,7 @@ constexpr int kStatsThreads = NOPFS_STATS_THREADS;
 constexpr int kNextThreads = NOPFS_NEXT_THREADS;
 static_assert(kNextThreads >= 64 && kNextThreads % 64 == 0, "next_tile block size");
 static_assert(kStatsThreads >= 64 && kStatsThreads % 64 == 0, "stats_tile block size");
+static_assert((1 << NOPFS_STATS_WS) % (4 * NOPFS_STATS_THREADS) == 0, "stats_tile window per thread");
 constexpr int kStatsWin = 1 << NOPFS_STATS_WS;  // samples held in LDS by stats_tile
 constexpr int kNextEnt = NOPFS_NEXT_ENT;   // reads per next_tile window (fast path)
 constexpr int kSlowWin = 8192;          // samples per pass of the epoch-serial path
@@ -266,11 +267,17 @@ __device__ __forceinline__ void for_each_read(const SegParams& p, int64_t i, uin
 // pair of loads and no workgroup-wide scan before the LDS updates.
 constexpr int kRunLoads = 8;
 
-template <bool kVec>
+// kCompact (fused planning call): the tile also lists its read cells for the
+// tier plan, entry {first, count << 24 | offset in window}, at the worker's
+// offset base = its reads in earlier windows (the sum of the run starts).
+template <bool kVec, bool kCompact>
 __global__ void __launch_bounds__(kStatsThreads)
 stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
-           uint8_t* __restrict__ count, int32_t* __restrict__ first, uint32_t ntiles) {
+           uint8_t* __restrict__ count, int32_t* __restrict__ first, uint32_t ntiles,
+           uint2* __restrict__ cent, int32_t* __restrict__ cbase, uint32_t* __restrict__ cnum) {
   extern __shared__ uint32_t sm[];
+  __shared__ uint32_t s_cnt, s_base;
+  __shared__ uint32_t s_tmp[65];
   uint32_t* cw = sm;                                   // kStatsWin / 4 words of byte counters
   int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsWin / 4);
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
@@ -286,6 +293,11 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;  // run starts in window kb
   const uint16_t* ob = oa + runs;                            // run ends
   const uint32_t nsc = uint32_t(p.nsc);
+  uint2* crow_ent = kCompact ? cent + i * p.M_max : nullptr;
+  if (kCompact && threadIdx.x == 0) {
+    s_cnt = 0;
+    s_base = 0;
+  }
   for (int64_t w0 = k0; w0 < kend; w0 += kStatsWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kStatsWin ? kend - w0 : kStatsWin);
     const uint32_t xoff = uint32_t(w0 - k0);
@@ -298,11 +310,13 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     for (uint32_t x = threadIdx.x; x < (wlen + 3) / 4; x += kStatsThreads) cw[x] = 0;
     for (uint32_t x = threadIdx.x; x < wlen; x += kStatsThreads) fi[x] = INT_MAX;
     __syncthreads();
+    uint32_t start_sum = 0;
     for (int64_t r = threadIdx.x; r < runs; r += kStatsThreads) {
       if (r != threadIdx.x) {
         ra = oa[r];
         rb = ob[r];
       }
+      start_sum += ra;
       const uint32_t e = uint32_t(r) / nsc, sc = uint32_t(r) - e * nsc;
       const int64_t fb = int64_t(e) * Li + int64_t(sc) * kSC;
       const uint32_t* src = prow + fb;
@@ -320,34 +334,86 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
         }
       }
     }
+    if (kCompact && w0 == k0) {
+#pragma unroll
+      for (int d = 32; d >= 1; d >>= 1) start_sum += __shfl_xor(start_sum, d, 64);
+      if (__lane_id() == 0 && start_sum) atomicAdd(&s_base, start_sum);
+    }
     __syncthreads();
     uint8_t* crow = count + i * p.F + w0;
     int32_t* frow = first + i * p.F + w0;
+    uint2* cdst = kCompact ? crow_ent + s_base : nullptr;
     auto cnt_at = [&](uint32_t x) { return (cw[x >> 2] >> ((x & 3u) * 8u)) & 0xFFu; };
+    auto single = [&](uint32_t x) {
+      const uint32_t c = cnt_at(x);
+      crow[x] = uint8_t(c);
+      frow[x] = c ? fi[x] : -1;
+      if (kCompact && c) cdst[atomicAdd(&s_cnt, 1u)] = make_uint2(uint32_t(fi[x]), (c << 24) | (xoff + x));
+    };
     // cells up to the first flat index divisible by 4 and after the last
     // group of 4 go one per thread; the rest as 4-cell groups per lane
     uint32_t head = kVec ? uint32_t((4 - ((i * p.F + w0) & 3)) & 3) : wlen;
     if (head > wlen) head = wlen;
     const uint32_t nunits = (wlen - head) >> 2;
     const uint32_t tail0 = head + 4 * nunits;
-    for (uint32_t x = threadIdx.x; x < head; x += kStatsThreads) {
-      const uint32_t c = cnt_at(x);
-      crow[x] = uint8_t(c);
-      frow[x] = c ? fi[x] : -1;
-    }
-    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kStatsThreads) {
-      const uint32_t c = cnt_at(x);
-      crow[x] = uint8_t(c);
-      frow[x] = c ? fi[x] : -1;
-    }
-    for (uint32_t u = threadIdx.x; u < nunits; u += kStatsThreads) {
+    for (uint32_t x = threadIdx.x; x < head; x += kStatsThreads) single(x);
+    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kStatsThreads) single(x);
+    // each thread keeps the first reads of its (at most kUnits) 4-cell
+    // groups, so the compact entries can be written once the first-read
+    // table is free (the count table stays intact)
+    constexpr int kUnits = kStatsWin / 4 / kStatsThreads;
+    int32_t fr[kUnits][4];
+    uint32_t nmine = 0;
+#pragma unroll
+    for (int m = 0; m < kUnits; ++m) {
+      const uint32_t u = threadIdx.x + uint32_t(m) * kStatsThreads;
       const uint32_t x = head + 4 * u;
-      const uint32_t c0 = cnt_at(x), c1 = cnt_at(x + 1), c2 = cnt_at(x + 2), c3 = cnt_at(x + 3);
-      *reinterpret_cast<uint32_t*>(crow + x) = c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
-      *reinterpret_cast<int4*>(frow + x) =
-          make_int4(c0 ? fi[x] : -1, c1 ? fi[x + 1] : -1, c2 ? fi[x + 2] : -1, c3 ? fi[x + 3] : -1);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) fr[m][q] = -1;
+      if (u < nunits) {
+        uint32_t cq[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          cq[q] = cnt_at(x + q);
+          if (cq[q]) fr[m][q] = fi[x + q];
+          nmine += cq[q] != 0;
+        }
+        *reinterpret_cast<uint32_t*>(crow + x) = cq[0] | (cq[1] << 8) | (cq[2] << 16) | (cq[3] << 24);
+        *reinterpret_cast<int4*>(frow + x) = make_int4(fr[m][0], fr[m][1], fr[m][2], fr[m][3]);
+      }
+    }
+    if (kCompact) {
+      // slots of this thread's entries; the scan's barriers also end every
+      // read of the LDS tables and every single cell's slot claim
+      uint32_t total;
+      uint32_t slot = block_exclusive_scan(nmine, s_tmp, &total);
+      const uint32_t run0 = s_cnt;  // entries already listed for this tile
+      // stage the entries in the (now free) first-read table, then write them
+      // out as one contiguous run; a run too long for the table goes direct
+      uint2* stage = reinterpret_cast<uint2*>(fi);
+      const bool staged = total <= uint32_t(kStatsWin / 2);
+#pragma unroll
+      for (int m = 0; m < kUnits; ++m) {
+        const uint32_t x = head + 4 * (threadIdx.x + uint32_t(m) * kStatsThreads);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (fr[m][q] >= 0) {
+            const uint2 ent = make_uint2(uint32_t(fr[m][q]), (cnt_at(x + q) << 24) | (xoff + x + q));
+            if (staged) stage[slot] = ent; else cdst[run0 + slot] = ent;
+            ++slot;
+          }
+        }
+      }
+      __syncthreads();
+      if (staged)
+        for (uint32_t t = threadIdx.x; t < total; t += kStatsThreads) cdst[run0 + t] = stage[t];
+      if (threadIdx.x == 0) s_cnt = run0 + total;
     }
     __syncthreads();
+  }
+  if (kCompact && threadIdx.x == 0) {
+    cbase[tile] = int32_t(s_base);
+    cnum[tile] = s_cnt;
   }
 }
 
@@ -564,6 +630,63 @@ int run_partition(const SegParams& p, const int32_t* R, Scratch& scr, uint32_t**
                 dim3(256), 0, st, p, (const uint16_t*)O, *OT);
 }
 
+int launch_stats(const SegParams& p, const uint32_t* Pk, const uint16_t* OT, uint8_t* count,
+                 int32_t* first, CompactCells* cc, hipStream_t st) {
+  const uint32_t ntiles = uint32_t(p.N * p.nbk);
+  const size_t smem = size_t(kStatsWin / 4 + kStatsWin) * 4;
+  // vector stores need 4-byte aligned count rows and 16-byte aligned first rows
+  const bool vec = (reinterpret_cast<uintptr_t>(count) & 3) == 0 &&
+                   (reinterpret_cast<uintptr_t>(first) & 15) == 0;
+  const dim3 grid(xcd_padded(ntiles)), block(kStatsThreads);
+  uint2* ent = cc ? cc->ent : nullptr;
+  int32_t* base = cc ? cc->base : nullptr;
+  uint32_t* num = cc ? cc->num : nullptr;
+  if (cc)
+    return vec ? launch("stats_tile", stats_tile<true, true>, grid, block, smem, st, p, Pk, OT, count,
+                        first, ntiles, ent, base, num)
+               : launch("stats_tile", stats_tile<false, true>, grid, block, smem, st, p, Pk, OT,
+                        count, first, ntiles, ent, base, num);
+  return vec ? launch("stats_tile", stats_tile<true, false>, grid, block, smem, st, p, Pk, OT, count,
+                      first, ntiles, ent, base, num)
+             : launch("stats_tile", stats_tile<false, false>, grid, block, smem, st, p, Pk, OT, count,
+                      first, ntiles, ent, base, num);
+}
+
+// Window width of the next-use pass: about three quarters of the fast-path
+// capacity of reads per window.
+int next_ws(const Shape& s) {
+  const double reads_per_sample = double(s.M_max) / double(s.F);
+  int ws = 0;
+  while (ws < NOPFS_NEXT_WSMAX && double(int64_t(1) << (ws + 1)) * reads_per_sample <= kNextEnt * 3 / 4)
+    ++ws;
+  return ws;
+}
+
+SegParams next_params(const Shape& s) {
+  SegParams p = seg_params(s, next_ws(s));
+  if (debug_value(2) > 0 && debug_value(2) < kNextEnt) p.ent_cap = int32_t(debug_value(2));
+  return p;
+}
+
+// nextP: scratch laid out like the partitioned reads (N * M_max int32).
+int launch_next(const SegParams& p, const uint32_t* Pk, const uint16_t* OT, int32_t* nextP,
+                int32_t* next, hipStream_t st) {
+  int rc;
+  const uint32_t ntiles = uint32_t(p.N * p.nbk);
+  size_t smem = sizeof(NextSmem);
+  if (smem < size_t(kSlowWin) * 4) smem = size_t(kSlowWin) * 4;
+  if ((rc = launch("next_tile", next_tile, dim3(xcd_padded(ntiles)), dim3(kNextThreads), smem, st, p,
+                   Pk, OT, nextP, ntiles)))
+    return rc;
+  const int64_t wgs = p.N * p.E * p.nsc;
+  if ((rc = launch("next_unpartition", next_unpartition, dim3(uint32_t(wgs)), dim3(kUnpartThreads), 0,
+                   st, p, Pk, (const int32_t*)nextP, next)))
+    return rc;
+  if (!p.drop_last && p.F % p.N != 0)
+    if ((rc = launch("pad_rows", pad_rows, dim3(uint32_t(p.N)), dim3(64), 0, st, p, next))) return rc;
+  return NOPFS_OK;
+}
+
 }  // namespace
 
 int stats_impl(const nopfs_job* job, const int32_t* R, uint8_t* count, int32_t* first,
@@ -585,16 +708,7 @@ int stats_impl(const nopfs_job* job, const int32_t* R, uint8_t* count, int32_t* 
   uint32_t* Pk;
   uint16_t* OT;
   if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
-  const uint32_t ntiles = uint32_t(s.N * p.nbk);
-  const size_t smem = size_t(kStatsWin / 4 + kStatsWin) * 4;
-  // vector stores need 4-byte aligned count rows and 16-byte aligned first rows
-  const bool vec = (reinterpret_cast<uintptr_t>(count) & 3) == 0 &&
-                   (reinterpret_cast<uintptr_t>(first) & 15) == 0;
-  if (vec)
-    return launch("stats_tile", stats_tile<true>, dim3(xcd_padded(ntiles)), dim3(kStatsThreads), smem,
-                  st, p, (const uint32_t*)Pk, (const uint16_t*)OT, count, first, ntiles);
-  return launch("stats_tile", stats_tile<false>, dim3(xcd_padded(ntiles)), dim3(kStatsThreads), smem,
-                st, p, (const uint32_t*)Pk, (const uint16_t*)OT, count, first, ntiles);
+  return launch_stats(p, Pk, OT, count, first, nullptr, st);
 }
 
 int next_impl(const nopfs_job* job, const int32_t* R, int32_t* next, hipStream_t st) {
@@ -603,33 +717,42 @@ int next_impl(const nopfs_job* job, const int32_t* R, int32_t* next, hipStream_t
   if (rc) return rc;
   if (s.M_max == 0) return NOPFS_OK;  // R and next have no elements and may be NULL
   if (!R || !next) return fail(NOPFS_EINVAL, "R and next must be non-NULL");
-  // window width: about three quarters of the fast-path capacity of reads
-  const double reads_per_sample = double(s.M_max) / double(s.F);
-  int ws = 0;
-  while (ws < NOPFS_NEXT_WSMAX && double(int64_t(1) << (ws + 1)) * reads_per_sample <= kNextEnt * 3 / 4)
-    ++ws;
-  SegParams p = seg_params(s, ws);
-  if (debug_value(2) > 0 && debug_value(2) < kNextEnt) p.ent_cap = int32_t(debug_value(2));
+  const SegParams p = next_params(s);
   Scratch scr(st);
   uint32_t* Pk;
   uint16_t* OT;
   int32_t* nextP;
   if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
   if ((rc = scr.alloc_n(&nextP, size_t(s.N * s.M_max)))) return rc;
-  const uint32_t ntiles = uint32_t(s.N * p.nbk);
-  size_t smem = sizeof(NextSmem);
-  if (smem < size_t(kSlowWin) * 4) smem = size_t(kSlowWin) * 4;
-  if ((rc = launch("next_tile", next_tile, dim3(xcd_padded(ntiles)), dim3(kNextThreads), smem, st, p,
-                   (const uint32_t*)Pk, (const uint16_t*)OT, nextP, ntiles)))
-    return rc;
-  const int64_t wgs = s.N * s.E * p.nsc;
-  if ((rc = launch("next_unpartition", next_unpartition, dim3(uint32_t(wgs)), dim3(kUnpartThreads), 0,
-                   st, p,
-                   (const uint32_t*)Pk, (const int32_t*)nextP, next)))
-    return rc;
-  if (!s.drop_last && s.F % s.N != 0)
-    if ((rc = launch("pad_rows", pad_rows, dim3(uint32_t(s.N)), dim3(64), 0, st, p, next))) return rc;
-  return NOPFS_OK;
+  return launch_next(p, Pk, OT, nextP, next, st);
+}
+
+int access_fused(const Shape& s, const int32_t* R, uint8_t* count, int32_t* first,
+                 int32_t* next, CompactCells* cc, Scratch& keep, SideWork& side,
+                 hipStream_t side_st, hipStream_t st) {
+  int rc;
+  const SegParams ps = seg_params(s, NOPFS_STATS_WS);
+  const SegParams pn = next_params(s);
+  uint32_t *Pk, *Pn;
+  uint16_t *OT, *OTn;
+  int32_t* nextP;
+  if ((rc = run_partition(ps, R, keep, &Pk, &OT, st))) return rc;
+  // the next-use pass shares the partition when it uses the same windows
+  Pn = Pk;
+  OTn = OT;
+  if (pn.ws != ps.ws)
+    if ((rc = run_partition(pn, R, keep, &Pn, &OTn, st))) return rc;
+  cc->ws = ps.ws;
+  cc->nbk = ps.nbk;
+  if ((rc = keep.alloc_n(&cc->ent, size_t(s.N * s.M_max)))) return rc;
+  if ((rc = keep.alloc_n(&cc->base, size_t(s.N) * ps.nbk))) return rc;
+  if ((rc = keep.alloc_n(&cc->num, size_t(s.N) * ps.nbk))) return rc;
+  if ((rc = keep.alloc_n(&nextP, size_t(s.N * s.M_max)))) return rc;
+  // next uses (read-heavy, latency-bound) run beside the counting pass and
+  // the tier plan (write-heavy), which they do not feed
+  if ((rc = side.begin())) return rc;
+  if ((rc = launch_next(pn, Pn, OTn, nextP, next, side_st))) return rc;
+  return launch_stats(ps, Pk, OT, count, first, cc, st);
 }
 
 }  // namespace nopfs

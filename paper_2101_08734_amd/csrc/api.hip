@@ -52,6 +52,36 @@ static int64_t g_debug[4] = {0, 0, 0, 0};
 
 int64_t debug_value(int which) { return (which >= 0 && which < 4) ? g_debug[which] : 0; }
 
+int side_stream(hipStream_t* s) {
+  static std::mutex mu;
+  static hipStream_t streams[64] = {};
+  int dev = 0;
+  NOPFS_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(NOPFS_EDEVICE, "device index out of range");
+  std::lock_guard<std::mutex> g(mu);
+  if (!streams[dev]) NOPFS_HIP(hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking));
+  *s = streams[dev];
+  return NOPFS_OK;
+}
+
+int SideWork::begin() {
+  NOPFS_HIP(hipEventCreateWithFlags(&ev_[0], hipEventDisableTiming));
+  NOPFS_HIP(hipEventCreateWithFlags(&ev_[1], hipEventDisableTiming));
+  NOPFS_HIP(hipEventRecord(ev_[0], main_));
+  active_ = true;  // from here on the destructor joins
+  NOPFS_HIP(hipStreamWaitEvent(side_, ev_[0], 0));
+  return NOPFS_OK;
+}
+
+SideWork::~SideWork() {
+  if (active_) {
+    (void)hipEventRecord(ev_[1], side_);
+    (void)hipStreamWaitEvent(main_, ev_[1], 0);
+  }
+  for (hipEvent_t e : ev_)
+    if (e) (void)hipEventDestroy(e);
+}
+
 bool take_alloc_failure() {
   if (g_debug[3]) {
     g_debug[3] = 0;

@@ -38,7 +38,7 @@
 #include <new>
 #include <vector>
 
-#include "common.hpp"
+#include "pipeline.hpp"
 
 namespace nopfs {
 namespace {
@@ -89,6 +89,15 @@ __device__ void build_class_table(const PlanArgs& a, ClassTable& t) {
     // counts above E break the precondition; they bin like class E
     for (int c = a.E + 1; c < 256; ++c) t.e[c] = t.e[a.E];
   }
+  __syncthreads();
+}
+
+// The same table computed once into global memory, and its copy into LDS
+// (for kernels with many small workgroups).
+__global__ void plan_classes(PlanArgs a, ClassTable* g) { build_class_table(a, *g); }
+
+__device__ void load_class_table(const ClassTable* __restrict__ g, ClassTable& t) {
+  for (int c = threadIdx.x; c < 256; c += blockDim.x) t.e[c] = g->e[c];
   __syncthreads();
 }
 
@@ -639,6 +648,190 @@ plan_exact(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
   }
 }
 
+// -- passes over the compact read-cell list (fused planning call) -----------------
+// The counting pass lists, per (worker, window of 2^ws samples), the cells the
+// worker reads: {first read, count << 24 | offset in window}. Cells missing
+// from the list are unread (class 0).
+struct CompactArgs {
+  const uint2* ent;
+  const int32_t* base;
+  const uint32_t* num;
+  int32_t ws;
+  uint32_t nbk;
+  uint32_t wps;  // windows per slice of kSliceCells samples
+};
+constexpr uint32_t kOffMask = (1u << 24) - 1;
+constexpr int kHistCU = 4;  // entries per lane in flight
+
+// Histogram of one (worker, slice): each wave takes whole windows of the
+// slice; class-0 read bytes and class >= 1 bins as in plan_hist.
+__global__ void __launch_bounds__(kThreads)
+plan_hist_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
+            const int64_t* __restrict__ sizes, uint64_t* __restrict__ Z, uint64_t* __restrict__ H,
+            uint32_t nslices) {
+  extern __shared__ uint64_t sm[];
+  uint64_t* h1 = sm;
+  unsigned long long* zs = reinterpret_cast<unsigned long long*>(sm + a.nbin1);
+  __shared__ ClassTable ct;
+  const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
+  if (t >= uint32_t(a.N) * nslices) return;
+  const int64_t sl = t / a.N, i = t - sl * a.N;
+  const int64_t ks = sl * kSliceCells;
+  const int64_t ke = ks + kSliceCells < a.F ? ks + kSliceCells : a.F;
+  const uint32_t zb0 = uint32_t(ks >> kClass0Shift);
+  const uint32_t nz = uint32_t((ke - ks + (1 << kClass0Shift) - 1) >> kClass0Shift);
+  for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads) h1[b] = 0;
+  for (uint32_t b = threadIdx.x; b < nz; b += kThreads) zs[b] = 0;
+  load_class_table(gct, ct);
+  const uint32_t kb0 = uint32_t(sl) * c.wps;
+  const uint32_t kb1 = kb0 + c.wps < c.nbk ? kb0 + c.wps : c.nbk;
+  const uint32_t lane = __lane_id();
+  for (uint32_t kb = kb0 + (threadIdx.x >> 6); kb < kb1; kb += kThreads / 64) {
+    const int64_t tix = i * int64_t(c.nbk) + kb;
+    const uint32_t n = c.num[tix];
+    const uint2* e = c.ent + i * a.M_max + c.base[tix];
+    const int64_t kw = int64_t(kb) << c.ws;
+    for (uint32_t t0 = 0; t0 < n; t0 += 64 * kHistCU) {
+      uint2 v[kHistCU];
+#pragma unroll
+      for (int u = 0; u < kHistCU; ++u) {
+        const uint32_t q = t0 + u * 64 + lane;
+        v[u] = q < n ? e[q] : make_uint2(0u, 0u);
+      }
+      uint64_t sz[kHistCU];
+#pragma unroll
+      for (int u = 0; u < kHistCU; ++u)
+        sz[u] = t0 + u * 64 + lane < n ? uint64_t(sizes[kw + (v[u].y & kOffMask)]) : 0ull;
+#pragma unroll
+      for (int u = 0; u < kHistCU; ++u) {
+        if (t0 + u * 64 + lane < n) {
+          const int64_t k = kw + (v[u].y & kOffMask);
+          atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_read(ct, v[u].y >> 24, int32_t(v[u].x))]),
+                    static_cast<unsigned long long>(sz[u]));
+          atomicAdd(&zs[uint32_t(k >> kClass0Shift) - zb0], static_cast<unsigned long long>(sz[u]));
+        }
+      }
+    }
+  }
+  __syncthreads();
+  uint64_t* Zi = Z + i * int64_t(a.nb0) + zb0;
+  for (uint32_t b = threadIdx.x; b < nz; b += kThreads) Zi[b] = zs[b];
+  uint64_t* Hi = H + i * int64_t(a.nbin + 1);
+  for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads)
+    if (h1[b]) atomicAdd(reinterpret_cast<unsigned long long*>(&Hi[b]),
+                         static_cast<unsigned long long>(h1[b]));
+}
+
+// Tier (or the candidate mark) of every bin of every worker, from the cut ranges.
+constexpr int8_t kCandMark = 127;
+
+__global__ void __launch_bounds__(256)
+plan_btier(PlanArgs a, const int32_t* __restrict__ ranges, int8_t* __restrict__ btier) {
+  const int64_t i = blockIdx.y;
+  const int32_t b = int32_t(blockIdx.x) * 256 + int32_t(threadIdx.x);
+  if (b >= int32_t(a.nbin)) return;
+  const int32_t* rg = ranges + i * 2 * a.J;
+  bool cand = false;
+  int tv = 0;
+  for (int j = 0; j < a.J; ++j) {
+    const int32_t lo = rg[2 * j], hi = rg[2 * j + 1];
+    cand |= b >= lo && b <= hi;
+    tv += hi < b;
+  }
+  btier[i * a.nbin + b] = cand ? kCandMark : (tv >= a.J ? int8_t(-1) : int8_t(tv));
+}
+
+// Tier row of one (worker, window): every cell starts with its class-0 bin's
+// tier, the listed read cells take their own bin's, and the cells of
+// candidate bins are appended to the worker's candidate list as in plan_write.
+constexpr int kWriteThreads = 256;
+constexpr int kWriteWin = 8192;  // cells held in LDS at once
+
+template <bool kVec>
+__global__ void __launch_bounds__(kWriteThreads)
+plan_write_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
+             const int8_t* __restrict__ btier, int8_t* __restrict__ tier,
+             CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t ntiles) {
+  __shared__ ClassTable ct;
+  __shared__ int8_t tb[kWriteWin];
+  __shared__ int8_t t0[kWriteWin / (1 << kClass0Shift) + 1];
+  __shared__ int s_c0cand;
+  const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
+  if (tile >= ntiles) return;
+  const int64_t i = tile / c.nbk;
+  const uint32_t kb = tile - uint32_t(i) * c.nbk;
+  load_class_table(gct, ct);
+  const int8_t* bt = btier + i * int64_t(a.nbin);
+  const int64_t k0 = int64_t(kb) << c.ws;
+  const int64_t kend = k0 + (int64_t(1) << c.ws) < a.F ? k0 + (int64_t(1) << c.ws) : a.F;
+  const int64_t tix = i * int64_t(c.nbk) + kb;
+  const uint32_t n = c.num[tix];
+  const uint2* ent = c.ent + i * a.M_max + c.base[tix];
+  CandRec* ci = cand + i * int64_t(a.cmax);
+  int8_t* trow = tier + i * a.F;
+  auto append = [&](uint64_t key, int64_t k) {
+    const int32_t slot = atomicAdd(&ccount[i], 1);
+    if (slot < a.cmax) ci[slot] = CandRec{key, uint32_t(k), 0u};
+  };
+  for (int64_t w0 = k0; w0 < kend; w0 += kWriteWin) {
+    const uint32_t wlen = uint32_t(kend - w0 < kWriteWin ? kend - w0 : kWriteWin);
+    const uint32_t xoff = uint32_t(w0 - k0);
+    const uint32_t zb0 = uint32_t(w0 >> kClass0Shift);
+    const uint32_t nzb = uint32_t((w0 + wlen - 1) >> kClass0Shift) - zb0 + 1;
+    if (threadIdx.x == 0) s_c0cand = 0;
+    __syncthreads();
+    for (uint32_t z = threadIdx.x; z < nzb; z += kWriteThreads) {
+      const int8_t v = bt[a.nbin1 + zb0 + z];
+      t0[z] = v;
+      if (v == kCandMark) s_c0cand = 1;
+    }
+    __syncthreads();
+    for (uint32_t x = threadIdx.x; x < wlen; x += kWriteThreads)
+      tb[x] = t0[((w0 + x) >> kClass0Shift) - zb0];
+    __syncthreads();
+    for (uint32_t q = threadIdx.x; q < n; q += kWriteThreads) {
+      const uint2 v = ent[q];
+      const uint32_t x = (v.y & kOffMask) - xoff;
+      if (x < wlen) {
+        const uint32_t b = bin_read(ct, v.y >> 24, int32_t(v.x));
+        const int8_t tv = bt[b];
+        if (tv == kCandMark) {
+          append((uint64_t(b) << 32) | uint64_t(v.x), w0 + x);
+          tb[x] = 0;
+        } else {
+          tb[x] = tv;
+        }
+      }
+    }
+    __syncthreads();
+    if (s_c0cand) {
+      // unread cells of candidate class-0 bins (read ones were overwritten)
+      for (uint32_t x = threadIdx.x; x < wlen; x += kWriteThreads) {
+        if (tb[x] == kCandMark) {
+          const int64_t k = w0 + x;
+          append((uint64_t(a.nbin1 + uint32_t(k >> kClass0Shift)) << 32) | uint64_t(k), k);
+          tb[x] = 0;
+        }
+      }
+      __syncthreads();
+    }
+    int8_t* dst = trow + w0;
+    uint32_t head = kVec ? uint32_t((4 - ((i * a.F + w0) & 3)) & 3) : wlen;
+    if (head > wlen) head = wlen;
+    const uint32_t nunits = (wlen - head) >> 2;
+    const uint32_t tail0 = head + 4 * nunits;
+    for (uint32_t x = threadIdx.x; x < head; x += kWriteThreads) dst[x] = tb[x];
+    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kWriteThreads) dst[x] = tb[x];
+    for (uint32_t u = threadIdx.x; u < nunits; u += kWriteThreads) {
+      const uint32_t x = head + 4 * u;
+      const uint32_t w = uint32_t(uint8_t(tb[x])) | (uint32_t(uint8_t(tb[x + 1])) << 8) |
+                         (uint32_t(uint8_t(tb[x + 2])) << 16) | (uint32_t(uint8_t(tb[x + 3])) << 24);
+      *reinterpret_cast<uint32_t*>(dst + x) = w;
+    }
+    __syncthreads();
+  }
+}
+
 // Bins per class c >= 1, in proportion to the expected number of cells of
 // class c (a worker reads a sample in each epoch with probability L/F, so
 // counts follow Binomial(E, L/F)); at least one bin per class.
@@ -666,7 +859,72 @@ void class_bins(int64_t F, int64_t E, int64_t L, uint16_t* nbc, uint32_t* nbin1)
   *nbin1 = total;
 }
 
+struct PlanBufs {
+  uint64_t *H, *binsum, *Z;
+  int32_t *ranges, *ccount, *overflow;
+  CandRec* cand;
+};
+
+void plan_args(const Shape& s, const int64_t* caps, int32_t J, PlanArgs* a) {
+  a->F = s.F;
+  a->N = s.N;
+  a->M_max = s.M_max;
+  a->E = int32_t(s.E);
+  a->J = J;
+  class_bins(s.F, s.E, s.L, a->nbc, &a->nbin1);
+  a->nb0 = uint32_t(ceil_div(s.F, int64_t(1) << kClass0Shift));
+  a->nbin = a->nbin1 + a->nb0;
+  a->cmax = kCandMax;
+  if (debug_value(2) > 0 && debug_value(2) < kCandMax) a->cmax = int32_t(debug_value(2));
+  for (int j = 0; j < 128; ++j) a->caps[j] = j < J ? caps[j] : 0;
+}
+
+// Scratch of both plan paths, the zeroed histogram and candidate counters,
+// and the per-bin byte totals of the sizes.
+int plan_begin(const Shape& s, const PlanArgs& a, const int64_t* sizes, Scratch& scr,
+               PlanBufs* b, hipStream_t st) {
+  int rc;
+  const int64_t hn = s.N * int64_t(a.nbin + 1);
+  if ((rc = scr.alloc_n(&b->H, size_t(hn)))) return rc;
+  if ((rc = scr.alloc_n(&b->binsum, size_t(a.nb0)))) return rc;
+  if ((rc = scr.alloc_n(&b->Z, size_t(s.N) * a.nb0))) return rc;
+  if ((rc = scr.alloc_n(&b->ranges, size_t(s.N * 2 * a.J)))) return rc;
+  if ((rc = scr.alloc_n(&b->ccount, size_t(s.N)))) return rc;
+  if ((rc = scr.alloc_n(&b->overflow, size_t(s.N)))) return rc;
+  if ((rc = scr.alloc_n(&b->cand, size_t(s.N * a.cmax)))) return rc;
+  int64_t fb = ceil_div(hn, 1024);
+  if (fb > 65536) fb = 65536;
+  if ((rc = launch("fill_u64", fill_u64, dim3(uint32_t(fb)), dim3(256), 0, st, b->H, hn))) return rc;
+  if ((rc = launch("fill_i32", fill_i32, dim3(uint32_t(ceil_div(s.N, 256))), dim3(256), 0, st,
+                   b->ccount, s.N)))
+    return rc;
+  return launch("plan_binsum", plan_binsum, dim3(uint32_t(ceil_div(a.nb0, 4))), dim3(256), 0, st,
+                s.F, a.nb0, sizes, b->binsum);
+}
+
+// Exact resolution of the candidates, and the full-row fallback for workers
+// whose candidate list overflowed.
+int plan_end(const Shape& s, const PlanArgs& a, const PlanBufs& b, const uint8_t* count,
+             const int32_t* first, const int64_t* sizes, int8_t* tier, int64_t* used,
+             hipStream_t st) {
+  int rc;
+  if ((rc = launch("plan_resolve", plan_resolve, dim3(uint32_t(s.N)), dim3(kResolveThreads), 0, st,
+                   a, (const uint64_t*)b.H, (const CandRec*)b.cand, (const int32_t*)b.ccount, sizes,
+                   tier, used, b.overflow)))
+    return rc;
+  return launch("plan_exact", plan_exact, dim3(uint32_t(s.N)), dim3(1024), 0, st, a, count, first,
+                sizes, (const int32_t*)b.overflow, tier, used);
+}
+
 }  // namespace
+
+int plan_check(const int64_t* caps, int32_t J) {
+  if (J < 1) return fail(NOPFS_EINVAL, "J must be >= 1");
+  if (J > 127) return fail(NOPFS_ERANGE, "J must be <= 127");
+  for (int j = 0; j < J; ++j)
+    if (caps[j] < 0) return fail(NOPFS_EINVAL, "capacities must be >= 0");
+  return NOPFS_OK;
+}
 
 int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
               const int64_t* sizes, const int64_t* caps, int32_t J, int8_t* tier, int64_t* used,
@@ -676,46 +934,12 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
   if (rc) return rc;
   if (!count || !first || !sizes || !caps || !tier || !used)
     return fail(NOPFS_EINVAL, "count, first, sizes, caps, tier and used must be non-NULL");
-  if (J < 1) return fail(NOPFS_EINVAL, "J must be >= 1");
-  if (J > 127) return fail(NOPFS_ERANGE, "J must be <= 127");
-  for (int j = 0; j < J; ++j)
-    if (caps[j] < 0) return fail(NOPFS_EINVAL, "capacities must be >= 0");
-
+  if ((rc = plan_check(caps, J))) return rc;
   PlanArgs a;
-  a.F = s.F;
-  a.N = s.N;
-  a.M_max = s.M_max;
-  a.E = int32_t(s.E);
-  a.J = J;
-  class_bins(s.F, s.E, s.L, a.nbc, &a.nbin1);
-  a.nb0 = uint32_t(ceil_div(s.F, int64_t(1) << kClass0Shift));
-  a.nbin = a.nbin1 + a.nb0;
-  a.cmax = kCandMax;
-  if (debug_value(2) > 0 && debug_value(2) < kCandMax) a.cmax = int32_t(debug_value(2));
-  for (int j = 0; j < 128; ++j) a.caps[j] = j < J ? caps[j] : 0;
-
+  plan_args(s, caps, J, &a);
   Scratch scr(st);
-  uint64_t *H, *binsum, *Z;
-  int32_t *ranges, *ccount, *overflow;
-  CandRec* cand;
-  const int64_t hn = s.N * int64_t(a.nbin + 1);
-  if ((rc = scr.alloc_n(&H, size_t(hn)))) return rc;
-  if ((rc = scr.alloc_n(&binsum, size_t(a.nb0)))) return rc;
-  if ((rc = scr.alloc_n(&Z, size_t(s.N) * a.nb0))) return rc;
-  if ((rc = scr.alloc_n(&ranges, size_t(s.N * 2 * J)))) return rc;
-  if ((rc = scr.alloc_n(&ccount, size_t(s.N)))) return rc;
-  if ((rc = scr.alloc_n(&overflow, size_t(s.N)))) return rc;
-  if ((rc = scr.alloc_n(&cand, size_t(s.N * a.cmax)))) return rc;
-
-  int64_t fb = ceil_div(hn, 1024);
-  if (fb > 65536) fb = 65536;
-  if ((rc = launch("fill_u64", fill_u64, dim3(uint32_t(fb)), dim3(256), 0, st, H, hn))) return rc;
-  if ((rc = launch("fill_i32", fill_i32, dim3(uint32_t(ceil_div(s.N, 256))), dim3(256), 0, st, ccount,
-                   s.N)))
-    return rc;
-  if ((rc = launch("plan_binsum", plan_binsum, dim3(uint32_t(ceil_div(a.nb0, 4))), dim3(256), 0, st,
-                   s.F, a.nb0, sizes, binsum)))
-    return rc;
+  PlanBufs b;
+  if ((rc = plan_begin(s, a, sizes, scr, &b, st))) return rc;
   // vector loads need 4-byte aligned count/tier rows and 16-byte aligned first rows
   const bool vec = (reinterpret_cast<uintptr_t>(count) & 3) == 0 &&
                    (reinterpret_cast<uintptr_t>(tier) & 3) == 0 &&
@@ -724,26 +948,62 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
   const uint32_t ntiles = uint32_t(s.N) * nslices;
   const size_t hsmem = (size_t(a.nbin1) + kSliceBins0) * 8;
   if ((rc = vec ? launch("plan_hist", plan_hist<true>, dim3(xcd_padded(ntiles)), dim3(kThreads), hsmem,
-                         st, a, count, first, sizes, Z, H, nslices)
+                         st, a, count, first, sizes, b.Z, b.H, nslices)
                 : launch("plan_hist", plan_hist<false>, dim3(xcd_padded(ntiles)), dim3(kThreads), hsmem,
-                         st, a, count, first, sizes, Z, H, nslices)))
+                         st, a, count, first, sizes, b.Z, b.H, nslices)))
     return rc;
   if ((rc = launch("plan_cut", plan_cut, dim3(uint32_t(s.N)), dim3(1024), 0, st, a,
-                   (const uint64_t*)binsum, (const uint64_t*)Z, H, ranges)))
+                   (const uint64_t*)b.binsum, (const uint64_t*)b.Z, b.H, b.ranges)))
     return rc;
   if ((rc = vec ? launch("plan_write", plan_write<true>, dim3(xcd_padded(ntiles)), dim3(kThreads), 0,
-                         st, a, count, first, (const int32_t*)ranges, tier, cand, ccount, nslices)
+                         st, a, count, first, (const int32_t*)b.ranges, tier, b.cand, b.ccount, nslices)
                 : launch("plan_write", plan_write<false>, dim3(xcd_padded(ntiles)), dim3(kThreads), 0,
-                         st, a, count, first, (const int32_t*)ranges, tier, cand, ccount, nslices)))
+                         st, a, count, first, (const int32_t*)b.ranges, tier, b.cand, b.ccount,
+                         nslices)))
     return rc;
-  if ((rc = launch("plan_resolve", plan_resolve, dim3(uint32_t(s.N)), dim3(kResolveThreads), 0, st,
-                   a, (const uint64_t*)H, (const CandRec*)cand, (const int32_t*)ccount, sizes, tier,
-                   used, overflow)))
+  return plan_end(s, a, b, count, first, sizes, tier, used, st);
+}
+
+int plan_compact(const Shape& s, const CompactCells& cc, const uint8_t* count,
+                 const int32_t* first, const int64_t* sizes, const int64_t* caps, int32_t J,
+                 int8_t* tier, int64_t* used, hipStream_t st) {
+  int rc;
+  if ((rc = plan_check(caps, J))) return rc;
+  if (cc.ws > 19) return fail(NOPFS_EDEVICE, "sample windows wider than a histogram slice");
+  PlanArgs a;
+  plan_args(s, caps, J, &a);
+  Scratch scr(st);
+  PlanBufs b;
+  if ((rc = plan_begin(s, a, sizes, scr, &b, st))) return rc;
+  ClassTable* gct;
+  int8_t* btier;
+  if ((rc = scr.alloc_n(&gct, 1))) return rc;
+  if ((rc = scr.alloc_n(&btier, size_t(s.N) * a.nbin))) return rc;
+  if ((rc = launch("plan_classes", plan_classes, dim3(1), dim3(64), 0, st, a, gct))) return rc;
+  const CompactArgs c{cc.ent, cc.base, cc.num, cc.ws, cc.nbk,
+                      uint32_t(kSliceCells >> cc.ws)};
+  const uint32_t nslices = uint32_t(ceil_div(s.F, kSliceCells));
+  const uint32_t nht = uint32_t(s.N) * nslices;
+  const size_t hsmem = (size_t(a.nbin1) + kSliceBins0) * 8;
+  if ((rc = launch("plan_hist", plan_hist_c, dim3(xcd_padded(nht)), dim3(kThreads), hsmem, st, a, c,
+                   (const ClassTable*)gct, sizes, b.Z, b.H, nslices)))
     return rc;
-  if ((rc = launch("plan_exact", plan_exact, dim3(uint32_t(s.N)), dim3(1024), 0, st, a, count, first,
-                   sizes, (const int32_t*)overflow, tier, used)))
+  if ((rc = launch("plan_cut", plan_cut, dim3(uint32_t(s.N)), dim3(1024), 0, st, a,
+                   (const uint64_t*)b.binsum, (const uint64_t*)b.Z, b.H, b.ranges)))
     return rc;
-  return NOPFS_OK;
+  if ((rc = launch("plan_btier", plan_btier, dim3(uint32_t(ceil_div(a.nbin, 256)), uint32_t(s.N)),
+                   dim3(256), 0, st, a, (const int32_t*)b.ranges, btier)))
+    return rc;
+  const uint32_t ntiles = uint32_t(s.N) * cc.nbk;
+  const bool vec = (reinterpret_cast<uintptr_t>(tier) & 3) == 0;
+  if ((rc = vec ? launch("plan_write", plan_write_c<true>, dim3(xcd_padded(ntiles)),
+                         dim3(kWriteThreads), 0, st, a, c, (const ClassTable*)gct,
+                         (const int8_t*)btier, tier, b.cand, b.ccount, ntiles)
+                : launch("plan_write", plan_write_c<false>, dim3(xcd_padded(ntiles)),
+                         dim3(kWriteThreads), 0, st, a, c, (const ClassTable*)gct,
+                         (const int8_t*)btier, tier, b.cand, b.ccount, ntiles)))
+    return rc;
+  return plan_end(s, a, b, count, first, sizes, tier, used, st);
 }
 
 }  // namespace nopfs

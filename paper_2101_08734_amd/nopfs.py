@@ -67,6 +67,7 @@ def lib() -> ctypes.CDLL:
             "nopfs_access_stats": [jp, P, P, P, P],
             "nopfs_reuse_next": [jp, P, P, P],
             "nopfs_tier_plan": [jp, P, P, P, P, I32, P, P, P],
+            "nopfs_plan_job": [jp, P, P, I32, P, P, P, P, P, P, P],
             "nopfs_profile_enable": [ctypes.c_int],
             "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
                                     ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)],
@@ -86,7 +87,7 @@ def lib() -> ctypes.CDLL:
 
 
 EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_stats",
-            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_strerror",
+            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_strerror",
             "nopfs_last_error", "nopfs_profile_enable", "nopfs_profile_query",
             "nopfs_calibration_copy", "nopfs_debug_set")
 
@@ -188,6 +189,29 @@ def tier_plan(job: Job, count, first, sizes, caps, tier=None, used=None, stream=
                                  ctypes.cast(caps_host, ctypes.c_void_p), J, _ptr(tier),
                                  _ptr(used), _stream(stream)), "nopfs_tier_plan")
     return tier, used
+
+
+def plan_job(job: Job, sizes, caps, out=None, stream=None):
+    """The whole path in one library call (nopfs_plan_job); the same outputs
+    as plan(). `out` may hold preallocated R, count, first, next, tier, used."""
+    _, M, _ = stream_shape(job)
+    _device_tensor(sizes, torch.int64, (job.F,), "sizes")
+    caps_list = [int(c) for c in caps]
+    J = len(caps_list)
+    caps_host = (ctypes.c_int64 * max(J, 1))(*caps_list)
+    shapes = dict(R=((job.N, M), torch.int32), count=((job.N, job.F), torch.uint8),
+                  first=((job.N, job.F), torch.int32), next=((job.N, M), torch.int32),
+                  tier=((job.N, job.F), torch.int8), used=((job.N, max(J, 1)), torch.int64))
+    o = dict(out or {})
+    for name, (shape, dt) in shapes.items():
+        if o.get(name) is None:
+            o[name] = torch.empty(shape, dtype=dt, device="cuda")
+        _device_tensor(o[name], dt, shape, name)
+    j = job.c()
+    _check(lib().nopfs_plan_job(ctypes.byref(j), _ptr(sizes), ctypes.cast(caps_host, ctypes.c_void_p),
+                                J, _ptr(o["R"]), _ptr(o["count"]), _ptr(o["first"]), _ptr(o["next"]),
+                                _ptr(o["tier"]), _ptr(o["used"]), _stream(stream)), "nopfs_plan_job")
+    return o
 
 
 def plan(job: Job, sizes, caps, stream=None):

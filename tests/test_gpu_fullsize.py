@@ -33,10 +33,14 @@ def _gpu():
     torch.cuda.empty_cache()
 
 
-def run(w):
+PATHS = ["staged", "fused"]  # four stage calls, or nopfs_plan_job (the benchmarked call)
+
+
+def run(w, path="fused"):
     job = nopfs.Job(*w.job_tuple())
     sizes = wl.sizes(w)
-    out = nopfs.plan(job, torch.from_numpy(sizes).cuda(), wl.caps(w))
+    s = torch.from_numpy(sizes).cuda()
+    out = nopfs.plan(job, s, wl.caps(w)) if path == "staged" else nopfs.plan_job(job, s, wl.caps(w))
     torch.cuda.synchronize()
     return job, sizes, out
 
@@ -84,12 +88,18 @@ def check_plan_rows(job, sizes, caps, out, rows):
     inv.check_plan(c, f, sizes, caps, t, u)
 
 
-def test_imagenet1k_full(oracle):
+@pytest.fixture(scope="module")
+def imagenet1k_expected(oracle):
     w = wl.WORKLOADS["imagenet1k"]
-    job, sizes, out = run(w)
-    exp = oracle.full_pipeline(oracle.make_job(*w.job_tuple()), sizes, wl.caps(w))
+    return oracle.full_pipeline(oracle.make_job(*w.job_tuple()), wl.sizes(w), wl.caps(w))
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_imagenet1k_full(imagenet1k_expected, path):
+    w = wl.WORKLOADS["imagenet1k"]
+    job, sizes, out = run(w, path)
     for n in ("R", "count", "first", "next", "tier", "used"):
-        np.testing.assert_array_equal(out[n].cpu().numpy(), exp[n], err_msg=n)
+        np.testing.assert_array_equal(out[n].cpu().numpy(), imagenet1k_expected[n], err_msg=n)
 
 
 @pytest.mark.parametrize("name", ["imagenet1k_256", "cosmoflow"])
@@ -110,9 +120,10 @@ def test_full_streams_stats_next_and_plan_rows(oracle, name):
     check_plan_rows(job, sizes, wl.caps(w), out, np.arange(1, w.N, w.N // 4))
 
 
-def test_imagenet22k_sampled(oracle):
+@pytest.mark.parametrize("path", PATHS)
+def test_imagenet22k_sampled(oracle, path):
     w = wl.WORKLOADS["imagenet22k"]
-    job, sizes, out = run(w)
+    job, sizes, out = run(w, path)
     check_sampled(oracle, w, job, out, n_samples=16)
     check_device_properties(job, out)
     check_plan_rows(job, sizes, wl.caps(w), out, [0, 131, 255])

@@ -26,8 +26,12 @@ def _gpu():
         nopfs.debug_set(which, 0)
 
 
-def gpu_pipeline(job, sizes, caps):
-    out = nopfs.plan(job, torch.from_numpy(sizes).cuda(), caps)
+PATHS = ["staged", "fused"]  # four stage calls, or nopfs_plan_job
+
+
+def gpu_pipeline(job, sizes, caps, path="staged"):
+    s = torch.from_numpy(sizes).cuda()
+    out = nopfs.plan(job, s, caps) if path == "staged" else nopfs.plan_job(job, s, caps)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in out.items()}
 
@@ -63,8 +67,9 @@ def _caps(sizes, fracs):
     return np.array([int(f * tot) for f in fracs], np.int64)
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("name,F,E,N,B,d,seed,fr", JOBS, ids=[j[0] for j in JOBS])
-def test_pipeline_matches_oracle(oracle, name, F, E, N, B, d, seed, fr):
+def test_pipeline_matches_oracle(oracle, name, F, E, N, B, d, seed, fr, path):
     if name == "small":
         w = wl.WORKLOADS["small"]
         sizes, caps = wl.sizes(w), wl.caps(w)
@@ -72,7 +77,7 @@ def test_pipeline_matches_oracle(oracle, name, F, E, N, B, d, seed, fr):
         sizes = wl.random_sizes(F, seed, 1_000, 2_000_000)
         caps = _caps(sizes, fr)
     job = nopfs.Job(F, E, N, B, d, seed)
-    got = gpu_pipeline(job, sizes, caps)
+    got = gpu_pipeline(job, sizes, caps, path)
     exp = oracle.full_pipeline(oracle.make_job(F, E, N, B, d, seed), sizes, caps)
     compare(got, exp)
 
@@ -98,12 +103,13 @@ def test_stage_isolation(oracle):
 
 @pytest.mark.parametrize("caps", [[0], [1], [10**15], [0, 0, 10**15], [5_000_000, 0, 7],
                                   [2_000_000] * 7])
-def test_plan_capacity_edges(oracle, caps):
+@pytest.mark.parametrize("path", PATHS)
+def test_plan_capacity_edges(oracle, caps, path):
     F, E, N, B, d, seed = 5_000, 4, 3, 8, 1, 31
     sizes = wl.random_sizes(F, seed, 1_000, 2_000_000)
     caps = np.array(caps, np.int64)
     job = nopfs.Job(F, E, N, B, d, seed)
-    got = gpu_pipeline(job, sizes, caps)
+    got = gpu_pipeline(job, sizes, caps, path)
     exp = oracle.full_pipeline(oracle.make_job(F, E, N, B, d, seed), sizes, caps)
     compare(got, exp)
     if caps.max() == 0:
@@ -112,19 +118,21 @@ def test_plan_capacity_edges(oracle, caps):
         assert (got["tier"] == 0).all()
 
 
-def test_equal_sizes_tie_breaks(oracle):
+@pytest.mark.parametrize("path", PATHS)
+def test_equal_sizes_tie_breaks(oracle, path):
     """All sizes equal (CosmoFlow-like): the cut positions are decided by the
     (count, first, id) tie-breaks alone."""
     F, E, N, B, d, seed = 8_192, 10, 64, 1, 1, 42
     sizes = np.full(F, 16_777_216, np.int64)
     caps = np.array([16_777_216 * 37, 16_777_216 * 500], np.int64)
     job = nopfs.Job(F, E, N, B, d, seed)
-    got = gpu_pipeline(job, sizes, caps)
+    got = gpu_pipeline(job, sizes, caps, path)
     exp = oracle.full_pipeline(oracle.make_job(F, E, N, B, d, seed), sizes, caps)
     compare(got, exp)
 
 
-def test_slow_paths(oracle):
+@pytest.mark.parametrize("path", PATHS)
+def test_slow_paths(oracle, path):
     """Force the oversized-bucket sort, the epoch-serial next-use path and the
     exact plan fallback with the test hooks; results must not change."""
     F, E, N, B, d, seed = 20_000, 6, 4, 8, 0, 41
@@ -135,20 +143,42 @@ def test_slow_paths(oracle):
     try:
         nopfs.debug_set(1, 64)   # tiny LDS bucket capacity: most buckets overflow
         nopfs.debug_set(2, 8)    # tiny candidate / next-use capacities
-        got = gpu_pipeline(job, sizes, caps)
+        got = gpu_pipeline(job, sizes, caps, path)
     finally:
         nopfs.debug_set(1, 0)
         nopfs.debug_set(2, 0)
     compare(got, exp)
 
 
-def test_deterministic():
+@pytest.mark.parametrize("path", PATHS)
+def test_deterministic(path):
     F, E, N, B, d, seed = 100_000, 5, 16, 8, 1, 5
     sizes = wl.random_sizes(F, seed)
     job = nopfs.Job(F, E, N, B, d, seed)
-    a = gpu_pipeline(job, sizes, [10**9, 10**10])
-    b = gpu_pipeline(job, sizes, [10**9, 10**10])
+    a = gpu_pipeline(job, sizes, [10**9, 10**10], path)
+    b = gpu_pipeline(job, sizes, [10**9, 10**10], path)
     compare(a, b)
+
+
+WIDE = (34_000_000, 1, 1, 4, 0, 51)  # F, E, N, B, drop_last, seed
+
+
+@pytest.fixture(scope="module")
+def wide_case(oracle):
+    F, E, N, B, d, seed = WIDE
+    sizes = wl.random_sizes(F, seed, 1_000, 2_000_000)
+    caps = _caps(sizes, (0.1, 0.3))
+    return sizes, caps, oracle.full_pipeline(oracle.make_job(*WIDE), sizes, caps)
+
+
+@pytest.mark.parametrize("path", PATHS)
+def test_wide_windows(wide_case, path):
+    """F above 4096 * 8192: sample windows wider than the counting pass holds
+    in LDS at once (several passes per tile), and more reads per window than
+    the next-use fast path takes (the epoch-serial path)."""
+    sizes, caps, exp = wide_case
+    got = gpu_pipeline(nopfs.Job(*WIDE), sizes, caps, path)
+    compare(got, exp)
 
 
 def test_invariants_medium():
