@@ -19,7 +19,10 @@
  *  - `hip_stream` is a hipStream_t (NULL = the null stream). GPU calls only
  *    enqueue work on it and return; the caller keeps the buffers alive until
  *    the stream has completed. Internal scratch is allocated and freed in
- *    stream order on the same stream.
+ *    stream order on the same stream, from the device's default
+ *    stream-ordered memory pool; on first use the library raises that pool's
+ *    release threshold so freed scratch stays mapped for the next call (use
+ *    hipDeviceGetDefaultMemPool / hipMemPoolTrimTo to give it back).
  *  - Return 0 on success, a negative NOPFS_E* code otherwise. Argument errors
  *    are detected on the host before anything is enqueued. No C++ exception
  *    crosses this boundary. nopfs_last_error() gives a thread-local detail.
@@ -185,6 +188,7 @@ int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes,
  *   which=2  candidate records per worker in the tier plan's fast path, and
  *            reads per window in the next-use fast path
  *   which=3  fail the next internal scratch allocation (value 1)
+ *   which=4  run all of nopfs_plan_job on the caller's stream (value 1)
  * Not thread-safe; meant for tests only. */
 int nopfs_debug_set(int which, int64_t value);
 

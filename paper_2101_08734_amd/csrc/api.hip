@@ -48,9 +48,9 @@ int make_shape(const nopfs_job* job, Shape* s) {
 }
 
 // ---------------------------------------------------------------- scratch --
-static int64_t g_debug[4] = {0, 0, 0, 0};
+static int64_t g_debug[5] = {0, 0, 0, 0, 0};
 
-int64_t debug_value(int which) { return (which >= 0 && which < 4) ? g_debug[which] : 0; }
+int64_t debug_value(int which) { return (which >= 0 && which < 5) ? g_debug[which] : 0; }
 
 int side_stream(hipStream_t* s) {
   static std::mutex mu;
@@ -65,6 +65,7 @@ int side_stream(hipStream_t* s) {
 }
 
 int SideWork::begin() {
+  if (main_ == side_) return NOPFS_OK;  // one stream: already in order
   NOPFS_HIP(hipEventCreateWithFlags(&ev_[0], hipEventDisableTiming));
   NOPFS_HIP(hipEventCreateWithFlags(&ev_[1], hipEventDisableTiming));
   NOPFS_HIP(hipEventRecord(ev_[0], main_));
@@ -94,8 +95,33 @@ Scratch::~Scratch() {
   for (int i = n_ - 1; i >= 0; --i) (void)hipFreeAsync(ptrs_[i], stream_);
 }
 
+// The default stream-ordered pool returns freed memory to the system at
+// every synchronisation (release threshold 0), so the next call would map
+// its scratch again (milliseconds to hundreds of milliseconds for gigabytes,
+// with the host blocked). Once per device the threshold is raised so freed
+// scratch stays mapped for reuse.
+static void keep_pool_mapped() {
+  static std::mutex mu;
+  static bool done[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return;
+  }
+  std::lock_guard<std::mutex> g(mu);
+  if (done[dev]) return;
+  done[dev] = true;
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+    uint64_t keep = UINT64_MAX;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+  }
+  (void)hipGetLastError();
+}
+
 int Scratch::alloc(void** p, size_t bytes) {
   *p = nullptr;
+  keep_pool_mapped();
   if (n_ >= 32) return fail(NOPFS_ENOMEM, "too many scratch buffers");
   if (take_alloc_failure()) return fail(NOPFS_ENOMEM, "scratch allocation failed (test hook)");
   bytes = (bytes + 255) & ~size_t(255);
@@ -248,7 +274,7 @@ int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes, void* hip_
 }
 
 int nopfs_debug_set(int which, int64_t value) {
-  if (which < 1 || which > 3 || value < 0) return NOPFS_EINVAL;
+  if (which < 1 || which > 4 || value < 0) return NOPFS_EINVAL;
   g_debug[which] = value;
   return NOPFS_OK;
 }

@@ -28,8 +28,9 @@ int plan_job_impl(const nopfs_job* job, const int64_t* sizes, const int64_t* cap
     if ((rc = stats_impl(job, R, count, first, st))) return rc;
     return plan_impl(job, count, first, sizes, caps, J, tier, used, st);
   }
-  hipStream_t side_st;
-  if ((rc = side_stream(&side_st))) return rc;
+  hipStream_t side_st = st;  // test hook 4: everything on the caller's stream
+  if (debug_value(4) == 0)
+    if ((rc = side_stream(&side_st))) return rc;
   Scratch keep(st);
   SideWork side(st, side_st);  // joins before `keep` frees its buffers
   CompactCells cc;

@@ -66,6 +66,7 @@ struct PlanArgs {
   int64_t F, N, M_max;
   int32_t E, J;
   uint32_t nbin1, nb0, nbin;
+  uint32_t btp;  // row pitch of the per-bin tier table (nbin rounded up to 16)
   int32_t cmax;
   uint16_t nbc[256];   // bins of class c (1 <= c <= E)
   int64_t caps[128];
@@ -661,10 +662,17 @@ struct CompactArgs {
   uint32_t wps;  // windows per slice of kSliceCells samples
 };
 constexpr uint32_t kOffMask = (1u << 24) - 1;
-constexpr int kHistCU = 4;  // entries per lane in flight
+#ifndef NOPFS_HIST_CU
+#define NOPFS_HIST_CU 4
+#endif
+constexpr int kHistCU = NOPFS_HIST_CU;  // list entries per lane in flight
 
 // Histogram of one (worker, slice): each wave takes whole windows of the
-// slice; class-0 read bytes and class >= 1 bins as in plan_hist.
+// slice; class-0 read bytes and class >= 1 bins as in plan_hist. The list
+// bounds of up to kHistWins windows are staged in LDS at once, and a wave
+// requests the next window's entries before waiting for this window's sizes.
+constexpr uint32_t kHistWins = 1024;
+
 __global__ void __launch_bounds__(kThreads)
 plan_hist_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
             const int64_t* __restrict__ sizes, uint64_t* __restrict__ Z, uint64_t* __restrict__ H,
@@ -673,6 +681,8 @@ plan_hist_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
   uint64_t* h1 = sm;
   unsigned long long* zs = reinterpret_cast<unsigned long long*>(sm + a.nbin1);
   __shared__ ClassTable ct;
+  __shared__ uint32_t wnum[kHistWins];
+  __shared__ int32_t wbase[kHistWins];
   const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
   if (t >= uint32_t(a.N) * nslices) return;
   const int64_t sl = t / a.N, i = t - sl * a.N;
@@ -685,35 +695,67 @@ plan_hist_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
   load_class_table(gct, ct);
   const uint32_t kb0 = uint32_t(sl) * c.wps;
   const uint32_t kb1 = kb0 + c.wps < c.nbk ? kb0 + c.wps : c.nbk;
-  const uint32_t lane = __lane_id();
-  for (uint32_t kb = kb0 + (threadIdx.x >> 6); kb < kb1; kb += kThreads / 64) {
-    const int64_t tix = i * int64_t(c.nbk) + kb;
-    const uint32_t n = c.num[tix];
-    const uint2* e = c.ent + i * a.M_max + c.base[tix];
-    const int64_t kw = int64_t(kb) << c.ws;
-    for (uint32_t t0 = 0; t0 < n; t0 += 64 * kHistCU) {
-      uint2 v[kHistCU];
+  const uint32_t lane = __lane_id(), wave = threadIdx.x >> 6;
+  constexpr uint32_t kWaves = kThreads / 64;
+  const uint2* erow = c.ent + i * a.M_max;
+  for (uint32_t g0 = kb0; g0 < kb1; g0 += kHistWins) {
+    const uint32_t g1 = g0 + kHistWins < kb1 ? g0 + kHistWins : kb1;
+    for (uint32_t kb = g0 + threadIdx.x; kb < g1; kb += kThreads) {
+      wnum[kb - g0] = c.num[i * int64_t(c.nbk) + kb];
+      wbase[kb - g0] = c.base[i * int64_t(c.nbk) + kb];
+    }
+    __syncthreads();
+    uint2 v[kHistCU];
+    auto fetch = [&](uint32_t kb) {
+      const uint32_t n = kb < g1 ? wnum[kb - g0] : 0u;
+      const uint2* e = erow + (kb < g1 ? wbase[kb - g0] : 0);
 #pragma unroll
       for (int u = 0; u < kHistCU; ++u) {
-        const uint32_t q = t0 + u * 64 + lane;
+        const uint32_t q = u * 64 + lane;
         v[u] = q < n ? e[q] : make_uint2(0u, 0u);
       }
+    };
+    auto add = [&](uint2 e, uint64_t sz, int64_t kw) {
+      const int64_t k = kw + (e.y & kOffMask);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_read(ct, e.y >> 24, int32_t(e.x))]),
+                static_cast<unsigned long long>(sz));
+      atomicAdd(&zs[uint32_t(k >> kClass0Shift) - zb0], static_cast<unsigned long long>(sz));
+    };
+    fetch(g0 + wave);
+    for (uint32_t kb = g0 + wave; kb < g1; kb += kWaves) {
+      const uint32_t n = wnum[kb - g0];
+      const uint2* e = erow + wbase[kb - g0];
+      const int64_t kw = int64_t(kb) << c.ws;
+      uint2 cur[kHistCU];
+#pragma unroll
+      for (int u = 0; u < kHistCU; ++u) cur[u] = v[u];
+      fetch(kb + kWaves);  // next window's first entries
       uint64_t sz[kHistCU];
 #pragma unroll
       for (int u = 0; u < kHistCU; ++u)
-        sz[u] = t0 + u * 64 + lane < n ? uint64_t(sizes[kw + (v[u].y & kOffMask)]) : 0ull;
+        sz[u] = u * 64 + lane < n ? uint64_t(sizes[kw + (cur[u].y & kOffMask)]) : 0ull;
 #pragma unroll
-      for (int u = 0; u < kHistCU; ++u) {
-        if (t0 + u * 64 + lane < n) {
-          const int64_t k = kw + (v[u].y & kOffMask);
-          atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_read(ct, v[u].y >> 24, int32_t(v[u].x))]),
-                    static_cast<unsigned long long>(sz[u]));
-          atomicAdd(&zs[uint32_t(k >> kClass0Shift) - zb0], static_cast<unsigned long long>(sz[u]));
+      for (int u = 0; u < kHistCU; ++u)
+        if (u * 64 + lane < n) add(cur[u], sz[u], kw);
+      // entries beyond the prefetched ones
+      for (uint32_t q0 = kHistCU * 64; q0 < n; q0 += kHistCU * 64) {
+        uint2 w[kHistCU];
+#pragma unroll
+        for (int u = 0; u < kHistCU; ++u) {
+          const uint32_t q = q0 + u * 64 + lane;
+          w[u] = q < n ? e[q] : make_uint2(0u, 0u);
         }
+        uint64_t wz[kHistCU];
+#pragma unroll
+        for (int u = 0; u < kHistCU; ++u)
+          wz[u] = q0 + u * 64 + lane < n ? uint64_t(sizes[kw + (w[u].y & kOffMask)]) : 0ull;
+#pragma unroll
+        for (int u = 0; u < kHistCU; ++u)
+          if (q0 + u * 64 + lane < n) add(w[u], wz[u], kw);
       }
     }
+    __syncthreads();
   }
-  __syncthreads();
   uint64_t* Zi = Z + i * int64_t(a.nb0) + zb0;
   for (uint32_t b = threadIdx.x; b < nz; b += kThreads) Zi[b] = zs[b];
   uint64_t* Hi = H + i * int64_t(a.nbin + 1);
@@ -738,14 +780,19 @@ plan_btier(PlanArgs a, const int32_t* __restrict__ ranges, int8_t* __restrict__ 
     cand |= b >= lo && b <= hi;
     tv += hi < b;
   }
-  btier[i * a.nbin + b] = cand ? kCandMark : (tv >= a.J ? int8_t(-1) : int8_t(tv));
+  btier[i * a.btp + b] = cand ? kCandMark : (tv >= a.J ? int8_t(-1) : int8_t(tv));
 }
 
 // Tier row of one (worker, window): every cell starts with its class-0 bin's
 // tier, the listed read cells take their own bin's, and the cells of
 // candidate bins are appended to the worker's candidate list as in plan_write.
+// All loads a tile needs go out in two rounds: the class table, the bin
+// tiers of classes >= 1 (into LDS), the tile's list bounds and class-0 tiers,
+// then the list entries.
 constexpr int kWriteThreads = 256;
 constexpr int kWriteWin = 8192;  // cells held in LDS at once
+constexpr int kWriteEnt = 4;     // list entries per thread loaded up front
+constexpr uint32_t kBt1Max = ((kBins1Budget + 256 + 15) / 16) * 16;  // class >= 1 bins, padded
 
 template <bool kVec>
 __global__ void __launch_bounds__(kWriteThreads)
@@ -753,6 +800,7 @@ plan_write_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
              const int8_t* __restrict__ btier, int8_t* __restrict__ tier,
              CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t ntiles) {
   __shared__ ClassTable ct;
+  __shared__ __align__(16) int8_t bt1[kBt1Max];
   __shared__ int8_t tb[kWriteWin];
   __shared__ int8_t t0[kWriteWin / (1 << kClass0Shift) + 1];
   __shared__ int s_c0cand;
@@ -760,18 +808,53 @@ plan_write_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
   if (tile >= ntiles) return;
   const int64_t i = tile / c.nbk;
   const uint32_t kb = tile - uint32_t(i) * c.nbk;
-  load_class_table(gct, ct);
-  const int8_t* bt = btier + i * int64_t(a.nbin);
+  const int8_t* bt = btier + i * int64_t(a.btp);  // 16-byte aligned rows
   const int64_t k0 = int64_t(kb) << c.ws;
   const int64_t kend = k0 + (int64_t(1) << c.ws) < a.F ? k0 + (int64_t(1) << c.ws) : a.F;
   const int64_t tix = i * int64_t(c.nbk) + kb;
+  // round one: tables, list bounds, class-0 tiers of the first piece
+  const float2 cte = gct->e[threadIdx.x];  // 256 classes, one per thread
+  const uint32_t nb1w = (a.nbin1 + 15) / 16;
+  uint4 btw[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t w = threadIdx.x + uint32_t(h) * kWriteThreads;
+    btw[h] = make_uint4(0, 0, 0, 0);
+    if (w < nb1w) btw[h] = *reinterpret_cast<const uint4*>(bt + 16 * w);  // inside the padded row
+  }
   const uint32_t n = c.num[tix];
   const uint2* ent = c.ent + i * a.M_max + c.base[tix];
+  // round two: the list entries
+  uint2 ev[kWriteEnt];
+#pragma unroll
+  for (int u = 0; u < kWriteEnt; ++u) {
+    const uint32_t q = threadIdx.x + uint32_t(u) * kWriteThreads;
+    ev[u] = q < n ? ent[q] : make_uint2(0u, 0u);
+  }
+  ct.e[threadIdx.x] = cte;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t w = threadIdx.x + uint32_t(h) * kWriteThreads;
+    if (w < nb1w) *reinterpret_cast<uint4*>(bt1 + 16 * w) = btw[h];
+  }
   CandRec* ci = cand + i * int64_t(a.cmax);
   int8_t* trow = tier + i * a.F;
   auto append = [&](uint64_t key, int64_t k) {
     const int32_t slot = atomicAdd(&ccount[i], 1);
     if (slot < a.cmax) ci[slot] = CandRec{key, uint32_t(k), 0u};
+  };
+  auto apply = [&](uint2 v, uint32_t xoff, uint32_t wlen, int64_t w0) {
+    const uint32_t x = (v.y & kOffMask) - xoff;
+    if (x < wlen) {
+      const uint32_t b = bin_read(ct, v.y >> 24, int32_t(v.x));
+      const int8_t tv = bt1[b];
+      if (tv == kCandMark) {
+        append((uint64_t(b) << 32) | uint64_t(v.x), w0 + x);
+        tb[x] = 0;
+      } else {
+        tb[x] = tv;
+      }
+    }
   };
   for (int64_t w0 = k0; w0 < kend; w0 += kWriteWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kWriteWin ? kend - w0 : kWriteWin);
@@ -779,30 +862,22 @@ plan_write_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
     const uint32_t zb0 = uint32_t(w0 >> kClass0Shift);
     const uint32_t nzb = uint32_t((w0 + wlen - 1) >> kClass0Shift) - zb0 + 1;
     if (threadIdx.x == 0) s_c0cand = 0;
+    int8_t zt = 0;
+    if (threadIdx.x < nzb) zt = bt[a.nbin1 + zb0 + threadIdx.x];
     __syncthreads();
-    for (uint32_t z = threadIdx.x; z < nzb; z += kWriteThreads) {
-      const int8_t v = bt[a.nbin1 + zb0 + z];
-      t0[z] = v;
-      if (v == kCandMark) s_c0cand = 1;
+    if (threadIdx.x < nzb) {
+      t0[threadIdx.x] = zt;
+      if (zt == kCandMark) s_c0cand = 1;
     }
     __syncthreads();
     for (uint32_t x = threadIdx.x; x < wlen; x += kWriteThreads)
       tb[x] = t0[((w0 + x) >> kClass0Shift) - zb0];
     __syncthreads();
-    for (uint32_t q = threadIdx.x; q < n; q += kWriteThreads) {
-      const uint2 v = ent[q];
-      const uint32_t x = (v.y & kOffMask) - xoff;
-      if (x < wlen) {
-        const uint32_t b = bin_read(ct, v.y >> 24, int32_t(v.x));
-        const int8_t tv = bt[b];
-        if (tv == kCandMark) {
-          append((uint64_t(b) << 32) | uint64_t(v.x), w0 + x);
-          tb[x] = 0;
-        } else {
-          tb[x] = tv;
-        }
-      }
-    }
+#pragma unroll
+    for (int u = 0; u < kWriteEnt; ++u)
+      if (threadIdx.x + uint32_t(u) * kWriteThreads < n) apply(ev[u], xoff, wlen, w0);
+    for (uint32_t q = threadIdx.x + kWriteEnt * kWriteThreads; q < n; q += kWriteThreads)
+      apply(ent[q], xoff, wlen, w0);
     __syncthreads();
     if (s_c0cand) {
       // unread cells of candidate class-0 bins (read ones were overwritten)
@@ -874,6 +949,7 @@ void plan_args(const Shape& s, const int64_t* caps, int32_t J, PlanArgs* a) {
   class_bins(s.F, s.E, s.L, a->nbc, &a->nbin1);
   a->nb0 = uint32_t(ceil_div(s.F, int64_t(1) << kClass0Shift));
   a->nbin = a->nbin1 + a->nb0;
+  a->btp = (a->nbin + 15u) & ~15u;
   a->cmax = kCandMax;
   if (debug_value(2) > 0 && debug_value(2) < kCandMax) a->cmax = int32_t(debug_value(2));
   for (int j = 0; j < 128; ++j) a->caps[j] = j < J ? caps[j] : 0;
@@ -978,7 +1054,7 @@ int plan_compact(const Shape& s, const CompactCells& cc, const uint8_t* count,
   ClassTable* gct;
   int8_t* btier;
   if ((rc = scr.alloc_n(&gct, 1))) return rc;
-  if ((rc = scr.alloc_n(&btier, size_t(s.N) * a.nbin))) return rc;
+  if ((rc = scr.alloc_n(&btier, size_t(s.N) * a.btp))) return rc;
   if ((rc = launch("plan_classes", plan_classes, dim3(1), dim3(64), 0, st, a, gct))) return rc;
   const CompactArgs c{cc.ent, cc.base, cc.num, cc.ws, cc.nbk,
                       uint32_t(kSliceCells >> cc.ws)};
