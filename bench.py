@@ -37,15 +37,16 @@ SIDE_STREAM_KERNELS = ("next_tile", "next_unpartition", "pad_rows")
 def algorithmic_bytes(job, M_w, D, fused):
     """Bytes each kernel must move given the C ABI's dense layouts, per
     launch: A reads, N*F cells, D distinct (worker, sample) cells read. In the
-    fused call the counting pass also lists the D read cells (8 B each) and
-    the tier plan reads that list instead of the dense count/first tables."""
+    fused call the counting pass also lists the D read cells (4 B each: the
+    cell's bin and offset) and the tier plan reads that list instead of the
+    dense count/first tables."""
     A = int(sum(M_w))
     NF = job.N * job.F
     out = {
         # streams: write R (4 B per read)
         "stream_sort": 4 * A,
         # stats: read R (partitioned), write count (1 B) and first (4 B) per cell
-        "stats_tile": 4 * A + 5 * NF + (8 * D if fused else 0),
+        "stats_tile": 4 * A + 5 * NF + (4 * D if fused else 0),
         # next: read R, write next
         "next_unpartition": 8 * A,
         "seg_partition": 8 * A,
@@ -54,8 +55,8 @@ def algorithmic_bytes(job, M_w, D, fused):
     }
     if fused:
         # list entry and the size of each read cell; tier bytes for every cell
-        out["plan_hist"] = 16 * D
-        out["plan_write"] = 8 * D + NF
+        out["plan_hist"] = 12 * D
+        out["plan_write"] = 4 * D + NF
     else:
         # read count and first (and sizes), write tier
         out["plan_hist"] = 5 * NF + 8 * job.F

@@ -268,16 +268,19 @@ __device__ __forceinline__ void for_each_read(const SegParams& p, int64_t i, uin
 constexpr int kRunLoads = 8;
 
 // kCompact (fused planning call): the tile also lists its read cells for the
-// tier plan, entry {first, count << 24 | offset in window}, at the worker's
-// offset base = its reads in earlier windows (the sum of the run starts).
+// tier plan, entry = the cell's rank-ordered bin << kListOffBits | offset in
+// window, at the worker's offset base = its reads in earlier windows (the
+// sum of the run starts).
 template <bool kVec, bool kCompact>
 __global__ void __launch_bounds__(kStatsThreads)
 stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
            uint8_t* __restrict__ count, int32_t* __restrict__ first, uint32_t ntiles,
-           uint2* __restrict__ cent, int32_t* __restrict__ cbase, uint32_t* __restrict__ cnum) {
+           uint32_t* __restrict__ cent, int32_t* __restrict__ cbase, uint32_t* __restrict__ cnum,
+           const ClassTable* __restrict__ classes) {
   extern __shared__ uint32_t sm[];
   __shared__ uint32_t s_cnt, s_base;
   __shared__ uint32_t s_tmp[65];
+  __shared__ ClassTable s_ct;  // kCompact: the bin table
   uint32_t* cw = sm;                                   // kStatsWin / 4 words of byte counters
   int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsWin / 4);
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
@@ -293,11 +296,13 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;  // run starts in window kb
   const uint16_t* ob = oa + runs;                            // run ends
   const uint32_t nsc = uint32_t(p.nsc);
-  uint2* crow_ent = kCompact ? cent + i * p.M_max : nullptr;
+  uint32_t* crow_ent = kCompact ? cent + i * p.M_max : nullptr;
   if (kCompact && threadIdx.x == 0) {
     s_cnt = 0;
     s_base = 0;
   }
+  if (kCompact)
+    for (int c = threadIdx.x; c < 256; c += kStatsThreads) s_ct.e[c] = classes->e[c];
   for (int64_t w0 = k0; w0 < kend; w0 += kStatsWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kStatsWin ? kend - w0 : kStatsWin);
     const uint32_t xoff = uint32_t(w0 - k0);
@@ -342,13 +347,16 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     __syncthreads();
     uint8_t* crow = count + i * p.F + w0;
     int32_t* frow = first + i * p.F + w0;
-    uint2* cdst = kCompact ? crow_ent + s_base : nullptr;
+    uint32_t* cdst = kCompact ? crow_ent + s_base : nullptr;
+    auto entry = [&](uint32_t c, int32_t f, uint32_t xw) {
+      return (bin_read(s_ct, c, f) << kListOffBits) | xw;
+    };
     auto cnt_at = [&](uint32_t x) { return (cw[x >> 2] >> ((x & 3u) * 8u)) & 0xFFu; };
     auto single = [&](uint32_t x) {
       const uint32_t c = cnt_at(x);
       crow[x] = uint8_t(c);
       frow[x] = c ? fi[x] : -1;
-      if (kCompact && c) cdst[atomicAdd(&s_cnt, 1u)] = make_uint2(uint32_t(fi[x]), (c << 24) | (xoff + x));
+      if (kCompact && c) cdst[atomicAdd(&s_cnt, 1u)] = entry(c, fi[x], xoff + x);
     };
     // cells up to the first flat index divisible by 4 and after the last
     // group of 4 go one per thread; the rest as 4-cell groups per lane
@@ -390,15 +398,15 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
       const uint32_t run0 = s_cnt;  // entries already listed for this tile
       // stage the entries in the (now free) first-read table, then write them
       // out as one contiguous run; a run too long for the table goes direct
-      uint2* stage = reinterpret_cast<uint2*>(fi);
-      const bool staged = total <= uint32_t(kStatsWin / 2);
+      uint32_t* stage = reinterpret_cast<uint32_t*>(fi);  // holds a window's worth
+      const bool staged = total <= uint32_t(kStatsWin);
 #pragma unroll
       for (int m = 0; m < kUnits; ++m) {
         const uint32_t x = head + 4 * (threadIdx.x + uint32_t(m) * kStatsThreads);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if (fr[m][q] >= 0) {
-            const uint2 ent = make_uint2(uint32_t(fr[m][q]), (cnt_at(x + q) << 24) | (xoff + x + q));
+            const uint32_t ent = entry(cnt_at(x + q), fr[m][q], xoff + x + q);
             if (staged) stage[slot] = ent; else cdst[run0 + slot] = ent;
             ++slot;
           }
@@ -631,25 +639,25 @@ int run_partition(const SegParams& p, const int32_t* R, Scratch& scr, uint32_t**
 }
 
 int launch_stats(const SegParams& p, const uint32_t* Pk, const uint16_t* OT, uint8_t* count,
-                 int32_t* first, CompactCells* cc, hipStream_t st) {
+                 int32_t* first, CompactCells* cc, const ClassTable* classes, hipStream_t st) {
   const uint32_t ntiles = uint32_t(p.N * p.nbk);
   const size_t smem = size_t(kStatsWin / 4 + kStatsWin) * 4;
   // vector stores need 4-byte aligned count rows and 16-byte aligned first rows
   const bool vec = (reinterpret_cast<uintptr_t>(count) & 3) == 0 &&
                    (reinterpret_cast<uintptr_t>(first) & 15) == 0;
   const dim3 grid(xcd_padded(ntiles)), block(kStatsThreads);
-  uint2* ent = cc ? cc->ent : nullptr;
+  uint32_t* ent = cc ? cc->ent : nullptr;
   int32_t* base = cc ? cc->base : nullptr;
   uint32_t* num = cc ? cc->num : nullptr;
   if (cc)
     return vec ? launch("stats_tile", stats_tile<true, true>, grid, block, smem, st, p, Pk, OT, count,
-                        first, ntiles, ent, base, num)
+                        first, ntiles, ent, base, num, classes)
                : launch("stats_tile", stats_tile<false, true>, grid, block, smem, st, p, Pk, OT,
-                        count, first, ntiles, ent, base, num);
+                        count, first, ntiles, ent, base, num, classes);
   return vec ? launch("stats_tile", stats_tile<true, false>, grid, block, smem, st, p, Pk, OT, count,
-                      first, ntiles, ent, base, num)
+                      first, ntiles, ent, base, num, classes)
              : launch("stats_tile", stats_tile<false, false>, grid, block, smem, st, p, Pk, OT, count,
-                      first, ntiles, ent, base, num);
+                      first, ntiles, ent, base, num, classes);
 }
 
 // Window width of the next-use pass: about three quarters of the fast-path
@@ -708,7 +716,7 @@ int stats_impl(const nopfs_job* job, const int32_t* R, uint8_t* count, int32_t* 
   uint32_t* Pk;
   uint16_t* OT;
   if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
-  return launch_stats(p, Pk, OT, count, first, nullptr, st);
+  return launch_stats(p, Pk, OT, count, first, nullptr, nullptr, st);
 }
 
 int next_impl(const nopfs_job* job, const int32_t* R, int32_t* next, hipStream_t st) {
@@ -727,8 +735,8 @@ int next_impl(const nopfs_job* job, const int32_t* R, int32_t* next, hipStream_t
   return launch_next(p, Pk, OT, nextP, next, st);
 }
 
-int access_fused(const Shape& s, const int32_t* R, uint8_t* count, int32_t* first,
-                 int32_t* next, CompactCells* cc, Scratch& keep, SideWork& side,
+int access_fused(const Shape& s, const int32_t* R, const ClassTable* classes, uint8_t* count,
+                 int32_t* first, int32_t* next, CompactCells* cc, Scratch& keep, SideWork& side,
                  hipStream_t side_st, hipStream_t st) {
   int rc;
   const SegParams ps = seg_params(s, NOPFS_STATS_WS);
@@ -752,7 +760,7 @@ int access_fused(const Shape& s, const int32_t* R, uint8_t* count, int32_t* firs
   // the tier plan (write-heavy), which they do not feed
   if ((rc = side.begin())) return rc;
   if ((rc = launch_next(pn, Pn, OTn, nextP, next, side_st))) return rc;
-  return launch_stats(ps, Pk, OT, count, first, cc, st);
+  return launch_stats(ps, Pk, OT, count, first, cc, classes, st);
 }
 
 }  // namespace nopfs

@@ -32,10 +32,20 @@ int plan_job_impl(const nopfs_job* job, const int64_t* sizes, const int64_t* cap
   if (debug_value(4) == 0)
     if ((rc = side_stream(&side_st))) return rc;
   Scratch keep(st);
+  CompactPlan* cp = nullptr;
+  struct FreePlan {
+    CompactPlan*& cp;
+    ~FreePlan() {
+      if (cp) compact_plan_free(cp);
+    }
+  } free_plan{cp};
+  const ClassTable* classes = nullptr;
+  if ((rc = compact_plan_prepare(s, caps, J, keep, st, &cp, &classes))) return rc;
   SideWork side(st, side_st);  // joins before `keep` frees its buffers
   CompactCells cc;
-  if ((rc = access_fused(s, R, count, first, next, &cc, keep, side, side_st, st))) return rc;
-  return plan_compact(s, cc, count, first, sizes, caps, J, tier, used, st);
+  if ((rc = access_fused(s, R, classes, count, first, next, &cc, keep, side, side_st, st)))
+    return rc;
+  return compact_plan_run(cp, cc, count, first, sizes, tier, used, st);
 }
 
 }  // namespace

@@ -8,14 +8,35 @@
 
 namespace nopfs {
 
+// Rank-ordered bins of the tier plan for read cells (count class c >= 1,
+// first read f): one 8-byte record per class, the bin scale and, packed, the
+// class's first bin (high 16 bits) and its last bin offset (low 16). Classes
+// above E (outside the precondition) hold class E's record.
+struct ClassTable {
+  float2 e[256];  // x = scale, y = bits of (base << 16 | top)
+};
+
+__device__ __forceinline__ uint32_t bin_read(const ClassTable& t, uint32_t c, int32_t f) {
+  const float2 r = t.e[c];
+  const uint32_t bt = __float_as_uint(r.y);
+  // a negative f (not a first read) lands in the class's first bin
+  const uint32_t xi0 = uint32_t(fmaxf(float(f) * r.x, 0.f));
+  const uint32_t top = bt & 0xFFFFu;
+  return (bt >> 16) + (xi0 < top ? xi0 : top);
+}
+
+// Read-cell list entry: bin << kListOffBits | offset of the sample in its
+// window (bins of classes >= 1 are fewer than 2^13, windows at most 2^19).
+constexpr int kListOffBits = 19;
+constexpr uint32_t kListOffMask = (1u << kListOffBits) - 1;
+
 // Read cells per (worker i, sample window kb) tile, windows of 2^ws samples.
 // Tile (i, kb) owns entries ent[i * M_max + base[i * nbk + kb] + t] for
 // t < num[i * nbk + kb] (a worker reads at most M_max cells, and base is the
-// number of its reads in earlier windows, so tiles never overlap). Entry =
-// {first read f, count << 24 | offset of the sample in its window}, in no
-// particular order inside the tile.
+// number of its reads in earlier windows, so tiles never overlap). One entry
+// per read cell, in no particular order inside the tile.
 struct CompactCells {
-  uint2* ent = nullptr;
+  uint32_t* ent = nullptr;
   int32_t* base = nullptr;
   uint32_t* num = nullptr;
   int32_t ws = 0;
@@ -26,16 +47,22 @@ struct CompactCells {
 // nopfs_access_stats and nopfs_reuse_next) that also fills *cc. The next-use
 // kernels go on `side_st` after side.begin(); every buffer comes from `keep`,
 // which the caller frees only after `side` has joined. Requires M_max > 0.
-int access_fused(const Shape& s, const int32_t* R, uint8_t* count, int32_t* first,
-                 int32_t* next, CompactCells* cc, Scratch& keep, SideWork& side,
+int access_fused(const Shape& s, const int32_t* R, const ClassTable* classes, uint8_t* count,
+                 int32_t* first, int32_t* next, CompactCells* cc, Scratch& keep, SideWork& side,
                  hipStream_t side_st, hipStream_t st);
 
-// Tier plan (the stage of nopfs_tier_plan) from the compact list; count and
-// first are the dense tables of the same pass (read only if a worker's
-// candidate list overflows).
-int plan_compact(const Shape& s, const CompactCells& cc, const uint8_t* count,
-                 const int32_t* first, const int64_t* sizes, const int64_t* caps, int32_t J,
-                 int8_t* tier, int64_t* used, hipStream_t st);
+// Tier plan (the stage of nopfs_tier_plan) from the compact list, in two
+// steps: prepare() checks the arguments, allocates from `keep` and fills the
+// class table the counting pass bins with; run() does the rest. count and
+// first are the dense tables of the same call (first read for candidate
+// cells, both for a worker whose candidate list overflows).
+struct CompactPlan;
+int compact_plan_prepare(const Shape& s, const int64_t* caps, int32_t J, Scratch& keep,
+                         hipStream_t st, CompactPlan** out, const ClassTable** classes);
+int compact_plan_run(CompactPlan* cp, const CompactCells& cc, const uint8_t* count,
+                     const int32_t* first, const int64_t* sizes, int8_t* tier, int64_t* used,
+                     hipStream_t st);
+void compact_plan_free(CompactPlan* cp);
 
 // Argument checks of the tier plan (J and the capacities).
 int plan_check(const int64_t* caps, int32_t J);

@@ -72,12 +72,6 @@ struct PlanArgs {
   int64_t caps[128];
 };
 
-// One 8-byte LDS record per count class: the bin scale and, packed, the
-// first bin of the class (high 16 bits) and its last bin offset (low 16).
-struct ClassTable {
-  float2 e[256];  // x = scale, y = bits of (base << 16 | top)
-};
-
 __device__ void build_class_table(const PlanArgs& a, ClassTable& t) {
   if (threadIdx.x == 0) {
     uint32_t b = 0;
@@ -93,24 +87,10 @@ __device__ void build_class_table(const PlanArgs& a, ClassTable& t) {
   __syncthreads();
 }
 
-// The same table computed once into global memory, and its copy into LDS
-// (for kernels with many small workgroups).
+// The same table computed once into global memory (the fused call's
+// counting pass bins the read cells with it).
 __global__ void plan_classes(PlanArgs a, ClassTable* g) { build_class_table(a, *g); }
 
-__device__ void load_class_table(const ClassTable* __restrict__ g, ClassTable& t) {
-  for (int c = threadIdx.x; c < 256; c += blockDim.x) t.e[c] = g->e[c];
-  __syncthreads();
-}
-
-// Bin of a read cell (class c in [1, 255], first read f >= 0).
-__device__ __forceinline__ uint32_t bin_read(const ClassTable& t, uint32_t c, int32_t f) {
-  const float2 r = t.e[c];
-  const uint32_t bt = __float_as_uint(r.y);
-  // a negative f (not a first read) lands in the class's first bin
-  const uint32_t xi0 = uint32_t(fmaxf(float(f) * r.x, 0.f));
-  const uint32_t top = bt & 0xFFFFu;
-  return (bt >> 16) + (xi0 < top ? xi0 : top);
-}
 
 // Rank-ordered bin of a cell; identical in every kernel that uses it.
 __device__ __forceinline__ uint32_t bin_of(const PlanArgs& a, const ClassTable& t, uint32_t c,
@@ -651,17 +631,16 @@ plan_exact(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
 
 // -- passes over the compact read-cell list (fused planning call) -----------------
 // The counting pass lists, per (worker, window of 2^ws samples), the cells the
-// worker reads: {first read, count << 24 | offset in window}. Cells missing
-// from the list are unread (class 0).
+// worker reads: bin << kListOffBits | offset in window. Cells missing from the
+// list are unread (class 0).
 struct CompactArgs {
-  const uint2* ent;
+  const uint32_t* ent;
   const int32_t* base;
   const uint32_t* num;
   int32_t ws;
   uint32_t nbk;
   uint32_t wps;  // windows per slice of kSliceCells samples
 };
-constexpr uint32_t kOffMask = (1u << 24) - 1;
 #ifndef NOPFS_HIST_CU
 #define NOPFS_HIST_CU 4
 #endif
@@ -674,13 +653,11 @@ constexpr int kHistCU = NOPFS_HIST_CU;  // list entries per lane in flight
 constexpr uint32_t kHistWins = 1024;
 
 __global__ void __launch_bounds__(kThreads)
-plan_hist_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
-            const int64_t* __restrict__ sizes, uint64_t* __restrict__ Z, uint64_t* __restrict__ H,
-            uint32_t nslices) {
+plan_hist_c(PlanArgs a, CompactArgs c, const int64_t* __restrict__ sizes, uint64_t* __restrict__ Z,
+            uint64_t* __restrict__ H, uint32_t nslices) {
   extern __shared__ uint64_t sm[];
   uint64_t* h1 = sm;
   unsigned long long* zs = reinterpret_cast<unsigned long long*>(sm + a.nbin1);
-  __shared__ ClassTable ct;
   __shared__ uint32_t wnum[kHistWins];
   __shared__ int32_t wbase[kHistWins];
   const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
@@ -692,12 +669,11 @@ plan_hist_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
   const uint32_t nz = uint32_t((ke - ks + (1 << kClass0Shift) - 1) >> kClass0Shift);
   for (uint32_t b = threadIdx.x; b < a.nbin1; b += kThreads) h1[b] = 0;
   for (uint32_t b = threadIdx.x; b < nz; b += kThreads) zs[b] = 0;
-  load_class_table(gct, ct);
   const uint32_t kb0 = uint32_t(sl) * c.wps;
   const uint32_t kb1 = kb0 + c.wps < c.nbk ? kb0 + c.wps : c.nbk;
   const uint32_t lane = __lane_id(), wave = threadIdx.x >> 6;
   constexpr uint32_t kWaves = kThreads / 64;
-  const uint2* erow = c.ent + i * a.M_max;
+  const uint32_t* erow = c.ent + i * a.M_max;
   for (uint32_t g0 = kb0; g0 < kb1; g0 += kHistWins) {
     const uint32_t g1 = g0 + kHistWins < kb1 ? g0 + kHistWins : kb1;
     for (uint32_t kb = g0 + threadIdx.x; kb < g1; kb += kThreads) {
@@ -705,50 +681,50 @@ plan_hist_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
       wbase[kb - g0] = c.base[i * int64_t(c.nbk) + kb];
     }
     __syncthreads();
-    uint2 v[kHistCU];
+    uint32_t v[kHistCU];
     auto fetch = [&](uint32_t kb) {
       const uint32_t n = kb < g1 ? wnum[kb - g0] : 0u;
-      const uint2* e = erow + (kb < g1 ? wbase[kb - g0] : 0);
+      const uint32_t* e = erow + (kb < g1 ? wbase[kb - g0] : 0);
 #pragma unroll
       for (int u = 0; u < kHistCU; ++u) {
         const uint32_t q = u * 64 + lane;
-        v[u] = q < n ? e[q] : make_uint2(0u, 0u);
+        v[u] = q < n ? e[q] : 0u;
       }
     };
-    auto add = [&](uint2 e, uint64_t sz, int64_t kw) {
-      const int64_t k = kw + (e.y & kOffMask);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&h1[bin_read(ct, e.y >> 24, int32_t(e.x))]),
+    auto add = [&](uint32_t e, uint64_t sz, int64_t kw) {
+      const int64_t k = kw + (e & kListOffMask);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&h1[e >> kListOffBits]),
                 static_cast<unsigned long long>(sz));
       atomicAdd(&zs[uint32_t(k >> kClass0Shift) - zb0], static_cast<unsigned long long>(sz));
     };
     fetch(g0 + wave);
     for (uint32_t kb = g0 + wave; kb < g1; kb += kWaves) {
       const uint32_t n = wnum[kb - g0];
-      const uint2* e = erow + wbase[kb - g0];
+      const uint32_t* e = erow + wbase[kb - g0];
       const int64_t kw = int64_t(kb) << c.ws;
-      uint2 cur[kHistCU];
+      uint32_t cur[kHistCU];
 #pragma unroll
       for (int u = 0; u < kHistCU; ++u) cur[u] = v[u];
       fetch(kb + kWaves);  // next window's first entries
       uint64_t sz[kHistCU];
 #pragma unroll
       for (int u = 0; u < kHistCU; ++u)
-        sz[u] = u * 64 + lane < n ? uint64_t(sizes[kw + (cur[u].y & kOffMask)]) : 0ull;
+        sz[u] = u * 64 + lane < n ? uint64_t(sizes[kw + (cur[u] & kListOffMask)]) : 0ull;
 #pragma unroll
       for (int u = 0; u < kHistCU; ++u)
         if (u * 64 + lane < n) add(cur[u], sz[u], kw);
       // entries beyond the prefetched ones
       for (uint32_t q0 = kHistCU * 64; q0 < n; q0 += kHistCU * 64) {
-        uint2 w[kHistCU];
+        uint32_t w[kHistCU];
 #pragma unroll
         for (int u = 0; u < kHistCU; ++u) {
           const uint32_t q = q0 + u * 64 + lane;
-          w[u] = q < n ? e[q] : make_uint2(0u, 0u);
+          w[u] = q < n ? e[q] : 0u;
         }
         uint64_t wz[kHistCU];
 #pragma unroll
         for (int u = 0; u < kHistCU; ++u)
-          wz[u] = q0 + u * 64 + lane < n ? uint64_t(sizes[kw + (w[u].y & kOffMask)]) : 0ull;
+          wz[u] = q0 + u * 64 + lane < n ? uint64_t(sizes[kw + (w[u] & kListOffMask)]) : 0ull;
 #pragma unroll
         for (int u = 0; u < kHistCU; ++u)
           if (q0 + u * 64 + lane < n) add(w[u], wz[u], kw);
@@ -796,10 +772,9 @@ constexpr uint32_t kBt1Max = ((kBins1Budget + 256 + 15) / 16) * 16;  // class >=
 
 template <bool kVec>
 __global__ void __launch_bounds__(kWriteThreads)
-plan_write_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
+plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
              const int8_t* __restrict__ btier, int8_t* __restrict__ tier,
              CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t ntiles) {
-  __shared__ ClassTable ct;
   __shared__ __align__(16) int8_t bt1[kBt1Max];
   __shared__ int8_t tb[kWriteWin];
   __shared__ int8_t t0[kWriteWin / (1 << kClass0Shift) + 1];
@@ -812,8 +787,7 @@ plan_write_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
   const int64_t k0 = int64_t(kb) << c.ws;
   const int64_t kend = k0 + (int64_t(1) << c.ws) < a.F ? k0 + (int64_t(1) << c.ws) : a.F;
   const int64_t tix = i * int64_t(c.nbk) + kb;
-  // round one: tables, list bounds, class-0 tiers of the first piece
-  const float2 cte = gct->e[threadIdx.x];  // 256 classes, one per thread
+  // round one: bin tiers, list bounds, class-0 tiers of the first piece
   const uint32_t nb1w = (a.nbin1 + 15) / 16;
   uint4 btw[2];
 #pragma unroll
@@ -823,15 +797,14 @@ plan_write_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
     if (w < nb1w) btw[h] = *reinterpret_cast<const uint4*>(bt + 16 * w);  // inside the padded row
   }
   const uint32_t n = c.num[tix];
-  const uint2* ent = c.ent + i * a.M_max + c.base[tix];
+  const uint32_t* ent = c.ent + i * a.M_max + c.base[tix];
   // round two: the list entries
-  uint2 ev[kWriteEnt];
+  uint32_t ev[kWriteEnt];
 #pragma unroll
   for (int u = 0; u < kWriteEnt; ++u) {
     const uint32_t q = threadIdx.x + uint32_t(u) * kWriteThreads;
-    ev[u] = q < n ? ent[q] : make_uint2(0u, 0u);
+    ev[u] = q < n ? ent[q] : 0u;
   }
-  ct.e[threadIdx.x] = cte;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const uint32_t w = threadIdx.x + uint32_t(h) * kWriteThreads;
@@ -843,13 +816,15 @@ plan_write_c(PlanArgs a, CompactArgs c, const ClassTable* __restrict__ gct,
     const int32_t slot = atomicAdd(&ccount[i], 1);
     if (slot < a.cmax) ci[slot] = CandRec{key, uint32_t(k), 0u};
   };
-  auto apply = [&](uint2 v, uint32_t xoff, uint32_t wlen, int64_t w0) {
-    const uint32_t x = (v.y & kOffMask) - xoff;
+  const int32_t* frow = first + i * a.F;
+  auto apply = [&](uint32_t v, uint32_t xoff, uint32_t wlen, int64_t w0) {
+    const uint32_t x = (v & kListOffMask) - xoff;
     if (x < wlen) {
-      const uint32_t b = bin_read(ct, v.y >> 24, int32_t(v.x));
+      const uint32_t b = v >> kListOffBits;
       const int8_t tv = bt1[b];
       if (tv == kCandMark) {
-        append((uint64_t(b) << 32) | uint64_t(v.x), w0 + x);
+        // the rank key needs the first read itself (few cells per worker)
+        append((uint64_t(b) << 32) | uint64_t(uint32_t(frow[w0 + x])), w0 + x);
         tb[x] = 0;
       } else {
         tb[x] = tv;
@@ -974,6 +949,7 @@ int plan_begin(const Shape& s, const PlanArgs& a, const int64_t* sizes, Scratch&
   if ((rc = launch("fill_i32", fill_i32, dim3(uint32_t(ceil_div(s.N, 256))), dim3(256), 0, st,
                    b->ccount, s.N)))
     return rc;
+  if (!sizes) return NOPFS_OK;  // the caller sums the bins later
   return launch("plan_binsum", plan_binsum, dim3(uint32_t(ceil_div(a.nb0, 4))), dim3(256), 0, st,
                 s.F, a.nb0, sizes, b->binsum);
 }
@@ -1040,47 +1016,66 @@ int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,
   return plan_end(s, a, b, count, first, sizes, tier, used, st);
 }
 
-int plan_compact(const Shape& s, const CompactCells& cc, const uint8_t* count,
-                 const int32_t* first, const int64_t* sizes, const int64_t* caps, int32_t J,
-                 int8_t* tier, int64_t* used, hipStream_t st) {
-  int rc;
-  if ((rc = plan_check(caps, J))) return rc;
-  if (cc.ws > 19) return fail(NOPFS_EDEVICE, "sample windows wider than a histogram slice");
+struct CompactPlan {
+  Shape s;
   PlanArgs a;
-  plan_args(s, caps, J, &a);
-  Scratch scr(st);
   PlanBufs b;
-  if ((rc = plan_begin(s, a, sizes, scr, &b, st))) return rc;
   ClassTable* gct;
   int8_t* btier;
-  if ((rc = scr.alloc_n(&gct, 1))) return rc;
-  if ((rc = scr.alloc_n(&btier, size_t(s.N) * a.btp))) return rc;
-  if ((rc = launch("plan_classes", plan_classes, dim3(1), dim3(64), 0, st, a, gct))) return rc;
-  const CompactArgs c{cc.ent, cc.base, cc.num, cc.ws, cc.nbk,
-                      uint32_t(kSliceCells >> cc.ws)};
+};
+
+int compact_plan_prepare(const Shape& s, const int64_t* caps, int32_t J, Scratch& keep,
+                         hipStream_t st, CompactPlan** out, const ClassTable** classes) {
+  int rc;
+  if ((rc = plan_check(caps, J))) return rc;
+  CompactPlan* cp = new CompactPlan;
+  *out = cp;
+  cp->s = s;
+  plan_args(s, caps, J, &cp->a);
+  if ((rc = keep.alloc_n(&cp->gct, 1))) return rc;
+  if ((rc = keep.alloc_n(&cp->btier, size_t(s.N) * cp->a.btp))) return rc;
+  if ((rc = plan_begin(s, cp->a, nullptr, keep, &cp->b, st))) return rc;
+  *classes = cp->gct;
+  return launch("plan_classes", plan_classes, dim3(1), dim3(64), 0, st, cp->a, cp->gct);
+}
+
+int compact_plan_run(CompactPlan* cp, const CompactCells& cc, const uint8_t* count,
+                     const int32_t* first, const int64_t* sizes, int8_t* tier, int64_t* used,
+                     hipStream_t st) {
+  int rc;
+  if (cc.ws > kListOffBits) return fail(NOPFS_EDEVICE, "sample windows wider than a list offset");
+  const Shape& s = cp->s;
+  const PlanArgs& a = cp->a;
+  const PlanBufs& b = cp->b;
+  if ((rc = launch("plan_binsum", plan_binsum, dim3(uint32_t(ceil_div(a.nb0, 4))), dim3(256), 0, st,
+                   s.F, a.nb0, sizes, b.binsum)))
+    return rc;
+  const CompactArgs c{cc.ent, cc.base, cc.num, cc.ws, cc.nbk, uint32_t(kSliceCells >> cc.ws)};
   const uint32_t nslices = uint32_t(ceil_div(s.F, kSliceCells));
   const uint32_t nht = uint32_t(s.N) * nslices;
   const size_t hsmem = (size_t(a.nbin1) + kSliceBins0) * 8;
   if ((rc = launch("plan_hist", plan_hist_c, dim3(xcd_padded(nht)), dim3(kThreads), hsmem, st, a, c,
-                   (const ClassTable*)gct, sizes, b.Z, b.H, nslices)))
+                   sizes, b.Z, b.H, nslices)))
     return rc;
   if ((rc = launch("plan_cut", plan_cut, dim3(uint32_t(s.N)), dim3(1024), 0, st, a,
                    (const uint64_t*)b.binsum, (const uint64_t*)b.Z, b.H, b.ranges)))
     return rc;
   if ((rc = launch("plan_btier", plan_btier, dim3(uint32_t(ceil_div(a.nbin, 256)), uint32_t(s.N)),
-                   dim3(256), 0, st, a, (const int32_t*)b.ranges, btier)))
+                   dim3(256), 0, st, a, (const int32_t*)b.ranges, cp->btier)))
     return rc;
   const uint32_t ntiles = uint32_t(s.N) * cc.nbk;
   const bool vec = (reinterpret_cast<uintptr_t>(tier) & 3) == 0;
   if ((rc = vec ? launch("plan_write", plan_write_c<true>, dim3(xcd_padded(ntiles)),
-                         dim3(kWriteThreads), 0, st, a, c, (const ClassTable*)gct,
-                         (const int8_t*)btier, tier, b.cand, b.ccount, ntiles)
+                         dim3(kWriteThreads), 0, st, a, c, first, (const int8_t*)cp->btier, tier,
+                         b.cand, b.ccount, ntiles)
                 : launch("plan_write", plan_write_c<false>, dim3(xcd_padded(ntiles)),
-                         dim3(kWriteThreads), 0, st, a, c, (const ClassTable*)gct,
-                         (const int8_t*)btier, tier, b.cand, b.ccount, ntiles)))
+                         dim3(kWriteThreads), 0, st, a, c, first, (const int8_t*)cp->btier, tier,
+                         b.cand, b.ccount, ntiles)))
     return rc;
   return plan_end(s, a, b, count, first, sizes, tier, used, st);
 }
+
+void compact_plan_free(CompactPlan* cp) { delete cp; }
 
 }  // namespace nopfs
 
