@@ -271,6 +271,13 @@ constexpr int kRunLoads = 8;
 // tier plan, entry = the cell's rank-ordered bin << kListOffBits | offset in
 // window, at the worker's offset base = its reads in earlier windows (the
 // sum of the run starts).
+//
+// The LDS tables are laid out so that cell x of a pass sits at position
+// x + sh, sh = (flat index of the pass's first cell) mod 4: a 4-cell group of
+// the output rows is then one aligned 32-bit count word and one aligned
+// 128-bit first-read word in LDS.
+constexpr int kStatsCwWords = ((kStatsWin + 4) / 4 + 3) & ~3;  // byte counters, 16-byte padded
+
 template <bool kVec, bool kCompact>
 __global__ void __launch_bounds__(kStatsThreads)
 stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
@@ -281,8 +288,8 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   __shared__ uint32_t s_cnt, s_base;
   __shared__ uint32_t s_tmp[65];
   __shared__ ClassTable s_ct;  // kCompact: the bin table
-  uint32_t* cw = sm;                                   // kStatsWin / 4 words of byte counters
-  int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsWin / 4);
+  uint32_t* cw = sm;                                        // byte counters
+  int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsCwWords);  // first reads
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
   const int64_t i = tile / p.nbk;
@@ -306,14 +313,15 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   for (int64_t w0 = k0; w0 < kend; w0 += kStatsWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kStatsWin ? kend - w0 : kStatsWin);
     const uint32_t xoff = uint32_t(w0 - k0);
+    const uint32_t sh = kVec ? uint32_t((i * p.F + w0) & 3) : 0u;
     // bounds of this thread's first run, requested before the LDS is cleared
     uint32_t ra = 0, rb = 0;
     if (threadIdx.x < runs) {
       ra = oa[threadIdx.x];
       rb = ob[threadIdx.x];
     }
-    for (uint32_t x = threadIdx.x; x < (wlen + 3) / 4; x += kStatsThreads) cw[x] = 0;
-    for (uint32_t x = threadIdx.x; x < wlen; x += kStatsThreads) fi[x] = INT_MAX;
+    for (uint32_t x = threadIdx.x; x < (wlen + sh + 3) / 4; x += kStatsThreads) cw[x] = 0;
+    for (uint32_t x = threadIdx.x; x < wlen + sh; x += kStatsThreads) fi[x] = INT_MAX;
     __syncthreads();
     uint32_t start_sum = 0;
     for (int64_t r = threadIdx.x; r < runs; r += kStatsThreads) {
@@ -333,8 +341,9 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
         for (int u = 0; u < kRunLoads; ++u) {
           const uint32_t x = (v[u] >> kScShift) - xoff;
           if (q + u < rb && x < wlen) {
-            atomicAdd(&cw[x >> 2], 1u << ((x & 3u) * 8u));
-            atomicMin(&fi[x], int32_t(fb + (v[u] & kJMask)));
+            const uint32_t px = x + sh;
+            atomicAdd(&cw[px >> 2], 1u << ((px & 3u) * 8u));
+            atomicMin(&fi[px], int32_t(fb + (v[u] & kJMask)));
           }
         }
       }
@@ -348,15 +357,19 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     uint8_t* crow = count + i * p.F + w0;
     int32_t* frow = first + i * p.F + w0;
     uint32_t* cdst = kCompact ? crow_ent + s_base : nullptr;
+    auto cnt_at = [&](uint32_t x) {  // x: cell of the pass
+      const uint32_t px = x + sh;
+      return (cw[px >> 2] >> ((px & 3u) * 8u)) & 0xFFu;
+    };
     auto entry = [&](uint32_t c, int32_t f, uint32_t xw) {
       return (bin_read(s_ct, c, f) << kListOffBits) | xw;
     };
-    auto cnt_at = [&](uint32_t x) { return (cw[x >> 2] >> ((x & 3u) * 8u)) & 0xFFu; };
     auto single = [&](uint32_t x) {
       const uint32_t c = cnt_at(x);
+      const int32_t f = fi[x + sh];
       crow[x] = uint8_t(c);
-      frow[x] = c ? fi[x] : -1;
-      if (kCompact && c) cdst[atomicAdd(&s_cnt, 1u)] = entry(c, fi[x], xoff + x);
+      frow[x] = c ? f : -1;
+      if (kCompact && c) cdst[atomicAdd(&s_cnt, 1u)] = entry(c, f, xoff + x);
     };
     // cells up to the first flat index divisible by 4 and after the last
     // group of 4 go one per thread; the rest as 4-cell groups per lane
@@ -366,55 +379,61 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     const uint32_t tail0 = head + 4 * nunits;
     for (uint32_t x = threadIdx.x; x < head; x += kStatsThreads) single(x);
     for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kStatsThreads) single(x);
-    // each thread keeps the first reads of its (at most kUnits) 4-cell
-    // groups, so the compact entries can be written once the first-read
-    // table is free (the count table stays intact)
+    // 4-cell groups: one count word and one first-read quad from LDS; each
+    // thread keeps its groups' words for the list below
     constexpr int kUnits = kStatsWin / 4 / kStatsThreads;
-    int32_t fr[kUnits][4];
+    uint32_t cwr[kUnits];
+    int4 frr[kUnits];
     uint32_t nmine = 0;
 #pragma unroll
     for (int m = 0; m < kUnits; ++m) {
       const uint32_t u = threadIdx.x + uint32_t(m) * kStatsThreads;
-      const uint32_t x = head + 4 * u;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) fr[m][q] = -1;
+      const uint32_t x = head + 4 * u;  // x + sh is a multiple of 4
+      cwr[m] = 0;
       if (u < nunits) {
-        uint32_t cq[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          cq[q] = cnt_at(x + q);
-          if (cq[q]) fr[m][q] = fi[x + q];
-          nmine += cq[q] != 0;
-        }
-        *reinterpret_cast<uint32_t*>(crow + x) = cq[0] | (cq[1] << 8) | (cq[2] << 16) | (cq[3] << 24);
-        *reinterpret_cast<int4*>(frow + x) = make_int4(fr[m][0], fr[m][1], fr[m][2], fr[m][3]);
+        const uint32_t word = cw[(x + sh) >> 2];
+        const int4 fq = *reinterpret_cast<const int4*>(&fi[x + sh]);
+        const int4 fo = make_int4((word & 0xFFu) ? fq.x : -1, (word & 0xFF00u) ? fq.y : -1,
+                                  (word & 0xFF0000u) ? fq.z : -1, (word >> 24) ? fq.w : -1);
+        *reinterpret_cast<uint32_t*>(crow + x) = word;
+        *reinterpret_cast<int4*>(frow + x) = fo;
+        cwr[m] = word;
+        frr[m] = fo;
+        nmine += ((word & 0xFFu) != 0) + ((word & 0xFF00u) != 0) + ((word & 0xFF0000u) != 0) +
+                 ((word >> 24) != 0);
       }
     }
     if (kCompact) {
-      // slots of this thread's entries; the scan's barriers also end every
-      // read of the LDS tables and every single cell's slot claim
+      // list: slots from one block scan (its barriers also end every read of
+      // the LDS tables and every single cell's slot claim); the read cells
+      // are staged raw in the (now free) first-read table, then binned and
+      // written out as one contiguous run. More than the table holds: binned
+      // and written directly.
       uint32_t total;
       uint32_t slot = block_exclusive_scan(nmine, s_tmp, &total);
       const uint32_t run0 = s_cnt;  // entries already listed for this tile
-      // stage the entries in the (now free) first-read table, then write them
-      // out as one contiguous run; a run too long for the table goes direct
-      uint32_t* stage = reinterpret_cast<uint32_t*>(fi);  // holds a window's worth
-      const bool staged = total <= uint32_t(kStatsWin);
+      uint2* stage = reinterpret_cast<uint2*>(fi);
+      const bool staged = total <= uint32_t(kStatsWin / 2);
 #pragma unroll
       for (int m = 0; m < kUnits; ++m) {
         const uint32_t x = head + 4 * (threadIdx.x + uint32_t(m) * kStatsThreads);
+        const int32_t fv[4] = {frr[m].x, frr[m].y, frr[m].z, frr[m].w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          if (fr[m][q] >= 0) {
-            const uint32_t ent = entry(cnt_at(x + q), fr[m][q], xoff + x + q);
-            if (staged) stage[slot] = ent; else cdst[run0 + slot] = ent;
+          const uint32_t c = (cwr[m] >> (8 * q)) & 0xFFu;
+          if (c) {
+            if (staged) stage[slot] = make_uint2(uint32_t(fv[q]), (c << 24) | (xoff + x + q));
+            else cdst[run0 + slot] = entry(c, fv[q], xoff + x + q);
             ++slot;
           }
         }
       }
       __syncthreads();
       if (staged)
-        for (uint32_t t = threadIdx.x; t < total; t += kStatsThreads) cdst[run0 + t] = stage[t];
+        for (uint32_t t = threadIdx.x; t < total; t += kStatsThreads) {
+          const uint2 e = stage[t];
+          cdst[run0 + t] = entry(e.y >> 24, int32_t(e.x), e.y & 0xFFFFFFu);
+        }
       if (threadIdx.x == 0) s_cnt = run0 + total;
     }
     __syncthreads();
@@ -641,7 +660,7 @@ int run_partition(const SegParams& p, const int32_t* R, Scratch& scr, uint32_t**
 int launch_stats(const SegParams& p, const uint32_t* Pk, const uint16_t* OT, uint8_t* count,
                  int32_t* first, CompactCells* cc, const ClassTable* classes, hipStream_t st) {
   const uint32_t ntiles = uint32_t(p.N * p.nbk);
-  const size_t smem = size_t(kStatsWin / 4 + kStatsWin) * 4;
+  const size_t smem = size_t(kStatsCwWords + kStatsWin + 4) * 4;
   // vector stores need 4-byte aligned count rows and 16-byte aligned first rows
   const bool vec = (reinterpret_cast<uintptr_t>(count) & 3) == 0 &&
                    (reinterpret_cast<uintptr_t>(first) & 15) == 0;
