@@ -31,7 +31,6 @@ sys.path.insert(0, ROOT)
 METRIC = "planned sample-accesses/sec (E×F×stats+plan) and % of HBM peak, 1 MI355X"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 DEFAULT_WORKLOAD = "imagenet22k"
-SIDE_STREAM_KERNELS = ("next_tile", "next_unpartition", "pad_rows")
 
 
 def algorithmic_bytes(job, M_w, D, fused):
@@ -266,13 +265,7 @@ def main():
     alg, A = algorithmic_bytes(job, M_w, D, args.path == "fused")
     per_kernel = {k: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps,
                       "avg_ms": ms / n} for k, (n, ms) in kernels.items()}
-    # In the fused call the next-use kernels run on a second stream beside the
-    # counting pass and the tier plan: their event-timed spans include the
-    # time they share the GPU, so the dominant kernel is taken among the
-    # kernels of the caller's stream.
-    side = SIDE_STREAM_KERNELS if args.path == "fused" else ()
-    dominant = max((k for k in per_kernel if k not in side),
-                   key=lambda k: per_kernel[k]["ms_per_step"])
+    dominant = max(per_kernel, key=lambda k: per_kernel[k]["ms_per_step"])
     dom = per_kernel[dominant]
     roofline = None
     if dominant in alg:

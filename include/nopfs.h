@@ -188,7 +188,6 @@ int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes,
  *   which=2  candidate records per worker in the tier plan's fast path, and
  *            reads per window in the next-use fast path
  *   which=3  fail the next internal scratch allocation (value 1)
- *   which=4  run all of nopfs_plan_job on the caller's stream (value 1)
  * Not thread-safe; meant for tests only. */
 int nopfs_debug_set(int which, int64_t value);
 

@@ -40,10 +40,10 @@ constexpr uint32_t kMaxWindows = 8192;  // sample windows per worker
 // Tuning knobs (measured on MI355X; see the benchmark notes). Every value
 // gives identical results; only speed changes.
 #ifndef NOPFS_STATS_THREADS
-#define NOPFS_STATS_THREADS 256
+#define NOPFS_STATS_THREADS 512
 #endif
 #ifndef NOPFS_STATS_WS
-#define NOPFS_STATS_WS 12
+#define NOPFS_STATS_WS 13
 #endif
 #ifndef NOPFS_NEXT_THREADS
 #define NOPFS_NEXT_THREADS 256
@@ -679,8 +679,9 @@ int launch_stats(const SegParams& p, const uint32_t* Pk, const uint16_t* OT, uin
                       first, ntiles, ent, base, num, classes);
 }
 
-// Window width of the next-use pass: about three quarters of the fast-path
-// capacity of reads per window.
+// Window width of the next-use pass: the widest whose expected reads stay
+// within three quarters of the fast-path capacity (windows that overflow it
+// take the epoch-serial path).
 int next_ws(const Shape& s) {
   const double reads_per_sample = double(s.M_max) / double(s.F);
   int ws = 0;
@@ -755,8 +756,7 @@ int next_impl(const nopfs_job* job, const int32_t* R, int32_t* next, hipStream_t
 }
 
 int access_fused(const Shape& s, const int32_t* R, const ClassTable* classes, uint8_t* count,
-                 int32_t* first, int32_t* next, CompactCells* cc, Scratch& keep, SideWork& side,
-                 hipStream_t side_st, hipStream_t st) {
+                 int32_t* first, int32_t* next, CompactCells* cc, Scratch& keep, hipStream_t st) {
   int rc;
   const SegParams ps = seg_params(s, NOPFS_STATS_WS);
   const SegParams pn = next_params(s);
@@ -764,22 +764,19 @@ int access_fused(const Shape& s, const int32_t* R, const ClassTable* classes, ui
   uint16_t *OT, *OTn;
   int32_t* nextP;
   if ((rc = run_partition(ps, R, keep, &Pk, &OT, st))) return rc;
-  // the next-use pass shares the partition when it uses the same windows
-  Pn = Pk;
-  OTn = OT;
-  if (pn.ws != ps.ws)
-    if ((rc = run_partition(pn, R, keep, &Pn, &OTn, st))) return rc;
   cc->ws = ps.ws;
   cc->nbk = ps.nbk;
   if ((rc = keep.alloc_n(&cc->ent, size_t(s.N * s.M_max)))) return rc;
   if ((rc = keep.alloc_n(&cc->base, size_t(s.N) * ps.nbk))) return rc;
   if ((rc = keep.alloc_n(&cc->num, size_t(s.N) * ps.nbk))) return rc;
+  if ((rc = launch_stats(ps, Pk, OT, count, first, cc, classes, st))) return rc;
+  // the next-use pass shares the partition when it uses the same windows
+  Pn = Pk;
+  OTn = OT;
+  if (pn.ws != ps.ws)
+    if ((rc = run_partition(pn, R, keep, &Pn, &OTn, st))) return rc;
   if ((rc = keep.alloc_n(&nextP, size_t(s.N * s.M_max)))) return rc;
-  // next uses (read-heavy, latency-bound) run beside the counting pass and
-  // the tier plan (write-heavy), which they do not feed
-  if ((rc = side.begin())) return rc;
-  if ((rc = launch_next(pn, Pn, OTn, nextP, next, side_st))) return rc;
-  return launch_stats(ps, Pk, OT, count, first, cc, classes, st);
+  return launch_next(pn, Pn, OTn, nextP, next, st);
 }
 
 }  // namespace nopfs

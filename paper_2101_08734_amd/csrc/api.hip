@@ -48,40 +48,9 @@ int make_shape(const nopfs_job* job, Shape* s) {
 }
 
 // ---------------------------------------------------------------- scratch --
-static int64_t g_debug[5] = {0, 0, 0, 0, 0};
+static int64_t g_debug[4] = {0, 0, 0, 0};
 
-int64_t debug_value(int which) { return (which >= 0 && which < 5) ? g_debug[which] : 0; }
-
-int side_stream(hipStream_t* s) {
-  static std::mutex mu;
-  static hipStream_t streams[64] = {};
-  int dev = 0;
-  NOPFS_HIP(hipGetDevice(&dev));
-  if (dev < 0 || dev >= 64) return fail(NOPFS_EDEVICE, "device index out of range");
-  std::lock_guard<std::mutex> g(mu);
-  if (!streams[dev]) NOPFS_HIP(hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking));
-  *s = streams[dev];
-  return NOPFS_OK;
-}
-
-int SideWork::begin() {
-  if (main_ == side_) return NOPFS_OK;  // one stream: already in order
-  NOPFS_HIP(hipEventCreateWithFlags(&ev_[0], hipEventDisableTiming));
-  NOPFS_HIP(hipEventCreateWithFlags(&ev_[1], hipEventDisableTiming));
-  NOPFS_HIP(hipEventRecord(ev_[0], main_));
-  active_ = true;  // from here on the destructor joins
-  NOPFS_HIP(hipStreamWaitEvent(side_, ev_[0], 0));
-  return NOPFS_OK;
-}
-
-SideWork::~SideWork() {
-  if (active_) {
-    (void)hipEventRecord(ev_[1], side_);
-    (void)hipStreamWaitEvent(main_, ev_[1], 0);
-  }
-  for (hipEvent_t e : ev_)
-    if (e) (void)hipEventDestroy(e);
-}
+int64_t debug_value(int which) { return (which >= 0 && which < 4) ? g_debug[which] : 0; }
 
 bool take_alloc_failure() {
   if (g_debug[3]) {
@@ -274,7 +243,7 @@ int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes, void* hip_
 }
 
 int nopfs_debug_set(int which, int64_t value) {
-  if (which < 1 || which > 4 || value < 0) return NOPFS_EINVAL;
+  if (which < 1 || which > 3 || value < 0) return NOPFS_EINVAL;
   g_debug[which] = value;
   return NOPFS_OK;
 }

@@ -82,25 +82,6 @@ int launch(const char* name, Kernel k, dim3 grid, dim3 block, size_t shmem,
   return NOPFS_OK;
 }
 
-// A second stream on the current device (non-blocking, default priority),
-// created once per device, for work that may run beside the caller's stream.
-int side_stream(hipStream_t* s);
-
-// Runs the work enqueued on `side` beside `main`: the constructor makes
-// `side` wait for what `main` has enqueued so far, the destructor makes
-// `main` wait for everything enqueued on `side` (also on error returns, so
-// buffers freed on `main` afterwards are no longer in use).
-class SideWork {
- public:
-  SideWork(hipStream_t main, hipStream_t side) : main_(main), side_(side) {}
-  ~SideWork();
-  int begin();  // NOPFS_OK or EDEVICE
- private:
-  hipStream_t main_, side_;
-  hipEvent_t ev_[2] = {nullptr, nullptr};
-  bool active_ = false;
-};
-
 // Debug overrides (nopfs_debug_set).
 int64_t debug_value(int which);
 bool take_alloc_failure();

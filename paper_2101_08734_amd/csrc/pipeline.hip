@@ -2,10 +2,9 @@
 // nopfs_access_streams, nopfs_access_stats, nopfs_reuse_next and
 // nopfs_tier_plan called in order; inside, the counting pass and the
 // next-use pass share one partition of the streams when their sample
-// windows agree, the next-use kernels run on a second stream beside the
-// counting pass and the tier plan, and the counting pass lists each worker's
-// read cells so the tier plan reads that list instead of the dense count and
-// first tables.
+// windows agree, and the counting pass lists each worker's read cells (bin
+// and offset, 4 bytes) so the tier plan reads that list instead of the dense
+// count and first tables.
 #include <new>
 
 #include "pipeline.hpp"
@@ -28,9 +27,6 @@ int plan_job_impl(const nopfs_job* job, const int64_t* sizes, const int64_t* cap
     if ((rc = stats_impl(job, R, count, first, st))) return rc;
     return plan_impl(job, count, first, sizes, caps, J, tier, used, st);
   }
-  hipStream_t side_st = st;  // test hook 4: everything on the caller's stream
-  if (debug_value(4) == 0)
-    if ((rc = side_stream(&side_st))) return rc;
   Scratch keep(st);
   CompactPlan* cp = nullptr;
   struct FreePlan {
@@ -41,10 +37,8 @@ int plan_job_impl(const nopfs_job* job, const int64_t* sizes, const int64_t* cap
   } free_plan{cp};
   const ClassTable* classes = nullptr;
   if ((rc = compact_plan_prepare(s, caps, J, keep, st, &cp, &classes))) return rc;
-  SideWork side(st, side_st);  // joins before `keep` frees its buffers
   CompactCells cc;
-  if ((rc = access_fused(s, R, classes, count, first, next, &cc, keep, side, side_st, st)))
-    return rc;
+  if ((rc = access_fused(s, R, classes, count, first, next, &cc, keep, st))) return rc;
   return compact_plan_run(cp, cc, count, first, sizes, tier, used, st);
 }
 

@@ -44,12 +44,11 @@ struct CompactCells {
 };
 
 // Counting pass, first reads and next uses of R (the stages of
-// nopfs_access_stats and nopfs_reuse_next) that also fills *cc. The next-use
-// kernels go on `side_st` after side.begin(); every buffer comes from `keep`,
-// which the caller frees only after `side` has joined. Requires M_max > 0.
+// nopfs_access_stats and nopfs_reuse_next); the counting pass also fills *cc,
+// binning the read cells with `classes`. Scratch that must outlive the call
+// (the list) is taken from `keep`. Requires M_max > 0.
 int access_fused(const Shape& s, const int32_t* R, const ClassTable* classes, uint8_t* count,
-                 int32_t* first, int32_t* next, CompactCells* cc, Scratch& keep, SideWork& side,
-                 hipStream_t side_st, hipStream_t st);
+                 int32_t* first, int32_t* next, CompactCells* cc, Scratch& keep, hipStream_t st);
 
 // Tier plan (the stage of nopfs_tier_plan) from the compact list, in two
 // steps: prepare() checks the arguments, allocates from `keep` and fills the

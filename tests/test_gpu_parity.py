@@ -22,24 +22,16 @@ def _gpu():
         pytest.skip("no GPU")
     nopfs.lib()
     yield
-    for which in (1, 2, 3, 4):
+    for which in (1, 2, 3):
         nopfs.debug_set(which, 0)
 
 
-# four stage calls; nopfs_plan_job; nopfs_plan_job kept on one stream (hook 4)
-PATHS = ["staged", "fused", "fused_one_stream"]
+PATHS = ["staged", "fused"]  # four stage calls, or nopfs_plan_job
 
 
 def gpu_pipeline(job, sizes, caps, path="staged"):
     s = torch.from_numpy(sizes).cuda()
-    if path == "staged":
-        out = nopfs.plan(job, s, caps)
-    else:
-        nopfs.debug_set(4, 1 if path == "fused_one_stream" else 0)
-        try:
-            out = nopfs.plan_job(job, s, caps)
-        finally:
-            nopfs.debug_set(4, 0)
+    out = nopfs.plan(job, s, caps) if path == "staged" else nopfs.plan_job(job, s, caps)
     torch.cuda.synchronize()
     return {k: v.cpu().numpy() for k, v in out.items()}
 
