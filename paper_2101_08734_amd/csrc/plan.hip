@@ -767,7 +767,11 @@ plan_btier(PlanArgs a, const int32_t* __restrict__ ranges, int8_t* __restrict__ 
 // then the list entries.
 constexpr int kWriteThreads = 256;
 constexpr int kWriteWin = 8192;  // cells held in LDS at once
-constexpr int kWriteEnt = 4;     // list entries per thread loaded up front
+#ifndef NOPFS_WRITE_ENT
+#define NOPFS_WRITE_ENT 6
+#endif
+constexpr int kWriteEnt = NOPFS_WRITE_ENT;  // list entries per thread loaded up front
+
 constexpr uint32_t kBt1Max = ((kBins1Budget + 256 + 15) / 16) * 16;  // class >= 1 bins, padded
 
 template <bool kVec>
