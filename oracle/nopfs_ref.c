@@ -347,6 +347,81 @@ int nopfs_ref_tier_plan(const nopfs_ref_job* job, const uint8_t* count,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Prefetch order (Design: a worker fills each storage class in the order it */
+/* will first need the samples -- the first rule of optimal prefetching of   */
+/* I/O Access Patterns, fetch the next sample of R that is not cached).      */
+/* Walk R_i; at the first read of a sample placed in tier j, append it to    */
+/* tier j's queue.                                                           */
+/* ------------------------------------------------------------------------ */
+int nopfs_ref_prefetch_order(const nopfs_ref_job* job, const int32_t* R,
+                             const int32_t* first, const int8_t* tier, int32_t J,
+                             int32_t* order, int64_t* qlen) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if ((!R && M_max > 0) || !first || !tier || !qlen || (!order && M_max > 0)) return REF_EINVAL;
+  if (J < 1) return REF_EINVAL;
+  if (J > 127) return REF_ERANGE;
+  int64_t F = job->F;
+  for (int64_t i = 0; i < job->N; ++i) {
+    const int32_t* Ri = R ? R + i * M_max : NULL;
+    int64_t Mi = job->E * epoch_len(job, i);
+    /* pass 1: queue lengths; pass 2: each queue in stream order */
+    for (int32_t j = 0; j < J; ++j) qlen[i * J + j] = 0;
+    for (int64_t f = 0; f < Mi; ++f) {
+      int32_t k = Ri[f];
+      int8_t t = tier[i * F + k];
+      if (first[i * F + k] == f && t >= 0 && t < J) qlen[i * J + t]++;
+    }
+    int64_t start[128];
+    int64_t acc = 0;
+    for (int32_t j = 0; j < J; ++j) {
+      start[j] = acc;
+      acc += qlen[i * J + j];
+    }
+    for (int64_t f = 0; f < Mi; ++f) {
+      int32_t k = Ri[f];
+      int8_t t = tier[i * F + k];
+      if (first[i * F + k] == f && t >= 0 && t < J) order[i * M_max + start[t]++] = k;
+    }
+    for (int64_t q = acc; q < M_max; ++q) order[i * M_max + q] = -1;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Staging schedule (Design: the staging buffer is filled in the order of R  */
+/* and a sample is dropped as soon as it has been read; Implementation: the  */
+/* buffer is filled circularly). While the worker has read positions < f,    */
+/* the buffer holds the samples at f, f+1, ...; the sample at h can be       */
+/* fetched once those at f..h fit in d0 bytes. The window's left end only    */
+/* moves forward as h grows (sizes are >= 1), so one running sum does.       */
+/* ------------------------------------------------------------------------ */
+int nopfs_ref_staging_schedule(const nopfs_ref_job* job, const int32_t* R,
+                               const int64_t* sizes, int64_t d0, int32_t* fill) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if ((!R && M_max > 0) || !sizes || (!fill && M_max > 0)) return REF_EINVAL;
+  if (d0 < 0) return REF_EINVAL;
+  for (int64_t i = 0; i < job->N; ++i) {
+    const int32_t* Ri = R ? R + i * M_max : NULL;
+    int64_t Mi = job->E * epoch_len(job, i);
+    int64_t f = 0, sum = 0; /* sum of sizes at positions f..h */
+    for (int64_t h = 0; h < Mi; ++h) {
+      sum += sizes[Ri[h]];
+      while (sum > d0 && f < h) {
+        sum -= sizes[Ri[f]];
+        f++;
+      }
+      fill[i * M_max + h] = (int32_t)f; /* f == h: alone, or alone too large */
+    }
+    for (int64_t h = Mi; h < M_max; ++h) fill[i * M_max + h] = -1;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Sampled columns. The position of sample s in epoch e is, by definition   */
 /* of the sorted order, the number of samples whose (key, id) is smaller.   */
 /* Everything else for s follows from its positions in the E epochs.        */

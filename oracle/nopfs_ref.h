@@ -75,6 +75,21 @@ int nopfs_ref_tier_plan(const nopfs_ref_job* job, const uint8_t* count,
                         const int64_t* caps, int32_t J, int8_t* tier,
                         int64_t* used);
 
+/* Prefetch order per cache tier: for worker i and tier j in [0, J), the
+ * samples k with tier[i][k] == j that worker i reads, each once, in order of
+ * first read. order[N][M_max]: tier 0's queue, then tier 1's, ..., then -1;
+ * qlen[N][J]: the queue lengths. */
+int nopfs_ref_prefetch_order(const nopfs_ref_job* job, const int32_t* R,
+                             const int32_t* first, const int8_t* tier, int32_t J,
+                             int32_t* order, int64_t* qlen);
+
+/* Staging-buffer schedule for a buffer of d0 bytes: fill[i][h] is the
+ * smallest f <= h such that the samples at stream positions f..h of worker i
+ * fit together (sum of sizes <= d0), or h when the sample at h alone is
+ * larger than d0; -1 in padding. */
+int nopfs_ref_staging_schedule(const nopfs_ref_job* job, const int32_t* R,
+                               const int64_t* sizes, int64_t d0, int32_t* fill);
+
 /* Per-sample columns for S chosen samples, computed one sample at a time
  * from the definition of the shuffle (for checks at sizes where the full
  * oracle is too slow):

@@ -65,12 +65,15 @@ def lib():
         L.nopfs_ref_tier_plan.argtypes = [jp, P, P, P, P, ctypes.c_int32, P, P]
         L.nopfs_ref_sample_columns.argtypes = [jp, P, ctypes.c_int64, P, P, P,
                                                P, P, P]
+        L.nopfs_ref_prefetch_order.argtypes = [jp, P, P, P, ctypes.c_int32, P, P]
+        L.nopfs_ref_staging_schedule.argtypes = [jp, P, P, ctypes.c_int64, P]
         for name in ("nopfs_ref_stream_shape", "nopfs_ref_epoch_keys",
                      "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms",
                      "nopfs_ref_access_streams", "nopfs_ref_access_stats",
                      "nopfs_ref_reuse_next", "nopfs_ref_tier_plan",
                      "nopfs_ref_sample_columns", "nopfs_ref_access_stats_rows",
-                     "nopfs_ref_reuse_next_rows"):
+                     "nopfs_ref_reuse_next_rows", "nopfs_ref_prefetch_order",
+                     "nopfs_ref_staging_schedule"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -190,6 +193,28 @@ def tier_plan(job: RefJob, count, first, sizes, caps):
                                      len(caps), _ptr(tier), _ptr(used)),
            "tier_plan")
     return tier, used
+
+
+def prefetch_order(job: RefJob, R, first, tier, J):
+    """order[N][M_max] (tier 0's queue, tier 1's, ..., then -1), qlen[N][J]."""
+    R = np.ascontiguousarray(R, dtype=np.int32)
+    first = np.ascontiguousarray(first, dtype=np.int32)
+    tier = np.ascontiguousarray(tier, dtype=np.int8)
+    order = np.empty_like(R)
+    qlen = np.empty((job.N, J), np.int64)
+    _check(lib().nopfs_ref_prefetch_order(ctypes.byref(job), _ptr(R), _ptr(first), _ptr(tier),
+                                          int(J), _ptr(order), _ptr(qlen)), "prefetch_order")
+    return order, qlen
+
+
+def staging_schedule(job: RefJob, R, sizes, d0):
+    """fill[N][M_max]: first position from which the sample at h may be staged."""
+    R = np.ascontiguousarray(R, dtype=np.int32)
+    sizes = np.ascontiguousarray(sizes, dtype=np.int64)
+    fill = np.empty_like(R)
+    _check(lib().nopfs_ref_staging_schedule(ctypes.byref(job), _ptr(R), _ptr(sizes), int(d0),
+                                            _ptr(fill)), "staging_schedule")
+    return fill
 
 
 def sample_columns(job: RefJob, samples):

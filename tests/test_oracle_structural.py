@@ -1,7 +1,8 @@
 """Hand-worked structural examples (tests/golden/structural_example.json).
 
-The permutations are given, so these pin the shard, stats, next-use and plan
-stages of the oracle independently of the keys."""
+The permutations are given, so these pin the shard, stats, next-use, plan,
+prefetch-order and staging-schedule stages of the oracle independently of the
+keys."""
 import json
 import os
 
@@ -26,3 +27,9 @@ def test_structural_example(oracle, case):
                                   np.array(case["caps"]))
     np.testing.assert_array_equal(tier, case["tier"])
     np.testing.assert_array_equal(used, case["used"])
+    order, qlen = oracle.prefetch_order(job, R, first, tier, len(case["caps"]))
+    np.testing.assert_array_equal(order, case["prefetch_order"])
+    np.testing.assert_array_equal(qlen, case["qlen"])
+    for st in case["staging"]:
+        fill = oracle.staging_schedule(job, R, np.array(case["sizes"]), st["d0"])
+        np.testing.assert_array_equal(fill, st["fill"], err_msg=f"d0={st['d0']}")
