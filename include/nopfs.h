@@ -154,6 +154,50 @@ int nopfs_plan_job(const nopfs_job* job, const int64_t* sizes, const int64_t* ca
                    int32_t J, int32_t* R, uint8_t* count, int32_t* first, int32_t* next,
                    int8_t* tier, int64_t* used, void* hip_stream);
 
+/* Prefetch order of the cache tiers (section 5.1: samples are always fetched
+ * in their order of access, following the first of the prefetching rules of
+ * section 3; a worker fills each storage class with the samples placed
+ * there). For worker i, tier j's queue lists the samples k with
+ * tier[i][k] == j that the worker reads, by increasing first[i][k]; the
+ * queues are concatenated fastest tier first and the row is padded with -1.
+ * Samples placed in tier j that the worker never reads are not listed (they
+ * can be fetched after the queue, in any order).
+ *   R:     int32 [N][M_max], as for nopfs_access_stats.
+ *   first: int32 [N][F], as written by nopfs_access_stats for this R
+ *          (precondition: first[i][k] == f >= 0 exactly when f is the first
+ *          position of k in R_i; other contents give unspecified but
+ *          in-bounds results).
+ *   tier:  int8 [N][F], a placement (as written by nopfs_tier_plan); entries
+ *          outside [0, J) are not queued.
+ *   J:     number of cache tiers, 1 <= J <= 127.
+ *   order: int32 [N][M_max], output: queue of tier 0, then tier 1, ..., then -1.
+ *   qlen:  int64 [N][J], output: queue lengths (tier j's queue starts at
+ *          the sum of qlen[i][0..j-1]).
+ * Scratch: about one byte per stream position. Errors: EINVAL (also J < 1),
+ * ERANGE (J > 127), ENOMEM, EDEVICE. */
+int nopfs_prefetch_order(const nopfs_job* job, const int32_t* R, const int32_t* first,
+                         const int8_t* tier, int32_t J, int32_t* order, int64_t* qlen,
+                         void* hip_stream);
+
+/* Staging-buffer schedule (section 5.1: samples enter the staging buffer in
+ * access order and leave it as soon as they are read; section 5.2: the
+ * buffer is filled circularly). While worker i has read the positions
+ * before f, its buffer of d0 bytes holds the samples at positions f, f+1, ...
+ * of R_i that fit; the sample at position h can be fetched once the worker
+ * has read position fill[i][h] - 1:
+ *   fill[i][h] = smallest f <= h with sizes[R_i[f]] + ... + sizes[R_i[h]] <= d0,
+ *                or h when sizes[R_i[h]] alone exceeds d0;
+ * -1 in padding. fill never decreases along a row.
+ *   R:     int32 [N][M_max], as for nopfs_access_stats.
+ *   sizes: int64 [F] sample sizes in bytes, each >= 1 (precondition; other
+ *          values give unspecified but in-bounds results).
+ *   d0:    staging buffer capacity in bytes, >= 0.
+ *   fill:  int32 [N][M_max], output.
+ * Scratch: about 8 bytes per stream position. Errors: EINVAL (also d0 < 0),
+ * ERANGE, ENOMEM, EDEVICE. */
+int nopfs_staging_schedule(const nopfs_job* job, const int32_t* R, const int64_t* sizes,
+                           int64_t d0, int32_t* fill, void* hip_stream);
+
 /* Static description of a status code. Never NULL. */
 const char* nopfs_strerror(int code);
 
@@ -188,6 +232,8 @@ int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes,
  *   which=2  candidate records per worker in the tier plan's fast path, and
  *            reads per window in the next-use fast path
  *   which=3  fail the next internal scratch allocation (value 1)
+ *   which=4  longest range of buffer starts the staging schedule keeps in
+ *            LDS per chunk (wider ranges take the global-memory search)
  * Not thread-safe; meant for tests only. */
 int nopfs_debug_set(int which, int64_t value);
 

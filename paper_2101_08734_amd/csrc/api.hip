@@ -48,9 +48,9 @@ int make_shape(const nopfs_job* job, Shape* s) {
 }
 
 // ---------------------------------------------------------------- scratch --
-static int64_t g_debug[4] = {0, 0, 0, 0};
+static int64_t g_debug[5] = {0, 0, 0, 0, 0};
 
-int64_t debug_value(int which) { return (which >= 0 && which < 4) ? g_debug[which] : 0; }
+int64_t debug_value(int which) { return (which >= 0 && which < 5) ? g_debug[which] : 0; }
 
 bool take_alloc_failure() {
   if (g_debug[3]) {
@@ -243,7 +243,7 @@ int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes, void* hip_
 }
 
 int nopfs_debug_set(int which, int64_t value) {
-  if (which < 1 || which > 3 || value < 0) return NOPFS_EINVAL;
+  if (which < 1 || which > 4 || value < 0) return NOPFS_EINVAL;
   g_debug[which] = value;
   return NOPFS_OK;
 }

@@ -68,6 +68,8 @@ def lib() -> ctypes.CDLL:
             "nopfs_reuse_next": [jp, P, P, P],
             "nopfs_tier_plan": [jp, P, P, P, P, I32, P, P, P],
             "nopfs_plan_job": [jp, P, P, I32, P, P, P, P, P, P, P],
+            "nopfs_prefetch_order": [jp, P, P, P, I32, P, P, P],
+            "nopfs_staging_schedule": [jp, P, P, I64, P, P],
             "nopfs_profile_enable": [ctypes.c_int],
             "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
                                     ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)],
@@ -87,7 +89,8 @@ def lib() -> ctypes.CDLL:
 
 
 EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_stats",
-            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_strerror",
+            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_prefetch_order",
+            "nopfs_staging_schedule", "nopfs_strerror",
             "nopfs_last_error", "nopfs_profile_enable", "nopfs_profile_query",
             "nopfs_calibration_copy", "nopfs_debug_set")
 
@@ -212,6 +215,43 @@ def plan_job(job: Job, sizes, caps, out=None, stream=None):
                                 J, _ptr(o["R"]), _ptr(o["count"]), _ptr(o["first"]), _ptr(o["next"]),
                                 _ptr(o["tier"]), _ptr(o["used"]), _stream(stream)), "nopfs_plan_job")
     return o
+
+
+def prefetch_order(job: Job, R, first, tier, J, order=None, qlen=None, stream=None):
+    """Per-tier prefetch queues (nopfs_prefetch_order): order [N][M_max] int32
+    (tier 0's queue, tier 1's, ..., then -1) and qlen [N][J] int64."""
+    _, M, _ = stream_shape(job)
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    _device_tensor(first, torch.int32, (job.N, job.F), "first")
+    _device_tensor(tier, torch.int8, (job.N, job.F), "tier")
+    J = int(J)
+    if order is None:
+        order = torch.empty((job.N, M), dtype=torch.int32, device="cuda")
+    if qlen is None:
+        qlen = torch.empty((job.N, max(J, 1)), dtype=torch.int64, device="cuda")
+    _device_tensor(order, torch.int32, (job.N, M), "order")
+    _device_tensor(qlen, torch.int64, (job.N, max(J, 1)), "qlen")
+    j = job.c()
+    _check(lib().nopfs_prefetch_order(ctypes.byref(j), _ptr(R), _ptr(first), _ptr(tier), J,
+                                      _ptr(order), _ptr(qlen), _stream(stream)),
+           "nopfs_prefetch_order")
+    return order, qlen
+
+
+def staging_schedule(job: Job, R, sizes, d0, fill=None, stream=None):
+    """Staging-buffer schedule (nopfs_staging_schedule): fill [N][M_max] int32,
+    the first stream position from which each read's sample may be staged
+    into a buffer of d0 bytes (-1 in padding)."""
+    _, M, _ = stream_shape(job)
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    _device_tensor(sizes, torch.int64, (job.F,), "sizes")
+    if fill is None:
+        fill = torch.empty((job.N, M), dtype=torch.int32, device="cuda")
+    _device_tensor(fill, torch.int32, (job.N, M), "fill")
+    j = job.c()
+    _check(lib().nopfs_staging_schedule(ctypes.byref(j), _ptr(R), _ptr(sizes), int(d0), _ptr(fill),
+                                        _stream(stream)), "nopfs_staging_schedule")
+    return fill
 
 
 def plan(job: Job, sizes, caps, stream=None):

@@ -14,6 +14,11 @@ Stand-ins (the datasets themselves are not used):
   imagenet1k_256 -- the same dataset over 256 workers
   imagenet22k -- ImageNet-22k, 14,197,103 samples, N=256 (largest)
   cosmoflow   -- CosmoFlow, 262,144 samples of 16 MiB, N=1024
+
+Staging-buffer capacities (d0, the input of the staging schedule): 5 GB for
+the ImageNet stand-ins (the simulated ImageNet-22k configuration fixes the
+staging buffer at 5 GB), 5 GiB for CosmoFlow (the per-rank staging buffer of
+the evaluation runs), 20 MB for the sanity case.
 """
 from __future__ import annotations
 
@@ -51,7 +56,7 @@ class Workload:
 WORKLOADS = {
     "small": Workload("small", 1, 10_000, 5, 4, 16, 1, (100e6, 500e6),
                       size_mu=math.log(110e3), size_sigma=0.5,
-                      size_lo=1_000, size_hi=2_000_000),
+                      size_lo=1_000, size_hi=2_000_000, staging=20e6),
     "imagenet1k": Workload("imagenet1k", 2, 1_281_167, 90, 16, 32, 1,
                            (64e9, 800e9), size_mu=math.log(110e3),
                            size_sigma=0.6, size_lo=1_000, size_hi=15_000_000,
@@ -59,12 +64,13 @@ WORKLOADS = {
     "imagenet1k_256": Workload("imagenet1k_256", 3, 1_281_167, 90, 256, 32, 1,
                                (16e9, 200e9), size_mu=math.log(110e3),
                                size_sigma=0.6, size_lo=1_000,
-                               size_hi=15_000_000),
+                               size_hi=15_000_000, staging=5e9),
     "imagenet22k": Workload("imagenet22k", 4, 14_197_103, 40, 256, 32, 1,
                             (64e9, 400e9), size_mu=math.log(90e3),
-                            size_sigma=0.7, size_lo=1_000, size_hi=20_000_000),
+                            size_sigma=0.7, size_lo=1_000, size_hi=20_000_000,
+                            staging=5e9),
     "cosmoflow": Workload("cosmoflow", 5, 262_144, 40, 1_024, 1, 1,
-                          (32e9, 256e9), fixed_size=16_777_216),
+                          (32e9, 256e9), fixed_size=16_777_216, staging=5 * 2**30),
 }
 
 ORDER = ["small", "imagenet1k", "imagenet1k_256", "imagenet22k", "cosmoflow"]

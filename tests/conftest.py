@@ -20,3 +20,12 @@ def oracle():
     from oracle import ref
     ref.build()
     return ref
+
+
+@pytest.fixture(scope="session")
+def imagenet1k_expected(oracle):
+    """The oracle's whole pipeline at ImageNet-1k size (N=16), shared by the
+    full-size GPU tests."""
+    from paper_2101_08734_amd import workloads as wl
+    w = wl.WORKLOADS["imagenet1k"]
+    return oracle.full_pipeline(oracle.make_job(*w.job_tuple()), wl.sizes(w), wl.caps(w))

@@ -88,12 +88,6 @@ def check_plan_rows(job, sizes, caps, out, rows):
     inv.check_plan(c, f, sizes, caps, t, u)
 
 
-@pytest.fixture(scope="module")
-def imagenet1k_expected(oracle):
-    w = wl.WORKLOADS["imagenet1k"]
-    return oracle.full_pipeline(oracle.make_job(*w.job_tuple()), wl.sizes(w), wl.caps(w))
-
-
 @pytest.mark.parametrize("path", PATHS)
 def test_imagenet1k_full(imagenet1k_expected, path):
     w = wl.WORKLOADS["imagenet1k"]
