@@ -64,10 +64,19 @@ __global__ void __launch_bounds__(256) pf_zero(uint4* __restrict__ p, int64_t n1
   for (; t < n16; t += stride) p[t] = make_uint4(0u, 0u, 0u, 0u);
 }
 
+// Mark rows have a pitch of mp bytes (a multiple of 16). Marks are plain
+// byte stores: atomic ORs on the 4-byte words (executed in L2) measured
+// twice as slow.
 __device__ __forceinline__ void mark_cell(int32_t f, int32_t t, int64_t M_max, int32_t J,
                                           uint8_t* __restrict__ mr) {
   // first reads outside the row or tiers outside [0, J) are not queued
   if (f >= 0 && f < M_max && t >= 0 && t < J) mr[f] = uint8_t(t + 1);
+}
+
+// Mark byte -> tier code in [0, J] (codes above J, which no valid mark
+// holds, are dropped so every queue slot stays inside the row).
+__device__ __forceinline__ uint32_t mark_code(uint32_t m, int32_t J) {
+  return m <= uint32_t(J) ? m : 0u;
 }
 
 // Tile (i, sl) covers the flat cells [i*F + sl*kMarkTile, ...) of row i. The
@@ -78,7 +87,7 @@ __device__ __forceinline__ void mark_cell(int32_t f, int32_t t, int64_t M_max, i
 template <bool kVec>
 __global__ void __launch_bounds__(256)
 pf_mark(RowShape r, int32_t J, const int32_t* __restrict__ first, const int8_t* __restrict__ tier,
-        uint8_t* __restrict__ mark, uint32_t nslices, uint32_t ntiles) {
+        uint8_t* __restrict__ mark, int64_t mp, uint32_t nslices, uint32_t ntiles) {
   const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
   if (t >= ntiles) return;
   const int64_t i = t / nslices;
@@ -86,7 +95,7 @@ pf_mark(RowShape r, int32_t J, const int32_t* __restrict__ first, const int8_t* 
   const int64_t row0 = i * r.F;
   const int64_t lo = row0 + sl * kMarkTile;
   const int64_t hi = lo + kMarkTile < row0 + r.F ? lo + kMarkTile : row0 + r.F;
-  uint8_t* mr = mark + i * r.M_max;
+  uint8_t* mr = mark + i * mp;
   if (!kVec) {
     for (int64_t x = lo + threadIdx.x; x < hi; x += 256)
       mark_cell(first[x], tier[x], r.M_max, J, mr);
@@ -146,8 +155,8 @@ __device__ __forceinline__ bool pf_block(uint32_t nbw, uint32_t nblocks, int64_t
 
 // cnt layout: [N][nch][J]. Each wave counts one chunk; no workgroup barrier.
 __global__ void __launch_bounds__(256)
-pf_count(RowShape r, int32_t J, const uint8_t* __restrict__ mark, uint32_t nch, uint32_t nbw,
-         uint32_t nblocks, int32_t* __restrict__ cnt) {
+pf_count(RowShape r, int32_t J, const uint8_t* __restrict__ mark, int64_t mp, uint32_t nch,
+         uint32_t nbw, uint32_t nblocks, int32_t* __restrict__ cnt) {
   __shared__ uint32_t s_cnt[kPfWaves][kPfMaxJ];
   int64_t i;
   uint32_t cb;
@@ -157,13 +166,13 @@ pf_count(RowShape r, int32_t J, const uint8_t* __restrict__ mark, uint32_t nch, 
   if (c >= nch) return;
   for (int x = lane; x < J; x += 64) s_cnt[w][x] = 0;
   const int64_t Mi = row_len(r, i);
-  const uint8_t* mr = mark + i * r.M_max;
+  const uint8_t* mr = mark + i * mp;
   const int64_t f0 = int64_t(c) * kPfChunk + lane;
   uint32_t code[kPfSteps];
 #pragma unroll
   for (int u = 0; u < kPfSteps; ++u) {
     const int64_t f = f0 + int64_t(u) * 64;
-    code[u] = f < Mi ? mr[f] : 0u;
+    code[u] = f < Mi ? mark_code(mr[f], J) : 0u;
   }
 #pragma unroll
   for (int u = 0; u < kPfSteps; ++u) {
@@ -206,9 +215,10 @@ pf_scan(int32_t J, uint32_t nch, int32_t* __restrict__ cnt, int64_t* __restrict_
 }
 
 __global__ void __launch_bounds__(256)
-pf_write(RowShape r, int32_t J, const uint8_t* __restrict__ mark, const int32_t* __restrict__ R,
-         uint32_t nch, uint32_t nbw, uint32_t nblocks, const int32_t* __restrict__ slot0,
-         const int64_t* __restrict__ tot, int32_t* __restrict__ order) {
+pf_write(RowShape r, int32_t J, const uint8_t* __restrict__ mark, int64_t mp,
+         const int32_t* __restrict__ R, uint32_t nch, uint32_t nbw, uint32_t nblocks,
+         const int32_t* __restrict__ slot0, const int64_t* __restrict__ tot,
+         int32_t* __restrict__ order) {
   __shared__ int32_t s_run[kPfWaves][kPfMaxJ];
   int64_t i;
   uint32_t cb;
@@ -219,7 +229,7 @@ pf_write(RowShape r, int32_t J, const uint8_t* __restrict__ mark, const int32_t*
   const int32_t* sl = slot0 + (i * nch + c) * J;
   for (int x = lane; x < J; x += 64) s_run[w][x] = sl[x];
   const int64_t Mi = row_len(r, i);
-  const uint8_t* mr = mark + i * r.M_max;
+  const uint8_t* mr = mark + i * mp;
   const int32_t* Rr = R + i * r.M_max;
   int32_t* orow = order + i * r.M_max;
   const int64_t f0 = int64_t(c) * kPfChunk + lane;
@@ -227,7 +237,7 @@ pf_write(RowShape r, int32_t J, const uint8_t* __restrict__ mark, const int32_t*
 #pragma unroll
   for (int u = 0; u < kPfSteps; ++u) {
     const int64_t f = f0 + int64_t(u) * 64;
-    code[u] = f < Mi ? mr[f] : 0u;
+    code[u] = f < Mi ? mark_code(mr[f], J) : 0u;
   }
   int32_t k[kPfSteps];
 #pragma unroll
@@ -484,7 +494,8 @@ int prefetch_impl(const nopfs_job* job, const int32_t* R, const int32_t* first,
   int64_t* tot;
   int32_t* cnt;
   uint8_t* mark;
-  const int64_t nm16 = ceil_div(s.N * s.M_max, 16);
+  const int64_t mp = ceil_div(s.M_max, 16) * 16;  // mark row pitch
+  const int64_t nm16 = s.N * mp / 16;
   if ((rc = scr.alloc_n(&tot, size_t(s.N)))) return rc;
   if ((rc = scr.alloc_n(&cnt, size_t(s.N) * nch * size_t(J)))) return rc;
   if ((rc = scr.alloc_n(&mark, size_t(nm16) * 16))) return rc;
@@ -497,12 +508,12 @@ int prefetch_impl(const nopfs_job* job, const int32_t* R, const int32_t* first,
     const bool vec = (reinterpret_cast<uintptr_t>(first) & 15) == 0 &&
                      (reinterpret_cast<uintptr_t>(tier) & 3) == 0;
     rc = vec ? launch("pf_mark", pf_mark<true>, dim3(xcd_padded(ntiles)), dim3(256), 0, st, r, J,
-                      first, tier, mark, uint32_t(nslices), ntiles)
+                      first, tier, mark, mp, uint32_t(nslices), ntiles)
              : launch("pf_mark", pf_mark<false>, dim3(xcd_padded(ntiles)), dim3(256), 0, st, r, J,
-                      first, tier, mark, uint32_t(nslices), ntiles);
+                      first, tier, mark, mp, uint32_t(nslices), ntiles);
     if (rc) return rc;
     if ((rc = launch("pf_count", pf_count, dim3(xcd_padded(uint32_t(nblocks))), dim3(256), 0, st,
-                     r, J, (const uint8_t*)mark, nch, nbw, uint32_t(nblocks), cnt)))
+                     r, J, (const uint8_t*)mark, mp, nch, nbw, uint32_t(nblocks), cnt)))
       return rc;
   }
   if ((rc = launch("pf_scan", pf_scan, dim3(uint32_t(s.N)), dim3(1024), 0, st, J, nch, cnt, qlen,
@@ -510,8 +521,8 @@ int prefetch_impl(const nopfs_job* job, const int32_t* R, const int32_t* first,
     return rc;
   if (nm16 > 0 &&
       (rc = launch("pf_write", pf_write, dim3(xcd_padded(uint32_t(nblocks))), dim3(256), 0, st, r,
-                   J, (const uint8_t*)mark, R, nch, nbw, uint32_t(nblocks), (const int32_t*)cnt,
-                   (const int64_t*)tot, order)))
+                   J, (const uint8_t*)mark, mp, R, nch, nbw, uint32_t(nblocks),
+                   (const int32_t*)cnt, (const int64_t*)tot, order)))
     return rc;
   return NOPFS_OK;
 }
