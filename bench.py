@@ -6,6 +6,11 @@ preallocated; by default one nopfs_plan_job call (--path staged: the four
 stage calls). The metric is planned sample-accesses per second: the number of
 reads the job issues (A = N * E * L) over the device time of one step.
 
+After the timed steps, the per-tier prefetch queues and the staging
+schedule of the planned job (the step's outputs as inputs, the workload's
+staging-buffer capacity as d0) are timed the same way and reported under
+"schedule"; they are not part of the step.
+
 Prints ONE JSON line. Per-kernel durations come from HIP events recorded by
 the library around each of its launches, on the stream it launches on, over
 the timed steps. The dominant kernel's roofline uses the algorithmic bytes of
@@ -61,6 +66,24 @@ def algorithmic_bytes(job, M_w, D, fused):
         out["plan_hist"] = 5 * NF + 8 * job.F
         out["plan_write"] = 5 * NF + NF
     return out, A
+
+
+def schedule_algorithmic_bytes(job, M, M_w):
+    """Bytes the two schedule calls must move given the C ABI's dense
+    layouts, attributed to the kernel that moves them: A reads, N*F cells,
+    M_max positions per row. The prefetch order reads R once (its first reads
+    are R's), the tier of every cell, and writes the whole order table; the
+    staging schedule reads R once, each sample's size once and writes the
+    whole fill table. Everything else (the partition of R, codes and sizes in
+    partitioned order, per-chunk counts, scans and prefix sums, and the
+    second read of R for the queued samples) is the implementation's own
+    scratch traffic."""
+    A = int(sum(M_w))
+    NF = job.N * job.F
+    NM = job.N * M
+    prefetch = {"seg_partition": 4 * A, "pf_tile": NF, "pf_write": 4 * NM}
+    staging = {"seg_partition": 4 * A, "st_tile": 8 * job.F, "st_fill": 4 * NM}
+    return prefetch, staging
 
 
 def kernel_source_hash():
@@ -179,6 +202,67 @@ def cpu_baseline(w, sizes, caps, epochs=2, workers=2):
     }
 
 
+def roofline_of(workload, kernel, alg_bytes, avg_ms):
+    achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
+    return {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": committed_traffic(workload, kernel), "algorithmic_bytes": alg_bytes,
+            "avg_ms": round(avg_ms, 4)}
+
+
+def time_schedule(nopfs, torch, w, job, M, M_w, R, tier, sizes, caps, steps, warmup, stream):
+    """The per-tier prefetch queues and the staging schedule of the planned
+    job (the planning step's own outputs as inputs), each timed over `steps`
+    calls with HIP events on the stream the library launches on."""
+    J = len(caps)
+    d0 = int(w.staging)
+    dev = R.device
+    order = torch.empty((job.N, M), dtype=torch.int32, device=dev)
+    qlen = torch.empty((job.N, J), dtype=torch.int64, device=dev)
+    fill = torch.empty((job.N, M), dtype=torch.int32, device=dev)
+    calls = {
+        "prefetch_order": lambda: nopfs.prefetch_order(job, R, tier, J, order, qlen,
+                                                       stream=stream),
+        "staging_schedule": lambda: nopfs.staging_schedule(job, R, sizes, d0, fill, stream=stream),
+    }
+    for _ in range(warmup):
+        for f in calls.values():
+            f()
+    torch.cuda.synchronize()
+    Q = int(qlen.sum())
+    pf_alg, st_alg = schedule_algorithmic_bytes(job, M, M_w)
+    out = {"J": J, "d0_bytes": d0, "queued": Q}
+    for name, f in calls.items():
+        alg = pf_alg if name == "prefetch_order" else st_alg
+        nopfs.profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        nopfs.profile_enable(False)
+        ms = e0.elapsed_time(e1) / steps
+        kern = {k: {"ms_per_call": t / steps, "avg_ms": t / n}
+                for k, (n, t) in nopfs.profile_results().items()}
+        for k, v in kern.items():
+            if k in alg:
+                v["alg_GBps"] = round(alg[k] / (v["avg_ms"] * 1e-3) / 1e9, 1)
+        dominant = max(kern, key=lambda k: kern[k]["ms_per_call"])
+        total_alg = sum(alg.values())
+        out[name] = {
+            "ms_per_call": round(ms, 4),
+            "alg_bytes": total_alg,
+            "alg_GBps": round(total_alg / (ms * 1e-3) / 1e9, 1),
+            "kernels": {k: {kk: round(vv, 4) for kk, vv in v.items()} for k, v in kern.items()},
+            "roofline": (roofline_of(w.name, dominant, alg[dominant], kern[dominant]["avg_ms"])
+                         if dominant in alg else {"kernel": dominant, "algorithmic_bytes": 0}),
+        }
+        print(f"[bench] {name}: {ms:.3f} ms/call, dominant {dominant}", file=sys.stderr,
+              flush=True)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -188,6 +272,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--path", choices=["fused", "staged"], default="fused",
                     help="fused: one nopfs_plan_job call per step; staged: the four stage calls")
+    ap.add_argument("--no-schedule", action="store_true",
+                    help="skip timing the prefetch queues and staging schedule")
     ap.add_argument("--calibrate-bytes", type=int, default=1 << 30,
                     help="size of the calibration copy run after the timed steps")
     ap.add_argument("--rocprof-summary", metavar="DIR",
@@ -269,17 +355,16 @@ def main():
     dom = per_kernel[dominant]
     roofline = None
     if dominant in alg:
-        achieved = alg[dominant] / (dom["avg_ms"] * 1e-3) / 1e9
-        traffic = committed_traffic(w.name, dominant)
-        roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": traffic, "algorithmic_bytes": alg[dominant],
-                    "avg_ms": round(dom["avg_ms"], 4)}
+        roofline = roofline_of(w.name, dominant, alg[dominant], dom["avg_ms"])
     for k, v in per_kernel.items():
         if k in alg:
             v["alg_GBps"] = round(alg[k] / (v["avg_ms"] * 1e-3) / 1e9, 1)
     print("[bench] kernels: " + json.dumps(per_kernel), file=sys.stderr, flush=True)
+
+    schedule = None
+    if not args.no_schedule:
+        schedule = time_schedule(nopfs, torch, w, job, M, M_w, R, tier, sizes, caps, args.steps,
+                                 args.warmup, stream)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -304,6 +389,7 @@ def main():
                    "tier_caps_bytes": caps, "parallelism": "none (all N workers on one GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "schedule": schedule,
     }
     print(json.dumps(line), flush=True)
 

@@ -158,26 +158,23 @@ int nopfs_plan_job(const nopfs_job* job, const int64_t* sizes, const int64_t* ca
  * in their order of access, following the first of the prefetching rules of
  * section 3; a worker fills each storage class with the samples placed
  * there). For worker i, tier j's queue lists the samples k with
- * tier[i][k] == j that the worker reads, by increasing first[i][k]; the
- * queues are concatenated fastest tier first and the row is padded with -1.
- * Samples placed in tier j that the worker never reads are not listed (they
- * can be fetched after the queue, in any order).
+ * tier[i][k] == j that the worker reads, by increasing first read (the
+ * smallest f with R_i[f] == k); the queues are concatenated fastest tier
+ * first and the row is padded with -1. Samples placed in tier j that the
+ * worker never reads are not listed (they can be fetched after the queue, in
+ * any order). First reads are taken from R itself, so the dense first-read
+ * table is not an argument.
  *   R:     int32 [N][M_max], as for nopfs_access_stats.
- *   first: int32 [N][F], as written by nopfs_access_stats for this R
- *          (precondition: first[i][k] == f >= 0 exactly when f is the first
- *          position of k in R_i; other contents give unspecified but
- *          in-bounds results).
  *   tier:  int8 [N][F], a placement (as written by nopfs_tier_plan); entries
  *          outside [0, J) are not queued.
  *   J:     number of cache tiers, 1 <= J <= 127.
  *   order: int32 [N][M_max], output: queue of tier 0, then tier 1, ..., then -1.
  *   qlen:  int64 [N][J], output: queue lengths (tier j's queue starts at
  *          the sum of qlen[i][0..j-1]).
- * Scratch: about one byte per stream position. Errors: EINVAL (also J < 1),
+ * Scratch: about 5 bytes per stream position. Errors: EINVAL (also J < 1),
  * ERANGE (J > 127), ENOMEM, EDEVICE. */
-int nopfs_prefetch_order(const nopfs_job* job, const int32_t* R, const int32_t* first,
-                         const int8_t* tier, int32_t J, int32_t* order, int64_t* qlen,
-                         void* hip_stream);
+int nopfs_prefetch_order(const nopfs_job* job, const int32_t* R, const int8_t* tier, int32_t J,
+                         int32_t* order, int64_t* qlen, void* hip_stream);
 
 /* Staging-buffer schedule (section 5.1: samples enter the staging buffer in
  * access order and leave it as soon as they are read; section 5.2: the
@@ -193,7 +190,7 @@ int nopfs_prefetch_order(const nopfs_job* job, const int32_t* R, const int32_t* 
  *          values give unspecified but in-bounds results).
  *   d0:    staging buffer capacity in bytes, >= 0.
  *   fill:  int32 [N][M_max], output.
- * Scratch: about 8 bytes per stream position. Errors: EINVAL (also d0 < 0),
+ * Scratch: about 20 bytes per stream position. Errors: EINVAL (also d0 < 0),
  * ERANGE, ENOMEM, EDEVICE. */
 int nopfs_staging_schedule(const nopfs_job* job, const int32_t* R, const int64_t* sizes,
                            int64_t d0, int32_t* fill, void* hip_stream);

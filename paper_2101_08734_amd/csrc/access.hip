@@ -28,15 +28,12 @@
 
 #include <new>
 
+#include "partition.hpp"
 #include "pipeline.hpp"
 
 namespace nopfs {
 namespace {
 
-constexpr int kScShift = 14;
-constexpr int kSC = 1 << kScShift;  // reads per sub-chunk
-constexpr uint32_t kJMask = kSC - 1;
-constexpr uint32_t kMaxWindows = 8192;  // sample windows per worker
 // Tuning knobs (measured on MI355X; see the benchmark notes). Every value
 // gives identical results; only speed changes.
 #ifndef NOPFS_STATS_THREADS
@@ -63,23 +60,6 @@ static_assert((1 << NOPFS_STATS_WS) % (4 * NOPFS_STATS_THREADS) == 0, "stats_til
 constexpr int kStatsWin = 1 << NOPFS_STATS_WS;  // samples held in LDS by stats_tile
 constexpr int kNextEnt = NOPFS_NEXT_ENT;   // reads per next_tile window (fast path)
 constexpr int kSlowWin = 8192;          // samples per pass of the epoch-serial path
-
-struct SegParams {
-  int64_t F, N, B, L, M_max;
-  int32_t E, drop_last;
-  int32_t ws;     // log2 of the window width W
-  uint32_t nbk;   // windows per worker: ceil(F / W)
-  int32_t nsc;    // sub-chunks per (worker, epoch) segment
-  int32_t ent_cap;  // next_tile fast-path capacity (reads)
-};
-
-__device__ __forceinline__ int64_t seg_len(const SegParams& p, int64_t i) {
-  return p.drop_last ? p.L : epoch_len(p.F, p.N, p.B, 0, i);
-}
-
-__device__ __forceinline__ int64_t orow(const SegParams& p, int64_t i, int64_t e, int64_t sc) {
-  return ((i * p.E + e) * p.nsc + sc) * int64_t(p.nbk + 1);
-}
 
 // -- partition ----------------------------------------------------------------
 constexpr int kPartThreads = 512;
@@ -140,46 +120,6 @@ seg_partition(SegParams p, const int32_t* __restrict__ R, uint32_t* __restrict__
   for (uint32_t q = threadIdx.x; q < len; q += kPartThreads) Pk[base + q] = stage[q];
 }
 
-constexpr uint32_t kRunMap = 2048;  // reads whose run index is kept in LDS
-
-template <int NT>
-struct RunTable {
-  uint32_t pref[NT + 1];
-  int32_t start[NT];  // position in the row of the run's first read
-  int32_t fbase[NT];  // stream position of the sub-chunk start
-  uint32_t tmp[65];
-  uint16_t run_of[kRunMap];  // run index of each read (when total <= kRunMap)
-};
-
-// Loads the run table of runs [r0, r0 + NT) of epochs [e_lo, e_hi)
-// and returns the number of reads they hold. Leaves rt ready for lookups.
-template <int NT>
-__device__ __forceinline__ uint32_t load_runs(const SegParams& p, int64_t i, uint32_t kb,
-                                              const uint16_t* __restrict__ OT, RunTable<NT>& rt,
-                                              int64_t e_lo, int64_t runs, int64_t r0) {
-  const int64_t Li = seg_len(p, i);
-  const int64_t R = int64_t(p.E) * p.nsc;
-  const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * R;  // window kb: run starts
-  const uint16_t* ob = oa + R;                            // window kb+1: run ends
-  const int64_t r = r0 + threadIdx.x;
-  uint32_t len = 0;
-  if (r < runs) {
-    const int64_t run = e_lo * p.nsc + r;
-    const uint32_t e = uint32_t(run) / uint32_t(p.nsc), sc = uint32_t(run) - e * uint32_t(p.nsc);
-    const uint32_t a = oa[run], b = ob[run];
-    len = b - a;
-    rt.fbase[threadIdx.x] = int32_t(e * Li + sc * kSC);
-    rt.start[threadIdx.x] = int32_t(e * Li + sc * kSC + a);
-  }
-  uint32_t total;
-  const uint32_t ex = block_exclusive_scan(len, rt.tmp, &total);
-  rt.pref[threadIdx.x] = ex;
-  if (total <= kRunMap)
-    for (uint32_t q = 0; q < len; ++q) rt.run_of[ex + q] = uint16_t(threadIdx.x);
-  __syncthreads();
-  return total;
-}
-
 // Window-major copy of the partition offsets: OT[i][b][run] = O[i][run][b],
 // so a tile reads the starts and ends of all its runs contiguously.
 __global__ void __launch_bounds__(256)
@@ -200,63 +140,6 @@ offsets_transpose(SegParams p, const uint16_t* __restrict__ O, uint16_t* __restr
   for (int y = ty; y < 64; y += 4) {
     const int64_t c = c0 + y, r = r0 + tx;
     if (r < R && c < C) dst[c * R + r] = tile[tx][y];
-  }
-}
-
-// Calls fn(pos, f_base, v, idx) for the `total` reads of the loaded runs:
-// pos is the read's position in the partitioned row, f_base the stream
-// position of its sub-chunk start, v the packed read and idx its running
-// index in (epoch, sub-chunk, position) order. Four loads per thread are in
-// flight before any is consumed.
-template <int NT, typename Fn>
-__device__ __forceinline__ void consume_runs(const RunTable<NT>& rt, int nr, uint32_t total,
-                                             const uint32_t* __restrict__ prow, uint32_t done,
-                                             Fn fn) {
-  for (uint32_t t0 = threadIdx.x; t0 < total; t0 += 4 * NT) {
-    int64_t pos[4], fb[4];
-    uint32_t v[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t t = t0 + u * NT;
-      pos[u] = -1;
-      fb[u] = 0;
-      if (t < total) {
-        int lo;
-        if (total <= kRunMap) {
-          lo = rt.run_of[t];
-        } else {
-          lo = 0;  // last run with pref <= t
-          int hi = nr - 1;
-          while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (rt.pref[mid] <= t) lo = mid; else hi = mid - 1;
-          }
-        }
-        pos[u] = rt.start[lo] + (t - rt.pref[lo]);
-        fb[u] = rt.fbase[lo];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = pos[u] >= 0 ? prow[pos[u]] : 0u;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (pos[u] >= 0) fn(pos[u], fb[u], v[u], done + t0 + u * NT);
-  }
-}
-
-template <int NT, typename Fn>
-__device__ __forceinline__ void for_each_read(const SegParams& p, int64_t i, uint32_t kb,
-                                              const uint16_t* __restrict__ O,
-                                              const uint32_t* __restrict__ prow, RunTable<NT>& rt,
-                                              int64_t e_lo, int64_t e_hi, Fn fn) {
-  const int64_t runs = (e_hi - e_lo) * p.nsc;
-  uint32_t done = 0;
-  for (int64_t r0 = 0; r0 < runs; r0 += NT) {
-    const uint32_t total = load_runs(p, i, kb, O, rt, e_lo, runs, r0);
-    const int nr = int(runs - r0 < NT ? runs - r0 : NT);
-    consume_runs(rt, nr, total, prow, done, fn);
-    done += total;
-    __syncthreads();
   }
 }
 
@@ -615,48 +498,6 @@ __global__ void fill_stats_empty(int64_t n, uint8_t* __restrict__ count, int32_t
   }
 }
 
-int log2_ceil(int64_t v) {
-  int b = 0;
-  while ((int64_t(1) << b) < v) ++b;
-  return b;
-}
-
-SegParams seg_params(const Shape& s, int ws) {
-  SegParams p;
-  p.F = s.F; p.N = s.N; p.B = s.B; p.L = s.L; p.M_max = s.M_max;
-  p.E = int32_t(s.E);
-  p.drop_last = s.drop_last;
-  const int ws_min = log2_ceil(ceil_div(s.F, kMaxWindows));
-  p.ws = ws < ws_min ? ws_min : ws;
-  p.nbk = uint32_t(ceil_div(s.F, int64_t(1) << p.ws));
-  p.nsc = int32_t(ceil_div(s.L, kSC));
-  if (p.nsc < 1) p.nsc = 1;
-  p.ent_cap = kNextEnt;
-  return p;
-}
-
-size_t partition_smem(const SegParams& p) {
-  return size_t(((p.nbk + 4) & ~3u) + kSC) * 4;
-}
-
-int run_partition(const SegParams& p, const int32_t* R, Scratch& scr, uint32_t** Pk,
-                  uint16_t** OT, hipStream_t st) {
-  int rc;
-  uint16_t* O;
-  const size_t on = size_t(p.N * p.E * p.nsc) * (p.nbk + 1);
-  if ((rc = scr.alloc_n(Pk, size_t(p.N * p.M_max)))) return rc;
-  if ((rc = scr.alloc_n(&O, on))) return rc;
-  if ((rc = scr.alloc_n(OT, on))) return rc;
-  const int64_t wgs = p.N * p.E * p.nsc;
-  if ((rc = launch("seg_partition", seg_partition, dim3(uint32_t(wgs)), dim3(kPartThreads),
-                   partition_smem(p), st, p, R, *Pk, O)))
-    return rc;
-  const int64_t runs = int64_t(p.E) * p.nsc;
-  return launch("offsets_transpose", offsets_transpose,
-                dim3(uint32_t(ceil_div(runs, 64)), uint32_t(ceil_div(p.nbk + 1, 64)), uint32_t(p.N)),
-                dim3(256), 0, st, p, (const uint16_t*)O, *OT);
-}
-
 int launch_stats(const SegParams& p, const uint32_t* Pk, const uint16_t* OT, uint8_t* count,
                  int32_t* first, CompactCells* cc, const ClassTable* classes, hipStream_t st) {
   const uint32_t ntiles = uint32_t(p.N * p.nbk);
@@ -716,6 +557,48 @@ int launch_next(const SegParams& p, const uint32_t* Pk, const uint16_t* OT, int3
 }
 
 }  // namespace
+
+static int log2_ceil(int64_t v) {
+  int b = 0;
+  while ((int64_t(1) << b) < v) ++b;
+  return b;
+}
+
+SegParams seg_params(const Shape& s, int ws) {
+  SegParams p;
+  p.F = s.F; p.N = s.N; p.B = s.B; p.L = s.L; p.M_max = s.M_max;
+  p.E = int32_t(s.E);
+  p.drop_last = s.drop_last;
+  const int ws_min = log2_ceil(ceil_div(s.F, kMaxWindows));
+  p.ws = ws < ws_min ? ws_min : ws;
+  p.nbk = uint32_t(ceil_div(s.F, int64_t(1) << p.ws));
+  p.nsc = int32_t(ceil_div(s.L, kSC));
+  if (p.nsc < 1) p.nsc = 1;
+  p.ent_cap = kNextEnt;
+  return p;
+}
+
+static size_t partition_smem(const SegParams& p) {
+  return size_t(((p.nbk + 4) & ~3u) + kSC) * 4;
+}
+
+int run_partition(const SegParams& p, const int32_t* R, Scratch& scr, uint32_t** Pk,
+                  uint16_t** OT, hipStream_t st) {
+  int rc;
+  uint16_t* O;
+  const size_t on = size_t(p.N * p.E * p.nsc) * (p.nbk + 1);
+  if ((rc = scr.alloc_n(Pk, size_t(p.N * p.M_max)))) return rc;
+  if ((rc = scr.alloc_n(&O, on))) return rc;
+  if ((rc = scr.alloc_n(OT, on))) return rc;
+  const int64_t wgs = p.N * p.E * p.nsc;
+  if ((rc = launch("seg_partition", seg_partition, dim3(uint32_t(wgs)), dim3(kPartThreads),
+                   partition_smem(p), st, p, R, *Pk, O)))
+    return rc;
+  const int64_t runs = int64_t(p.E) * p.nsc;
+  return launch("offsets_transpose", offsets_transpose,
+                dim3(uint32_t(ceil_div(runs, 64)), uint32_t(ceil_div(p.nbk + 1, 64)), uint32_t(p.N)),
+                dim3(256), 0, st, p, (const uint16_t*)O, *OT);
+}
 
 int stats_impl(const nopfs_job* job, const int32_t* R, uint8_t* count, int32_t* first,
                hipStream_t st) {

@@ -1,23 +1,30 @@
 // nopfs_prefetch_order and nopfs_staging_schedule: what the Design section
 // derives from the streams and the placement for a worker's prefetchers.
 //
+// Both need R grouped by sample (a first read, a size) and then results in
+// stream order, so both run on the per-worker partition of R by sample
+// window (the one the counting pass uses, windows of 2^13 samples): a tile
+// per window does the per-sample work in LDS and writes one value per read
+// in partitioned order; a pass per sub-chunk of 2^14 reads puts the values
+// back in stream order through LDS. No pass scatters into or gathers from
+// HBM at random.
+//
 // Prefetch order. Each storage class is filled in the order the worker first
 // needs its samples (the first rule of optimal prefetching, I/O Access
 // Patterns section). Tier t's queue holds the samples placed in t that the
 // worker reads, by first read; the queues are concatenated fastest tier first.
-//   pf_mark   -- every cell (i, k) with a first read f and a cache tier t
-//                marks its stream position: mark[i][f] = t + 1 (one byte per
-//                position). Tiles are worker-major and grouped per XCD, so a
-//                worker's mark row (one byte per read) stays in one L2 while
-//                its cells are visited.
-//   pf_count  -- per (worker, chunk of 2048 positions, one wave each): marks
-//                per tier.
-//   pf_scan   -- per worker and tier: exclusive scan over chunks plus the
-//                start of the tier's queue; the queue lengths.
-//   pf_write  -- per chunk, in stream order: each wave step of 64 positions
-//                splits its marked positions by tier (one ballot per tier
-//                present) and writes R[i][f] to the next queue slots; then
-//                the chunk's share of the -1 padding after the queues.
+//   pf_tile   -- per (worker, window): first read of each sample of the
+//                window (LDS atomic min over its reads) and the window's
+//                tiers; each read gets code t + 1 if it is its sample's first
+//                read and the sample sits in cache tier t < J, else 0
+//                (one byte per read, partitioned order).
+//   pf_count  -- per sub-chunk: codes per tier.
+//   pf_scan   -- per worker and tier: exclusive scan over sub-chunks plus
+//                the start of the tier's queue; the queue lengths.
+//   pf_write  -- per sub-chunk: codes back in stream order in LDS; each wave
+//                step of 64 positions splits its coded positions by tier
+//                (one ballot per tier present) and writes R[i][f] to the
+//                next queue slots; then its share of the -1 padding.
 // Staging schedule. The staging buffer is filled in stream order and a
 // sample is dropped once read (Design); it is filled circularly
 // (Implementation). With S the prefix sum of the sizes along R_i (S(-1) = 0),
@@ -25,172 +32,256 @@
 // fill(h) - 1: fill(h) is the smallest f <= h with S(h) - S(f - 1) <= d0,
 // or h when the sample alone is larger than d0. Equivalently fill(h) is one
 // past the smallest g in [-1, h] with S(g) >= S(h) - d0, capped at h.
-//   st_sum    -- per (worker, chunk of 4096 positions): the sizes of the
-//                samples read, their inclusive prefix sums inside the chunk
-//                and the chunk total.
-//   st_base   -- per worker: exclusive scan of the chunk totals.
-//   st_bounds -- per chunk: the g of its first and of its last position
-//                (binary search over S; g never decreases along R).
-//   st_fill   -- per chunk: S over that g range is staged in LDS, each thread
+//   st_tile   -- per (window, group of workers): the window's sizes in LDS;
+//                every read of the group's workers gets its sample's size
+//                (partitioned order).
+//   st_sum    -- per sub-chunk: sizes back in stream order in LDS, their
+//                inclusive prefix sums inside the sub-chunk, its total.
+//   st_base   -- per worker: exclusive scan of the sub-chunk totals.
+//   st_bounds -- per quarter of a sub-chunk (4096 positions): the g of its
+//                first and of its last position (binary search over S; g
+//                never decreases along R).
+//   st_fill   -- per quarter: S over that g range is staged in LDS (the few
+//                sub-chunks it spans give the bases), each thread
 //                binary-searches the g of its first position there and walks
 //                its other positions with two pointers; -1 in padding.
+#include <limits.h>
+
 #include <new>
 
-#include "common.hpp"
+#include "partition.hpp"
 
 namespace nopfs {
 namespace {
 
-struct RowShape {
-  int64_t F, N, B, M_max, E;
-  int32_t drop_last;
-};
+// Tuning knob (identical results; only speed changes): workers per st_tile
+// workgroup (each loads the window's sizes once for all of them).
+#ifndef NOPFS_ST_GROUP
+#define NOPFS_ST_GROUP 16
+#endif
 
-__device__ __forceinline__ int64_t row_len(const RowShape& r, int64_t i) {
-  return r.E * epoch_len(r.F, r.N, r.B, r.drop_last, i);
+
+constexpr int kSchedWs = 13;             // partition windows: 2^13 samples
+constexpr int kWin = 1 << kSchedWs;      // samples per LDS pass of a tile
+constexpr int kTileThreads = 256;
+constexpr int kRunBatch = 8;             // loads in flight per run walk
+constexpr int kPfMaxJ = 128;
+
+__device__ __forceinline__ int64_t sub_len(int64_t Li, int64_t sc) {
+  const int64_t len = Li - sc * kSC;
+  return len < 0 ? 0 : (len > kSC ? kSC : len);
+}
+
+// Calls fn(fb, q, v) for every read of runs r = r0, r0 + stride, ... of
+// window kb of worker i: fb is the stream position of the run's sub-chunk,
+// q the read's index in the sub-chunk's partitioned entries (its
+// partitioned position is fb + q) and v the packed read.
+template <typename Fn>
+__device__ __forceinline__ void walk_runs(const SegParams& p, int64_t i, uint32_t kb,
+                                          const uint32_t* __restrict__ Pk,
+                                          const uint16_t* __restrict__ OT, int64_t r0,
+                                          int64_t stride, Fn fn) {
+  const int64_t Li = seg_len(p, i);
+  const int64_t runs = int64_t(p.E) * p.nsc;
+  const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;  // run starts in window kb
+  const uint16_t* ob = oa + runs;                            // run ends
+  const uint32_t* prow = Pk + i * p.M_max;
+  const uint32_t nsc = uint32_t(p.nsc);
+  for (int64_t r = r0; r < runs; r += stride) {
+    const uint32_t ra = oa[r], rb = ob[r];
+    const uint32_t e = uint32_t(r) / nsc, sc = uint32_t(r) - e * nsc;
+    const int64_t fb = int64_t(e) * Li + int64_t(sc) * kSC;
+    const uint32_t* src = prow + fb;
+    for (uint32_t q = ra; q < rb; q += kRunBatch) {
+      uint32_t v[kRunBatch];
+#pragma unroll
+      for (int u = 0; u < kRunBatch; ++u) v[u] = q + u < rb ? src[q + u] : 0u;
+#pragma unroll
+      for (int u = 0; u < kRunBatch; ++u)
+        if (q + u < rb) fn(fb, q + u, v[u]);
+    }
+  }
 }
 
 // ------------------------------------------------------------- prefetch --
-constexpr int kPfWaves = 4;                              // waves per workgroup
-constexpr int kPfSteps = 32;                             // steps of 64 positions per wave
-constexpr int64_t kPfChunk = int64_t(64) * kPfSteps;     // 2048 positions per chunk
-constexpr int kPfMaxJ = 128;
-constexpr int kMarkGroupsPerThread = 16;                 // 4-cell groups
-constexpr int64_t kMarkTile = int64_t(256) * 4 * kMarkGroupsPerThread;  // 16384 cells
+constexpr int kPfKeep = 8;  // reads per thread kept in registers between the passes
 
-__global__ void __launch_bounds__(256) pf_zero(uint4* __restrict__ p, int64_t n16) {
-  int64_t t = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-  for (; t < n16; t += stride) p[t] = make_uint4(0u, 0u, 0u, 0u);
+// Per read of the tile: first-read candidate for its sample (pass 1), then
+// its code (pass 2). When the tile's runs fit one run table and its reads fit
+// kPfKeep per thread, the reads are spread evenly over the threads through
+// the run table and kept in registers between the passes (two dependent
+// global loads per tile); otherwise each thread walks whole runs twice.
+__global__ void __launch_bounds__(kTileThreads)
+pf_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
+        const int8_t* __restrict__ tier, int32_t J, uint8_t* __restrict__ code,
+        uint32_t ntiles) {
+  __shared__ int32_t fi[kWin];  // first read of each sample of the pass
+  __shared__ int8_t tw[kWin];   // its tier
+  __shared__ RunTable<kTileThreads> rt;
+  const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
+  if (tile >= ntiles) return;
+  const int64_t i = tile / p.nbk;
+  const uint32_t kb = tile - uint32_t(i) * p.nbk;
+  const int64_t k0 = int64_t(kb) << p.ws;
+  const int64_t kend = k0 + (int64_t(1) << p.ws) < p.F ? k0 + (int64_t(1) << p.ws) : p.F;
+  const int8_t* trow = tier + i * p.F;
+  uint8_t* crow = code + i * p.M_max;
+  const uint32_t* prow = Pk + i * p.M_max;
+  const int64_t runs = int64_t(p.E) * p.nsc;
+  const bool one_table = runs <= kTileThreads && kend - k0 <= kWin;  // uniform
+  if (one_table) {
+    const uint32_t wl = uint32_t(kend - k0);
+    constexpr int kTb = kWin / kTileThreads;  // tier bytes per thread
+    int8_t tv[kTb];
+#pragma unroll
+    for (int u = 0; u < kTb; ++u) {
+      const uint32_t x = threadIdx.x + u * kTileThreads;
+      tv[u] = x < wl ? trow[k0 + x] : int8_t(-1);
+    }
+#pragma unroll
+    for (int u = 0; u < kTb; ++u) {
+      const uint32_t x = threadIdx.x + u * kTileThreads;
+      if (x < wl) {
+        fi[x] = INT_MAX;
+        tw[x] = tv[u];
+      }
+    }
+    // run table (its scan's barriers also publish fi and tw)
+    const uint32_t total = load_runs(p, i, kb, OT, rt, 0, runs, 0);
+    if (total <= uint32_t(kPfKeep * kTileThreads)) {
+      uint32_t v[kPfKeep];
+      int32_t pos[kPfKeep], fb[kPfKeep];
+#pragma unroll
+      for (int u = 0; u < kPfKeep; ++u) {
+        const uint32_t t = threadIdx.x + u * kTileThreads;
+        pos[u] = -1;
+        fb[u] = 0;
+        if (t < total) {
+          int lo;
+          if (total <= kRunMap) {
+            lo = rt.run_of[t];
+          } else {
+            lo = 0;  // last run with pref <= t
+            int hi = int(runs) - 1;
+            while (lo < hi) {
+              const int mid = (lo + hi + 1) >> 1;
+              if (rt.pref[mid] <= t) lo = mid; else hi = mid - 1;
+            }
+          }
+          pos[u] = rt.start[lo] + int32_t(t - rt.pref[lo]);
+          fb[u] = rt.fbase[lo];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kPfKeep; ++u) v[u] = pos[u] >= 0 ? prow[pos[u]] : 0u;
+#pragma unroll
+      for (int u = 0; u < kPfKeep; ++u)
+        if (pos[u] >= 0) {
+          const uint32_t x = v[u] >> kScShift;
+          if (x < wl) atomicMin(&fi[x], fb[u] + int32_t(v[u] & kJMask));
+        }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kPfKeep; ++u)
+        if (pos[u] >= 0) {
+          const uint32_t x = v[u] >> kScShift;
+          if (x < wl) {
+            const int32_t t = tw[x];
+            const bool queued = fi[x] == fb[u] + int32_t(v[u] & kJMask) && t >= 0 && t < J;
+            crow[pos[u]] = queued ? uint8_t(t + 1) : uint8_t(0);
+          }
+        }
+      return;
+    }
+    __syncthreads();  // the table is no longer read
+  }
+  for (int64_t w0 = k0; w0 < kend; w0 += kWin) {
+    const uint32_t wl = uint32_t(kend - w0 < kWin ? kend - w0 : kWin);
+    const uint32_t xoff = uint32_t(w0 - k0);
+    for (uint32_t x = threadIdx.x; x < wl; x += kTileThreads) {
+      fi[x] = INT_MAX;
+      tw[x] = trow[w0 + x];
+    }
+    __syncthreads();
+    walk_runs(p, i, kb, Pk, OT, threadIdx.x, kTileThreads, [&](int64_t fb, uint32_t, uint32_t v) {
+      const uint32_t x = (v >> kScShift) - xoff;
+      if (x < wl) atomicMin(&fi[x], int32_t(fb + (v & kJMask)));
+    });
+    __syncthreads();
+    walk_runs(p, i, kb, Pk, OT, threadIdx.x, kTileThreads, [&](int64_t fb, uint32_t q, uint32_t v) {
+      const uint32_t x = (v >> kScShift) - xoff;
+      if (x < wl) {
+        const int32_t t = tw[x];
+        const bool queued = fi[x] == int32_t(fb + (v & kJMask)) && t >= 0 && t < J;
+        crow[fb + q] = queued ? uint8_t(t + 1) : uint8_t(0);
+      }
+    });
+    __syncthreads();
+  }
 }
 
-// Mark rows have a pitch of mp bytes (a multiple of 16). Marks are plain
-// byte stores: atomic ORs on the 4-byte words (executed in L2) measured
-// twice as slow.
-__device__ __forceinline__ void mark_cell(int32_t f, int32_t t, int64_t M_max, int32_t J,
-                                          uint8_t* __restrict__ mr) {
-  // first reads outside the row or tiers outside [0, J) are not queued
-  if (f >= 0 && f < M_max && t >= 0 && t < J) mr[f] = uint8_t(t + 1);
-}
-
-// Mark byte -> tier code in [0, J] (codes above J, which no valid mark
-// holds, are dropped so every queue slot stays inside the row).
-__device__ __forceinline__ uint32_t mark_code(uint32_t m, int32_t J) {
+// Code byte -> tier code in [0, J] (codes above J, which pf_tile never
+// writes, are dropped so every queue slot stays inside the row).
+__device__ __forceinline__ uint32_t clamp_code(uint32_t m, int32_t J) {
   return m <= uint32_t(J) ? m : 0u;
 }
 
-// Tile (i, sl) covers the flat cells [i*F + sl*kMarkTile, ...) of row i. The
-// vector form reads first as int4 and tier as 4-byte words over 4-cell groups
-// aligned to the flat index (first 16-byte and tier 4-byte aligned), masking
-// the cells of neighbouring rows; the last partial group of the table is read
-// cell by cell.
-template <bool kVec>
-__global__ void __launch_bounds__(256)
-pf_mark(RowShape r, int32_t J, const int32_t* __restrict__ first, const int8_t* __restrict__ tier,
-        uint8_t* __restrict__ mark, int64_t mp, uint32_t nslices, uint32_t ntiles) {
-  const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
-  if (t >= ntiles) return;
-  const int64_t i = t / nslices;
-  const int64_t sl = t - i * nslices;
-  const int64_t row0 = i * r.F;
-  const int64_t lo = row0 + sl * kMarkTile;
-  const int64_t hi = lo + kMarkTile < row0 + r.F ? lo + kMarkTile : row0 + r.F;
-  uint8_t* mr = mark + i * mp;
-  if (!kVec) {
-    for (int64_t x = lo + threadIdx.x; x < hi; x += 256)
-      mark_cell(first[x], tier[x], r.M_max, J, mr);
-    return;
-  }
-  const int64_t NF = r.N * r.F;
-  const int64_t gfull = NF >> 2;  // groups lying wholly inside the table
-  const int64_t g0 = lo >> 2, g1 = (hi + 3) >> 2;
-  const int4* f4 = reinterpret_cast<const int4*>(first);
-  const uint32_t* t4 = reinterpret_cast<const uint32_t*>(tier);
-  constexpr int kBatch = 4;
-  for (int64_t gb = g0 + threadIdx.x; gb < g1; gb += int64_t(256) * kBatch) {
-    int32_t fv[kBatch][4];
-    uint32_t tv[kBatch];
-#pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int64_t g = gb + int64_t(b) * 256;
-      if (g < g1 && g < gfull) {
-        const int4 a = f4[g];
-        fv[b][0] = a.x;
-        fv[b][1] = a.y;
-        fv[b][2] = a.z;
-        fv[b][3] = a.w;
-        tv[b] = t4[g];
-      } else {
-        tv[b] = 0xFFFFFFFFu;  // tier -1: nothing queued
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int64_t x = g * 4 + q;
-          const bool in = g < g1 && x < NF;
-          fv[b][q] = in ? first[x] : -1;
-          if (in) tv[b] = (tv[b] & ~(0xFFu << (8 * q))) | (uint32_t(uint8_t(tier[x])) << (8 * q));
-        }
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int64_t g = gb + int64_t(b) * 256;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t x = g * 4 + q;
-        if (x >= lo && x < hi)
-          mark_cell(fv[b][q], int32_t(int8_t(uint8_t(tv[b] >> (8 * q)))), r.M_max, J, mr);
-      }
-    }
-  }
+// Sub-chunk c = e * nsc + sc of worker i covers stream positions
+// [e*Li + sc*kSC, + len).
+struct SubChunk {
+  int64_t i, c, Li, len, base;  // base: offset of its first position in [N][M_max]
+};
+
+__device__ __forceinline__ SubChunk sub_chunk(const SegParams& p, uint32_t nch, uint32_t blk) {
+  SubChunk s;
+  s.i = blk / nch;
+  s.c = blk - s.i * nch;
+  const int64_t e = s.c / p.nsc, sc = s.c - e * p.nsc;
+  s.Li = seg_len(p, s.i);
+  s.len = sub_len(s.Li, sc);
+  s.base = s.i * p.M_max + e * s.Li + sc * kSC;
+  return s;
 }
 
-// Logical block id -> (worker, block of kPfWaves chunks), worker-major per XCD.
-__device__ __forceinline__ bool pf_block(uint32_t nbw, uint32_t nblocks, int64_t* i, uint32_t* cb) {
-  const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
-  if (t >= nblocks) return false;
-  *i = t / nbw;
-  *cb = t - uint32_t(*i) * nbw;
-  return true;
-}
-
-// cnt layout: [N][nch][J]. Each wave counts one chunk; no workgroup barrier.
+// cnt layout: [N][nch][J]. Order of positions does not matter for counting,
+// so the codes are read in partitioned order.
 __global__ void __launch_bounds__(256)
-pf_count(RowShape r, int32_t J, const uint8_t* __restrict__ mark, int64_t mp, uint32_t nch,
-         uint32_t nbw, uint32_t nblocks, int32_t* __restrict__ cnt) {
-  __shared__ uint32_t s_cnt[kPfWaves][kPfMaxJ];
-  int64_t i;
-  uint32_t cb;
-  if (!pf_block(nbw, nblocks, &i, &cb)) return;
+pf_count(SegParams p, int32_t J, const uint8_t* __restrict__ code, uint32_t nch,
+         int32_t* __restrict__ cnt) {
+  __shared__ uint32_t s_cnt[kPfMaxJ];
+  const SubChunk s = sub_chunk(p, nch, blockIdx.x);
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const uint32_t c = cb * kPfWaves + w;
-  if (c >= nch) return;
-  for (int x = lane; x < J; x += 64) s_cnt[w][x] = 0;
-  const int64_t Mi = row_len(r, i);
-  const uint8_t* mr = mark + i * mp;
-  const int64_t f0 = int64_t(c) * kPfChunk + lane;
-  uint32_t code[kPfSteps];
+  for (int x = threadIdx.x; x < J; x += 256) s_cnt[x] = 0;
+  __syncthreads();
+  const uint8_t* src = code + s.base;
+  constexpr int kBatch = 8;
+  for (int64_t j0 = int64_t(w) * 64 * kBatch; j0 < s.len; j0 += 256 * kBatch) {
+    uint32_t m[kBatch];
 #pragma unroll
-  for (int u = 0; u < kPfSteps; ++u) {
-    const int64_t f = f0 + int64_t(u) * 64;
-    code[u] = f < Mi ? mark_code(mr[f], J) : 0u;
-  }
+    for (int u = 0; u < kBatch; ++u) {
+      const int64_t j = j0 + u * 64 + lane;
+      m[u] = j < s.len ? clamp_code(src[j], J) : 0u;
+    }
 #pragma unroll
-  for (int u = 0; u < kPfSteps; ++u) {
-    uint64_t act = __ballot(code[u] != 0);
-    while (act) {
-      const int lead = __builtin_ctzll(act);
-      const uint32_t tc = __builtin_amdgcn_readlane(code[u], lead);
-      const uint64_t same = __ballot(code[u] == tc);
-      if (lane == lead) s_cnt[w][tc - 1] += uint32_t(__popcll(same));
-      act &= ~same;
+    for (int u = 0; u < kBatch; ++u) {
+      uint64_t act = __ballot(m[u] != 0);
+      while (act) {
+        const int lead = __builtin_ctzll(act);
+        const uint32_t tc = __builtin_amdgcn_readlane(m[u], lead);
+        const uint64_t same = __ballot(m[u] == tc);
+        if (lane == lead) atomicAdd(&s_cnt[tc - 1], uint32_t(__popcll(same)));
+        act &= ~same;
+      }
     }
   }
-  int32_t* out = cnt + (i * nch + c) * J;
-  for (int x = lane; x < J; x += 64) out[x] = int32_t(s_cnt[w][x]);
+  __syncthreads();
+  int32_t* out = cnt + (s.i * nch + s.c) * J;
+  for (int x = threadIdx.x; x < J; x += 256) out[x] = int32_t(s_cnt[x]);
 }
 
 // In place: cnt[i][c][j] becomes the queue slot (within row i of order) of
-// chunk c's first tier-j sample; qlen[i][j] the queue lengths; tot[i] their sum.
+// sub-chunk c's first tier-j sample; qlen[i][j] the queue lengths; tot[i]
+// their sum.
 __global__ void __launch_bounds__(1024)
 pf_scan(int32_t J, uint32_t nch, int32_t* __restrict__ cnt, int64_t* __restrict__ qlen,
         int64_t* __restrict__ tot) {
@@ -214,116 +305,188 @@ pf_scan(int32_t J, uint32_t nch, int32_t* __restrict__ cnt, int64_t* __restrict_
   if (threadIdx.x == 0) tot[i] = int64_t(start);
 }
 
-__global__ void __launch_bounds__(256)
-pf_write(RowShape r, int32_t J, const uint8_t* __restrict__ mark, int64_t mp,
-         const int32_t* __restrict__ R, uint32_t nch, uint32_t nbw, uint32_t nblocks,
-         const int32_t* __restrict__ slot0, const int64_t* __restrict__ tot,
-         int32_t* __restrict__ order) {
+constexpr int kPfWaves = 4;
+constexpr int kPfQuarter = kSC / kPfWaves;  // positions per wave: 4096
+constexpr int kPfBatch = 8;                 // wave steps whose loads are issued together
+
+__global__ void __launch_bounds__(64 * kPfWaves)
+pf_write(SegParams p, int32_t J, const uint32_t* __restrict__ Pk, const uint8_t* __restrict__ code,
+         const int32_t* __restrict__ R, uint32_t nch, const int32_t* __restrict__ slot0,
+         const int64_t* __restrict__ tot, int32_t* __restrict__ order) {
+  __shared__ uint8_t s_code[kSC];
+  __shared__ uint32_t s_wcnt[kPfWaves][kPfMaxJ];
   __shared__ int32_t s_run[kPfWaves][kPfMaxJ];
-  int64_t i;
-  uint32_t cb;
-  if (!pf_block(nbw, nblocks, &i, &cb)) return;
+  const SubChunk s = sub_chunk(p, nch, blockIdx.x);
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const uint32_t c = cb * kPfWaves + w;
-  if (c >= nch) return;
-  const int32_t* sl = slot0 + (i * nch + c) * J;
-  for (int x = lane; x < J; x += 64) s_run[w][x] = sl[x];
-  const int64_t Mi = row_len(r, i);
-  const uint8_t* mr = mark + i * mp;
-  const int32_t* Rr = R + i * r.M_max;
-  int32_t* orow = order + i * r.M_max;
-  const int64_t f0 = int64_t(c) * kPfChunk + lane;
-  uint32_t code[kPfSteps];
-#pragma unroll
-  for (int u = 0; u < kPfSteps; ++u) {
-    const int64_t f = f0 + int64_t(u) * 64;
-    code[u] = f < Mi ? mark_code(mr[f], J) : 0u;
-  }
-  int32_t k[kPfSteps];
-#pragma unroll
-  for (int u = 0; u < kPfSteps; ++u) k[u] = code[u] ? Rr[f0 + int64_t(u) * 64] : 0;
-  const uint64_t below = lanemask_lt();
-#pragma unroll
-  for (int u = 0; u < kPfSteps; ++u) {
-    uint64_t act = __ballot(code[u] != 0);
+  // codes to stream order (every position of the sub-chunk has one entry)
+  for (int64_t q = threadIdx.x; q < s.len; q += 64 * kPfWaves)
+    s_code[Pk[s.base + q] & kJMask] = code[s.base + q];
+  for (int x = lane; x < J; x += 64) s_wcnt[w][x] = 0;
+  __syncthreads();
+  const int64_t j0 = int64_t(w) * kPfQuarter;
+  // this wave's codes per tier
+  for (int u = 0; u < kPfQuarter / 64; ++u) {
+    const int64_t j = j0 + u * 64 + lane;
+    const uint32_t m = j < s.len ? clamp_code(s_code[j], J) : 0u;
+    uint64_t act = __ballot(m != 0);
     while (act) {
       const int lead = __builtin_ctzll(act);
-      const uint32_t tc = __builtin_amdgcn_readlane(code[u], lead);
-      const uint64_t same = __ballot(code[u] == tc);
-      const int32_t run = s_run[w][tc - 1];
-      if (code[u] == tc) orow[run + __popcll(same & below)] = k[u];
-      if (lane == lead) s_run[w][tc - 1] = run + __popcll(same);
+      const uint32_t tc = __builtin_amdgcn_readlane(m, lead);
+      const uint64_t same = __ballot(m == tc);
+      if (lane == lead) s_wcnt[w][tc - 1] += uint32_t(__popcll(same));
       act &= ~same;
     }
   }
-  // padding after the last queue, within this chunk's range of the row
-  const int64_t q0 = int64_t(c) * kPfChunk;
-  const int64_t q1 = q0 + kPfChunk < r.M_max ? q0 + kPfChunk : r.M_max;
-  const int64_t T = tot[i];
-  for (int64_t q = (T > q0 ? T : q0) + lane; q < q1; q += 64) orow[q] = -1;
+  __syncthreads();
+  const int32_t* sl = slot0 + (s.i * nch + s.c) * J;
+  for (int x = lane; x < J; x += 64) {
+    int32_t run = sl[x];
+    for (int v = 0; v < w; ++v) run += int32_t(s_wcnt[v][x]);
+    s_run[w][x] = run;
+  }
+  // s_run[w] is this wave's own row: its writes above and the reads below
+  // come from the same wave, in order
+  const int32_t* Rsub = R + s.base;
+  int32_t* orow = order + s.i * p.M_max;
+  const uint64_t below = lanemask_lt();
+  for (int u0 = 0; u0 < kPfQuarter / 64; u0 += kPfBatch) {
+    uint32_t m[kPfBatch];
+    int32_t k[kPfBatch];
+#pragma unroll
+    for (int u = 0; u < kPfBatch; ++u) {
+      const int64_t j = j0 + (u0 + u) * 64 + lane;
+      m[u] = j < s.len ? clamp_code(s_code[j], J) : 0u;
+      k[u] = m[u] ? Rsub[j] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kPfBatch; ++u) {
+      uint64_t act = __ballot(m[u] != 0);
+      while (act) {
+        const int lead = __builtin_ctzll(act);
+        const uint32_t tc = __builtin_amdgcn_readlane(m[u], lead);
+        const uint64_t same = __ballot(m[u] == tc);
+        const int32_t run = s_run[w][tc - 1];
+        if (m[u] == tc) orow[run + __popcll(same & below)] = k[u];
+        if (lane == lead) s_run[w][tc - 1] = run + __popcll(same);
+        act &= ~same;
+      }
+    }
+  }
+  // padding after the last queue: this sub-chunk's range of the row, and
+  // the row's tail past its last read for the row's last sub-chunk
+  const int64_t T = tot[s.i];
+  const int64_t q0 = s.base - s.i * p.M_max;
+  for (int64_t q = (T > q0 ? T : q0) + threadIdx.x; q < q0 + s.len; q += 64 * kPfWaves)
+    orow[q] = -1;
+  if (s.c == int64_t(nch) - 1) {
+    const int64_t Mi = int64_t(p.E) * s.Li;
+    for (int64_t q = (T > Mi ? T : Mi) + threadIdx.x; q < p.M_max; q += 64 * kPfWaves) orow[q] = -1;
+  }
 }
 
 // -------------------------------------------------------------- staging --
-constexpr int kStThreads = 256;
-constexpr int kStPer = 16;
-constexpr int kStShift = 12;
-constexpr int64_t kStChunk = int64_t(1) << kStShift;  // 4096 positions = 256 * 16
-constexpr int kStPad = kStChunk + kStChunk / kStPer;  // LDS slots with one pad per 16
-constexpr int kGCap = 6144;                            // g values staged in LDS
+constexpr int kStGroup = NOPFS_ST_GROUP;
+constexpr int kSumThreads = 1024;
+constexpr int kHalf = kSC / 2;                // positions per LDS pass of st_sum
+constexpr int kSumPer = kHalf / kSumThreads;  // 8 positions per thread
+constexpr int kSumEnt = kSC / kSumThreads;    // 16 entries per thread
 
-static_assert(kStThreads * kStPer == kStChunk, "staging chunk");
+static_assert(kSumPer * kSumThreads == kHalf && kSumEnt * kSumThreads == kSC, "st_sum shape");
 
-__device__ __forceinline__ int lds_slot(int p) { return p + (p >> 4); }
+__device__ __forceinline__ int sum_slot(int p) { return p + (p >> 3); }
 
-// S is chunk-local: S[i*Sp + f] = sum of the sizes at the positions of f's
-// chunk up to and including f. Sp is a multiple of kStChunk.
-__global__ void __launch_bounds__(kStThreads)
-st_sum(RowShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ sizes,
-       uint32_t nch, int64_t Sp, int64_t* __restrict__ S, int64_t* __restrict__ ctot) {
-  __shared__ int64_t sv[kStPad];
-  __shared__ uint64_t tmp[65];
-  const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
-  if (t >= uint32_t(r.N) * nch) return;
-  const int64_t i = t / nch;
-  const int64_t c = t - i * nch;
-  const int64_t Mi = row_len(r, i);
-  const int64_t f0 = c * kStChunk;
-  const int32_t* Rr = R + i * r.M_max;
-  int32_t k[kStPer];
-#pragma unroll
-  for (int u = 0; u < kStPer; ++u) {
-    const int64_t f = f0 + u * kStThreads + threadIdx.x;
-    k[u] = f < Mi ? Rr[f] : -1;
+constexpr int kStTileThreads = 1024;
+
+__global__ void __launch_bounds__(kStTileThreads)
+st_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
+        const int64_t* __restrict__ sizes, int64_t* __restrict__ zP,
+        uint32_t ntiles) {
+  __shared__ int64_t sz[kWin];
+  // group-major tiles, like the other tile passes: a group's consecutive
+  // windows run together on one XCD, so the partial lines their runs write
+  // are completed there (window-major order, which shares a window's sizes
+  // between groups instead, measured 1.7x slower)
+  const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
+  if (tile >= ntiles) return;
+  const int64_t g = tile / p.nbk;
+  const uint32_t kb = tile - uint32_t(g) * p.nbk;
+  const int64_t i0 = g * kStGroup;
+  const int64_t gw = p.N - i0 < kStGroup ? p.N - i0 : kStGroup;  // workers in the group
+  const int64_t k0 = int64_t(kb) << p.ws;
+  const int64_t kend = k0 + (int64_t(1) << p.ws) < p.F ? k0 + (int64_t(1) << p.ws) : p.F;
+  const int64_t runs = int64_t(p.E) * p.nsc;
+  for (int64_t w0 = k0; w0 < kend; w0 += kWin) {
+    const uint32_t wl = uint32_t(kend - w0 < kWin ? kend - w0 : kWin);
+    const uint32_t xoff = uint32_t(w0 - k0);
+    for (uint32_t x = threadIdx.x; x < wl; x += kStTileThreads) sz[x] = sizes[w0 + x];
+    __syncthreads();
+    // (worker, run) pairs of the group, spread over the threads
+    for (int64_t pr = threadIdx.x; pr < gw * runs; pr += kStTileThreads) {
+      const int64_t i = i0 + pr / runs;
+      int64_t* zrow = zP + i * p.M_max;
+      walk_runs(p, i, kb, Pk, OT, pr % runs, runs, [&](int64_t fb, uint32_t q, uint32_t v) {
+        const uint32_t x = (v >> kScShift) - xoff;
+        if (x < wl) zrow[fb + q] = sz[x];
+      });
+    }
+    __syncthreads();
   }
-#pragma unroll
-  for (int u = 0; u < kStPer; ++u) {
-    // entries outside [0, F) break the precondition; they weigh nothing
-    const int64_t s = (k[u] >= 0 && k[u] < r.F) ? sizes[k[u]] : 0;
-    sv[lds_slot(u * kStThreads + threadIdx.x)] = s;
-  }
-  __syncthreads();
-  uint64_t v[kStPer];
-  uint64_t run = 0;
-#pragma unroll
-  for (int u = 0; u < kStPer; ++u) {
-    run += uint64_t(sv[lds_slot(threadIdx.x * kStPer + u)]);
-    v[u] = run;
-  }
-  uint64_t total;
-  const uint64_t ex = block_exclusive_scan64(run, tmp, &total);
-#pragma unroll
-  for (int u = 0; u < kStPer; ++u) sv[lds_slot(threadIdx.x * kStPer + u)] = int64_t(ex + v[u]);
-  __syncthreads();
-  int64_t* Sr = S + i * Sp;
-#pragma unroll
-  for (int u = 0; u < kStPer; ++u) {
-    const int p = u * kStThreads + threadIdx.x;
-    if (f0 + p < Mi) Sr[f0 + p] = sv[lds_slot(p)];
-  }
-  if (threadIdx.x == 0) ctot[i * nch + c] = int64_t(total);
 }
 
-// In place: ctot[i][c] becomes the sum of the sizes in the chunks before c.
+// S[i*M_max + f] = sum of the sizes at the positions of f's sub-chunk up to
+// and including f; ctot[i][c] = the sub-chunk's total.
+__global__ void __launch_bounds__(kSumThreads)
+st_sum(SegParams p, const uint32_t* __restrict__ Pk, const int64_t* __restrict__ zP, uint32_t nch,
+       int64_t* __restrict__ S, int64_t* __restrict__ ctot) {
+  __shared__ int64_t sv[kHalf + kHalf / kSumPer];
+  __shared__ uint64_t tmp[65];
+  const SubChunk s = sub_chunk(p, nch, blockIdx.x);
+  uint32_t jj[kSumEnt];
+  int64_t vv[kSumEnt];
+#pragma unroll
+  for (int u = 0; u < kSumEnt; ++u) {
+    const int64_t q = int64_t(u) * kSumThreads + threadIdx.x;
+    jj[u] = q < s.len ? (Pk[s.base + q] & kJMask) : 0xFFFFFFFFu;
+    vv[u] = q < s.len ? zP[s.base + q] : 0;
+  }
+  uint64_t carry = 0;
+  for (int64_t j0 = 0; j0 < s.len; j0 += kHalf) {
+    const uint32_t hl = uint32_t(s.len - j0 < kHalf ? s.len - j0 : kHalf);
+#pragma unroll
+    for (int u = 0; u < kSumEnt; ++u) {
+      const uint32_t x = jj[u] - uint32_t(j0);
+      if (x < hl) sv[sum_slot(int(x))] = vv[u];
+    }
+    __syncthreads();
+    uint64_t v[kSumPer];
+    uint64_t run = 0;
+#pragma unroll
+    for (int u = 0; u < kSumPer; ++u) {
+      const int x = int(threadIdx.x) * kSumPer + u;
+      run += x < int(hl) ? uint64_t(sv[sum_slot(x)]) : 0ull;
+      v[u] = run;
+    }
+    uint64_t total;
+    const uint64_t ex = block_exclusive_scan64(run, tmp, &total);
+#pragma unroll
+    for (int u = 0; u < kSumPer; ++u) {
+      const int x = int(threadIdx.x) * kSumPer + u;
+      if (x < int(hl)) sv[sum_slot(x)] = int64_t(carry + ex + v[u]);
+    }
+    __syncthreads();
+    int64_t* dst = S + s.base + j0;
+#pragma unroll
+    for (int u = 0; u < kSumPer; ++u) {
+      const int x = u * kSumThreads + int(threadIdx.x);
+      if (x < int(hl)) dst[x] = sv[sum_slot(x)];
+    }
+    carry += total;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ctot[s.i * nch + s.c] = int64_t(carry);
+}
+
+// In place: ctot[i][c] becomes the sum of the sizes in the sub-chunks before c.
 __global__ void __launch_bounds__(1024)
 st_base(uint32_t nch, int64_t* __restrict__ ctot) {
   __shared__ uint64_t tmp[65];
@@ -339,12 +502,24 @@ st_base(uint32_t nch, int64_t* __restrict__ ctot) {
   }
 }
 
+// Prefix sums along row i of R: at(x) = sum of the sizes at positions 0..x.
 struct Prefix {
-  const int64_t* S;     // row i of S
-  const int64_t* base;  // row i of the chunk bases
-  // sum of the sizes at positions 0..x of the row; 0 at x = -1
+  const int64_t* S;     // row i of S (prefix sums local to each sub-chunk)
+  const int64_t* base;  // row i of the sub-chunk bases
+  int64_t Li;           // reads per epoch of worker i (> 0 whenever at() is used)
+  double rinv;          // 1 / Li
+  int64_t nsc;
+  // sub-chunk of position x >= 0
+  __device__ __forceinline__ int64_t chunk_of(int64_t x) const {
+    // epoch of x: the double quotient is off by at most one
+    int64_t e = int64_t(double(x) * rinv);
+    if (e * Li > x) --e;
+    else if ((e + 1) * Li <= x) ++e;
+    return e * nsc + ((x - e * Li) >> kScShift);
+  }
   __device__ __forceinline__ int64_t at(int64_t x) const {
-    return x < 0 ? 0 : int64_t(uint64_t(base[x >> kStShift]) + uint64_t(S[x]));
+    if (x < 0) return 0;
+    return int64_t(uint64_t(base[chunk_of(x)]) + uint64_t(S[x]));
   }
   // smallest g in [-1, h] with at(g) >= target (h qualifies when target <= at(h))
   __device__ int64_t lower_bound(int64_t h, int64_t target) const {
@@ -358,72 +533,150 @@ struct Prefix {
   }
 };
 
+__device__ __forceinline__ Prefix row_prefix(const SegParams& p, int64_t i, uint32_t nch,
+                                             const int64_t* S, const int64_t* base) {
+  Prefix P;
+  P.S = S + i * p.M_max;
+  P.base = base + i * int64_t(nch);
+  P.Li = seg_len(p, i);
+  P.rinv = P.Li > 0 ? 1.0 / double(P.Li) : 0.0;
+  P.nsc = p.nsc;
+  return P;
+}
+
 __device__ __forceinline__ int64_t sub_sat(int64_t a, int64_t b) {
   // a - b without overflow (b >= 0)
   return a < INT64_MIN + b ? INT64_MIN : a - b;
 }
 
-// bnd[i][c] = (g of the chunk's first position, g of its last position).
+constexpr int kStThreads = 256;
+constexpr int kStPer = 16;
+constexpr int64_t kStChunk = int64_t(kStThreads) * kStPer;  // 4096 positions
+constexpr int kStParts = int(kSC / kStChunk);                // quarters of a sub-chunk
+constexpr int kStPad = kStChunk + kStChunk / kStPer;        // LDS slots with one pad per 16
+constexpr int kGCap = 5120;                                  // g values staged in LDS
+constexpr int kSegMax = 8;  // sub-chunks a staged g range may span
+
+static_assert(kStParts * kStChunk == kSC, "staging quarters");
+
+__device__ __forceinline__ int lds_slot(int p) { return p + (p >> 4); }
+
+// Block b of the fill covers quarter `part` of sub-chunk c of worker i:
+// positions [h0, h0 + hl) of row i (hl may be 0).
+struct FillPart {
+  int64_t i, c, part, Li, h0, hl;
+};
+
+__device__ __forceinline__ FillPart fill_part(const SegParams& p, uint32_t nch, int64_t b) {
+  FillPart f;
+  const int64_t per = int64_t(nch) * kStParts;
+  f.i = b / per;
+  const int64_t rem = b - f.i * per;
+  f.c = rem / kStParts;
+  f.part = rem - f.c * kStParts;
+  f.Li = seg_len(p, f.i);
+  const int64_t e = f.c / p.nsc, sc = f.c - e * p.nsc;
+  const int64_t len = sub_len(f.Li, sc) - f.part * kStChunk;
+  f.hl = len < 0 ? 0 : (len > kStChunk ? kStChunk : len);
+  f.h0 = e * f.Li + sc * kSC + f.part * kStChunk;
+  return f;
+}
+
+// bnd[b] = (g of the part's first position, g of its last position, the
+// sub-chunk holding the first g (-1 when it is -1), 0).
 __global__ void __launch_bounds__(256)
-st_bounds(RowShape r, int64_t d0, uint32_t nch, int64_t Sp, const int64_t* __restrict__ S,
-          const int64_t* __restrict__ base, int2* __restrict__ bnd) {
-  const int64_t id = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (id >= r.N * int64_t(nch)) return;
-  const int64_t i = id / nch;
-  const int64_t c = id - i * nch;
-  const int64_t Mi = row_len(r, i);
-  const int64_t h0 = c * kStChunk;
-  if (h0 >= Mi) {
-    bnd[id] = make_int2(0, -1);
+st_bounds(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __restrict__ S,
+          const int64_t* __restrict__ base, int4* __restrict__ bnd) {
+  const int64_t b = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (b >= nparts) return;
+  const FillPart f = fill_part(p, nch, b);
+  if (f.hl == 0) {
+    bnd[b] = make_int4(0, -1, -1, 0);
     return;
   }
-  const int64_t h1 = (h0 + kStChunk < Mi ? h0 + kStChunk : Mi) - 1;
-  const Prefix P{S + i * Sp, base + i * int64_t(nch)};
-  const int64_t glo = P.lower_bound(h0, sub_sat(P.at(h0), d0));
+  const Prefix P = row_prefix(p, f.i, nch, S, base);
+  const int64_t h1 = f.h0 + f.hl - 1;
+  const int64_t glo = P.lower_bound(f.h0, sub_sat(P.at(f.h0), d0));
   const int64_t ghi = P.lower_bound(h1, sub_sat(P.at(h1), d0));
-  bnd[id] = make_int2(int32_t(glo), int32_t(ghi));
+  bnd[b] = make_int4(int32_t(glo), int32_t(ghi), int32_t(glo >= 0 ? P.chunk_of(glo) : -1), 0);
 }
 
 __global__ void __launch_bounds__(kStThreads)
-st_fill(RowShape r, int64_t d0, uint32_t nch, int64_t Sp, const int64_t* __restrict__ S,
-        const int64_t* __restrict__ base, const int2* __restrict__ bnd, int32_t gcap,
+st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __restrict__ S,
+        const int64_t* __restrict__ base, const int4* __restrict__ bnd, int32_t gcap,
         int32_t* __restrict__ fill) {
   // the staged g values, then (after a barrier) the results for the transpose
   __shared__ int64_t gS[kGCap];
   static_assert(kStPad * sizeof(int32_t) <= sizeof(gS), "result staging fits");
   int32_t* fo = reinterpret_cast<int32_t*>(gS);
-  const uint32_t t = xcd_logical(blockIdx.x, gridDim.x);
-  if (t >= uint32_t(r.N) * nch) return;
-  const int64_t i = t / nch;
-  const int64_t c = t - i * nch;
-  const int64_t Mi = row_len(r, i);
-  const int64_t h0c = c * kStChunk;
-  const int64_t hend = h0c + kStChunk < r.M_max ? h0c + kStChunk : r.M_max;
-  int32_t* out = fill + i * r.M_max;
-  if (h0c >= Mi) {
-    for (int64_t h = h0c + threadIdx.x; h < hend; h += kStThreads) out[h] = -1;
-    return;
+  __shared__ int64_t seg_hi[kSegMax], seg_base[kSegMax];
+  __shared__ int32_t s_staged;
+  const int64_t b = xcd_logical(blockIdx.x, gridDim.x);
+  if (b >= nparts) return;
+  const FillPart f = fill_part(p, nch, b);
+  int32_t* out = fill + f.i * p.M_max;
+  if (f.c == int64_t(nch) - 1 && f.part == 0) {
+    // the row's padding past its last read
+    for (int64_t h = int64_t(p.E) * f.Li + threadIdx.x; h < p.M_max; h += kStThreads) out[h] = -1;
   }
-  const int64_t h1c = h0c + kStChunk < Mi ? h0c + kStChunk : Mi;
-  const Prefix P{S + i * Sp, base + i * int64_t(nch)};
-  const int2 b = bnd[t];
-  const int64_t glo = b.x;
-  const int64_t Lg = int64_t(b.y) - glo + 1;
-  const bool staged = Lg >= 1 && Lg <= gcap;  // uniform over the workgroup (gcap <= kGCap)
-  if (staged)
-    for (int64_t x = threadIdx.x; x < Lg; x += kStThreads) gS[x] = P.at(glo + x);
+  if (f.hl == 0) return;
+  const int64_t* Srow = S + f.i * p.M_max;
+  const int64_t* brow = base + f.i * int64_t(nch);
+  // this thread's positions: prefix sums within sub-chunk c (loads first)
+  const int64_t ht0 = int64_t(threadIdx.x) * kStPer;  // offset in the part
+  int64_t sh[kStPer];
+#pragma unroll
+  for (int u = 0; u < kStPer; ++u) sh[u] = ht0 + u < f.hl ? Srow[f.h0 + ht0 + u] : 0;
+  const int64_t hbase = brow[f.c];  // every position of the part is in sub-chunk c
+  const int4 bb = bnd[b];
+  const int64_t glo = bb.x, ghi = bb.y;
+  const int64_t Lg = ghi - glo + 1;
+  // sub-chunks c0, c0 + 1, ... spanned by [max(glo, 0), ghi], one per lane
+  // of the first wave: the end position and base of each
+  const int64_t c0 = bb.z >= 0 ? bb.z : 0;
+  const bool fits = Lg >= 1 && Lg <= gcap;  // uniform
+  if (threadIdx.x < 64) {
+    bool need = false, covered = false;
+    if (fits && threadIdx.x < kSegMax && ghi >= 0) {
+      const int64_t c = c0 + threadIdx.x;
+      if (c < int64_t(nch)) {
+        const int64_t e = c / p.nsc, sc = c - e * p.nsc;
+        const int64_t lo = e * f.Li + sc * kSC;
+        const int64_t hi = lo + sub_len(f.Li, sc);
+        need = lo <= ghi;
+        covered = need && hi > ghi;
+        seg_hi[threadIdx.x] = hi;
+        seg_base[threadIdx.x] = need ? brow[c] : 0;
+      }
+    }
+    const uint64_t cov = __ballot(covered);
+    if (threadIdx.x == 0) s_staged = fits && (ghi < 0 || cov != 0);
+  }
   __syncthreads();
-  const int64_t ht0 = h0c + int64_t(threadIdx.x) * kStPer;
-  const int64_t cb = P.base[c];
+  const bool staged = s_staged;  // uniform over the workgroup
+  if (staged) {
+    for (int64_t x = threadIdx.x; x < Lg; x += kStThreads) {
+      const int64_t g = glo + x;
+      int64_t v = 0;
+      if (g >= 0) {
+        int k = 0;
+        while (g >= seg_hi[k]) ++k;  // the covering sub-chunk ends past ghi
+        v = int64_t(uint64_t(seg_base[k]) + uint64_t(Srow[g]));
+      }
+      gS[x] = v;
+    }
+  }
+  __syncthreads();
+  const Prefix P = row_prefix(p, f.i, nch, S, base);
   int32_t res[kStPer];
   int64_t x = 0;
   bool started = false;
 #pragma unroll
   for (int u = 0; u < kStPer; ++u) {
-    const int64_t h = ht0 + u;
+    const int64_t h = f.h0 + ht0 + u;
     res[u] = -1;
-    if (h < h1c) {
-      const int64_t target = sub_sat(int64_t(uint64_t(cb) + uint64_t(P.S[h])), d0);
+    if (ht0 + u < f.hl) {
+      const int64_t target = sub_sat(int64_t(uint64_t(hbase) + uint64_t(sh[u])), d0);
       int64_t g;
       if (staged) {
         if (!started) {
@@ -447,8 +700,8 @@ st_fill(RowShape r, int64_t d0, uint32_t nch, int64_t Sp, const int64_t* __restr
         while (x < h && P.at(x) < target) ++x;
         g = x;
       }
-      const int64_t f = g + 1 < h ? g + 1 : h;
-      res[u] = int32_t(f > 0 ? f : 0);
+      const int64_t fv = g + 1 < h ? g + 1 : h;
+      res[u] = int32_t(fv > 0 ? fv : 0);
     }
   }
   __syncthreads();
@@ -457,74 +710,52 @@ st_fill(RowShape r, int64_t d0, uint32_t nch, int64_t Sp, const int64_t* __restr
   __syncthreads();
 #pragma unroll
   for (int u = 0; u < kStPer; ++u) {
-    const int p = u * kStThreads + threadIdx.x;
-    const int64_t h = h0c + p;
-    if (h < hend) out[h] = h < h1c ? fo[lds_slot(p)] : -1;
+    const int q = u * kStThreads + threadIdx.x;
+    if (q < f.hl) out[f.h0 + q] = fo[lds_slot(q)];
   }
 }
 
-RowShape row_shape(const Shape& s) {
-  RowShape r;
-  r.F = s.F;
-  r.N = s.N;
-  r.B = s.B;
-  r.M_max = s.M_max;
-  r.E = s.E;
-  r.drop_last = s.drop_last;
-  return r;
-}
-
-int prefetch_impl(const nopfs_job* job, const int32_t* R, const int32_t* first,
-                  const int8_t* tier, int32_t J, int32_t* order, int64_t* qlen, hipStream_t st) {
+int prefetch_impl(const nopfs_job* job, const int32_t* R, const int8_t* tier, int32_t J,
+                  int32_t* order, int64_t* qlen, hipStream_t st) {
   Shape s;
   int rc = make_shape(job, &s);
   if (rc) return rc;
-  if (!first || !tier || !qlen) return fail(NOPFS_EINVAL, "first, tier and qlen must be non-NULL");
+  if (!tier || !qlen) return fail(NOPFS_EINVAL, "tier and qlen must be non-NULL");
   if (s.M_max > 0 && (!R || !order)) return fail(NOPFS_EINVAL, "R and order must be non-NULL");
   if (J < 1) return fail(NOPFS_EINVAL, "J must be >= 1");
   if (J > 127) return fail(NOPFS_ERANGE, "J must be <= 127");
-  const RowShape r = row_shape(s);
-  const uint32_t nch = uint32_t(ceil_div(s.M_max, kPfChunk));
-  const uint32_t nbw = uint32_t(ceil_div(nch, kPfWaves));
-  const int64_t nblocks = s.N * int64_t(nbw);
-  const int64_t nslices = ceil_div(s.F, kMarkTile);
-  if (nblocks >= (int64_t(1) << 31) || s.N * nslices >= (int64_t(1) << 31))
+  const SegParams p = seg_params(s, kSchedWs);
+  const uint32_t nch = uint32_t(s.E * p.nsc);  // sub-chunks per worker
+  const int64_t nblk = s.N * int64_t(nch);
+  const int64_t ntiles = s.N * int64_t(p.nbk);
+  if (nblk >= (int64_t(1) << 31) || ntiles >= (int64_t(1) << 31))
     return fail(NOPFS_ERANGE, "job too large for one launch");
   Scratch scr(st);
   int64_t* tot;
   int32_t* cnt;
-  uint8_t* mark;
-  const int64_t mp = ceil_div(s.M_max, 16) * 16;  // mark row pitch
-  const int64_t nm16 = s.N * mp / 16;
   if ((rc = scr.alloc_n(&tot, size_t(s.N)))) return rc;
-  if ((rc = scr.alloc_n(&cnt, size_t(s.N) * nch * size_t(J)))) return rc;
-  if ((rc = scr.alloc_n(&mark, size_t(nm16) * 16))) return rc;
-  if (nm16 > 0) {
-    const int64_t zb = ceil_div(nm16, 256 * 4) < 65536 ? ceil_div(nm16, 256 * 4) : 65536;
-    if ((rc = launch("pf_zero", pf_zero, dim3(uint32_t(zb)), dim3(256), 0, st,
-                     reinterpret_cast<uint4*>(mark), nm16)))
-      return rc;
-    const uint32_t ntiles = uint32_t(s.N * nslices);
-    const bool vec = (reinterpret_cast<uintptr_t>(first) & 15) == 0 &&
-                     (reinterpret_cast<uintptr_t>(tier) & 3) == 0;
-    rc = vec ? launch("pf_mark", pf_mark<true>, dim3(xcd_padded(ntiles)), dim3(256), 0, st, r, J,
-                      first, tier, mark, mp, uint32_t(nslices), ntiles)
-             : launch("pf_mark", pf_mark<false>, dim3(xcd_padded(ntiles)), dim3(256), 0, st, r, J,
-                      first, tier, mark, mp, uint32_t(nslices), ntiles);
-    if (rc) return rc;
-    if ((rc = launch("pf_count", pf_count, dim3(xcd_padded(uint32_t(nblocks))), dim3(256), 0, st,
-                     r, J, (const uint8_t*)mark, mp, nch, nbw, uint32_t(nblocks), cnt)))
-      return rc;
-  }
+  if ((rc = scr.alloc_n(&cnt, size_t(nblk) * size_t(J)))) return rc;
+  if (s.M_max == 0)  // no reads at all: empty queues
+    return launch("pf_scan", pf_scan, dim3(uint32_t(s.N)), dim3(1024), 0, st, J, 0u, cnt, qlen,
+                  tot);
+  uint32_t* Pk;
+  uint16_t* OT;
+  uint8_t* code;
+  if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
+  if ((rc = scr.alloc_n(&code, size_t(s.N * s.M_max)))) return rc;
+  if ((rc = launch("pf_tile", pf_tile, dim3(xcd_padded(uint32_t(ntiles))), dim3(kTileThreads), 0,
+                   st, p, (const uint32_t*)Pk, (const uint16_t*)OT, tier, J, code,
+                   uint32_t(ntiles))))
+    return rc;
+  if ((rc = launch("pf_count", pf_count, dim3(uint32_t(nblk)), dim3(256), 0, st, p, J,
+                   (const uint8_t*)code, nch, cnt)))
+    return rc;
   if ((rc = launch("pf_scan", pf_scan, dim3(uint32_t(s.N)), dim3(1024), 0, st, J, nch, cnt, qlen,
                    tot)))
     return rc;
-  if (nm16 > 0 &&
-      (rc = launch("pf_write", pf_write, dim3(xcd_padded(uint32_t(nblocks))), dim3(256), 0, st, r,
-                   J, (const uint8_t*)mark, mp, R, nch, nbw, uint32_t(nblocks),
-                   (const int32_t*)cnt, (const int64_t*)tot, order)))
-    return rc;
-  return NOPFS_OK;
+  return launch("pf_write", pf_write, dim3(uint32_t(nblk)), dim3(64 * kPfWaves), 0, st, p, J,
+                (const uint32_t*)Pk, (const uint8_t*)code, R, nch, (const int32_t*)cnt,
+                (const int64_t*)tot, order);
 }
 
 int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, int64_t d0,
@@ -536,38 +767,48 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
   if (s.M_max > 0 && (!R || !fill)) return fail(NOPFS_EINVAL, "R and fill must be non-NULL");
   if (d0 < 0) return fail(NOPFS_EINVAL, "d0 must be >= 0");
   if (s.M_max == 0) return NOPFS_OK;
-  const RowShape r = row_shape(s);
-  const uint32_t nch = uint32_t(ceil_div(s.M_max, kStChunk));
-  const int64_t nblocks = s.N * int64_t(nch);
-  if (nblocks >= (int64_t(1) << 31)) return fail(NOPFS_ERANGE, "job too large for one launch");
-  const int64_t Sp = int64_t(nch) * kStChunk;
+  const SegParams p = seg_params(s, kSchedWs);
+  const uint32_t nch = uint32_t(s.E * p.nsc);  // sub-chunks per worker
+  const uint32_t ngroups = uint32_t(ceil_div(s.N, kStGroup));
+  const int64_t nblk = s.N * int64_t(nch);
+  const int64_t nparts = nblk * kStParts;
+  const int64_t ntiles = int64_t(p.nbk) * ngroups;
+  if (nparts >= (int64_t(1) << 31) || ntiles >= (int64_t(1) << 31))
+    return fail(NOPFS_ERANGE, "job too large for one launch");
   Scratch scr(st);
-  int64_t *S, *ctot;
-  int2* bnd;
-  if ((rc = scr.alloc_n(&S, size_t(s.N) * size_t(Sp)))) return rc;
-  if ((rc = scr.alloc_n(&ctot, size_t(nblocks)))) return rc;
-  if ((rc = scr.alloc_n(&bnd, size_t(nblocks)))) return rc;
-  const dim3 grid(xcd_padded(uint32_t(nblocks)));
-  if ((rc = launch("st_sum", st_sum, grid, dim3(kStThreads), 0, st, r, R, sizes, nch, Sp, S, ctot)))
+  uint32_t* Pk;
+  uint16_t* OT;
+  int64_t *zP, *S, *ctot;
+  int4* bnd;
+  if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
+  if ((rc = scr.alloc_n(&zP, size_t(s.N * s.M_max)))) return rc;
+  if ((rc = scr.alloc_n(&S, size_t(s.N * s.M_max)))) return rc;
+  if ((rc = scr.alloc_n(&ctot, size_t(nblk)))) return rc;
+  if ((rc = scr.alloc_n(&bnd, size_t(nparts)))) return rc;
+  if ((rc = launch("st_tile", st_tile, dim3(xcd_padded(uint32_t(ntiles))), dim3(kStTileThreads), 0,
+                   st, p, (const uint32_t*)Pk, (const uint16_t*)OT, sizes, zP,
+                   uint32_t(ntiles))))
+    return rc;
+  if ((rc = launch("st_sum", st_sum, dim3(uint32_t(nblk)), dim3(kSumThreads), 0, st, p,
+                   (const uint32_t*)Pk, (const int64_t*)zP, nch, S, ctot)))
     return rc;
   if ((rc = launch("st_base", st_base, dim3(uint32_t(s.N)), dim3(1024), 0, st, nch, ctot))) return rc;
-  if ((rc = launch("st_bounds", st_bounds, dim3(uint32_t(ceil_div(nblocks, 256))), dim3(256), 0, st,
-                   r, d0, nch, Sp, (const int64_t*)S, (const int64_t*)ctot, bnd)))
+  if ((rc = launch("st_bounds", st_bounds, dim3(uint32_t(ceil_div(nparts, 256))), dim3(256), 0, st,
+                   p, d0, nch, nparts, (const int64_t*)S, (const int64_t*)ctot, bnd)))
     return rc;
   const int32_t gcap = (debug_value(4) > 0 && debug_value(4) < kGCap) ? int32_t(debug_value(4)) : kGCap;
-  return launch("st_fill", st_fill, grid, dim3(kStThreads), 0, st, r, d0, nch, Sp,
-                (const int64_t*)S, (const int64_t*)ctot, (const int2*)bnd, gcap, fill);
+  return launch("st_fill", st_fill, dim3(xcd_padded(uint32_t(nparts))), dim3(kStThreads), 0, st, p,
+                d0, nch, nparts, (const int64_t*)S, (const int64_t*)ctot, (const int4*)bnd, gcap,
+                fill);
 }
 
 }  // namespace
 }  // namespace nopfs
 
-extern "C" int nopfs_prefetch_order(const nopfs_job* job, const int32_t* R, const int32_t* first,
-                                    const int8_t* tier, int32_t J, int32_t* order, int64_t* qlen,
-                                    void* hip_stream) {
+extern "C" int nopfs_prefetch_order(const nopfs_job* job, const int32_t* R, const int8_t* tier,
+                                    int32_t J, int32_t* order, int64_t* qlen, void* hip_stream) {
   try {
-    return nopfs::prefetch_impl(job, R, first, tier, J, order, qlen,
-                                static_cast<hipStream_t>(hip_stream));
+    return nopfs::prefetch_impl(job, R, tier, J, order, qlen, static_cast<hipStream_t>(hip_stream));
   } catch (const std::bad_alloc&) {
     return nopfs::fail(NOPFS_ENOMEM, "host allocation failed");
   } catch (...) {

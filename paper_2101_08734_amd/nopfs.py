@@ -68,7 +68,7 @@ def lib() -> ctypes.CDLL:
             "nopfs_reuse_next": [jp, P, P, P],
             "nopfs_tier_plan": [jp, P, P, P, P, I32, P, P, P],
             "nopfs_plan_job": [jp, P, P, I32, P, P, P, P, P, P, P],
-            "nopfs_prefetch_order": [jp, P, P, P, I32, P, P, P],
+            "nopfs_prefetch_order": [jp, P, P, I32, P, P, P],
             "nopfs_staging_schedule": [jp, P, P, I64, P, P],
             "nopfs_profile_enable": [ctypes.c_int],
             "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
@@ -217,12 +217,11 @@ def plan_job(job: Job, sizes, caps, out=None, stream=None):
     return o
 
 
-def prefetch_order(job: Job, R, first, tier, J, order=None, qlen=None, stream=None):
+def prefetch_order(job: Job, R, tier, J, order=None, qlen=None, stream=None):
     """Per-tier prefetch queues (nopfs_prefetch_order): order [N][M_max] int32
     (tier 0's queue, tier 1's, ..., then -1) and qlen [N][J] int64."""
     _, M, _ = stream_shape(job)
     _device_tensor(R, torch.int32, (job.N, M), "R")
-    _device_tensor(first, torch.int32, (job.N, job.F), "first")
     _device_tensor(tier, torch.int8, (job.N, job.F), "tier")
     J = int(J)
     if order is None:
@@ -232,7 +231,7 @@ def prefetch_order(job: Job, R, first, tier, J, order=None, qlen=None, stream=No
     _device_tensor(order, torch.int32, (job.N, M), "order")
     _device_tensor(qlen, torch.int64, (job.N, max(J, 1)), "qlen")
     j = job.c()
-    _check(lib().nopfs_prefetch_order(ctypes.byref(j), _ptr(R), _ptr(first), _ptr(tier), J,
+    _check(lib().nopfs_prefetch_order(ctypes.byref(j), _ptr(R), _ptr(tier), J,
                                       _ptr(order), _ptr(qlen), _stream(stream)),
            "nopfs_prefetch_order")
     return order, qlen

@@ -72,7 +72,7 @@ def test_invalid_jobs(L, kw, code):
     assert L.nopfs_reuse_next(ctypes.byref(j), FAKE, FAKE, None) == code
     caps = (ctypes.c_int64 * 1)(10)
     assert L.nopfs_tier_plan(ctypes.byref(j), FAKE, FAKE, FAKE, caps, 1, FAKE, FAKE, None) == code
-    assert L.nopfs_prefetch_order(ctypes.byref(j), FAKE, FAKE, FAKE, 1, FAKE, FAKE, None) == code
+    assert L.nopfs_prefetch_order(ctypes.byref(j), FAKE, FAKE, 1, FAKE, FAKE, None) == code
     assert L.nopfs_staging_schedule(ctypes.byref(j), FAKE, FAKE, 10, FAKE, None) == code
     assert L.nopfs_last_error()  # a detail string is recorded
 
@@ -89,12 +89,11 @@ def test_null_pointers(L):
     assert L.nopfs_tier_plan(ctypes.byref(j), FAKE, FAKE, None, caps, 2, FAKE, FAKE, None) == E
     assert L.nopfs_tier_plan(ctypes.byref(j), FAKE, FAKE, FAKE, None, 2, FAKE, FAKE, None) == E
     po = L.nopfs_prefetch_order
-    assert po(ctypes.byref(j), None, FAKE, FAKE, 1, FAKE, FAKE, None) == E
-    assert po(ctypes.byref(j), FAKE, None, FAKE, 1, FAKE, FAKE, None) == E
-    assert po(ctypes.byref(j), FAKE, FAKE, None, 1, FAKE, FAKE, None) == E
-    assert po(ctypes.byref(j), FAKE, FAKE, FAKE, 1, None, FAKE, None) == E
-    assert po(ctypes.byref(j), FAKE, FAKE, FAKE, 1, FAKE, None, None) == E
-    assert po(None, FAKE, FAKE, FAKE, 1, FAKE, FAKE, None) == E
+    assert po(ctypes.byref(j), None, FAKE, 1, FAKE, FAKE, None) == E
+    assert po(ctypes.byref(j), FAKE, None, 1, FAKE, FAKE, None) == E
+    assert po(ctypes.byref(j), FAKE, FAKE, 1, None, FAKE, None) == E
+    assert po(ctypes.byref(j), FAKE, FAKE, 1, FAKE, None, None) == E
+    assert po(None, FAKE, FAKE, 1, FAKE, FAKE, None) == E
     ss = L.nopfs_staging_schedule
     assert ss(ctypes.byref(j), None, FAKE, 10, FAKE, None) == E
     assert ss(ctypes.byref(j), FAKE, None, 10, FAKE, None) == E
@@ -114,9 +113,9 @@ def test_plan_argument_checks(L):
 def test_schedule_argument_checks(L):
     j = _job()
     po = L.nopfs_prefetch_order
-    assert po(ctypes.byref(j), FAKE, FAKE, FAKE, 0, FAKE, FAKE, None) == nopfs.NOPFS_EINVAL
-    assert po(ctypes.byref(j), FAKE, FAKE, FAKE, -3, FAKE, FAKE, None) == nopfs.NOPFS_EINVAL
-    assert po(ctypes.byref(j), FAKE, FAKE, FAKE, 128, FAKE, FAKE, None) == nopfs.NOPFS_ERANGE
+    assert po(ctypes.byref(j), FAKE, FAKE, 0, FAKE, FAKE, None) == nopfs.NOPFS_EINVAL
+    assert po(ctypes.byref(j), FAKE, FAKE, -3, FAKE, FAKE, None) == nopfs.NOPFS_EINVAL
+    assert po(ctypes.byref(j), FAKE, FAKE, 128, FAKE, FAKE, None) == nopfs.NOPFS_ERANGE
     ss = L.nopfs_staging_schedule
     assert ss(ctypes.byref(j), FAKE, FAKE, -1, FAKE, None) == nopfs.NOPFS_EINVAL
     assert b"d0" in L.nopfs_last_error()
@@ -135,7 +134,7 @@ def test_scratch_failure_is_enomem(L):
         lambda: L.nopfs_access_stats(ctypes.byref(j), FAKE, FAKE, FAKE, None),
         lambda: L.nopfs_reuse_next(ctypes.byref(j), FAKE, FAKE, None),
         lambda: L.nopfs_tier_plan(ctypes.byref(j), FAKE, FAKE, FAKE, caps, 1, FAKE, FAKE, None),
-        lambda: L.nopfs_prefetch_order(ctypes.byref(j), FAKE, FAKE, FAKE, 1, FAKE, FAKE, None),
+        lambda: L.nopfs_prefetch_order(ctypes.byref(j), FAKE, FAKE, 1, FAKE, FAKE, None),
         lambda: L.nopfs_staging_schedule(ctypes.byref(j), FAKE, FAKE, 10, FAKE, None),
     ]
     for call in calls:

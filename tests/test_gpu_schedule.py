@@ -1,12 +1,13 @@
 """Prefetch queues and staging schedule on the GPU vs the CPU oracle.
 
-Stage isolation: R, first and tier are the oracle's own (streams, stats and
-plan on the host), so a mismatch names these two entry points. Comparisons
+Stage isolation: R and tier (and, for the oracle, first) are the oracle's
+own (streams, stats and plan on the host), so a mismatch names these two
+entry points. Comparisons
 are element by element (all integer work). Sizes span many 2048-position
 prefetch chunks and 4096-position staging chunks with ragged tails; edge
 cases cover empty streams, rows of different lengths (drop_last=0), more
 workers than samples, J below and above the placement's tier count,
-misaligned first/tier tables (the cell-by-cell marking path), buffers from 0
+a tier table at an odd address, buffers from 0
 bytes to more than a worker reads, and the staging search's global-memory
 path. At ImageNet-1k size the oracle runs in full; at ImageNet-22k size the
 outputs are checked on the device by the properties that define them.
@@ -81,9 +82,9 @@ def _d0s(sizes, R, N):
 def test_prefetch_order_matches_oracle(oracle, name, F, E, N, B, d, seed, fr):
     rjob, sizes, caps, out = _oracle_inputs(oracle, F, E, N, B, d, seed, fr)
     job = nopfs.Job(F, E, N, B, d, seed)
-    R, first, tier = _dev(out["R"]), _dev(out["first"]), _dev(out["tier"])
+    R, tier = _dev(out["R"]), _dev(out["tier"])
     for J in sorted({1, len(caps), len(caps) + 2}):
-        order, qlen = nopfs.prefetch_order(job, R, first, tier, J)
+        order, qlen = nopfs.prefetch_order(job, R, tier, J)
         torch.cuda.synchronize()
         eo, eq = oracle.prefetch_order(rjob, out["R"], out["first"], out["tier"], J)
         _equal(f"order J={J}", order, eo)
@@ -162,27 +163,24 @@ def test_prefetch_arbitrary_placement(oracle):
     tier = rng.integers(-3, 9, size=(N, F)).astype(np.int8)
     job = nopfs.Job(F, E, N, B, d, seed)
     for J in (1, 4, 6, 127):
-        order, qlen = nopfs.prefetch_order(job, _dev(R), _dev(first), _dev(tier), J)
+        order, qlen = nopfs.prefetch_order(job, _dev(R), _dev(tier), J)
         torch.cuda.synchronize()
         eo, eq = oracle.prefetch_order(rjob, R, first, tier, J)
         _equal(f"order J={J}", order, eo)
         _equal(f"qlen J={J}", qlen, eq)
 
 
-def test_prefetch_misaligned_tables(oracle):
-    """first and tier views that are not 16- and 4-byte aligned take the
-    cell-by-cell marking path."""
+def test_prefetch_tier_view_with_offset(oracle):
+    """A tier table that starts at an odd address (a view into a larger
+    buffer) is read like any other."""
     rjob, sizes, caps, out = _oracle_inputs(oracle, *JOBS[1][1:])
     F, N = JOBS[1][1], JOBS[1][3]
     job = nopfs.Job(*JOBS[1][1:7])
-    fbuf = torch.empty(N * F + 4, dtype=torch.int32, device="cuda")
     tbuf = torch.empty(N * F + 4, dtype=torch.int8, device="cuda")
-    first = fbuf[1:1 + N * F].view(N, F)
     tier = tbuf[3:3 + N * F].view(N, F)
-    assert first.data_ptr() % 16 != 0 and tier.data_ptr() % 4 != 0
-    first.copy_(_dev(out["first"]))
+    assert tier.data_ptr() % 4 != 0
     tier.copy_(_dev(out["tier"]))
-    order, qlen = nopfs.prefetch_order(job, _dev(out["R"]), first, tier, len(caps))
+    order, qlen = nopfs.prefetch_order(job, _dev(out["R"]), tier, len(caps))
     torch.cuda.synchronize()
     eo, eq = oracle.prefetch_order(rjob, out["R"], out["first"], out["tier"], len(caps))
     _equal("order", order, eo)
@@ -194,10 +192,9 @@ def test_outputs_fully_written():
     still writes its queue lengths)."""
     job = nopfs.Job(10, 2, 4, 3, 1, 17)  # T = 0, M_max = 0
     R = torch.empty((4, 0), dtype=torch.int32, device="cuda")
-    first = torch.full((4, 10), -1, dtype=torch.int32, device="cuda")
     tier = torch.zeros((4, 10), dtype=torch.int8, device="cuda")
     qlen = torch.full((4, 2), 77, dtype=torch.int64, device="cuda")
-    order, qlen = nopfs.prefetch_order(job, R, first, tier, 2, qlen=qlen)
+    order, qlen = nopfs.prefetch_order(job, R, tier, 2, qlen=qlen)
     torch.cuda.synchronize()
     assert order.shape == (4, 0) and int(qlen.abs().sum()) == 0
 
@@ -209,9 +206,9 @@ def test_imagenet1k_full(oracle, imagenet1k_expected):
     sizes = wl.sizes(w)
     out = imagenet1k_expected
     job = nopfs.Job(*w.job_tuple())
-    R, first, tier = _dev(out["R"]), _dev(out["first"]), _dev(out["tier"])
+    R, tier = _dev(out["R"]), _dev(out["tier"])
     J = len(w.caps)
-    order, qlen = nopfs.prefetch_order(job, R, first, tier, J)
+    order, qlen = nopfs.prefetch_order(job, R, tier, J)
     fill = nopfs.staging_schedule(job, R, _dev(sizes), int(w.staging))
     torch.cuda.synchronize()
     eo, eq = oracle.prefetch_order(rjob, out["R"], out["first"], out["tier"], J)
@@ -271,7 +268,7 @@ def test_imagenet22k_properties():
     del out["count"], out["next"]
     torch.cuda.empty_cache()
     J = len(w.caps)
-    order, qlen = nopfs.prefetch_order(job, out["R"], out["first"], out["tier"], J)
+    order, qlen = nopfs.prefetch_order(job, out["R"], out["tier"], J)
     torch.cuda.synchronize()
     rows = [0, 1, 77, 131, 255]
     check_prefetch_properties(job, out["R"], out["first"], out["tier"], J, order, qlen.cpu(), rows)
