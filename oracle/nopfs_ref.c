@@ -422,6 +422,103 @@ int nopfs_ref_staging_schedule(const nopfs_ref_job* job, const int32_t* R,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Performance model (section 4). Worker i consumes its f-th read at         */
+/*   t(f) = max(avail(f), t(f-1) + s(R[f-1]) / c),                          */
+/* where avail(f) = (read time of R[0..f] summed) / p0 is when the read is  */
+/* in the staging buffer (prefetch threads load-balanced), and a read takes */
+/* fetch + write: write = max(s / beta, s / (w0 / p0)) (preprocessing and   */
+/* buffer writes pipelined), fetch = s over the fastest applicable          */
+/* throughput among the PFS (t(gamma) / gamma), another worker's tier j     */
+/* (min(b_c, r_j / p_j)) and the worker's own tier j (r_j / p_j). The first */
+/* read has no predecessor: t(0) = avail(0). Placement is static: a sample  */
+/* is in tier j of worker i exactly when tier[i][k] == j.                   */
+/* ------------------------------------------------------------------------ */
+static int model_ok(const nopfs_ref_model* m) {
+  if (!m || m->J < 1 || m->J > 32) return 0;
+  const double v[7] = {m->c, m->beta, m->b_c, m->pfs_t, m->pfs_gamma, m->w0, m->p0};
+  for (int q = 0; q < 7; ++q)
+    if (!(v[q] > 0) || v[q] * 0 != 0) return 0; /* positive and finite */
+  for (int32_t j = 0; j < m->J; ++j)
+    if (!(m->r[j] > 0) || !(m->p[j] > 0) || m->r[j] * 0 != 0 || m->p[j] * 0 != 0) return 0;
+  return 1;
+}
+
+int nopfs_ref_fetch_model_rows(const nopfs_ref_job* job, const int32_t* R,
+                               const int8_t* tier, const int64_t* sizes,
+                               const nopfs_ref_model* m, int64_t i0, int64_t i1,
+                               int16_t* src, double* t) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!tier || !sizes || !model_ok(m)) return REF_EINVAL;
+  if (i0 < 0 || i1 > job->N || i0 > i1) return REF_EINVAL;
+  if (M_max > 0 && i1 > i0 && (!R || !src || !t)) return REF_EINVAL;
+  const int64_t F = job->F, N = job->N;
+  const int32_t J = m->J;
+  /* holders[k][j]: how many workers hold sample k in tier j */
+  int32_t* holders = (int32_t*)calloc((size_t)F * (size_t)J, sizeof(int32_t));
+  if (!holders) return REF_ENOMEM;
+  for (int64_t w = 0; w < N; ++w)
+    for (int64_t k = 0; k < F; ++k) {
+      int8_t q = tier[w * F + k];
+      if (q >= 0 && q < J) holders[k * J + q]++;
+    }
+  const double pfs = m->pfs_t / m->pfs_gamma;
+  for (int64_t i = i0; i < i1; ++i) {
+    const int32_t* Ri = R + (i - i0) * M_max;
+    int16_t* si = src + (i - i0) * M_max;
+    double* ti = t + (i - i0) * M_max;
+    int64_t Mi = job->E * epoch_len(job, i);
+    double read_sum = 0, t_prev = 0, s_prev = 0;
+    for (int64_t f = 0; f < Mi; ++f) {
+      int32_t k = Ri[f];
+      double s = (double)sizes[k];
+      int8_t own = tier[i * F + k];
+      /* candidates in order of preference; a later one must be strictly faster */
+      double best = -1;
+      int16_t code = 0;
+      if (own >= 0 && own < J) {
+        best = m->r[own] / m->p[own];
+        code = (int16_t)(256 + own);
+      }
+      for (int32_t j = 0; j < J; ++j) {
+        int32_t elsewhere = holders[(int64_t)k * J + j] - (own == j ? 1 : 0);
+        if (elsewhere > 0) {
+          double thr = m->r[j] / m->p[j];
+          if (m->b_c < thr) thr = m->b_c;
+          if (thr > best) {
+            best = thr;
+            code = (int16_t)(128 + j);
+          }
+        }
+      }
+      if (pfs > best) {
+        best = pfs;
+        code = 0;
+      }
+      double fetch = s / best;
+      double wr = s / m->beta;
+      double wb = s / (m->w0 / m->p0);
+      if (wb > wr) wr = wb;
+      read_sum += fetch + wr;
+      double avail = read_sum / m->p0;
+      double tf = avail;
+      if (f > 0 && t_prev + s_prev / m->c > tf) tf = t_prev + s_prev / m->c;
+      si[f] = code;
+      ti[f] = tf;
+      t_prev = tf;
+      s_prev = s;
+    }
+    for (int64_t f = Mi; f < M_max; ++f) {
+      si[f] = -1;
+      ti[f] = -1.0;
+    }
+  }
+  free(holders);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Sampled columns. The position of sample s in epoch e is, by definition   */
 /* of the sorted order, the number of samples whose (key, id) is smaller.   */
 /* Everything else for s follows from its positions in the E epochs.        */

@@ -90,6 +90,35 @@ int nopfs_ref_prefetch_order(const nopfs_ref_job* job, const int32_t* R,
 int nopfs_ref_staging_schedule(const nopfs_ref_job* job, const int32_t* R,
                                const int64_t* sizes, int64_t d0, int32_t* fill);
 
+/* Parameters of the performance model (section 4), in bytes, bytes per
+ * second and seconds. Cache tier j (j = 0..J-1) is the model's storage class
+ * j + 1; class 0 is the staging buffer. */
+typedef struct nopfs_ref_model {
+  double c;          /* compute throughput for training                      */
+  double beta;       /* preprocessing rate                                   */
+  double b_c;        /* inter-worker network bandwidth                       */
+  double pfs_t;      /* aggregate random read throughput of the PFS, t(gamma) */
+  double pfs_gamma;  /* the number of PFS readers gamma it is measured at     */
+  double w0;         /* staging-buffer write throughput with p0 threads      */
+  double p0;         /* prefetch threads of the staging buffer               */
+  int32_t J;         /* cache tiers, 1..32                                   */
+  int32_t pad_;
+  double r[32];      /* tier j: aggregate random read throughput, p[j] threads */
+  double p[32];      /* tier j: prefetch threads                             */
+} nopfs_ref_model;
+
+/* Fetch source and consumption time of every read (section 4) for workers
+ * [i0, i1): R points at row i0 of the streams, tier is the placement of all
+ * N workers ([N][F]), src and t point at row i0 of their [N][M_max] tables.
+ * src: 0 = the PFS, 128 + j = another worker's tier j, 256 + j = the
+ * worker's own tier j (the fastest applicable source; on equal throughput
+ * own before remote before PFS, lower tier first); t: the time the worker
+ * consumes the read, in seconds. Padding: src -1, t -1. */
+int nopfs_ref_fetch_model_rows(const nopfs_ref_job* job, const int32_t* R,
+                               const int8_t* tier, const int64_t* sizes,
+                               const nopfs_ref_model* m, int64_t i0, int64_t i1,
+                               int16_t* src, double* t);
+
 /* Per-sample columns for S chosen samples, computed one sample at a time
  * from the definition of the shuffle (for checks at sizes where the full
  * oracle is too slow):

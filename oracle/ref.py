@@ -33,6 +33,25 @@ class RefJob(ctypes.Structure):
                 ("drop_last", ctypes.c_int32), ("seed", ctypes.c_uint64)]
 
 
+class RefModel(ctypes.Structure):
+    _fields_ = [("c", ctypes.c_double), ("beta", ctypes.c_double), ("b_c", ctypes.c_double),
+                ("pfs_t", ctypes.c_double), ("pfs_gamma", ctypes.c_double),
+                ("w0", ctypes.c_double), ("p0", ctypes.c_double),
+                ("J", ctypes.c_int32), ("pad_", ctypes.c_int32),
+                ("r", ctypes.c_double * 32), ("p", ctypes.c_double * 32)]
+
+
+def make_model(c, beta, b_c, pfs_t, pfs_gamma, w0, p0, r, p) -> RefModel:
+    """Model parameters in bytes, bytes/s; r and p per cache tier."""
+    m = RefModel()
+    m.c, m.beta, m.b_c = float(c), float(beta), float(b_c)
+    m.pfs_t, m.pfs_gamma, m.w0, m.p0 = float(pfs_t), float(pfs_gamma), float(w0), float(p0)
+    m.J = len(r)
+    for j, (rj, pj) in enumerate(zip(r, p)):
+        m.r[j], m.p[j] = float(rj), float(pj)
+    return m
+
+
 def build(force: bool = False) -> str:
     """Compile the oracle with gcc (plain C, no GPU code)."""
     if force or not os.path.exists(_LIB) or \
@@ -67,13 +86,15 @@ def lib():
                                                P, P, P]
         L.nopfs_ref_prefetch_order.argtypes = [jp, P, P, P, ctypes.c_int32, P, P]
         L.nopfs_ref_staging_schedule.argtypes = [jp, P, P, ctypes.c_int64, P]
+        L.nopfs_ref_fetch_model_rows.argtypes = [jp, P, P, P, ctypes.POINTER(RefModel),
+                                                 ctypes.c_int64, ctypes.c_int64, P, P]
         for name in ("nopfs_ref_stream_shape", "nopfs_ref_epoch_keys",
                      "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms",
                      "nopfs_ref_access_streams", "nopfs_ref_access_stats",
                      "nopfs_ref_reuse_next", "nopfs_ref_tier_plan",
                      "nopfs_ref_sample_columns", "nopfs_ref_access_stats_rows",
                      "nopfs_ref_reuse_next_rows", "nopfs_ref_prefetch_order",
-                     "nopfs_ref_staging_schedule"):
+                     "nopfs_ref_staging_schedule", "nopfs_ref_fetch_model_rows"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -215,6 +236,25 @@ def staging_schedule(job: RefJob, R, sizes, d0):
     _check(lib().nopfs_ref_staging_schedule(ctypes.byref(job), _ptr(R), _ptr(sizes), int(d0),
                                             _ptr(fill)), "staging_schedule")
     return fill
+
+
+def fetch_model(job: RefJob, R, tier, sizes, model: RefModel, rows=None):
+    """(src, t) for the given workers (default all): src int16 fetch source
+    (0 PFS, 128 + j remote tier j, 256 + j own tier j, -1 padding), t float64
+    consumption time in seconds (-1 in padding). R holds those workers' rows;
+    tier is the placement of all N workers."""
+    _, M, _ = stream_shape(job)
+    i0, i1 = (0, job.N) if rows is None else rows
+    R = np.ascontiguousarray(R, dtype=np.int32)
+    tier = np.ascontiguousarray(tier, dtype=np.int8)
+    sizes = np.ascontiguousarray(sizes, dtype=np.int64)
+    assert R.shape == (i1 - i0, M) and tier.shape == (job.N, job.F)
+    src = np.empty((i1 - i0, M), np.int16)
+    t = np.empty((i1 - i0, M), np.float64)
+    _check(lib().nopfs_ref_fetch_model_rows(ctypes.byref(job), _ptr(R), _ptr(tier), _ptr(sizes),
+                                            ctypes.byref(model), int(i0), int(i1), _ptr(src),
+                                            _ptr(t)), "fetch_model")
+    return src, t
 
 
 def sample_columns(job: RefJob, samples):
