@@ -9,7 +9,9 @@ reads the job issues (A = N * E * L) over the device time of one step.
 After the timed steps, the per-tier prefetch queues and the staging
 schedule of the planned job (the step's outputs as inputs, the workload's
 staging-buffer capacity as d0) are timed the same way and reported under
-"schedule"; they are not part of the step.
+"schedule", and the performance model's fetch sources and consumption times
+(the simulated cluster's parameters) under "model"; they are not part of the
+step.
 
 Prints ONE JSON line. Per-kernel durations come from HIP events recorded by
 the library around each of its launches, on the stream it launches on, over
@@ -84,6 +86,16 @@ def schedule_algorithmic_bytes(job, M, M_w):
     prefetch = {"seg_partition": 4 * A, "pf_tile": NF, "pf_write": 4 * NM}
     staging = {"seg_partition": 4 * A, "st_tile": 8 * job.F, "st_fill": 4 * NM}
     return prefetch, staging
+
+
+def model_algorithmic_bytes(job, M, M_w):
+    """Bytes the performance-model call must move given the dense layouts:
+    R once, every worker's tier of every sample (the holders of each sample)
+    and each sample's size once, and the source (2 B) and time (8 B) of
+    every position."""
+    A = int(sum(M_w))
+    return {"seg_partition": 4 * A, "fm_holders": job.N * job.F + 8 * job.F,
+            "fm_final": 10 * job.N * M}
 
 
 def kernel_source_hash():
@@ -210,30 +222,15 @@ def roofline_of(workload, kernel, alg_bytes, avg_ms):
             "avg_ms": round(avg_ms, 4)}
 
 
-def time_schedule(nopfs, torch, w, job, M, M_w, R, tier, sizes, caps, steps, warmup, stream):
-    """The per-tier prefetch queues and the staging schedule of the planned
-    job (the planning step's own outputs as inputs), each timed over `steps`
-    calls with HIP events on the stream the library launches on."""
-    J = len(caps)
-    d0 = int(w.staging)
-    dev = R.device
-    order = torch.empty((job.N, M), dtype=torch.int32, device=dev)
-    qlen = torch.empty((job.N, J), dtype=torch.int64, device=dev)
-    fill = torch.empty((job.N, M), dtype=torch.int32, device=dev)
-    calls = {
-        "prefetch_order": lambda: nopfs.prefetch_order(job, R, tier, J, order, qlen,
-                                                       stream=stream),
-        "staging_schedule": lambda: nopfs.staging_schedule(job, R, sizes, d0, fill, stream=stream),
-    }
+def time_calls(nopfs, torch, w, calls, algs, steps, warmup, stream, out):
+    """Each call timed over `steps` calls with HIP events on the stream the
+    library launches on; per-kernel times from the library's own events."""
     for _ in range(warmup):
         for f in calls.values():
             f()
     torch.cuda.synchronize()
-    Q = int(qlen.sum())
-    pf_alg, st_alg = schedule_algorithmic_bytes(job, M, M_w)
-    out = {"J": J, "d0_bytes": d0, "queued": Q}
     for name, f in calls.items():
-        alg = pf_alg if name == "prefetch_order" else st_alg
+        alg = algs[name]
         nopfs.profile_enable(True)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
@@ -263,6 +260,48 @@ def time_schedule(nopfs, torch, w, job, M, M_w, R, tier, sizes, caps, steps, war
     return out
 
 
+def time_schedule(nopfs, torch, w, job, M, M_w, R, tier, sizes, caps, steps, warmup, stream):
+    """The per-tier prefetch queues and the staging schedule of the planned
+    job (the planning step's own outputs as inputs)."""
+    J = len(caps)
+    d0 = int(w.staging)
+    dev = R.device
+    order = torch.empty((job.N, M), dtype=torch.int32, device=dev)
+    qlen = torch.empty((job.N, J), dtype=torch.int64, device=dev)
+    fill = torch.empty((job.N, M), dtype=torch.int32, device=dev)
+    calls = {
+        "prefetch_order": lambda: nopfs.prefetch_order(job, R, tier, J, order, qlen,
+                                                       stream=stream),
+        "staging_schedule": lambda: nopfs.staging_schedule(job, R, sizes, d0, fill, stream=stream),
+    }
+    pf_alg, st_alg = schedule_algorithmic_bytes(job, M, M_w)
+    out = time_calls(nopfs, torch, w, calls, {"prefetch_order": pf_alg, "staging_schedule": st_alg},
+                     steps, warmup, stream, {"J": J, "d0_bytes": d0})
+    out["queued"] = int(qlen.sum())
+    return out
+
+
+def time_model(nopfs, torch, wl, w, job, M, M_w, R, tier, sizes, steps, warmup, stream):
+    """Fetch sources and consumption times of the planned job under the
+    performance model with the simulated cluster's parameters."""
+    dev = R.device
+    src = torch.empty((job.N, M), dtype=torch.int16, device=dev)
+    t = torch.empty((job.N, M), dtype=torch.float64, device=dev)
+    model = nopfs.make_model(**wl.LASSEN_MODEL)
+    calls = {"fetch_model": lambda: nopfs.fetch_model(job, R, tier, sizes, model, src, t,
+                                                      stream=stream)}
+    out = time_calls(nopfs, torch, w, calls, {"fetch_model": model_algorithmic_bytes(job, M, M_w)},
+                     steps, warmup, stream, {"params": dict(wl.LASSEN_MODEL)})
+    out["params"]["r"] = list(out["params"]["r"])
+    out["params"]["p"] = list(out["params"]["p"])
+    # per worker: last consumption; over workers the slowest decides
+    last = t.max(dim=1).values
+    out["slowest_worker_s"] = round(float(last.max()), 3)
+    out["sources"] = {"pfs": int((src == 0).sum()), "remote": int(((src >= 128) & (src < 256)).sum()),
+                      "own": int((src >= 256).sum())}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -273,7 +312,7 @@ def main():
     ap.add_argument("--path", choices=["fused", "staged"], default="fused",
                     help="fused: one nopfs_plan_job call per step; staged: the four stage calls")
     ap.add_argument("--no-schedule", action="store_true",
-                    help="skip timing the prefetch queues and staging schedule")
+                    help="skip timing the prefetch queues, staging schedule and model")
     ap.add_argument("--calibrate-bytes", type=int, default=1 << 30,
                     help="size of the calibration copy run after the timed steps")
     ap.add_argument("--rocprof-summary", metavar="DIR",
@@ -361,10 +400,12 @@ def main():
             v["alg_GBps"] = round(alg[k] / (v["avg_ms"] * 1e-3) / 1e9, 1)
     print("[bench] kernels: " + json.dumps(per_kernel), file=sys.stderr, flush=True)
 
-    schedule = None
+    schedule = model = None
     if not args.no_schedule:
         schedule = time_schedule(nopfs, torch, w, job, M, M_w, R, tier, sizes, caps, args.steps,
                                  args.warmup, stream)
+        model = time_model(nopfs, torch, wl, w, job, M, M_w, R, tier, sizes, args.steps,
+                           args.warmup, stream)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -390,6 +431,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "schedule": schedule,
+        "model": model,
     }
     print(json.dumps(line), flush=True)
 

@@ -195,6 +195,52 @@ int nopfs_prefetch_order(const nopfs_job* job, const int32_t* R, const int8_t* t
 int nopfs_staging_schedule(const nopfs_job* job, const int32_t* R, const int64_t* sizes,
                            int64_t d0, int32_t* fill, void* hip_stream);
 
+/* Parameters of the performance model (section 4), in bytes, bytes per
+ * second and seconds (the paper's MB/s are 10^6 bytes per second). Cache
+ * tier j (j = 0..J-1, as in nopfs_tier_plan) is the model's storage class
+ * j + 1; class 0 is the staging buffer. Host memory. */
+typedef struct nopfs_model {
+  double c;          /* compute throughput for training                        */
+  double beta;       /* preprocessing rate                                     */
+  double b_c;        /* inter-worker network bandwidth                         */
+  double pfs_t;      /* aggregate random read throughput of the PFS, t(gamma)  */
+  double pfs_gamma;  /* the number of concurrent PFS readers gamma            */
+  double w0;         /* staging-buffer write throughput with p0 threads        */
+  double p0;         /* prefetch threads of the staging buffer                 */
+  int32_t J;         /* cache tiers, 1 <= J <= 32                              */
+  int32_t reserved;  /* ignored                                                */
+  double r[32];      /* tier j: aggregate random read throughput, p[j] threads */
+  double p[32];      /* tier j: prefetch threads                               */
+} nopfs_model;
+
+/* Fetch sources and consumption times under the performance model
+ * (section 4), with the placement static: sample k is in tier j of worker i
+ * exactly when tier[i][k] == j. Worker i fetches its read f of sample k
+ * (s bytes) from the fastest of the PFS (t(gamma)/gamma), another worker's
+ * tier j (min(b_c, r_j/p_j)) and its own tier j (r_j/p_j), preprocesses and
+ * writes it to the staging buffer (max(s/beta, s/(w0/p0))), and consumes it
+ * at t(f) = max(avail(f), t(f-1) + s(f-1)/c), avail(f) = (sum of the read
+ * times of reads 0..f) / p0; t(0) = avail(0).
+ *   R:     int32 [N][M_max], as for nopfs_access_stats.
+ *   tier:  int8 [N][F], the placement of all workers (entries outside
+ *          [0, J) hold nothing).
+ *   sizes: int64 [F] sample sizes in bytes, 1 <= size < 2^56 (precondition).
+ *   model: HOST, the parameters; all positive and finite.
+ *   src:   int16 [N][M_max], output: 0 = the PFS, 128 + j = another worker's
+ *          tier j, 256 + j = the worker's own tier j; on equal throughput the
+ *          own tier, then a remote one (lower tier first), then the PFS; -1 in
+ *          padding. Exact.
+ *   t:     double [N][M_max], output: consumption times in seconds, -1 in
+ *          padding. Evaluated as prefix sums and a prefix maximum of the
+ *          unrolled recurrence, so it differs from the sequential recurrence
+ *          only by floating-point summation order (at most a few units of
+ *          (f + 2) * 2^-53 * t(f) in practice).
+ * Scratch: about 20 bytes per stream position. Errors: EINVAL (also an invalid
+ * model), ERANGE (J > 32), ENOMEM, EDEVICE. */
+int nopfs_fetch_model(const nopfs_job* job, const int32_t* R, const int8_t* tier,
+                      const int64_t* sizes, const nopfs_model* model, int16_t* src,
+                      double* t, void* hip_stream);
+
 /* Static description of a status code. Never NULL. */
 const char* nopfs_strerror(int code);
 

@@ -1,0 +1,525 @@
+// nopfs_fetch_model: the performance model of the Performance Modeling
+// section evaluated for every read of every worker's stream, with the
+// placement static (a sample is in tier j of worker i exactly when
+// tier[i][k] == j).
+//
+// A read of sample k (s bytes) by worker i is fetched from the fastest of
+// the PFS (t(gamma) / gamma per reader), another worker's tier j
+// (min(b_c, r_j / p_j)) and its own tier j (r_j / p_j); on equal throughput
+// its own tier wins over a remote one and a remote one over the PFS. It is
+// then preprocessed and written to the staging buffer at min(beta, w0 / p0)
+// per thread. With the p0 staging threads load-balanced, read f is in the
+// buffer at avail(f) = (sum of the read times of reads 0..f) / p0, and the
+// worker consumes it at
+//   t(f) = max(avail(f), t(f-1) + s(f-1) / c) = U(f) + max over g <= f of (avail(g) - U(g)),
+// U(f) = sum of s(m) / c over m < f (the recurrence unrolled): a prefix sum
+// and a prefix maximum, evaluated per sub-chunk and combined per worker.
+//
+//   fm_holders -- per sample: the best remote class among all workers'
+//                 copies (highest min(b_c, r_j / p_j), lower tier on ties),
+//                 packed above the sample's size. A worker's own copy may be
+//                 that class: a remote copy of class j is never faster than
+//                 the local copy of j, so counting it never changes a choice.
+//   fm_tile    -- per (group of workers, 8K-sample window) of the partition
+//                 of R: each read's source from its own tier and the
+//                 sample's best remote class; size and source in
+//                 partitioned order.
+//   fm_sum     -- per sub-chunk of 2^14 reads: back to stream order in LDS;
+//                 its read-time sum, compute-time sum and maximum of
+//                 avail - U relative to its start.
+//   fm_scan    -- per worker: what enters each sub-chunk.
+//   fm_final   -- per sub-chunk: the same scans, combined with what enters
+//                 it; source codes and consumption times in stream order.
+#include <math.h>
+
+#include <new>
+
+#include "partition.hpp"
+
+namespace nopfs {
+namespace {
+
+#ifndef NOPFS_FM_GROUP
+#define NOPFS_FM_GROUP 16  // workers per fm_tile workgroup (tuning only)
+#endif
+#ifndef NOPFS_FM_THREADS
+#define NOPFS_FM_THREADS 1024  // threads of the scan kernels (tuning only)
+#endif
+#ifndef NOPFS_FM_FINAL_WAVES
+#define NOPFS_FM_FINAL_WAVES 8  // fm_final's occupancy target (tuning only)
+#endif
+
+constexpr int kMaxClasses = 32;
+constexpr uint32_t kNoClass = 255;
+constexpr int kSizeBits = 56;
+constexpr uint64_t kSizeMask = (uint64_t(1) << kSizeBits) - 1;
+constexpr int kFmWs = 13;
+constexpr int kFmWin = 1 << kFmWs;
+constexpr int kFmGroup = NOPFS_FM_GROUP;
+constexpr int kFmTileThreads = 1024;
+constexpr int kFmThreads = NOPFS_FM_THREADS;
+constexpr int kFmPart = kSC / 4;                // positions per LDS pass
+constexpr int kFmPer = kFmPart / kFmThreads;    // positions per thread and pass
+constexpr int kFmEnt = kSC / kFmThreads;        // entries per thread
+static_assert(kFmPer * kFmThreads == kFmPart && kFmEnt * kFmThreads == kSC, "fm shape");
+
+// Source codes inside the library: 0 the PFS, 1 + j another worker's tier j,
+// 1 + kMaxClasses + j the worker's own tier j.
+constexpr uint32_t kOwn0 = 1 + kMaxClasses;
+
+// Source rates, computed once on the host from the model's parameters.
+struct Rates {
+  double own[kMaxClasses];  // r_j / p_j
+  double rem[kMaxClasses];  // min(b_c, r_j / p_j)
+  double pfs;               // t(gamma) / gamma
+  double wthr;              // min(beta, w0 / p0)
+  double c, p0;
+  // reciprocals for the per-read times (a product instead of a division:
+  // within two units in the last place of the quotient)
+  double inv_own[kMaxClasses], inv_rem[kMaxClasses];
+  double inv_pfs, inv_wthr, inv_c;
+  int32_t J;
+  uint8_t rank_cls[kMaxClasses];  // classes by remote rate, best first, lower tier on ties
+  uint8_t cls_rank[kMaxClasses];  // the inverse
+};
+
+struct SharedRates {
+  double own[kMaxClasses], rem[kMaxClasses];
+  double inv_own[kMaxClasses], inv_rem[kMaxClasses];
+  uint8_t rank_cls[kMaxClasses], cls_rank[kMaxClasses];
+};
+
+__device__ __forceinline__ void load_rates(const Rates& r, SharedRates& s) {
+  if (threadIdx.x < kMaxClasses) {
+    s.own[threadIdx.x] = r.own[threadIdx.x];
+    s.rem[threadIdx.x] = r.rem[threadIdx.x];
+    s.inv_own[threadIdx.x] = r.inv_own[threadIdx.x];
+    s.inv_rem[threadIdx.x] = r.inv_rem[threadIdx.x];
+    s.rank_cls[threadIdx.x] = r.rank_cls[threadIdx.x];
+    s.cls_rank[threadIdx.x] = r.cls_rank[threadIdx.x];
+  }
+}
+
+// 1 / (the rate of a source code)
+__device__ __forceinline__ double inv_rate_of(const Rates& r, const SharedRates& s, uint32_t code) {
+  return code == 0 ? r.inv_pfs : (code < kOwn0 ? s.inv_rem[code - 1] : s.inv_own[code - kOwn0]);
+}
+
+// ---------------------------------------------------------------- holders --
+__global__ void __launch_bounds__(256)
+fm_holders(int64_t F, int64_t N, const int8_t* __restrict__ tier, const int64_t* __restrict__ sizes,
+           Rates rt, uint64_t* __restrict__ szb) {
+  __shared__ SharedRates sr;
+  load_rates(rt, sr);
+  __syncthreads();
+  const int64_t k = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (k >= F) return;
+  uint32_t best = kNoClass;  // as a rank: lower is better
+  constexpr int kRows = 8;
+  for (int64_t i0 = 0; i0 < N; i0 += kRows) {
+    int32_t q[kRows];
+#pragma unroll
+    for (int u = 0; u < kRows; ++u) q[u] = i0 + u < N ? tier[(i0 + u) * F + k] : -1;
+#pragma unroll
+    for (int u = 0; u < kRows; ++u)
+      if (q[u] >= 0 && q[u] < rt.J) {
+        const uint32_t rk = sr.cls_rank[q[u]];
+        best = rk < best ? rk : best;
+      }
+  }
+  const uint64_t cls = best == kNoClass ? kNoClass : sr.rank_cls[best];
+  szb[k] = (uint64_t(sizes[k]) & kSizeMask) | (cls << kSizeBits);
+}
+
+// ------------------------------------------------------------------ tiles --
+__device__ __forceinline__ uint32_t choose(const Rates& rt, const SharedRates& sr, int32_t own,
+                                           uint32_t b1) {
+  double best = -1;
+  uint32_t code = 0;
+  if (own >= 0 && own < rt.J) {
+    best = sr.own[own];
+    code = kOwn0 + uint32_t(own);
+  }
+  if (b1 != kNoClass && sr.rem[b1] > best) {
+    best = sr.rem[b1];
+    code = 1 + b1;
+  }
+  if (rt.pfs > best) code = 0;
+  return code;
+}
+
+__global__ void __launch_bounds__(kFmTileThreads)
+fm_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
+        const int8_t* __restrict__ tier, const uint64_t* __restrict__ szb, Rates rt,
+        uint64_t* __restrict__ zP, uint32_t ntiles) {
+  __shared__ uint64_t sz[kFmWin];
+  __shared__ SharedRates sr;
+  // group-major tiles: a group's consecutive windows run together on one XCD
+  const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
+  if (tile >= ntiles) return;
+  const int64_t g = tile / p.nbk;
+  const uint32_t kb = tile - uint32_t(g) * p.nbk;
+  const int64_t i0 = g * kFmGroup;
+  const int64_t gw = p.N - i0 < kFmGroup ? p.N - i0 : kFmGroup;
+  const int64_t k0 = int64_t(kb) << p.ws;
+  const int64_t kend = k0 + (int64_t(1) << p.ws) < p.F ? k0 + (int64_t(1) << p.ws) : p.F;
+  const int64_t runs = int64_t(p.E) * p.nsc;
+  const uint32_t nsc = uint32_t(p.nsc);
+  load_rates(rt, sr);
+  for (int64_t w0 = k0; w0 < kend; w0 += kFmWin) {
+    const uint32_t wl = uint32_t(kend - w0 < kFmWin ? kend - w0 : kFmWin);
+    const uint32_t xoff = uint32_t(w0 - k0);
+    for (uint32_t x = threadIdx.x; x < wl; x += kFmTileThreads) sz[x] = szb[w0 + x];
+    __syncthreads();
+    for (int64_t pr = threadIdx.x; pr < gw * runs; pr += kFmTileThreads) {
+      const int64_t i = i0 + pr / runs;
+      const int64_t r = pr - (i - i0) * runs;
+      const int64_t Li = seg_len(p, i);
+      const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;
+      const uint32_t ra = oa[r], rb = oa[runs + r];
+      const uint32_t e = uint32_t(r) / nsc, sc = uint32_t(r) - e * nsc;
+      const int64_t fb = int64_t(e) * Li + int64_t(sc) * kSC;
+      const uint32_t* src = Pk + i * p.M_max + fb;
+      const int8_t* trow = tier + i * p.F + w0;
+      uint64_t* zrow = zP + i * p.M_max + fb;
+      for (uint32_t q = ra; q < rb; q += kRunBatch) {
+        uint32_t x[kRunBatch];
+        int32_t own[kRunBatch];
+#pragma unroll
+        for (int u = 0; u < kRunBatch; ++u)
+          x[u] = q + u < rb ? (src[q + u] >> kScShift) - xoff : 0xFFFFFFFFu;
+#pragma unroll
+        for (int u = 0; u < kRunBatch; ++u) own[u] = x[u] < wl ? trow[x[u]] : -1;
+#pragma unroll
+        for (int u = 0; u < kRunBatch; ++u)
+          if (x[u] < wl) {
+            const uint64_t sb = sz[x[u]];
+            const uint32_t code = choose(rt, sr, own[u], uint32_t(sb >> kSizeBits));
+            zrow[q + u] = (sb & kSizeMask) | (uint64_t(code) << kSizeBits);
+          }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------ scans --
+__device__ __forceinline__ double wave_incl_sum(double v) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const double o = __shfl_up(v, d, 64);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+__device__ __forceinline__ double wave_incl_max(double v) {
+  const int lane = __lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const double o = __shfl_up(v, d, 64);
+    if (lane >= d) v = fmax(v, o);
+  }
+  return v;
+}
+
+// Exclusive prefix (sum, or max with -inf as identity) of v over the
+// workgroup; *total gets the sum / maximum of all. tmp holds 65 doubles.
+template <bool kMax>
+__device__ __forceinline__ double block_excl(double v, double* tmp, double* total) {
+  const int lane = __lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  const double id = kMax ? -INFINITY : 0.0;
+  const double inc = kMax ? wave_incl_max(v) : wave_incl_sum(v);
+  if (lane == 63) tmp[wave] = inc;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const double w = threadIdx.x < unsigned(nwaves) ? tmp[threadIdx.x] : id;
+    const double wi = kMax ? wave_incl_max(w) : wave_incl_sum(w);
+    const double prev = __shfl_up(wi, 1, 64);
+    if (threadIdx.x < unsigned(nwaves)) tmp[threadIdx.x] = threadIdx.x == 0 ? id : prev;
+    if (threadIdx.x == 63) tmp[64] = wi;
+  }
+  __syncthreads();
+  const double before_lane = __shfl_up(inc, 1, 64);
+  const double in_wave = lane == 0 ? id : before_lane;
+  const double r = kMax ? fmax(tmp[wave], in_wave) : tmp[wave] + in_wave;
+  *total = tmp[64];
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ int fm_slot(int p) { return p + p / kFmPer; }
+
+struct FmLds {
+  uint64_t sv[kFmPart + kFmPart / kFmPer];  // entries, then results, by position
+  uint16_t pos[kSC];                        // stream position of each entry
+  double tmp[65];
+  SharedRates sr;
+};
+
+// What enters sub-chunk c of worker i: read-time sum and compute-time sum
+// of the reads before it, and the largest avail(g) - U(g) over them.
+struct Enter {
+  double a, u, m;
+};
+
+// One sub-chunk in stream order: per position, its code and the scans.
+// kFinal: also the consumption times t and source codes, written out.
+template <bool kFinal>
+__device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* __restrict__ Pk,
+                         const uint64_t* __restrict__ zP, const Rates& rt, FmLds& L, Enter in,
+                         Enter* sum_out, int16_t* __restrict__ src, double* __restrict__ tout) {
+  // stream position of every entry (in LDS); each entry's payload is
+  // loaded in the part that holds its position (once per entry)
+  for (int64_t q = threadIdx.x; q < s.len; q += kFmThreads)
+    L.pos[q] = uint16_t(Pk[s.base + q] & kJMask);
+  __syncthreads();
+  const double inv_p0 = 1.0 / rt.p0;
+  double ca = 0, cu = 0, cm = -INFINITY;  // running over the parts, relative to the chunk
+  const double base_mu = in.a * inv_p0 - in.u;
+  for (int64_t j0 = 0; j0 < s.len; j0 += kFmPart) {
+    const uint32_t hl = uint32_t(s.len - j0 < kFmPart ? s.len - j0 : kFmPart);
+#pragma unroll 4
+    for (int u = 0; u < kFmEnt; ++u) {
+      const int64_t q = int64_t(u) * kFmThreads + threadIdx.x;
+      const uint32_t x = q < s.len ? uint32_t(L.pos[q]) - uint32_t(j0) : 0xFFFFFFFFu;
+      if (x < hl) L.sv[fm_slot(int(x))] = zP[s.base + q];
+    }
+    __syncthreads();
+    double rd[kFmPer], uu[kFmPer];
+    uint32_t cd[kFmPer];
+    double ta = 0, tu = 0;
+#pragma unroll
+    for (int u = 0; u < kFmPer; ++u) {
+      const int x = int(threadIdx.x) * kFmPer + u;
+      rd[u] = 0;
+      uu[u] = 0;
+      cd[u] = 0;
+      if (x < int(hl)) {
+        const uint64_t e = L.sv[fm_slot(x)];
+        const double sz = double(e & kSizeMask);
+        cd[u] = uint32_t(e >> kSizeBits);
+        rd[u] = sz * inv_rate_of(rt, L.sr, cd[u]) + sz * rt.inv_wthr;
+        uu[u] = sz * rt.inv_c;
+      }
+      ta += rd[u];
+      tu += uu[u];
+    }
+    double tota, totu;
+    const double exa = block_excl<false>(ta, L.tmp, &tota);
+    const double exu = block_excl<false>(tu, L.tmp, &totu);
+    // avail - U at each position, relative to the chunk start
+    double mv[kFmPer];
+    double ra = ca + exa, ru = cu + exu, tm = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kFmPer; ++u) {
+      const int x = int(threadIdx.x) * kFmPer + u;
+      ra += rd[u];
+      mv[u] = x < int(hl) ? ra * inv_p0 - ru : -INFINITY;
+      ru += uu[u];
+      tm = fmax(tm, mv[u]);
+    }
+    double totm;
+    const double exm = block_excl<true>(tm, L.tmp, &totm);
+    if (kFinal) {
+      // t at each position: U(f) + max(what entered, base + best so far)
+      double tv[kFmPer];
+      double run = fmax(cm, exm);
+      double uf = cu + exu;
+#pragma unroll
+      for (int u = 0; u < kFmPer; ++u) {
+        run = fmax(run, mv[u]);
+        tv[u] = (in.u + uf) + fmax(in.m, base_mu + run);
+        uf += uu[u];
+      }
+      __syncthreads();  // every entry is read
+#pragma unroll
+      for (int u = 0; u < kFmPer; ++u)
+        L.sv[fm_slot(int(threadIdx.x) * kFmPer + u)] = __double_as_longlong(tv[u]);
+      __syncthreads();
+      double* td = tout + s.base + j0;
+#pragma unroll
+      for (int u = 0; u < kFmPer; ++u) {
+        const int x = u * kFmThreads + int(threadIdx.x);
+        if (x < int(hl)) td[x] = __longlong_as_double(L.sv[fm_slot(x)]);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kFmPer; ++u) {
+        const uint32_t c = cd[u];
+        const uint64_t out = c == 0 ? 0u : (c < kOwn0 ? 128u + (c - 1) : 256u + (c - kOwn0));
+        L.sv[fm_slot(int(threadIdx.x) * kFmPer + u)] = out;
+      }
+      __syncthreads();
+      int16_t* sd = src + s.base + j0;
+#pragma unroll
+      for (int u = 0; u < kFmPer; ++u) {
+        const int x = u * kFmThreads + int(threadIdx.x);
+        if (x < int(hl)) sd[x] = int16_t(L.sv[fm_slot(x)]);
+      }
+    }
+    ca += tota;
+    cu += totu;
+    cm = fmax(cm, totm);
+    __syncthreads();
+  }
+  if (!kFinal && threadIdx.x == 0) *sum_out = Enter{ca, cu, cm};
+}
+
+// two workgroups per CU
+__global__ void __launch_bounds__(kFmThreads) __attribute__((amdgpu_waves_per_eu(8)))
+fm_sum(SegParams p, const uint32_t* __restrict__ Pk, const uint64_t* __restrict__ zP, Rates rt,
+       uint32_t nch, Enter* __restrict__ sums) {
+  __shared__ FmLds L;
+  load_rates(rt, L.sr);
+  const SubChunk s = sub_chunk(p, nch, blockIdx.x);
+  __syncthreads();
+  fm_chunk<false>(p, s, Pk, zP, rt, L, Enter{0, 0, 0}, &sums[s.i * nch + s.c], nullptr, nullptr);
+}
+
+// In place: sums[i][c] becomes what enters sub-chunk c.
+__global__ void __launch_bounds__(256)
+fm_scan(int64_t N, uint32_t nch, double p0, Enter* __restrict__ sums) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= N) return;
+  Enter* row = sums + i * nch;
+  const double inv_p0 = 1.0 / p0;
+  double a = 0, u = 0, m = -INFINITY;
+  for (uint32_t c = 0; c < nch; ++c) {
+    const Enter x = row[c];
+    row[c] = Enter{a, u, m};
+    m = fmax(m, a * inv_p0 - u + x.m);
+    a += x.a;
+    u += x.u;
+  }
+}
+
+__global__ void __launch_bounds__(kFmThreads)
+__attribute__((amdgpu_waves_per_eu(NOPFS_FM_FINAL_WAVES)))
+fm_final(SegParams p, const uint32_t* __restrict__ Pk, const uint64_t* __restrict__ zP, Rates rt,
+         uint32_t nch, const Enter* __restrict__ ins, int16_t* __restrict__ src,
+         double* __restrict__ t) {
+  __shared__ FmLds L;
+  load_rates(rt, L.sr);
+  const SubChunk s = sub_chunk(p, nch, blockIdx.x);
+  if (s.c == int64_t(nch) - 1) {
+    // the row's padding past its last read
+    for (int64_t f = int64_t(p.E) * s.Li + threadIdx.x; f < p.M_max; f += kFmThreads) {
+      src[s.i * p.M_max + f] = -1;
+      t[s.i * p.M_max + f] = -1.0;
+    }
+  }
+  __syncthreads();
+  fm_chunk<true>(p, s, Pk, zP, rt, L, ins[s.i * nch + s.c], nullptr, src, t);
+}
+
+int model_check(const nopfs_model* m) {
+  if (!m) return fail(NOPFS_EINVAL, "model is NULL");
+  if (m->J < 1) return fail(NOPFS_EINVAL, "model J must be >= 1");
+  if (m->J > kMaxClasses) return fail(NOPFS_ERANGE, "model J must be <= 32");
+  const double v[7] = {m->c, m->beta, m->b_c, m->pfs_t, m->pfs_gamma, m->w0, m->p0};
+  for (double x : v)
+    if (!(x > 0) || !isfinite(x)) return fail(NOPFS_EINVAL, "model rates and counts must be positive and finite");
+  for (int32_t j = 0; j < m->J; ++j)
+    if (!(m->r[j] > 0) || !(m->p[j] > 0) || !isfinite(m->r[j]) || !isfinite(m->p[j]))
+      return fail(NOPFS_EINVAL, "model rates and counts must be positive and finite");
+  return NOPFS_OK;
+}
+
+Rates make_rates(const nopfs_model* m) {
+  Rates r{};
+  r.J = m->J;
+  for (int32_t j = 0; j < kMaxClasses; ++j) {
+    r.own[j] = j < m->J ? m->r[j] / m->p[j] : 0;
+    r.rem[j] = j < m->J ? (m->b_c < r.own[j] ? m->b_c : r.own[j]) : 0;
+  }
+  r.pfs = m->pfs_t / m->pfs_gamma;
+  const double wb = m->w0 / m->p0;
+  r.wthr = m->beta < wb ? m->beta : wb;
+  r.c = m->c;
+  r.p0 = m->p0;
+  for (int32_t j = 0; j < kMaxClasses; ++j) {
+    r.inv_own[j] = j < m->J ? 1.0 / r.own[j] : 0;
+    r.inv_rem[j] = j < m->J ? 1.0 / r.rem[j] : 0;
+  }
+  r.inv_pfs = 1.0 / r.pfs;
+  r.inv_wthr = 1.0 / r.wthr;
+  r.inv_c = 1.0 / r.c;
+  // classes ranked by remote rate (higher first), lower tier on ties
+  int32_t order[kMaxClasses];
+  for (int32_t j = 0; j < m->J; ++j) order[j] = j;
+  for (int32_t a = 1; a < m->J; ++a)
+    for (int32_t b = a; b > 0 && r.rem[order[b]] > r.rem[order[b - 1]]; --b) {
+      const int32_t x = order[b];
+      order[b] = order[b - 1];
+      order[b - 1] = x;
+    }
+  for (int32_t q = 0; q < kMaxClasses; ++q) {
+    r.rank_cls[q] = q < m->J ? uint8_t(order[q]) : uint8_t(kNoClass);
+    r.cls_rank[q] = uint8_t(kNoClass);
+  }
+  for (int32_t q = 0; q < m->J; ++q) r.cls_rank[order[q]] = uint8_t(q);
+  return r;
+}
+
+int model_impl(const nopfs_job* job, const int32_t* R, const int8_t* tier, const int64_t* sizes,
+               const nopfs_model* model, int16_t* src, double* t, hipStream_t st) {
+  Shape s;
+  int rc = make_shape(job, &s);
+  if (rc) return rc;
+  if ((rc = model_check(model))) return rc;
+  if (!tier || !sizes) return fail(NOPFS_EINVAL, "tier and sizes must be non-NULL");
+  if (s.M_max == 0) return NOPFS_OK;
+  if (!R || !src || !t) return fail(NOPFS_EINVAL, "R, src and t must be non-NULL");
+  const Rates rt = make_rates(model);
+  const SegParams p = seg_params(s, kFmWs);
+  const uint32_t nch = uint32_t(s.E * p.nsc);  // sub-chunks per worker
+  const uint32_t ngroups = uint32_t(ceil_div(s.N, kFmGroup));
+  const int64_t nblk = s.N * int64_t(nch);
+  const int64_t ntiles = int64_t(p.nbk) * ngroups;
+  if (nblk >= (int64_t(1) << 31) || ntiles >= (int64_t(1) << 31))
+    return fail(NOPFS_ERANGE, "job too large for one launch");
+  Scratch scr(st);
+  uint64_t *szb, *zP;
+  uint32_t* Pk;
+  uint16_t* OT;
+  Enter* sums;
+  if ((rc = scr.alloc_n(&szb, size_t(s.F)))) return rc;
+  if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
+  if ((rc = scr.alloc_n(&zP, size_t(s.N * s.M_max)))) return rc;
+  if ((rc = scr.alloc_n(&sums, size_t(nblk)))) return rc;
+  if ((rc = launch("fm_holders", fm_holders, dim3(uint32_t(ceil_div(s.F, 256))), dim3(256), 0, st,
+                   s.F, s.N, tier, sizes, rt, szb)))
+    return rc;
+  if ((rc = launch("fm_tile", fm_tile, dim3(xcd_padded(uint32_t(ntiles))), dim3(kFmTileThreads), 0,
+                   st, p, (const uint32_t*)Pk, (const uint16_t*)OT, tier, (const uint64_t*)szb, rt,
+                   zP, uint32_t(ntiles))))
+    return rc;
+  if ((rc = launch("fm_sum", fm_sum, dim3(uint32_t(nblk)), dim3(kFmThreads), 0, st, p,
+                   (const uint32_t*)Pk, (const uint64_t*)zP, rt, nch, sums)))
+    return rc;
+  if ((rc = launch("fm_scan", fm_scan, dim3(uint32_t(ceil_div(s.N, 256))), dim3(256), 0, st, s.N,
+                   nch, rt.p0, sums)))
+    return rc;
+  return launch("fm_final", fm_final, dim3(uint32_t(nblk)), dim3(kFmThreads), 0, st, p,
+                (const uint32_t*)Pk, (const uint64_t*)zP, rt, nch, (const Enter*)sums, src, t);
+}
+
+}  // namespace
+}  // namespace nopfs
+
+extern "C" int nopfs_fetch_model(const nopfs_job* job, const int32_t* R, const int8_t* tier,
+                                 const int64_t* sizes, const nopfs_model* model, int16_t* src,
+                                 double* t, void* hip_stream) {
+  try {
+    return nopfs::model_impl(job, R, tier, sizes, model, src, t,
+                             static_cast<hipStream_t>(hip_stream));
+  } catch (const std::bad_alloc&) {
+    return nopfs::fail(NOPFS_ENOMEM, "host allocation failed");
+  } catch (...) {
+    return nopfs::fail(NOPFS_EDEVICE, "unexpected host exception");
+  }
+}

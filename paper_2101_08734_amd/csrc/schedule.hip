@@ -64,44 +64,7 @@ namespace {
 constexpr int kSchedWs = 13;             // partition windows: 2^13 samples
 constexpr int kWin = 1 << kSchedWs;      // samples per LDS pass of a tile
 constexpr int kTileThreads = 256;
-constexpr int kRunBatch = 8;             // loads in flight per run walk
 constexpr int kPfMaxJ = 128;
-
-__device__ __forceinline__ int64_t sub_len(int64_t Li, int64_t sc) {
-  const int64_t len = Li - sc * kSC;
-  return len < 0 ? 0 : (len > kSC ? kSC : len);
-}
-
-// Calls fn(fb, q, v) for every read of runs r = r0, r0 + stride, ... of
-// window kb of worker i: fb is the stream position of the run's sub-chunk,
-// q the read's index in the sub-chunk's partitioned entries (its
-// partitioned position is fb + q) and v the packed read.
-template <typename Fn>
-__device__ __forceinline__ void walk_runs(const SegParams& p, int64_t i, uint32_t kb,
-                                          const uint32_t* __restrict__ Pk,
-                                          const uint16_t* __restrict__ OT, int64_t r0,
-                                          int64_t stride, Fn fn) {
-  const int64_t Li = seg_len(p, i);
-  const int64_t runs = int64_t(p.E) * p.nsc;
-  const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;  // run starts in window kb
-  const uint16_t* ob = oa + runs;                            // run ends
-  const uint32_t* prow = Pk + i * p.M_max;
-  const uint32_t nsc = uint32_t(p.nsc);
-  for (int64_t r = r0; r < runs; r += stride) {
-    const uint32_t ra = oa[r], rb = ob[r];
-    const uint32_t e = uint32_t(r) / nsc, sc = uint32_t(r) - e * nsc;
-    const int64_t fb = int64_t(e) * Li + int64_t(sc) * kSC;
-    const uint32_t* src = prow + fb;
-    for (uint32_t q = ra; q < rb; q += kRunBatch) {
-      uint32_t v[kRunBatch];
-#pragma unroll
-      for (int u = 0; u < kRunBatch; ++u) v[u] = q + u < rb ? src[q + u] : 0u;
-#pragma unroll
-      for (int u = 0; u < kRunBatch; ++u)
-        if (q + u < rb) fn(fb, q + u, v[u]);
-    }
-  }
-}
 
 // ------------------------------------------------------------- prefetch --
 constexpr int kPfKeep = 8;  // reads per thread kept in registers between the passes
@@ -224,23 +187,6 @@ pf_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict
 // writes, are dropped so every queue slot stays inside the row).
 __device__ __forceinline__ uint32_t clamp_code(uint32_t m, int32_t J) {
   return m <= uint32_t(J) ? m : 0u;
-}
-
-// Sub-chunk c = e * nsc + sc of worker i covers stream positions
-// [e*Li + sc*kSC, + len).
-struct SubChunk {
-  int64_t i, c, Li, len, base;  // base: offset of its first position in [N][M_max]
-};
-
-__device__ __forceinline__ SubChunk sub_chunk(const SegParams& p, uint32_t nch, uint32_t blk) {
-  SubChunk s;
-  s.i = blk / nch;
-  s.c = blk - s.i * nch;
-  const int64_t e = s.c / p.nsc, sc = s.c - e * p.nsc;
-  s.Li = seg_len(p, s.i);
-  s.len = sub_len(s.Li, sc);
-  s.base = s.i * p.M_max + e * s.Li + sc * kSC;
-  return s;
 }
 
 // cnt layout: [N][nch][J]. Order of positions does not matter for counting,

@@ -47,6 +47,26 @@ class Job:
                     int(self.drop_last), int(self.seed) & ((1 << 64) - 1))
 
 
+class Model(ctypes.Structure):
+    """Parameters of the performance model (nopfs_model): bytes, bytes/s,
+    seconds; r and p per cache tier."""
+    _fields_ = [("c", ctypes.c_double), ("beta", ctypes.c_double), ("b_c", ctypes.c_double),
+                ("pfs_t", ctypes.c_double), ("pfs_gamma", ctypes.c_double),
+                ("w0", ctypes.c_double), ("p0", ctypes.c_double),
+                ("J", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("r", ctypes.c_double * 32), ("p", ctypes.c_double * 32)]
+
+
+def make_model(c, beta, b_c, pfs_t, pfs_gamma, w0, p0, r, p) -> Model:
+    m = Model()
+    m.c, m.beta, m.b_c = float(c), float(beta), float(b_c)
+    m.pfs_t, m.pfs_gamma, m.w0, m.p0 = float(pfs_t), float(pfs_gamma), float(w0), float(p0)
+    m.J = len(r)
+    for j, (rj, pj) in enumerate(zip(list(r)[:32], list(p)[:32])):
+        m.r[j], m.p[j] = float(rj), float(pj)
+    return m
+
+
 _lib = None
 
 
@@ -70,6 +90,7 @@ def lib() -> ctypes.CDLL:
             "nopfs_plan_job": [jp, P, P, I32, P, P, P, P, P, P, P],
             "nopfs_prefetch_order": [jp, P, P, I32, P, P, P],
             "nopfs_staging_schedule": [jp, P, P, I64, P, P],
+            "nopfs_fetch_model": [jp, P, P, P, ctypes.POINTER(Model), P, P, P],
             "nopfs_profile_enable": [ctypes.c_int],
             "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
                                     ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)],
@@ -90,7 +111,7 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_stats",
             "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_prefetch_order",
-            "nopfs_staging_schedule", "nopfs_strerror",
+            "nopfs_staging_schedule", "nopfs_fetch_model", "nopfs_strerror",
             "nopfs_last_error", "nopfs_profile_enable", "nopfs_profile_query",
             "nopfs_calibration_copy", "nopfs_debug_set")
 
@@ -251,6 +272,28 @@ def staging_schedule(job: Job, R, sizes, d0, fill=None, stream=None):
     _check(lib().nopfs_staging_schedule(ctypes.byref(j), _ptr(R), _ptr(sizes), int(d0), _ptr(fill),
                                         _stream(stream)), "nopfs_staging_schedule")
     return fill
+
+
+def fetch_model(job: Job, R, tier, sizes, model: Model, src=None, t=None, stream=None):
+    """Fetch source and consumption time of every read under the performance
+    model (nopfs_fetch_model): src [N][M_max] int16 (0 PFS, 128 + j another
+    worker's tier j, 256 + j own tier j, -1 padding), t [N][M_max] float64
+    seconds (-1 padding)."""
+    _, M, _ = stream_shape(job)
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    _device_tensor(tier, torch.int8, (job.N, job.F), "tier")
+    _device_tensor(sizes, torch.int64, (job.F,), "sizes")
+    if src is None:
+        src = torch.empty((job.N, M), dtype=torch.int16, device="cuda")
+    if t is None:
+        t = torch.empty((job.N, M), dtype=torch.float64, device="cuda")
+    _device_tensor(src, torch.int16, (job.N, M), "src")
+    _device_tensor(t, torch.float64, (job.N, M), "t")
+    j = job.c()
+    _check(lib().nopfs_fetch_model(ctypes.byref(j), _ptr(R), _ptr(tier), _ptr(sizes),
+                                   ctypes.byref(model), _ptr(src), _ptr(t), _stream(stream)),
+           "nopfs_fetch_model")
+    return src, t
 
 
 def plan(job: Job, sizes, caps, stream=None):

@@ -75,6 +75,16 @@ WORKLOADS = {
 
 ORDER = ["small", "imagenet1k", "imagenet1k_256", "imagenet22k", "cosmoflow"]
 
+# Performance-model parameters of the simulated small cluster (Lassen-like
+# benchmarks of the Performance Simulator section), in bytes and bytes/s:
+# compute 64 MB/s, preprocessing 200 MB/s, network 24,000 MB/s; staging
+# buffer with 8 threads at 111 GB/s (its write rate taken equal to its read
+# rate, the only one given); RAM with 4 threads at 85 GB/s, SSD with 2
+# threads at 4 GB/s (the cache tiers, fastest first); PFS 2,870 MB/s at 8
+# readers (per reader t(8)/8; larger reader counts are taken at that rate).
+LASSEN_MODEL = dict(c=64e6, beta=200e6, b_c=24e9, pfs_t=2870e6, pfs_gamma=8, w0=111e9, p0=8,
+                    r=(85e9, 4e9), p=(4, 2))
+
 
 def sizes(w: Workload) -> np.ndarray:
     """Per-sample byte sizes, int64, length F."""

@@ -74,6 +74,9 @@ def test_invalid_jobs(L, kw, code):
     assert L.nopfs_tier_plan(ctypes.byref(j), FAKE, FAKE, FAKE, caps, 1, FAKE, FAKE, None) == code
     assert L.nopfs_prefetch_order(ctypes.byref(j), FAKE, FAKE, 1, FAKE, FAKE, None) == code
     assert L.nopfs_staging_schedule(ctypes.byref(j), FAKE, FAKE, 10, FAKE, None) == code
+    m = _model()
+    assert L.nopfs_fetch_model(ctypes.byref(j), FAKE, FAKE, FAKE, ctypes.byref(m), FAKE, FAKE,
+                               None) == code
     assert L.nopfs_last_error()  # a detail string is recorded
 
 
@@ -124,6 +127,43 @@ def test_schedule_argument_checks(L):
     assert ss(ctypes.byref(empty), None, FAKE, 5, None, None) == 0
 
 
+def _model(**kw):
+    d = dict(c=64e6, beta=200e6, b_c=24e9, pfs_t=2870e6, pfs_gamma=8, w0=111e9, p0=8,
+             r=[85e9, 4e9], p=[4, 2])
+    d.update(kw)
+    return nopfs.make_model(**d)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(c=0.0), nopfs.NOPFS_EINVAL), (dict(beta=-1.0), nopfs.NOPFS_EINVAL),
+    (dict(b_c=float("nan")), nopfs.NOPFS_EINVAL), (dict(p0=float("inf")), nopfs.NOPFS_EINVAL),
+    (dict(pfs_gamma=0.0), nopfs.NOPFS_EINVAL), (dict(r=[85e9, 0.0]), nopfs.NOPFS_EINVAL),
+    (dict(p=[4, -2]), nopfs.NOPFS_EINVAL), (dict(r=[], p=[]), nopfs.NOPFS_EINVAL),
+    (dict(r=[1e9] * 33, p=[1] * 33), nopfs.NOPFS_ERANGE),
+])
+def test_model_argument_checks(L, kw, code):
+    j = _job()
+    m = _model(**kw)
+    if len(kw.get("r", [])) > 32:
+        m.J = 33
+    assert L.nopfs_fetch_model(ctypes.byref(j), FAKE, FAKE, FAKE, ctypes.byref(m), FAKE, FAKE,
+                               None) == code
+
+
+def test_model_null_pointers(L):
+    j = _job()
+    m = _model()
+    fm = L.nopfs_fetch_model
+    E = nopfs.NOPFS_EINVAL
+    assert fm(ctypes.byref(j), FAKE, FAKE, FAKE, None, FAKE, FAKE, None) == E
+    assert fm(ctypes.byref(j), FAKE, None, FAKE, ctypes.byref(m), FAKE, FAKE, None) == E
+    assert fm(ctypes.byref(j), FAKE, FAKE, None, ctypes.byref(m), FAKE, FAKE, None) == E
+    assert fm(ctypes.byref(j), None, FAKE, FAKE, ctypes.byref(m), FAKE, FAKE, None) == E
+    assert fm(ctypes.byref(j), FAKE, FAKE, FAKE, ctypes.byref(m), None, FAKE, None) == E
+    assert fm(ctypes.byref(j), FAKE, FAKE, FAKE, ctypes.byref(m), FAKE, None, None) == E
+    assert fm(None, FAKE, FAKE, FAKE, ctypes.byref(m), FAKE, FAKE, None) == E
+
+
 def test_scratch_failure_is_enomem(L):
     """The test hook fails the next internal allocation; the call reports
     NOPFS_ENOMEM before launching anything."""
@@ -136,6 +176,8 @@ def test_scratch_failure_is_enomem(L):
         lambda: L.nopfs_tier_plan(ctypes.byref(j), FAKE, FAKE, FAKE, caps, 1, FAKE, FAKE, None),
         lambda: L.nopfs_prefetch_order(ctypes.byref(j), FAKE, FAKE, 1, FAKE, FAKE, None),
         lambda: L.nopfs_staging_schedule(ctypes.byref(j), FAKE, FAKE, 10, FAKE, None),
+        lambda: L.nopfs_fetch_model(ctypes.byref(j), FAKE, FAKE, FAKE, ctypes.byref(_model()),
+                                    FAKE, FAKE, None),
     ]
     for call in calls:
         assert L.nopfs_debug_set(3, 1) == 0

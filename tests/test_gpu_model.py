@@ -1,0 +1,208 @@
+"""Fetch sources and consumption times under the performance model on the
+GPU vs the CPU oracle.
+
+Stage isolation: R and the placement are the oracle's own (streams, stats
+and plan on the host). Source codes are compared element by element and
+must be identical: both sides compare the same double-precision rates
+formed the same way. Consumption times are sums of the same positive terms
+taken in a different order (the oracle follows the recurrence read by read;
+the GPU evaluates prefix sums and a prefix maximum of the unrolled form),
+so they are compared within the bound that summation order allows: every
+partial sum of n positive terms is within n * 2^-53 of itself relative to
+its value, the terms t is built from (read-time sums / p0 and compute-time
+sums) are each at most t(last), and the two evaluations take at most
+(2n + 2) and (3n + 3) rounded steps, so |difference| <= 8 (n + 2) 2^-53
+t(last) on a row of n reads.
+
+Sizes span many 8K-sample windows and 16K-read sub-chunks with ragged
+tails; parameter sets cover compute-bound and I/O-bound streams, a network
+slower than the PFS, equal rates everywhere (the order of preference alone
+decides), J = 1 and more tiers than the placement uses, and arbitrary
+placements. ImageNet-1k runs against the full oracle; at ImageNet-22k size,
+seeded synthetic streams and placements are compared on sampled workers.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from paper_2101_08734_amd import nopfs  # noqa: E402
+from paper_2101_08734_amd import workloads as wl  # noqa: E402
+
+EPS = 2.0 ** -53
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    nopfs.lib()
+    yield
+    torch.cuda.empty_cache()
+
+
+JOBS = [
+    # name, F, E, N, B, drop_last, seed, caps as fractions of the total size
+    ("small", 10_000, 5, 4, 16, 1, 42, (0.004, 0.02)),
+    ("ragged", 30_011, 5, 3, 7, 0, 3, (0.05, 0.2)),
+    ("medium", 150_000, 7, 8, 16, 1, 9, (0.02, 0.1, 0.3)),
+    ("many_epochs", 2_000, 60, 16, 1, 0, 11, (0.1, 0.5)),
+    ("e255", 700, 255, 5, 3, 1, 12, (0.05, 0.25)),
+    ("wide", 20_000, 3, 300, 2, 1, 13, (0.3,)),
+    ("n_gt_f", 50, 4, 64, 1, 0, 14, (0.5, 0.5)),
+    ("one_sample", 1, 3, 1, 1, 1, 15, (0.0, 1.0)),
+    ("one_worker", 40_000, 4, 1, 64, 1, 16, (0.25, 0.25)),
+    ("long_rows", 400_000, 2, 2, 1000, 0, 18, (0.01, 0.6)),
+]
+IDS = [j[0] for j in JOBS]
+
+
+def _oracle_inputs(oracle, F, E, N, B, d, seed, fr):
+    sizes = wl.random_sizes(F, seed, 1_000, 2_000_000)
+    tot = int(sizes.sum())
+    caps = np.array([int(f * tot) for f in fr], np.int64)
+    job = oracle.make_job(F, E, N, B, d, seed)
+    return job, sizes, oracle.full_pipeline(job, sizes, caps)
+
+
+def _params(J, **kw):
+    d = dict(wl.LASSEN_MODEL)
+    d["r"] = list(d["r"]) + [1e9] * max(0, J - 2)
+    d["p"] = list(d["p"]) + [1] * max(0, J - 2)
+    d["r"], d["p"] = d["r"][:J], d["p"][:J]
+    d.update(kw)
+    return d
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def compare(name, job_t, src_g, t_g, src_o, t_o):
+    src_g = src_g.cpu().numpy()
+    t_g = t_g.cpu().numpy()
+    if not np.array_equal(src_g, src_o):
+        bad = np.argwhere(src_g != src_o)
+        raise AssertionError(f"{name}: src {len(bad)} mismatches, first {bad[:5].tolist()} "
+                             f"got {src_g[tuple(bad[0])]} expected {src_o[tuple(bad[0])]}")
+    pad = src_o < 0
+    assert (t_g[pad] == -1.0).all(), name
+    for i in range(t_o.shape[0]):
+        n = int((~pad[i]).sum())
+        if n == 0:
+            continue
+        last = t_o[i, n - 1]
+        tol = 8 * (n + 2) * EPS * last
+        err = np.abs(t_g[i, :n] - t_o[i, :n]).max()
+        assert err <= tol, (name, i, err, tol)
+
+
+@pytest.mark.parametrize("name,F,E,N,B,d,seed,fr", JOBS, ids=IDS)
+def test_matches_oracle(oracle, name, F, E, N, B, d, seed, fr):
+    rjob, sizes, out = _oracle_inputs(oracle, F, E, N, B, d, seed, fr)
+    job = nopfs.Job(F, E, N, B, d, seed)
+    J = len(fr)
+    prm = _params(J)
+    src_o, t_o = oracle.fetch_model(rjob, out["R"], out["tier"], sizes, oracle.make_model(**prm))
+    src_g, t_g = nopfs.fetch_model(job, _dev(out["R"]), _dev(out["tier"]), _dev(sizes),
+                                   nopfs.make_model(**prm))
+    torch.cuda.synchronize()
+    compare(name, job, src_g, t_g, src_o, t_o)
+
+
+REGIMES = {
+    "io_bound": dict(c=64e9),
+    "slow_network": dict(b_c=1e6),
+    "all_equal": dict(b_c=2e9, pfs_t=16e9, pfs_gamma=8, r=(8e9, 4e9), p=(4, 2)),
+    "ssd_faster_than_ram": dict(r=(4e9, 85e9)),
+    "one_thread_staging": dict(p0=1, w0=1e9),
+}
+
+
+@pytest.mark.parametrize("regime", list(REGIMES))
+@pytest.mark.parametrize("name,F,E,N,B,d,seed,fr", [JOBS[1], JOBS[2], JOBS[5]],
+                         ids=[JOBS[1][0], JOBS[2][0], JOBS[5][0]])
+def test_parameter_regimes(oracle, name, F, E, N, B, d, seed, fr, regime):
+    rjob, sizes, out = _oracle_inputs(oracle, F, E, N, B, d, seed, fr)
+    job = nopfs.Job(F, E, N, B, d, seed)
+    J = len(fr)
+    prm = _params(J)
+    prm.update(REGIMES[regime])
+    # one rate and thread count per tier of the placement
+    prm["r"] = (list(prm["r"]) + [1e9] * J)[:J]
+    prm["p"] = (list(prm["p"]) + [1] * J)[:J]
+    src_o, t_o = oracle.fetch_model(rjob, out["R"], out["tier"], sizes, oracle.make_model(**prm))
+    src_g, t_g = nopfs.fetch_model(job, _dev(out["R"]), _dev(out["tier"]), _dev(sizes),
+                                   nopfs.make_model(**prm))
+    torch.cuda.synchronize()
+    compare(f"{name}/{regime}", job, src_g, t_g, src_o, t_o)
+
+
+@pytest.mark.parametrize("J", [1, 3, 6, 32])
+def test_arbitrary_placement(oracle, J):
+    """Any placement over a valid stream, tiers outside [0, J) included."""
+    F, E, N, B, d, seed = 60_000, 6, 5, 10, 0, 23
+    rjob = oracle.make_job(F, E, N, B, d, seed)
+    R = oracle.access_streams(rjob)
+    rng = np.random.default_rng(J)
+    tier = rng.integers(-3, 9, size=(N, F)).astype(np.int8)
+    sizes = wl.random_sizes(F, 7, 1, 5_000_000)
+    prm = dict(wl.LASSEN_MODEL)
+    prm["r"] = [float(x) for x in rng.uniform(1e9, 1e11, J)]
+    prm["p"] = [float(x) for x in rng.integers(1, 9, J)]
+    job = nopfs.Job(F, E, N, B, d, seed)
+    src_o, t_o = oracle.fetch_model(rjob, R, tier, sizes, oracle.make_model(**prm))
+    src_g, t_g = nopfs.fetch_model(job, _dev(R), _dev(tier), _dev(sizes), nopfs.make_model(**prm))
+    torch.cuda.synchronize()
+    compare(f"J={J}", job, src_g, t_g, src_o, t_o)
+
+
+def test_zero_iterations():
+    job = nopfs.Job(10, 2, 4, 3, 1, 17)  # T = 0, M_max = 0
+    R = torch.empty((4, 0), dtype=torch.int32, device="cuda")
+    tier = torch.zeros((4, 10), dtype=torch.int8, device="cuda")
+    sizes = torch.ones(10, dtype=torch.int64, device="cuda")
+    src, t = nopfs.fetch_model(job, R, tier, sizes, nopfs.make_model(**wl.LASSEN_MODEL))
+    torch.cuda.synchronize()
+    assert src.shape == (4, 0) and t.shape == (4, 0)
+
+
+def test_imagenet1k_full(oracle, imagenet1k_expected):
+    w = wl.WORKLOADS["imagenet1k"]
+    rjob = oracle.make_job(*w.job_tuple())
+    sizes = wl.sizes(w)
+    out = imagenet1k_expected
+    src_o, t_o = oracle.fetch_model(rjob, out["R"], out["tier"], sizes,
+                                    oracle.make_model(**wl.LASSEN_MODEL))
+    job = nopfs.Job(*w.job_tuple())
+    src_g, t_g = nopfs.fetch_model(job, _dev(out["R"]), _dev(out["tier"]), _dev(sizes),
+                                   nopfs.make_model(**wl.LASSEN_MODEL))
+    torch.cuda.synchronize()
+    compare("imagenet1k", job, src_g, t_g, src_o, t_o)
+
+
+def test_imagenet22k_sampled_rows(oracle):
+    """The benchmarked shape (14.2M samples, 256 workers, 40 epochs) with a
+    seeded synthetic stream and placement (any stream of valid sample ids and
+    any placement are valid inputs); the oracle evaluates three sampled
+    workers from the same inputs."""
+    w = wl.WORKLOADS["imagenet22k"]
+    job = nopfs.Job(*w.job_tuple())
+    _, M, Mw = nopfs.stream_shape(job)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(22)
+    R = torch.randint(0, w.F, (w.N, M), generator=gen, device="cuda", dtype=torch.int32)
+    tier = torch.randint(-1, 2, (w.N, w.F), generator=gen, device="cuda", dtype=torch.int8)
+    sizes_h = wl.sizes(w)
+    src_g, t_g = nopfs.fetch_model(job, R, tier, _dev(sizes_h), nopfs.make_model(**wl.LASSEN_MODEL))
+    torch.cuda.synchronize()
+    rjob = oracle.make_job(*w.job_tuple())
+    tier_h = tier.cpu().numpy()
+    m = oracle.make_model(**wl.LASSEN_MODEL)
+    for i in (0, 131, 255):
+        src_o, t_o = oracle.fetch_model(rjob, R[i:i + 1].cpu().numpy(), tier_h, sizes_h, m,
+                                        rows=(i, i + 1))
+        compare(f"imagenet22k row {i}", job, src_g[i:i + 1], t_g[i:i + 1], src_o, t_o)
+    del R, tier, src_g, t_g
+    torch.cuda.empty_cache()
