@@ -519,6 +519,91 @@ int nopfs_ref_fetch_model_rows(const nopfs_ref_job* job, const int32_t* R,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Clairvoyant buffer (section 3). Held entries are keyed by the stream     */
+/* position of their next use, so at position f the sample read is held     */
+/* exactly when key f is. A binary max-heap of keys with lazy deletion (a   */
+/* popped key that is no longer held is skipped) gives the furthest entry. */
+/* ------------------------------------------------------------------------ */
+static void heap_push(int32_t* h, int64_t* n, int32_t key) {
+  int64_t i = (*n)++;
+  h[i] = key;
+  while (i > 0 && h[(i - 1) / 2] < h[i]) {
+    int32_t t = h[i];
+    h[i] = h[(i - 1) / 2];
+    h[(i - 1) / 2] = t;
+    i = (i - 1) / 2;
+  }
+}
+
+static int32_t heap_pop(int32_t* h, int64_t* n) {
+  int32_t top = h[0];
+  h[0] = h[--(*n)];
+  int64_t i = 0;
+  for (;;) {
+    int64_t l = 2 * i + 1, r = l + 1, m = i;
+    if (l < *n && h[l] > h[m]) m = l;
+    if (r < *n && h[r] > h[m]) m = r;
+    if (m == i) break;
+    int32_t t = h[i];
+    h[i] = h[m];
+    h[m] = t;
+    i = m;
+  }
+  return top;
+}
+
+int nopfs_ref_buffer_sim(const nopfs_ref_job* job, const int32_t* R, const int32_t* next,
+                         const int64_t* sizes, int64_t d0, int8_t* hit, int64_t* hits) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!sizes || !hits || d0 < 0) return REF_EINVAL;
+  if (M_max > 0 && (!R || !next || !hit)) return REF_EINVAL;
+  uint8_t* held = (uint8_t*)malloc((size_t)(M_max > 0 ? M_max : 1));
+  int32_t* heap = (int32_t*)malloc((size_t)(M_max > 0 ? M_max : 1) * sizeof(int32_t));
+  if (!held || !heap) { free(held); free(heap); return REF_ENOMEM; }
+  for (int64_t i = 0; i < job->N; ++i) {
+    const int32_t* Ri = R + i * M_max;
+    const int32_t* Xi = next + i * M_max;
+    int8_t* Hi = hit + i * M_max;
+    int64_t Mi = job->E * epoch_len(job, i);
+    memset(held, 0, (size_t)(M_max > 0 ? M_max : 1));
+    int64_t nh = 0, used = 0, h_count = 0, h_bytes = 0;
+    for (int64_t f = 0; f < Mi; ++f) {
+      int64_t s = sizes[Ri[f]];
+      if (held[f]) { /* the sample is in the buffer: a hit; its entry ends here */
+        Hi[f] = 1;
+        h_count++;
+        h_bytes += s;
+        held[f] = 0;
+        used -= s;
+      } else {
+        Hi[f] = 0;
+      }
+      int32_t nx = Xi[f];
+      if (nx >= 0 && s <= d0) { /* admit under the next use, then discard furthest */
+        held[nx] = 1;
+        heap_push(heap, &nh, nx);
+        used += s;
+        while (used > d0) {
+          int32_t x = heap_pop(heap, &nh);
+          if (!held[x]) continue; /* stale key */
+          held[x] = 0;
+          used -= sizes[Ri[x]];
+        }
+      }
+    }
+    for (int64_t f = Mi; f < M_max; ++f) Hi[f] = -1;
+    hits[i * 2] = h_count;
+    hits[i * 2 + 1] = h_bytes;
+    nh = 0;
+  }
+  free(held);
+  free(heap);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Sampled columns. The position of sample s in epoch e is, by definition   */
 /* of the sorted order, the number of samples whose (key, id) is smaller.   */
 /* Everything else for s follows from its positions in the E epochs.        */

@@ -119,6 +119,19 @@ int nopfs_ref_fetch_model_rows(const nopfs_ref_job* job, const int32_t* R,
                                const nopfs_ref_model* m, int64_t i0, int64_t i1,
                                int16_t* src, double* t);
 
+/* Clairvoyant buffer of d0 bytes (section 3: Belady's replacement, the
+ * optimal-replacement and do-no-harm rules), per worker, from R, next and
+ * the sizes. The buffer holds samples keyed by their next use; an access is
+ * a hit when its sample is held. After an access with a next use the sample
+ * is (re)admitted under that key, then, while the held bytes exceed d0, the
+ * entry whose next use is furthest is discarded (possibly the admitted one:
+ * nothing used before it is ever discarded for it). A sample with no next
+ * use, or larger than d0, is not admitted.
+ *   hit[N][M_max]: 1 hit, 0 miss, -1 padding; hits[N][2]: hit count and
+ *   hit bytes per worker. */
+int nopfs_ref_buffer_sim(const nopfs_ref_job* job, const int32_t* R, const int32_t* next,
+                         const int64_t* sizes, int64_t d0, int8_t* hit, int64_t* hits);
+
 /* Per-sample columns for S chosen samples, computed one sample at a time
  * from the definition of the shuffle (for checks at sizes where the full
  * oracle is too slow):

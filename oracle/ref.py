@@ -88,13 +88,15 @@ def lib():
         L.nopfs_ref_staging_schedule.argtypes = [jp, P, P, ctypes.c_int64, P]
         L.nopfs_ref_fetch_model_rows.argtypes = [jp, P, P, P, ctypes.POINTER(RefModel),
                                                  ctypes.c_int64, ctypes.c_int64, P, P]
+        L.nopfs_ref_buffer_sim.argtypes = [jp, P, P, P, ctypes.c_int64, P, P]
         for name in ("nopfs_ref_stream_shape", "nopfs_ref_epoch_keys",
                      "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms",
                      "nopfs_ref_access_streams", "nopfs_ref_access_stats",
                      "nopfs_ref_reuse_next", "nopfs_ref_tier_plan",
                      "nopfs_ref_sample_columns", "nopfs_ref_access_stats_rows",
                      "nopfs_ref_reuse_next_rows", "nopfs_ref_prefetch_order",
-                     "nopfs_ref_staging_schedule", "nopfs_ref_fetch_model_rows"):
+                     "nopfs_ref_staging_schedule", "nopfs_ref_fetch_model_rows",
+                     "nopfs_ref_buffer_sim"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -255,6 +257,19 @@ def fetch_model(job: RefJob, R, tier, sizes, model: RefModel, rows=None):
                                             ctypes.byref(model), int(i0), int(i1), _ptr(src),
                                             _ptr(t)), "fetch_model")
     return src, t
+
+
+def buffer_sim(job: RefJob, R, nxt, sizes, d0):
+    """(hit [N][M_max] int8: 1 hit, 0 miss, -1 padding; hits [N][2]: hit count
+    and hit bytes) of a clairvoyant buffer of d0 bytes per worker."""
+    R = np.ascontiguousarray(R, dtype=np.int32)
+    nxt = np.ascontiguousarray(nxt, dtype=np.int32)
+    sizes = np.ascontiguousarray(sizes, dtype=np.int64)
+    hit = np.empty(R.shape, np.int8)
+    hits = np.empty((job.N, 2), np.int64)
+    _check(lib().nopfs_ref_buffer_sim(ctypes.byref(job), _ptr(R), _ptr(nxt), _ptr(sizes), int(d0),
+                                      _ptr(hit), _ptr(hits)), "buffer_sim")
+    return hit, hits
 
 
 def sample_columns(job: RefJob, samples):
