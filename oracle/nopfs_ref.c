@@ -554,18 +554,25 @@ static int32_t heap_pop(int32_t* h, int64_t* n) {
 
 int nopfs_ref_buffer_sim(const nopfs_ref_job* job, const int32_t* R, const int32_t* next,
                          const int64_t* sizes, int64_t d0, int8_t* hit, int64_t* hits) {
+  return nopfs_ref_buffer_sim_rows(job, R, 0, job ? job->N : 0, next, sizes, d0, hit, hits);
+}
+
+int nopfs_ref_buffer_sim_rows(const nopfs_ref_job* job, const int32_t* R, int64_t i0, int64_t i1,
+                              const int32_t* next, const int64_t* sizes, int64_t d0, int8_t* hit,
+                              int64_t* hits) {
   int64_t M_max;
   int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
   if (rc) return rc;
+  if (i0 < 0 || i1 > job->N || i0 > i1) return REF_EINVAL;
   if (!sizes || !hits || d0 < 0) return REF_EINVAL;
   if (M_max > 0 && (!R || !next || !hit)) return REF_EINVAL;
   uint8_t* held = (uint8_t*)malloc((size_t)(M_max > 0 ? M_max : 1));
   int32_t* heap = (int32_t*)malloc((size_t)(M_max > 0 ? M_max : 1) * sizeof(int32_t));
   if (!held || !heap) { free(held); free(heap); return REF_ENOMEM; }
-  for (int64_t i = 0; i < job->N; ++i) {
-    const int32_t* Ri = R + i * M_max;
-    const int32_t* Xi = next + i * M_max;
-    int8_t* Hi = hit + i * M_max;
+  for (int64_t i = i0; i < i1; ++i) {
+    const int32_t* Ri = R + (i - i0) * M_max;
+    const int32_t* Xi = next + (i - i0) * M_max;
+    int8_t* Hi = hit + (i - i0) * M_max;
     int64_t Mi = job->E * epoch_len(job, i);
     memset(held, 0, (size_t)(M_max > 0 ? M_max : 1));
     int64_t nh = 0, used = 0, h_count = 0, h_bytes = 0;
@@ -594,8 +601,8 @@ int nopfs_ref_buffer_sim(const nopfs_ref_job* job, const int32_t* R, const int32
       }
     }
     for (int64_t f = Mi; f < M_max; ++f) Hi[f] = -1;
-    hits[i * 2] = h_count;
-    hits[i * 2 + 1] = h_bytes;
+    hits[(i - i0) * 2] = h_count;
+    hits[(i - i0) * 2 + 1] = h_bytes;
     nh = 0;
   }
   free(held);

@@ -131,6 +131,11 @@ int nopfs_ref_fetch_model_rows(const nopfs_ref_job* job, const int32_t* R,
  *   hit bytes per worker. */
 int nopfs_ref_buffer_sim(const nopfs_ref_job* job, const int32_t* R, const int32_t* next,
                          const int64_t* sizes, int64_t d0, int8_t* hit, int64_t* hits);
+/* The same for workers [i0, i1) only: R, next and hit hold those rows,
+ * hits holds their [i1 - i0][2] totals. */
+int nopfs_ref_buffer_sim_rows(const nopfs_ref_job* job, const int32_t* R, int64_t i0, int64_t i1,
+                              const int32_t* next, const int64_t* sizes, int64_t d0, int8_t* hit,
+                              int64_t* hits);
 
 /* Per-sample columns for S chosen samples, computed one sample at a time
  * from the definition of the shuffle (for checks at sizes where the full

@@ -89,6 +89,8 @@ def lib():
         L.nopfs_ref_fetch_model_rows.argtypes = [jp, P, P, P, ctypes.POINTER(RefModel),
                                                  ctypes.c_int64, ctypes.c_int64, P, P]
         L.nopfs_ref_buffer_sim.argtypes = [jp, P, P, P, ctypes.c_int64, P, P]
+        L.nopfs_ref_buffer_sim_rows.argtypes = [jp, P, ctypes.c_int64, ctypes.c_int64, P, P,
+                                                ctypes.c_int64, P, P]
         for name in ("nopfs_ref_stream_shape", "nopfs_ref_epoch_keys",
                      "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms",
                      "nopfs_ref_access_streams", "nopfs_ref_access_stats",
@@ -96,7 +98,7 @@ def lib():
                      "nopfs_ref_sample_columns", "nopfs_ref_access_stats_rows",
                      "nopfs_ref_reuse_next_rows", "nopfs_ref_prefetch_order",
                      "nopfs_ref_staging_schedule", "nopfs_ref_fetch_model_rows",
-                     "nopfs_ref_buffer_sim"):
+                     "nopfs_ref_buffer_sim", "nopfs_ref_buffer_sim_rows"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -259,16 +261,21 @@ def fetch_model(job: RefJob, R, tier, sizes, model: RefModel, rows=None):
     return src, t
 
 
-def buffer_sim(job: RefJob, R, nxt, sizes, d0):
+def buffer_sim(job: RefJob, R, nxt, sizes, d0, rows=None):
     """(hit [N][M_max] int8: 1 hit, 0 miss, -1 padding; hits [N][2]: hit count
-    and hit bytes) of a clairvoyant buffer of d0 bytes per worker."""
+    and hit bytes) of a clairvoyant buffer of d0 bytes per worker. With rows =
+    (i0, i1), R and nxt hold only those workers' rows and so do the results."""
     R = np.ascontiguousarray(R, dtype=np.int32)
     nxt = np.ascontiguousarray(nxt, dtype=np.int32)
     sizes = np.ascontiguousarray(sizes, dtype=np.int64)
+    i0, i1 = (0, job.N) if rows is None else rows
     hit = np.empty(R.shape, np.int8)
-    hits = np.empty((job.N, 2), np.int64)
-    _check(lib().nopfs_ref_buffer_sim(ctypes.byref(job), _ptr(R), _ptr(nxt), _ptr(sizes), int(d0),
-                                      _ptr(hit), _ptr(hits)), "buffer_sim")
+    hits = np.empty((i1 - i0, 2), np.int64)
+    if R.shape[0] != i1 - i0 or nxt.shape != R.shape:
+        raise ValueError("R and nxt must hold the rows asked for")
+    _check(lib().nopfs_ref_buffer_sim_rows(ctypes.byref(job), _ptr(R), i0, i1, _ptr(nxt),
+                                           _ptr(sizes), int(d0), _ptr(hit), _ptr(hits)),
+           "buffer_sim")
     return hit, hits
 
 

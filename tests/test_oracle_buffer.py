@@ -161,3 +161,19 @@ def test_argument_errors(oracle):
     nx = oracle.reuse_next(job, R)
     with pytest.raises(Exception):
         oracle.buffer_sim(job, R, nx, np.ones(10, np.int64), -1)
+
+
+def test_rows_match_full(oracle):
+    """Workers are independent: a range of rows gives those rows of the full
+    result (the sampled-row check at the largest size relies on this)."""
+    F, E, N, B, d = 3_001, 4, 5, 7, 0
+    job = oracle.make_job(F, E, N, B, d, 21)
+    R = oracle.access_streams(job)
+    nx = oracle.reuse_next(job, R)
+    sizes = wl.random_sizes(F, 22, 1_000, 2_000_000)
+    hit, hits = oracle.buffer_sim(job, R, nx, sizes, 50_000_000)
+    for i0, i1 in ((0, 1), (2, 5), (4, 5), (1, 1)):
+        h, t = oracle.buffer_sim(job, R[i0:i1], nx[i0:i1], sizes, 50_000_000, rows=(i0, i1))
+        assert np.array_equal(h, hit[i0:i1]) and np.array_equal(t, hits[i0:i1])
+    with pytest.raises(Exception):
+        oracle.buffer_sim(job, R[:2], nx[:2], sizes, 1, rows=(4, 6))
