@@ -241,6 +241,29 @@ int nopfs_fetch_model(const nopfs_job* job, const int32_t* R, const int8_t* tier
                       const int64_t* sizes, const nopfs_model* model, int16_t* src,
                       double* t, void* hip_stream);
 
+/* Clairvoyant buffer of d0 bytes per worker (section 3: Belady's
+ * replacement, discard the sample whose next use is furthest in the future,
+ * and never one used before the sample being brought in). The buffer holds
+ * samples keyed by their next use; read f of worker i hits when its sample
+ * is held. After a read with a next use the sample is (re)admitted under
+ * it, then, while the held bytes exceed d0, the entry used furthest in the
+ * future is discarded (possibly the admitted one). A sample with no next
+ * use, or larger than d0, is not admitted. With all sizes equal this is
+ * Belady's optimal replacement with bypass.
+ *   R, next: int32 [N][M_max], as written by nopfs_access_streams and
+ *            nopfs_reuse_next for this job (precondition; other contents give
+ *            unspecified but in-bounds results).
+ *   sizes:   int64 [F] sample sizes in bytes, >= 1.
+ *   d0:      buffer capacity in bytes, >= 0.
+ *   hit:     int8 [N][M_max], output: 1 hit, 0 miss, -1 padding.
+ *   hits:    int64 [N][2], output: hits and hit bytes per worker.
+ * The replay is sequential per worker (one wave each). M_max < 2^24.
+ * Scratch: about 8 bytes per stream position. Errors: EINVAL (also d0 < 0),
+ * ERANGE (M_max >= 2^24), ENOMEM, EDEVICE. */
+int nopfs_buffer_sim(const nopfs_job* job, const int32_t* R, const int32_t* next,
+                     const int64_t* sizes, int64_t d0, int8_t* hit, int64_t* hits,
+                     void* hip_stream);
+
 /* Static description of a status code. Never NULL. */
 const char* nopfs_strerror(int code);
 

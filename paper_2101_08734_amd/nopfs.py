@@ -91,6 +91,7 @@ def lib() -> ctypes.CDLL:
             "nopfs_prefetch_order": [jp, P, P, I32, P, P, P],
             "nopfs_staging_schedule": [jp, P, P, I64, P, P],
             "nopfs_fetch_model": [jp, P, P, P, ctypes.POINTER(Model), P, P, P],
+            "nopfs_buffer_sim": [jp, P, P, P, I64, P, P, P],
             "nopfs_profile_enable": [ctypes.c_int],
             "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
                                     ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)],
@@ -111,7 +112,8 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_stats",
             "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_prefetch_order",
-            "nopfs_staging_schedule", "nopfs_fetch_model", "nopfs_strerror",
+            "nopfs_staging_schedule", "nopfs_fetch_model", "nopfs_buffer_sim",
+            "nopfs_strerror",
             "nopfs_last_error", "nopfs_profile_enable", "nopfs_profile_query",
             "nopfs_calibration_copy", "nopfs_debug_set")
 
@@ -294,6 +296,26 @@ def fetch_model(job: Job, R, tier, sizes, model: Model, src=None, t=None, stream
                                    ctypes.byref(model), _ptr(src), _ptr(t), _stream(stream)),
            "nopfs_fetch_model")
     return src, t
+
+
+def buffer_sim(job: Job, R, next, sizes, d0, hit=None, hits=None, stream=None):
+    """Clairvoyant buffer of d0 bytes per worker (nopfs_buffer_sim): hit
+    [N][M_max] int8 (1 hit, 0 miss, -1 padding), hits [N][2] int64 (hits, hit
+    bytes)."""
+    _, M, _ = stream_shape(job)
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    _device_tensor(next, torch.int32, (job.N, M), "next")
+    _device_tensor(sizes, torch.int64, (job.F,), "sizes")
+    if hit is None:
+        hit = torch.empty((job.N, M), dtype=torch.int8, device="cuda")
+    if hits is None:
+        hits = torch.empty((job.N, 2), dtype=torch.int64, device="cuda")
+    _device_tensor(hit, torch.int8, (job.N, M), "hit")
+    _device_tensor(hits, torch.int64, (job.N, 2), "hits")
+    j = job.c()
+    _check(lib().nopfs_buffer_sim(ctypes.byref(j), _ptr(R), _ptr(next), _ptr(sizes), int(d0),
+                                  _ptr(hit), _ptr(hits), _stream(stream)), "nopfs_buffer_sim")
+    return hit, hits
 
 
 def plan(job: Job, sizes, caps, stream=None):

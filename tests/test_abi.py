@@ -164,6 +164,29 @@ def test_model_null_pointers(L):
     assert fm(None, FAKE, FAKE, FAKE, ctypes.byref(m), FAKE, FAKE, None) == E
 
 
+def test_buffer_argument_checks(L):
+    j = _job()
+    bs = L.nopfs_buffer_sim
+    E = nopfs.NOPFS_EINVAL
+    assert bs(ctypes.byref(j), FAKE, FAKE, FAKE, -1, FAKE, FAKE, None) == E
+    assert bs(None, FAKE, FAKE, FAKE, 10, FAKE, FAKE, None) == E
+    assert bs(ctypes.byref(j), None, FAKE, FAKE, 10, FAKE, FAKE, None) == E
+    assert bs(ctypes.byref(j), FAKE, None, FAKE, 10, FAKE, FAKE, None) == E
+    assert bs(ctypes.byref(j), FAKE, FAKE, None, 10, FAKE, FAKE, None) == E
+    assert bs(ctypes.byref(j), FAKE, FAKE, FAKE, 10, None, FAKE, None) == E
+    assert bs(ctypes.byref(j), FAKE, FAKE, FAKE, 10, FAKE, None, None) == E
+    bad = _job(B=0)
+    assert bs(ctypes.byref(bad), FAKE, FAKE, FAKE, 10, FAKE, FAKE, None) == E
+    # a worker's stream of 2^24 reads or more is refused before any device work
+    big = _job(F=1 << 24, E=1, N=1, B=1)
+    assert bs(ctypes.byref(big), FAKE, FAKE, FAKE, 10, FAKE, FAKE, None) == nopfs.NOPFS_ERANGE
+    ok = _job(F=(1 << 24) - 1, E=1, N=1, B=1)
+    assert nopfs.stream_shape(nopfs.Job((1 << 24) - 1, 1, 1, 1, 1, 1))[1] == (1 << 24) - 1
+    assert L.nopfs_debug_set(3, 1) == 0
+    assert bs(ctypes.byref(ok), FAKE, FAKE, FAKE, 10, FAKE, FAKE, None) == nopfs.NOPFS_ENOMEM
+    assert L.nopfs_debug_set(3, 0) == 0
+
+
 def test_scratch_failure_is_enomem(L):
     """The test hook fails the next internal allocation; the call reports
     NOPFS_ENOMEM before launching anything."""
@@ -178,6 +201,7 @@ def test_scratch_failure_is_enomem(L):
         lambda: L.nopfs_staging_schedule(ctypes.byref(j), FAKE, FAKE, 10, FAKE, None),
         lambda: L.nopfs_fetch_model(ctypes.byref(j), FAKE, FAKE, FAKE, ctypes.byref(_model()),
                                     FAKE, FAKE, None),
+        lambda: L.nopfs_buffer_sim(ctypes.byref(j), FAKE, FAKE, FAKE, 10, FAKE, FAKE, None),
     ]
     for call in calls:
         assert L.nopfs_debug_set(3, 1) == 0
