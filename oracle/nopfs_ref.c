@@ -519,6 +519,101 @@ int nopfs_ref_fetch_model_rows(const nopfs_ref_job* job, const int32_t* R,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Policy simulation (section 6: the Perfect, Naive, StagingBuffer and       */
+/* NoPFS policies on the section 4 model). For read f of a worker, with      */
+/* s its size: u(f) = s / c is its compute time, read(f) = fetch(f) +       */
+/* write(f) the time to stage it, write(f) = max(s / beta, s / (w0 / p0)),  */
+/* fetch(f) = s over the throughput of its source.                          */
+/*   Perfect:       never stalls: t(0) = 0, t(f) = t(f-1) + u(f-1).         */
+/*   Naive:         one read at a time from the PFS, after the previous     */
+/*                  compute: t(0) = read(0), t(f) = t(f-1) + u(f-1) + read(f)*/
+/*   StagingBuffer: p0 threads stage the reads in stream order from the PFS */
+/*   NoPFS:         the same, each read from the source src gives.          */
+/* The two staging policies keep Q(f), the thread-time spent staging reads  */
+/* 0..f (so avail(f) = Q(f) / p0 as in section 4), with the buffer of d0    */
+/* bytes as the extra condition that read f can start only once the reads   */
+/* before fill(f) (the staging schedule) are consumed:                      */
+/*   Q(f) = max(Q(f-1), p0 * t(fill(f) - 1)) + read(f)   (t(-1) = 0),       */
+/*   t(0) = Q(0) / p0,  t(f) = max(Q(f) / p0, t(f-1) + u(f-1)).             */
+/* finish = t(last) + u(last); io[c] sums fetch times by source class c:    */
+/* 0 the PFS, 1 + j another worker's tier j, 1 + J + j the own tier j.      */
+/* ------------------------------------------------------------------------ */
+int nopfs_ref_policy_sim_rows(const nopfs_ref_job* job, const int32_t* R, const int64_t* sizes,
+                              const int16_t* src, const int32_t* fill, const nopfs_ref_model* m,
+                              int32_t policy, int64_t i0, int64_t i1, double* t, double* finish,
+                              double* io) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!sizes || !model_ok(m) || policy < 0 || policy > 3) return REF_EINVAL;
+  if (i0 < 0 || i1 > job->N || i0 > i1) return REF_EINVAL;
+  if (i1 > i0 && (!finish || !io)) return REF_EINVAL;
+  if (M_max > 0 && i1 > i0) {
+    if (!R || !t) return REF_EINVAL;
+    if (policy >= 2 && !fill) return REF_EINVAL;
+    if (policy == 3 && !src) return REF_EINVAL;
+  }
+  const int32_t J = m->J;
+  const int64_t K = 1 + 2 * (int64_t)J;
+  const double pfs = m->pfs_t / m->pfs_gamma;
+  for (int64_t i = i0; i < i1; ++i) {
+    const int64_t row = (i - i0) * M_max;
+    double* ti = t ? t + row : NULL;
+    double* ioi = io + (i - i0) * K;
+    for (int64_t c = 0; c < K; ++c) ioi[c] = 0.0;
+    int64_t Mi = job->E * epoch_len(job, i);
+    double Q = 0, t_prev = 0, u_prev = 0;
+    for (int64_t f = 0; f < Mi; ++f) {
+      double s = (double)sizes[R[row + f]];
+      double u = s / m->c;
+      /* the source: the PFS unless NoPFS names a valid tier */
+      double thr = pfs;
+      int64_t cls = 0;
+      if (policy == 3) {
+        int32_t code = src[row + f];
+        if (code >= 128 && code < 128 + J) {
+          int32_t j = code - 128;
+          thr = m->r[j] / m->p[j];
+          if (m->b_c < thr) thr = m->b_c;
+          cls = 1 + j;
+        } else if (code >= 256 && code < 256 + J) {
+          int32_t j = code - 256;
+          thr = m->r[j] / m->p[j];
+          cls = 1 + J + j;
+        }
+      }
+      double fetch = s / thr;
+      double wr = s / m->beta;
+      double wb = s / (m->w0 / m->p0);
+      if (wb > wr) wr = wb;
+      double rd = fetch + wr;
+      double tf;
+      if (policy == 0) {
+        tf = f == 0 ? 0.0 : t_prev + u_prev;
+      } else if (policy == 1) {
+        tf = f == 0 ? rd : (t_prev + u_prev) + rd;
+      } else {
+        /* the latest consumed read the buffer must wait for */
+        int64_t g = (int64_t)fill[row + f] - 1;
+        if (g > f - 1) g = f - 1;
+        double wait = g >= 0 ? m->p0 * ti[g] : 0.0;
+        if (wait > Q) Q = wait;
+        Q = Q + rd;
+        tf = Q / m->p0;
+        if (f > 0 && t_prev + u_prev > tf) tf = t_prev + u_prev;
+      }
+      if (policy != 0) ioi[cls] += fetch;
+      ti[f] = tf;
+      t_prev = tf;
+      u_prev = u;
+    }
+    for (int64_t f = Mi; f < M_max; ++f) ti[f] = -1.0;
+    finish[i - i0] = Mi > 0 ? t_prev + u_prev : 0.0;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Clairvoyant buffer (section 3). Held entries are keyed by the stream     */
 /* position of their next use, so at position f the sample read is held     */
 /* exactly when key f is. A binary max-heap of keys with lazy deletion (a   */

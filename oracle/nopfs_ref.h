@@ -119,6 +119,22 @@ int nopfs_ref_fetch_model_rows(const nopfs_ref_job* job, const int32_t* R,
                                const nopfs_ref_model* m, int64_t i0, int64_t i1,
                                int16_t* src, double* t);
 
+/* Policy simulation (section 6) for workers [i0, i1): policy 0 Perfect (no
+ * stalls), 1 Naive (one PFS read at a time after each compute), 2
+ * StagingBuffer (p0 threads stage reads in stream order from the PFS into a
+ * buffer whose schedule is fill, from nopfs_ref_staging_schedule), 3 NoPFS
+ * (the same, each read from the source in src, from
+ * nopfs_ref_fetch_model_rows; other codes read from the PFS). R, src, fill
+ * and t point at row i0 of their [N][M_max] tables (src only for policy 3,
+ * fill for 2 and 3). Outputs: t, when each read is consumed (-1 padding);
+ * finish[i1 - i0], when the last read's compute ends; io[i1 - i0][1 + 2J],
+ * fetch time summed by source class (0 the PFS, 1 + j another worker's tier
+ * j, 1 + J + j the own tier j). */
+int nopfs_ref_policy_sim_rows(const nopfs_ref_job* job, const int32_t* R, const int64_t* sizes,
+                              const int16_t* src, const int32_t* fill, const nopfs_ref_model* m,
+                              int32_t policy, int64_t i0, int64_t i1, double* t, double* finish,
+                              double* io);
+
 /* Clairvoyant buffer of d0 bytes (section 3: Belady's replacement, the
  * optimal-replacement and do-no-harm rules), per worker, from R, next and
  * the sizes. The buffer holds samples keyed by their next use; an access is

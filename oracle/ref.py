@@ -91,6 +91,9 @@ def lib():
         L.nopfs_ref_buffer_sim.argtypes = [jp, P, P, P, ctypes.c_int64, P, P]
         L.nopfs_ref_buffer_sim_rows.argtypes = [jp, P, ctypes.c_int64, ctypes.c_int64, P, P,
                                                 ctypes.c_int64, P, P]
+        L.nopfs_ref_policy_sim_rows.argtypes = [jp, P, P, P, P, ctypes.POINTER(RefModel),
+                                                ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
+                                                P, P, P]
         for name in ("nopfs_ref_stream_shape", "nopfs_ref_epoch_keys",
                      "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms",
                      "nopfs_ref_access_streams", "nopfs_ref_access_stats",
@@ -98,7 +101,8 @@ def lib():
                      "nopfs_ref_sample_columns", "nopfs_ref_access_stats_rows",
                      "nopfs_ref_reuse_next_rows", "nopfs_ref_prefetch_order",
                      "nopfs_ref_staging_schedule", "nopfs_ref_fetch_model_rows",
-                     "nopfs_ref_buffer_sim", "nopfs_ref_buffer_sim_rows"):
+                     "nopfs_ref_buffer_sim", "nopfs_ref_buffer_sim_rows",
+                     "nopfs_ref_policy_sim_rows"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -277,6 +281,36 @@ def buffer_sim(job: RefJob, R, nxt, sizes, d0, rows=None):
                                            _ptr(sizes), int(d0), _ptr(hit), _ptr(hits)),
            "buffer_sim")
     return hit, hits
+
+
+PERFECT, NAIVE, STAGING, NOPFS = 0, 1, 2, 3
+
+
+def policy_sim(job: RefJob, R, sizes, model: RefModel, policy, src=None, fill=None, rows=None):
+    """(t, finish, io) of a policy (PERFECT, NAIVE, STAGING, NOPFS) for the
+    given workers (default all): t float64 [rows][M_max] consumption times
+    (-1 padding), finish float64 [rows], io float64 [rows][1 + 2J] fetch time
+    per source class. R, src and fill hold those workers' rows."""
+    _, M, _ = stream_shape(job)
+    i0, i1 = (0, job.N) if rows is None else rows
+    R = np.ascontiguousarray(R, dtype=np.int32)
+    sizes = np.ascontiguousarray(sizes, dtype=np.int64)
+    if R.shape != (i1 - i0, M):
+        raise ValueError("R must hold the rows asked for")
+    if src is not None:
+        src = np.ascontiguousarray(src, dtype=np.int16)
+        assert src.shape == R.shape
+    if fill is not None:
+        fill = np.ascontiguousarray(fill, dtype=np.int32)
+        assert fill.shape == R.shape
+    t = np.empty((i1 - i0, M), np.float64)
+    finish = np.empty(i1 - i0, np.float64)
+    io = np.empty((i1 - i0, 1 + 2 * model.J), np.float64)
+    _check(lib().nopfs_ref_policy_sim_rows(
+        ctypes.byref(job), _ptr(R), _ptr(sizes), None if src is None else _ptr(src),
+        None if fill is None else _ptr(fill), ctypes.byref(model), int(policy), i0, i1, _ptr(t),
+        _ptr(finish), _ptr(io)), "policy_sim")
+    return t, finish, io
 
 
 def sample_columns(job: RefJob, samples):
