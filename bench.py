@@ -11,8 +11,9 @@ schedule of the planned job (the step's outputs as inputs, the workload's
 staging-buffer capacity as d0) are timed the same way and reported under
 "schedule", the performance model's fetch sources and consumption times
 (the simulated cluster's parameters) under "model", and the clairvoyant
-buffer replay (the staging capacity) under "buffer"; they are not part of
-the step.
+buffer replay (the staging capacity) under "buffer", and the simulator's
+four data-loading policies (Perfect, Naive, StagingBuffer, NoPFS) under
+"policies"; they are not part of the step.
 
 Prints ONE JSON line. Per-kernel durations come from HIP events recorded by
 the library around each of its launches, on the stream it launches on, over
@@ -123,11 +124,20 @@ def committed_traffic(workload, kernel):
     return None
 
 
+POLICY_NAMES = ("perfect", "naive", "staging", "nopfs")
+
+
 def _kernel_short_name(full):
-    """'ns::(anonymous namespace)::plan_hist<true>(args...)' -> 'plan_hist'."""
+    """'ns::(anonymous namespace)::plan_hist<true>(args...)' -> 'plan_hist';
+    the policy kernel keeps its policy: 'ps_sim<2>(...)' -> 'ps_sim_staging'."""
     import re
-    m = re.findall(r"(\w+)(?:<[^>()]*>)?\(", full)
-    return m[-1] if m else full
+    m = re.findall(r"(\w+)(?:<([^>()]*)>)?\(", full)
+    if not m:
+        return full
+    name, targ = m[-1]
+    if name == "ps_sim" and targ.strip().isdigit() and int(targ) < len(POLICY_NAMES):
+        return f"ps_sim_{POLICY_NAMES[int(targ)]}"
+    return name
 
 
 def rocprof_summary(d, workload):
@@ -220,6 +230,19 @@ def buffer_algorithmic_bytes(job, M, M_w):
     R and next once, each sample's size once, and a hit flag per position."""
     A = int(sum(M_w))
     return {"bs_sim": 8 * A + 8 * job.F + job.N * M + 16 * job.N}
+
+
+def policy_algorithmic_bytes(job, M, M_w, policy):
+    """Bytes a policy simulation must move given the dense layouts: R once,
+    each size once, the sources (NoPFS) and the staging windows (staging
+    policies), and every consumption time."""
+    A = int(sum(M_w))
+    b = 4 * A + 8 * job.F + 8 * job.N * M
+    if policy >= 2:
+        b += 4 * A
+    if policy == 3:
+        b += 2 * A
+    return {f"ps_sim_{POLICY_NAMES[policy]}": b}
 
 
 def roofline_of(workload, kernel, alg_bytes, avg_ms):
@@ -337,6 +360,40 @@ def time_buffer(nopfs, torch, w, job, M, M_w, R, nxt, sizes, steps, warmup, stre
     return out
 
 
+def time_policies(nopfs, torch, wl, w, job, M, M_w, R, tier, sizes, steps, warmup, stream):
+    """The four data-loading policies of the simulator on the planned job:
+    its streams and placement, the fetch model's sources (the simulated
+    cluster's parameters) and the staging schedule of the workload's
+    staging buffer. Each policy is one sequential replay per worker."""
+    dev = R.device
+    d0 = int(w.staging)
+    model = nopfs.make_model(**wl.LASSEN_MODEL)
+    fill = torch.empty((job.N, M), dtype=torch.int32, device=dev)
+    nopfs.staging_schedule(job, R, sizes, d0, fill, stream=stream)
+    src, _ = nopfs.fetch_model(job, R, tier, sizes, model, stream=stream)
+    t = torch.empty((job.N, M), dtype=torch.float64, device=dev)
+    fin = torch.empty(job.N, dtype=torch.float64, device=dev)
+    io = torch.empty((job.N, 1 + 2 * model.J), dtype=torch.float64, device=dev)
+    out = {"d0_bytes": d0}
+    for pol, name in enumerate(POLICY_NAMES):
+        calls = {name: lambda pol=pol: nopfs.policy_sim(job, R, sizes, model, pol, src=src,
+                                                        fill=fill, t=t, finish=fin, io=io,
+                                                        stream=stream)}
+        time_calls(nopfs, torch, w, calls,
+                   {name: policy_algorithmic_bytes(job, M, M_w, pol)},
+                   max(1, min(steps, 3)), min(warmup, 1), stream, out)
+        f = fin.cpu()
+        tot = io.sum(dim=0).cpu()
+        J = model.J
+        out[name]["slowest_worker_s"] = round(float(f.max()), 3)
+        out[name]["mean_worker_s"] = round(float(f.mean()), 3)
+        out[name]["fetch_s"] = {"pfs": round(float(tot[0]), 1),
+                                "remote": round(float(tot[1:1 + J].sum()), 1),
+                                "own": round(float(tot[1 + J:].sum()), 1)}
+    del fill, src, t
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -347,7 +404,7 @@ def main():
     ap.add_argument("--path", choices=["fused", "staged"], default="fused",
                     help="fused: one nopfs_plan_job call per step; staged: the four stage calls")
     ap.add_argument("--no-schedule", action="store_true",
-                    help="skip timing the prefetch queues, staging schedule, model and buffer")
+                    help="skip timing the schedule, model, buffer and policy calls")
     ap.add_argument("--calibrate-bytes", type=int, default=1 << 30,
                     help="size of the calibration copy run after the timed steps")
     ap.add_argument("--rocprof-summary", metavar="DIR",
@@ -435,7 +492,7 @@ def main():
             v["alg_GBps"] = round(alg[k] / (v["avg_ms"] * 1e-3) / 1e9, 1)
     print("[bench] kernels: " + json.dumps(per_kernel), file=sys.stderr, flush=True)
 
-    schedule = model = buffer = None
+    schedule = model = buffer = policies = None
     if not args.no_schedule:
         schedule = time_schedule(nopfs, torch, w, job, M, M_w, R, tier, sizes, caps, args.steps,
                                  args.warmup, stream)
@@ -443,6 +500,8 @@ def main():
                            args.warmup, stream)
         buffer = time_buffer(nopfs, torch, w, job, M, M_w, R, nxt, sizes, args.steps,
                              args.warmup, stream)
+        policies = time_policies(nopfs, torch, wl, w, job, M, M_w, R, tier, sizes, args.steps,
+                                 args.warmup, stream)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -470,6 +529,7 @@ def main():
         "schedule": schedule,
         "model": model,
         "buffer": buffer,
+        "policies": policies,
     }
     print(json.dumps(line), flush=True)
 

@@ -264,6 +264,56 @@ int nopfs_buffer_sim(const nopfs_job* job, const int32_t* R, const int32_t* next
                      const int64_t* sizes, int64_t d0, int8_t* hit, int64_t* hits,
                      void* hip_stream);
 
+/* Data-loading policies of section 6, simulated on the model of section 4
+ * (nopfs_policy_sim). */
+#define NOPFS_POLICY_PERFECT 0 /* no stalls: only compute (a lower bound)        */
+#define NOPFS_POLICY_NAIVE 1   /* one PFS read at a time, after each compute      */
+#define NOPFS_POLICY_STAGING 2 /* a staging buffer filled in stream order from    */
+                               /* the PFS, each sample dropped once consumed      */
+#define NOPFS_POLICY_NOPFS 3   /* the same buffer, each read from the fastest     */
+                               /* source of the placement (nopfs_fetch_model)     */
+
+/* Simulated training time of every worker under one of the policies of
+ * section 6, on the performance model of section 4. For read f of a worker,
+ * with s its size: u(f) = s / c (compute), read(f) = fetch(f) + write(f),
+ * write(f) = max(s / beta, s / (w0 / p0)), fetch(f) = s over its source's
+ * throughput (PFS t(gamma) / gamma; another worker's tier j
+ * min(b_c, r_j / p_j); own tier j r_j / p_j).
+ *   PERFECT: t(0) = 0, t(f) = t(f-1) + u(f-1).
+ *   NAIVE:   t(0) = read(0), t(f) = t(f-1) + u(f-1) + read(f), every read
+ *            from the PFS.
+ *   STAGING, NOPFS: p0 threads stage reads in stream order (from the PFS,
+ *            or from the source src names), and read f can start only once
+ *            the reads before fill(f) are consumed (fill: the schedule of
+ *            nopfs_staging_schedule for the buffer's d0). With Q(f) the
+ *            thread-time spent staging reads 0..f:
+ *              Q(f) = max(Q(f-1), p0 t(fill(f) - 1)) + read(f), t(-1) = 0,
+ *              t(0) = Q(0) / p0, t(f) = max(Q(f) / p0, t(f-1) + u(f-1)).
+ *            With fill all 0 (an unlimited buffer), NOPFS is
+ *            nopfs_fetch_model's t (avail = the summed read times / p0).
+ * The evaluation is sequential per worker, in this order, with IEEE double
+ * operations: results do not depend on the launch.
+ *   R:      int32 [N][M_max], nopfs_access_streams' output for this job.
+ *   sizes:  int64 [F] sample sizes in bytes.
+ *   src:    int16 [N][M_max], nopfs_fetch_model's sources (NOPFS only; may
+ *           be NULL otherwise). Codes other than 0, 128 + j, 256 + j with
+ *           j < J read from the PFS.
+ *   fill:   int32 [N][M_max], nopfs_staging_schedule's output (STAGING and
+ *           NOPFS; may be NULL otherwise).
+ *   t:      double [N][M_max], output: when each read is consumed, seconds;
+ *           -1 in padding.
+ *   finish: double [N], output: when the worker's last compute ends (0 for a
+ *           worker with no reads).
+ *   io:     double [N][1 + 2J], output: fetch time summed by source class,
+ *           0 the PFS, 1 + j another worker's tier j, 1 + J + j the own tier
+ *           j (all 0 for PERFECT).
+ * One wave per worker replays its stream. No scratch. Errors: EINVAL (also
+ * a policy outside 0..3, or a missing src or fill the policy needs), ERANGE
+ * (J > 32), EDEVICE. */
+int nopfs_policy_sim(const nopfs_job* job, const int32_t* R, const int64_t* sizes,
+                     const int16_t* src, const int32_t* fill, const nopfs_model* model,
+                     int32_t policy, double* t, double* finish, double* io, void* hip_stream);
+
 /* Static description of a status code. Never NULL. */
 const char* nopfs_strerror(int code);
 

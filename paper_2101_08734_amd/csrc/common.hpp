@@ -39,6 +39,9 @@ struct Shape {
 
 // Validates the job and fills the shape. Returns a NOPFS_* code.
 int make_shape(const nopfs_job* job, Shape* s);
+// Validates the performance model's parameters (J in 1..32, every rate and
+// thread count positive and finite).
+int model_check(const nopfs_model* m);
 
 // Per-epoch reads of worker i (same rule as the public header).
 __host__ __device__ inline int64_t epoch_len(int64_t F, int64_t N, int64_t B,

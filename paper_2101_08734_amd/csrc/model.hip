@@ -416,19 +416,6 @@ fm_final(SegParams p, const uint32_t* __restrict__ Pk, const uint64_t* __restric
   fm_chunk<true>(p, s, Pk, zP, rt, L, ins[s.i * nch + s.c], nullptr, src, t);
 }
 
-int model_check(const nopfs_model* m) {
-  if (!m) return fail(NOPFS_EINVAL, "model is NULL");
-  if (m->J < 1) return fail(NOPFS_EINVAL, "model J must be >= 1");
-  if (m->J > kMaxClasses) return fail(NOPFS_ERANGE, "model J must be <= 32");
-  const double v[7] = {m->c, m->beta, m->b_c, m->pfs_t, m->pfs_gamma, m->w0, m->p0};
-  for (double x : v)
-    if (!(x > 0) || !isfinite(x)) return fail(NOPFS_EINVAL, "model rates and counts must be positive and finite");
-  for (int32_t j = 0; j < m->J; ++j)
-    if (!(m->r[j] > 0) || !(m->p[j] > 0) || !isfinite(m->r[j]) || !isfinite(m->p[j]))
-      return fail(NOPFS_EINVAL, "model rates and counts must be positive and finite");
-  return NOPFS_OK;
-}
-
 Rates make_rates(const nopfs_model* m) {
   Rates r{};
   r.J = m->J;
@@ -509,6 +496,20 @@ int model_impl(const nopfs_job* job, const int32_t* R, const int8_t* tier, const
 }
 
 }  // namespace
+
+int model_check(const nopfs_model* m) {
+  if (!m) return fail(NOPFS_EINVAL, "model is NULL");
+  if (m->J < 1) return fail(NOPFS_EINVAL, "model J must be >= 1");
+  if (m->J > kMaxClasses) return fail(NOPFS_ERANGE, "model J must be <= 32");
+  const double v[7] = {m->c, m->beta, m->b_c, m->pfs_t, m->pfs_gamma, m->w0, m->p0};
+  for (double x : v)
+    if (!(x > 0) || !isfinite(x)) return fail(NOPFS_EINVAL, "model rates and counts must be positive and finite");
+  for (int32_t j = 0; j < m->J; ++j)
+    if (!(m->r[j] > 0) || !(m->p[j] > 0) || !isfinite(m->r[j]) || !isfinite(m->p[j]))
+      return fail(NOPFS_EINVAL, "model rates and counts must be positive and finite");
+  return NOPFS_OK;
+}
+
 }  // namespace nopfs
 
 extern "C" int nopfs_fetch_model(const nopfs_job* job, const int32_t* R, const int8_t* tier,

@@ -92,6 +92,7 @@ def lib() -> ctypes.CDLL:
             "nopfs_staging_schedule": [jp, P, P, I64, P, P],
             "nopfs_fetch_model": [jp, P, P, P, ctypes.POINTER(Model), P, P, P],
             "nopfs_buffer_sim": [jp, P, P, P, I64, P, P, P],
+            "nopfs_policy_sim": [jp, P, P, P, P, ctypes.POINTER(Model), ctypes.c_int32, P, P, P, P],
             "nopfs_profile_enable": [ctypes.c_int],
             "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
                                     ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)],
@@ -112,7 +113,7 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_stats",
             "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_prefetch_order",
-            "nopfs_staging_schedule", "nopfs_fetch_model", "nopfs_buffer_sim",
+            "nopfs_staging_schedule", "nopfs_fetch_model", "nopfs_buffer_sim", "nopfs_policy_sim",
             "nopfs_strerror",
             "nopfs_last_error", "nopfs_profile_enable", "nopfs_profile_query",
             "nopfs_calibration_copy", "nopfs_debug_set")
@@ -316,6 +317,40 @@ def buffer_sim(job: Job, R, next, sizes, d0, hit=None, hits=None, stream=None):
     _check(lib().nopfs_buffer_sim(ctypes.byref(j), _ptr(R), _ptr(next), _ptr(sizes), int(d0),
                                   _ptr(hit), _ptr(hits), _stream(stream)), "nopfs_buffer_sim")
     return hit, hits
+
+
+POLICY_PERFECT, POLICY_NAIVE, POLICY_STAGING, POLICY_NOPFS = 0, 1, 2, 3
+
+
+def policy_sim(job: Job, R, sizes, model, policy, src=None, fill=None, t=None, finish=None,
+               io=None, stream=None):
+    """Simulated training time under a data-loading policy (nopfs_policy_sim):
+    t [N][M_max] float64 consumption times (-1 padding), finish [N], io
+    [N][1 + 2J] fetch time by source class."""
+    _, M, _ = stream_shape(job)
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    _device_tensor(sizes, torch.int64, (job.F,), "sizes")
+    if src is not None:
+        _device_tensor(src, torch.int16, (job.N, M), "src")
+    if fill is not None:
+        _device_tensor(fill, torch.int32, (job.N, M), "fill")
+    K = 1 + 2 * model.J
+    if t is None:
+        t = torch.empty((job.N, M), dtype=torch.float64, device="cuda")
+    if finish is None:
+        finish = torch.empty(job.N, dtype=torch.float64, device="cuda")
+    if io is None:
+        io = torch.empty((job.N, K), dtype=torch.float64, device="cuda")
+    _device_tensor(t, torch.float64, (job.N, M), "t")
+    _device_tensor(finish, torch.float64, (job.N,), "finish")
+    _device_tensor(io, torch.float64, (job.N, K), "io")
+    j = job.c()
+    _check(lib().nopfs_policy_sim(ctypes.byref(j), _ptr(R), _ptr(sizes),
+                                  None if src is None else _ptr(src),
+                                  None if fill is None else _ptr(fill), ctypes.byref(model),
+                                  int(policy), _ptr(t), _ptr(finish), _ptr(io), _stream(stream)),
+           "nopfs_policy_sim")
+    return t, finish, io
 
 
 def plan(job: Job, sizes, caps, stream=None):

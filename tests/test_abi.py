@@ -187,6 +187,34 @@ def test_buffer_argument_checks(L):
     assert L.nopfs_debug_set(3, 0) == 0
 
 
+def test_policy_argument_checks(L):
+    j = _job()
+    m = _model()
+    ps = L.nopfs_policy_sim
+    E = nopfs.NOPFS_EINVAL
+    mp = ctypes.byref(m)
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, FAKE, mp, 4, FAKE, FAKE, FAKE, None) == E
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, FAKE, mp, -1, FAKE, FAKE, FAKE, None) == E
+    assert ps(None, FAKE, FAKE, FAKE, FAKE, mp, 0, FAKE, FAKE, FAKE, None) == E
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, FAKE, None, 0, FAKE, FAKE, FAKE, None) == E
+    assert ps(ctypes.byref(j), None, FAKE, FAKE, FAKE, mp, 0, FAKE, FAKE, FAKE, None) == E
+    assert ps(ctypes.byref(j), FAKE, None, FAKE, FAKE, mp, 0, FAKE, FAKE, FAKE, None) == E
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, FAKE, mp, 0, None, FAKE, FAKE, None) == E
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, FAKE, mp, 0, FAKE, None, FAKE, None) == E
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, FAKE, mp, 0, FAKE, FAKE, None, None) == E
+    # the staging policies need the schedule, NoPFS the sources
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, None, mp, 2, FAKE, FAKE, FAKE, None) == E
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, None, mp, 3, FAKE, FAKE, FAKE, None) == E
+    assert ps(ctypes.byref(j), FAKE, FAKE, None, FAKE, mp, 3, FAKE, FAKE, FAKE, None) == E
+    bad = _model(p0=0.0)
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, FAKE, ctypes.byref(bad), 0, FAKE, FAKE, FAKE,
+              None) == E
+    big = _model(r=[1e9] * 33, p=[1] * 33)
+    big.J = 33
+    assert ps(ctypes.byref(j), FAKE, FAKE, FAKE, FAKE, ctypes.byref(big), 0, FAKE, FAKE, FAKE,
+              None) == nopfs.NOPFS_ERANGE
+
+
 def test_scratch_failure_is_enomem(L):
     """The test hook fails the next internal allocation; the call reports
     NOPFS_ENOMEM before launching anything."""
