@@ -22,7 +22,9 @@
 // The recurrence is sequential within a worker (a read may wait for the
 // consumption of any earlier read), so each worker is one wave, and the
 // arithmetic is the same IEEE operations in the same order as the
-// definition: results are bit-identical to a read-by-read evaluation.
+// definition: results are bit-identical to a read-by-read evaluation. (The
+// maxima are taken with fmax: every operand is finite and non-negative and
+// never -0, where fmax and "the larger of the two" agree bit for bit.)
 //
 //   ps_sim -- one wave per worker, 64 reads per batch, one per lane. The
 //             per-read terms (u, fetch, read) and the wait p0 t(g) of every
@@ -104,21 +106,26 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
   for (int c = lane; c < kPsClasses; c += 64) thr[c] = rt.thr[c];
   __syncthreads();
 
-  // per-lane inputs of a batch: id, class, lookback position g
-  auto load_ids = [&](int64_t f0, int32_t& k, int32_t& cls, int64_t& g) {
+  // per-lane raw inputs of a batch: id, source code, window start (only
+  // loads here, so nothing waits for them until they are used)
+  auto load_ids = [&](int64_t f0, int32_t& k, int32_t& code, int32_t& fl) {
     const int64_t f = f0 + lane;
     k = -1;
-    cls = 0;
-    g = -1;
+    code = 0;
+    fl = 0;
     if (f < Mi) {
       k = Rr[f];
-      if (kPolicy == kNoPFS) cls = ps_class(kPolicy, Sr[f], rt.J);
-      if (kStaged) {
-        g = int64_t(Fr[f]) - 1;
-        if (g > f - 1) g = f - 1;
-        if (g < -1) g = -1;
-      }
+      if (kPolicy == kNoPFS) code = Sr[f];
+      if (kStaged) fl = Fr[f];
     }
+  };
+  // the lookback position g = fill - 1 of read f, clamped to [-1, f - 1]
+  auto look = [&](int64_t f0, int32_t fl) -> int64_t {
+    const int64_t f = f0 + lane;
+    int64_t g = int64_t(fl) - 1;
+    if (g > f - 1) g = f - 1;
+    if (g < -1 || f >= Mi) g = -1;
+    return g;
   };
   auto size_of = [&](int32_t k) -> int64_t {
     return (k >= 0 && k < r.F) ? sizes[k] : int64_t(0);
@@ -128,21 +135,21 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
     return (g >= 0 && g < f0 - kPsRing) ? tr[g] : 0.0;
   };
 
-  double acc0 = 0.0, acc1 = 0.0;  // fetch time of class lane, and of class 64 + lane
+  double acc0 = 0.0, acc1 = 0.0;  // NoPFS: fetch time of class lane, and of class 64 + lane
+  double pfs_acc = 0.0;           // Naive and StagingBuffer: fetch time from the PFS
   double Q = 0.0, tprev = 0.0, uprev = 0.0;
 
   // pipeline: ids two batches ahead, sizes and far lookbacks one
-  int32_t kA, cA, kB, cB;
-  int64_t gA, gB;
-  load_ids(0, kB, cB, gB);
+  int32_t kA, cA, fA, kB, cB, fB;
+  load_ids(0, kB, cB, fB);
   int64_t sB = size_of(kB);
   double farB = 0.0;  // nothing is older than the ring in the first batch
-  load_ids(64, kA, cA, gA);
+  load_ids(64, kA, cA, fA);
   for (int64_t f0 = 0; f0 < Mi; f0 += 64) {
     // this batch's inputs
     const double s = double(sB);
-    const int cls = cB;
-    const int64_t g = gB;
+    const int cls = ps_class(kPolicy, cB, rt.J);
+    const int64_t g = kStaged ? look(f0, fB) : -1;
     const double far = farB;
     // per-read terms, lane-parallel, in the definition's expressions
     const double u = s / rt.c;
@@ -162,9 +169,9 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
     // the next batch's sizes and far lookbacks, the one after's ids
     sB = size_of(kA);
     cB = cA;
-    gB = gA;
-    farB = far_wait(f0 + 64, gA);
-    load_ids(f0 + 128, kA, cA, gA);
+    fB = fA;
+    farB = kStaged ? far_wait(f0 + 64, look(f0 + 64, fA)) : 0.0;
+    load_ids(f0 + 128, kA, cA, fA);
 
     const int nb = Mi - f0 < 64 ? int(Mi - f0) : 64;
     double tb = -1.0;  // lane q: t of read f0 + q
@@ -180,17 +187,18 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
       } else if (kPolicy == kNaive) {
         tf = f == 0 ? rq : (tprev + uprev) + rq;
       } else {
-        if (Wq > Q) Q = Wq;
+        Q = __builtin_fmax(Q, Wq);
         Q = Q + rq;
         tf = Q / rt.p0;
         if (f > 0) {
           const double a = tprev + uprev;
-          if (a > tf) tf = a;
+          tf = __builtin_fmax(tf, a);
         }
       }
       tb = lane == q ? tf : tb;
       tprev = tf;
       uprev = uq;
+      if (kPolicy == kNaive || kPolicy == kStaging) pfs_acc = pfs_acc + rl_d(fetch, q);
     };
     if (kStaged && inb_mask == 0) {
       // every wait is known: Q does not depend on this batch's t, so its
@@ -201,14 +209,14 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
 #pragma unroll
         for (int q = 0; q < 64; ++q) {
           const double Wq = rl_d(W, q);
-          if (Wq > Q) Q = Wq;
+          Q = __builtin_fmax(Q, Wq);
           Q = Q + rl_d(rd, q);
           Qb = lane == q ? Q : Qb;
         }
       } else {
         for (int q = 0; q < nb; ++q) {
           const double Wq = rl_d(W, q);
-          if (Wq > Q) Q = Wq;
+          Q = __builtin_fmax(Q, Wq);
           Q = Q + rl_d(rd, q);
           Qb = lane == q ? Q : Qb;
         }
@@ -218,11 +226,12 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
         double tf = rl_d(av, q);
         if (f0 + q > 0) {
           const double a = tprev + uprev;
-          if (a > tf) tf = a;
+          tf = __builtin_fmax(tf, a);
         }
         tb = lane == q ? tf : tb;
         tprev = tf;
         uprev = rl_d(u, q);
+        if (kPolicy == kStaging) pfs_acc = pfs_acc + rl_d(fetch, q);
       };
       if (nb == 64) {
 #pragma unroll
@@ -254,16 +263,19 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
       tr[f] = tb;
       if (kStaged) ring[f & (kPsRing - 1)] = tb;
     }
-    // fetch time by class, in stream order
-    if (kPolicy != kPerfect) {
-#pragma unroll 8
-      for (int q = 0; q < nb; ++q) {
-        const int cq = __builtin_amdgcn_readlane(cls, q);
-        const double fq = rl_d(fetch, q);
-        if (cq < 64) {
-          acc0 = acc0 + (lane == cq ? fq : 0.0);
+    if (kPolicy == kNoPFS) {
+      // fetch time by class: each class's reads of the batch in stream order
+      uint64_t rem = nb == 64 ? ~uint64_t(0) : (uint64_t(1) << nb) - 1;
+      while (rem) {
+        const int c = __builtin_amdgcn_readlane(cls, __builtin_ctzll(rem));
+        const uint64_t m = __ballot(cls == c) & rem;
+        rem &= ~m;
+        double a = c < 64 ? rl_d(acc0, c) : rl_d(acc1, c - 64);
+        for (uint64_t mm = m; mm; mm &= mm - 1) a = a + rl_d(fetch, __builtin_ctzll(mm));
+        if (c < 64) {
+          acc0 = lane == c ? a : acc0;
         } else {
-          acc1 = acc1 + (lane == cq - 64 ? fq : 0.0);
+          acc1 = lane == c - 64 ? a : acc1;
         }
       }
     }
@@ -271,6 +283,7 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
   for (int64_t f = Mi + lane; f < M; f += 64) tr[f] = -1.0;
   const int K = 1 + 2 * rt.J;
   double* ior = io + i * K;
+  if (kPolicy == kNaive || kPolicy == kStaging) acc0 = lane == 0 ? pfs_acc : 0.0;
   if (lane < K) ior[lane] = acc0;
   if (64 + lane < K) ior[64 + lane] = acc1;
   if (lane == 0) finish[i] = Mi > 0 ? tprev + uprev : 0.0;
