@@ -14,21 +14,25 @@
 //               the replay reads sizes with plain coalesced loads.
 //   bs_sim   -- one wave per worker. Held keys in a three-level bitmap: a
 //               bit per position in 64-bit words in global memory, one word
-//               per batch of 64 reads, changed and read only by lane 0's
-//               atomics so it is always current; a bit per nonzero word, and
-//               a bit per nonzero word of that, in LDS. A batch of 64 reads
+//               per batch of 64 reads, changed and read only by atomics so it
+//               is always current; a bit per word that may hold keys, and a
+//               bit per such level-1 word, in LDS. A batch of 64 reads
 //               arrives one per lane (sizes, next uses and the batch's word
 //               loaded a batch ahead, with changes to that word made meanwhile
 //               kept as set and clear masks); only the reads that can change
 //               anything are visited, in order: those whose key is held (a
-//               hit) and those with a next use that fits (an admission).
-//               The top word, the highest word holding a key, lives in
-//               registers with the size of each of its keys in the lane of
-//               its bit: the furthest key is discarded from there, and only
-//               when that word empties is the next one found through the LDS
-//               levels and loaded. An admission above the top key that does
-//               not fit is a bypass and touches nothing.
+//               hit) and those with a next use that fits (an admission). The
+//               highest held keys (up to 64) live in registers, ascending
+//               across the lanes with their sizes: the furthest key is
+//               discarded from there, an admitted key above the lowest cached
+//               one joins in order, and an admission above the highest that
+//               does not fit is a bypass that touches nothing. Only when the
+//               cache empties are the highest keys gathered again from the two
+//               highest level-1 words, one word per lane (discards do not
+//               clear level bits; words found empty clear theirs then).
+
 #include <algorithm>
+#include <climits>
 #include <new>
 
 #include "common.hpp"
@@ -62,6 +66,25 @@ __device__ __forceinline__ uint64_t rfl64(uint64_t v) {
 }
 
 __device__ __forceinline__ int hi_bit(uint32_t v) { return 31 - __builtin_clz(v); }
+
+// whole-wave lane shifts: lane i takes lane i + 1 (shl1) or lane i - 1
+// (shr1); the lane with no source keeps `edge`
+__device__ __forceinline__ int32_t shl1(int32_t v, int32_t edge) {
+  return __builtin_amdgcn_update_dpp(edge, v, 0x130, 0xf, 0xf, false);
+}
+__device__ __forceinline__ int32_t shr1(int32_t v, int32_t edge) {
+  return __builtin_amdgcn_update_dpp(edge, v, 0x138, 0xf, 0xf, false);
+}
+__device__ __forceinline__ int64_t shl1_64(int64_t v) {
+  const uint32_t lo = uint32_t(shl1(int32_t(uint32_t(uint64_t(v))), 0));
+  const uint32_t hi = uint32_t(shl1(int32_t(uint32_t(uint64_t(v) >> 32)), 0));
+  return int64_t((uint64_t(hi) << 32) | lo);
+}
+__device__ __forceinline__ int64_t shr1_64(int64_t v) {
+  const uint32_t lo = uint32_t(shr1(int32_t(uint32_t(uint64_t(v))), 0));
+  const uint32_t hi = uint32_t(shr1(int32_t(uint32_t(uint64_t(v) >> 32)), 0));
+  return int64_t((uint64_t(hi) << 32) | lo);
+}
 __device__ __forceinline__ int hi_bit64(uint64_t v) { return 63 - __builtin_clzll(v); }
 
 __device__ __forceinline__ uint64_t l0_load(const uint64_t* p) {
@@ -113,11 +136,14 @@ bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ 
   __threadfence();  // the cleared words reach L2 before the atomics below
   __syncthreads();
 
+  __shared__ int32_t kslot[64];
   int64_t used = 0, hc = 0, hb = 0;
-  // top word (-1: nothing held), its bits, lane b: size of key 64 tw + b
-  int64_t tw = -1;
-  uint64_t tv = 0;
-  int64_t zs = 0;
+  // the highest held keys, ascending in lanes 0..n-1, with their sizes;
+  // every held key >= ck[0] is cached, and n == 0 only when nothing is held
+  int32_t ck = INT32_MAX;
+  int64_t cz = 0;
+  int n = 0;
+  int64_t nheld = 0;
 
   // clears the level bits above a level-0 word that has become zero
   auto word_emptied = [&](int64_t w) {
@@ -127,48 +153,148 @@ bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ 
       if (v1 == 0u) atomicAnd(&l2[a >> 5], ~(1u << (a & 31)));
     }
   };
-  // finds the highest word holding a key and loads it with its sizes
-  auto descend = [&]() {
-    int64_t w2 = -1;
-    for (int64_t base = ((W2 - 1) >> 6) << 6; base >= 0; base -= 64) {
-      const int64_t idx = base + lane;
-      const uint32_t v = idx < W2 ? l2[idx] : 0u;
-      const uint64_t b = __ballot(v != 0u);
-      if (b) {
-        w2 = base + (63 - __builtin_clzll(b));
-        break;
-      }
+  // the cache's lowest key leaves (it stays held in the bitmap)
+  auto drop_min = [&]() {
+    ck = shl1(ck, INT32_MAX);
+    cz = shl1_64(cz);
+    --n;
+  };
+  // a key above ck[0] (or into an empty cache) joins in order; a full cache
+  // first lets its lowest key go
+  auto cache_insert = [&](int32_t key, int64_t sz) {
+    if (n == 64) drop_min();
+    const int p = __builtin_popcountll(__ballot(lane < n && ck < key));
+    const int32_t uk = shr1(ck, INT32_MAX);
+    const int64_t uz = shr1_64(cz);
+    if (lane > p && lane <= n) {
+      ck = uk;
+      cz = uz;
     }
-    tw = -1;
-    tv = 0;
-    if (w2 < 0) return;
-    const int64_t w1 = (w2 << 5) + hi_bit(l2[w2]);
-    const uint32_t v1 = l1[w1];
-    if (v1 == 0u) return;  // cannot happen: the level bits mirror level 0
-    const int64_t w0 = (w1 << 5) + hi_bit(v1);
-    uint64_t v0 = 0;
-    if (lane == 0) v0 = l0_load(&l0[w0]);
-    const int64_t x = (w0 << 6) + lane;
-    zs = x < Mi ? zr[x] : 0;
-    v0 = rfl64(v0);
-    // the sizes are complete here, so later reads of zs wait for nothing
-    __builtin_amdgcn_s_waitcnt(0);
-    if (v0 == 0u) return;  // cannot happen either
-    tw = w0;
-    tv = v0;
+    if (lane == p) {
+      ck = key;
+      cz = sz;
+    }
+    ++n;
+  };
+  // fills the empty cache with the highest held keys: the words of the two
+  // highest level-1 words that have set bits, one word per lane, highest
+  // first; level bits of words found empty (keys discarded from the cache
+  // leave them set) are cleared on the way
+  auto refill = [&]() {
+    __builtin_amdgcn_s_waitcnt(0);  // lane 0's atomics are in L2 before other lanes load
+    n = 0;
+    while (n == 0 && nheld > 0) {
+      int64_t w2 = -1;
+      for (int64_t base = ((W2 - 1) >> 6) << 6; base >= 0; base -= 64) {
+        const int64_t idx = base + lane;
+        const uint32_t v = idx < W2 ? l2[idx] : 0u;
+        const uint64_t bl = __ballot(v != 0u);
+        if (bl) {
+          w2 = base + (63 - __builtin_clzll(bl));
+          break;
+        }
+      }
+      if (w2 < 0) break;  // nothing marked (only if sizes or next uses break the precondition)
+      const uint32_t v2 = l2[w2];
+      const int64_t a1 = (w2 << 5) + hi_bit(v2);
+      const uint32_t v1a = l1[a1];
+      if (v1a == 0u) {  // a level-2 bit over an empty level-1 word
+        if (lane == 0) atomicAnd(&l2[w2], ~(1u << (a1 & 31)));
+        __builtin_amdgcn_s_waitcnt(0);
+        continue;
+      }
+      // the next level-1 word with a level-2 bit, below a1
+      int64_t a2 = -1;
+      const uint32_t below = v2 & ((1u << (a1 & 31)) - 1u);
+      if (below) {
+        a2 = (w2 << 5) + hi_bit(below);
+      } else {
+        for (int64_t base = ((w2 - 1) >> 6) << 6; w2 > 0 && base >= 0; base -= 64) {
+          const int64_t idx = base + lane;
+          const uint32_t v = idx < w2 ? l2[idx] : 0u;
+          const uint64_t bl = __ballot(v != 0u);
+          if (bl) {
+            const int64_t w2b = base + (63 - __builtin_clzll(bl));
+            a2 = (w2b << 5) + hi_bit(l2[w2b]);
+            break;
+          }
+        }
+      }
+      const uint32_t v1b = a2 >= 0 ? l1[a2] : 0u;
+      const int jj = lane & 31;
+      const uint32_t v1 = lane < 32 ? v1a : v1b;
+      const int64_t a = lane < 32 ? a1 : a2;
+      const bool has = a >= 0 && ((v1 >> (31 - jj)) & 1u);
+      const int64_t w = a * 32 + (31 - jj);
+      uint64_t v = has ? l0_load(&l0[w]) : uint64_t(0);
+      if (has && v == 0u) {  // marked but empty: clear the marks
+        const uint32_t m1 = 1u << (w & 31);
+        const uint32_t left = atomicAnd(&l1[w >> 5], ~m1) & ~m1;
+        if (left == 0u) atomicAnd(&l2[w >> 10], ~(1u << ((w >> 5) & 31)));
+      }
+      const uint32_t pop = uint32_t(__builtin_popcountll(v));
+      const uint32_t incl = wave_inclusive_scan(pop);
+      const uint32_t ex = incl - pop;
+      const uint32_t sum = __builtin_amdgcn_readlane(incl, 63);
+      const int total = sum < 64u ? int(sum) : 64;
+      __builtin_amdgcn_s_waitcnt(0);
+      if (total == 0) continue;  // only empty words: their marks are gone now
+      const int k = ex >= 64u ? 0 : (int(pop) < 64 - int(ex) ? int(pop) : 64 - int(ex));
+      for (int it = 0; it < 64; ++it) {
+        if (!__ballot(it < k)) break;
+        if (it < k) {
+          const int bp = hi_bit64(v);
+          v &= ~(uint64_t(1) << bp);
+          kslot[total - 1 - (int(ex) + it)] = int32_t((w << 6) + bp);
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      const int32_t key = lane < total ? kslot[lane] : INT32_MAX;
+      ck = key;
+      cz = (lane < total && key >= 0 && key < Mi) ? zr[key] : 0;
+      n = total;
+      // wait for the sizes here, once: an empty asm that takes and redefines
+      // them, so no later use of the cache waits on memory (such a wait would
+      // also wait for lane 0's latest atomics)
+      asm volatile("" : "+v"(cz), "+v"(ck));
+    }
+  };
+  // the batch: its index, held keys among its positions, and the changes
+  // made to the next batch's word since lane 0 loaded it
+  int64_t b = 0;
+  uint64_t hw = 0, nset = 0, nclr = 0;
+  // discards the highest key
+  auto evict = [&]() -> bool {
+    const int32_t x = __builtin_amdgcn_readlane(ck, n - 1);
+    const int64_t sx = rl64(cz, n - 1);
+    --n;
+    if (x < 0 || x >= Mi) return false;  // cannot happen: cached keys are held positions
+    const int64_t w = x >> 6;
+    const uint64_t bx = uint64_t(1) << (x & 63);
+    if (lane == 0) atomicAnd(reinterpret_cast<unsigned long long*>(&l0[w]), ~bx);
+    // this batch's word or the next one's (branch-free: keeps them in registers)
+    const uint64_t mb = w == b ? bx : uint64_t(0);
+    const uint64_t mn = w == b + 1 ? bx : uint64_t(0);
+    hw &= ~mb;
+    nclr |= mn;
+    nset &= ~mn;
+    used -= sx;
+    --nheld;
+    if (n == 0 && nheld > 0) refill();
+    return true;
   };
 
   // the next batch: sizes, next uses, lane 0's copy of its word, and the
   // changes made to that word since it was loaded
   int64_t sN = lane < Mi ? zr[lane] : 0;
   int32_t nN = lane < Mi ? Xr[lane] : -1;
-  uint64_t hN = 0, nset = 0, nclr = 0;  // every word starts empty
-  for (int64_t f0 = 0, b = 0; f0 < Mi; f0 += 64, ++b) {
+  uint64_t hN = 0;  // every word starts empty
+  for (int64_t f0 = 0; f0 < Mi; f0 += 64, ++b) {
     const int64_t f = f0 + lane;
     const int64_t s = sN;
     int32_t nx = nN;
     if (nx <= f || nx >= Mi) nx = -1;
-    uint64_t hw = (rfl64(hN) & ~nclr) | nset;  // held keys among this batch's positions
+    hw = (rfl64(hN) & ~nclr) | nset;
     const uint64_t cand = __ballot(nx >= 0 && s <= d0);
     nset = nclr = 0;
     hN = 0;
@@ -190,17 +316,18 @@ bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ 
         hb += sq;
         hm |= bit;
         used -= sq;
+        --nheld;
         hw &= ~bit;
         if (lane == 0) atomicAnd(reinterpret_cast<unsigned long long*>(&l0[b]), ~bit);
-        if (b == tw) tv = hw;
-        if (hw == 0u) {
-          word_emptied(b);
-          if (b == tw) descend();
+        if (hw == 0u) word_emptied(b);
+        if (n > 0 && __builtin_amdgcn_readlane(ck, 0) == int32_t(f0 + q)) {
+          drop_min();
+          if (n == 0 && nheld > 0) refill();
         }
       }
       if (!(cand & bit)) continue;
       const int32_t nq = __builtin_amdgcn_readlane(nx, q);
-      const int64_t top = tw >= 0 ? (tw << 6) + hi_bit64(tv) : -1;
+      const int64_t top = n > 0 ? int64_t(__builtin_amdgcn_readlane(ck, n - 1)) : -1;
       if (nq > top && sq > d0 - used) continue;  // the furthest and it does not fit: bypass
       {  // admit under the next use
         const int64_t w = nq >> 6;
@@ -210,43 +337,22 @@ bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ 
           atomicOr(&l1[w >> 5], 1u << (w & 31));
           atomicOr(&l2[w >> 10], 1u << ((w >> 5) & 31));
         }
-        if (w == b) {  // a later read of this batch
-          hw |= bn;
-          mask |= bn;
-        } else if (w == b + 1) {
-          nset |= bn;
-          nclr &= ~bn;
-        }
-        if (w > tw) {  // every word above the top is empty
-          tw = w;
-          tv = 0;
-        }
-        if (w == tw) {
-          tv |= bn;
-          if (lane == (nq & 63)) zs = sq;
-        }
+        // a later read of this batch, or of the next one
+        const uint64_t mb = w == b ? bn : uint64_t(0);
+        const uint64_t mn = w == b + 1 ? bn : uint64_t(0);
+        hw |= mb;
+        mask |= mb;
+        nset |= mn;
+        nclr &= ~mn;
+        if (n == 0 || nq > __builtin_amdgcn_readlane(ck, 0)) cache_insert(nq, sq);
+        ++nheld;
         used += sq;
       }
       // discard the furthest while over capacity
       while (used > d0) {
-        if (tw < 0) {  // nothing held (only if sizes break the precondition)
+        if (n == 0 || !evict()) {  // nothing held (broken precondition)
           used = 0;
           break;
-        }
-        const int xb = hi_bit64(tv);
-        const uint64_t bx = uint64_t(1) << xb;
-        used -= rl64(zs, xb);
-        tv &= ~bx;
-        if (lane == 0) atomicAnd(reinterpret_cast<unsigned long long*>(&l0[tw]), ~bx);
-        if (tw == b) {
-          hw &= ~bx;
-        } else if (tw == b + 1) {
-          nclr |= bx;
-          nset &= ~bx;
-        }
-        if (tv == 0u) {
-          word_emptied(tw);
-          descend();
         }
       }
     }
