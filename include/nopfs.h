@@ -258,7 +258,7 @@ int nopfs_fetch_model(const nopfs_job* job, const int32_t* R, const int8_t* tier
  *   hit:     int8 [N][M_max], output: 1 hit, 0 miss, -1 padding.
  *   hits:    int64 [N][2], output: hits and hit bytes per worker.
  * The replay is sequential per worker (one wave each). M_max < 2^24.
- * Scratch: about 8 bytes per stream position. Errors: EINVAL (also d0 < 0),
+ * Scratch: one bit per stream position. Errors: EINVAL (also d0 < 0),
  * ERANGE (M_max >= 2^24), ENOMEM, EDEVICE. */
 int nopfs_buffer_sim(const nopfs_job* job, const int32_t* R, const int32_t* next,
                      const int64_t* sizes, int64_t d0, int8_t* hit, int64_t* hits,

@@ -7,19 +7,19 @@
 // so the read at position f hits exactly when key f is held. After a read
 // with a next use n the sample is (re)admitted under key n, then, while the
 // held bytes exceed d0, the furthest key is discarded (possibly n itself).
-// The size of the sample held under key x is that of the sample read at x.
+// The size of the sample held under key x is that of the sample read at x,
+// sizes[R[x]].
 // The replay is sequential per worker and the workers are independent.
 //
-//   bs_sizes -- every position's sample size, sizes[R[f]], in parallel, so
-//               the replay reads sizes with plain coalesced loads.
 //   bs_sim   -- one wave per worker. Held keys in a three-level bitmap: a
 //               bit per position in 64-bit words in global memory, one word
 //               per batch of 64 reads, changed and read only by atomics so it
 //               is always current; a bit per word that may hold keys, and a
 //               bit per such level-1 word, in LDS. A batch of 64 reads
-//               arrives one per lane (sizes, next uses and the batch's word
-//               loaded a batch ahead, with changes to that word made meanwhile
-//               kept as set and clear masks); only the reads that can change
+//               arrives one per lane (ids and next uses loaded two batches
+//               ahead, sizes gathered and the batch's word loaded one ahead,
+//               with changes to that word made meanwhile kept as set and
+//               clear masks); only the reads that can change
 //               anything are visited, in order: those whose key is held (a
 //               hit) and those with a next use that fits (an admission). The
 //               highest held keys (up to 64) live in registers, ascending
@@ -91,32 +91,9 @@ __device__ __forceinline__ uint64_t l0_load(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// z[i][f] = sizes[R[i][f]] for f < M_i (0 for an id outside [0, F))
-__global__ void __launch_bounds__(256)
-bs_sizes(BsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ sizes,
-         int64_t* __restrict__ z) {
-  for (int64_t i = blockIdx.y; i < r.N; i += gridDim.y) {
-    const int64_t Mi = bs_row_len(r, i);
-    const int32_t* Rr = R + i * r.M_max;
-    int64_t* zr = z + i * r.M_max;
-    // four independent reads in flight per thread
-    const int64_t S = int64_t(gridDim.x) * blockDim.x;
-    for (int64_t f = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; f < Mi; f += 4 * S) {
-      int32_t k[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) k[u] = f + u * S < Mi ? Rr[f + u * S] : -1;
-      int64_t v[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = (k[u] >= 0 && k[u] < r.F) ? sizes[k[u]] : 0;
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (f + u * S < Mi) zr[f + u * S] = v[u];
-    }
-  }
-}
-
 __global__ void __launch_bounds__(64)
-bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ z, int64_t d0,
+bs_sim(BsShape r, const int32_t* __restrict__ R, const int32_t* __restrict__ next,
+       const int64_t* __restrict__ sizes, int64_t d0,
        uint64_t* __restrict__ L0, int8_t* __restrict__ hit, int64_t* __restrict__ hits) {
   __shared__ uint32_t l1[kBsW1];
   __shared__ uint32_t l2[kBsW2];
@@ -128,7 +105,11 @@ bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ 
   const int64_t W2 = (W1 + 31) >> 5;
   uint64_t* l0 = L0 + i * W0;
   const int32_t* Xr = next + i * r.M_max;
-  const int64_t* zr = z + i * r.M_max;
+  const int32_t* Rr = R + i * r.M_max;
+  // a sample's size (0 for an id outside [0, F))
+  auto size_at_id = [&](int32_t k) -> int64_t {
+    return (k >= 0 && k < r.F) ? sizes[k] : int64_t(0);
+  };
   int8_t* hrow = hit + i * r.M_max;
   for (int64_t w = lane; w < W0; w += 64) l0[w] = 0u;
   for (int64_t w = lane; w < W1; w += 64) l1[w] = 0u;
@@ -251,7 +232,8 @@ bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ 
       __builtin_amdgcn_wave_barrier();
       const int32_t key = lane < total ? kslot[lane] : INT32_MAX;
       ck = key;
-      cz = (lane < total && key >= 0 && key < Mi) ? zr[key] : 0;
+      const int32_t kid = (lane < total && key >= 0 && key < Mi) ? Rr[key] : -1;
+      cz = size_at_id(kid);
       n = total;
       // wait for the sizes here, once: an empty asm that takes and redefines
       // them, so no later use of the cache waits on memory (such a wait would
@@ -286,7 +268,10 @@ bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ 
 
   // the next batch: sizes, next uses, lane 0's copy of its word, and the
   // changes made to that word since it was loaded
-  int64_t sN = lane < Mi ? zr[lane] : 0;
+  // pipeline: ids and next uses two batches ahead, sizes one
+  int32_t kN2 = 64 + lane < Mi ? Rr[64 + lane] : -1;
+  int32_t nN2 = 64 + lane < Mi ? Xr[64 + lane] : -1;
+  int64_t sN = size_at_id(lane < Mi ? Rr[lane] : -1);
   int32_t nN = lane < Mi ? Xr[lane] : -1;
   uint64_t hN = 0;  // every word starts empty
   for (int64_t f0 = 0; f0 < Mi; f0 += 64, ++b) {
@@ -298,10 +283,12 @@ bs_sim(BsShape r, const int32_t* __restrict__ next, const int64_t* __restrict__ 
     const uint64_t cand = __ballot(nx >= 0 && s <= d0);
     nset = nclr = 0;
     hN = 0;
-    {  // the next batch's loads, after this batch's values are in use
-      const int64_t g = f + 64;
-      sN = g < Mi ? zr[g] : 0;
-      nN = g < Mi ? Xr[g] : -1;
+    {  // the next batches' loads, after this batch's values are in use
+      sN = size_at_id(kN2);
+      nN = nN2;
+      const int64_t g = f + 128;
+      kN2 = g < Mi ? Rr[g] : -1;
+      nN2 = g < Mi ? Xr[g] : -1;
       if (lane == 0 && b + 1 < W0) hN = l0_load(&l0[b + 1]);
     }
     uint64_t mask = cand | hw;
@@ -379,17 +366,8 @@ int buffer_impl(const nopfs_job* job, const int32_t* R, const int32_t* next, con
   const int64_t W0 = (s.M_max + 63) >> 6;
   Scratch scr(st);
   uint64_t* L0;
-  int64_t* z;
   if ((rc = scr.alloc_n(&L0, size_t(s.N * W0)))) return rc;
-  if ((rc = scr.alloc_n(&z, size_t(s.N * s.M_max)))) return rc;
-  if (s.M_max > 0) {
-    const int64_t bx = std::min<int64_t>((s.M_max + 1023) / 1024, 64);
-    const int64_t by = std::min<int64_t>(s.N, 65535);
-    if ((rc = launch("bs_sizes", bs_sizes, dim3(uint32_t(bx), uint32_t(by)), dim3(256), 0, st, r,
-                     R, sizes, z)))
-      return rc;
-  }
-  return launch("bs_sim", bs_sim, dim3(uint32_t(s.N)), dim3(64), 0, st, r, next, z, d0, L0, hit,
+  return launch("bs_sim", bs_sim, dim3(uint32_t(s.N)), dim3(64), 0, st, r, R, next, sizes, d0, L0, hit,
                 hits);
 }
 
