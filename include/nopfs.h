@@ -93,6 +93,19 @@ int nopfs_stream_shape(const nopfs_job* job, int64_t* T, int64_t* M_max,
  * Errors: EINVAL, ERANGE, ENOMEM, EDEVICE. */
 int nopfs_access_streams(const nopfs_job* job, int32_t* R, void* hip_stream);
 
+/* The access streams of epochs [e_begin, e_end) only, as a job resumed at
+ * epoch e_begin would regenerate them (every epoch's shuffle depends only on
+ * the seed and the epoch). R is laid out as the streams of a job with the
+ * same F, N, B, drop_last and e_end - e_begin epochs: int32
+ * [N][(e_end - e_begin) * max_i L_i], row i = columns [e_begin * L_i,
+ * e_end * L_i) of nopfs_access_streams' row i, then -1 padding. That job
+ * (E = e_end - e_begin) is the shape to pass to nopfs_access_stats,
+ * nopfs_reuse_next and nopfs_tier_plan for the remaining epochs. An empty
+ * range writes nothing. Errors: EINVAL (also unless 0 <= e_begin <= e_end
+ * <= E), ERANGE, ENOMEM, EDEVICE. */
+int nopfs_access_streams_range(const nopfs_job* job, int32_t e_begin, int32_t e_end,
+                               int32_t* R, void* hip_stream);
+
 /* Access frequencies and first reads (section 3.1: worker i's access
  * frequency X of sample k over all E epochs; section 5.1 names it r_k).
  *   R:     int32 [N][M_max], as written by nopfs_access_streams for this job

@@ -22,7 +22,7 @@ int plan_job_impl(const nopfs_job* job, const int64_t* sizes, const int64_t* cap
     return fail(NOPFS_EINVAL, "sizes, caps, count, first, tier and used must be non-NULL");
   if (s.M_max > 0 && (!R || !next)) return fail(NOPFS_EINVAL, "R and next must be non-NULL");
   if ((rc = plan_check(caps, J))) return rc;
-  if ((rc = streams_impl(job, R, st))) return rc;
+  if ((rc = streams_impl(job, R, st, -1, -1))) return rc;
   if (s.M_max == 0) {  // nothing is read: every cell is class 0
     if ((rc = stats_impl(job, R, count, first, st))) return rc;
     return plan_impl(job, count, first, sizes, caps, J, tier, used, st);

@@ -67,7 +67,10 @@ void compact_plan_free(CompactPlan* cp);
 int plan_check(const int64_t* caps, int32_t J);
 
 // Stage bodies shared by the separate entry points and the fused call.
-int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st);
+// Streams of epochs [e_begin, e_end) (e_begin < 0: all epochs), written as
+// the rows of a job of e_end - e_begin epochs.
+int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st, int32_t e_begin,
+                 int32_t e_end);
 int stats_impl(const nopfs_job* job, const int32_t* R, uint8_t* count, int32_t* first,
                hipStream_t st);
 int plan_impl(const nopfs_job* job, const uint8_t* count, const int32_t* first,

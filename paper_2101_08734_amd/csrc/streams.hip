@@ -61,7 +61,8 @@ struct StreamParams {
   uint32_t nb;        // fine buckets per epoch
   uint32_t nb1;       // coarse buckets per epoch
   uint32_t nf;        // fine buckets per coarse bucket (nb = nb1 * nf)
-  int32_t e0;         // first epoch of the batch
+  int32_t e0;         // first epoch of the batch (the epoch its keys are drawn for)
+  int32_t e_first;    // epoch written at the start of the rows
   int32_t sort_bits;  // significant bits of a key inside its bucket
   int32_t cap;        // largest bucket sorted in LDS
 };
@@ -355,7 +356,7 @@ __device__ void global_bitonic(uint32_t* gk, int32_t* gi, uint32_t n) {
 
 __device__ __forceinline__ int64_t row_offset(const StreamParams& p, uint32_t i, int64_t e) {
   const int64_t Li = p.drop_last ? p.L : epoch_len(p.F, p.N, p.B, 0, i);
-  return int64_t(i) * p.M_max + e * Li;
+  return int64_t(i) * p.M_max + (e - p.e_first) * Li;
 }
 
 __global__ void __launch_bounds__(kSortThreads)
@@ -518,10 +519,20 @@ __global__ void stream_pad(StreamParams p, int32_t* __restrict__ R) {
 
 }  // namespace
 
-int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st) {
+int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st, int32_t e_begin,
+                 int32_t e_end) {
   Shape s;
   int rc = make_shape(job, &s);
   if (rc) return rc;
+  if (e_begin < 0) e_begin = 0, e_end = int32_t(s.E);  // the whole job
+  if (e_end < e_begin || e_end > s.E) return fail(NOPFS_EINVAL, "epochs must satisfy 0 <= e_begin <= e_end <= E");
+  // rows of the range: a job of e_end - e_begin epochs (same F, N, B)
+  if (e_end - e_begin != s.E) {
+    if (e_end == e_begin) return NOPFS_OK;  // no epochs: R has no elements
+    nopfs_job sub = *job;
+    sub.E = e_end - e_begin;
+    if ((rc = make_shape(&sub, &s))) return rc;
+  }
   if (s.M_max == 0) return NOPFS_OK;  // no reads: R has no elements and may be NULL
   if (!R) return fail(NOPFS_EINVAL, "R is NULL");
 
@@ -548,6 +559,7 @@ int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st) {
   p.nf = nf;
   p.sort_bits = bits;
   p.cap = int32_t(cap);
+  p.e_first = e_begin;
 
   // epochs per batch: the pair arrays of a batch stay under ~16 GB of scratch
   const int64_t budget = int64_t(16) << 30;
@@ -574,7 +586,7 @@ int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st) {
 
   for (int64_t e0 = 0; e0 < s.E; e0 += EB) {
     const uint32_t eb = uint32_t(e0 + EB <= s.E ? EB : s.E - e0);
-    p.e0 = int32_t(e0);
+    p.e0 = int32_t(e_begin + e0);
     if ((rc = launch("stream_count", stream_count, dim3(nchunks, eb), dim3(kChunkThreads),
                      size_t(nb) * 4, st, p, nchunks, cnt)))
       return rc;
@@ -608,7 +620,19 @@ int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st) {
 
 extern "C" int nopfs_access_streams(const nopfs_job* job, int32_t* R, void* hip_stream) {
   try {
-    return nopfs::streams_impl(job, R, static_cast<hipStream_t>(hip_stream));
+    return nopfs::streams_impl(job, R, static_cast<hipStream_t>(hip_stream), -1, -1);
+  } catch (const std::bad_alloc&) {
+    return nopfs::fail(NOPFS_ENOMEM, "host allocation failed");
+  } catch (...) {
+    return nopfs::fail(NOPFS_EDEVICE, "unexpected host exception");
+  }
+}
+
+extern "C" int nopfs_access_streams_range(const nopfs_job* job, int32_t e_begin, int32_t e_end,
+                                          int32_t* R, void* hip_stream) {
+  try {
+    if (e_begin < 0) return nopfs::fail(NOPFS_EINVAL, "epochs must satisfy 0 <= e_begin <= e_end <= E");
+    return nopfs::streams_impl(job, R, static_cast<hipStream_t>(hip_stream), e_begin, e_end);
   } catch (const std::bad_alloc&) {
     return nopfs::fail(NOPFS_ENOMEM, "host allocation failed");
   } catch (...) {

@@ -46,6 +46,13 @@ class Job:
         return _Job(int(self.F), int(self.E), int(self.N), int(self.B),
                     int(self.drop_last), int(self.seed) & ((1 << 64) - 1))
 
+    def epochs(self, e_begin: int, e_end: int) -> "Job":
+        """The shape of epochs [e_begin, e_end) of this job: what
+        access_streams_range writes, and what the stats, next-use and plan
+        calls take for those epochs' streams. (Its own access_streams would
+        draw epochs 0.., not e_begin..: use access_streams_range.)"""
+        return Job(self.F, int(e_end) - int(e_begin), self.N, self.B, self.drop_last, self.seed)
+
 
 class Model(ctypes.Structure):
     """Parameters of the performance model (nopfs_model): bytes, bytes/s,
@@ -92,6 +99,7 @@ def lib() -> ctypes.CDLL:
             "nopfs_staging_schedule": [jp, P, P, I64, P, P],
             "nopfs_fetch_model": [jp, P, P, P, ctypes.POINTER(Model), P, P, P],
             "nopfs_buffer_sim": [jp, P, P, P, I64, P, P, P],
+            "nopfs_access_streams_range": [jp, ctypes.c_int32, ctypes.c_int32, P, P],
             "nopfs_policy_sim": [jp, P, P, P, P, ctypes.POINTER(Model), ctypes.c_int32, P, P, P, P],
             "nopfs_profile_enable": [ctypes.c_int],
             "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
@@ -111,7 +119,8 @@ def lib() -> ctypes.CDLL:
     return _lib
 
 
-EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_stats",
+EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_streams_range",
+            "nopfs_access_stats",
             "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_prefetch_order",
             "nopfs_staging_schedule", "nopfs_fetch_model", "nopfs_buffer_sim", "nopfs_policy_sim",
             "nopfs_strerror",
@@ -183,6 +192,20 @@ def access_stats(job: Job, R, count=None, first=None, stream=None):
     _check(lib().nopfs_access_stats(ctypes.byref(j), _ptr(R), _ptr(count), _ptr(first),
                                     _stream(stream)), "nopfs_access_stats")
     return count, first
+
+
+def access_streams_range(job: Job, e_begin: int, e_end: int, R=None, stream=None):
+    """Streams of epochs [e_begin, e_end) (nopfs_access_streams_range), shaped
+    as the streams of job.epochs(e_begin, e_end)."""
+    sub = job.epochs(e_begin, e_end)
+    M = stream_shape(sub)[1] if e_end > e_begin else 0
+    if R is None:
+        R = torch.empty((job.N, M), dtype=torch.int32, device="cuda")
+    _device_tensor(R, torch.int32, (job.N, M), "R")
+    j = job.c()
+    _check(lib().nopfs_access_streams_range(ctypes.byref(j), int(e_begin), int(e_end), _ptr(R),
+                                            _stream(stream)), "nopfs_access_streams_range")
+    return R
 
 
 def reuse_next(job: Job, R, next=None, stream=None):

@@ -215,6 +215,25 @@ def test_policy_argument_checks(L):
               None) == nopfs.NOPFS_ERANGE
 
 
+def test_stream_range_checks(L):
+    j = _job(E=5)
+    rs = L.nopfs_access_streams_range
+    E = nopfs.NOPFS_EINVAL
+    assert rs(ctypes.byref(j), -1, 3, FAKE, None) == E
+    assert rs(ctypes.byref(j), 3, 2, FAKE, None) == E
+    assert rs(ctypes.byref(j), 0, 6, FAKE, None) == E
+    assert rs(ctypes.byref(j), 1, 3, None, None) == E
+    assert rs(None, 0, 1, FAKE, None) == E
+    # an empty range writes nothing and touches no pointer
+    assert rs(ctypes.byref(j), 2, 2, None, None) == 0
+    assert rs(ctypes.byref(j), 5, 5, None, None) == 0
+    assert L.nopfs_debug_set(3, 1) == 0
+    assert rs(ctypes.byref(j), 1, 4, FAKE, None) == nopfs.NOPFS_ENOMEM
+    assert L.nopfs_debug_set(3, 0) == 0
+    sub = nopfs.Job(100, 5, 2, 4, 1, 1).epochs(1, 4)
+    assert (sub.E, sub.F, sub.N, sub.B) == (3, 100, 2, 4)
+
+
 def test_scratch_failure_is_enomem(L):
     """The test hook fails the next internal allocation; the call reports
     NOPFS_ENOMEM before launching anything."""
