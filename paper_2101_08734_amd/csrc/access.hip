@@ -169,7 +169,6 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
            const ClassTable* __restrict__ classes) {
   extern __shared__ uint32_t sm[];
   __shared__ uint32_t s_cnt, s_base;
-  __shared__ uint32_t s_tmp[65];
   __shared__ ClassTable s_ct;  // kCompact: the bin table
   uint32_t* cw = sm;                                        // byte counters
   int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsCwWords);  // first reads
@@ -287,16 +286,14 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
       }
     }
     if (kCompact) {
-      // list: slots from one block scan (its barriers also end every read of
-      // the LDS tables and every single cell's slot claim); the read cells
-      // are staged raw in the (now free) first-read table, then binned and
-      // written out as one contiguous run. More than the table holds: binned
-      // and written directly.
-      uint32_t total;
-      uint32_t slot = block_exclusive_scan(nmine, s_tmp, &total);
-      const uint32_t run0 = s_cnt;  // entries already listed for this tile
-      uint2* stage = reinterpret_cast<uint2*>(fi);
-      const bool staged = total <= uint32_t(kStatsWin / 2);
+      // list: each wave claims one run of slots for its read cells with a
+      // single atomic (the list's users do not depend on the order of a
+      // tile's entries) and writes the entries there directly
+      const uint32_t incl = wave_inclusive_scan(nmine);
+      const uint32_t wtot = __shfl(incl, 63, 64);
+      uint32_t wbase = 0;
+      if (__lane_id() == 0 && wtot) wbase = atomicAdd(&s_cnt, wtot);
+      uint32_t slot = __shfl(wbase, 0, 64) + incl - nmine;
 #pragma unroll
       for (int m = 0; m < kUnits; ++m) {
         const uint32_t x = head + 4 * (threadIdx.x + uint32_t(m) * kStatsThreads);
@@ -304,20 +301,9 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const uint32_t c = (cwr[m] >> (8 * q)) & 0xFFu;
-          if (c) {
-            if (staged) stage[slot] = make_uint2(uint32_t(fv[q]), (c << 24) | (xoff + x + q));
-            else cdst[run0 + slot] = entry(c, fv[q], xoff + x + q);
-            ++slot;
-          }
+          if (c) cdst[slot++] = entry(c, fv[q], xoff + x + q);
         }
       }
-      __syncthreads();
-      if (staged)
-        for (uint32_t t = threadIdx.x; t < total; t += kStatsThreads) {
-          const uint2 e = stage[t];
-          cdst[run0 + t] = entry(e.y >> 24, int32_t(e.x), e.y & 0xFFFFFFu);
-        }
-      if (threadIdx.x == 0) s_cnt = run0 + total;
     }
     __syncthreads();
   }
