@@ -125,6 +125,9 @@ def committed_traffic(workload, kernel):
 
 
 POLICY_NAMES = ("perfect", "naive", "staging", "nopfs")
+SEQUENTIAL_NOTE = ("sequential per worker (each read depends on every earlier one), one wave "
+                   "per worker: bound by the wave's instruction issue and latency, not by HBM; "
+                   "frac is the HBM fraction for reference")
 
 
 def _kernel_short_name(full):
@@ -357,6 +360,7 @@ def time_buffer(nopfs, torch, w, job, M, M_w, R, nxt, sizes, steps, warmup, stre
     out["hit_rate"] = round(int(h[:, 0].sum()) / A, 4)
     out["hit_bytes"] = int(h[:, 1].sum())
     out["reads_per_s_per_worker"] = round(A / job.N / (out["buffer_sim"]["ms_per_call"] * 1e-3), 1)
+    out["buffer_sim"]["roofline"]["note"] = SEQUENTIAL_NOTE
     return out
 
 
@@ -387,6 +391,7 @@ def time_policies(nopfs, torch, wl, w, job, M, M_w, R, tier, sizes, steps, warmu
         J = model.J
         out[name]["slowest_worker_s"] = round(float(f.max()), 3)
         out[name]["mean_worker_s"] = round(float(f.mean()), 3)
+        out[name]["roofline"]["note"] = SEQUENTIAL_NOTE
         out[name]["fetch_s"] = {"pfs": round(float(tot[0]), 1),
                                 "remote": round(float(tot[1:1 + J].sum()), 1),
                                 "own": round(float(tot[1 + J:].sum()), 1)}
