@@ -24,7 +24,9 @@
 //                 of R: each read's source from its own tier and the
 //                 sample's best remote class; size and source in
 //                 partitioned order.
-//   fm_sum     -- per sub-chunk of 2^14 reads: back to stream order in LDS;
+//   fm_sum     -- per sub-chunk of 2^14 reads: every entry loaded once into
+//                 the LDS slot of its stream position (the whole sub-chunk,
+//                 135 KB), then scanned in four parts of 4,096 positions:
 //                 its read-time sum, compute-time sum and maximum of
 //                 avail - U relative to its start.
 //   fm_scan    -- per worker: what enters each sub-chunk.
@@ -44,9 +46,6 @@ namespace {
 #endif
 #ifndef NOPFS_FM_THREADS
 #define NOPFS_FM_THREADS 1024  // threads of the scan kernels (tuning only)
-#endif
-#ifndef NOPFS_FM_FINAL_WAVES
-#define NOPFS_FM_FINAL_WAVES 8  // fm_final's occupancy target (tuning only)
 #endif
 
 constexpr int kMaxClasses = 32;
@@ -251,11 +250,13 @@ __device__ __forceinline__ double block_excl(double v, double* tmp, double* tota
   return r;
 }
 
-__device__ __forceinline__ int fm_slot(int p) { return p + p / kFmPer; }
+// LDS slot of position p: one pad per 32 positions, so the four
+// consecutive positions each thread takes fall on distinct banks across a
+// half-wave
+__device__ __forceinline__ int fm_slot(int p) { return p + (p >> 5); }
 
 struct FmLds {
-  uint64_t sv[kFmPart + kFmPart / kFmPer];  // entries, then results, by position
-  uint16_t pos[kSC];                        // stream position of each entry
+  uint64_t sv[kSC + kSC / 32];  // the sub-chunk's entries by position, then results
   double tmp[65];
   SharedRates sr;
 };
@@ -272,23 +273,17 @@ template <bool kFinal>
 __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* __restrict__ Pk,
                          const uint64_t* __restrict__ zP, const Rates& rt, FmLds& L, Enter in,
                          Enter* sum_out, int16_t* __restrict__ src, double* __restrict__ tout) {
-  // stream position of every entry (in LDS); each entry's payload is
-  // loaded in the part that holds its position (once per entry)
+  // every entry of the sub-chunk, loaded once and coalesced, into the LDS
+  // slot of its stream position
   for (int64_t q = threadIdx.x; q < s.len; q += kFmThreads)
-    L.pos[q] = uint16_t(Pk[s.base + q] & kJMask);
+    L.sv[fm_slot(int(Pk[s.base + q] & kJMask))] = zP[s.base + q];
   __syncthreads();
   const double inv_p0 = 1.0 / rt.p0;
   double ca = 0, cu = 0, cm = -INFINITY;  // running over the parts, relative to the chunk
   const double base_mu = in.a * inv_p0 - in.u;
   for (int64_t j0 = 0; j0 < s.len; j0 += kFmPart) {
     const uint32_t hl = uint32_t(s.len - j0 < kFmPart ? s.len - j0 : kFmPart);
-#pragma unroll 4
-    for (int u = 0; u < kFmEnt; ++u) {
-      const int64_t q = int64_t(u) * kFmThreads + threadIdx.x;
-      const uint32_t x = q < s.len ? uint32_t(L.pos[q]) - uint32_t(j0) : 0xFFFFFFFFu;
-      if (x < hl) L.sv[fm_slot(int(x))] = zP[s.base + q];
-    }
-    __syncthreads();
+    const int jb = int(j0);
     double rd[kFmPer], uu[kFmPer];
     uint32_t cd[kFmPer];
     double ta = 0, tu = 0;
@@ -299,7 +294,7 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
       uu[u] = 0;
       cd[u] = 0;
       if (x < int(hl)) {
-        const uint64_t e = L.sv[fm_slot(x)];
+        const uint64_t e = L.sv[fm_slot(jb + x)];
         const double sz = double(e & kSizeMask);
         cd[u] = uint32_t(e >> kSizeBits);
         rd[u] = sz * inv_rate_of(rt, L.sr, cd[u]) + sz * rt.inv_wthr;
@@ -338,27 +333,27 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
       __syncthreads();  // every entry is read
 #pragma unroll
       for (int u = 0; u < kFmPer; ++u)
-        L.sv[fm_slot(int(threadIdx.x) * kFmPer + u)] = __double_as_longlong(tv[u]);
+        L.sv[fm_slot(jb + int(threadIdx.x) * kFmPer + u)] = __double_as_longlong(tv[u]);
       __syncthreads();
       double* td = tout + s.base + j0;
 #pragma unroll
       for (int u = 0; u < kFmPer; ++u) {
         const int x = u * kFmThreads + int(threadIdx.x);
-        if (x < int(hl)) td[x] = __longlong_as_double(L.sv[fm_slot(x)]);
+        if (x < int(hl)) td[x] = __longlong_as_double(L.sv[fm_slot(jb + x)]);
       }
       __syncthreads();
 #pragma unroll
       for (int u = 0; u < kFmPer; ++u) {
         const uint32_t c = cd[u];
         const uint64_t out = c == 0 ? 0u : (c < kOwn0 ? 128u + (c - 1) : 256u + (c - kOwn0));
-        L.sv[fm_slot(int(threadIdx.x) * kFmPer + u)] = out;
+        L.sv[fm_slot(jb + int(threadIdx.x) * kFmPer + u)] = out;
       }
       __syncthreads();
       int16_t* sd = src + s.base + j0;
 #pragma unroll
       for (int u = 0; u < kFmPer; ++u) {
         const int x = u * kFmThreads + int(threadIdx.x);
-        if (x < int(hl)) sd[x] = int16_t(L.sv[fm_slot(x)]);
+        if (x < int(hl)) sd[x] = int16_t(L.sv[fm_slot(jb + x)]);
       }
     }
     ca += tota;
@@ -370,7 +365,7 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
 }
 
 // two workgroups per CU
-__global__ void __launch_bounds__(kFmThreads) __attribute__((amdgpu_waves_per_eu(8)))
+__global__ void __launch_bounds__(kFmThreads)
 fm_sum(SegParams p, const uint32_t* __restrict__ Pk, const uint64_t* __restrict__ zP, Rates rt,
        uint32_t nch, Enter* __restrict__ sums) {
   __shared__ FmLds L;
@@ -398,7 +393,6 @@ fm_scan(int64_t N, uint32_t nch, double p0, Enter* __restrict__ sums) {
 }
 
 __global__ void __launch_bounds__(kFmThreads)
-__attribute__((amdgpu_waves_per_eu(NOPFS_FM_FINAL_WAVES)))
 fm_final(SegParams p, const uint32_t* __restrict__ Pk, const uint64_t* __restrict__ zP, Rates rt,
          uint32_t nch, const Enter* __restrict__ ins, int16_t* __restrict__ src,
          double* __restrict__ t) {
