@@ -419,8 +419,8 @@ def main():
         rocprof_summary(args.rocprof_summary, args.workload)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py plans all N workers of a job on one GPU; runs on more than one "
-              "GPU are not part of this build (use --gpus 1).", file=sys.stderr)
+        print("bench.py plans all N workers of a job on one GPU; it does not run on more "
+              "than one GPU (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch
