@@ -156,21 +156,25 @@ constexpr int kRunLoads = 8;
 // sum of the run starts).
 //
 // The LDS tables are laid out so that cell x of a pass sits at position
-// x + sh, sh = (flat index of the pass's first cell) mod 4: a 4-cell group of
-// the output rows is then one aligned 32-bit count word and one aligned
-// 128-bit first-read word in LDS.
-constexpr int kStatsCwWords = ((kStatsWin + 4) / 4 + 3) & ~3;  // byte counters, 16-byte padded
+// (x + sh) mod kStatsWin, sh = (flat index of the pass's first cell) mod 4: a
+// 4-cell group of the output rows is then one aligned 32-bit count word and
+// one aligned 128-bit first-read word in LDS. Only cells after the last
+// group wrap around, so the tables take exactly kStatsWin cells (40 KB, four
+// workgroups per CU) and the workgroup uses no other LDS: each wave sums the
+// run starts itself, holds the bin records of classes below 64 one per lane
+// (looked up with a lane shuffle), and claims list slots with one atomic on
+// the tile's entry count in global memory.
+constexpr int kStatsCwWords = kStatsWin / 4;  // byte counters
+constexpr uint32_t kStatsPosMask = kStatsWin - 1;
 
 template <bool kVec, bool kCompact>
-__global__ void __launch_bounds__(kStatsThreads)
+__global__ void __launch_bounds__(kStatsThreads) __attribute__((amdgpu_waves_per_eu(8)))
 stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
            uint8_t* __restrict__ count, int32_t* __restrict__ first, uint32_t ntiles,
            uint32_t* __restrict__ cent, int32_t* __restrict__ cbase, uint32_t* __restrict__ cnum,
            const ClassTable* __restrict__ classes) {
   extern __shared__ uint32_t sm[];
-  __shared__ uint32_t s_cnt, s_base;
-  __shared__ ClassTable s_ct;  // kCompact: the bin table
-  uint32_t* cw = sm;                                        // byte counters
+  uint32_t* cw = sm;                                             // byte counters
   int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsCwWords);  // first reads
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
@@ -185,33 +189,53 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;  // run starts in window kb
   const uint16_t* ob = oa + runs;                            // run ends
   const uint32_t nsc = uint32_t(p.nsc);
-  uint32_t* crow_ent = kCompact ? cent + i * p.M_max : nullptr;
-  if (kCompact && threadIdx.x == 0) {
-    s_cnt = 0;
-    s_base = 0;
+  const uint32_t lane = __lane_id();
+  // kCompact: the worker's reads in earlier windows (the run starts are
+  // requested four per lane at once), and the tile's entry count zeroed
+  uint32_t base = 0, zold = 0;
+  if (kCompact) {
+    if (threadIdx.x == 0) zold = atomicExch(&cnum[tile], 0u);
+    for (int64_t r0 = lane; r0 < runs; r0 += 256) {
+      uint32_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {  // clamped index: the loads are unconditional
+        const int64_t r = r0 + 64 * u;
+        v[u] = oa[r < runs ? r : runs - 1];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = r0 + 64 * u < runs ? v[u] : 0u;
+      base += v[0] + v[1] + v[2] + v[3];
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) base += __shfl_xor(base, d, 64);
+    base = __builtin_amdgcn_readfirstlane(base);
   }
-  if (kCompact)
-    for (int c = threadIdx.x; c < 256; c += kStatsThreads) s_ct.e[c] = classes->e[c];
   for (int64_t w0 = k0; w0 < kend; w0 += kStatsWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kStatsWin ? kend - w0 : kStatsWin);
     const uint32_t xoff = uint32_t(w0 - k0);
     const uint32_t sh = kVec ? uint32_t((i * p.F + w0) & 3) : 0u;
+    // addresses below are formed anew in each pass (the empty asm keeps
+    // the compiler from holding them in registers across the pass)
+    uint32_t tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
     // bounds of this thread's first run, requested before the LDS is cleared
     uint32_t ra = 0, rb = 0;
-    if (threadIdx.x < runs) {
-      ra = oa[threadIdx.x];
-      rb = ob[threadIdx.x];
+    if (tid < runs) {
+      ra = oa[tid];
+      rb = ob[tid];
     }
-    for (uint32_t x = threadIdx.x; x < (wlen + sh + 3) / 4; x += kStatsThreads) cw[x] = 0;
-    for (uint32_t x = threadIdx.x; x < wlen + sh; x += kStatsThreads) fi[x] = INT_MAX;
+    const uint32_t ncl = wlen + sh < uint32_t(kStatsWin) ? wlen + sh : uint32_t(kStatsWin);
+    for (uint32_t x = threadIdx.x; x < (ncl + 3) / 4; x += kStatsThreads) cw[x] = 0;
+    for (uint32_t x = threadIdx.x; x < ncl; x += kStatsThreads) fi[x] = INT_MAX;
+    // kCompact: the zeroing of the entry count has been performed (its old
+    // value returned) before this barrier; every claim comes after it
+    if (kCompact && w0 == k0) asm volatile("" ::"v"(zold));
     __syncthreads();
-    uint32_t start_sum = 0;
     for (int64_t r = threadIdx.x; r < runs; r += kStatsThreads) {
       if (r != threadIdx.x) {
         ra = oa[r];
         rb = ob[r];
       }
-      start_sum += ra;
       const uint32_t e = uint32_t(r) / nsc, sc = uint32_t(r) - e * nsc;
       const int64_t fb = int64_t(e) * Li + int64_t(sc) * kSC;
       const uint32_t* src = prow + fb;
@@ -223,94 +247,147 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
         for (int u = 0; u < kRunLoads; ++u) {
           const uint32_t x = (v[u] >> kScShift) - xoff;
           if (q + u < rb && x < wlen) {
-            const uint32_t px = x + sh;
+            const uint32_t px = (x + sh) & kStatsPosMask;
             atomicAdd(&cw[px >> 2], 1u << ((px & 3u) * 8u));
             atomicMin(&fi[px], int32_t(fb + (v[u] & kJMask)));
           }
         }
       }
     }
-    if (kCompact && w0 == k0) {
-#pragma unroll
-      for (int d = 32; d >= 1; d >>= 1) start_sum += __shfl_xor(start_sum, d, 64);
-      if (__lane_id() == 0 && start_sum) atomicAdd(&s_base, start_sum);
-    }
     __syncthreads();
+    // kCompact: bin record of class `lane`, requested here so that it
+    // arrives while the tables are read out
+    float rec_s = 0.f;
+    uint32_t rec_b = 0;
+    if (kCompact && kVec) {
+      const float2 r = classes->e[tid & 63u];
+      rec_s = r.x;
+      rec_b = __float_as_uint(r.y);
+    }
+    // bin of a read cell of class c < 64 (all lanes call it: the shuffle
+    // reads other lanes), and of any class from the table in memory
+    auto bin_lane = [&](uint32_t c, int32_t f) {
+      return bin_of(__shfl(rec_s, int(c), 64), __shfl(rec_b, int(c), 64), f);
+    };
+    auto bin_mem = [&](uint32_t c, int32_t f) { return bin_read(*classes, c, f); };
     uint8_t* crow = count + i * p.F + w0;
     int32_t* frow = first + i * p.F + w0;
-    uint32_t* cdst = kCompact ? crow_ent + s_base : nullptr;
-    auto cnt_at = [&](uint32_t x) {  // x: cell of the pass
-      const uint32_t px = x + sh;
-      return (cw[px >> 2] >> ((px & 3u) * 8u)) & 0xFFu;
-    };
-    auto entry = [&](uint32_t c, int32_t f, uint32_t xw) {
-      return (bin_read(s_ct, c, f) << kListOffBits) | xw;
-    };
-    auto single = [&](uint32_t x) {
-      const uint32_t c = cnt_at(x);
-      const int32_t f = fi[x + sh];
-      crow[x] = uint8_t(c);
-      frow[x] = c ? f : -1;
-      if (kCompact && c) cdst[atomicAdd(&s_cnt, 1u)] = entry(c, f, xoff + x);
-    };
-    // cells up to the first flat index divisible by 4 and after the last
-    // group of 4 go one per thread; the rest as 4-cell groups per lane
+    // cells up to the first flat index divisible by 4 (head, at most 3) and
+    // after the last group of 4 (at most 3) go one per thread; the rest as
+    // 4-cell groups per lane
     uint32_t head = kVec ? uint32_t((4 - ((i * p.F + w0) & 3)) & 3) : wlen;
     if (head > wlen) head = wlen;
     const uint32_t nunits = (wlen - head) >> 2;
     const uint32_t tail0 = head + 4 * nunits;
-    for (uint32_t x = threadIdx.x; x < head; x += kStatsThreads) single(x);
-    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kStatsThreads) single(x);
-    // 4-cell groups: one count word and one first-read quad from LDS; each
-    // thread keeps its groups' words for the list below
+    auto cell = [&](uint32_t x, uint32_t& c, int32_t& f) {
+      const uint32_t px = (x + sh) & kStatsPosMask;
+      c = (cw[px >> 2] >> ((px & 3u) * 8u)) & 0xFFu;
+      f = c ? fi[px] : -1;
+    };
+    uint32_t c1 = 0, c2 = 0;
+    int32_t f1 = -1, f2 = -1;
+    if (kVec) {
+      if (threadIdx.x < head) cell(threadIdx.x, c1, f1);
+      if (tail0 + threadIdx.x < wlen) cell(tail0 + threadIdx.x, c2, f2);
+    } else {
+      for (uint32_t x = threadIdx.x; x < wlen; x += kStatsThreads) {
+        uint32_t c;
+        int32_t f;
+        cell(x, c, f);
+        crow[x] = uint8_t(c);
+        frow[x] = f;
+        if (kCompact && c) {  // unaligned rows: one list slot per cell
+          const uint32_t b = bin_of(classes->e[c].x, __float_as_uint(classes->e[c].y), f);
+          cent[i * p.M_max + base + atomicAdd(&cnum[tile], 1u)] = (b << kListOffBits) | (xoff + x);
+        }
+      }
+    }
+    // 4-cell groups: one count word and one first-read quad from LDS
     constexpr int kUnits = kStatsWin / 4 / kStatsThreads;
     uint32_t cwr[kUnits];
     int4 frr[kUnits];
-    uint32_t nmine = 0;
+    uint32_t nmine = (c1 != 0) + (c2 != 0);
 #pragma unroll
     for (int m = 0; m < kUnits; ++m) {
       const uint32_t u = threadIdx.x + uint32_t(m) * kStatsThreads;
       const uint32_t x = head + 4 * u;  // x + sh is a multiple of 4
       cwr[m] = 0;
+      frr[m] = make_int4(-1, -1, -1, -1);
       if (u < nunits) {
-        const uint32_t word = cw[(x + sh) >> 2];
-        const int4 fq = *reinterpret_cast<const int4*>(&fi[x + sh]);
-        const int4 fo = make_int4((word & 0xFFu) ? fq.x : -1, (word & 0xFF00u) ? fq.y : -1,
-                                  (word & 0xFF0000u) ? fq.z : -1, (word >> 24) ? fq.w : -1);
-        *reinterpret_cast<uint32_t*>(crow + x) = word;
-        *reinterpret_cast<int4*>(frow + x) = fo;
+        const uint32_t px = (x + sh) & kStatsPosMask;  // no group wraps
+        const uint32_t word = cw[px >> 2];
+        const int4 fq = *reinterpret_cast<const int4*>(&fi[px]);
         cwr[m] = word;
-        frr[m] = fo;
+        frr[m] = make_int4((word & 0xFFu) ? fq.x : -1, (word & 0xFF00u) ? fq.y : -1,
+                           (word & 0xFF0000u) ? fq.z : -1, (word >> 24) ? fq.w : -1);
         nmine += ((word & 0xFFu) != 0) + ((word & 0xFF00u) != 0) + ((word & 0xFF0000u) != 0) +
                  ((word >> 24) != 0);
       }
     }
-    if (kCompact) {
-      // list: each wave claims one run of slots for its read cells with a
-      // single atomic (the list's users do not depend on the order of a
-      // tile's entries) and writes the entries there directly
-      const uint32_t incl = wave_inclusive_scan(nmine);
+    // list: each wave claims one run of slots for its read cells with a
+    // single atomic (the list's users do not depend on the order of a tile's
+    // entries), issued before the row stores so that its result does not
+    // wait for them
+    uint32_t incl = 0, wbase = 0;
+    if (kCompact && kVec) {
+      incl = wave_inclusive_scan(nmine);
       const uint32_t wtot = __shfl(incl, 63, 64);
-      uint32_t wbase = 0;
-      if (__lane_id() == 0 && wtot) wbase = atomicAdd(&s_cnt, wtot);
-      uint32_t slot = __shfl(wbase, 0, 64) + incl - nmine;
-#pragma unroll
-      for (int m = 0; m < kUnits; ++m) {
-        const uint32_t x = head + 4 * (threadIdx.x + uint32_t(m) * kStatsThreads);
-        const int32_t fv[4] = {frr[m].x, frr[m].y, frr[m].z, frr[m].w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t c = (cwr[m] >> (8 * q)) & 0xFFu;
-          if (c) cdst[slot++] = entry(c, fv[q], xoff + x + q);
-        }
+      // a per-lane zero offset keeps the compiler from rewriting this
+      // one-lane atomic into a wave reduction that waits for its result here
+      uint32_t z;
+      asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+      if (lane == 0 && wtot) wbase = atomicAdd(cnum + tile + z, wtot);
+    }
+    if (kVec) {
+      if (threadIdx.x < head) {
+        crow[threadIdx.x] = uint8_t(c1);
+        frow[threadIdx.x] = f1;
+      }
+      if (tail0 + threadIdx.x < wlen) {
+        crow[tail0 + threadIdx.x] = uint8_t(c2);
+        frow[tail0 + threadIdx.x] = f2;
       }
     }
-    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < kUnits; ++m) {
+      const uint32_t u = threadIdx.x + uint32_t(m) * kStatsThreads;
+      const uint32_t x = head + 4 * u;
+      if (u < nunits) {
+        *reinterpret_cast<uint32_t*>(crow + x) = cwr[m];
+        *reinterpret_cast<int4*>(frow + x) = frr[m];
+      }
+    }
+    if (kCompact && kVec) {
+      uint32_t* cdst = cent + i * p.M_max + base;
+      uint32_t slot = __builtin_amdgcn_readlane(wbase, 0) + incl - nmine;
+      auto emit = [&](auto bin) {
+        const uint32_t b1 = bin(c1, f1), b2 = bin(c2, f2);
+        if (c1) cdst[slot++] = (b1 << kListOffBits) | (xoff + threadIdx.x);
+        if (c2) cdst[slot++] = (b2 << kListOffBits) | (xoff + tail0 + threadIdx.x);
+#pragma unroll
+        for (int m = 0; m < kUnits; ++m) {
+          const uint32_t x = head + 4 * (threadIdx.x + uint32_t(m) * kStatsThreads);
+          const int32_t fv[4] = {frr[m].x, frr[m].y, frr[m].z, frr[m].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t c = (cwr[m] >> (8 * q)) & 0xFFu;
+            const uint32_t b = bin(c, fv[q]);
+            if (c) cdst[slot++] = (b << kListOffBits) | (xoff + x + q);
+          }
+        }
+      };
+      // counts of 64 or more (jobs of more epochs) take the table in memory
+      uint32_t hi = (c1 | c2) & 0xC0u;
+#pragma unroll
+      for (int m = 0; m < kUnits; ++m) hi |= cwr[m] & 0xC0C0C0C0u;
+      if (__any(hi != 0))
+        emit(bin_mem);
+      else
+        emit(bin_lane);
+    }
+    if (w0 + kStatsWin < kend) __syncthreads();  // the tables are reused
   }
-  if (kCompact && threadIdx.x == 0) {
-    cbase[tile] = int32_t(s_base);
-    cnum[tile] = s_cnt;
-  }
+  if (kCompact && threadIdx.x == 0) cbase[tile] = int32_t(base);
 }
 
 // -- next ---------------------------------------------------------------------
@@ -487,7 +564,7 @@ __global__ void fill_stats_empty(int64_t n, uint8_t* __restrict__ count, int32_t
 int launch_stats(const SegParams& p, const uint32_t* Pk, const uint16_t* OT, uint8_t* count,
                  int32_t* first, CompactCells* cc, const ClassTable* classes, hipStream_t st) {
   const uint32_t ntiles = uint32_t(p.N * p.nbk);
-  const size_t smem = size_t(kStatsCwWords + kStatsWin + 4) * 4;
+  const size_t smem = size_t(kStatsCwWords + kStatsWin) * 4;
   // vector stores need 4-byte aligned count rows and 16-byte aligned first rows
   const bool vec = (reinterpret_cast<uintptr_t>(count) & 3) == 0 &&
                    (reinterpret_cast<uintptr_t>(first) & 15) == 0;

@@ -16,13 +16,17 @@ struct ClassTable {
   float2 e[256];  // x = scale, y = bits of (base << 16 | top)
 };
 
-__device__ __forceinline__ uint32_t bin_read(const ClassTable& t, uint32_t c, int32_t f) {
-  const float2 r = t.e[c];
-  const uint32_t bt = __float_as_uint(r.y);
+// Bin of a read cell with first read f from its class's record (scale, bits).
+__device__ __forceinline__ uint32_t bin_of(float scale, uint32_t bt, int32_t f) {
   // a negative f (not a first read) lands in the class's first bin
-  const uint32_t xi0 = uint32_t(fmaxf(float(f) * r.x, 0.f));
+  const uint32_t xi0 = uint32_t(fmaxf(float(f) * scale, 0.f));
   const uint32_t top = bt & 0xFFFFu;
   return (bt >> 16) + (xi0 < top ? xi0 : top);
+}
+
+__device__ __forceinline__ uint32_t bin_read(const ClassTable& t, uint32_t c, int32_t f) {
+  const float2 r = t.e[c];
+  return bin_of(r.x, __float_as_uint(r.y), f);
 }
 
 // Read-cell list entry: bin << kListOffBits | offset of the sample in its

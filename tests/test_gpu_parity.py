@@ -181,6 +181,37 @@ def test_wide_windows(wide_case, path):
     compare(got, exp)
 
 
+def _offset_view(shape, dtype):
+    """A contiguous tensor one element into its allocation: rows that are
+    not 4- or 16-byte aligned (the counting pass's one-cell-at-a-time path)."""
+    n = int(np.prod(shape))
+    return torch.full((n + 1,), 7, dtype=dtype, device="cuda")[1:].view(shape)
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("name,F,E,N,B,d,seed,fr", [JOBS[1], JOBS[4]], ids=["ragged", "e255"])
+def test_unaligned_outputs(oracle, name, F, E, N, B, d, seed, fr, path):
+    sizes = wl.random_sizes(F, seed, 1_000, 2_000_000)
+    caps = _caps(sizes, fr)
+    job = nopfs.Job(F, E, N, B, d, seed)
+    exp = oracle.full_pipeline(oracle.make_job(F, E, N, B, d, seed), sizes, caps)
+    count = _offset_view((N, F), torch.uint8)
+    first = _offset_view((N, F), torch.int32)
+    assert count.data_ptr() % 4 and first.data_ptr() % 16
+    s = torch.from_numpy(sizes).cuda()
+    if path == "staged":
+        R = nopfs.access_streams(job)
+        nopfs.access_stats(job, R, count, first)
+        tier, used = nopfs.tier_plan(job, count, first, s, caps)
+        got = dict(count=count, first=first, tier=tier, used=used)
+    else:
+        got = nopfs.plan_job(job, s, caps, out=dict(count=count, first=first))
+        assert got["count"].data_ptr() == count.data_ptr()
+    torch.cuda.synchronize()
+    compare({k: v.cpu().numpy() for k, v in got.items()}, exp,
+            names=("count", "first", "tier", "used"))
+
+
 def test_invariants_medium():
     F, E, N, B, d, seed = 300_000, 9, 12, 16, 0, 77
     sizes = wl.random_sizes(F, seed, 1_000, 2_000_000)
