@@ -19,7 +19,7 @@
 //   5. stream_split   -- each coarse bucket read back in 16K-pair pieces and
 //                        split into its nf fine buckets (skipped when nf = 1).
 //   6. stream_sort    -- one workgroup per fine bucket: counting sort in LDS
-//                        by the top 11 bits of the key inside the bucket,
+//                        by the top 13 bits of the key inside the bucket,
 //                        each pair then placed inside its (tiny) digit group
 //                        by its rank in (key, id) order, and
 //                        the sorted positions p sharded straight into R:
@@ -51,7 +51,7 @@ constexpr uint32_t kMaxBuckets = 8192;
 constexpr int kSortThreads = NOPFS_SORT_THREADS;
 constexpr int kItems = NOPFS_SORT_ITEMS;
 constexpr int kSortCap = kSortThreads * kItems;  // 8192 (key, id) pairs in LDS
-constexpr int kDigitBits = 11;
+constexpr int kDigitBits = 13;
 constexpr int kDigits = 1 << kDigitBits;
 
 struct StreamParams {
@@ -311,11 +311,15 @@ stream_split(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __res
 }
 
 // -- 6. per-bucket sort and shard --------------------------------------------
+// 80 KB: two workgroups per CU. Digit counts and group starts are at most
+// kSortCap (< 2^16), so they are kept as 16-bit halves of 32-bit words, and
+// the scan's scratch lives in the pair array, which is unused until the
+// pairs are placed.
 struct SortSmem {
-  uint2 kv[kSortCap];  // (key, id) pairs; later the sorted ids and the shard stage
-  uint32_t hist[kDigits];
-  uint32_t tmp[65];
+  uint2 kv[kSortCap];          // (key, id) pairs; later the sorted ids and the shard stage
+  uint32_t hist[kDigits / 2];  // 16-bit digit counts, then group starts, two per word
 };
+static_assert(kSortCap < 65536, "16-bit digit counts");
 
 __device__ __forceinline__ bool pair_greater(uint32_t ka, int32_t ia, uint32_t kb, int32_t ib) {
   return ka > kb || (ka == kb && ia > ib);
@@ -389,7 +393,8 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
   const uint32_t key_lo = uint32_t(((uint64_t(b) << 32) + nb - 1) / nb);
   const int db = p.sort_bits < kDigitBits ? p.sort_bits : kDigitBits;
   const int dshift = p.sort_bits - db;
-  for (int x = threadIdx.x; x < kDigits; x += kSortThreads) s.hist[x] = 0;
+  for (int x = threadIdx.x; x < kDigits / 2; x += kSortThreads) s.hist[x] = 0;
+  const uint16_t* h16 = reinterpret_cast<const uint16_t*>(s.hist);  // digit d at [d]
   __syncthreads();
   // counting sort by the top bits of the key inside the bucket
   uint32_t k[kItems], slot[kItems];
@@ -405,24 +410,30 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
-    if (q < n) slot[r] = atomicAdd(&s.hist[k[r] >> dshift], 1u);
+    if (q < n) {
+      const uint32_t d = k[r] >> dshift;
+      const uint32_t half = (d & 1u) * 16u;
+      slot[r] = (atomicAdd(&s.hist[d >> 1], 1u << half) >> half) & 0xFFFFu;
+    }
   }
   __syncthreads();
   {
-    constexpr int kPer = kDigits / kSortThreads;
-    uint32_t v[kPer];
+    constexpr int kPerW = kDigits / 2 / kSortThreads;  // count words per thread
+    uint32_t v[kPerW];
     uint32_t sum = 0;
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      v[j] = s.hist[threadIdx.x * kPer + j];
-      sum += v[j];
+    for (int j = 0; j < kPerW; ++j) {
+      v[j] = s.hist[threadIdx.x * kPerW + j];
+      sum += (v[j] & 0xFFFFu) + (v[j] >> 16);
     }
     uint32_t total;
-    uint32_t ex = block_exclusive_scan(sum, s.tmp, &total);
+    uint32_t ex = block_exclusive_scan(sum, reinterpret_cast<uint32_t*>(s.kv), &total);
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      s.hist[threadIdx.x * kPer + j] = ex;
-      ex += v[j];
+    for (int j = 0; j < kPerW; ++j) {
+      const uint32_t lo16 = ex;
+      ex += v[j] & 0xFFFFu;
+      s.hist[threadIdx.x * kPerW + j] = lo16 | (ex << 16);
+      ex += v[j] >> 16;
     }
   }
   __syncthreads();
@@ -431,7 +442,7 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
   for (int r = 0; r < kItems; ++r) {
     const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
     if (q < n) {
-      dst[r] = s.hist[k[r] >> dshift] + slot[r];
+      dst[r] = h16[k[r] >> dshift] + slot[r];
       s.kv[dst[r]] = make_uint2(k[r], uint32_t(id[r]));
     }
   }
@@ -444,8 +455,8 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
     const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
     if (q < n) {
       const uint32_t d = k[r] >> dshift;
-      const uint32_t a0 = s.hist[d];
-      const uint32_t a1 = d + 1 < uint32_t(kDigits) ? s.hist[d + 1] : n;
+      const uint32_t a0 = h16[d];
+      const uint32_t a1 = d + 1 < uint32_t(kDigits) ? h16[d + 1] : n;
       uint32_t rank = 0;
       for (uint32_t v = a0; v < a1; ++v) {
         const uint2 o = s.kv[v];
