@@ -764,7 +764,9 @@ plan_btier(PlanArgs a, const int32_t* __restrict__ ranges, int8_t* __restrict__ 
 // candidate bins are appended to the worker's candidate list as in plan_write.
 // All loads a tile needs go out in two rounds: the class table, the bin
 // tiers of classes >= 1 (into LDS), the tile's list bounds and class-0 tiers,
-// then the list entries.
+// then the list entries. Cell x of the row sits at LDS byte x + sh, sh = (flat
+// index of the window's first cell) mod 16, so the row is filled a 32-bit
+// word (4 cells) at a time and written out as 16-byte stores.
 constexpr int kWriteThreads = 256;
 constexpr int kWriteWin = 8192;  // cells held in LDS at once
 #ifndef NOPFS_WRITE_ENT
@@ -775,13 +777,14 @@ constexpr int kWriteEnt = NOPFS_WRITE_ENT;  // list entries per thread loaded up
 constexpr uint32_t kBt1Max = ((kBins1Budget + 256 + 15) / 16) * 16;  // class >= 1 bins, padded
 
 template <bool kVec>
-__global__ void __launch_bounds__(kWriteThreads)
+__global__ void __launch_bounds__(kWriteThreads) __attribute__((amdgpu_waves_per_eu(8)))
 plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
              const int8_t* __restrict__ btier, int8_t* __restrict__ tier,
              CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t ntiles) {
   __shared__ __align__(16) int8_t bt1[kBt1Max];
-  __shared__ int8_t tb[kWriteWin];
+  __shared__ __align__(16) uint32_t tbw[kWriteWin / 4 + 4];  // the row's tiers, shifted by sh
   __shared__ int8_t t0[kWriteWin / (1 << kClass0Shift) + 1];
+  int8_t* tb = reinterpret_cast<int8_t*>(tbw);
   __shared__ int s_c0cand;
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
@@ -821,7 +824,7 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
     if (slot < a.cmax) ci[slot] = CandRec{key, uint32_t(k), 0u};
   };
   const int32_t* frow = first + i * a.F;
-  auto apply = [&](uint32_t v, uint32_t xoff, uint32_t wlen, int64_t w0) {
+  auto apply = [&](uint32_t v, uint32_t xoff, uint32_t wlen, int64_t w0, uint32_t sh) {
     const uint32_t x = (v & kListOffMask) - xoff;
     if (x < wlen) {
       const uint32_t b = v >> kListOffBits;
@@ -829,9 +832,9 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
       if (tv == kCandMark) {
         // the rank key needs the first read itself (few cells per worker)
         append((uint64_t(b) << 32) | uint64_t(uint32_t(frow[w0 + x])), w0 + x);
-        tb[x] = 0;
+        tb[x + sh] = 0;
       } else {
-        tb[x] = tv;
+        tb[x + sh] = tv;
       }
     }
   };
@@ -840,6 +843,7 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
     const uint32_t xoff = uint32_t(w0 - k0);
     const uint32_t zb0 = uint32_t(w0 >> kClass0Shift);
     const uint32_t nzb = uint32_t((w0 + wlen - 1) >> kClass0Shift) - zb0 + 1;
+    const uint32_t sh = kVec ? uint32_t((i * a.F + w0) & 15) : 0u;
     if (threadIdx.x == 0) s_c0cand = 0;
     int8_t zt = 0;
     if (threadIdx.x < nzb) zt = bt[a.nbin1 + zb0 + threadIdx.x];
@@ -849,38 +853,57 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
       if (zt == kCandMark) s_c0cand = 1;
     }
     __syncthreads();
-    for (uint32_t x = threadIdx.x; x < wlen; x += kWriteThreads)
-      tb[x] = t0[((w0 + x) >> kClass0Shift) - zb0];
+    {
+      // word wd holds cells 4 wd - sh .. 4 wd - sh + 3; bytes of cells
+      // outside the window are never written out
+      const uint32_t lo8 = uint32_t(w0) & ((1u << kClass0Shift) - 1);  // w0 = zb0 * 256 + lo8
+      auto zbin = [&](int32_t x) {
+        x = x < 0 ? 0 : (x >= int32_t(wlen) ? int32_t(wlen) - 1 : x);
+        return (lo8 + uint32_t(x)) >> kClass0Shift;
+      };
+      const uint32_t nw = (wlen + sh + 3) / 4;
+      for (uint32_t wd = threadIdx.x; wd < nw; wd += kWriteThreads) {
+        const int32_t xa = int32_t(4 * wd) - int32_t(sh);
+        const uint32_t za = zbin(xa), zd = zbin(xa + 3);
+        uint32_t word = uint32_t(uint8_t(t0[za])) * 0x01010101u;
+        if (za != zd)  // the word spans two class-0 bins
+          word = uint32_t(uint8_t(t0[za])) | (uint32_t(uint8_t(t0[zbin(xa + 1)])) << 8) |
+                 (uint32_t(uint8_t(t0[zbin(xa + 2)])) << 16) | (uint32_t(uint8_t(t0[zd])) << 24);
+        tbw[wd] = word;
+      }
+    }
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < kWriteEnt; ++u)
-      if (threadIdx.x + uint32_t(u) * kWriteThreads < n) apply(ev[u], xoff, wlen, w0);
+      if (threadIdx.x + uint32_t(u) * kWriteThreads < n) apply(ev[u], xoff, wlen, w0, sh);
     for (uint32_t q = threadIdx.x + kWriteEnt * kWriteThreads; q < n; q += kWriteThreads)
-      apply(ent[q], xoff, wlen, w0);
+      apply(ent[q], xoff, wlen, w0, sh);
     __syncthreads();
     if (s_c0cand) {
       // unread cells of candidate class-0 bins (read ones were overwritten)
       for (uint32_t x = threadIdx.x; x < wlen; x += kWriteThreads) {
-        if (tb[x] == kCandMark) {
+        if (tb[x + sh] == kCandMark) {
           const int64_t k = w0 + x;
           append((uint64_t(a.nbin1 + uint32_t(k >> kClass0Shift)) << 32) | uint64_t(k), k);
-          tb[x] = 0;
+          tb[x + sh] = 0;
         }
       }
       __syncthreads();
     }
+    // cells before the first 16-byte aligned cell of the output row and
+    // after the last whole group of 16 go one per thread, the rest as one
+    // 16-byte LDS read and one 16-byte store per group (x + sh is a
+    // multiple of 16 there)
     int8_t* dst = trow + w0;
-    uint32_t head = kVec ? uint32_t((4 - ((i * a.F + w0) & 3)) & 3) : wlen;
+    uint32_t head = kVec ? (16u - sh) & 15u : wlen;
     if (head > wlen) head = wlen;
-    const uint32_t nunits = (wlen - head) >> 2;
-    const uint32_t tail0 = head + 4 * nunits;
-    for (uint32_t x = threadIdx.x; x < head; x += kWriteThreads) dst[x] = tb[x];
-    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kWriteThreads) dst[x] = tb[x];
+    const uint32_t nunits = (wlen - head) >> 4;
+    const uint32_t tail0 = head + 16 * nunits;
+    for (uint32_t x = threadIdx.x; x < head; x += kWriteThreads) dst[x] = tb[x + sh];
+    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kWriteThreads) dst[x] = tb[x + sh];
     for (uint32_t u = threadIdx.x; u < nunits; u += kWriteThreads) {
-      const uint32_t x = head + 4 * u;
-      const uint32_t w = uint32_t(uint8_t(tb[x])) | (uint32_t(uint8_t(tb[x + 1])) << 8) |
-                         (uint32_t(uint8_t(tb[x + 2])) << 16) | (uint32_t(uint8_t(tb[x + 3])) << 24);
-      *reinterpret_cast<uint32_t*>(dst + x) = w;
+      const uint32_t x = head + 16 * u;
+      *reinterpret_cast<uint4*>(dst + x) = *reinterpret_cast<const uint4*>(tb + x + sh);
     }
     __syncthreads();
   }
@@ -1068,7 +1091,7 @@ int compact_plan_run(CompactPlan* cp, const CompactCells& cc, const uint8_t* cou
                    dim3(256), 0, st, a, (const int32_t*)b.ranges, cp->btier)))
     return rc;
   const uint32_t ntiles = uint32_t(s.N) * cc.nbk;
-  const bool vec = (reinterpret_cast<uintptr_t>(tier) & 3) == 0;
+  const bool vec = (reinterpret_cast<uintptr_t>(tier) & 15) == 0;  // 16-byte row stores
   if ((rc = vec ? launch("plan_write", plan_write_c<true>, dim3(xcd_padded(ntiles)),
                          dim3(kWriteThreads), 0, st, a, c, first, (const int8_t*)cp->btier, tier,
                          b.cand, b.ccount, ntiles)

@@ -197,16 +197,18 @@ def test_unaligned_outputs(oracle, name, F, E, N, B, d, seed, fr, path):
     exp = oracle.full_pipeline(oracle.make_job(F, E, N, B, d, seed), sizes, caps)
     count = _offset_view((N, F), torch.uint8)
     first = _offset_view((N, F), torch.int32)
-    assert count.data_ptr() % 4 and first.data_ptr() % 16
+    tier = _offset_view((N, F), torch.int8)
+    assert count.data_ptr() % 4 and first.data_ptr() % 16 and tier.data_ptr() % 4
     s = torch.from_numpy(sizes).cuda()
     if path == "staged":
         R = nopfs.access_streams(job)
         nopfs.access_stats(job, R, count, first)
-        tier, used = nopfs.tier_plan(job, count, first, s, caps)
+        _, used = nopfs.tier_plan(job, count, first, s, caps, tier)
         got = dict(count=count, first=first, tier=tier, used=used)
     else:
-        got = nopfs.plan_job(job, s, caps, out=dict(count=count, first=first))
+        got = nopfs.plan_job(job, s, caps, out=dict(count=count, first=first, tier=tier))
         assert got["count"].data_ptr() == count.data_ptr()
+        assert got["tier"].data_ptr() == tier.data_ptr()
     torch.cuda.synchronize()
     compare({k: v.cpu().numpy() for k, v in got.items()}, exp,
             names=("count", "first", "tier", "used"))
