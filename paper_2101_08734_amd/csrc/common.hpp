@@ -109,14 +109,18 @@ __device__ inline uint64_t lanemask_lt() {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Inclusive scan of a 32-bit value across the 64 lanes of a wave.
+// Inclusive scan of a 32-bit value across the 64 lanes of a wave (all lanes
+// active), in registers: shifts by 1, 2, 4 and 8 lanes inside each row of
+// 16 (lanes shifted in from outside the row add 0), then the last lane of
+// row 0 is added to row 1 and that of row 2 to row 3, then the last lane of
+// row 1 (the sum of rows 0 and 1) to rows 2 and 3.
 __device__ inline uint32_t wave_inclusive_scan(uint32_t v) {
-  const int lane = __lane_id();
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    uint32_t o = __shfl_up(v, d, 64);
-    if (lane >= d) v += o;
-  }
+  v += __builtin_amdgcn_update_dpp(0u, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0u, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0u, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0u, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0u, v, 0x142, 0xa, 0xf, false);  // row_bcast:15, rows 1 and 3
+  v += __builtin_amdgcn_update_dpp(0u, v, 0x143, 0xc, 0xf, false);  // row_bcast:31, rows 2 and 3
   return v;
 }
 
