@@ -206,9 +206,7 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
       for (int u = 0; u < 4; ++u) v[u] = r0 + 64 * u < runs ? v[u] : 0u;
       base += v[0] + v[1] + v[2] + v[3];
     }
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) base += __shfl_xor(base, d, 64);
-    base = __builtin_amdgcn_readfirstlane(base);
+    base = __builtin_amdgcn_readlane(wave_inclusive_scan(base), 63);
   }
   for (int64_t w0 = k0; w0 < kend; w0 += kStatsWin) {
     const uint32_t wlen = uint32_t(kend - w0 < kStatsWin ? kend - w0 : kStatsWin);
@@ -331,7 +329,7 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     uint32_t incl = 0, wbase = 0;
     if (kCompact && kVec) {
       incl = wave_inclusive_scan(nmine);
-      const uint32_t wtot = __shfl(incl, 63, 64);
+      const uint32_t wtot = __builtin_amdgcn_readlane(incl, 63);
       // a per-lane zero offset keeps the compiler from rewriting this
       // one-lane atomic into a wave reduction that waits for its result here
       uint32_t z;

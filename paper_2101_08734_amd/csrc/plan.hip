@@ -445,10 +445,10 @@ plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
       }
       if (__ballot(nc > 0)) {
         const uint32_t inc = wave_inclusive_scan(uint32_t(nc));
-        const uint32_t tot = __shfl(inc, 63, 64);
+        const uint32_t tot = __builtin_amdgcn_readlane(inc, 63);
         int32_t basev = 0;
         if (__lane_id() == 63) basev = atomicAdd(&ccount[i], int32_t(tot));
-        basev = __shfl(basev, 63, 64);
+        basev = __builtin_amdgcn_readlane(basev, 63);
         int32_t slot = basev + int32_t(inc) - nc;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -681,54 +681,64 @@ plan_hist_c(PlanArgs a, CompactArgs c, const int64_t* __restrict__ sizes, uint64
       wbase[kb - g0] = c.base[i * int64_t(c.nbk) + kb];
     }
     __syncthreads();
-    uint32_t v[kHistCU];
-    auto fetch = [&](uint32_t kb) {
-      const uint32_t n = kb < g1 ? wnum[kb - g0] : 0u;
-      const uint32_t* e = erow + (kb < g1 ? wbase[kb - g0] : 0);
-#pragma unroll
-      for (int u = 0; u < kHistCU; ++u) {
-        const uint32_t q = u * 64 + lane;
-        v[u] = q < n ? e[q] : 0u;
-      }
-    };
+    // Each wave walks its windows kb = g0 + wave, + kWaves, ... in steps of
+    // kHistCU * 64 entries, as one pipeline: a step requests its entries'
+    // sizes, then the next step's entries, and adds its bins while those are
+    // in flight. Loads are unconditional (clamped indices), so waiting for the
+    // sizes leaves the later entry loads outstanding.
+    constexpr uint32_t kStep = kHistCU * 64;
     auto add = [&](uint32_t e, uint64_t sz, int64_t kw) {
       const int64_t k = kw + (e & kListOffMask);
       atomicAdd(reinterpret_cast<unsigned long long*>(&h1[e >> kListOffBits]),
                 static_cast<unsigned long long>(sz));
       atomicAdd(&zs[uint32_t(k >> kClass0Shift) - zb0], static_cast<unsigned long long>(sz));
     };
-    fetch(g0 + wave);
-    for (uint32_t kb = g0 + wave; kb < g1; kb += kWaves) {
-      const uint32_t n = wnum[kb - g0];
-      const uint32_t* e = erow + wbase[kb - g0];
-      const int64_t kw = int64_t(kb) << c.ws;
-      uint32_t cur[kHistCU];
+    auto window = [&](uint32_t kb, uint32_t& n, const uint32_t*& e) {
+      n = kb < g1 ? wnum[kb - g0] : 0u;
+      e = erow + (kb < g1 ? wbase[kb - g0] : 0);
+    };
+    auto next_window = [&](uint32_t& kb, uint32_t& n, const uint32_t*& e) {
+      do {
+        kb += kWaves;
+        window(kb, n, e);
+      } while (kb < g1 && n == 0u);
+    };
+    auto load = [&](uint32_t (&dst)[kHistCU], const uint32_t* e, uint32_t q0, uint32_t n) {
+      const uint32_t last = n ? n - 1 : 0u;  // entry 0 of the row exists (M_max >= 1)
 #pragma unroll
-      for (int u = 0; u < kHistCU; ++u) cur[u] = v[u];
-      fetch(kb + kWaves);  // next window's first entries
+      for (int u = 0; u < kHistCU; ++u) {
+        const uint32_t q = q0 + u * 64 + lane;
+        dst[u] = e[q < last ? q : last];
+      }
+    };
+    uint32_t kb = g0 + wave, q0 = 0, n;
+    const uint32_t* e;
+    window(kb, n, e);
+    if (kb < g1 && n == 0u) next_window(kb, n, e);
+    uint32_t cur[kHistCU];
+    load(cur, e, 0, n);
+    while (kb < g1) {
+      const int64_t kw = int64_t(kb) << c.ws;
       uint64_t sz[kHistCU];
 #pragma unroll
-      for (int u = 0; u < kHistCU; ++u)
-        sz[u] = u * 64 + lane < n ? uint64_t(sizes[kw + (cur[u] & kListOffMask)]) : 0ull;
-#pragma unroll
-      for (int u = 0; u < kHistCU; ++u)
-        if (u * 64 + lane < n) add(cur[u], sz[u], kw);
-      // entries beyond the prefetched ones
-      for (uint32_t q0 = kHistCU * 64; q0 < n; q0 += kHistCU * 64) {
-        uint32_t w[kHistCU];
-#pragma unroll
-        for (int u = 0; u < kHistCU; ++u) {
-          const uint32_t q = q0 + u * 64 + lane;
-          w[u] = q < n ? e[q] : 0u;
-        }
-        uint64_t wz[kHistCU];
-#pragma unroll
-        for (int u = 0; u < kHistCU; ++u)
-          wz[u] = q0 + u * 64 + lane < n ? uint64_t(sizes[kw + (w[u] & kListOffMask)]) : 0ull;
-#pragma unroll
-        for (int u = 0; u < kHistCU; ++u)
-          if (q0 + u * 64 + lane < n) add(w[u], wz[u], kw);
+      for (int u = 0; u < kHistCU; ++u) sz[u] = uint64_t(sizes[kw + (cur[u] & kListOffMask)]);
+      uint32_t nkb = kb, nq0 = q0 + kStep, nn = n;
+      const uint32_t* ne = e;
+      if (nq0 >= n) {
+        nq0 = 0;
+        next_window(nkb, nn, ne);
       }
+      uint32_t nxt[kHistCU];
+      load(nxt, ne, nq0, nn);
+#pragma unroll
+      for (int u = 0; u < kHistCU; ++u)
+        if (q0 + u * 64 + lane < n) add(cur[u], sz[u], kw);
+#pragma unroll
+      for (int u = 0; u < kHistCU; ++u) cur[u] = nxt[u];
+      kb = nkb;
+      q0 = nq0;
+      n = nn;
+      e = ne;
     }
     __syncthreads();
   }
