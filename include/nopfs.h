@@ -18,19 +18,23 @@
  *    after the enqueued work completes.
  *  - `hip_stream` is a hipStream_t (NULL = the null stream). GPU calls only
  *    enqueue work on it and return; the caller keeps the buffers alive until
- *    the stream has completed. Internal scratch is allocated and freed in
- *    stream order on the same stream, from the device's default
- *    stream-ordered memory pool; on first use the library raises that pool's
- *    release threshold so freed scratch stays mapped for the next call (use
- *    hipDeviceGetDefaultMemPool / hipMemPoolTrimTo to give it back).
+ *    the stream has completed. Internal scratch comes from one block of
+ *    device memory per (device, stream), reused in stream order by every call
+ *    on that stream: a call that needs more than the block allocates the rest
+ *    (hipMalloc), synchronises the stream at its end and replaces the block
+ *    by one of its peak size, so later calls of that size allocate nothing.
+ *    The block is kept until the process ends (at most the largest call's
+ *    scratch per stream). Calls on one stream from several host threads run
+ *    one at a time.
  *  - Return 0 on success, a negative NOPFS_E* code otherwise. Argument errors
  *    are detected on the host before anything is enqueued. No C++ exception
  *    crosses this boundary. nopfs_last_error() gives a thread-local detail.
  *  - An array with no elements (R and next when M_max == 0) may be NULL.
  *  - Layouts are row-major; [N][F] tables are indexed i*F + k with 64-bit
  *    arithmetic (N*F may exceed 2^31).
- *  - Entry points are stateless and reentrant: several jobs (say a training
- *    and a validation job) can be planned concurrently on different streams.
+ *  - Entry points keep no state but the scratch blocks and are reentrant:
+ *    several jobs (say a training and a validation job) can be planned
+ *    concurrently on different streams.
  *  - Every result is exact integer work and deterministic: the output is a
  *    pure function of the inputs.
  *
@@ -159,8 +163,8 @@ int nopfs_tier_plan(const nopfs_job* job, const uint8_t* count,
  * there. R and next may be NULL when M_max == 0. Fewer passes over memory:
  * the counting and next-use passes share their partition of R where they
  * can, and the tier plan reads a compact list of the read cells produced by
- * the counting pass (scratch of about 8 bytes per read, freed in stream
- * order when the enqueued work ends).
+ * the counting pass (scratch of about 8 bytes per read, returned to the
+ * stream's scratch block when the call returns).
  * Errors: EINVAL, ERANGE, ENOMEM, EDEVICE, all detected before any launch
  * except ENOMEM/EDEVICE from a later stage (outputs are then unspecified). */
 int nopfs_plan_job(const nopfs_job* job, const int64_t* sizes, const int64_t* caps,

@@ -1,6 +1,7 @@
 // Host-side plumbing of the planner library: argument validation and shape
 // arithmetic, error reporting, stream-ordered scratch, per-kernel event
 // timing, and the calibration copy kernel.
+#include <map>
 #include <mutex>
 #include <new>
 #include <string>
@@ -60,49 +61,117 @@ bool take_alloc_failure() {
   return false;
 }
 
-Scratch::~Scratch() {
-  for (int i = n_ - 1; i >= 0; --i) (void)hipFreeAsync(ptrs_[i], stream_);
-}
+// Scratch of one (device, stream): one block of device memory reused by
+// every call on that stream, handed out as a stack (the Scratch objects of a
+// call nest, and a buffer's space is taken back once every buffer above it
+// is released). A call that needs more than the block gets extra blocks; at
+// its end the stream is synchronised and the block is replaced by one of the
+// call's peak size, so later calls of that size allocate nothing. Per-call
+// stream-ordered allocations of gigabytes stalled the host for hundreds of
+// milliseconds per call after ~100 calls (the allocator returned and mapped
+// memory again); the arena keeps its memory until the process ends.
+struct Arena {
+  std::recursive_mutex mu;
+  int depth = 0;            // live Scratch objects
+  char* block = nullptr;    // the reused block
+  size_t cap = 0;
+  size_t top = 0;           // bytes of the block in use
+  size_t extent = 0;        // top plus live extra blocks
+  size_t peak = 0;          // largest extent of the current call
+  bool failed = false;      // an allocation of the current call failed
+  std::vector<void*> extra; // blocks beyond `block`, freed at the call's end
+  struct Rec {
+    size_t off, bytes;
+    bool in_block, live;
+  };
+  std::vector<Rec> stack;
+};
 
-// The default stream-ordered pool returns freed memory to the system at
-// every synchronisation (release threshold 0), so the next call would map
-// its scratch again (milliseconds to hundreds of milliseconds for gigabytes,
-// with the host blocked). Once per device the threshold is raised so freed
-// scratch stays mapped for reuse.
-static void keep_pool_mapped() {
+static Arena* arena_of(hipStream_t s) {
   static std::mutex mu;
-  static bool done[64] = {};
+  static std::map<std::pair<int, hipStream_t>, Arena*> arenas;  // kept until exit
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+  if (hipGetDevice(&dev) != hipSuccess) {
     (void)hipGetLastError();
-    return;
+    return nullptr;
   }
   std::lock_guard<std::mutex> g(mu);
-  if (done[dev]) return;
-  done[dev] = true;
-  hipMemPool_t pool;
-  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-    uint64_t keep = UINT64_MAX;
-    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+  Arena*& a = arenas[{dev, s}];
+  if (!a) a = new (std::nothrow) Arena;
+  return a;
+}
+
+Scratch::Scratch(hipStream_t s) : stream_(s), arena_(arena_of(s)) {
+  if (!arena_) return;
+  arena_->mu.lock();
+  ++arena_->depth;
+}
+
+Scratch::~Scratch() {
+  Arena* a = arena_;
+  if (!a) return;
+  for (int i = 0; i < n_; ++i) a->stack[recs_[i]].live = false;
+  while (!a->stack.empty() && !a->stack.back().live) {
+    const Arena::Rec& r = a->stack.back();
+    if (r.in_block) a->top = r.off;
+    a->extent -= r.bytes;
+    a->stack.pop_back();
   }
-  (void)hipGetLastError();
+  if (--a->depth == 0) {
+    if (!a->extra.empty()) {
+      // the call outgrew the block: after its work, one block of its peak
+      // (a call that ran out of memory keeps the old block)
+      (void)hipStreamSynchronize(stream_);
+      for (void* q : a->extra) (void)hipFree(q);
+      a->extra.clear();
+      if (!a->failed) {
+        if (a->block) (void)hipFree(a->block);
+        a->block = nullptr;
+        a->cap = 0;
+        void* q = nullptr;
+        if (hipMalloc(&q, a->peak) == hipSuccess && q) {
+          a->block = static_cast<char*>(q);
+          a->cap = a->peak;
+        }
+      }
+      (void)hipGetLastError();
+    }
+    a->peak = 0;
+    a->failed = false;
+  }
+  a->mu.unlock();
 }
 
 int Scratch::alloc(void** p, size_t bytes) {
   *p = nullptr;
-  keep_pool_mapped();
   if (n_ >= 32) return fail(NOPFS_ENOMEM, "too many scratch buffers");
   if (take_alloc_failure()) return fail(NOPFS_ENOMEM, "scratch allocation failed (test hook)");
+  Arena* a = arena_;
+  if (!a) return fail(NOPFS_ENOMEM, "no device memory for scratch (no current device)");
   bytes = (bytes + 255) & ~size_t(255);
   if (bytes == 0) bytes = 256;
-  hipError_t e = hipMallocAsync(p, bytes, stream_);
-  if (e != hipSuccess || !*p) {
-    (void)hipGetLastError();
-    *p = nullptr;
-    return fail(NOPFS_ENOMEM, std::string("scratch allocation of ") +
-                                  std::to_string(bytes) + " bytes failed");
+  Arena::Rec r{0, bytes, false, true};
+  if (a->top + bytes <= a->cap) {
+    r.off = a->top;
+    r.in_block = true;
+    a->top += bytes;
+    *p = a->block + r.off;
+  } else {
+    void* q = nullptr;
+    const hipError_t e = hipMalloc(&q, bytes);
+    if (e != hipSuccess || !q) {
+      (void)hipGetLastError();
+      a->failed = true;
+      return fail(NOPFS_ENOMEM, std::string("scratch allocation of ") + std::to_string(bytes) +
+                                    " bytes failed");
+    }
+    a->extra.push_back(q);
+    *p = q;
   }
-  ptrs_[n_++] = *p;
+  a->extent += bytes;
+  if (a->extent > a->peak) a->peak = a->extent;
+  recs_[n_++] = a->stack.size();
+  a->stack.push_back(r);
   return NOPFS_OK;
 }
 

@@ -55,8 +55,13 @@ __host__ __device__ inline int64_t epoch_len(int64_t F, int64_t N, int64_t B,
 // Stream-ordered device scratch (hipMallocAsync / hipFreeAsync).
 class Scratch {
  public:
-  explicit Scratch(hipStream_t s) : stream_(s) {}
+  // Takes the scratch arena of (current device, s): calls on one stream share
+  // it and run one at a time (a Scratch holds the arena's lock while it lives;
+  // Scratch objects of one call nest).
+  explicit Scratch(hipStream_t s);
   ~Scratch();
+  Scratch(const Scratch&) = delete;
+  Scratch& operator=(const Scratch&) = delete;
   // Allocates `bytes` (rounded up to 256) and returns NOPFS_OK or ENOMEM.
   int alloc(void** p, size_t bytes);
   template <typename T>
@@ -64,7 +69,8 @@ class Scratch {
 
  private:
   hipStream_t stream_;
-  void* ptrs_[32] = {};
+  struct Arena* arena_ = nullptr;
+  size_t recs_[32] = {};  // this object's entries on the arena's stack
   int n_ = 0;
 };
 
