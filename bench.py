@@ -15,10 +15,8 @@ buffer replay (the staging capacity) under "buffer", and the simulator's
 four data-loading policies (Perfect, Naive, StagingBuffer, NoPFS) under
 "policies"; they are not part of the step.
 
-The default warm-up (100 steps, ~2.5 s at ImageNet-22k) brings the GPU to its
-steady state before the timed steps: in the first ~2 s of sustained load the
-bucket-scatter kernel runs up to ~40% slower. The later calls, timed after
-the step, warm up with at most 2 calls of their own.
+The later calls, timed after the step, warm up with at most 2 calls of their
+own.
 
 Prints ONE JSON line. Per-kernel durations come from HIP events recorded by
 the library around each of its launches, on the stream it launches on, over
@@ -408,7 +406,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--path", choices=["fused", "staged"], default="fused",
@@ -504,7 +502,7 @@ def main():
 
     schedule = model = buffer = policies = None
     if not args.no_schedule:
-        later_warmup = min(args.warmup, 2)  # the GPU is warm after the step's warm-up
+        later_warmup = min(args.warmup, 2)
         schedule = time_schedule(nopfs, torch, w, job, M, M_w, R, tier, sizes, caps, args.steps,
                                  later_warmup, stream)
         model = time_model(nopfs, torch, wl, w, job, M, M_w, R, tier, sizes, args.steps,
