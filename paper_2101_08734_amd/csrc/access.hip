@@ -474,14 +474,37 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
     s.f[idx] = int32_t(fbase + (v & kJMask));
     s.link[idx] = uint16_t(atomicExch(&s.head[x & (kNextSlots - 1)], idx));
   };
+  // With at most kNextThreads runs, read idx = threadIdx.x + q * kNextThreads
+  // is this thread's in the gather and in the output: its position in the
+  // partitioned row, found once through the run table, stays in a register,
+  // and all of the thread's reads are requested at once.
+  constexpr int kPerThread = (kNextEnt + kNextThreads - 1) / kNextThreads;
+  static_assert(kNextEnt <= int(kRunMap), "the run table maps every read of a fast-path window");
+  int32_t posq[kPerThread];
   if (runs <= kNextThreads) {
-    consume_runs(rt, int(runs), total, prow, 0u, gather);
+    uint32_t vq[kPerThread];
+    int32_t fbq[kPerThread];
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+      const uint32_t idx = threadIdx.x + q * kNextThreads;
+      posq[q] = -1;
+      fbq[q] = 0;
+      if (idx < total) {
+        const int r = rt.run_of[idx];
+        posq[q] = rt.start[r] + int32_t(idx - rt.pref[r]);
+        fbq[q] = rt.fbase[r];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) vq[q] = posq[q] >= 0 ? prow[posq[q]] : 0u;
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q)
+      if (posq[q] >= 0) gather(posq[q], fbq[q], vq[q], threadIdx.x + q * kNextThreads);
   } else {
     for_each_read(p, i, kb, OT, prow, rt, 0, p.E, gather);
   }
   __syncthreads();
   // each read: smallest later position of the same sample on its chain
-  constexpr int kPerThread = (kNextEnt + kNextThreads - 1) / kNextThreads;
   int32_t res[kPerThread];
 #pragma unroll
   for (int q = 0; q < kPerThread; ++q) {
@@ -498,16 +521,10 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
       res[q] = best == INT_MAX ? -1 : best;
     }
   }
-  if (runs <= kNextThreads && total <= kRunMap) {
-    // output position from the read's index through the run table
+  if (runs <= kNextThreads) {
 #pragma unroll
-    for (int q = 0; q < kPerThread; ++q) {
-      const uint32_t idx = threadIdx.x + q * kNextThreads;
-      if (idx < total) {
-        const int r = rt.run_of[idx];
-        nrow[rt.start[r] + (idx - rt.pref[r])] = res[q];
-      }
-    }
+    for (int q = 0; q < kPerThread; ++q)
+      if (posq[q] >= 0) nrow[posq[q]] = res[q];
   } else {
     __syncthreads();  // every chain walk is done before f is overwritten
 #pragma unroll
