@@ -161,9 +161,10 @@ constexpr int kRunLoads = 8;
 // one aligned 128-bit first-read word in LDS. Only cells after the last
 // group wrap around, so the tables take exactly kStatsWin cells (40 KB, four
 // workgroups per CU) and the workgroup uses no other LDS: each wave sums the
-// run starts itself, holds the bin records of classes below 64 one per lane
-// (looked up with a lane shuffle), and claims list slots with one atomic on
-// the tile's entry count in global memory.
+// run starts itself, and holds the bin records of classes below 64 one per
+// lane (looked up with a lane shuffle). Once every wave has read its cells
+// into registers, the waves exchange their read-cell totals through the
+// first words of the (then free) tables to place their list entries.
 constexpr int kStatsCwWords = kStatsWin / 4;  // byte counters
 constexpr uint32_t kStatsPosMask = kStatsWin - 1;
 
@@ -191,10 +192,11 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   const uint32_t nsc = uint32_t(p.nsc);
   const uint32_t lane = __lane_id();
   // kCompact: the worker's reads in earlier windows (the run starts are
-  // requested four per lane at once), and the tile's entry count zeroed
-  uint32_t base = 0, zold = 0;
+  // requested four per lane at once); unaligned rows (one list slot per
+  // cell, claimed with an atomic) start from a zeroed entry count
+  uint32_t base = 0, zold = 0, listed = 0;
   if (kCompact) {
-    if (threadIdx.x == 0) zold = atomicExch(&cnum[tile], 0u);
+    if (!kVec && threadIdx.x == 0) zold = atomicExch(&cnum[tile], 0u);
     for (int64_t r0 = lane; r0 < runs; r0 += 256) {
       uint32_t v[4];
 #pragma unroll
@@ -227,7 +229,7 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     for (uint32_t x = threadIdx.x; x < ncl; x += kStatsThreads) fi[x] = INT_MAX;
     // kCompact: the zeroing of the entry count has been performed (its old
     // value returned) before this barrier; every claim comes after it
-    if (kCompact && w0 == k0) asm volatile("" ::"v"(zold));
+    if (kCompact && !kVec && w0 == k0) asm volatile("" ::"v"(zold));
     __syncthreads();
     for (int64_t r = threadIdx.x; r < runs; r += kStatsThreads) {
       if (r != threadIdx.x) {
@@ -322,19 +324,32 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
                  ((word >> 24) != 0);
       }
     }
-    // list: each wave claims one run of slots for its read cells with a
-    // single atomic (the list's users do not depend on the order of a tile's
-    // entries), issued before the row stores so that its result does not
-    // wait for them
+    // list: the waves' read cells go in wave order, each wave's as one run
+    // (the list's users do not depend on the order of a tile's entries).
+    // The totals are exchanged through LDS with barriers that wait for LDS
+    // work only (the row stores stay in flight).
     uint32_t incl = 0, wbase = 0;
     if (kCompact && kVec) {
+      constexpr int kWaves = kStatsThreads / 64;
+      const uint32_t wave = threadIdx.x >> 6;
       incl = wave_inclusive_scan(nmine);
       const uint32_t wtot = __builtin_amdgcn_readlane(incl, 63);
-      // a per-lane zero offset keeps the compiler from rewriting this
-      // one-lane atomic into a wave reduction that waits for its result here
-      uint32_t z;
-      asm volatile("v_mov_b32 %0, 0" : "=v"(z));
-      if (lane == 0 && wtot) wbase = atomicAdd(cnum + tile + z, wtot);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");  // tables read
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      if (lane == 0) sm[wave] = wtot;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      uint32_t before = 0, all = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const uint32_t t = sm[w];
+        before += uint32_t(w) < wave ? t : 0u;
+        all += t;
+      }
+      wbase = listed + before;
+      listed += all;
     }
     if (kVec) {
       if (threadIdx.x < head) {
@@ -357,7 +372,7 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     }
     if (kCompact && kVec) {
       uint32_t* cdst = cent + i * p.M_max + base;
-      uint32_t slot = __builtin_amdgcn_readlane(wbase, 0) + incl - nmine;
+      uint32_t slot = wbase + incl - nmine;
       auto emit = [&](auto bin) {
         const uint32_t b1 = bin(c1, f1), b2 = bin(c2, f2);
         if (c1) cdst[slot++] = (b1 << kListOffBits) | (xoff + threadIdx.x);
@@ -385,7 +400,10 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     }
     if (w0 + kStatsWin < kend) __syncthreads();  // the tables are reused
   }
-  if (kCompact && threadIdx.x == 0) cbase[tile] = int32_t(base);
+  if (kCompact && threadIdx.x == 0) {
+    cbase[tile] = int32_t(base);
+    if (kVec) cnum[tile] = listed;
+  }
 }
 
 // -- next ---------------------------------------------------------------------
