@@ -464,8 +464,9 @@ plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
 
 // -- exact resolution of the candidates --------------------------------------------------
 struct ResolveSmem {
-  uint64_t key[kCandMax];
+  uint64_t key[kCandMax];  // rank keys; after the sort, the bytes of the whole bins before each
   uint32_t k[kCandMax];
+  uint64_t sz[kCandMax];   // each candidate's size
 };
 
 __global__ void __launch_bounds__(kResolveThreads)
@@ -508,21 +509,40 @@ plan_resolve(PlanArgs a, const uint64_t* __restrict__ H, const CandRec* __restri
       __syncthreads();
     }
   }
+  // every thread gathers, for its candidates in sorted order, the size and
+  // the bytes of the whole bins between the previous candidate's bin and
+  // this one's (zero within a bin), so the serial fill below reads LDS only
+  constexpr int kPerT = kCandMax / kResolveThreads;
+  static_assert(kCandMax % kResolveThreads == 0, "candidates per thread");
+  const int64_t last_bin = n > 0 ? int64_t(s.key[n - 1] >> 32) : -1;
+  uint64_t gap[kPerT];
+#pragma unroll
+  for (int q = 0; q < kPerT; ++q) {
+    const int32_t x = int32_t(threadIdx.x) + q * kResolveThreads;
+    gap[q] = 0;
+    if (x < n) {
+      const int64_t b = int64_t(s.key[x] >> 32);
+      const int64_t pb = x > 0 ? int64_t(s.key[x - 1] >> 32) : -1;
+      if (b != pb) gap[q] = Hi[b] - (pb < 0 ? 0ull : Hi[pb + 1]);
+      s.sz[x] = uint64_t(sizes[s.k[x]]);
+    }
+  }
+  __syncthreads();  // every key is read before any is replaced
+#pragma unroll
+  for (int q = 0; q < kPerT; ++q) {
+    const int32_t x = int32_t(threadIdx.x) + q * kResolveThreads;
+    if (x < n) s.key[x] = gap[q];
+  }
+  __syncthreads();
   if (threadIdx.x != 0) return;
   // replay the greedy fill: definite bins between candidates are added whole
   int64_t* ui = used + i * a.J;
   int8_t* trow = tier + i * a.F;
   int j = 0;
   uint64_t u = 0;
-  int64_t last_bin = -1;
   for (int32_t x = 0; x < n; ++x) {
-    const int64_t b = int64_t(s.key[x] >> 32);
-    if (b != last_bin) {
-      const uint64_t gap_start = last_bin < 0 ? 0ull : Hi[last_bin + 1];
-      u += Hi[b] - gap_start;
-      last_bin = b;
-    }
-    const uint64_t sz = uint64_t(sizes[s.k[x]]);
+    u += s.key[x];
+    const uint64_t sz = s.sz[x];
     while (j < a.J && u + sz > uint64_t(a.caps[j])) {
       ui[j] = int64_t(u);
       ++j;
