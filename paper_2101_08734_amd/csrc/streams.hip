@@ -499,13 +499,21 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
     // row; t < 2^13, so the float reciprocal gives t / nj up to one step
     const uint32_t total = nj * N;
     const float inv_nj = 1.0f / float(nj);
-    for (uint32_t t = threadIdx.x; t < total; t += kSortThreads) {
-      uint32_t i = uint32_t(float(t) * inv_nj);
-      if (i * nj > t) --i;
-      else if ((i + 1) * nj <= t) ++i;
-      const uint32_t jj = t - i * nj;
-      const uint32_t pp = (j0 + jj) * N + i;
-      if (pp >= lo && pp < pend) R[row_offset(p, i, e) + j0 + jj] = int32_t(stage[jj * Np + i]);
+    auto write = [&](auto row) {
+      for (uint32_t t = threadIdx.x; t < total; t += kSortThreads) {
+        uint32_t i = uint32_t(float(t) * inv_nj);
+        if (i * nj > t) --i;
+        else if ((i + 1) * nj <= t) ++i;
+        const uint32_t jj = t - i * nj;
+        const uint32_t pp = (j0 + jj) * N + i;
+        if (pp >= lo && pp < pend) row(i)[jj] = int32_t(stage[jj * Np + i]);
+      }
+    };
+    if (p.drop_last) {  // every row holds L reads per epoch: one offset for all rows
+      int32_t* const Re = R + (e - p.e_first) * p.L + j0;
+      write([&](uint32_t i) { return Re + int64_t(i) * p.M_max; });
+    } else {
+      write([&](uint32_t i) { return R + row_offset(p, i, e) + j0; });
     }
   } else {
     for (uint32_t q = threadIdx.x; lo + q < pend; q += kSortThreads) {
