@@ -1,0 +1,95 @@
+"""The per-stream scratch block behind every call (include/nopfs.h, conventions).
+
+A call that needs more scratch than its stream's block grows the block at its
+end; later calls reuse it. Results must not depend on which calls came before
+(sizes of the block, reuse of memory written by earlier calls) nor on the
+stream: each job here is checked against its own first result and, for the
+small one, against the oracle.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from paper_2101_08734_amd import nopfs  # noqa: E402
+from paper_2101_08734_amd import workloads as wl  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    nopfs.lib()
+    yield
+
+
+SMALL = (20_000, 4, 4, 16, 1, 31)
+LARGE = (1_500_000, 6, 16, 32, 0, 32)
+
+
+def _run(shape, stream=None):
+    F = shape[0]
+    job = nopfs.Job(*shape)
+    sizes = torch.from_numpy(wl.random_sizes(F, shape[-1], 1_000, 2_000_000)).cuda()
+    tot = int(sizes.sum())
+    caps = [tot // 50, tot // 5]
+    torch.cuda.synchronize()  # the inputs are in place before another stream reads them
+    if stream is None:
+        out = nopfs.plan_job(job, sizes, caps)
+    else:
+        with torch.cuda.stream(stream):
+            out = nopfs.plan_job(job, sizes, caps, stream=stream)
+    return out
+
+
+def _host(out):
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy() for k, v in out.items()}
+
+
+def _same(a, b):
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_alternating_sizes_reuse_the_block(oracle):
+    small0 = _host(_run(SMALL))
+    large0 = _host(_run(LARGE))       # grows the block
+    small1 = _host(_run(SMALL))       # runs inside the larger block
+    large1 = _host(_run(LARGE))       # reuses it
+    _same(small0, small1)
+    _same(large0, large1)
+    F, E, N, B, d, seed = SMALL
+    sizes = wl.random_sizes(F, seed, 1_000, 2_000_000)
+    tot = int(sizes.sum())
+    exp = oracle.full_pipeline(oracle.make_job(F, E, N, B, d, seed), sizes,
+                               np.array([tot // 50, tot // 5], np.int64))
+    for k in ("R", "count", "first", "next", "tier", "used"):
+        assert np.array_equal(small1[k], exp[k]), k
+
+
+def test_two_streams_have_their_own_blocks():
+    want_small = _host(_run(SMALL))
+    want_large = _host(_run(LARGE))
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    a = _run(LARGE, s1)
+    b = _run(SMALL, s2)
+    got_large, got_small = _host(a), _host(b)
+    _same(want_large, got_large)
+    _same(want_small, got_small)
+
+
+def test_repeated_calls_allocate_nothing_more():
+    _host(_run(LARGE))
+    free0, _ = torch.cuda.mem_get_info()
+    job = nopfs.Job(*LARGE)
+    sizes = torch.from_numpy(wl.random_sizes(LARGE[0], LARGE[-1], 1_000, 2_000_000)).cuda()
+    out = nopfs.plan_job(job, sizes, [10**9, 10**10])
+    for _ in range(20):
+        nopfs.plan_job(job, sizes, [10**9, 10**10], out)
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    # the outputs of the first call above are the only new memory
+    out_bytes = sum(v.numel() * v.element_size() for v in out.values())
+    assert free0 - free1 <= out_bytes + (64 << 20)
