@@ -202,6 +202,27 @@ int nopfs_ref_streams_from_perms(const nopfs_ref_job* job, const int32_t* perms,
   return 0;
 }
 
+/* Rows [i0, i1) of the same streams, walked row by row: worker i's j-th read
+ * of epoch e is global position j*N + i, for each of its L_i reads per epoch
+ * (positions past the issued prefix belong to no worker's L_i reads). R
+ * points at row i0; rows are padded with -1 like the full streams. */
+int nopfs_ref_streams_rows(const nopfs_ref_job* job, const int32_t* perms, int64_t i0,
+                           int64_t i1, int32_t* R) {
+  int64_t M_max;
+  int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);
+  if (rc) return rc;
+  if (!perms || !R || i0 < 0 || i1 > job->N || i0 > i1) return REF_EINVAL;
+  int64_t N = job->N, F = job->F;
+  for (int64_t i = i0; i < i1; ++i) {
+    int32_t* row = R + (i - i0) * M_max;
+    int64_t L = epoch_len(job, i);
+    for (int32_t e = 0; e < job->E; ++e)
+      for (int64_t j = 0; j < L; ++j) row[(int64_t)e * L + j] = perms[(int64_t)e * F + j * N + i];
+    for (int64_t f = (int64_t)job->E * L; f < M_max; ++f) row[f] = -1;
+  }
+  return 0;
+}
+
 int nopfs_ref_access_streams(const nopfs_ref_job* job, int32_t* R) {
   int64_t M_max;
   int rc = nopfs_ref_stream_shape(job, NULL, &M_max, NULL);

@@ -48,6 +48,11 @@ int nopfs_ref_epoch_perm(const nopfs_ref_job* job, int32_t e, int32_t* perm);
 int nopfs_ref_streams_from_perms(const nopfs_ref_job* job, const int32_t* perms,
                                  int32_t* R);
 
+/* Rows [i0, i1) of the streams sharded from perms[E][F]; R points at row
+ * i0 and holds i1 - i0 rows of M_max entries. */
+int nopfs_ref_streams_rows(const nopfs_ref_job* job, const int32_t* perms, int64_t i0,
+                           int64_t i1, int32_t* R);
+
 /* Every worker's access stream R[N][M_max] (rows padded with -1). */
 int nopfs_ref_access_streams(const nopfs_ref_job* job, int32_t* R);
 

@@ -76,6 +76,7 @@ def lib():
         L.nopfs_ref_epoch_keys.argtypes = [jp, ctypes.c_int32, P]
         L.nopfs_ref_epoch_perm.argtypes = [jp, ctypes.c_int32, P]
         L.nopfs_ref_streams_from_perms.argtypes = [jp, P, P]
+        L.nopfs_ref_streams_rows.argtypes = [jp, P, ctypes.c_int64, ctypes.c_int64, P]
         L.nopfs_ref_access_streams.argtypes = [jp, P]
         L.nopfs_ref_access_stats.argtypes = [jp, P, P, P]
         L.nopfs_ref_reuse_next.argtypes = [jp, P, P]
@@ -95,7 +96,7 @@ def lib():
                                                 ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
                                                 P, P, P]
         for name in ("nopfs_ref_stream_shape", "nopfs_ref_epoch_keys",
-                     "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms",
+                     "nopfs_ref_epoch_perm", "nopfs_ref_streams_from_perms", "nopfs_ref_streams_rows",
                      "nopfs_ref_access_streams", "nopfs_ref_access_stats",
                      "nopfs_ref_reuse_next", "nopfs_ref_tier_plan",
                      "nopfs_ref_sample_columns", "nopfs_ref_access_stats_rows",
@@ -160,6 +161,17 @@ def streams_from_perms(job: RefJob, perms: np.ndarray) -> np.ndarray:
     R = np.empty((job.N, Mmax), np.int32)
     _check(lib().nopfs_ref_streams_from_perms(ctypes.byref(job), _ptr(perms),
                                               _ptr(R)), "streams_from_perms")
+    return R
+
+
+def streams_rows(job: RefJob, perms: np.ndarray, i0: int, i1: int) -> np.ndarray:
+    """Rows [i0, i1) of streams_from_perms(job, perms), sharded row by row."""
+    _, Mmax, _ = stream_shape(job)
+    perms = np.ascontiguousarray(perms, dtype=np.int32)
+    assert perms.shape == (job.E, job.F)
+    R = np.empty((i1 - i0, Mmax), np.int32)
+    _check(lib().nopfs_ref_streams_rows(ctypes.byref(job), _ptr(perms), int(i0), int(i1),
+                                        _ptr(R)), "streams_rows")
     return R
 
 
