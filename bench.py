@@ -45,34 +45,38 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 DEFAULT_WORKLOAD = "imagenet22k"
 
 
-def algorithmic_bytes(job, M_w, D, fused):
-    """Bytes each kernel must move given the C ABI's dense layouts, per
-    launch: A reads, N*F cells, D distinct (worker, sample) cells read. In the
-    fused call the counting pass also lists the D read cells (4 B each: the
-    cell's bin and offset) and the tier plan reads that list instead of the
-    dense count/first tables."""
+# The planning path's stages and the kernels each one launches (library
+# launch names). The counting and next-use passes share one partition of R in
+# the fused call; its kernels are counted with the counting stage.
+STAGES = {
+    "streams": ("stream_count", "stream_offsets", "stream_scan", "stream_scatter", "stream_split",
+                "stream_sort", "stream_pad"),
+    "stats": ("seg_partition", "offsets_transpose", "stats_tile", "fill_stats_empty"),
+    "next": ("next_tile", "next_unpartition", "pad_rows"),
+    "plan": ("plan_classes", "plan_binsum", "plan_hist", "plan_cut", "plan_btier", "plan_write",
+             "plan_resolve", "plan_exact", "fill_u64", "fill_i32"),
+}
+
+
+def stage_bytes(job, M_w):
+    """Algorithmic bytes of each stage per step, as the measurement section
+    of the survey defines them for the C ABI's dense layouts (A reads, N*F
+    cells): streams write R (4A; the key/id exchange allowance 16*E*F is
+    reported beside it), stats read R and write count + first (4A + 5NF),
+    next reads R and writes next (8A), the plan reads count, first and sizes
+    and writes tier (6NF + 8F)."""
     A = int(sum(M_w))
     NF = job.N * job.F
-    out = {
-        # streams: write R (4 B per read)
-        "stream_sort": 4 * A,
-        # stats: read R (partitioned), write count (1 B) and first (4 B) per cell
-        "stats_tile": 4 * A + 5 * NF + (4 * D if fused else 0),
-        # next: read R, write next
-        "next_unpartition": 8 * A,
-        "seg_partition": 8 * A,
-        "next_tile": 8 * A,
-        "stream_scatter": 8 * job.E * job.F,
-    }
-    if fused:
-        # list entry and the size of each read cell; tier bytes for every cell
-        out["plan_hist"] = 12 * D
-        out["plan_write"] = 4 * D + NF
-    else:
-        # read count and first (and sizes), write tier
-        out["plan_hist"] = 5 * NF + 8 * job.F
-        out["plan_write"] = 5 * NF + NF
-    return out, A
+    return {"streams": 4 * A, "stats": 4 * A + 5 * NF, "next": 8 * A,
+            "plan": 6 * NF + 8 * job.F}, A, 16 * job.E * job.F
+
+
+def kernel_bytes(job, M_w):
+    """Algorithmic bytes per launch of the kernel that carries each stage's
+    output: the stage's bytes (stage_bytes) attributed to its final kernel."""
+    sb, A, _ = stage_bytes(job, M_w)
+    return {"stream_sort": sb["streams"], "stats_tile": sb["stats"],
+            "next_unpartition": sb["next"], "plan_write": sb["plan"]}
 
 
 def schedule_algorithmic_bytes(job, M, M_w):
@@ -146,11 +150,27 @@ def _kernel_short_name(full):
     return name
 
 
+# rocprofv3 counter passes of the profile summary (one run each; every pass
+# stays within the per-block counter limits of one run).
+PMC_PASSES = {
+    "rd": ["TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum", "TCC_EA0_RDREQ_128B_sum",
+           "TCC_EA0_RDREQ_sum"],
+    "wr": ["TCC_EA0_WRREQ_sum", "TCC_EA0_WRREQ_64B_sum"],
+    "sq": ["VALUBusy", "LDSBankConflict", "OccupancyPercent", "LdsUtil", "SQ_INSTS_VALU",
+           "SQ_INSTS_LDS", "SQ_WAVES"],
+}
+
+
 def rocprof_summary(d, workload):
-    """Summarises rocprofv3 output under d (kt/ kernel trace with --stats,
-    fetch/ and write/ counter runs of FETCH_SIZE and WRITE_SIZE), all made by
-    this script's benchmark command. Counters are scaled by what they read
-    for the calibration copy (1 GiB read + 1 GiB written). Prints a Markdown
+    """Summarises rocprofv3 output under d: kt/ (kernel trace with --stats),
+    rd/ and wr/ (L2-to-memory read and write requests by size), sq/ (VALU
+    busy, LDS bank conflicts, LDS utilisation, occupancy, instruction and
+    wave counts), all made by this script's benchmark command.
+
+    Read bytes are counted per request size, 32 x (32 B requests) + 64 x
+    (64 B) + 128 x (128 B); write bytes 32 x (32 B) + 64 x (64 B). Each is
+    then scaled by what the same sum reads for the calibration copy (1 GiB
+    read + 1 GiB written), and the factors are printed. Prints a Markdown
     report ending with one JSON line that the benchmark reads back."""
     import collections
     import csv
@@ -160,74 +180,130 @@ def rocprof_summary(d, workload):
             stats[_kernel_short_name(r["Name"])] = (int(r["Calls"]), float(r["AverageNs"]) / 1e6,
                                                     float(r["Percentage"]))
     ctr = collections.defaultdict(lambda: collections.defaultdict(list))
-    for sub in ("fetch", "write"):
+    for sub in PMC_PASSES:
         for path in glob.glob(os.path.join(d, sub, "*counter_collection.csv")):
             for r in csv.DictReader(open(path)):
                 ctr[_kernel_short_name(r["Kernel_Name"])][r["Counter_Name"]].append(
                     float(r["Counter_Value"]))
+
+    def mean(c, name):
+        v = c.get(name)
+        return sum(v) / len(v) if v else None
+
+    def raw_read(c):
+        n32, n64, n128, n = (mean(c, k) for k in PMC_PASSES["rd"])
+        if None in (n32, n64, n128, n):
+            return None, None
+        return 32 * n32 + 64 * n64 + 128 * n128, n - n32 - n64 - n128
+
+    def raw_write(c):
+        n, n64 = (mean(c, k) for k in PMC_PASSES["wr"])
+        if None in (n, n64):
+            return None
+        return 32 * (n - n64) + 64 * n64
+
     cal = ctr.get("calibration_copy_kernel", {})
-    gib_kib = float(1 << 20)
-    ff = gib_kib / (sum(cal["FETCH_SIZE"]) / len(cal["FETCH_SIZE"])) if cal.get("FETCH_SIZE") else None
-    wf = gib_kib / (sum(cal["WRITE_SIZE"]) / len(cal["WRITE_SIZE"])) if cal.get("WRITE_SIZE") else None
+    cr, _ = raw_read(cal)
+    cw = raw_write(cal)
+    gib = float(1 << 30)
+    rf = gib / cr if cr else None
+    wf = gib / cw if cw else None
     out = {"source_hash": kernel_source_hash(), "workload": workload,
-           "fetch_factor": ff, "write_factor": wf, "kernels": {}}
-    lines = [f"| kernel | calls | avg ms | % time | HBM read GB/launch | HBM write GB/launch | GB/s |",
-             "|---|---|---|---|---|---|---|"]
+           "read_factor": rf, "write_factor": wf, "kernels": {}}
+    lines = ["| kernel | calls | avg ms | % time | HBM read GB/launch | HBM write GB/launch | GB/s "
+             "| VALU busy % | LDS bank conflict % | LDS util % | occupancy % | VALU inst/wave "
+             "| LDS inst/wave |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    fmt = lambda v, f: "" if v is None else format(v, f)  # noqa: E731
     for k, (calls, avg_ms, pct) in sorted(stats.items(), key=lambda x: -x[1][2]):
         c = ctr.get(k, {})
-        rd = wr = None
-        if c.get("FETCH_SIZE") and ff:
-            rd = sum(c["FETCH_SIZE"]) / len(c["FETCH_SIZE"]) * 1024 * ff
-        if c.get("WRITE_SIZE") and wf:
-            wr = sum(c["WRITE_SIZE"]) / len(c["WRITE_SIZE"]) * 1024 * wf
+        r, other = raw_read(c)
+        wr = raw_write(c)
+        rd = r * rf if r is not None and rf else None
+        wr = wr * wf if wr is not None and wf else None
         tot = (rd or 0) + (wr or 0)
+        waves = mean(c, "SQ_WAVES")
+        sq = {"valu_busy_pct": mean(c, "VALUBusy"), "lds_bank_conflict_pct": mean(c, "LDSBankConflict"),
+              "lds_util_pct": mean(c, "LdsUtil"), "occupancy_pct": mean(c, "OccupancyPercent"),
+              "valu_insts_per_wave": (mean(c, "SQ_INSTS_VALU") / waves) if waves else None,
+              "lds_insts_per_wave": (mean(c, "SQ_INSTS_LDS") / waves) if waves else None,
+              "waves": waves}
         out["kernels"][k] = {"calls": calls, "avg_ms": round(avg_ms, 5),
                              "hbm_read_bytes_per_launch": rd, "hbm_write_bytes_per_launch": wr,
-                             "hbm_bytes_per_launch": tot if rd is not None and wr is not None else None}
+                             "hbm_bytes_per_launch": tot if rd is not None and wr is not None else None,
+                             "read_requests_of_other_sizes": other, **sq}
         gbs = f"{tot / (avg_ms * 1e-3) / 1e9:.0f}" if avg_ms > 0 and tot else ""
-        lines.append(f"| {k} | {calls} | {avg_ms:.4f} | {pct:.2f} | "
-                     f"{'' if rd is None else f'{rd / 1e9:.3f}'} | "
-                     f"{'' if wr is None else f'{wr / 1e9:.3f}'} | {gbs} |")
+        lines.append(f"| {k} | {calls} | {avg_ms:.4f} | {pct:.2f} | {fmt(rd and rd / 1e9, '.3f')} | "
+                     f"{fmt(wr and wr / 1e9, '.3f')} | {gbs} | {fmt(sq['valu_busy_pct'], '.1f')} | "
+                     f"{fmt(sq['lds_bank_conflict_pct'], '.2f')} | {fmt(sq['lds_util_pct'], '.1f')} | "
+                     f"{fmt(sq['occupancy_pct'], '.1f')} | {fmt(sq['valu_insts_per_wave'], '.0f')} | "
+                     f"{fmt(sq['lds_insts_per_wave'], '.0f')} |")
     print("\n".join(lines))
     print()
-    print(f"Counter scaling from the calibration copy: FETCH_SIZE x {ff}, WRITE_SIZE x {wf}.")
+    print(f"Counter scaling from the calibration copy (1 GiB read, 1 GiB written): read bytes x {rf}, "
+          f"write bytes x {wf}.")
     print()
     print(json.dumps(out))
 
 
+def cpu_model():
+    """The host CPU's model name (the first "model name" of /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(w, sizes, caps, epochs=2, workers=2):
-    """The oracle on a bounded sample of the same workload: `epochs` of the E
-    epochs sorted and sharded for all workers, and stats, next use and plan
-    for `workers` of the N workers on those streams; each stage's time is
-    scaled linearly to the full job (streams by E/epochs, per-worker stages
-    by N/workers)."""
+    """The oracle, single-threaded, on a bounded sample of the same workload:
+     - `epochs` of the E epochs generated, sorted and sharded for all N
+       workers, scaled by E/epochs;
+     - for `workers` of the N workers, rows of the full length (E epochs: the
+       sampled epochs' streams repeated, so each row has the full job's reads
+       and the same access pattern), counted, linked (next use) and planned,
+       scaled by N/workers."""
     import numpy as np
     from oracle import ref
     ref.build()
     job = ref.make_job(w.F, epochs, w.N, w.B, w.drop_last, w.seed)
     full = ref.make_job(*w.job_tuple())
-    _, _, Mw = ref.stream_shape(full)
+    _, M_full, Mw = ref.stream_shape(full)
+    _, _, Mw_s = ref.stream_shape(job)
     A = int(Mw.sum())
     t0 = time.perf_counter()
     R = ref.access_streams(job)
     t1 = time.perf_counter()
-    count, first = ref.access_stats_rows(job, R[:workers], 0)
+    rows = np.full((workers, M_full), -1, np.int32)
+    for i in range(workers):
+        L = int(Mw_s[i]) // epochs
+        for e in range(w.E):
+            rows[i, e * L:(e + 1) * L] = R[i, (e % epochs) * L:(e % epochs + 1) * L]
+    del R
     t2 = time.perf_counter()
-    ref.reuse_next_rows(job, R[:workers], 0)
+    count, first = ref.access_stats_rows(full, rows, 0)
     t3 = time.perf_counter()
-    ref.tier_plan(full, count, first, sizes, np.asarray(caps, np.int64))
+    ref.reuse_next_rows(full, rows, 0)
     t4 = time.perf_counter()
-    est = (t1 - t0) * (w.E / epochs) + (t4 - t1) * (w.N / workers)
+    ref.tier_plan(full, count, first, sizes, np.asarray(caps, np.int64))
+    t5 = time.perf_counter()
+    scale_e, scale_n = w.E / epochs, w.N / workers
+    est = (t1 - t0) * scale_e + (t5 - t2) * scale_n
     return {
         "value": A / est,
         "unit": "accesses/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": (f"{w.name}: {epochs} of {w.E} epochs sorted+sharded for all {w.N} workers "
-                   f"({t1 - t0:.1f}s), stats {t2 - t1:.2f}s + next {t3 - t2:.2f}s + plan "
-                   f"{t4 - t3:.1f}s for {workers} of {w.N} workers; scaled x{w.E // epochs} "
-                   f"(streams) and x{w.N // workers} (per-worker stages) to {est:.0f}s for the "
-                   f"full job; single-threaded, {os.cpu_count()} host cores present"),
+        "cpu": cpu_model(),
+        "sample": (f"{w.name}: streams of {epochs} of {w.E} epochs generated, sorted and sharded "
+                   f"for all {w.N} workers ({t1 - t0:.1f}s, x{scale_e:g}); for {workers} of "
+                   f"{w.N} workers, full-length rows ({w.E} epochs, the sampled epochs' streams "
+                   f"repeated): stats {t3 - t2:.2f}s + next {t4 - t3:.2f}s + plan {t5 - t4:.1f}s "
+                   f"(x{scale_n:g}); {est:.0f}s estimated for the full job; single-threaded "
+                   f"(1 of {os.cpu_count()} host cores), {cpu_model()}"),
     }
 
 
@@ -402,6 +478,122 @@ def time_policies(nopfs, torch, wl, w, job, M, M_w, R, tier, sizes, steps, warmu
     return out
 
 
+def copy_ceiling(nopfs, torch, nbytes, stream, calls=10):
+    """A plain device copy of nbytes (read nbytes, write nbytes) with the
+    library's calibration kernel, timed with HIP events on `stream`: the
+    measured HBM ceiling of a streaming kernel on this part. The same kernel
+    calibrates the byte counters of the rocprofv3 runs."""
+    dev = torch.device("cuda:0")
+    a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        nopfs.calibration_copy(a, b, nbytes, stream=stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(calls):
+        nopfs.calibration_copy(a, b, nbytes, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / calls
+    del a, b
+    gbs = 2 * nbytes / (ms * 1e-3) / 1e9
+    return {"bytes_read": nbytes, "bytes_written": nbytes, "ms": round(ms, 4),
+            "GBps": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def measure(nopfs, torch, wl, w, path, steps, warmup, stream, keep=False):
+    """One workload: `warmup` untimed steps, then `steps` timed steps of the
+    whole planning path (fused: one nopfs_plan_job call; staged: the four
+    stage calls), device time from HIP events on `stream`, per-kernel times
+    from the library's own events. Returns the result dict (and the outputs
+    when keep)."""
+    job = nopfs.Job(*w.job_tuple())
+    T, M, M_w = nopfs.stream_shape(job)
+    caps = [int(c) for c in wl.caps(w)]
+    dev = torch.device("cuda:0")
+    sizes = torch.from_numpy(wl.sizes(w)).to(dev)
+    out = dict(R=torch.empty((job.N, M), dtype=torch.int32, device=dev),
+               count=torch.empty((job.N, job.F), dtype=torch.uint8, device=dev),
+               first=torch.empty((job.N, job.F), dtype=torch.int32, device=dev),
+               next=torch.empty((job.N, M), dtype=torch.int32, device=dev),
+               tier=torch.empty((job.N, job.F), dtype=torch.int8, device=dev),
+               used=torch.empty((job.N, len(caps)), dtype=torch.int64, device=dev))
+
+    def step():
+        if path == "fused":
+            nopfs.plan_job(job, sizes, caps, out, stream=stream)
+            return
+        nopfs.access_streams(job, out["R"], stream=stream)
+        nopfs.access_stats(job, out["R"], out["count"], out["first"], stream=stream)
+        nopfs.reuse_next(job, out["R"], out["next"], stream=stream)
+        nopfs.tier_plan(job, out["count"], out["first"], sizes, caps, out["tier"], out["used"],
+                        stream=stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    nopfs.profile_enable(True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    nopfs.profile_enable(False)
+    kernels = nopfs.profile_results()
+    ms_per_step = ev0.elapsed_time(ev1) / steps
+    print(f"[bench] {w.name} ({path}): {steps} steps, {ms_per_step:.3f} ms/step "
+          f"(wall {wall:.2f}s)", file=sys.stderr, flush=True)
+
+    sb, A, exch = stage_bytes(job, M_w)
+    kb = kernel_bytes(job, M_w)
+    per_kernel = {k: {"launches_per_step": n / steps, "ms_per_step": ms / steps, "avg_ms": ms / n}
+                  for k, (n, ms) in kernels.items()}
+    for k, v in per_kernel.items():
+        if k in kb:
+            v["alg_GBps"] = round(kb[k] / (v["avg_ms"] * 1e-3) / 1e9, 1)
+    stages = {}
+    for st, names in STAGES.items():
+        ms = sum(per_kernel[k]["ms_per_step"] for k in names if k in per_kernel)
+        gbs = sb[st] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+        stages[st] = {"ms_per_step": round(ms, 4), "alg_bytes": sb[st], "alg_GBps": round(gbs, 1),
+                      "frac": round(gbs / HBM_PEAK_GBS, 4),
+                      "kernels": [k for k in names if k in per_kernel]}
+        if st == "streams" and ms > 0:
+            b = sb[st] + exch
+            stages[st]["alg_bytes_with_exchange"] = b
+            stages[st]["frac_with_exchange"] = round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+    dominant = max(per_kernel, key=lambda k: per_kernel[k]["ms_per_step"])
+    roofline = None
+    if dominant in kb:
+        roofline = roofline_of(w.name, dominant, kb[dominant], per_kernel[dominant]["avg_ms"])
+    res = {
+        "value": A / (ms_per_step * 1e-3),
+        "unit": "accesses/s",
+        "ms_per_step": round(ms_per_step, 4),
+        "config": {"workload": w.name, "path": path, "F": w.F, "E": w.E, "N": w.N, "B": w.B,
+                   "drop_last": w.drop_last, "seed": w.seed, "accesses": A,
+                   "tier_caps_bytes": caps},
+        "roofline": roofline,
+        "stages": stages,
+        "kernels": {k: {kk: round(vv, 4) for kk, vv in v.items()} for k, v in per_kernel.items()},
+    }
+    if path == "fused":
+        # the read-cell list the counting pass writes for the tier plan (4 B
+        # per distinct (worker, sample) cell read): the implementation's own
+        # scratch traffic, reported beside the stage bytes, not in them
+        D = int((out["count"] != 0).sum())
+        res["read_cells"] = D
+        res["read_cell_list_bytes"] = 4 * D
+    if keep:
+        return res, job, M, M_w, sizes, caps, out
+    del out, sizes
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -413,8 +605,10 @@ def main():
                     help="fused: one nopfs_plan_job call per step; staged: the four stage calls")
     ap.add_argument("--no-schedule", action="store_true",
                     help="skip timing the schedule, model, buffer and policy calls")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other full-size workloads (reported under \"configs\")")
     ap.add_argument("--calibrate-bytes", type=int, default=1 << 30,
-                    help="size of the calibration copy run after the timed steps")
+                    help="bytes read (and written) by the copy-ceiling / calibration kernel")
     ap.add_argument("--rocprof-summary", metavar="DIR",
                     help="summarise rocprofv3 output of this benchmark (no GPU needed)")
     args = ap.parse_args()
@@ -430,75 +624,18 @@ def main():
     from paper_2101_08734_amd import nopfs
     from paper_2101_08734_amd import workloads as wl
 
-    w = wl.WORKLOADS[args.workload]
-    job = nopfs.Job(*w.job_tuple())
-    T, M, M_w = nopfs.stream_shape(job)
-    sizes_h = wl.sizes(w)
-    caps = [int(c) for c in wl.caps(w)]
-    dev = torch.device("cuda:0")
-    sizes = torch.from_numpy(sizes_h).to(dev)
-    R = torch.empty((job.N, M), dtype=torch.int32, device=dev)
-    count = torch.empty((job.N, job.F), dtype=torch.uint8, device=dev)
-    first = torch.empty((job.N, job.F), dtype=torch.int32, device=dev)
-    nxt = torch.empty((job.N, M), dtype=torch.int32, device=dev)
-    tier = torch.empty((job.N, job.F), dtype=torch.int8, device=dev)
-    used = torch.empty((job.N, len(caps)), dtype=torch.int64, device=dev)
     stream = torch.cuda.current_stream()
+    w = wl.WORKLOADS[args.workload]
+    res, job, M, M_w, sizes, caps, out = measure(nopfs, torch, wl, w, args.path, args.steps,
+                                                 args.warmup, stream, keep=True)
+    R, nxt, tier = out["R"], out["next"], out["tier"]
+    del out["count"], out["first"]
+    torch.cuda.empty_cache()
 
-    out = dict(R=R, count=count, first=first, next=nxt, tier=tier, used=used)
-
-    def step():
-        if args.path == "fused":
-            nopfs.plan_job(job, sizes, caps, out, stream=stream)
-            return
-        nopfs.access_streams(job, R, stream=stream)
-        nopfs.access_stats(job, R, count, first, stream=stream)
-        nopfs.reuse_next(job, R, nxt, stream=stream)
-        nopfs.tier_plan(job, count, first, sizes, caps, tier, used, stream=stream)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    print(f"[bench] {w.name}: warmup done", file=sys.stderr, flush=True)
-
-    nopfs.profile_enable(True)
-    torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step()
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    nopfs.profile_enable(False)
-    kernels = nopfs.profile_results()
-    dev_ms = ev0.elapsed_time(ev1)
-    ms_per_step = dev_ms / args.steps
-    print(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall:.2f}s)",
-          file=sys.stderr, flush=True)
-
-    # calibration copy (known traffic) for the counter runs
+    ceiling = None
     if args.calibrate_bytes > 0:
-        a = torch.empty(args.calibrate_bytes, dtype=torch.uint8, device=dev)
-        b = torch.empty_like(a)
-        nopfs.calibration_copy(a, b, args.calibrate_bytes, stream=stream)
-        torch.cuda.synchronize()
-        del a, b
-
-    D = int((count != 0).sum())  # distinct (worker, sample) cells read
-    alg, A = algorithmic_bytes(job, M_w, D, args.path == "fused")
-    per_kernel = {k: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps,
-                      "avg_ms": ms / n} for k, (n, ms) in kernels.items()}
-    dominant = max(per_kernel, key=lambda k: per_kernel[k]["ms_per_step"])
-    dom = per_kernel[dominant]
-    roofline = None
-    if dominant in alg:
-        roofline = roofline_of(w.name, dominant, alg[dominant], dom["avg_ms"])
-    for k, v in per_kernel.items():
-        if k in alg:
-            v["alg_GBps"] = round(alg[k] / (v["avg_ms"] * 1e-3) / 1e9, 1)
-    print("[bench] kernels: " + json.dumps(per_kernel), file=sys.stderr, flush=True)
+        ceiling = copy_ceiling(nopfs, torch, args.calibrate_bytes, stream)
+        print(f"[bench] copy ceiling {ceiling['GBps']} GB/s", file=sys.stderr, flush=True)
 
     schedule = model = buffer = policies = None
     if not args.no_schedule:
@@ -511,30 +648,45 @@ def main():
                              args.warmup, stream)
         policies = time_policies(nopfs, torch, wl, w, job, M, M_w, R, tier, sizes, args.steps,
                                  args.warmup, stream)
+    del out, R, nxt, tier, sizes
+    torch.cuda.empty_cache()
+
+    configs = None
+    if not args.no_configs:
+        configs = {}
+        for name in wl.ORDER:
+            if name in (w.name, "small"):
+                continue
+            configs[name] = measure(nopfs, torch, wl, wl.WORKLOADS[name], args.path,
+                                    max(args.steps, 20), args.warmup, stream)
 
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on a bounded sample ...", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, sizes_h, caps)
+        cpu = cpu_baseline(w, wl.sizes(w), caps)
 
     line = {
         "metric": METRIC,
-        "value": A / (ms_per_step * 1e-3),
+        "value": res["value"],
         "unit": "accesses/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int32",
         "data": "synthetic",
-        "config": {"workload": w.name, "path": args.path, "F": w.F, "E": w.E, "N": w.N, "B": w.B,
-                   "drop_last": w.drop_last, "seed": w.seed, "accesses": A,
-                   "tier_caps_bytes": caps, "parallelism": "none (all N workers on one GPU)"},
-        "roofline": roofline,
+        "config": dict(res["config"], parallelism="none (all N workers on one GPU)"),
+        "roofline": res["roofline"],
         "cpu_baseline": cpu,
+        "stages": res["stages"],
+        "read_cells": res.get("read_cells"),
+        "read_cell_list_bytes": res.get("read_cell_list_bytes"),
+        "copy_ceiling": ceiling,
+        "kernels": res["kernels"],
+        "configs": configs,
         "schedule": schedule,
         "model": model,
         "buffer": buffer,

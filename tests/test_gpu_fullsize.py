@@ -1,21 +1,25 @@
 """The five workloads at full size on the GPU, in the launch configuration the
-benchmark times.
+benchmark times, compared element by element with the oracle.
 
- - imagenet1k (N=16, 1.28M samples, 90 epochs): the oracle runs in full and
-   every output is compared element by element.
- - imagenet1k_256 and cosmoflow: streams, counts, first reads and next uses
-   compared in full; the tier plan in full for a subset of workers (the
-   oracle's per-worker sort of all samples is the slow part) and by its
-   defining properties for the others.
- - imagenet22k (14.2M samples, N=256, 26.5 GB of outputs): sampled samples,
-   whose positions in every epoch the oracle computes one by one from the
-   definition of the shuffle; every output touching them is compared, plus
-   the properties that hold at any size, checked on the device.
+ - imagenet1k (N=16, 1.28M samples, 90 epochs): the oracle's whole pipeline.
+ - imagenet1k_256, cosmoflow and imagenet22k (14.2M samples, N=256, 26.5 GB
+   of outputs per path): every element of R, count, first, next, tier and
+   used, for every worker, on both paths (the four stage calls and the fused
+   nopfs_plan_job). The oracle runs in a host thread pool: one task per
+   epoch permutation, then one per chunk of worker rows (its per-worker
+   counting, next-use and plan functions on its own rows of R); each chunk
+   of device rows is copied back and compared as it is reached.
+ - imagenet22k also checks the properties that hold at any size on the
+   device (row sums of count, column sums at most E, first = -1 exactly
+   where count = 0, distinct samples in each epoch segment of every row).
 """
+import sys
+import time
+
 import numpy as np
 import pytest
 
-import invariants as inv
+import oracle_pool
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -36,6 +40,10 @@ def _gpu():
 PATHS = ["staged", "fused"]  # four stage calls, or nopfs_plan_job (the benchmarked call)
 
 
+def log(msg):
+    print(f"[fullsize {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
 def run(w, path="fused"):
     job = nopfs.Job(*w.job_tuple())
     sizes = wl.sizes(w)
@@ -43,25 +51,6 @@ def run(w, path="fused"):
     out = nopfs.plan(job, s, wl.caps(w)) if path == "staged" else nopfs.plan_job(job, s, wl.caps(w))
     torch.cuda.synchronize()
     return job, sizes, out
-
-
-def check_sampled(oracle, w, job, out, n_samples=24, seed=0):
-    rng = np.random.default_rng(seed)
-    samples = np.unique(np.concatenate([rng.choice(w.F, n_samples, replace=False),
-                                        [0, w.F - 1]])).astype(np.int32)
-    cols = oracle.sample_columns(oracle.make_job(*w.job_tuple()), samples)
-    ks = torch.from_numpy(samples.astype(np.int64)).cuda()
-    np.testing.assert_array_equal(out["count"][:, ks].cpu().numpy(), cols["col_count"])
-    np.testing.assert_array_equal(out["first"][:, ks].cpu().numpy(), cols["col_first"])
-    occ_i = cols["occ_worker"].ravel()
-    occ_f = cols["occ_f"].ravel()
-    keep = occ_i >= 0
-    ii = torch.from_numpy(occ_i[keep].astype(np.int64)).cuda()
-    ff = torch.from_numpy(occ_f[keep].astype(np.int64)).cuda()
-    np.testing.assert_array_equal(out["R"][ii, ff].cpu().numpy(),
-                                  np.broadcast_to(samples, cols["occ_f"].shape).ravel()[keep])
-    np.testing.assert_array_equal(out["next"][ii, ff].cpu().numpy(),
-                                  cols["occ_next"].ravel()[keep])
 
 
 def check_device_properties(job, out):
@@ -72,20 +61,11 @@ def check_device_properties(job, out):
                        torch.tensor(Mw, dtype=torch.int64))
     assert int(count.sum(dim=0, dtype=torch.int64).max()) <= job.E
     assert torch.equal(first == -1, count == 0)
-    # each epoch segment of a row holds distinct samples
     L = M // job.E
-    for i in range(0, job.N, max(1, job.N // 8)):
-        seg = R[i].view(job.E, L).to(torch.int64).sort(dim=1).values
-        assert bool((seg[:, 1:] > seg[:, :-1]).all())
+    for i in range(0, job.N, 16):
+        seg = R[i:i + 16].view(-1, job.E, L).to(torch.int64).sort(dim=2).values
+        assert bool((seg[..., 1:] > seg[..., :-1]).all())
         assert int(seg.min()) >= 0 and int(seg.max()) < job.F
-
-
-def check_plan_rows(job, sizes, caps, out, rows):
-    c = out["count"][rows].cpu().numpy()
-    f = out["first"][rows].cpu().numpy()
-    t = out["tier"][rows].cpu().numpy()
-    u = out["used"][rows].cpu().numpy()
-    inv.check_plan(c, f, sizes, caps, t, u)
 
 
 @pytest.mark.parametrize("path", PATHS)
@@ -96,33 +76,68 @@ def test_imagenet1k_full(imagenet1k_expected, path):
         np.testing.assert_array_equal(out[n].cpu().numpy(), imagenet1k_expected[n], err_msg=n)
 
 
-@pytest.mark.parametrize("name", ["imagenet1k_256", "cosmoflow"])
-def test_full_streams_stats_next_and_plan_rows(oracle, name):
+def run_both(name):
     w = wl.WORKLOADS[name]
-    job, sizes, out = run(w)
+    t0 = time.perf_counter()
+    outs = {}
+    for path in PATHS:
+        job, sizes, outs[path] = run(w, path)
+    log(f"{name}: both paths on the device ({time.perf_counter() - t0:.1f}s)")
+    return w, job, sizes, outs
+
+
+@pytest.mark.parametrize("name", ["imagenet1k_256", "cosmoflow"])
+def test_full_size_every_element(oracle, name):
+    w, job, sizes, outs = run_both(name)
     rj = oracle.make_job(*w.job_tuple())
-    R = oracle.access_streams(rj)
-    np.testing.assert_array_equal(out["R"].cpu().numpy(), R)
-    count, first = oracle.access_stats(rj, R)
-    np.testing.assert_array_equal(out["count"].cpu().numpy(), count)
-    np.testing.assert_array_equal(out["first"].cpu().numpy(), first)
-    np.testing.assert_array_equal(out["next"].cpu().numpy(), oracle.reuse_next(rj, R))
-    rows = np.arange(0, w.N, w.N // 8)
-    tier, used = oracle.tier_plan(rj, count[rows], first[rows], sizes, wl.caps(w))
-    np.testing.assert_array_equal(out["tier"][torch.from_numpy(rows).cuda()].cpu().numpy(), tier)
-    np.testing.assert_array_equal(out["used"][torch.from_numpy(rows).cuda()].cpu().numpy(), used)
-    check_plan_rows(job, sizes, wl.caps(w), out, np.arange(1, w.N, w.N // 4))
-
-
-@pytest.mark.parametrize("path", PATHS)
-def test_imagenet22k_sampled(oracle, path):
-    w = wl.WORKLOADS["imagenet22k"]
-    job, sizes, out = run(w, path)
-    check_sampled(oracle, w, job, out, n_samples=16)
-    check_device_properties(job, out)
-    check_plan_rows(job, sizes, wl.caps(w), out, [0, 131, 255])
-    # the first tier boundary sits among samples read once (RAM 64 GB < the
-    # ~237 GB a worker reads), the second among unread samples: no -1 left
-    # unless the worker's whole row exceeds both tiers
-    del out
+    perms = oracle_pool.oracle_perms(oracle, rj)
+    mism = oracle_pool.compare_all_rows(oracle, rj, sizes, wl.caps(w), outs, perms=perms,
+                                        chunk=8, log=log)
+    assert not mism, "\n".join(mism[:20])
+    del outs, perms
     torch.cuda.empty_cache()
+
+
+# ImageNet-22k: both paths run once (53 GB of outputs stay on the device),
+# the oracle's 40 permutations are computed once, and the 256 workers are
+# compared in 8 parts of 32 (each part a test of its own, ~20 s of oracle work
+# on 16 host threads).
+I22K_PARTS = 8
+
+
+@pytest.fixture(scope="module")
+def i22k_device():
+    w, job, sizes, outs = run_both("imagenet22k")
+    yield w, job, sizes, outs
+    del outs
+    torch.cuda.empty_cache()
+
+
+@pytest.fixture(scope="module")
+def i22k_perms(oracle):
+    w = wl.WORKLOADS["imagenet22k"]
+    rj = oracle.make_job(*w.job_tuple())
+    t0 = time.perf_counter()
+    perms = oracle_pool.oracle_perms(oracle, rj)
+    log(f"imagenet22k: oracle permutations ({time.perf_counter() - t0:.1f}s, "
+        f"{oracle_pool.pool_threads()} threads)")
+    return rj, perms
+
+
+def test_imagenet22k_device_properties(i22k_device):
+    _, job, _, outs = i22k_device
+    for path in PATHS:
+        check_device_properties(job, outs[path])
+
+
+@pytest.mark.parametrize("part", range(I22K_PARTS))
+def test_imagenet22k_every_element(oracle, i22k_device, i22k_perms, part):
+    w, job, sizes, outs = i22k_device
+    rj, perms = i22k_perms
+    per = job.N // I22K_PARTS
+    i0, i1 = part * per, (part + 1) * per
+    t0 = time.perf_counter()
+    mism = oracle_pool.compare_all_rows(oracle, rj, sizes, wl.caps(w), outs, perms=perms,
+                                        chunk=2, rows=(i0, i1))
+    log(f"imagenet22k: workers {i0}..{i1 - 1} compared ({time.perf_counter() - t0:.1f}s)")
+    assert not mism, "\n".join(mism[:20])
