@@ -17,10 +17,16 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "nopfs_ref.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# NOPFS_ORACLE_SANITIZE=1 selects a build with AddressSanitizer and
+# UndefinedBehaviorSanitizer (every report aborts); the sanitizer runtimes
+# must then be preloaded into the interpreter (oracle/run_sanitized_tests.sh).
+SANITIZE = os.environ.get("NOPFS_ORACLE_SANITIZE") == "1"
+_LIB = os.path.join(_HERE, "liboracle_san.so" if SANITIZE else "liboracle.so")
 
-GCC_CMD = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra",
-           "-o", _LIB, _SRC]
+GCC_CMD = (["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Wextra"]
+           + (["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+               "-fno-sanitize-recover=all"] if SANITIZE else [])
+           + ["-o", _LIB, _SRC])
 
 
 class OracleError(RuntimeError):
