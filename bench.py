@@ -247,15 +247,23 @@ def rocprof_summary(d, workload):
 
 
 def cpu_model():
-    """The host CPU's model name (the first "model name" of /proc/cpuinfo)."""
+    """The host CPU's model name: lscpu's "Model name", else the first
+    "model name" of /proc/cpuinfo."""
+    import subprocess
+    try:
+        r = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10)
+        for line in r.stdout.splitlines():
+            if line.strip().startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
     try:
         for line in open("/proc/cpuinfo"):
             if line.startswith("model name"):
                 return line.split(":", 1)[1].strip()
     except OSError:
         pass
-    import platform
-    return platform.processor() or "unknown"
+    return "unknown"
 
 
 def cpu_baseline(w, sizes, caps, epochs=2, workers=2):
@@ -565,10 +573,12 @@ def measure(nopfs, torch, wl, w, path, steps, warmup, stream, keep=False):
             b = sb[st] + exch
             stages[st]["alg_bytes_with_exchange"] = b
             stages[st]["frac_with_exchange"] = round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
-    dominant = max(per_kernel, key=lambda k: per_kernel[k]["ms_per_step"])
-    roofline = None
-    if dominant in kb:
-        roofline = roofline_of(w.name, dominant, kb[dominant], per_kernel[dominant]["avg_ms"])
+    # the roofline is that of the slowest kernel carrying a stage's bytes; the
+    # slowest kernel overall is named beside it
+    slowest = max(per_kernel, key=lambda k: per_kernel[k]["ms_per_step"])
+    dominant = max((k for k in per_kernel if k in kb), key=lambda k: per_kernel[k]["ms_per_step"])
+    roofline = roofline_of(w.name, dominant, kb[dominant], per_kernel[dominant]["avg_ms"])
+    roofline["slowest_kernel"] = slowest
     res = {
         "value": A / (ms_per_step * 1e-3),
         "unit": "accesses/s",

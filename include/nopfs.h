@@ -16,16 +16,22 @@
  *    marked "host". Outputs are preallocated by the caller; the library writes
  *    every element of every output (no zeroing needed) and keeps no pointer
  *    after the enqueued work completes.
- *  - `hip_stream` is a hipStream_t (NULL = the null stream). GPU calls only
+ *  - `hip_stream` is a hipStream_t (NULL = the null stream). GPU calls
  *    enqueue work on it and return; the caller keeps the buffers alive until
  *    the stream has completed. Internal scratch comes from one block of
  *    device memory per (device, stream), reused in stream order by every call
  *    on that stream: a call that needs more than the block allocates the rest
- *    (hipMalloc), synchronises the stream at its end and replaces the block
- *    by one of its peak size, so later calls of that size allocate nothing.
- *    The block is kept until the process ends (at most the largest call's
- *    scratch per stream). Calls on one stream from several host threads run
- *    one at a time.
+ *    (hipMalloc) and replaces the block by one of its peak size at its end,
+ *    so later calls of that size allocate nothing. The block is kept until
+ *    nopfs_scratch_release (or the end of the process): at most the largest
+ *    call's scratch per stream. Calls on one stream from several host
+ *    threads are enqueued one at a time.
+ *  - Host waits: a GPU call returns without waiting for the device, except
+ *    a call that outgrows its stream's block (the first call of a larger job
+ *    on a stream, or the first after nopfs_scratch_release), which
+ *    synchronises the stream after enqueueing its work, before it frees and
+ *    replaces the block. nopfs_scratch_release and nopfs_profile_query wait
+ *    too; nothing else does.
  *  - Return 0 on success, a negative NOPFS_E* code otherwise. Argument errors
  *    are detected on the host before anything is enqueued. No C++ exception
  *    crosses this boundary. nopfs_last_error() gives a thread-local detail.
@@ -357,6 +363,13 @@ int nopfs_profile_query(int idx, const char** name, int64_t* launches,
 int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes,
                            void* hip_stream);
 
+/* Returns the scratch block of (current device, hip_stream) to the device:
+ * waits for the work enqueued on the stream (hipStreamSynchronize), then
+ * frees the block (hipFree). The next call on that stream allocates a new
+ * one. A call being enqueued on the stream from another host thread
+ * finishes first. Nothing to release is not an error. Errors: EDEVICE. */
+int nopfs_scratch_release(void* hip_stream);
+
 /* ---- Test hooks ------------------------------------------------------- */
 
 /* Overrides internal capacities so tests can drive the slow paths on small
@@ -367,7 +380,8 @@ int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes,
  *   which=3  fail the next internal scratch allocation (value 1)
  *   which=4  longest range of buffer starts the staging schedule keeps in
  *            LDS per chunk (wider ranges take the global-memory search)
- * Not thread-safe; meant for tests only. */
+ * The overrides are per host thread: they apply only to calls made from the
+ * thread that set them. Meant for tests only. */
 int nopfs_debug_set(int which, int64_t value);
 
 #ifdef __cplusplus

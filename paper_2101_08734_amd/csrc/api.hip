@@ -1,6 +1,6 @@
 // Host-side plumbing of the planner library: argument validation and shape
-// arithmetic, error reporting, stream-ordered scratch, per-kernel event
-// timing, and the calibration copy kernel.
+// arithmetic, error reporting, the per-stream scratch blocks, per-kernel
+// event timing, and the calibration copy kernel.
 #include <map>
 #include <mutex>
 #include <new>
@@ -49,7 +49,9 @@ int make_shape(const nopfs_job* job, Shape* s) {
 }
 
 // ---------------------------------------------------------------- scratch --
-static int64_t g_debug[5] = {0, 0, 0, 0, 0};
+// Test overrides (nopfs_debug_set): per host thread, so a test that forces a
+// slow path affects only the calls it makes itself.
+static thread_local int64_t g_debug[5] = {0, 0, 0, 0, 0};
 
 int64_t debug_value(int which) { return (which >= 0 && which < 5) ? g_debug[which] : 0; }
 
@@ -69,7 +71,8 @@ bool take_alloc_failure() {
 // call's peak size, so later calls of that size allocate nothing. Per-call
 // stream-ordered allocations of gigabytes stalled the host for hundreds of
 // milliseconds per call after ~100 calls (the allocator returned and mapped
-// memory again); the arena keeps its memory until the process ends.
+// memory again); the arena keeps its memory until nopfs_scratch_release or
+// the end of the process.
 struct Arena {
   std::recursive_mutex mu;
   int depth = 0;            // live Scratch objects
@@ -87,17 +90,23 @@ struct Arena {
   std::vector<Rec> stack;
 };
 
-static Arena* arena_of(hipStream_t s) {
-  static std::mutex mu;
-  static std::map<std::pair<int, hipStream_t>, Arena*> arenas;  // kept until exit
+static std::mutex g_arenas_mu;
+static std::map<std::pair<int, hipStream_t>, Arena*> g_arenas;  // kept until exit
+
+// The arena of (current device, s); created on first use unless `create` is
+// false (then nullptr when there is none).
+static Arena* arena_of(hipStream_t s, bool create = true) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) {
     (void)hipGetLastError();
     return nullptr;
   }
-  std::lock_guard<std::mutex> g(mu);
-  Arena*& a = arenas[{dev, s}];
-  if (!a) a = new (std::nothrow) Arena;
+  std::lock_guard<std::mutex> g(g_arenas_mu);
+  auto it = g_arenas.find({dev, s});
+  if (it != g_arenas.end()) return it->second;
+  if (!create) return nullptr;
+  Arena* a = new (std::nothrow) Arena;
+  if (a) g_arenas[{dev, s}] = a;
   return a;
 }
 
@@ -309,6 +318,25 @@ int nopfs_calibration_copy(const void* src, void* dst, int64_t bytes, void* hip_
   return launch("calibration_copy", calibration_copy_kernel, dim3(uint32_t(blocks)), dim3(256), 0,
                 static_cast<hipStream_t>(hip_stream), static_cast<const uint4*>(src),
                 static_cast<uint4*>(dst), n);
+}
+
+int nopfs_scratch_release(void* hip_stream) {
+  try {
+    const hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    Arena* a = arena_of(s, false);
+    if (!a) return NOPFS_OK;  // no block on this stream
+    std::lock_guard<std::recursive_mutex> g(a->mu);  // waits for a call being enqueued
+    if (a->depth != 0) return fail(NOPFS_EINVAL, "scratch release from inside a call");
+    if (!a->block) return NOPFS_OK;
+    NOPFS_HIP(hipStreamSynchronize(s));
+    NOPFS_HIP(hipFree(a->block));
+    a->block = nullptr;
+    a->cap = 0;
+    a->top = 0;
+    return NOPFS_OK;
+  } catch (...) {
+    return fail(NOPFS_EDEVICE, "unexpected host exception");
+  }
 }
 
 int nopfs_debug_set(int which, int64_t value) {

@@ -52,7 +52,7 @@ __host__ __device__ inline int64_t epoch_len(int64_t F, int64_t N, int64_t B,
 }
 
 // --------------------------------------------------------------- scratch --
-// Stream-ordered device scratch (hipMallocAsync / hipFreeAsync).
+// Device scratch of a call, from the block of (current device, stream).
 class Scratch {
  public:
   // Takes the scratch arena of (current device, s): calls on one stream share

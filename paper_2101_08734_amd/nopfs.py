@@ -105,6 +105,7 @@ def lib() -> ctypes.CDLL:
             "nopfs_profile_query": [ctypes.c_int, ctypes.POINTER(ctypes.c_char_p),
                                     ctypes.POINTER(I64), ctypes.POINTER(ctypes.c_double)],
             "nopfs_calibration_copy": [P, P, I64, P],
+            "nopfs_scratch_release": [P],
             "nopfs_debug_set": [ctypes.c_int, I64],
         }
         for name, args in sig.items():
@@ -121,11 +122,12 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_streams_range",
             "nopfs_access_stats",
-            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_prefetch_order",
+            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job",
+            "nopfs_prefetch_order",
             "nopfs_staging_schedule", "nopfs_fetch_model", "nopfs_buffer_sim", "nopfs_policy_sim",
             "nopfs_strerror",
             "nopfs_last_error", "nopfs_profile_enable", "nopfs_profile_query",
-            "nopfs_calibration_copy", "nopfs_debug_set")
+            "nopfs_calibration_copy", "nopfs_scratch_release", "nopfs_debug_set")
 
 
 def _check(rc: int, what: str):
@@ -244,6 +246,10 @@ def tier_plan(job: Job, count, first, sizes, caps, tier=None, used=None, stream=
 def plan_job(job: Job, sizes, caps, out=None, stream=None):
     """The whole path in one library call (nopfs_plan_job); the same outputs
     as plan(). `out` may hold preallocated R, count, first, next, tier, used."""
+    return _plan_job("nopfs_plan_job", job, sizes, caps, out, stream)
+
+
+def _plan_job(fn, job: Job, sizes, caps, out, stream):
     _, M, _ = stream_shape(job)
     _device_tensor(sizes, torch.int64, (job.F,), "sizes")
     caps_list = [int(c) for c in caps]
@@ -258,9 +264,9 @@ def plan_job(job: Job, sizes, caps, out=None, stream=None):
             o[name] = torch.empty(shape, dtype=dt, device="cuda")
         _device_tensor(o[name], dt, shape, name)
     j = job.c()
-    _check(lib().nopfs_plan_job(ctypes.byref(j), _ptr(sizes), ctypes.cast(caps_host, ctypes.c_void_p),
-                                J, _ptr(o["R"]), _ptr(o["count"]), _ptr(o["first"]), _ptr(o["next"]),
-                                _ptr(o["tier"]), _ptr(o["used"]), _stream(stream)), "nopfs_plan_job")
+    _check(getattr(lib(), fn)(ctypes.byref(j), _ptr(sizes), ctypes.cast(caps_host, ctypes.c_void_p),
+                              J, _ptr(o["R"]), _ptr(o["count"]), _ptr(o["first"]), _ptr(o["next"]),
+                              _ptr(o["tier"]), _ptr(o["used"]), _stream(stream)), fn)
     return o
 
 
@@ -405,6 +411,12 @@ def profile_results():
         out[name.value.decode()] = (n.value, ms.value)
         idx += 1
     return out
+
+
+def scratch_release(stream=None):
+    """Frees the scratch block of (current device, stream) after the
+    stream's work completes (nopfs_scratch_release)."""
+    _check(lib().nopfs_scratch_release(_stream(stream)), "nopfs_scratch_release")
 
 
 def calibration_copy(src, dst, nbytes: int, stream=None):

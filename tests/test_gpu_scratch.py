@@ -93,3 +93,20 @@ def test_repeated_calls_allocate_nothing_more():
     # the outputs of the first call above are the only new memory
     out_bytes = sum(v.numel() * v.element_size() for v in out.values())
     assert free0 - free1 <= out_bytes + (64 << 20)
+
+
+def test_release_returns_the_block_and_later_calls_still_agree():
+    want = _host(_run(LARGE))
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    free0, _ = torch.cuda.mem_get_info()
+    nopfs.scratch_release()
+    free1, _ = torch.cuda.mem_get_info()
+    # LARGE needs well over 100 MB of scratch (pairs of all epochs alone:
+    # 16 B x E x F = 144 MB)
+    assert free1 - free0 >= 100 << 20
+    nopfs.scratch_release()  # nothing left to release: not an error
+    got = _host(_run(LARGE))  # grows a new block
+    _same(want, got)
+    s = torch.cuda.Stream()
+    nopfs.scratch_release(stream=s)  # a stream that never had a block
