@@ -177,6 +177,26 @@ int nopfs_plan_job(const nopfs_job* job, const int64_t* sizes, const int64_t* ca
                    int32_t J, int32_t* R, uint8_t* count, int32_t* first, int32_t* next,
                    int8_t* tier, int64_t* used, void* hip_stream);
 
+/* nopfs_plan_job for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, outputs and errors, but no call to hipMalloc, hipFree
+ * or any allocating routine, and no host wait. Its scratch is one fixed
+ * array of 64 MiB (67,108,864 bytes) per device, part of the library's code
+ * object, held by every device the library runs on until the process ends;
+ * its address on a device is looked up once, on the first call there. A job
+ * whose scratch exceeds it is rejected with ERANGE before anything is
+ * enqueued (the peak is the shuffle's exchange, about 16 bytes per sample
+ * and epoch: F = 200,000 samples over 10 epochs fits, F = 1,000,000 over 10
+ * epochs needs 164 MB and is rejected). Every call on a
+ * device shares that device's array, and each call initialises what it
+ * reads there, so consecutive calls need nothing from each other; calls
+ * that overlap in time on one device (other streams, other host threads'
+ * streams) race on the array and must be ordered by the caller (one stream,
+ * or events). Calls from several host threads are enqueued one at a time. */
+int nopfs_plan_job_noalloc(const nopfs_job* job, const int64_t* sizes, const int64_t* caps,
+                           int32_t J, int32_t* R, uint8_t* count, int32_t* first,
+                           int32_t* next, int8_t* tier, int64_t* used, void* hip_stream);
+
 /* Prefetch order of the cache tiers (section 5.1: samples are always fetched
  * in their order of access, following the first of the prefetching rules of
  * section 3; a worker fills each storage class with the samples placed

@@ -1,6 +1,7 @@
 // Host-side plumbing of the planner library: argument validation and shape
 // arithmetic, error reporting, the per-stream scratch blocks, per-kernel
 // event timing, and the calibration copy kernel.
+#include <functional>
 #include <map>
 #include <mutex>
 #include <new>
@@ -75,12 +76,14 @@ bool take_alloc_failure() {
 // the end of the process.
 struct Arena {
   std::recursive_mutex mu;
+  bool fixed = false;       // a fixed block that never grows (no allocation)
   int depth = 0;            // live Scratch objects
   char* block = nullptr;    // the reused block
   size_t cap = 0;
   size_t top = 0;           // bytes of the block in use
   size_t extent = 0;        // top plus live extra blocks
   size_t peak = 0;          // largest extent of the current call
+  size_t peak_total = 0;    // largest extent of any call (sizing passes)
   bool failed = false;      // an allocation of the current call failed
   std::vector<void*> extra; // blocks beyond `block`, freed at the call's end
   struct Rec {
@@ -110,7 +113,68 @@ static Arena* arena_of(hipStream_t s, bool create = true) {
   return a;
 }
 
-Scratch::Scratch(hipStream_t s) : stream_(s), arena_(arena_of(s)) {
+// A fixed arena installed for the calls of this thread (sizing passes and
+// the allocation-free entry point), and whether launches are only counted.
+static thread_local Arena* t_fixed_arena = nullptr;
+static thread_local bool t_sizing = false;
+
+bool sizing_only() { return t_sizing; }
+
+int run_sizing(const std::function<int()>& call, size_t* peak) {
+  // The call runs its host logic with every scratch buffer carved from a
+  // block that is never dereferenced and no kernel launched. No decision of
+  // the library depends on where its scratch lies (only on the job and the
+  // caller's pointers), so the sizes are those of a real call.
+  Arena a;
+  a.fixed = true;
+  a.block = reinterpret_cast<char*>(uintptr_t(1) << 46);
+  a.cap = size_t(1) << 45;
+  Arena* prev = t_fixed_arena;
+  const bool prev_sizing = t_sizing;
+  t_fixed_arena = &a;
+  t_sizing = true;
+  int rc;
+  try {
+    rc = call();
+  } catch (...) {
+    rc = fail(NOPFS_EDEVICE, "unexpected host exception");
+  }
+  t_fixed_arena = prev;
+  t_sizing = prev_sizing;
+  *peak = a.peak_total;
+  return rc;
+}
+
+int run_in_fixed_block(char* block, size_t cap, const std::function<int()>& call) {
+  static std::mutex mu;
+  static std::map<char*, Arena*> arenas;  // one per block (per device), kept until exit
+  Arena* a;
+  {
+    std::lock_guard<std::mutex> g(mu);
+    Arena*& r = arenas[block];
+    if (!r) {
+      r = new (std::nothrow) Arena;
+      if (!r) return fail(NOPFS_ENOMEM, "host allocation failed");
+      r->fixed = true;
+      r->block = block;
+      r->cap = cap;
+    }
+    a = r;
+  }
+  std::lock_guard<std::recursive_mutex> g(a->mu);  // one call per block at a time
+  Arena* prev = t_fixed_arena;
+  t_fixed_arena = a;
+  int rc;
+  try {
+    rc = call();
+  } catch (...) {
+    rc = fail(NOPFS_EDEVICE, "unexpected host exception");
+  }
+  t_fixed_arena = prev;
+  return rc;
+}
+
+Scratch::Scratch(hipStream_t s) : stream_(s), arena_(t_fixed_arena ? t_fixed_arena : arena_of(s)) {
   if (!arena_) return;
   arena_->mu.lock();
   ++arena_->depth;
@@ -127,7 +191,8 @@ Scratch::~Scratch() {
     a->stack.pop_back();
   }
   if (--a->depth == 0) {
-    if (!a->extra.empty()) {
+    if (a->peak > a->peak_total) a->peak_total = a->peak;
+    if (!a->fixed && !a->extra.empty()) {
       // the call outgrew the block: after its work, one block of its peak
       // (a call that ran out of memory keeps the old block)
       (void)hipStreamSynchronize(stream_);
@@ -165,6 +230,9 @@ int Scratch::alloc(void** p, size_t bytes) {
     r.in_block = true;
     a->top += bytes;
     *p = a->block + r.off;
+  } else if (a->fixed) {
+    return fail(NOPFS_ENOMEM, std::string("scratch of ") + std::to_string(a->top + bytes) +
+                                  " bytes exceeds the fixed block of " + std::to_string(a->cap));
   } else {
     void* q = nullptr;
     const hipError_t e = hipMalloc(&q, bytes);

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <functional>
 #include <string>
 
 #include "nopfs.h"
@@ -74,6 +75,18 @@ class Scratch {
   int n_ = 0;
 };
 
+// Runs `call` (an entry point's implementation) on this thread with every
+// scratch buffer carved from a stand-in block that is never dereferenced and
+// no kernel launched; *peak receives the most scratch the call held at once.
+// Returns the call's status (argument errors as usual).
+int run_sizing(const std::function<int()>& call, size_t* peak);
+// Runs `call` on this thread with its scratch carved from the fixed device
+// block [block, block + cap), which never grows: a call that needs more
+// fails with ENOMEM. Calls on one block are enqueued one at a time.
+int run_in_fixed_block(char* block, size_t cap, const std::function<int()>& call);
+// True inside run_sizing on this thread.
+bool sizing_only();
+
 // ---------------------------------------------------------------- launch --
 // Records HIP events around a launch when profiling is on.
 void prof_begin(const char* name, hipStream_t s);
@@ -83,6 +96,7 @@ template <typename Kernel, typename... Args>
 int launch(const char* name, Kernel k, dim3 grid, dim3 block, size_t shmem,
            hipStream_t s, Args... args) {
   if (grid.x == 0 || grid.y == 0 || grid.z == 0) return NOPFS_OK;
+  if (sizing_only()) return NOPFS_OK;
   prof_begin(name, s);
   hipLaunchKernelGGL(k, grid, block, shmem, s, args...);
   hipError_t e = hipGetLastError();

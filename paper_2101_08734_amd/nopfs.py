@@ -95,6 +95,7 @@ def lib() -> ctypes.CDLL:
             "nopfs_reuse_next": [jp, P, P, P],
             "nopfs_tier_plan": [jp, P, P, P, P, I32, P, P, P],
             "nopfs_plan_job": [jp, P, P, I32, P, P, P, P, P, P, P],
+            "nopfs_plan_job_noalloc": [jp, P, P, I32, P, P, P, P, P, P, P],
             "nopfs_prefetch_order": [jp, P, P, I32, P, P, P],
             "nopfs_staging_schedule": [jp, P, P, I64, P, P],
             "nopfs_fetch_model": [jp, P, P, P, ctypes.POINTER(Model), P, P, P],
@@ -122,7 +123,7 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED = ("nopfs_stream_shape", "nopfs_access_streams", "nopfs_access_streams_range",
             "nopfs_access_stats",
-            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job",
+            "nopfs_reuse_next", "nopfs_tier_plan", "nopfs_plan_job", "nopfs_plan_job_noalloc",
             "nopfs_prefetch_order",
             "nopfs_staging_schedule", "nopfs_fetch_model", "nopfs_buffer_sim", "nopfs_policy_sim",
             "nopfs_strerror",
@@ -247,6 +248,16 @@ def plan_job(job: Job, sizes, caps, out=None, stream=None):
     """The whole path in one library call (nopfs_plan_job); the same outputs
     as plan(). `out` may hold preallocated R, count, first, next, tier, used."""
     return _plan_job("nopfs_plan_job", job, sizes, caps, out, stream)
+
+
+def plan_job_noalloc(job: Job, sizes, caps, out, stream=None):
+    """nopfs_plan_job_noalloc: plan_job with the library's fixed per-device
+    scratch array, no device allocation by the library. `out` must hold all
+    six preallocated outputs."""
+    for name in ("R", "count", "first", "next", "tier", "used"):
+        if out.get(name) is None:
+            raise ValueError(f"plan_job_noalloc needs a preallocated {name}")
+    return _plan_job("nopfs_plan_job_noalloc", job, sizes, caps, out, stream)
 
 
 def _plan_job(fn, job: Job, sizes, caps, out, stream):

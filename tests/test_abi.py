@@ -264,3 +264,21 @@ def test_strerror(L):
     assert L.nopfs_debug_set(1, -5) == nopfs.NOPFS_EINVAL
     assert L.nopfs_debug_set(5, 1) == nopfs.NOPFS_EINVAL
     assert L.nopfs_debug_set(4, 0) == 0
+
+
+def test_noalloc_rejects_a_job_beyond_its_scratch_on_the_host():
+    """nopfs_plan_job_noalloc sizes a job's scratch on the host before it
+    touches the device: a job that needs more than the fixed array is
+    rejected with ERANGE (no GPU needed; the pointers are never used)."""
+    L = nopfs.lib()
+    fake = ctypes.c_void_p(1 << 40)
+    caps = (ctypes.c_int64 * 2)(10**9, 10**10)
+    j = nopfs.Job(1_000_000, 10, 8, 32).c()
+    rc = L.nopfs_plan_job_noalloc(ctypes.byref(j), fake, ctypes.cast(caps, ctypes.c_void_p), 2,
+                                  fake, fake, fake, fake, fake, fake, None)
+    assert rc == nopfs.NOPFS_ERANGE
+    assert "bytes of scratch" in L.nopfs_last_error().decode()
+    j = nopfs.Job(1_000_000, 300, 8, 32).c()  # argument errors come first
+    rc = L.nopfs_plan_job_noalloc(ctypes.byref(j), fake, ctypes.cast(caps, ctypes.c_void_p), 2,
+                                  fake, fake, fake, fake, fake, fake, None)
+    assert rc == nopfs.NOPFS_ERANGE and "E must be" in L.nopfs_last_error().decode()
