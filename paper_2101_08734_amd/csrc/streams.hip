@@ -5,29 +5,38 @@
 // the N workers and a worker's stream R is the concatenation of its batches.
 //
 // Epoch e orders the samples by (key_e(k), k), key_e(k) a Philox-4x32-10
-// word. The order is built as a bucket sort over all epochs of a batch at
-// once. Fine bucket b = umulhi(key, nb) holds a few thousand keys; coarse
-// bucket c = umulhi(key, nb1) (nb = nb1 * nf) groups nf consecutive fine ones.
-//   1. stream_count   -- Philox keys in registers; per (epoch, chunk of 64K
-//                        ids) histogram of the fine buckets.
-//   2. stream_offsets -- per (epoch, fine bucket) running sum over chunks.
-//   3. stream_scan    -- fine bucket start positions per epoch.
-//   4. stream_scatter -- keys regenerated and (key, id) pairs written into
-//                        their coarse bucket (at most 64 per epoch, so each
-//                        workgroup's open cache lines fit in L2 and every
-//                        line is completed there before it is written back).
-//   5. stream_split   -- each coarse bucket read back in 16K-pair pieces and
-//                        split into its nf fine buckets (skipped when nf = 1).
-//   6. stream_sort    -- one workgroup per fine bucket: counting sort in LDS
-//                        by the top 13 bits of the key inside the bucket,
-//                        each pair then placed inside its (tiny) digit group
-//                        by its rank in (key, id) order, and
-//                        the sorted positions p sharded straight into R:
-//                        R[p mod N][e*L_i + p div N], through an LDS
-//                        transpose so each worker row gets a run.
-// Buckets larger than the LDS capacity (not expected for uniform keys, but
-// possible in principle) are sorted in place in global memory by a bitonic
-// network inside the same workgroup.
+// word. The order is a bucket sort with one level of buckets: bucket
+// b = key >> (32 - m) (2^m buckets per epoch, a few thousand keys each), all
+// epochs of a batch at once. The ids of an epoch are cut into chunks of C
+// consecutive ids; inside a bucket the keys of each chunk form one run, runs
+// in chunk order. Every element travels as ONE 32-bit word:
+//     word = kb << cbits | (id - chunk * C)
+// where kb is the top (32 - cbits) bits of the key below the bucket bits.
+// The chunk of a word follows from its position in the bucket (the run
+// bounds are known from the counting pass), so the id is exact; kb orders
+// the bucket except where two words share kb, which is resolved by the full
+// keys (regenerated from the ids) and then the ids.
+//   1. stream_count   -- Philox keys in registers; per (epoch, chunk)
+//                        histogram of the buckets.
+//   2. stream_offsets -- per (epoch, bucket) running sum over chunks: the
+//                        run starts, in chunk-major and bucket-major copies.
+//   3. stream_scan    -- bucket starts per epoch.
+//   4. stream_scatter -- keys regenerated; each chunk counting-sorted by
+//                        bucket in LDS (rounds of 24,576 ids, one workgroup
+//                        per CU) and written as words, one contiguous run per
+//                        bucket and round.
+//   5. stream_sort    -- one workgroup per bucket: words decoded (chunk from
+//                        the run table), counting sort in LDS by the top 13
+//                        bits of kb, the digit groups of two or more (a fifth
+//                        of them) insertion-sorted, and the sorted positions p
+//                        sharded straight into R: R[p mod N][e*L_i + p div N],
+//                        through an LDS transpose so each worker row gets a
+//                        run of consecutive positions.
+// At most 4,096 buckets are handled per pass ("window" of buckets); larger
+// jobs (F above ~31M) make several passes over the keys, each keeping the
+// keys of its window. Buckets larger than the LDS capacity (not expected for
+// uniform keys, but possible in principle) are sorted in place in global
+// memory by a bitonic network inside the same workgroup.
 #include <limits.h>
 
 #include "common.hpp"
@@ -36,323 +45,292 @@
 namespace nopfs {
 namespace {
 
-constexpr int kChunkThreads = 1024;
-constexpr int kBlocksPerThread = 16;                                   // Philox blocks
-constexpr int64_t kChunkIds = int64_t(kChunkThreads) * kBlocksPerThread * 4;  // 65536
-constexpr uint32_t kMaxBuckets = 8192;
+constexpr int kThreads = 1024;
+constexpr int kRoundBlocks = 6;                            // Philox blocks per thread and round
+constexpr int kRound = kThreads * 4 * kRoundBlocks;        // 24,576 ids per scatter round
+#ifndef NOPFS_CHUNK_ROUNDS
+#define NOPFS_CHUNK_ROUNDS 1
+#endif
+constexpr int kChunkRounds = NOPFS_CHUNK_ROUNDS;           // smallest chunk, in rounds
+constexpr uint32_t kMaxChunks = 2048;                      // chunks per epoch (sort's run table)
+constexpr uint32_t kMaxWin = 4096;                         // buckets per pass
+constexpr int64_t kMeanBucket = 7700;                      // largest mean bucket size
+constexpr int kBlkShift = 3;                               // run-table lookup granularity
 
-// Tuning knobs: bucket capacity = threads x items (identical results).
-#ifndef NOPFS_SORT_THREADS
-#define NOPFS_SORT_THREADS 1024
+#ifndef NOPFS_SORT_CAP
+#define NOPFS_SORT_CAP 8192
 #endif
-#ifndef NOPFS_SORT_ITEMS
-#define NOPFS_SORT_ITEMS 8
-#endif
-constexpr int kSortThreads = NOPFS_SORT_THREADS;
-constexpr int kItems = NOPFS_SORT_ITEMS;
-constexpr int kSortCap = kSortThreads * kItems;  // 8192 (key, id) pairs in LDS
-constexpr int kDigitBits = 13;
-constexpr int kDigits = 1 << kDigitBits;
+constexpr int kSortCap = NOPFS_SORT_CAP;  // largest bucket sorted in LDS
+constexpr int kItems = kSortCap / kThreads;
+static_assert(kSortCap % kThreads == 0 && kSortCap < 65536, "16-bit digit counts");
 
 struct StreamParams {
   int64_t F, N, B, P, L, M_max;
   int32_t drop_last;
   uint32_t seed_lo, seed_hi;
-  uint32_t nb;        // fine buckets per epoch
-  uint32_t nb1;       // coarse buckets per epoch
-  uint32_t nf;        // fine buckets per coarse bucket (nb = nb1 * nf)
-  int32_t e0;         // first epoch of the batch (the epoch its keys are drawn for)
-  int32_t e_first;    // epoch written at the start of the rows
-  int32_t sort_bits;  // significant bits of a key inside its bucket
-  int32_t cap;        // largest bucket sorted in LDS
+  uint32_t m;        // log2 of the buckets per epoch
+  uint32_t wb0;      // first bucket of this pass
+  uint32_t nbw;      // buckets of this pass
+  uint32_t C;        // ids per chunk (a multiple of kRound)
+  uint32_t cbits;    // C <= 2^cbits
+  uint32_t nchunks;  // chunks per epoch
+  int32_t e0;        // epoch of the batch's first keys
+  int32_t e_first;   // epoch written at the start of the rows
+  int32_t cap;       // largest bucket sorted in LDS
 };
 
+__device__ __forceinline__ uint32_t bucket_of(uint32_t key, uint32_t m) {
+  return m ? key >> (32u - m) : 0u;
+}
+
+// kb: the top (32 - cbits) bits of the key's offset inside its bucket
+// (32 - m bits); monotone in the key inside a bucket.
+__device__ __forceinline__ uint32_t stored_bits(uint32_t key, uint32_t m, uint32_t cbits) {
+  const uint32_t off = m ? key & (0xFFFFFFFFu >> m) : key;
+  return cbits >= m ? off >> (cbits - m) : off << (m - cbits);
+}
+
+__device__ __forceinline__ uint32_t philox_key(uint32_t id, uint32_t e, uint32_t slo, uint32_t shi) {
+  const Philox4 r = philox_block(id >> 2, e, slo, shi);
+  const uint32_t s = id & 3u;
+  return s == 0 ? r.x : (s == 1 ? r.y : (s == 2 ? r.z : r.w));
+}
+
 // -- 1. histogram of buckets per chunk ----------------------------------------
-// cnt layout: [epoch][chunk][bucket]
-__global__ void __launch_bounds__(kChunkThreads)
-stream_count(StreamParams p, uint32_t nchunks, uint32_t* __restrict__ cnt) {
+// cnt layout: [epoch][chunk][bucket of the pass]
+__global__ void __launch_bounds__(kThreads)
+stream_count(StreamParams p, uint32_t* __restrict__ cnt) {
   extern __shared__ uint32_t hist[];
-  const uint32_t nb = p.nb;
-  for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) hist[b] = 0;
+  const uint32_t nbw = p.nbw;
+  for (uint32_t b = threadIdx.x; b < nbw; b += kThreads) hist[b] = 0;
   __syncthreads();
   const uint32_t e = uint32_t(p.e0) + blockIdx.y;
-  const int64_t blk0 = int64_t(blockIdx.x) * (kChunkIds / 4);
-#pragma unroll 4
-  for (int it = 0; it < kBlocksPerThread; ++it) {
-    const int64_t blk = blk0 + it * kChunkThreads + threadIdx.x;
+  const int64_t blk0 = int64_t(blockIdx.x) * (p.C / 4);
+  const int iters = int(p.C / (4 * kThreads));
+  for (int it = 0; it < iters; ++it) {
+    const int64_t blk = blk0 + int64_t(it) * kThreads + threadIdx.x;
     const int64_t id0 = blk * 4;
     if (id0 < p.F) {
       const Philox4 r = philox_block(uint32_t(blk), e, p.seed_lo, p.seed_hi);
       const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (id0 + c < p.F) atomicAdd(&hist[__umulhi(w[c], nb)], 1u);
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t b = bucket_of(w[c], p.m) - p.wb0;
+        if (id0 + c < p.F && b < nbw) atomicAdd(&hist[b], 1u);
+      }
     }
   }
   __syncthreads();
-  uint32_t* out = cnt + (int64_t(blockIdx.y) * nchunks + blockIdx.x) * nb;
-  for (uint32_t b = threadIdx.x; b < nb; b += blockDim.x) out[b] = hist[b];
+  uint32_t* out = cnt + (int64_t(blockIdx.y) * p.nchunks + blockIdx.x) * nbw;
+  for (uint32_t b = threadIdx.x; b < nbw; b += kThreads) out[b] = hist[b];
 }
 
-// -- 2. chunk offsets inside each bucket --------------------------------------
+// -- 2. run starts --------------------------------------------------------------
 // In place: cnt[e][c][b] becomes the number of bucket-b keys of epoch e in
-// chunks before c; tot[e][b] receives the bucket size.
+// chunks before c; offb[e][b][c] receives the same values bucket-major, with
+// offb[e][b][nchunks] and tot[e][b] the bucket size.
 __global__ void __launch_bounds__(256)
-stream_offsets(uint32_t nb, uint32_t nchunks, uint32_t* __restrict__ cnt,
+stream_offsets(StreamParams p, uint32_t* __restrict__ cnt, uint32_t* __restrict__ offb,
                uint32_t* __restrict__ tot) {
-  const uint32_t b = blockIdx.x * 256 + threadIdx.x;
-  if (b >= nb) return;
-  uint32_t* col = cnt + int64_t(blockIdx.y) * nchunks * nb + b;
-  uint32_t run = 0;
-  uint32_t c = 0;
-  for (; c + 8 <= nchunks; c += 8) {
-    uint32_t v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = col[int64_t(c + u) * nb];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      col[int64_t(c + u) * nb] = run;
-      run += v[u];
-    }
-  }
-  for (; c < nchunks; ++c) {
-    const uint32_t v = col[int64_t(c) * nb];
-    col[int64_t(c) * nb] = run;
-    run += v;
-  }
-  tot[int64_t(blockIdx.y) * nb + b] = run;
-}
-
-// -- 3. bucket starts --------------------------------------------------------
-__global__ void __launch_bounds__(1024)
-stream_scan(uint32_t nb, const uint32_t* __restrict__ tot, uint32_t* __restrict__ start,
-            uint32_t* __restrict__ cursor) {
-  __shared__ uint32_t tmp[65];
-  const uint32_t* t = tot + int64_t(blockIdx.x) * nb;
-  uint32_t* st = start + int64_t(blockIdx.x) * (nb + 1);
-  uint32_t* cu = cursor + int64_t(blockIdx.x) * nb;
-  uint32_t carry = 0;
-  for (uint32_t base = 0; base < nb; base += blockDim.x) {
-    const uint32_t b = base + threadIdx.x;
-    const uint32_t v = b < nb ? t[b] : 0u;
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan(v, tmp, &total);
-    if (b < nb) {
-      st[b] = carry + ex;
-      cu[b] = carry + ex;
-    }
-    carry += total;
-  }
-  if (threadIdx.x == 0) st[nb] = carry;
-}
-
-// -- 4. scatter into coarse buckets ------------------------------------------
-// Target bucket t = umulhi(key, nt): the fine bucket when nf = 1 (nt = nb),
-// else the coarse bucket (nt = nb1); nt <= 64 either way. A chunk's share of
-// bucket t starts at the bucket's first fine start plus the chunk's offsets
-// in each of its fine buckets. The chunk is processed in rounds of 8K ids:
-// each round is counting-sorted by bucket in LDS and every bucket's part of
-// the round is written as one contiguous run after the previous rounds'.
-constexpr int kRoundIds = 8192;
-constexpr int kRoundBlocks = kRoundIds / 4 / kChunkThreads;  // Philox blocks per thread
-constexpr int kMaxTargets = 64;
-
-struct ScatterSmem {
-  uint32_t key[kRoundIds];
-  int32_t id[kRoundIds];
-  uint32_t cnt[kMaxTargets];
-  uint32_t off[kMaxTargets];   // start of each bucket's run in the round
-  uint32_t base[kMaxTargets];  // next free position of each bucket (global)
-};
-
-__global__ void __launch_bounds__(kChunkThreads)
-stream_scatter(StreamParams p, uint32_t nchunks, const uint32_t* __restrict__ cnt,
-               const uint32_t* __restrict__ start, uint32_t* __restrict__ keys,
-               int32_t* __restrict__ ids) {
-  __shared__ ScatterSmem s;
-  const uint32_t nb = p.nb, nf = p.nf;
-  const uint32_t nt = nf == 1 ? nb : p.nb1;
-  const uint32_t chunk = xcd_logical(blockIdx.x, gridDim.x);
-  if (chunk >= nchunks) return;
-  const uint32_t* off = cnt + (int64_t(blockIdx.y) * nchunks + chunk) * nb;
-  const uint32_t* st = start + int64_t(blockIdx.y) * (nb + 1);
-  for (uint32_t b = threadIdx.x; b < nt; b += blockDim.x) {
-    uint32_t o = 0;
-    for (uint32_t f = b * nf; f < (b + 1) * nf; ++f) o += off[f];
-    s.base[b] = st[b * nf] + o;
-  }
-  const uint32_t e = uint32_t(p.e0) + blockIdx.y;
-  uint32_t* ko = keys + int64_t(blockIdx.y) * p.F;
-  int32_t* io = ids + int64_t(blockIdx.y) * p.F;
-  const int64_t id_chunk = int64_t(chunk) * kChunkIds;
-  for (int64_t r0 = id_chunk; r0 < id_chunk + kChunkIds && r0 < p.F; r0 += kRoundIds) {
-    if (threadIdx.x < nt) s.cnt[threadIdx.x] = 0;
-    __syncthreads();
-    uint32_t w[kRoundBlocks][4], slot[kRoundBlocks][4];
-#pragma unroll
-    for (int it = 0; it < kRoundBlocks; ++it) {
-      const int64_t blk = r0 / 4 + it * kChunkThreads + threadIdx.x;
-      const int64_t id0 = blk * 4;
-      const Philox4 r = philox_block(uint32_t(blk), e, p.seed_lo, p.seed_hi);
-      w[it][0] = r.x; w[it][1] = r.y; w[it][2] = r.z; w[it][3] = r.w;
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (id0 + c < p.F) slot[it][c] = atomicAdd(&s.cnt[__umulhi(w[it][c], nt)], 1u);
+  __shared__ uint32_t tile[64][65];
+  const uint32_t nbw = p.nbw, nch = p.nchunks;
+  const int64_t e = blockIdx.y;
+  const uint32_t b0 = blockIdx.x * 64;
+  const uint32_t tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  uint32_t* ce = cnt + e * int64_t(nch) * nbw;
+  uint32_t* oe = offb + e * int64_t(nbw) * (nch + 1);
+  uint32_t run = 0;  // column threadIdx.x (< 64): running sum of bucket b0 + threadIdx.x
+  for (uint32_t c0 = 0; c0 < nch; c0 += 64) {
+    for (uint32_t y = ty; y < 64; y += 4) {
+      const uint32_t c = c0 + y, b = b0 + tx;
+      tile[y][tx] = (c < nch && b < nbw) ? ce[int64_t(c) * nbw + b] : 0u;
     }
     __syncthreads();
     if (threadIdx.x < 64) {
-      const uint32_t v = threadIdx.x < nt ? s.cnt[threadIdx.x] : 0u;
-      const uint32_t inc = wave_inclusive_scan(v);
-      if (threadIdx.x < nt) s.off[threadIdx.x] = inc - v;
+      for (int y = 0; y < 64; ++y) {
+        const uint32_t v = tile[y][threadIdx.x];
+        tile[y][threadIdx.x] = run;
+        run += v;
+      }
     }
     __syncthreads();
+    for (uint32_t y = ty; y < 64; y += 4) {
+      const uint32_t c = c0 + y, b = b0 + tx;
+      if (c < nch && b < nbw) ce[int64_t(c) * nbw + b] = tile[y][tx];
+      const uint32_t bb = b0 + y, cc = c0 + tx;
+      if (bb < nbw && cc < nch) oe[int64_t(bb) * (nch + 1) + cc] = tile[tx][y];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x < 64 && b0 + threadIdx.x < nbw) {
+    const uint32_t b = b0 + threadIdx.x;
+    oe[int64_t(b) * (nch + 1) + nch] = run;
+    tot[e * nbw + b] = run;
+  }
+}
+
+// -- 3. bucket starts ----------------------------------------------------------
+// wst[e][b]: start of bucket b inside the pass's part of epoch e (its words'
+// position), wst[e][nbw] the part's size; wbase[e]: the part's first
+// position in the epoch (the keys of earlier passes), wpos[e] advanced past
+// the part for the next pass.
+__global__ void __launch_bounds__(1024)
+stream_scan(uint32_t nbw, const uint32_t* __restrict__ tot, uint32_t* __restrict__ wst,
+            uint32_t* __restrict__ wpos, uint32_t* __restrict__ wbase) {
+  __shared__ uint32_t tmp[65];
+  const uint32_t* t = tot + int64_t(blockIdx.x) * nbw;
+  uint32_t* st = wst + int64_t(blockIdx.x) * (nbw + 1);
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < nbw; base += blockDim.x) {
+    const uint32_t b = base + threadIdx.x;
+    const uint32_t v = b < nbw ? t[b] : 0u;
+    uint32_t total;
+    const uint32_t ex = block_exclusive_scan(v, tmp, &total);
+    if (b < nbw) st[b] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0) {
+    st[nbw] = carry;
+    const uint32_t w = wpos[blockIdx.x];
+    wbase[blockIdx.x] = w;
+    wpos[blockIdx.x] = w + carry;
+  }
+}
+
+__global__ void stream_zero(uint32_t* __restrict__ a, uint32_t n) {
+  for (uint32_t x = threadIdx.x; x < n; x += blockDim.x) a[x] = 0;
+}
+
+// -- 4. scatter ------------------------------------------------------------------
+// One workgroup per (chunk, epoch). Per round of kRound ids (the larger the
+// round, the longer each bucket's run and the fewer partly written cache
+// lines: 24,576 ids take 126 KB of LDS, one workgroup per CU, which measured
+// 1.54 ms at ImageNet-22k against 1.82 ms for 12,288-id rounds at two per
+// CU): the pass's keys
+// are counting-sorted by bucket in LDS (16-bit counts, two per word) and
+// written as words, consecutive threads on consecutive positions; the bucket
+// of staged position q is found from a table of the bucket at every 8th
+// position and a short forward walk over the bucket starts.
+__global__ void __launch_bounds__(kThreads)
+stream_scatter(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __restrict__ offc,
+               uint32_t* __restrict__ words) {
+  __shared__ uint32_t stage[kRound];                      // staged words
+  __shared__ uint32_t cntw[kMaxWin / 2 + 1];              // 16-bit counts / starts
+  __shared__ int32_t dl[kMaxWin];                         // run position - start, per bucket
+  __shared__ uint16_t blk[kRound >> kBlkShift];           // bucket at every 8th position
+  __shared__ uint32_t tmp[65];
+  const uint32_t nbw = p.nbw;
+  uint16_t* c16 = reinterpret_cast<uint16_t*>(cntw);      // bucket b at [b]
+  const uint32_t chunk = xcd_logical(blockIdx.x, gridDim.x);
+  if (chunk >= p.nchunks) return;
+  const uint32_t e = uint32_t(p.e0) + blockIdx.y;
+  const uint32_t* st = wst + int64_t(blockIdx.y) * (nbw + 1);
+  const uint32_t* oc = offc + (int64_t(blockIdx.y) * p.nchunks + chunk) * nbw;
+  uint32_t* out = words + int64_t(blockIdx.y) * p.F;
+  for (uint32_t b = threadIdx.x; b < nbw; b += kThreads) dl[b] = int32_t(st[b] + oc[b]);
+  const int64_t id_chunk = int64_t(chunk) * p.C;
+  for (int64_t r0 = id_chunk; r0 < id_chunk + p.C && r0 < p.F; r0 += kRound) {
+    for (uint32_t x = threadIdx.x; x < (nbw + 2) / 2; x += kThreads) cntw[x] = 0;
+    __syncthreads();
+    // per id: its word, and its bucket and slot packed as b << 16 | slot
+    // (b < 4096, slot < kRound), or ~0 when the id is not in this pass
+    uint32_t wd[kRoundBlocks][4], bs[kRoundBlocks][4];
 #pragma unroll
     for (int it = 0; it < kRoundBlocks; ++it) {
-      const int64_t blk = r0 / 4 + it * kChunkThreads + threadIdx.x;
-      const int64_t id0 = blk * 4;
+      const int64_t blk4 = r0 / 4 + it * kThreads + threadIdx.x;
+      const int64_t id0 = blk4 * 4;
+      const Philox4 r = philox_block(uint32_t(blk4), e, p.seed_lo, p.seed_hi);
+      const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        if (id0 + c < p.F) {
-          const uint32_t q = s.off[__umulhi(w[it][c], nt)] + slot[it][c];
-          s.key[q] = w[it][c];
-          s.id[q] = int32_t(id0 + c);
+        const uint32_t b = bucket_of(w[c], p.m) - p.wb0;
+        wd[it][c] = (stored_bits(w[c], p.m, p.cbits) << p.cbits) | uint32_t(id0 + c - id_chunk);
+        bs[it][c] = 0xFFFFFFFFu;
+        if (id0 + c < p.F && b < nbw) {
+          const uint32_t half = (b & 1u) * 16u;
+          bs[it][c] = (b << 16) | ((atomicAdd(&cntw[b >> 1], 1u << half) >> half) & 0xFFFFu);
         }
       }
     }
     __syncthreads();
-    const uint32_t n = uint32_t(p.F - r0 < kRoundIds ? p.F - r0 : kRoundIds);
-    for (uint32_t q = threadIdx.x; q < n; q += kChunkThreads) {
-      const uint32_t k = s.key[q];
-      const uint32_t b = __umulhi(k, nt);
-      const uint32_t dst = s.base[b] + (q - s.off[b]);
-      ko[dst] = k;
-      io[dst] = s.id[q];
-    }
-    __syncthreads();
-    if (threadIdx.x < nt) s.base[threadIdx.x] += s.cnt[threadIdx.x];
-  }
-}
-
-// -- 5. split coarse buckets into fine buckets ---------------------------------
-// A piece of 8K pairs of coarse bucket c per round: counting sort by fine
-// bucket in LDS, then one contiguous run per fine bucket at a position taken
-// from the bucket's cursor.
-constexpr int kSplitThreads = 1024;
-constexpr int kSplitItems = 8;
-constexpr uint32_t kSplitPiece = kSplitThreads * kSplitItems;
-constexpr uint32_t kMaxFine = 256;
-
-struct SplitSmem {
-  uint32_t key[kSplitPiece];
-  int32_t id[kSplitPiece];
-  uint32_t cnt[kMaxFine];
-  uint32_t off[kMaxFine];
-  uint32_t base[kMaxFine];
-  uint32_t tmp[65];
-};
-
-__global__ void __launch_bounds__(kSplitThreads)
-stream_split(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __restrict__ cursor,
-             const uint32_t* __restrict__ keys1, const int32_t* __restrict__ ids1,
-             uint32_t* __restrict__ keys, int32_t* __restrict__ ids) {
-  __shared__ SplitSmem s;
-  const uint32_t nb = p.nb, nf = p.nf;
-  const uint32_t c = blockIdx.y;
-  const int64_t eoff = int64_t(blockIdx.z) * p.F;
-  const uint32_t* st = start + int64_t(blockIdx.z) * (nb + 1);
-  uint32_t* cur = cursor + int64_t(blockIdx.z) * nb;
-  const uint32_t r0 = st[c * nf], r1 = st[(c + 1) * nf];
-  for (uint32_t q0 = r0 + blockIdx.x * kSplitPiece; q0 < r1; q0 += gridDim.x * kSplitPiece) {
-    for (uint32_t f = threadIdx.x; f < nf; f += kSplitThreads) s.cnt[f] = 0;
-    __syncthreads();
-    uint32_t k[kSplitItems], sl[kSplitItems];
-    int32_t id[kSplitItems];
-#pragma unroll
-    for (int r = 0; r < kSplitItems; ++r) {
-      const uint32_t q = q0 + r * kSplitThreads + threadIdx.x;
-      if (q < r1) {
-        k[r] = keys1[eoff + q];
-        id[r] = ids1[eoff + q];
-        sl[r] = atomicAdd(&s.cnt[__umulhi(k[r], nb) - c * nf], 1u);
-      }
-    }
-    __syncthreads();
+    // exclusive scan of the 16-bit counts (nbw <= 4096: at most two words
+    // per thread); c16[nbw] receives the round's total
+    uint32_t total;
     {
-      const uint32_t f = threadIdx.x;
-      const uint32_t v = f < nf ? s.cnt[f] : 0u;
-      uint32_t tot;
-      const uint32_t ex = block_exclusive_scan(v, s.tmp, &tot);
-      if (f < nf) {
-        s.off[f] = ex;
-        if (v) s.base[f] = atomicAdd(&cur[c * nf + f], v);
+      const uint32_t nw = (nbw + 1) / 2;
+      const uint32_t w0 = 2 * threadIdx.x, w1 = w0 + 1;
+      const uint32_t v0 = w0 < nw ? cntw[w0] : 0u, v1 = w1 < nw ? cntw[w1] : 0u;
+      const uint32_t s = (v0 & 0xFFFFu) + (v0 >> 16) + (v1 & 0xFFFFu) + (v1 >> 16);
+      uint32_t ex = block_exclusive_scan(s, tmp, &total);
+      if (w0 < nw) {
+        const uint32_t a = ex, b = a + (v0 & 0xFFFFu);
+        cntw[w0] = a | (b << 16);
+        ex = b + (v0 >> 16);
+      }
+      if (w1 < nw) {
+        const uint32_t a = ex, b = a + (v1 & 0xFFFFu);
+        cntw[w1] = a | (b << 16);
       }
     }
     __syncthreads();
+    if (threadIdx.x == 0) c16[nbw] = uint16_t(total);
 #pragma unroll
-    for (int r = 0; r < kSplitItems; ++r) {
-      const uint32_t q = q0 + r * kSplitThreads + threadIdx.x;
-      if (q < r1) {
-        const uint32_t d = s.off[__umulhi(k[r], nb) - c * nf] + sl[r];
-        s.key[d] = k[r];
-        s.id[d] = id[r];
-      }
+    for (int it = 0; it < kRoundBlocks; ++it)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (bs[it][c] != 0xFFFFFFFFu) stage[c16[bs[it][c] >> 16] + (bs[it][c] & 0xFFFFu)] = wd[it][c];
+    __syncthreads();
+    // bucket of every 8th staged position
+    for (uint32_t b = threadIdx.x; b < nbw; b += kThreads) {
+      const uint32_t a = c16[b], z = c16[b + 1];
+      for (uint32_t k = (a + (1u << kBlkShift) - 1) >> kBlkShift; (k << kBlkShift) < z; ++k)
+        blk[k] = uint16_t(b);
     }
     __syncthreads();
-    const uint32_t n = r1 - q0 < kSplitPiece ? r1 - q0 : kSplitPiece;
-    for (uint32_t q = threadIdx.x; q < n; q += kSplitThreads) {
-      const uint32_t kk = s.key[q];
-      const uint32_t f = __umulhi(kk, nb) - c * nf;
-      const uint32_t dst = s.base[f] + (q - s.off[f]);
-      keys[eoff + dst] = kk;
-      ids[eoff + dst] = s.id[q];
+    for (uint32_t q = threadIdx.x; q < total; q += kThreads) {
+      uint32_t b = blk[q >> kBlkShift];
+      while (c16[b + 1] <= q) ++b;
+      out[uint32_t(dl[b]) + q - c16[b]] = stage[q];
     }
     __syncthreads();
+    for (uint32_t b = threadIdx.x; b < nbw; b += kThreads) dl[b] += int32_t(c16[b + 1] - c16[b]);
+    __syncthreads();  // the counts are read above before the next round clears them
   }
 }
 
-// -- 6. per-bucket sort and shard --------------------------------------------
-// 80 KB: two workgroups per CU. Digit counts and group starts are at most
-// kSortCap (< 2^16), so they are kept as 16-bit halves of 32-bit words, and
-// the scan's scratch lives in the pair array, which is unused until the
-// pairs are placed.
-struct SortSmem {
-  uint2 kv[kSortCap];          // (key, id) pairs; later the sorted ids and the shard stage
-  uint32_t hist[kDigits / 2];  // 16-bit digit counts, then group starts, two per word
-};
-static_assert(kSortCap < 65536, "16-bit digit counts");
-
-__device__ __forceinline__ bool pair_greater(uint32_t ka, int32_t ia, uint32_t kb, int32_t ib) {
+// -- 5. per-bucket sort and shard ------------------------------------------------
+__device__ __forceinline__ bool key_id_greater(uint32_t ka, uint32_t ia, uint32_t kb, uint32_t ib) {
   return ka > kb || (ka == kb && ia > ib);
 }
 
-// In-place bitonic sort of n (key, id) pairs in global memory by one
-// workgroup. Every merge starts with a "flip" comparator, so all comparators
-// point the same way and the virtual padding (+inf beyond n) never moves.
-__device__ void global_bitonic(uint32_t* gk, int32_t* gi, uint32_t n) {
+// In-place bitonic sort of n ids in global memory by one workgroup, by
+// (key, id) with the keys regenerated per comparison. Every merge starts
+// with a "flip" comparator, so all comparators point the same way and the
+// virtual padding (+inf beyond n) never moves.
+__device__ void global_bitonic(int32_t* gi, uint32_t n, uint32_t e, uint32_t slo, uint32_t shi) {
   uint32_t P2 = 1;
   while (P2 < n) P2 <<= 1;
   for (uint32_t k = 2; k <= P2; k <<= 1) {
     for (uint32_t s = k >> 1; s >= 1; s >>= 1) {
       for (uint32_t t = threadIdx.x; t < P2 / 2; t += blockDim.x) {
+        const uint32_t blk = t / s, off = t % s;
         uint32_t i, j;
         if (s == (k >> 1)) {
-          const uint32_t blk = t / s, off = t % s;
           i = blk * k + off;
           j = blk * k + k - 1 - off;
         } else {
-          const uint32_t blk = t / s, off = t % s;
           i = blk * 2 * s + off;
           j = i + s;
         }
         if (j < n) {
-          const uint32_t ka = gk[i], kb = gk[j];
-          const int32_t ia = gi[i], ib = gi[j];
-          if (pair_greater(ka, ia, kb, ib)) {
-            gk[i] = kb; gi[i] = ib;
-            gk[j] = ka; gi[j] = ia;
+          const uint32_t ia = uint32_t(gi[i]), ib = uint32_t(gi[j]);
+          if (key_id_greater(philox_key(ia, e, slo, shi), ia, philox_key(ib, e, slo, shi), ib)) {
+            gi[i] = int32_t(ib);
+            gi[j] = int32_t(ia);
           }
         }
       }
+      __threadfence_block();
       __syncthreads();
     }
   }
@@ -363,130 +341,251 @@ __device__ __forceinline__ int64_t row_offset(const StreamParams& p, uint32_t i,
   return int64_t(i) * p.M_max + (e - p.e_first) * Li;
 }
 
-__global__ void __launch_bounds__(kSortThreads)
-stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __restrict__ keys,
-            int32_t* __restrict__ ids, int32_t* __restrict__ R) {
-  __shared__ SortSmem s;
-  const uint32_t nb = p.nb;
+// Largest c with ob[c] <= q (the run holding position q; empty runs share
+// their start with the next run, which the largest index skips).
+__device__ __forceinline__ uint32_t run_search(const uint32_t* ob, uint32_t nch, uint32_t q) {
+  uint32_t lo = 0, hi = nch;  // ob[lo] <= q < ob[hi] (ob[nch] = n > q)
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (ob[mid] <= q) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// A bucket larger than the LDS capacity: its words decoded into ids in
+// place (run table in LDS), sorted by (key, id) in global memory, sharded.
+__device__ void sort_in_global(const StreamParams& p, const uint32_t* ob, uint32_t* gw, uint32_t n,
+                               uint32_t e, uint32_t pos0, int64_t pend64, int32_t* __restrict__ R) {
+  const uint32_t lmask = (1u << p.cbits) - 1u;
+  for (uint32_t q = threadIdx.x; q < n; q += kThreads) {
+    const uint32_t w = gw[q];
+    const uint32_t c = run_search(ob, p.nchunks, q);
+    gw[q] = c * p.C + (w & lmask);
+  }
+  __threadfence_block();
+  __syncthreads();
+  int32_t* gi = reinterpret_cast<int32_t*>(gw);
+  global_bitonic(gi, n, e, p.seed_lo, p.seed_hi);
+  const uint32_t N = uint32_t(p.N);
+  for (int64_t q = threadIdx.x; int64_t(pos0) + q < pend64; q += kThreads) {
+    const uint32_t pp = pos0 + uint32_t(q);
+    const uint32_t i = pp % N, j = pp / N;
+    R[row_offset(p, i, e) + j] = gi[q];
+  }
+}
+
+// LDS: 64 KB of 8-byte entries (kb << 32 | id), later kb and the ids by
+// position (kb then gives way to full keys and the shard stage), and 16 KB
+// that first hold the run table (bucket-major run starts, the run at every
+// 8th position), then the 16-bit digit counts, then the list of tied runs:
+// 80 KB, two workgroups per CU.
+constexpr int kSortDigitBits = 13;
+constexpr int kSortDigits = 1 << kSortDigitBits;
+constexpr int kCountWords = kSortDigits / 2;
+static_assert(kMaxChunks + 1 + (kSortCap >> kBlkShift) / 2 <= kCountWords,
+              "the run table fits the digit counts' space");
+
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(8)))
+stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __restrict__ wbase,
+            const uint32_t* __restrict__ offb, uint32_t* __restrict__ words, int32_t* __restrict__ R) {
+  __shared__ uint64_t kv[kSortCap];
+  __shared__ uint32_t cw[kCountWords];
+  uint32_t* ob = cw;                                                 // [nchunks + 1]
+  uint16_t* blk = reinterpret_cast<uint16_t*>(cw + p.nchunks + 1);  // [kSortCap >> kBlkShift]
+  const uint16_t* h16 = reinterpret_cast<const uint16_t*>(cw);      // digit d at [d]
+  const uint32_t nbw = p.nbw, nch = p.nchunks;
   const uint32_t b = xcd_logical(blockIdx.x, gridDim.x);
-  if (b >= nb) return;
-  const int64_t e = int64_t(p.e0) + blockIdx.y;
-  const uint32_t* st = start + int64_t(blockIdx.y) * (nb + 1);
+  if (b >= nbw) return;
+  const uint32_t e = uint32_t(p.e0) + blockIdx.y;
+  const uint32_t* st = wst + int64_t(blockIdx.y) * (nbw + 1);
   const uint32_t lo = st[b];
   const uint32_t n = st[b + 1] - lo;
   if (n == 0) return;
-  uint32_t* gk = keys + int64_t(blockIdx.y) * p.F + lo;
-  int32_t* gi = ids + int64_t(blockIdx.y) * p.F + lo;
+  const uint32_t pos0 = wbase[blockIdx.y] + lo;  // epoch position of the bucket's first element
+  uint32_t* gw = words + int64_t(blockIdx.y) * p.F + lo;
   const uint32_t N = uint32_t(p.N);
-  const int64_t pend64 = int64_t(lo) + n < p.P ? int64_t(lo) + n : p.P;
-
-  if (n > uint32_t(p.cap)) {
-    global_bitonic(gk, gi, n);
-    for (int64_t q = threadIdx.x; int64_t(lo) + q < pend64; q += blockDim.x) {
-      const uint32_t pp = lo + uint32_t(q);
-      const uint32_t i = pp % N, j = pp / N;
-      R[row_offset(p, i, e) + j] = gi[q];
+  const int64_t pend64 = int64_t(pos0) + n < p.P ? int64_t(pos0) + n : p.P;
+  const uint32_t lmask = (1u << p.cbits) - 1u;
+  const uint32_t* obg = offb + (int64_t(blockIdx.y) * nbw + b) * (nch + 1);
+  const bool fast = n <= uint32_t(p.cap);
+  // the words are requested before the run table, so both round trips overlap
+  uint32_t kb[kItems], id[kItems];
+  if (fast) {
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+      const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
+      kb[r] = q < n ? gw[q] : 0u;
     }
+  }
+  for (uint32_t c = threadIdx.x; c <= nch; c += kThreads) ob[c] = obg[c];
+  __syncthreads();
+  if (!fast) {
+    sort_in_global(p, ob, gw, n, e, pos0, pend64, R);
     return;
   }
 
-  const uint32_t key_lo = uint32_t(((uint64_t(b) << 32) + nb - 1) / nb);
-  const int db = p.sort_bits < kDigitBits ? p.sort_bits : kDigitBits;
-  const int dshift = p.sort_bits - db;
-  for (int x = threadIdx.x; x < kDigits / 2; x += kSortThreads) s.hist[x] = 0;
-  const uint16_t* h16 = reinterpret_cast<const uint16_t*>(s.hist);  // digit d at [d]
+  // run at every 8th position of the bucket
+  for (uint32_t c = threadIdx.x; c < nch; c += kThreads) {
+    const uint32_t a = ob[c], z = ob[c + 1];
+    for (uint32_t k = (a + (1u << kBlkShift) - 1) >> kBlkShift; (k << kBlkShift) < z; ++k)
+      blk[k] = uint16_t(c);
+  }
   __syncthreads();
-  // counting sort by the top bits of the key inside the bucket
-  uint32_t k[kItems], slot[kItems];
-  int32_t id[kItems];
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
+    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
     if (q < n) {
-      k[r] = gk[q] - key_lo;
-      id[r] = gi[q];
+      uint32_t c = blk[q >> kBlkShift];
+      c += ob[c + 1] <= q;  // most positions are at most two runs on
+      c += ob[c + 1] <= q;
+      while (ob[c + 1] <= q) ++c;
+      id[r] = c * p.C + (kb[r] & lmask);
+      kb[r] >>= p.cbits;
     }
   }
+  __syncthreads();  // the run table is no longer needed: its space holds the digit counts
+  const uint32_t kbits = 32u - p.cbits;
+  const uint32_t dbits = kbits < uint32_t(kSortDigitBits) ? kbits : uint32_t(kSortDigitBits);
+  const uint32_t dshift = kbits - dbits;
+  const uint32_t ndig = 1u << dbits;
+  for (int x = threadIdx.x; x < kCountWords; x += kThreads) cw[x] = 0;
+  __syncthreads();
+  uint32_t pos[kItems];
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
+    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
     if (q < n) {
-      const uint32_t d = k[r] >> dshift;
+      const uint32_t d = kb[r] >> dshift;
       const uint32_t half = (d & 1u) * 16u;
-      slot[r] = (atomicAdd(&s.hist[d >> 1], 1u << half) >> half) & 0xFFFFu;
+      pos[r] = (atomicAdd(&cw[d >> 1], 1u << half) >> half) & 0xFFFFu;
     }
   }
   __syncthreads();
   {
-    constexpr int kPerW = kDigits / 2 / kSortThreads;  // count words per thread
+    constexpr int kPerW = kCountWords / kThreads;  // count words per thread
     uint32_t v[kPerW];
     uint32_t sum = 0;
 #pragma unroll
     for (int j = 0; j < kPerW; ++j) {
-      v[j] = s.hist[threadIdx.x * kPerW + j];
+      v[j] = cw[threadIdx.x * kPerW + j];
       sum += (v[j] & 0xFFFFu) + (v[j] >> 16);
     }
     uint32_t total;
-    uint32_t ex = block_exclusive_scan(sum, reinterpret_cast<uint32_t*>(s.kv), &total);
+    uint32_t ex = block_exclusive_scan(sum, reinterpret_cast<uint32_t*>(kv), &total);
 #pragma unroll
     for (int j = 0; j < kPerW; ++j) {
       const uint32_t lo16 = ex;
       ex += v[j] & 0xFFFFu;
-      s.hist[threadIdx.x * kPerW + j] = lo16 | (ex << 16);
+      cw[threadIdx.x * kPerW + j] = lo16 | (ex << 16);
       ex += v[j] >> 16;
     }
   }
   __syncthreads();
-  uint32_t dst[kItems];
+  uint32_t* kbs = reinterpret_cast<uint32_t*>(kv);  // [kSortCap] kb by counting-sort slot
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
+    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
     if (q < n) {
-      dst[r] = h16[k[r] >> dshift] + slot[r];
-      s.kv[dst[r]] = make_uint2(k[r], uint32_t(id[r]));
+      pos[r] += h16[kb[r] >> dshift];
+      kbs[pos[r]] = kb[r];
     }
   }
   __syncthreads();
-  // Inside its digit group (a few pairs), every pair's final position is
-  // the group start plus the number of group pairs ordered before it by
-  // (key, id); the loads of one pair's scan do not depend on each other.
+  // Inside its digit group (about two entries), an entry's place in kb
+  // order is the group start plus the group entries below it, entries of
+  // equal kb taking their slot order (their runs are re-sorted by full key
+  // and id below). The first kGroupLoads members are loaded unconditionally
+  // (the loads do not depend on each other and no lane waits for another's
+  // group size); a larger group walks the rest.
+  constexpr uint32_t kGroupLoads = 4;
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
+    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
     if (q < n) {
-      const uint32_t d = k[r] >> dshift;
+      const uint32_t d = kb[r] >> dshift;
       const uint32_t a0 = h16[d];
-      const uint32_t a1 = d + 1 < uint32_t(kDigits) ? h16[d + 1] : n;
-      uint32_t rank = 0;
-      for (uint32_t v = a0; v < a1; ++v) {
-        const uint2 o = s.kv[v];
-        rank += pair_greater(k[r], id[r], o.x, int32_t(o.y));
+      const uint32_t a1 = d + 1 < ndig ? h16[d + 1] : n;
+      const uint32_t me = pos[r], k = kb[r];
+      uint32_t o[kGroupLoads];
+#pragma unroll
+      for (uint32_t j = 0; j < kGroupLoads; ++j) {
+        const uint32_t v = a0 + j;
+        o[j] = kbs[v < uint32_t(kSortCap) ? v : uint32_t(kSortCap) - 1];
       }
-      dst[r] = a0 + rank;
+      uint32_t below = 0;
+#pragma unroll
+      for (uint32_t j = 0; j < kGroupLoads; ++j)
+        below += (a0 + j < a1) & ((o[j] < k) | ((o[j] == k) & (a0 + j < me)));
+      for (uint32_t v = a0 + kGroupLoads; v < a1; ++v) {
+        const uint32_t x = kbs[v];
+        below += (x < k) | ((x == k) & (v < me));
+      }
+      pos[r] = a0 + below;
+    }
+  }
+  __syncthreads();  // the slots and the digit counts are no longer needed
+  // kb and ids by (kb, id) position, then runs of equal kb (a few percent of
+  // the entries) re-sorted by (full key, id), one thread per run.
+  uint32_t* kbp = reinterpret_cast<uint32_t*>(kv);  // [kSortCap] kb, later full keys, later the shard stage
+  uint32_t* sorted = kbp + kSortCap;                // [kSortCap] ids in (key, id) order
+  uint16_t* runs = reinterpret_cast<uint16_t*>(cw); // [0..1]: run count (32-bit), then run starts
+  uint32_t* nruns = cw;
+  if (threadIdx.x == 0) *nruns = 0;
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
+    if (q < n) {
+      kbp[pos[r]] = kb[r];
+      sorted[pos[r]] = id[r];
     }
   }
   __syncthreads();
-  int32_t* sorted = reinterpret_cast<int32_t*>(s.kv);  // ids in (key, id) order
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kSortThreads) + threadIdx.x;
-    if (q < n) sorted[dst[r]] = id[r];
+    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
+    if (q + 1 < n) {
+      const uint32_t k0 = kbp[q];
+      if (k0 == kbp[q + 1] && (q == 0 || kbp[q - 1] != k0)) runs[2 + atomicAdd(nruns, 1u)] = uint16_t(q);
+    }
+  }
+  __syncthreads();
+  {
+    const uint32_t nr = *nruns;  // at most n / 2 runs: the list fits
+    for (uint32_t t = threadIdx.x; t < nr; t += kThreads) {
+      const uint32_t a0 = runs[2 + t];
+      const uint32_t kk = kbp[a0];
+      uint32_t a1 = a0 + 2;
+      while (a1 < n && kbp[a1] == kk) ++a1;
+      for (uint32_t x = a0; x < a1; ++x) kbp[x] = philox_key(sorted[x], e, p.seed_lo, p.seed_hi);
+      for (uint32_t x = a0 + 1; x < a1; ++x) {
+        const uint32_t fx = kbp[x], ix = sorted[x];
+        uint32_t y = x;
+        while (y > a0 && key_id_greater(kbp[y - 1], sorted[y - 1], fx, ix)) {
+          kbp[y] = kbp[y - 1];
+          sorted[y] = sorted[y - 1];
+          --y;
+        }
+        kbp[y] = fx;
+        sorted[y] = ix;
+      }
+    }
   }
   __syncthreads();
 
-  if (pend64 <= int64_t(lo)) return;
+  if (pend64 <= int64_t(pos0)) return;
   const uint32_t pend = uint32_t(pend64);
-  const uint32_t j0 = lo / N, j1 = (pend - 1) / N;
+  const uint32_t j0 = pos0 / N, j1 = (pend - 1) / N;
   const uint32_t nj = j1 - j0 + 1;
   const uint32_t Np = (N & 1u) ? N : N + 1u;  // odd row pitch: conflict-free columns
-  // (j, i) of position lo + threadIdx.x, stepped by kSortThreads positions
-  // per iteration without dividing
-  const uint32_t step_i = kSortThreads % N, step_j = kSortThreads / N;
-  uint32_t ci = (lo + threadIdx.x) % N, cj = (lo + threadIdx.x) / N;
+  // (j, i) of position pos0 + threadIdx.x, stepped by kThreads positions per
+  // iteration without dividing
+  const uint32_t step_i = kThreads % N, step_j = kThreads / N;
+  uint32_t ci = (pos0 + threadIdx.x) % N, cj = (pos0 + threadIdx.x) / N;
   if (uint64_t(nj) * Np <= uint64_t(kSortCap)) {
-    uint32_t* stage = reinterpret_cast<uint32_t*>(s.kv) + kSortCap;
-    for (uint32_t q = threadIdx.x; lo + q < pend; q += kSortThreads) {
-      stage[(cj - j0) * Np + ci] = uint32_t(sorted[q]);
+    uint32_t* stage = kbp;
+    for (uint32_t q = threadIdx.x; pos0 + q < pend; q += kThreads) {
+      stage[(cj - j0) * Np + ci] = sorted[q];
       ci += step_i;
       cj += step_j;
       if (ci >= N) {
@@ -496,28 +595,31 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ start, uint32_t* __rest
     }
     __syncthreads();
     // t -> (row i, column jj) with consecutive t on consecutive columns of a
-    // row; t < 2^13, so the float reciprocal gives t / nj up to one step
+    // row: one division per thread, then stepped by kThreads per iteration
     const uint32_t total = nj * N;
-    const float inv_nj = 1.0f / float(nj);
+    const uint32_t si = kThreads / nj, sj = kThreads % nj;
     auto write = [&](auto row) {
-      for (uint32_t t = threadIdx.x; t < total; t += kSortThreads) {
-        uint32_t i = uint32_t(float(t) * inv_nj);
-        if (i * nj > t) --i;
-        else if ((i + 1) * nj <= t) ++i;
-        const uint32_t jj = t - i * nj;
+      uint32_t i = threadIdx.x / nj, jj = threadIdx.x % nj;
+      for (uint32_t t = threadIdx.x; t < total; t += kThreads) {
         const uint32_t pp = (j0 + jj) * N + i;
-        if (pp >= lo && pp < pend) row(i)[jj] = int32_t(stage[jj * Np + i]);
+        if (pp >= pos0 && pp < pend) row(i)[jj] = int32_t(stage[jj * Np + i]);
+        i += si;
+        jj += sj;
+        if (jj >= nj) {
+          jj -= nj;
+          ++i;
+        }
       }
     };
     if (p.drop_last) {  // every row holds L reads per epoch: one offset for all rows
-      int32_t* const Re = R + (e - p.e_first) * p.L + j0;
+      int32_t* const Re = R + (int64_t(e) - p.e_first) * p.L + j0;
       write([&](uint32_t i) { return Re + int64_t(i) * p.M_max; });
     } else {
       write([&](uint32_t i) { return R + row_offset(p, i, e) + j0; });
     }
   } else {
-    for (uint32_t q = threadIdx.x; lo + q < pend; q += kSortThreads) {
-      R[row_offset(p, ci, e) + cj] = sorted[q];
+    for (uint32_t q = threadIdx.x; pos0 + q < pend; q += kThreads) {
+      R[row_offset(p, ci, e) + cj] = int32_t(sorted[q]);
       ci += step_i;
       cj += step_j;
       if (ci >= N) {
@@ -557,77 +659,72 @@ int streams_impl(const nopfs_job* job, int32_t* R, hipStream_t st, int32_t e_beg
 
   int64_t cap = kSortCap;
   if (debug_value(1) > 0 && debug_value(1) < cap) cap = debug_value(1);
-  int64_t nb64 = ceil_div(s.F, cap * 3 / 4 > 0 ? cap * 3 / 4 : 1);
-  if (nb64 < 1) nb64 = 1;
-  if (nb64 > int64_t(kMaxBuckets)) nb64 = kMaxBuckets;
-  // coarse buckets: at most 64 per epoch, nf fine buckets each
-  const uint32_t nb1 = uint32_t(nb64 < 64 ? nb64 : 64);
-  const uint32_t nf = uint32_t(ceil_div(nb64, nb1));
-  const uint32_t nb = nb1 * nf;
-  const uint64_t width = ((uint64_t(1) << 32) + nb - 1) / nb;
-  int bits = 0;
-  while ((uint64_t(1) << bits) < width) ++bits;
+  // 2^m buckets per epoch, the fewest with a mean of at most kMeanBucket
+  uint32_t m = 0;
+  while (m < 31 && (s.F >> m) > kMeanBucket) ++m;
+  const uint32_t nb = 1u << m;
+  const uint32_t nbw = nb < kMaxWin ? nb : kMaxWin;
+  // chunks: multiples of a scatter round, at most kMaxChunks per epoch
+  int64_t C = int64_t(kRound) * kChunkRounds;
+  while (ceil_div(s.F, C) > int64_t(kMaxChunks)) C *= 2;
+  uint32_t cbits = 0;
+  while ((int64_t(1) << cbits) < C) ++cbits;
+  const uint32_t nchunks = uint32_t(ceil_div(s.F, C));
 
   StreamParams p;
   p.F = s.F; p.N = s.N; p.B = s.B; p.P = s.P; p.L = s.L; p.M_max = s.M_max;
   p.drop_last = s.drop_last;
   p.seed_lo = uint32_t(s.seed);
   p.seed_hi = uint32_t(s.seed >> 32);
-  p.nb = nb;
-  p.nb1 = nb1;
-  p.nf = nf;
-  p.sort_bits = bits;
+  p.m = m;
+  p.nbw = nbw;
+  p.C = uint32_t(C);
+  p.cbits = cbits;
+  p.nchunks = nchunks;
   p.cap = int32_t(cap);
   p.e_first = e_begin;
 
-  // epochs per batch: the pair arrays of a batch stay under ~16 GB of scratch
+  // epochs per batch: the words of a batch stay under ~16 GB of scratch
   const int64_t budget = int64_t(16) << 30;
-  int64_t EB = budget / ((nf > 1 ? 16 : 8) * s.F);
+  int64_t EB = budget / (4 * s.F);
   if (EB < 1) EB = 1;
   if (EB > s.E) EB = s.E;
 
-  const uint32_t nchunks = uint32_t(ceil_div(s.F, kChunkIds));
   Scratch scr(st);
-  uint32_t *keys, *keys1 = nullptr, *cnt, *tot, *start, *cursor;
-  int32_t *ids, *ids1 = nullptr;
-  if ((rc = scr.alloc_n(&keys, size_t(EB * s.F)))) return rc;
-  if ((rc = scr.alloc_n(&ids, size_t(EB * s.F)))) return rc;
-  if (nf > 1) {
-    if ((rc = scr.alloc_n(&keys1, size_t(EB * s.F)))) return rc;
-    if ((rc = scr.alloc_n(&ids1, size_t(EB * s.F)))) return rc;
-  }
-  if ((rc = scr.alloc_n(&cnt, size_t(EB) * nchunks * nb))) return rc;
-  if ((rc = scr.alloc_n(&tot, size_t(EB * nb)))) return rc;
-  if ((rc = scr.alloc_n(&start, size_t(EB * (nb + 1))))) return rc;
-  if ((rc = scr.alloc_n(&cursor, size_t(EB * nb)))) return rc;
-  // pieces per coarse bucket for the split: about 1.25x the mean size
-  const uint32_t pieces = uint32_t(ceil_div(ceil_div(s.F, nb1) * 5 / 4, kSplitPiece));
+  uint32_t *words, *cnt, *offb, *tot, *wst, *wpos, *wbase;
+  if ((rc = scr.alloc_n(&words, size_t(EB * s.F)))) return rc;
+  if ((rc = scr.alloc_n(&cnt, size_t(EB) * nchunks * nbw))) return rc;
+  if ((rc = scr.alloc_n(&offb, size_t(EB) * nbw * (nchunks + 1)))) return rc;
+  if ((rc = scr.alloc_n(&tot, size_t(EB) * nbw))) return rc;
+  if ((rc = scr.alloc_n(&wst, size_t(EB) * (nbw + 1)))) return rc;
+  if ((rc = scr.alloc_n(&wpos, size_t(EB)))) return rc;
+  if ((rc = scr.alloc_n(&wbase, size_t(EB)))) return rc;
+
 
   for (int64_t e0 = 0; e0 < s.E; e0 += EB) {
     const uint32_t eb = uint32_t(e0 + EB <= s.E ? EB : s.E - e0);
     p.e0 = int32_t(e_begin + e0);
-    if ((rc = launch("stream_count", stream_count, dim3(nchunks, eb), dim3(kChunkThreads),
-                     size_t(nb) * 4, st, p, nchunks, cnt)))
-      return rc;
-    if ((rc = launch("stream_offsets", stream_offsets, dim3(uint32_t(ceil_div(nb, 256)), eb),
-                     dim3(256), 0, st, nb, nchunks, cnt, tot)))
-      return rc;
-    if ((rc = launch("stream_scan", stream_scan, dim3(eb), dim3(1024), 0, st, nb,
-                     (const uint32_t*)tot, start, cursor)))
-      return rc;
-    if ((rc = launch("stream_scatter", stream_scatter, dim3(xcd_padded(nchunks), eb),
-                     dim3(kChunkThreads), 0, st, p, nchunks, (const uint32_t*)cnt,
-                     (const uint32_t*)start, nf > 1 ? keys1 : keys, nf > 1 ? ids1 : ids)))
-      return rc;
-    if (nf > 1) {
-      if ((rc = launch("stream_split", stream_split, dim3(pieces, nb1, eb), dim3(kSplitThreads),
-                       0, st, p, (const uint32_t*)start, cursor,
-                       (const uint32_t*)keys1, (const int32_t*)ids1, keys, ids)))
+    if ((rc = launch("stream_zero", stream_zero, dim3(1), dim3(256), 0, st, wpos, eb))) return rc;
+    for (uint32_t wb0 = 0; wb0 < nb; wb0 += nbw) {
+      p.wb0 = wb0;
+      if ((rc = launch("stream_count", stream_count, dim3(nchunks, eb), dim3(kThreads),
+                       size_t(nbw) * 4, st, p, cnt)))
+        return rc;
+      if ((rc = launch("stream_offsets", stream_offsets, dim3(uint32_t(ceil_div(nbw, 64)), eb),
+                       dim3(256), 0, st, p, cnt, offb, tot)))
+        return rc;
+      if ((rc = launch("stream_scan", stream_scan, dim3(eb), dim3(1024), 0, st, nbw,
+                       (const uint32_t*)tot, wst, wpos, wbase)))
+        return rc;
+      if ((rc = launch("stream_scatter", stream_scatter, dim3(xcd_padded(nchunks), eb),
+                       dim3(kThreads), 0, st, p, (const uint32_t*)wst,
+                       (const uint32_t*)cnt, words)))
+        return rc;
+      if ((rc = launch("stream_sort", stream_sort, dim3(xcd_padded(nbw), eb), dim3(kThreads),
+                       0, st, p, (const uint32_t*)wst, (const uint32_t*)wbase,
+                       (const uint32_t*)offb, words, R)))
         return rc;
     }
-    if ((rc = launch("stream_sort", stream_sort, dim3(xcd_padded(nb), eb), dim3(kSortThreads), 0, st,
-                     p, (const uint32_t*)start, keys, ids, R)))
-      return rc;
   }
   if (!s.drop_last && s.F % s.N != 0) {
     if ((rc = launch("stream_pad", stream_pad, dim3(uint32_t(s.N)), dim3(64), 0, st, p, R))) return rc;
