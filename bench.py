@@ -93,7 +93,7 @@ def schedule_algorithmic_bytes(job, M, M_w):
     NF = job.N * job.F
     NM = job.N * M
     prefetch = {"seg_partition": 4 * A, "pf_tile": NF, "pf_write": 4 * NM}
-    staging = {"seg_partition": 4 * A, "st_tile": 8 * job.F, "st_fill": 4 * NM}
+    staging = {"seg_partition": 4 * A, "st_gather": 8 * job.F, "st_fill": 4 * NM}
     return prefetch, staging
 
 

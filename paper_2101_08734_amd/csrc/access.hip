@@ -43,7 +43,7 @@ namespace {
 #define NOPFS_STATS_WS 13
 #endif
 #ifndef NOPFS_NEXT_THREADS
-#define NOPFS_NEXT_THREADS 256
+#define NOPFS_NEXT_THREADS 512
 #endif
 #ifndef NOPFS_NEXT_ENT
 #define NOPFS_NEXT_ENT 2048
@@ -671,6 +671,7 @@ SegParams seg_params(const Shape& s, int ws) {
   p.nsc = int32_t(ceil_div(s.L, kSC));
   if (p.nsc < 1) p.nsc = 1;
   p.ent_cap = kNextEnt;
+  p.emul = 1;
   return p;
 }
 

@@ -144,14 +144,31 @@ __device__ inline uint32_t wave_inclusive_scan(uint32_t v) {
   return v;
 }
 
+// One DPP move of a 64-bit value (both halves with the same control); lanes
+// with no source, or in rows outside RowMask, receive 0.
+template <int Ctrl, int RowMask>
+__device__ __forceinline__ uint64_t dpp_move64(uint64_t v) {
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, uint32_t(v), Ctrl, RowMask, 0xf, false);
+  const uint32_t hi = __builtin_amdgcn_update_dpp(0u, uint32_t(v >> 32), Ctrl, RowMask, 0xf, false);
+  return (uint64_t(hi) << 32) | lo;
+}
+
+// The 64-bit form of wave_inclusive_scan, same steps (all lanes active).
 __device__ inline uint64_t wave_inclusive_scan64(uint64_t v) {
-  const int lane = __lane_id();
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    uint64_t o = __shfl_up(v, d, 64);
-    if (lane >= d) v += o;
-  }
+  v += dpp_move64<0x111, 0xf>(v);  // row_shr:1
+  v += dpp_move64<0x112, 0xf>(v);  // row_shr:2
+  v += dpp_move64<0x114, 0xf>(v);  // row_shr:4
+  v += dpp_move64<0x118, 0xf>(v);  // row_shr:8
+  v += dpp_move64<0x142, 0xa>(v);  // row_bcast:15, rows 1 and 3
+  v += dpp_move64<0x143, 0xc>(v);  // row_bcast:31, rows 2 and 3
   return v;
+}
+
+// A lane's 64-bit value, read by every lane (the lane index is uniform).
+__device__ __forceinline__ uint64_t read_lane64(uint64_t v, int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane(int(uint32_t(v)), lane);
+  const uint32_t hi = __builtin_amdgcn_readlane(int(uint32_t(v >> 32)), lane);
+  return (uint64_t(hi) << 32) | lo;
 }
 
 // Exclusive scan over the whole workgroup (blockDim.x a multiple of 64, at

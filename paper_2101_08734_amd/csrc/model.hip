@@ -168,7 +168,19 @@ fm_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict
   for (int64_t w0 = k0; w0 < kend; w0 += kFmWin) {
     const uint32_t wl = uint32_t(kend - w0 < kFmWin ? kend - w0 : kFmWin);
     const uint32_t xoff = uint32_t(w0 - k0);
-    for (uint32_t x = threadIdx.x; x < wl; x += kFmTileThreads) sz[x] = szb[w0 + x];
+    for (uint32_t x0 = 0; x0 < wl; x0 += 8 * kFmTileThreads) {  // eight loads in flight
+      uint64_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t x = x0 + u * kFmTileThreads + threadIdx.x;
+        v[u] = szb[w0 + (x < wl ? x : 0)];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint32_t x = x0 + u * kFmTileThreads + threadIdx.x;
+        if (x < wl) sz[x] = v[u];
+      }
+    }
     __syncthreads();
     for (int64_t pr = threadIdx.x; pr < gw * runs; pr += kFmTileThreads) {
       const int64_t i = i0 + pr / runs;
@@ -184,11 +196,16 @@ fm_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict
       for (uint32_t q = ra; q < rb; q += kRunBatch) {
         uint32_t x[kRunBatch];
         int32_t own[kRunBatch];
+        // unconditional loads (clamped indices), so that each batch waits once
+#pragma unroll
+        for (int u = 0; u < kRunBatch; ++u) x[u] = src[q + u < rb ? q + u : q];
 #pragma unroll
         for (int u = 0; u < kRunBatch; ++u)
-          x[u] = q + u < rb ? (src[q + u] >> kScShift) - xoff : 0xFFFFFFFFu;
+          x[u] = q + u < rb ? (x[u] >> kScShift) - xoff : 0xFFFFFFFFu;
 #pragma unroll
-        for (int u = 0; u < kRunBatch; ++u) own[u] = x[u] < wl ? trow[x[u]] : -1;
+        for (int u = 0; u < kRunBatch; ++u) own[u] = trow[x[u] < wl ? x[u] : 0u];
+#pragma unroll
+        for (int u = 0; u < kRunBatch; ++u) own[u] = x[u] < wl ? own[u] : -1;
 #pragma unroll
         for (int u = 0; u < kRunBatch; ++u)
           if (x[u] < wl) {

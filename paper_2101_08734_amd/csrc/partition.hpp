@@ -26,10 +26,13 @@ struct SegParams {
   uint32_t nbk;   // windows per worker: ceil(F / W)
   int32_t nsc;    // sub-chunks per (worker, epoch) segment
   int32_t ent_cap;  // next_tile fast-path capacity (reads)
+  int32_t emul;   // epochs per segment: 1, or E when a row is one segment (E = 1)
 };
 
+// Reads of one segment of worker i (an epoch, or the whole row when the
+// epochs are folded into one segment).
 __device__ __forceinline__ int64_t seg_len(const SegParams& p, int64_t i) {
-  return p.drop_last ? p.L : epoch_len(p.F, p.N, p.B, 0, i);
+  return int64_t(p.emul) * (p.drop_last ? p.L : epoch_len(p.F, p.N, p.B, 0, i));
 }
 
 __device__ __forceinline__ int64_t orow(const SegParams& p, int64_t i, int64_t e, int64_t sc) {

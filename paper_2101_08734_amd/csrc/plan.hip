@@ -515,7 +515,18 @@ plan_resolve(PlanArgs a, const uint64_t* __restrict__ H, const CandRec* __restri
   constexpr int kPerT = kCandMax / kResolveThreads;
   static_assert(kCandMax % kResolveThreads == 0, "candidates per thread");
   const int64_t last_bin = n > 0 ? int64_t(s.key[n - 1] >> 32) : -1;
-  uint64_t gap[kPerT];
+  uint64_t gap[kPerT], hb[kPerT], hp[kPerT], sk[kPerT];
+  // loads first, unconditional (clamped to entry 0), so they are in flight together
+#pragma unroll
+  for (int q = 0; q < kPerT; ++q) {
+    const int32_t x = int32_t(threadIdx.x) + q * kResolveThreads;
+    const bool in = x < n;
+    const int64_t b = in ? int64_t(s.key[x] >> 32) : 0;
+    const int64_t pb = in && x > 0 ? int64_t(s.key[x - 1] >> 32) : -1;
+    hb[q] = Hi[b];
+    hp[q] = Hi[pb + 1];
+    sk[q] = uint64_t(sizes[in ? s.k[x] : 0u]);
+  }
 #pragma unroll
   for (int q = 0; q < kPerT; ++q) {
     const int32_t x = int32_t(threadIdx.x) + q * kResolveThreads;
@@ -523,8 +534,8 @@ plan_resolve(PlanArgs a, const uint64_t* __restrict__ H, const CandRec* __restri
     if (x < n) {
       const int64_t b = int64_t(s.key[x] >> 32);
       const int64_t pb = x > 0 ? int64_t(s.key[x - 1] >> 32) : -1;
-      if (b != pb) gap[q] = Hi[b] - (pb < 0 ? 0ull : Hi[pb + 1]);
-      s.sz[x] = uint64_t(sizes[s.k[x]]);
+      if (b != pb) gap[q] = hb[q] - (pb < 0 ? 0ull : hp[q]);
+      s.sz[x] = sk[q];
     }
   }
   __syncthreads();  // every key is read before any is replaced

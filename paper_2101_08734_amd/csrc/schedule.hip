@@ -1,13 +1,16 @@
 // nopfs_prefetch_order and nopfs_staging_schedule: what the Design section
 // derives from the streams and the placement for a worker's prefetchers.
 //
-// Both need R grouped by sample (a first read, a size) and then results in
-// stream order, so both run on the per-worker partition of R by sample
-// window (the one the counting pass uses, windows of 2^13 samples): a tile
-// per window does the per-sample work in LDS and writes one value per read
-// in partitioned order; a pass per sub-chunk of 2^14 reads puts the values
-// back in stream order through LDS. No pass scatters into or gathers from
-// HBM at random.
+// Both calls need a per-sample value for every read (a first read, a size)
+// and then results in stream order, so both run on a partition of R by
+// sample window (counting sort of each sub-chunk of 2^14 reads by window, as
+// in the counting pass): a tile per window does the per-sample work in LDS
+// and writes one value per read in partitioned order; a pass per sub-chunk
+// puts the values back in stream order through LDS. No pass scatters into or
+// gathers from HBM at random: gathering each read's size straight from the
+// size table is bound by the rate of random cache-line requests (about 5e10
+// per second on MI355X, 11 ms for ImageNet-22k's 5.7e8 reads, more than this
+// whole pipeline).
 //
 // Prefetch order. Each storage class is filled in the order the worker first
 // needs its samples (the first rule of optimal prefetching, I/O Access
@@ -32,19 +35,23 @@
 // fill(h) - 1: fill(h) is the smallest f <= h with S(h) - S(f - 1) <= d0,
 // or h when the sample alone is larger than d0. Equivalently fill(h) is one
 // past the smallest g in [-1, h] with S(g) >= S(h) - d0, capped at h.
-//   st_tile   -- per (window, group of workers): the window's sizes in LDS;
-//                every read of the group's workers gets its sample's size
-//                (partitioned order).
-//   st_sum    -- per sub-chunk: sizes back in stream order in LDS, their
-//                inclusive prefix sums inside the sub-chunk, its total.
-//   st_base   -- per worker: exclusive scan of the sub-chunk totals.
-//   st_bounds -- per quarter of a sub-chunk (4096 positions): the g of its
-//                first and of its last position (binary search over S; g
-//                never decreases along R).
-//   st_fill   -- per quarter: S over that g range is staged in LDS (the few
-//                sub-chunks it spans give the bases), each thread
-//                binary-searches the g of its first position there and walks
-//                its other positions with two pointers; -1 in padding.
+// The staging passes fold each row's E epochs into one segment of E * L_i
+// reads, cut into spans of 2^14 positions, and partition the spans by
+// windows of 2^14 samples:
+//   st_gather -- per (window, group of 32 workers): the window's sizes in
+//                LDS (128 KB); every read of the group's spans gets its
+//                sample's size, written in partitioned order.
+//   st_unpart -- per span (in place): the sizes back in stream order in LDS,
+//                their inclusive prefix sums inside the span (a wave scan
+//                per 64 positions, in registers), the span's total.
+//   st_base   -- per worker: exclusive scan of the span totals.
+//   st_bounds -- per quarter of a span (4096 positions): the g of its first
+//                and of its last position (binary search over S; g never
+//                decreases along R).
+//   st_fill   -- per quarter: S over that g range is staged in LDS, each
+//                thread binary-searches the g of its first position there
+//                and walks its other positions with two pointers; -1 in
+//                padding.
 #include <limits.h>
 
 #include <new>
@@ -53,12 +60,6 @@
 
 namespace nopfs {
 namespace {
-
-// Tuning knob (identical results; only speed changes): workers per st_tile
-// workgroup (each loads the window's sizes once for all of them).
-#ifndef NOPFS_ST_GROUP
-#define NOPFS_ST_GROUP 16
-#endif
 
 
 constexpr int kSchedWs = 13;             // partition windows: 2^13 samples
@@ -204,10 +205,13 @@ pf_count(SegParams p, int32_t J, const uint8_t* __restrict__ code, uint32_t nch,
   for (int64_t j0 = int64_t(w) * 64 * kBatch; j0 < s.len; j0 += 256 * kBatch) {
     uint32_t m[kBatch];
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
+    for (int u = 0; u < kBatch; ++u) {  // unconditional loads, all in flight together
       const int64_t j = j0 + u * 64 + lane;
-      m[u] = j < s.len ? clamp_code(src[j], J) : 0u;
+      m[u] = src[j < s.len ? j : 0];
     }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      m[u] = j0 + u * 64 + lane < s.len ? clamp_code(uint8_t(m[u]), J) : 0u;
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       uint64_t act = __ballot(m[u] != 0);
@@ -331,108 +335,221 @@ pf_write(SegParams p, int32_t J, const uint32_t* __restrict__ Pk, const uint8_t*
 }
 
 // -------------------------------------------------------------- staging --
-constexpr int kStGroup = NOPFS_ST_GROUP;
-constexpr int kSumThreads = 1024;
-constexpr int kHalf = kSC / 2;                // positions per LDS pass of st_sum
-constexpr int kSumPer = kHalf / kSumThreads;  // 8 positions per thread
-constexpr int kSumEnt = kSC / kSumThreads;    // 16 entries per thread
+// The staging passes see each row of R as one segment of E * L_i reads (the
+// epochs folded together), cut into spans of kSC = 2^14 positions: position
+// h lies in span h >> kScShift. The partition of R by sample window is taken
+// over those spans.
+constexpr int kStWs = 14;           // staging windows: 2^14 samples (128 KB of sizes)
+constexpr int kStWin = 1 << kStWs;
+constexpr int kGThreads = 1024;
+constexpr int kGRows = 32;          // rows per st_gather tile
+constexpr int kGRuns = 1024;        // runs per pass of a tile
+constexpr int kGChunk = 4096;       // reads per inner pass (run index map in LDS)
+constexpr int kGPer = kGChunk / kGThreads;  // reads per thread and inner pass
+static_assert(kGRuns % kGThreads == 0 && kGChunk % kGThreads == 0, "st_gather shape");
 
-static_assert(kSumPer * kSumThreads == kHalf && kSumEnt * kSumThreads == kSC, "st_sum shape");
-
-__device__ __forceinline__ int sum_slot(int p) { return p + (p >> 3); }
-
-constexpr int kStTileThreads = 1024;
-
-__global__ void __launch_bounds__(kStTileThreads)
-st_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
-        const int64_t* __restrict__ sizes, int64_t* __restrict__ zP,
-        uint32_t ntiles) {
-  __shared__ int64_t sz[kWin];
-  // group-major tiles, like the other tile passes: a group's consecutive
-  // windows run together on one XCD, so the partial lines their runs write
-  // are completed there (window-major order, which shares a window's sizes
-  // between groups instead, measured 1.7x slower)
+// zP[x] = sizes[k] for every read of window kb of the tile's rows, x being
+// the read's place in the partitioned row (so zP holds the sizes in
+// partitioned order). Consecutive threads take consecutive reads of the
+// tile's runs (a run: the window's reads inside one span, contiguous in the
+// partitioned row), so loads and stores go out in run-long pieces. Tiles are
+// window-major: the tiles of one window, and of its neighbours (whose runs
+// adjoin in memory), run together on one XCD.
+__global__ void __launch_bounds__(kGThreads)
+st_gather(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
+          const int64_t* __restrict__ sizes, int64_t* __restrict__ zP, uint32_t ngroups,
+          uint32_t ntiles) {
+  __shared__ int64_t sz[kStWin];
+  __shared__ uint32_t pref[kGRuns + 1];
+  __shared__ int32_t rpos[kGRuns];   // span start + run start, in the row
+  __shared__ uint8_t rrow[kGRuns];   // row - first row of the tile
+  __shared__ uint16_t run_of[kGChunk];
+  __shared__ uint32_t tmp[65];
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
-  const int64_t g = tile / p.nbk;
-  const uint32_t kb = tile - uint32_t(g) * p.nbk;
-  const int64_t i0 = g * kStGroup;
-  const int64_t gw = p.N - i0 < kStGroup ? p.N - i0 : kStGroup;  // workers in the group
+  const uint32_t kb = tile / ngroups;
+  const int64_t i0 = int64_t(tile - kb * ngroups) * kGRows;
+  const int64_t rows = p.N - i0 < kGRows ? p.N - i0 : kGRows;
+  const int64_t nch = p.nsc;
+  const int64_t nruns = rows * nch;
   const int64_t k0 = int64_t(kb) << p.ws;
   const int64_t kend = k0 + (int64_t(1) << p.ws) < p.F ? k0 + (int64_t(1) << p.ws) : p.F;
-  const int64_t runs = int64_t(p.E) * p.nsc;
-  for (int64_t w0 = k0; w0 < kend; w0 += kWin) {
-    const uint32_t wl = uint32_t(kend - w0 < kWin ? kend - w0 : kWin);
+  for (int64_t w0 = k0; w0 < kend; w0 += kStWin) {  // one pass unless windows exceed kStWin
+    const uint32_t wl = uint32_t(kend - w0 < kStWin ? kend - w0 : kStWin);
     const uint32_t xoff = uint32_t(w0 - k0);
-    for (uint32_t x = threadIdx.x; x < wl; x += kStTileThreads) sz[x] = sizes[w0 + x];
-    __syncthreads();
-    // (worker, run) pairs of the group, spread over the threads
-    for (int64_t pr = threadIdx.x; pr < gw * runs; pr += kStTileThreads) {
-      const int64_t i = i0 + pr / runs;
-      int64_t* zrow = zP + i * p.M_max;
-      walk_runs(p, i, kb, Pk, OT, pr % runs, runs, [&](int64_t fb, uint32_t q, uint32_t v) {
-        const uint32_t x = (v >> kScShift) - xoff;
-        if (x < wl) zrow[fb + q] = sz[x];
-      });
+    // the window's sizes, sixteen loads per thread in flight at once
+    for (uint32_t x0 = 0; x0 < wl; x0 += 16 * kGThreads) {
+      int64_t v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const uint32_t x = x0 + u * kGThreads + threadIdx.x;
+        v[u] = sizes[w0 + (x < wl ? x : 0)];
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const uint32_t x = x0 + u * kGThreads + threadIdx.x;
+        if (x < wl) sz[x] = v[u];
+      }
+    }
+    for (int64_t r0 = 0; r0 < nruns; r0 += kGRuns) {
+      const uint32_t nr = uint32_t(nruns - r0 < kGRuns ? nruns - r0 : kGRuns);
+      uint32_t len[kGRuns / kGThreads];
+      uint32_t sum = 0;
+#pragma unroll
+      for (int m = 0; m < kGRuns / kGThreads; ++m) {
+        const uint32_t r = threadIdx.x * (kGRuns / kGThreads) + m;
+        // loads for runs past nr read run r0's bounds and are dropped
+        const uint32_t rr = uint32_t(r0) + (r < nr ? r : 0u);  // < 2^31 (rows * nch)
+        const uint32_t il = rr / uint32_t(nch), c = rr - il * uint32_t(nch);
+        const uint16_t* o = OT + ((i0 + il) * (p.nbk + 1) + kb) * nch + c;
+        const uint32_t a = o[0], b = o[nch];
+        len[m] = r < nr ? b - a : 0u;
+        if (r < nr) {
+          rpos[r] = int32_t((int64_t(c) << kScShift) + a);
+          rrow[r] = uint8_t(il);
+        }
+        sum += len[m];
+      }
+      uint32_t total;
+      uint32_t run = block_exclusive_scan(sum, tmp, &total);
+#pragma unroll
+      for (int m = 0; m < kGRuns / kGThreads; ++m) {
+        pref[threadIdx.x * (kGRuns / kGThreads) + m] = run;
+        run += len[m];
+      }
+      if (threadIdx.x == 0) pref[nr] = total;
+      __syncthreads();
+      for (uint32_t x0 = 0; x0 < total; x0 += kGChunk) {
+        const uint32_t xl = total - x0 < kGChunk ? total - x0 : kGChunk;
+        // run index of every read of the chunk, written by the runs' owners
+#pragma unroll
+        for (int m = 0; m < kGRuns / kGThreads; ++m) {
+          const uint32_t r = threadIdx.x * (kGRuns / kGThreads) + m;
+          if (r < nr) {
+            const uint32_t a = pref[r] > x0 ? pref[r] - x0 : 0u;
+            const uint32_t e = pref[r + 1] - x0 < xl ? pref[r + 1] - x0 : xl;
+            for (uint32_t y = a; y < e && pref[r + 1] > x0; ++y) run_of[y] = uint16_t(r);
+          }
+        }
+        __syncthreads();
+        int64_t pos[kGPer];
+        uint32_t v[kGPer];
+#pragma unroll
+        for (int u = 0; u < kGPer; ++u) {
+          const uint32_t t = u * kGThreads + threadIdx.x;
+          pos[u] = -1;
+          if (t < xl) {
+            const uint32_t r = run_of[t];
+            pos[u] = (i0 + rrow[r]) * p.M_max + rpos[r] + (x0 + t - pref[r]);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kGPer; ++u) v[u] = Pk[pos[u] >= 0 ? pos[u] : 0];  // unconditional
+#pragma unroll
+        for (int u = 0; u < kGPer; ++u) {
+          const uint32_t x = (v[u] >> kScShift) - xoff;
+          if (pos[u] >= 0 && x < wl) zP[pos[u]] = sz[x];
+        }
+        __syncthreads();
+      }
     }
     __syncthreads();
   }
 }
 
-// S[i*M_max + f] = sum of the sizes at the positions of f's sub-chunk up to
-// and including f; ctot[i][c] = the sub-chunk's total.
-__global__ void __launch_bounds__(kSumThreads)
-st_sum(SegParams p, const uint32_t* __restrict__ Pk, const int64_t* __restrict__ zP, uint32_t nch,
-       int64_t* __restrict__ S, int64_t* __restrict__ ctot) {
-  __shared__ int64_t sv[kHalf + kHalf / kSumPer];
-  __shared__ uint64_t tmp[65];
-  const SubChunk s = sub_chunk(p, nch, blockIdx.x);
-  uint32_t jj[kSumEnt];
-  int64_t vv[kSumEnt];
-#pragma unroll
-  for (int u = 0; u < kSumEnt; ++u) {
-    const int64_t q = int64_t(u) * kSumThreads + threadIdx.x;
-    jj[u] = q < s.len ? (Pk[s.base + q] & kJMask) : 0xFFFFFFFFu;
-    vv[u] = q < s.len ? zP[s.base + q] : 0;
-  }
-  uint64_t carry = 0;
-  for (int64_t j0 = 0; j0 < s.len; j0 += kHalf) {
-    const uint32_t hl = uint32_t(s.len - j0 < kHalf ? s.len - j0 : kHalf);
-#pragma unroll
-    for (int u = 0; u < kSumEnt; ++u) {
-      const uint32_t x = jj[u] - uint32_t(j0);
-      if (x < hl) sv[sum_slot(int(x))] = vv[u];
-    }
-    __syncthreads();
-    uint64_t v[kSumPer];
-    uint64_t run = 0;
-#pragma unroll
-    for (int u = 0; u < kSumPer; ++u) {
-      const int x = int(threadIdx.x) * kSumPer + u;
-      run += x < int(hl) ? uint64_t(sv[sum_slot(x)]) : 0ull;
-      v[u] = run;
-    }
-    uint64_t total;
-    const uint64_t ex = block_exclusive_scan64(run, tmp, &total);
-#pragma unroll
-    for (int u = 0; u < kSumPer; ++u) {
-      const int x = int(threadIdx.x) * kSumPer + u;
-      if (x < int(hl)) sv[sum_slot(x)] = int64_t(carry + ex + v[u]);
-    }
-    __syncthreads();
-    int64_t* dst = S + s.base + j0;
-#pragma unroll
-    for (int u = 0; u < kSumPer; ++u) {
-      const int x = u * kSumThreads + int(threadIdx.x);
-      if (x < int(hl)) dst[x] = sv[sum_slot(x)];
-    }
-    carry += total;
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) ctot[s.i * nch + s.c] = int64_t(carry);
+constexpr int kUThreads = 1024;
+constexpr int kUWaves = kUThreads / 64;
+constexpr int kURows = kSC / kUThreads;  // 64-lane rows per wave: 16
+
+// The reads of one span as loaded by st_unpart: thread t holds entries
+// t, t + 1024, ... of the span's partitioned order (packed entry, size).
+// The loads are unconditional (entries past the span's end load its first
+// entry and are skipped when consumed), so they stay in flight together.
+struct SpanRegs {
+  uint32_t j[kURows];
+  int64_t z[kURows];
+};
+
+__device__ __forceinline__ int64_t span_len(const SegParams& p, int64_t i, int64_t c) {
+  const int64_t len = seg_len(p, i) - (c << kScShift);
+  return len < 0 ? 0 : (len > kSC ? kSC : len);
 }
 
-// In place: ctot[i][c] becomes the sum of the sizes in the sub-chunks before c.
+__device__ __forceinline__ void span_load(const SegParams& p, const uint32_t* __restrict__ Pk,
+                                          const int64_t* __restrict__ zS, int64_t b, int64_t nblk,
+                                          SpanRegs& g) {
+  int64_t len = 0, base = 0;
+  if (b < nblk) {
+    const int64_t i = b / p.nsc, c = b - i * p.nsc;
+    len = span_len(p, i, c);
+    base = i * p.M_max + (c << kScShift);  // inside the row table even when len == 0
+  }
+#pragma unroll
+  for (int u = 0; u < kURows; ++u) {
+    const int64_t q = int64_t(u) * kUThreads + threadIdx.x;
+    const int64_t at = base + (q < len ? q : 0);
+    g.j[u] = Pk[at];
+    g.z[u] = zS[at];
+  }
+}
+
+// In place, per span c of row i: zS holds the span's sizes in partitioned
+// order on entry and S on exit, S[h] = sum of the sizes at positions
+// (h >> 14 << 14) .. h; ctot[i][c] = the span's total. The sizes go back to
+// stream order in LDS (each read's partitioned entry carries its position),
+// then wave w sums its 1024 consecutive positions, takes the totals of the
+// waves before it as its carry and scans them as 16 rows of 64 lanes in
+// registers (a wave scan per row plus the running carry); S is written in
+// whole lines. The span needs all of
+// the LDS a CU has for one workgroup, so each workgroup walks spans b,
+// b + gridDim.x, ... and loads the next span's entries before it scans the
+// current one.
+__global__ void __launch_bounds__(kUThreads)
+st_unpart(SegParams p, const uint32_t* __restrict__ Pk, int64_t* __restrict__ zS,
+          int64_t* __restrict__ ctot, int64_t nblk) {
+  __shared__ int64_t sv[kSC];
+  __shared__ uint64_t wtot[kUWaves];
+  const uint32_t lane = __lane_id(), wave = threadIdx.x >> 6;
+  const int64_t q0 = int64_t(wave) * (kURows * 64) + lane;
+  SpanRegs g;
+  span_load(p, Pk, zS, blockIdx.x, nblk, g);
+  for (int64_t b = blockIdx.x; b < nblk; b += gridDim.x) {
+    const int64_t i = b / p.nsc, c = b - i * p.nsc;
+    const int64_t len = span_len(p, i, c);
+#pragma unroll
+    for (int u = 0; u < kURows; ++u)
+      if (int64_t(u) * kUThreads + threadIdx.x < len) sv[g.j[u] & kJMask] = g.z[u];
+    __syncthreads();
+    // the next span's entries are in flight while this one is scanned
+    span_load(p, Pk, zS, b + gridDim.x, nblk, g);
+    // the wave's total first, so that each row is written as soon as it is scanned
+    uint64_t lsum = 0;
+#pragma unroll 4
+    for (int u = 0; u < kURows; ++u)
+      lsum += q0 + u * 64 < len ? uint64_t(sv[q0 + u * 64]) : 0ull;
+    const uint64_t wsum = read_lane64(wave_inclusive_scan64(lsum), 63);
+    if (lane == 0) wtot[wave] = wsum;
+    __syncthreads();
+    uint64_t carry = 0;
+    for (uint32_t w = 0; w < wave; ++w) carry += wtot[w];
+    int64_t* row = zS + i * p.M_max + (c << kScShift);
+#pragma unroll 4
+    for (int u = 0; u < kURows; ++u) {
+      const bool in = q0 + u * 64 < len;
+      const uint64_t v = wave_inclusive_scan64(in ? uint64_t(sv[q0 + u * 64]) : 0ull) + carry;
+      if (in) row[q0 + u * 64] = int64_t(v);
+      carry = read_lane64(v, 63);
+    }
+    if (threadIdx.x == 0) {
+      uint64_t t = 0;
+      for (int w = 0; w < kUWaves; ++w) t += wtot[w];
+      ctot[b] = int64_t(t);
+    }
+    __syncthreads();  // sv and wtot are rewritten for the next span
+  }
+}
+
+// In place: ctot[i][c] becomes the sum of the sizes in the spans before c.
 __global__ void __launch_bounds__(1024)
 st_base(uint32_t nch, int64_t* __restrict__ ctot) {
   __shared__ uint64_t tmp[65];
@@ -450,22 +567,11 @@ st_base(uint32_t nch, int64_t* __restrict__ ctot) {
 
 // Prefix sums along row i of R: at(x) = sum of the sizes at positions 0..x.
 struct Prefix {
-  const int64_t* S;     // row i of S (prefix sums local to each sub-chunk)
-  const int64_t* base;  // row i of the sub-chunk bases
-  int64_t Li;           // reads per epoch of worker i (> 0 whenever at() is used)
-  double rinv;          // 1 / Li
-  int64_t nsc;
-  // sub-chunk of position x >= 0
-  __device__ __forceinline__ int64_t chunk_of(int64_t x) const {
-    // epoch of x: the double quotient is off by at most one
-    int64_t e = int64_t(double(x) * rinv);
-    if (e * Li > x) --e;
-    else if ((e + 1) * Li <= x) ++e;
-    return e * nsc + ((x - e * Li) >> kScShift);
-  }
+  const int64_t* S;     // row i of S (prefix sums local to each span)
+  const int64_t* base;  // row i of the span bases
   __device__ __forceinline__ int64_t at(int64_t x) const {
     if (x < 0) return 0;
-    return int64_t(uint64_t(base[chunk_of(x)]) + uint64_t(S[x]));
+    return int64_t(uint64_t(base[x >> kScShift]) + uint64_t(S[x]));
   }
   // smallest g in [-1, h] with at(g) >= target (h qualifies when target <= at(h))
   __device__ int64_t lower_bound(int64_t h, int64_t target) const {
@@ -484,9 +590,6 @@ __device__ __forceinline__ Prefix row_prefix(const SegParams& p, int64_t i, uint
   Prefix P;
   P.S = S + i * p.M_max;
   P.base = base + i * int64_t(nch);
-  P.Li = seg_len(p, i);
-  P.rinv = P.Li > 0 ? 1.0 / double(P.Li) : 0.0;
-  P.nsc = p.nsc;
   return P;
 }
 
@@ -498,38 +601,33 @@ __device__ __forceinline__ int64_t sub_sat(int64_t a, int64_t b) {
 constexpr int kStThreads = 256;
 constexpr int kStPer = 16;
 constexpr int64_t kStChunk = int64_t(kStThreads) * kStPer;  // 4096 positions
-constexpr int kStParts = int(kSC / kStChunk);                // quarters of a sub-chunk
+constexpr int kStParts = int(kSC / kStChunk);                // quarters of a span
 constexpr int kStPad = kStChunk + kStChunk / kStPer;        // LDS slots with one pad per 16
 constexpr int kGCap = 5120;                                  // g values staged in LDS
-constexpr int kSegMax = 8;  // sub-chunks a staged g range may span
 
 static_assert(kStParts * kStChunk == kSC, "staging quarters");
 
 __device__ __forceinline__ int lds_slot(int p) { return p + (p >> 4); }
 
-// Block b of the fill covers quarter `part` of sub-chunk c of worker i:
+// Block b of the fill covers quarter `part` of span c of worker i:
 // positions [h0, h0 + hl) of row i (hl may be 0).
 struct FillPart {
-  int64_t i, c, part, Li, h0, hl;
+  int64_t i, c, q, h0, hl;
 };
 
 __device__ __forceinline__ FillPart fill_part(const SegParams& p, uint32_t nch, int64_t b) {
   FillPart f;
   const int64_t per = int64_t(nch) * kStParts;
   f.i = b / per;
-  const int64_t rem = b - f.i * per;
-  f.c = rem / kStParts;
-  f.part = rem - f.c * kStParts;
-  f.Li = seg_len(p, f.i);
-  const int64_t e = f.c / p.nsc, sc = f.c - e * p.nsc;
-  const int64_t len = sub_len(f.Li, sc) - f.part * kStChunk;
+  f.q = b - f.i * per;
+  f.c = f.q / kStParts;
+  f.h0 = f.q * kStChunk;
+  const int64_t len = seg_len(p, f.i) - f.h0;
   f.hl = len < 0 ? 0 : (len > kStChunk ? kStChunk : len);
-  f.h0 = e * f.Li + sc * kSC + f.part * kStChunk;
   return f;
 }
 
-// bnd[b] = (g of the part's first position, g of its last position, the
-// sub-chunk holding the first g (-1 when it is -1), 0).
+// bnd[b] = (g of the part's first position, g of its last position, 0, 0).
 __global__ void __launch_bounds__(256)
 st_bounds(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __restrict__ S,
           const int64_t* __restrict__ base, int4* __restrict__ bnd) {
@@ -537,14 +635,14 @@ st_bounds(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* 
   if (b >= nparts) return;
   const FillPart f = fill_part(p, nch, b);
   if (f.hl == 0) {
-    bnd[b] = make_int4(0, -1, -1, 0);
+    bnd[b] = make_int4(0, -1, 0, 0);
     return;
   }
   const Prefix P = row_prefix(p, f.i, nch, S, base);
   const int64_t h1 = f.h0 + f.hl - 1;
   const int64_t glo = P.lower_bound(f.h0, sub_sat(P.at(f.h0), d0));
   const int64_t ghi = P.lower_bound(h1, sub_sat(P.at(h1), d0));
-  bnd[b] = make_int4(int32_t(glo), int32_t(ghi), int32_t(glo >= 0 ? P.chunk_of(glo) : -1), 0);
+  bnd[b] = make_int4(int32_t(glo), int32_t(ghi), 0, 0);
 }
 
 __global__ void __launch_bounds__(kStThreads)
@@ -555,61 +653,46 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
   __shared__ int64_t gS[kGCap];
   static_assert(kStPad * sizeof(int32_t) <= sizeof(gS), "result staging fits");
   int32_t* fo = reinterpret_cast<int32_t*>(gS);
-  __shared__ int64_t seg_hi[kSegMax], seg_base[kSegMax];
-  __shared__ int32_t s_staged;
   const int64_t b = xcd_logical(blockIdx.x, gridDim.x);
   if (b >= nparts) return;
   const FillPart f = fill_part(p, nch, b);
   int32_t* out = fill + f.i * p.M_max;
-  if (f.c == int64_t(nch) - 1 && f.part == 0) {
+  if (f.q == 0) {
     // the row's padding past its last read
-    for (int64_t h = int64_t(p.E) * f.Li + threadIdx.x; h < p.M_max; h += kStThreads) out[h] = -1;
+    for (int64_t h = seg_len(p, f.i) + threadIdx.x; h < p.M_max; h += kStThreads)
+      out[h] = -1;
   }
   if (f.hl == 0) return;
   const int64_t* Srow = S + f.i * p.M_max;
   const int64_t* brow = base + f.i * int64_t(nch);
-  // this thread's positions: prefix sums within sub-chunk c (loads first)
+  // the part's g range first: the staging loads below wait for it
+  const int4 bb = bnd[b];
+  const int64_t hbase = brow[f.c];  // every position of the part is in span c
+  // this thread's positions: prefix sums within span c
   const int64_t ht0 = int64_t(threadIdx.x) * kStPer;  // offset in the part
   int64_t sh[kStPer];
 #pragma unroll
-  for (int u = 0; u < kStPer; ++u) sh[u] = ht0 + u < f.hl ? Srow[f.h0 + ht0 + u] : 0;
-  const int64_t hbase = brow[f.c];  // every position of the part is in sub-chunk c
-  const int4 bb = bnd[b];
+  for (int u = 0; u < kStPer; ++u)  // unconditional: past the part's end, its last position
+    sh[u] = Srow[f.h0 + (ht0 + u < f.hl ? ht0 + u : f.hl - 1)];
   const int64_t glo = bb.x, ghi = bb.y;
   const int64_t Lg = ghi - glo + 1;
-  // sub-chunks c0, c0 + 1, ... spanned by [max(glo, 0), ghi], one per lane
-  // of the first wave: the end position and base of each
-  const int64_t c0 = bb.z >= 0 ? bb.z : 0;
-  const bool fits = Lg >= 1 && Lg <= gcap;  // uniform
-  if (threadIdx.x < 64) {
-    bool need = false, covered = false;
-    if (fits && threadIdx.x < kSegMax && ghi >= 0) {
-      const int64_t c = c0 + threadIdx.x;
-      if (c < int64_t(nch)) {
-        const int64_t e = c / p.nsc, sc = c - e * p.nsc;
-        const int64_t lo = e * f.Li + sc * kSC;
-        const int64_t hi = lo + sub_len(f.Li, sc);
-        need = lo <= ghi;
-        covered = need && hi > ghi;
-        seg_hi[threadIdx.x] = hi;
-        seg_base[threadIdx.x] = need ? brow[c] : 0;
-      }
-    }
-    const uint64_t cov = __ballot(covered);
-    if (threadIdx.x == 0) s_staged = fits && (ghi < 0 || cov != 0);
-  }
-  __syncthreads();
-  const bool staged = s_staged;  // uniform over the workgroup
+  const bool staged = Lg >= 1 && Lg <= gcap;  // uniform over the workgroup
   if (staged) {
-    for (int64_t x = threadIdx.x; x < Lg; x += kStThreads) {
-      const int64_t g = glo + x;
-      int64_t v = 0;
-      if (g >= 0) {
-        int k = 0;
-        while (g >= seg_hi[k]) ++k;  // the covering sub-chunk ends past ghi
-        v = int64_t(uint64_t(seg_base[k]) + uint64_t(Srow[g]));
+    // four positions per thread and step, loads first (clamped to g >= 0)
+    for (int64_t x0 = 0; x0 < Lg; x0 += 4 * kStThreads) {
+      int64_t sv[4], bv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t x = x0 + u * kStThreads + threadIdx.x;
+        const int64_t g = x < Lg && glo + x > 0 ? glo + x : 0;
+        sv[u] = Srow[g];
+        bv[u] = brow[g >> kScShift];
       }
-      gS[x] = v;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t x = x0 + u * kStThreads + threadIdx.x;
+        if (x < Lg) gS[x] = glo + x >= 0 ? int64_t(uint64_t(bv[u]) + uint64_t(sv[u])) : 0;
+      }
     }
   }
   __syncthreads();
@@ -713,30 +796,34 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
   if (s.M_max > 0 && (!R || !fill)) return fail(NOPFS_EINVAL, "R and fill must be non-NULL");
   if (d0 < 0) return fail(NOPFS_EINVAL, "d0 must be >= 0");
   if (s.M_max == 0) return NOPFS_OK;
-  const SegParams p = seg_params(s, kSchedWs);
-  const uint32_t nch = uint32_t(s.E * p.nsc);  // sub-chunks per worker
-  const uint32_t ngroups = uint32_t(ceil_div(s.N, kStGroup));
+  // one segment per row: the E epochs folded together, cut into spans
+  SegParams p = seg_params(s, kStWs);
+  const uint32_t nch = uint32_t(ceil_div(s.M_max, kSC));  // spans per row
+  p.emul = int32_t(s.E);
+  p.E = 1;
+  p.nsc = int32_t(nch);
   const int64_t nblk = s.N * int64_t(nch);
   const int64_t nparts = nblk * kStParts;
+  const uint32_t ngroups = uint32_t(ceil_div(s.N, kGRows));
   const int64_t ntiles = int64_t(p.nbk) * ngroups;
   if (nparts >= (int64_t(1) << 31) || ntiles >= (int64_t(1) << 31))
     return fail(NOPFS_ERANGE, "job too large for one launch");
   Scratch scr(st);
   uint32_t* Pk;
   uint16_t* OT;
-  int64_t *zP, *S, *ctot;
+  int64_t *S, *ctot;
   int4* bnd;
   if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
-  if ((rc = scr.alloc_n(&zP, size_t(s.N * s.M_max)))) return rc;
   if ((rc = scr.alloc_n(&S, size_t(s.N * s.M_max)))) return rc;
   if ((rc = scr.alloc_n(&ctot, size_t(nblk)))) return rc;
   if ((rc = scr.alloc_n(&bnd, size_t(nparts)))) return rc;
-  if ((rc = launch("st_tile", st_tile, dim3(xcd_padded(uint32_t(ntiles))), dim3(kStTileThreads), 0,
-                   st, p, (const uint32_t*)Pk, (const uint16_t*)OT, sizes, zP,
+  if ((rc = launch("st_gather", st_gather, dim3(xcd_padded(uint32_t(ntiles))), dim3(kGThreads), 0,
+                   st, p, (const uint32_t*)Pk, (const uint16_t*)OT, sizes, S, ngroups,
                    uint32_t(ntiles))))
     return rc;
-  if ((rc = launch("st_sum", st_sum, dim3(uint32_t(nblk)), dim3(kSumThreads), 0, st, p,
-                   (const uint32_t*)Pk, (const int64_t*)zP, nch, S, ctot)))
+  const int64_t ugrid = nblk < 1024 ? nblk : 1024;
+  if ((rc = launch("st_unpart", st_unpart, dim3(uint32_t(ugrid)), dim3(kUThreads), 0, st, p,
+                   (const uint32_t*)Pk, S, ctot, nblk)))
     return rc;
   if ((rc = launch("st_base", st_base, dim3(uint32_t(s.N)), dim3(1024), 0, st, nch, ctot))) return rc;
   if ((rc = launch("st_bounds", st_bounds, dim3(uint32_t(ceil_div(nparts, 256))), dim3(256), 0, st,
