@@ -124,6 +124,24 @@ __device__ inline uint32_t xcd_logical(uint32_t bid, uint32_t padded) {
 
 inline uint32_t xcd_padded(uint32_t n) { return (n + 7u) & ~7u; }
 
+// Non-temporal stores, for outputs written once in whole lines that the same
+// pass does not read back: they stream to memory instead of being held in L2
+// (the dense count and first-read rows: 7.1 -> 6.3 ms at ImageNet-22k).
+// Scattered or partial-line stores must not use them: the read-cell list
+// stored this way (4-byte stores a few per line) took 14.4 ms instead.
+template <typename T>
+__device__ __forceinline__ void stream_store(T* p, T v) {
+  __builtin_nontemporal_store(v, p);
+}
+__device__ __forceinline__ void stream_store(int4* p, int4 v) {
+  typedef int v4 __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(v4{v.x, v.y, v.z, v.w}, reinterpret_cast<v4*>(p));
+}
+__device__ __forceinline__ void stream_store(uint4* p, uint4 v) {
+  typedef unsigned v4 __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(v4{v.x, v.y, v.z, v.w}, reinterpret_cast<v4*>(p));
+}
+
 __device__ inline uint64_t lanemask_lt() {
   const uint32_t lane = __lane_id();
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));

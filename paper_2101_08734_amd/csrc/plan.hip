@@ -940,11 +940,12 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
     if (head > wlen) head = wlen;
     const uint32_t nunits = (wlen - head) >> 4;
     const uint32_t tail0 = head + 16 * nunits;
-    for (uint32_t x = threadIdx.x; x < head; x += kWriteThreads) dst[x] = tb[x + sh];
-    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kWriteThreads) dst[x] = tb[x + sh];
+    for (uint32_t x = threadIdx.x; x < head; x += kWriteThreads) stream_store(dst + x, tb[x + sh]);
+    for (uint32_t x = tail0 + threadIdx.x; x < wlen; x += kWriteThreads)
+      stream_store(dst + x, tb[x + sh]);
     for (uint32_t u = threadIdx.x; u < nunits; u += kWriteThreads) {
       const uint32_t x = head + 16 * u;
-      *reinterpret_cast<uint4*>(dst + x) = *reinterpret_cast<const uint4*>(tb + x + sh);
+      stream_store(reinterpret_cast<uint4*>(dst + x), *reinterpret_cast<const uint4*>(tb + x + sh));
     }
     __syncthreads();
   }
