@@ -356,7 +356,7 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
 #pragma unroll
       for (int u = 0; u < kFmPer; ++u) {
         const int x = u * kFmThreads + int(threadIdx.x);
-        if (x < int(hl)) td[x] = __longlong_as_double(L.sv[fm_slot(jb + x)]);
+        if (x < int(hl)) stream_store(td + x, __longlong_as_double(L.sv[fm_slot(jb + x)]));
       }
       __syncthreads();
 #pragma unroll
@@ -370,7 +370,7 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
 #pragma unroll
       for (int u = 0; u < kFmPer; ++u) {
         const int x = u * kFmThreads + int(threadIdx.x);
-        if (x < int(hl)) sd[x] = int16_t(L.sv[fm_slot(jb + x)]);
+        if (x < int(hl)) stream_store(sd + x, int16_t(L.sv[fm_slot(jb + x)]));
       }
     }
     ca += tota;

@@ -441,7 +441,7 @@ plan_write(PlanArgs a, const uint8_t* __restrict__ count, const int32_t* __restr
           nc += tv[q] == 256;
           packed |= uint32_t(uint8_t(int8_t(tv[q] == 256 ? 0 : tv[q]))) << (8 * q);
         }
-        *reinterpret_cast<uint32_t*>(trow + k) = packed;
+        stream_store(reinterpret_cast<uint32_t*>(trow + k), packed);
       }
       if (__ballot(nc > 0)) {
         const uint32_t inc = wave_inclusive_scan(uint32_t(nc));

@@ -537,7 +537,7 @@ st_unpart(SegParams p, const uint32_t* __restrict__ Pk, int64_t* __restrict__ zS
     for (int u = 0; u < kURows; ++u) {
       const bool in = q0 + u * 64 < len;
       const uint64_t v = wave_inclusive_scan64(in ? uint64_t(sv[q0 + u * 64]) : 0ull) + carry;
-      if (in) row[q0 + u * 64] = int64_t(v);
+      if (in) stream_store(row + q0 + u * 64, int64_t(v));
       carry = read_lane64(v, 63);
     }
     if (threadIdx.x == 0) {
@@ -740,7 +740,7 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
 #pragma unroll
   for (int u = 0; u < kStPer; ++u) {
     const int q = u * kStThreads + threadIdx.x;
-    if (q < f.hl) out[f.h0 + q] = fo[lds_slot(q)];
+    if (q < f.hl) stream_store(out + f.h0 + q, fo[lds_slot(q)]);
   }
 }
 
