@@ -598,16 +598,18 @@ __device__ __forceinline__ int64_t sub_sat(int64_t a, int64_t b) {
   return a < INT64_MIN + b ? INT64_MIN : a - b;
 }
 
-constexpr int kStThreads = 256;
-constexpr int kStPer = 16;
+constexpr int kStThreads = 512;
+constexpr int kStPer = 8;
 constexpr int64_t kStChunk = int64_t(kStThreads) * kStPer;  // 4096 positions
 constexpr int kStParts = int(kSC / kStChunk);                // quarters of a span
-constexpr int kStPad = kStChunk + kStChunk / kStPer;        // LDS slots with one pad per 16
+constexpr int kStPad = kStChunk + kStChunk / kStPer;        // LDS slots with one pad per 8
 constexpr int kGCap = 5120;                                  // g values staged in LDS
+constexpr int kGPerT = (kGCap + kStThreads - 1) / kStThreads;  // staged g values per thread
 
 static_assert(kStParts * kStChunk == kSC, "staging quarters");
+static_assert(kGCap < kSC, "a staged g range spans at most two spans");
 
-__device__ __forceinline__ int lds_slot(int p) { return p + (p >> 4); }
+__device__ __forceinline__ int lds_slot(int p) { return p + (p >> 3); }
 
 // Block b of the fill covers quarter `part` of span c of worker i:
 // positions [h0, h0 + hl) of row i (hl may be 0).
@@ -645,7 +647,7 @@ st_bounds(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* 
   bnd[b] = make_int4(int32_t(glo), int32_t(ghi), 0, 0);
 }
 
-__global__ void __launch_bounds__(kStThreads)
+__global__ void __launch_bounds__(kStThreads) __attribute__((amdgpu_waves_per_eu(8)))
 st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __restrict__ S,
         const int64_t* __restrict__ base, const int4* __restrict__ bnd, int32_t gcap,
         int32_t* __restrict__ fill) {
@@ -678,21 +680,23 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
   const int64_t Lg = ghi - glo + 1;
   const bool staged = Lg >= 1 && Lg <= gcap;  // uniform over the workgroup
   if (staged) {
-    // four positions per thread and step, loads first (clamped to g >= 0)
-    for (int64_t x0 = 0; x0 < Lg; x0 += 4 * kStThreads) {
-      int64_t sv[4], bv[4];
+    // every load of the range at once (clamped to g >= 0); the range spans
+    // at most two spans, whose bases are loaded once
+    const int64_t sA = (glo > 0 ? glo : 0) >> kScShift;
+    const int64_t bA = brow[sA];
+    const int64_t bB = brow[sA + 1 < int64_t(nch) ? sA + 1 : sA];
+    int64_t gv[kGPerT];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int64_t x = x0 + u * kStThreads + threadIdx.x;
-        const int64_t g = x < Lg && glo + x > 0 ? glo + x : 0;
-        sv[u] = Srow[g];
-        bv[u] = brow[g >> kScShift];
-      }
+    for (int u = 0; u < kGPerT; ++u) {
+      const int64_t x = u * kStThreads + threadIdx.x;
+      gv[u] = Srow[x < Lg && glo + x > 0 ? glo + x : 0];
+    }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int64_t x = x0 + u * kStThreads + threadIdx.x;
-        if (x < Lg) gS[x] = glo + x >= 0 ? int64_t(uint64_t(bv[u]) + uint64_t(sv[u])) : 0;
-      }
+    for (int u = 0; u < kGPerT; ++u) {
+      const int64_t x = u * kStThreads + threadIdx.x;
+      const int64_t g = glo + x;
+      if (x < Lg)
+        gS[x] = g >= 0 ? int64_t(uint64_t((g >> kScShift) == sA ? bA : bB) + uint64_t(gv[u])) : 0;
     }
   }
   __syncthreads();
