@@ -610,8 +610,21 @@ next_unpartition(SegParams p, const uint32_t* __restrict__ Pk, const int32_t* __
   const uint32_t len = uint32_t(len64);
   if (len == 0) return;
   const int64_t base = int64_t(i) * p.M_max + int64_t(e) * Li + int64_t(sc) * kSC;
-  for (uint32_t q = threadIdx.x; q < len; q += kUnpartThreads)
-    stage[Pk[base + q] & kJMask] = nextP[base + q];
+  {
+    // all of the thread's loads at once (clamped), then the LDS stores
+    constexpr int kPer = kSC / kUnpartThreads;
+    uint32_t j[kPer];
+    int32_t v[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const uint32_t q = u * kUnpartThreads + threadIdx.x;
+      j[u] = Pk[base + (q < len ? q : 0u)];
+      v[u] = nextP[base + (q < len ? q : 0u)];
+    }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u)
+      if (u * kUnpartThreads + threadIdx.x < len) stage[j[u] & kJMask] = v[u];
+  }
   __syncthreads();
   for (uint32_t q = threadIdx.x; q < len; q += kUnpartThreads) stream_store(next + base + q, stage[q]);
 }

@@ -1,0 +1,141 @@
+// Window-major pass over the partition of R for per-sample values: for every
+// read, a value taken from its sample's window (held in LDS) is written at
+// the read's place in the partitioned row. Used by the staging schedule
+// (each read's size) and by the fetch model (each read's size and source).
+//
+// The rows are folded into one segment (E = 1 in SegParams, the epochs
+// counted by emul), so run c of a row is the window's reads inside span c
+// of 2^14 positions. A tile is (window of 2^14 samples, group of kGRows
+// rows); tiles are window-major, so the groups of one window and the tiles
+// of neighbouring windows (whose runs adjoin in memory) run together on one
+// XCD. Consecutive threads take consecutive reads of the tile's runs, so
+// loads and stores go out in run-long pieces (19 reads on average at
+// ImageNet-22k) instead of one store per lane into 64 different runs.
+#pragma once
+
+#include "partition.hpp"
+
+namespace nopfs {
+
+constexpr int kGatherWs = 14;                 // window: 2^14 samples
+constexpr int kGatherWin = 1 << kGatherWs;    // values held in LDS (8 bytes each)
+constexpr int kGThreads = 1024;
+constexpr int kGRows = 32;                    // rows per tile
+constexpr int kGRuns = 1024;                  // runs per pass of a tile
+constexpr int kGChunk = 4096;                 // reads per inner pass (run index map)
+constexpr int kGPer = kGChunk / kGThreads;    // reads per thread and inner pass
+static_assert(kGRuns % kGThreads == 0 && kGChunk % kGThreads == 0, "gather tile shape");
+
+struct GatherLds {
+  uint64_t win[kGatherWin];   // the window's values
+  uint32_t pref[kGRuns + 1];  // reads before each run of the pass
+  int32_t rpos[kGRuns];       // span start + run start, in the row
+  uint8_t rrow[kGRuns];       // row - first row of the tile
+  uint16_t run_of[kGChunk];   // run of each read of the inner pass
+  uint32_t tmp[65];
+};
+
+inline uint32_t gather_ngroups(int64_t N) { return uint32_t(ceil_div(N, kGRows)); }
+
+// Tile `tile` of the pass. value(k) gives sample k's 8-byte value (it is
+// called for k in [0, F) only); emit(pos, row, x, w0, wl) receives kGPer
+// reads of this thread at once: pos[u] the read's index in the row table
+// ([N][M_max], -1 for none), row[u] its row, x[u] its sample's offset in the
+// window pass starting at sample w0 (valid when x[u] < wl), with the window's
+// values in L.win.
+template <typename Value, typename Emit>
+__device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* __restrict__ Pk,
+                                            const uint16_t* __restrict__ OT, uint32_t tile,
+                                            uint32_t ngroups, GatherLds& L, Value value,
+                                            Emit emit) {
+  const uint32_t kb = tile / ngroups;
+  const int64_t i0 = int64_t(tile - kb * ngroups) * kGRows;
+  const int64_t rows = p.N - i0 < kGRows ? p.N - i0 : kGRows;
+  const int64_t nch = p.nsc;
+  const int64_t nruns = rows * nch;  // < 2^31
+  const int64_t k0 = int64_t(kb) << p.ws;
+  const int64_t kend = k0 + (int64_t(1) << p.ws) < p.F ? k0 + (int64_t(1) << p.ws) : p.F;
+  for (int64_t w0 = k0; w0 < kend; w0 += kGatherWin) {  // one pass unless windows are wider
+    const uint32_t wl = uint32_t(kend - w0 < kGatherWin ? kend - w0 : kGatherWin);
+    const uint32_t xoff = uint32_t(w0 - k0);
+    // the window's values, sixteen loads per thread in flight at once
+    for (uint32_t x0 = 0; x0 < wl; x0 += 16 * kGThreads) {
+      uint64_t v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const uint32_t x = x0 + u * kGThreads + threadIdx.x;
+        v[u] = value(w0 + (x < wl ? x : 0));
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const uint32_t x = x0 + u * kGThreads + threadIdx.x;
+        if (x < wl) L.win[x] = v[u];
+      }
+    }
+    for (int64_t r0 = 0; r0 < nruns; r0 += kGRuns) {
+      const uint32_t nr = uint32_t(nruns - r0 < kGRuns ? nruns - r0 : kGRuns);
+      uint32_t len[kGRuns / kGThreads];
+      uint32_t sum = 0;
+#pragma unroll
+      for (int m = 0; m < kGRuns / kGThreads; ++m) {
+        const uint32_t r = threadIdx.x * (kGRuns / kGThreads) + m;
+        // loads for runs past nr read run r0's bounds and are dropped
+        const uint32_t rr = uint32_t(r0) + (r < nr ? r : 0u);
+        const uint32_t il = rr / uint32_t(nch), c = rr - il * uint32_t(nch);
+        const uint16_t* o = OT + ((i0 + il) * (p.nbk + 1) + kb) * nch + c;
+        const uint32_t a = o[0], b = o[nch];
+        len[m] = r < nr ? b - a : 0u;
+        if (r < nr) {
+          L.rpos[r] = int32_t((int64_t(c) << kScShift) + a);
+          L.rrow[r] = uint8_t(il);
+        }
+        sum += len[m];
+      }
+      uint32_t total;
+      uint32_t run = block_exclusive_scan(sum, L.tmp, &total);
+#pragma unroll
+      for (int m = 0; m < kGRuns / kGThreads; ++m) {
+        L.pref[threadIdx.x * (kGRuns / kGThreads) + m] = run;
+        run += len[m];
+      }
+      if (threadIdx.x == 0) L.pref[nr] = total;
+      __syncthreads();
+      for (uint32_t x0 = 0; x0 < total; x0 += kGChunk) {
+        const uint32_t xl = total - x0 < kGChunk ? total - x0 : kGChunk;
+        // run index of every read of the inner pass, written by the runs' owners
+#pragma unroll
+        for (int m = 0; m < kGRuns / kGThreads; ++m) {
+          const uint32_t r = threadIdx.x * (kGRuns / kGThreads) + m;
+          if (r < nr) {
+            const uint32_t a = L.pref[r] > x0 ? L.pref[r] - x0 : 0u;
+            const uint32_t e = L.pref[r + 1] - x0 < xl ? L.pref[r + 1] - x0 : xl;
+            for (uint32_t y = a; y < e && L.pref[r + 1] > x0; ++y) L.run_of[y] = uint16_t(r);
+          }
+        }
+        __syncthreads();
+        int64_t pos[kGPer], row[kGPer];
+        uint32_t x[kGPer];
+#pragma unroll
+        for (int u = 0; u < kGPer; ++u) {
+          const uint32_t t = u * kGThreads + threadIdx.x;
+          pos[u] = -1;
+          row[u] = i0;
+          if (t < xl) {
+            const uint32_t r = L.run_of[t];
+            row[u] = i0 + L.rrow[r];
+            pos[u] = row[u] * p.M_max + L.rpos[r] + (x0 + t - L.pref[r]);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kGPer; ++u) x[u] = Pk[pos[u] >= 0 ? pos[u] : 0];  // unconditional
+#pragma unroll
+        for (int u = 0; u < kGPer; ++u) x[u] = pos[u] >= 0 ? (x[u] >> kScShift) - xoff : 0xFFFFFFFFu;
+        emit(pos, row, x, w0, wl);
+        __syncthreads();
+      }
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace nopfs

@@ -20,30 +20,29 @@
 //                 packed above the sample's size. A worker's own copy may be
 //                 that class: a remote copy of class j is never faster than
 //                 the local copy of j, so counting it never changes a choice.
-//   fm_tile    -- per (group of workers, 8K-sample window) of the partition
-//                 of R: each read's source from its own tier and the
-//                 sample's best remote class; size and source in
-//                 partitioned order.
-//   fm_sum     -- per sub-chunk of 2^14 reads: every entry loaded once into
+//   fm_gather  -- per (16K-sample window, group of 32 workers) of the
+//                 partition of R (rows folded into one segment of E * L_i
+//                 reads, cut into spans of 2^14): each read's source from
+//                 its own tier and the sample's best remote class; size and
+//                 source in partitioned order.
+//   fm_sum     -- per span of 2^14 reads: every entry loaded once into
 //                 the LDS slot of its stream position (the whole sub-chunk,
 //                 135 KB), then scanned in four parts of 4,096 positions:
 //                 its read-time sum, compute-time sum and maximum of
 //                 avail - U relative to its start.
-//   fm_scan    -- per worker: what enters each sub-chunk.
-//   fm_final   -- per sub-chunk: the same scans, combined with what enters
+//   fm_scan    -- per worker: what enters each span.
+//   fm_final   -- per span: the same scans, combined with what enters
 //                 it; source codes and consumption times in stream order.
 #include <math.h>
 
 #include <new>
 
+#include "gather.hpp"
 #include "partition.hpp"
 
 namespace nopfs {
 namespace {
 
-#ifndef NOPFS_FM_GROUP
-#define NOPFS_FM_GROUP 16  // workers per fm_tile workgroup (tuning only)
-#endif
 #ifndef NOPFS_FM_THREADS
 #define NOPFS_FM_THREADS 1024  // threads of the scan kernels (tuning only)
 #endif
@@ -52,10 +51,6 @@ constexpr int kMaxClasses = 32;
 constexpr uint32_t kNoClass = 255;
 constexpr int kSizeBits = 56;
 constexpr uint64_t kSizeMask = (uint64_t(1) << kSizeBits) - 1;
-constexpr int kFmWs = 13;
-constexpr int kFmWin = 1 << kFmWs;
-constexpr int kFmGroup = NOPFS_FM_GROUP;
-constexpr int kFmTileThreads = 1024;
 constexpr int kFmThreads = NOPFS_FM_THREADS;
 constexpr int kFmPart = kSC / 4;                // positions per LDS pass
 constexpr int kFmPer = kFmPart / kFmThreads;    // positions per thread and pass
@@ -147,76 +142,34 @@ __device__ __forceinline__ uint32_t choose(const Rates& rt, const SharedRates& s
   return code;
 }
 
-__global__ void __launch_bounds__(kFmTileThreads)
-fm_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
-        const int8_t* __restrict__ tier, const uint64_t* __restrict__ szb, Rates rt,
-        uint64_t* __restrict__ zP, uint32_t ntiles) {
-  __shared__ uint64_t sz[kFmWin];
+// Each read of the tile's window and rows gets its source (choose) and its
+// size, packed, at its place in the partitioned row.
+__global__ void __launch_bounds__(kGThreads)
+fm_gather(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
+          const int8_t* __restrict__ tier, const uint64_t* __restrict__ szb, Rates rt,
+          uint64_t* __restrict__ zP, uint32_t ngroups, uint32_t ntiles) {
+  __shared__ GatherLds L;
   __shared__ SharedRates sr;
-  // group-major tiles: a group's consecutive windows run together on one XCD
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
-  const int64_t g = tile / p.nbk;
-  const uint32_t kb = tile - uint32_t(g) * p.nbk;
-  const int64_t i0 = g * kFmGroup;
-  const int64_t gw = p.N - i0 < kFmGroup ? p.N - i0 : kFmGroup;
-  const int64_t k0 = int64_t(kb) << p.ws;
-  const int64_t kend = k0 + (int64_t(1) << p.ws) < p.F ? k0 + (int64_t(1) << p.ws) : p.F;
-  const int64_t runs = int64_t(p.E) * p.nsc;
-  const uint32_t nsc = uint32_t(p.nsc);
-  load_rates(rt, sr);
-  for (int64_t w0 = k0; w0 < kend; w0 += kFmWin) {
-    const uint32_t wl = uint32_t(kend - w0 < kFmWin ? kend - w0 : kFmWin);
-    const uint32_t xoff = uint32_t(w0 - k0);
-    for (uint32_t x0 = 0; x0 < wl; x0 += 8 * kFmTileThreads) {  // eight loads in flight
-      uint64_t v[8];
+  load_rates(rt, sr);  // visible after the tile's first barrier
+  gather_tile(
+      p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return szb[k]; },
+      [&](const int64_t (&pos)[kGPer], const int64_t (&row)[kGPer], const uint32_t (&x)[kGPer],
+          int64_t w0, uint32_t wl) {
+        // each read's own tier: a byte of its row's window slice (cached),
+        // loads first, unconditional
+        int32_t own[kGPer];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const uint32_t x = x0 + u * kFmTileThreads + threadIdx.x;
-        v[u] = szb[w0 + (x < wl ? x : 0)];
-      }
+        for (int u = 0; u < kGPer; ++u) own[u] = tier[row[u] * p.F + w0 + (x[u] < wl ? x[u] : 0u)];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const uint32_t x = x0 + u * kFmTileThreads + threadIdx.x;
-        if (x < wl) sz[x] = v[u];
-      }
-    }
-    __syncthreads();
-    for (int64_t pr = threadIdx.x; pr < gw * runs; pr += kFmTileThreads) {
-      const int64_t i = i0 + pr / runs;
-      const int64_t r = pr - (i - i0) * runs;
-      const int64_t Li = seg_len(p, i);
-      const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;
-      const uint32_t ra = oa[r], rb = oa[runs + r];
-      const uint32_t e = uint32_t(r) / nsc, sc = uint32_t(r) - e * nsc;
-      const int64_t fb = int64_t(e) * Li + int64_t(sc) * kSC;
-      const uint32_t* src = Pk + i * p.M_max + fb;
-      const int8_t* trow = tier + i * p.F + w0;
-      uint64_t* zrow = zP + i * p.M_max + fb;
-      for (uint32_t q = ra; q < rb; q += kRunBatch) {
-        uint32_t x[kRunBatch];
-        int32_t own[kRunBatch];
-        // unconditional loads (clamped indices), so that each batch waits once
-#pragma unroll
-        for (int u = 0; u < kRunBatch; ++u) x[u] = src[q + u < rb ? q + u : q];
-#pragma unroll
-        for (int u = 0; u < kRunBatch; ++u)
-          x[u] = q + u < rb ? (x[u] >> kScShift) - xoff : 0xFFFFFFFFu;
-#pragma unroll
-        for (int u = 0; u < kRunBatch; ++u) own[u] = trow[x[u] < wl ? x[u] : 0u];
-#pragma unroll
-        for (int u = 0; u < kRunBatch; ++u) own[u] = x[u] < wl ? own[u] : -1;
-#pragma unroll
-        for (int u = 0; u < kRunBatch; ++u)
-          if (x[u] < wl) {
-            const uint64_t sb = sz[x[u]];
+        for (int u = 0; u < kGPer; ++u)
+          if (pos[u] >= 0 && x[u] < wl) {
+            const uint64_t sb = L.win[x[u]];
             const uint32_t code = choose(rt, sr, own[u], uint32_t(sb >> kSizeBits));
-            zrow[q + u] = (sb & kSizeMask) | (uint64_t(code) << kSizeBits);
+            zP[pos[u]] = (sb & kSizeMask) | (uint64_t(code) << kSizeBits);
           }
-      }
-    }
-    __syncthreads();
-  }
+      });
 }
 
 // ------------------------------------------------------------------ scans --
@@ -292,8 +245,20 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
                          Enter* sum_out, int16_t* __restrict__ src, double* __restrict__ tout) {
   // every entry of the sub-chunk, loaded once and coalesced, into the LDS
   // slot of its stream position
-  for (int64_t q = threadIdx.x; q < s.len; q += kFmThreads)
-    L.sv[fm_slot(int(Pk[s.base + q] & kJMask))] = zP[s.base + q];
+  {
+    // all of the thread's loads at once (clamped), then the LDS stores
+    uint32_t j[kFmEnt];
+    uint64_t v[kFmEnt];
+#pragma unroll
+    for (int u = 0; u < kFmEnt; ++u) {
+      const int64_t q = int64_t(u) * kFmThreads + threadIdx.x;
+      j[u] = Pk[s.base + (q < s.len ? q : 0)];
+      v[u] = zP[s.base + (q < s.len ? q : 0)];
+    }
+#pragma unroll
+    for (int u = 0; u < kFmEnt; ++u)
+      if (int64_t(u) * kFmThreads + threadIdx.x < s.len) L.sv[fm_slot(int(j[u] & kJMask))] = v[u];
+  }
   __syncthreads();
   const double inv_p0 = 1.0 / rt.p0;
   double ca = 0, cu = 0, cm = -INFINITY;  // running over the parts, relative to the chunk
@@ -473,9 +438,14 @@ int model_impl(const nopfs_job* job, const int32_t* R, const int8_t* tier, const
   if (s.M_max == 0) return NOPFS_OK;
   if (!R || !src || !t) return fail(NOPFS_EINVAL, "R, src and t must be non-NULL");
   const Rates rt = make_rates(model);
-  const SegParams p = seg_params(s, kFmWs);
-  const uint32_t nch = uint32_t(s.E * p.nsc);  // sub-chunks per worker
-  const uint32_t ngroups = uint32_t(ceil_div(s.N, kFmGroup));
+  // one segment per row (the E epochs folded together), cut into spans of
+  // 2^14 positions, partitioned by windows of 2^14 samples
+  SegParams p = seg_params(s, kGatherWs);
+  const uint32_t nch = uint32_t(ceil_div(s.M_max, kSC));  // spans per row
+  p.emul = int32_t(s.E);
+  p.E = 1;
+  p.nsc = int32_t(nch);
+  const uint32_t ngroups = gather_ngroups(s.N);
   const int64_t nblk = s.N * int64_t(nch);
   const int64_t ntiles = int64_t(p.nbk) * ngroups;
   if (nblk >= (int64_t(1) << 31) || ntiles >= (int64_t(1) << 31))
@@ -492,9 +462,9 @@ int model_impl(const nopfs_job* job, const int32_t* R, const int8_t* tier, const
   if ((rc = launch("fm_holders", fm_holders, dim3(uint32_t(ceil_div(s.F, 256))), dim3(256), 0, st,
                    s.F, s.N, tier, sizes, rt, szb)))
     return rc;
-  if ((rc = launch("fm_tile", fm_tile, dim3(xcd_padded(uint32_t(ntiles))), dim3(kFmTileThreads), 0,
+  if ((rc = launch("fm_gather", fm_gather, dim3(xcd_padded(uint32_t(ntiles))), dim3(kGThreads), 0,
                    st, p, (const uint32_t*)Pk, (const uint16_t*)OT, tier, (const uint64_t*)szb, rt,
-                   zP, uint32_t(ntiles))))
+                   zP, ngroups, uint32_t(ntiles))))
     return rc;
   if ((rc = launch("fm_sum", fm_sum, dim3(uint32_t(nblk)), dim3(kFmThreads), 0, st, p,
                    (const uint32_t*)Pk, (const uint64_t*)zP, rt, nch, sums)))

@@ -56,6 +56,7 @@
 
 #include <new>
 
+#include "gather.hpp"
 #include "partition.hpp"
 
 namespace nopfs {
@@ -339,122 +340,26 @@ pf_write(SegParams p, int32_t J, const uint32_t* __restrict__ Pk, const uint8_t*
 // epochs folded together), cut into spans of kSC = 2^14 positions: position
 // h lies in span h >> kScShift. The partition of R by sample window is taken
 // over those spans.
-constexpr int kStWs = 14;           // staging windows: 2^14 samples (128 KB of sizes)
-constexpr int kStWin = 1 << kStWs;
-constexpr int kGThreads = 1024;
-constexpr int kGRows = 32;          // rows per st_gather tile
-constexpr int kGRuns = 1024;        // runs per pass of a tile
-constexpr int kGChunk = 4096;       // reads per inner pass (run index map in LDS)
-constexpr int kGPer = kGChunk / kGThreads;  // reads per thread and inner pass
-static_assert(kGRuns % kGThreads == 0 && kGChunk % kGThreads == 0, "st_gather shape");
+constexpr int kStWs = kGatherWs;  // staging windows: 2^14 samples (128 KB of sizes)
 
-// zP[x] = sizes[k] for every read of window kb of the tile's rows, x being
-// the read's place in the partitioned row (so zP holds the sizes in
-// partitioned order). Consecutive threads take consecutive reads of the
-// tile's runs (a run: the window's reads inside one span, contiguous in the
-// partitioned row), so loads and stores go out in run-long pieces. Tiles are
-// window-major: the tiles of one window, and of its neighbours (whose runs
-// adjoin in memory), run together on one XCD.
+// zP[x] = sizes[k] for every read of the tile's window and rows, x being the
+// read's place in the partitioned row (so zP holds the sizes in partitioned
+// order).
 __global__ void __launch_bounds__(kGThreads)
 st_gather(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
           const int64_t* __restrict__ sizes, int64_t* __restrict__ zP, uint32_t ngroups,
           uint32_t ntiles) {
-  __shared__ int64_t sz[kStWin];
-  __shared__ uint32_t pref[kGRuns + 1];
-  __shared__ int32_t rpos[kGRuns];   // span start + run start, in the row
-  __shared__ uint8_t rrow[kGRuns];   // row - first row of the tile
-  __shared__ uint16_t run_of[kGChunk];
-  __shared__ uint32_t tmp[65];
+  __shared__ GatherLds L;
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
-  const uint32_t kb = tile / ngroups;
-  const int64_t i0 = int64_t(tile - kb * ngroups) * kGRows;
-  const int64_t rows = p.N - i0 < kGRows ? p.N - i0 : kGRows;
-  const int64_t nch = p.nsc;
-  const int64_t nruns = rows * nch;
-  const int64_t k0 = int64_t(kb) << p.ws;
-  const int64_t kend = k0 + (int64_t(1) << p.ws) < p.F ? k0 + (int64_t(1) << p.ws) : p.F;
-  for (int64_t w0 = k0; w0 < kend; w0 += kStWin) {  // one pass unless windows exceed kStWin
-    const uint32_t wl = uint32_t(kend - w0 < kStWin ? kend - w0 : kStWin);
-    const uint32_t xoff = uint32_t(w0 - k0);
-    // the window's sizes, sixteen loads per thread in flight at once
-    for (uint32_t x0 = 0; x0 < wl; x0 += 16 * kGThreads) {
-      int64_t v[16];
+  gather_tile(
+      p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return uint64_t(sizes[k]); },
+      [&](const int64_t (&pos)[kGPer], const int64_t (&)[kGPer], const uint32_t (&x)[kGPer],
+          int64_t, uint32_t wl) {
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const uint32_t x = x0 + u * kGThreads + threadIdx.x;
-        v[u] = sizes[w0 + (x < wl ? x : 0)];
-      }
-#pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const uint32_t x = x0 + u * kGThreads + threadIdx.x;
-        if (x < wl) sz[x] = v[u];
-      }
-    }
-    for (int64_t r0 = 0; r0 < nruns; r0 += kGRuns) {
-      const uint32_t nr = uint32_t(nruns - r0 < kGRuns ? nruns - r0 : kGRuns);
-      uint32_t len[kGRuns / kGThreads];
-      uint32_t sum = 0;
-#pragma unroll
-      for (int m = 0; m < kGRuns / kGThreads; ++m) {
-        const uint32_t r = threadIdx.x * (kGRuns / kGThreads) + m;
-        // loads for runs past nr read run r0's bounds and are dropped
-        const uint32_t rr = uint32_t(r0) + (r < nr ? r : 0u);  // < 2^31 (rows * nch)
-        const uint32_t il = rr / uint32_t(nch), c = rr - il * uint32_t(nch);
-        const uint16_t* o = OT + ((i0 + il) * (p.nbk + 1) + kb) * nch + c;
-        const uint32_t a = o[0], b = o[nch];
-        len[m] = r < nr ? b - a : 0u;
-        if (r < nr) {
-          rpos[r] = int32_t((int64_t(c) << kScShift) + a);
-          rrow[r] = uint8_t(il);
-        }
-        sum += len[m];
-      }
-      uint32_t total;
-      uint32_t run = block_exclusive_scan(sum, tmp, &total);
-#pragma unroll
-      for (int m = 0; m < kGRuns / kGThreads; ++m) {
-        pref[threadIdx.x * (kGRuns / kGThreads) + m] = run;
-        run += len[m];
-      }
-      if (threadIdx.x == 0) pref[nr] = total;
-      __syncthreads();
-      for (uint32_t x0 = 0; x0 < total; x0 += kGChunk) {
-        const uint32_t xl = total - x0 < kGChunk ? total - x0 : kGChunk;
-        // run index of every read of the chunk, written by the runs' owners
-#pragma unroll
-        for (int m = 0; m < kGRuns / kGThreads; ++m) {
-          const uint32_t r = threadIdx.x * (kGRuns / kGThreads) + m;
-          if (r < nr) {
-            const uint32_t a = pref[r] > x0 ? pref[r] - x0 : 0u;
-            const uint32_t e = pref[r + 1] - x0 < xl ? pref[r + 1] - x0 : xl;
-            for (uint32_t y = a; y < e && pref[r + 1] > x0; ++y) run_of[y] = uint16_t(r);
-          }
-        }
-        __syncthreads();
-        int64_t pos[kGPer];
-        uint32_t v[kGPer];
-#pragma unroll
-        for (int u = 0; u < kGPer; ++u) {
-          const uint32_t t = u * kGThreads + threadIdx.x;
-          pos[u] = -1;
-          if (t < xl) {
-            const uint32_t r = run_of[t];
-            pos[u] = (i0 + rrow[r]) * p.M_max + rpos[r] + (x0 + t - pref[r]);
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < kGPer; ++u) v[u] = Pk[pos[u] >= 0 ? pos[u] : 0];  // unconditional
-#pragma unroll
-        for (int u = 0; u < kGPer; ++u) {
-          const uint32_t x = (v[u] >> kScShift) - xoff;
-          if (pos[u] >= 0 && x < wl) zP[pos[u]] = sz[x];
-        }
-        __syncthreads();
-      }
-    }
-    __syncthreads();
-  }
+        for (int u = 0; u < kGPer; ++u)
+          if (pos[u] >= 0 && x[u] < wl) zP[pos[u]] = int64_t(L.win[x[u]]);
+      });
 }
 
 constexpr int kUThreads = 1024;
@@ -808,7 +713,7 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
   p.nsc = int32_t(nch);
   const int64_t nblk = s.N * int64_t(nch);
   const int64_t nparts = nblk * kStParts;
-  const uint32_t ngroups = uint32_t(ceil_div(s.N, kGRows));
+  const uint32_t ngroups = gather_ngroups(s.N);
   const int64_t ntiles = int64_t(p.nbk) * ngroups;
   if (nparts >= (int64_t(1) << 31) || ntiles >= (int64_t(1) << 31))
     return fail(NOPFS_ERANGE, "job too large for one launch");
