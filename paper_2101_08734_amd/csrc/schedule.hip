@@ -269,9 +269,21 @@ pf_write(SegParams p, int32_t J, const uint32_t* __restrict__ Pk, const uint8_t*
   __shared__ int32_t s_run[kPfWaves][kPfMaxJ];
   const SubChunk s = sub_chunk(p, nch, blockIdx.x);
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  // codes to stream order (every position of the sub-chunk has one entry)
-  for (int64_t q = threadIdx.x; q < s.len; q += 64 * kPfWaves)
-    s_code[Pk[s.base + q] & kJMask] = code[s.base + q];
+  // codes to stream order (every position of the sub-chunk has one entry),
+  // sixteen entries per thread and step with their loads issued together
+  for (int64_t q0 = 0; q0 < s.len; q0 += 16 * 64 * kPfWaves) {
+    uint32_t j[16];
+    uint8_t c[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int64_t q = q0 + u * 64 * kPfWaves + threadIdx.x;
+      j[u] = Pk[s.base + (q < s.len ? q : 0)];
+      c[u] = code[s.base + (q < s.len ? q : 0)];
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (q0 + u * 64 * kPfWaves + threadIdx.x < s.len) s_code[j[u] & kJMask] = c[u];
+  }
   for (int x = lane; x < J; x += 64) s_wcnt[w][x] = 0;
   __syncthreads();
   const int64_t j0 = int64_t(w) * kPfQuarter;
