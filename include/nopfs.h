@@ -401,6 +401,9 @@ int nopfs_scratch_release(void* hip_stream);
  *   which=3  fail the next internal scratch allocation (value 1)
  *   which=4  longest range of buffer starts the staging schedule keeps in
  *            LDS per chunk (wider ranges take the global-memory search)
+ *   which=5  doublings (at most 4) of the sample windows of the staging
+ *            schedule and the fetch model, so each window tile covers its
+ *            window in several LDS passes, as for F above 2^27
  * The overrides are per host thread: they apply only to calls made from the
  * thread that set them. Meant for tests only. */
 int nopfs_debug_set(int which, int64_t value);

@@ -52,9 +52,9 @@ int make_shape(const nopfs_job* job, Shape* s) {
 // ---------------------------------------------------------------- scratch --
 // Test overrides (nopfs_debug_set): per host thread, so a test that forces a
 // slow path affects only the calls it makes itself.
-static thread_local int64_t g_debug[5] = {0, 0, 0, 0, 0};
+static thread_local int64_t g_debug[6] = {0, 0, 0, 0, 0, 0};
 
-int64_t debug_value(int which) { return (which >= 0 && which < 5) ? g_debug[which] : 0; }
+int64_t debug_value(int which) { return (which >= 0 && which < 6) ? g_debug[which] : 0; }
 
 bool take_alloc_failure() {
   if (g_debug[3]) {
@@ -408,7 +408,7 @@ int nopfs_scratch_release(void* hip_stream) {
 }
 
 int nopfs_debug_set(int which, int64_t value) {
-  if (which < 1 || which > 4 || value < 0) return NOPFS_EINVAL;
+  if (which < 1 || which > 5 || value < 0) return NOPFS_EINVAL;
   g_debug[which] = value;
   return NOPFS_OK;
 }

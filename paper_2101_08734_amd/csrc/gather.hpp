@@ -37,6 +37,14 @@ struct GatherLds {
 
 inline uint32_t gather_ngroups(int64_t N) { return uint32_t(ceil_div(N, kGRows)); }
 
+// Window width (log2) of a gather pass: kGatherWs, or wider by the test
+// hook's doublings (at most 4: the packed partition entries hold 18 bits of
+// offset), so that small jobs take the several-pass path of larger ones.
+inline int gather_ws() {
+  const int64_t x = debug_value(5);
+  return kGatherWs + int(x > 0 ? (x < 4 ? x : 4) : 0);
+}
+
 // Tile `tile` of the pass. value(k) gives sample k's 8-byte value (it is
 // called for k in [0, F) only); emit(pos, row, x, w0, wl) receives kGPer
 // reads of this thread at once: pos[u] the read's index in the row table

@@ -440,7 +440,7 @@ int model_impl(const nopfs_job* job, const int32_t* R, const int8_t* tier, const
   const Rates rt = make_rates(model);
   // one segment per row (the E epochs folded together), cut into spans of
   // 2^14 positions, partitioned by windows of 2^14 samples
-  SegParams p = seg_params(s, kGatherWs);
+  SegParams p = seg_params(s, gather_ws());
   const uint32_t nch = uint32_t(ceil_div(s.M_max, kSC));  // spans per row
   p.emul = int32_t(s.E);
   p.E = 1;

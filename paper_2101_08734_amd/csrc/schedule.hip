@@ -352,7 +352,6 @@ pf_write(SegParams p, int32_t J, const uint32_t* __restrict__ Pk, const uint8_t*
 // epochs folded together), cut into spans of kSC = 2^14 positions: position
 // h lies in span h >> kScShift. The partition of R by sample window is taken
 // over those spans.
-constexpr int kStWs = kGatherWs;  // staging windows: 2^14 samples (128 KB of sizes)
 
 // zP[x] = sizes[k] for every read of the tile's window and rows, x being the
 // read's place in the partitioned row (so zP holds the sizes in partitioned
@@ -718,7 +717,7 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
   if (d0 < 0) return fail(NOPFS_EINVAL, "d0 must be >= 0");
   if (s.M_max == 0) return NOPFS_OK;
   // one segment per row: the E epochs folded together, cut into spans
-  SegParams p = seg_params(s, kStWs);
+  SegParams p = seg_params(s, gather_ws());
   const uint32_t nch = uint32_t(ceil_div(s.M_max, kSC));  // spans per row
   p.emul = int32_t(s.E);
   p.E = 1;

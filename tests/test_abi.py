@@ -262,7 +262,7 @@ def test_strerror(L):
         assert L.nopfs_strerror(c)
     assert L.nopfs_debug_set(0, 1) == nopfs.NOPFS_EINVAL
     assert L.nopfs_debug_set(1, -5) == nopfs.NOPFS_EINVAL
-    assert L.nopfs_debug_set(5, 1) == nopfs.NOPFS_EINVAL
+    assert L.nopfs_debug_set(6, 1) == nopfs.NOPFS_EINVAL
     assert L.nopfs_debug_set(4, 0) == 0
 
 
@@ -282,3 +282,13 @@ def test_noalloc_rejects_a_job_beyond_its_scratch_on_the_host():
     rc = L.nopfs_plan_job_noalloc(ctypes.byref(j), fake, ctypes.cast(caps, ctypes.c_void_p), 2,
                                   fake, fake, fake, fake, fake, fake, None)
     assert rc == nopfs.NOPFS_ERANGE and "E must be" in L.nopfs_last_error().decode()
+
+
+def test_debug_hooks_accept_their_range_only(L):
+    """Test hooks 1 to 5 take values >= 0; other hooks and negative values
+    are EINVAL (host-only calls, no GPU work)."""
+    for which in (1, 2, 3, 4, 5):
+        assert L.nopfs_debug_set(which, 0) == 0
+    assert L.nopfs_debug_set(0, 1) == nopfs.NOPFS_EINVAL
+    assert L.nopfs_debug_set(6, 1) == nopfs.NOPFS_EINVAL
+    assert L.nopfs_debug_set(5, -1) == nopfs.NOPFS_EINVAL

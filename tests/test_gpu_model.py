@@ -111,6 +111,27 @@ def test_matches_oracle(oracle, name, F, E, N, B, d, seed, fr):
     compare(name, job, src_g, t_g, src_o, t_o)
 
 
+@pytest.mark.parametrize("widen", [1, 2, 4])
+@pytest.mark.parametrize("name,F,E,N,B,d,seed,fr", [JOBS[1], JOBS[2], JOBS[9]],
+                         ids=[JOBS[1][0], JOBS[2][0], JOBS[9][0]])
+def test_wide_windows(oracle, name, F, E, N, B, d, seed, fr, widen):
+    """Sample windows widened by the test hook (2^15 to 2^18 samples): each
+    window tile covers its window in 2 to 16 LDS passes, the path of jobs
+    above 2^27 samples."""
+    rjob, sizes, out = _oracle_inputs(oracle, F, E, N, B, d, seed, fr)
+    job = nopfs.Job(F, E, N, B, d, seed)
+    prm = _params(len(fr))
+    src_o, t_o = oracle.fetch_model(rjob, out["R"], out["tier"], sizes, oracle.make_model(**prm))
+    nopfs.debug_set(5, widen)
+    try:
+        src_g, t_g = nopfs.fetch_model(job, _dev(out["R"]), _dev(out["tier"]), _dev(sizes),
+                                       nopfs.make_model(**prm))
+        torch.cuda.synchronize()
+    finally:
+        nopfs.debug_set(5, 0)
+    compare(f"{name} widen={widen}", job, src_g, t_g, src_o, t_o)
+
+
 REGIMES = {
     "io_bound": dict(c=64e9),
     "slow_network": dict(b_c=1e6),

@@ -29,6 +29,7 @@ def _gpu():
     nopfs.lib()
     yield
     nopfs.debug_set(4, 0)
+    nopfs.debug_set(5, 0)
     torch.cuda.empty_cache()
 
 
@@ -119,6 +120,27 @@ def test_staging_global_search_path(oracle, name, F, E, N, B, d, seed, fr, gcap)
             _equal(f"fill d0={d0}", fill, oracle.staging_schedule(rjob, out["R"], sizes, d0))
     finally:
         nopfs.debug_set(4, 0)
+
+
+@pytest.mark.parametrize("widen", [1, 2, 4])
+@pytest.mark.parametrize("name,F,E,N,B,d,seed,fr", [JOBS[1], JOBS[2], JOBS[10]],
+                         ids=[JOBS[1][0], JOBS[2][0], JOBS[10][0]])
+def test_staging_wide_windows(oracle, name, F, E, N, B, d, seed, fr, widen):
+    """Sample windows widened by the test hook (2^15 to 2^18 samples): each
+    window tile covers its window in 2 to 16 LDS passes, the path of jobs
+    above 2^27 samples."""
+    rjob, sizes, caps, out = _oracle_inputs(oracle, F, E, N, B, d, seed, fr)
+    job = nopfs.Job(F, E, N, B, d, seed)
+    R, s = _dev(out["R"]), _dev(sizes)
+    nopfs.debug_set(5, widen)
+    try:
+        for d0 in _d0s(sizes, out["R"], N):
+            fill = nopfs.staging_schedule(job, R, s, d0)
+            torch.cuda.synchronize()
+            _equal(f"fill d0={d0} widen={widen}", fill,
+                   oracle.staging_schedule(rjob, out["R"], sizes, d0))
+    finally:
+        nopfs.debug_set(5, 0)
 
 
 def test_staging_heavy_tailed_sizes(oracle):
