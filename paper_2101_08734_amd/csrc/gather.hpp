@@ -17,8 +17,8 @@
 
 namespace nopfs {
 
-constexpr int kGatherWs = 14;                 // window: 2^14 samples
-constexpr int kGatherWin = 1 << kGatherWs;    // values held in LDS (8 bytes each)
+constexpr int kGatherWs = 14;                 // window: 2^14 samples of 8-byte values
+constexpr int kGatherWin = 1 << kGatherWs;    // 8-byte values held in LDS (128 KB)
 constexpr int kGThreads = 1024;
 constexpr int kGRows = 32;                    // rows per tile
 constexpr int kGRuns = 1024;                  // runs per pass of a tile
@@ -27,7 +27,10 @@ constexpr int kGPer = kGChunk / kGThreads;    // reads per thread and inner pass
 static_assert(kGRuns % kGThreads == 0 && kGChunk % kGThreads == 0, "gather tile shape");
 
 struct GatherLds {
-  uint64_t win[kGatherWin];   // the window's values
+  union {
+    uint64_t win[kGatherWin];        // the window's 8-byte values
+    uint32_t win4[2 * kGatherWin];   // or 4-byte values, twice as many
+  };
   uint32_t pref[kGRuns + 1];  // reads before each run of the pass
   int32_t rpos[kGRuns];       // span start + run start, in the row
   uint8_t rrow[kGRuns];       // row - first row of the tile
@@ -45,13 +48,13 @@ inline int gather_ws() {
   return kGatherWs + int(x > 0 ? (x < 4 ? x : 4) : 0);
 }
 
-// Tile `tile` of the pass. value(k) gives sample k's 8-byte value (it is
-// called for k in [0, F) only); emit(pos, row, x, w0, wl) receives kGPer
-// reads of this thread at once: pos[u] the read's index in the row table
-// ([N][M_max], -1 for none), row[u] its row, x[u] its sample's offset in the
-// window pass starting at sample w0 (valid when x[u] < wl), with the window's
-// values in L.win.
-template <typename Value, typename Emit>
+// Tile `tile` of the pass. value(k) gives sample k's value of type V (8 or
+// 4 bytes; it is called for k in [0, F) only); emit(pos, row, x, w0, wl)
+// receives kGPer reads of this thread at once: pos[u] the read's index in the
+// row table ([N][M_max], -1 for none), row[u] its row, x[u] its sample's
+// offset in the window pass starting at sample w0 (valid when x[u] < wl),
+// with the window's values in L.win (V = uint64_t) or L.win4 (uint32_t).
+template <typename V, typename Value, typename Emit>
 __device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* __restrict__ Pk,
                                             const uint16_t* __restrict__ OT, uint32_t tile,
                                             uint32_t ngroups, GatherLds& L, Value value,
@@ -63,12 +66,14 @@ __device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* 
   const int64_t nruns = rows * nch;  // < 2^31
   const int64_t k0 = int64_t(kb) << p.ws;
   const int64_t kend = k0 + (int64_t(1) << p.ws) < p.F ? k0 + (int64_t(1) << p.ws) : p.F;
-  for (int64_t w0 = k0; w0 < kend; w0 += kGatherWin) {  // one pass unless windows are wider
-    const uint32_t wl = uint32_t(kend - w0 < kGatherWin ? kend - w0 : kGatherWin);
+  constexpr int kWin = int(kGatherWin * sizeof(uint64_t) / sizeof(V));  // values per pass
+  V* win = sizeof(V) == 8 ? reinterpret_cast<V*>(L.win) : reinterpret_cast<V*>(L.win4);
+  for (int64_t w0 = k0; w0 < kend; w0 += kWin) {  // one pass unless windows are wider
+    const uint32_t wl = uint32_t(kend - w0 < kWin ? kend - w0 : kWin);
     const uint32_t xoff = uint32_t(w0 - k0);
     // the window's values, sixteen loads per thread in flight at once
     for (uint32_t x0 = 0; x0 < wl; x0 += 16 * kGThreads) {
-      uint64_t v[16];
+      V v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const uint32_t x = x0 + u * kGThreads + threadIdx.x;
@@ -77,7 +82,7 @@ __device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* 
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const uint32_t x = x0 + u * kGThreads + threadIdx.x;
-        if (x < wl) L.win[x] = v[u];
+        if (x < wl) win[x] = v[u];
       }
     }
     for (int64_t r0 = 0; r0 < nruns; r0 += kGRuns) {

@@ -153,7 +153,7 @@ fm_gather(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
   load_rates(rt, sr);  // visible after the tile's first barrier
-  gather_tile(
+  gather_tile<uint64_t>(
       p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return szb[k]; },
       [&](const int64_t (&pos)[kGPer], const int64_t (&row)[kGPer], const uint32_t (&x)[kGPer],
           int64_t w0, uint32_t wl) {

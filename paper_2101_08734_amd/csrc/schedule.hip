@@ -38,12 +38,14 @@
 // The staging passes fold each row's E epochs into one segment of E * L_i
 // reads, cut into spans of 2^14 positions, and partition the spans by
 // windows of 2^14 samples:
+//   st_range  -- whether every size fits 32 bits (then the sizes travel as
+//                4-byte values, else as 8-byte ones).
 //   st_gather -- per (window, group of 32 workers): the window's sizes in
 //                LDS (128 KB); every read of the group's spans gets its
 //                sample's size, written in partitioned order.
-//   st_unpart -- per span (in place): the sizes back in stream order in LDS,
-//                their inclusive prefix sums inside the span (a wave scan
-//                per 64 positions, in registers), the span's total.
+//   st_unpart -- per span: the sizes back in stream order in LDS, their
+//                inclusive prefix sums inside the span (a wave scan per 64
+//                positions, in registers), the span's total.
 //   st_base   -- per worker: exclusive scan of the span totals.
 //   st_bounds -- per quarter of a span (4096 positions): the g of its first
 //                and of its last position (binary search over S; g never
@@ -356,21 +358,50 @@ pf_write(SegParams p, int32_t J, const uint32_t* __restrict__ Pk, const uint8_t*
 // zP[x] = sizes[k] for every read of the tile's window and rows, x being the
 // read's place in the partitioned row (so zP holds the sizes in partitioned
 // order).
+// With every size in [0, 2^32) (*wide == 0, found by st_range) the sizes go
+// out as 4-byte values into zc, else as 8-byte values into zP.
 __global__ void __launch_bounds__(kGThreads)
 st_gather(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
-          const int64_t* __restrict__ sizes, int64_t* __restrict__ zP, uint32_t ngroups,
-          uint32_t ntiles) {
+          const int64_t* __restrict__ sizes, const uint32_t* __restrict__ wide,
+          uint32_t* __restrict__ zc, int64_t* __restrict__ zP, uint32_t ngroups, uint32_t ntiles) {
   __shared__ GatherLds L;
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
-  gather_tile(
-      p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return uint64_t(sizes[k]); },
-      [&](const int64_t (&pos)[kGPer], const int64_t (&)[kGPer], const uint32_t (&x)[kGPer],
-          int64_t, uint32_t wl) {
+  if (*wide != 0u) {  // uniform
+    gather_tile<uint64_t>(
+        p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return uint64_t(sizes[k]); },
+        [&](const int64_t (&pos)[kGPer], const int64_t (&)[kGPer], const uint32_t (&x)[kGPer],
+            int64_t, uint32_t wl) {
 #pragma unroll
-        for (int u = 0; u < kGPer; ++u)
-          if (pos[u] >= 0 && x[u] < wl) zP[pos[u]] = int64_t(L.win[x[u]]);
-      });
+          for (int u = 0; u < kGPer; ++u)
+            if (pos[u] >= 0 && x[u] < wl) zP[pos[u]] = int64_t(L.win[x[u]]);
+        });
+  } else {
+    gather_tile<uint32_t>(
+        p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return uint32_t(sizes[k]); },
+        [&](const int64_t (&pos)[kGPer], const int64_t (&)[kGPer], const uint32_t (&x)[kGPer],
+            int64_t, uint32_t wl) {
+#pragma unroll
+          for (int u = 0; u < kGPer; ++u)
+            if (pos[u] >= 0 && x[u] < wl) zc[pos[u]] = L.win4[x[u]];
+        });
+  }
+}
+
+// *wide = 1 when some size lies outside [0, 2^32); st_flag clears it first.
+__global__ void st_flag(uint32_t* __restrict__ wide) { *wide = 0u; }
+
+__global__ void __launch_bounds__(256)
+st_range(int64_t F, const int64_t* __restrict__ sizes, uint32_t* __restrict__ wide) {
+  const int64_t k0 = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 4;
+  bool out = false;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int64_t k = k0 + u;
+    const uint64_t v = uint64_t(sizes[k < F ? k : 0]);
+    out |= k < F && (v >> 32) != 0;
+  }
+  if (__any(out) && __lane_id() == 0) atomicOr(wide, 1u);
 }
 
 constexpr int kUThreads = 1024;
@@ -391,8 +422,10 @@ __device__ __forceinline__ int64_t span_len(const SegParams& p, int64_t i, int64
   return len < 0 ? 0 : (len > kSC ? kSC : len);
 }
 
+template <bool kWide>
 __device__ __forceinline__ void span_load(const SegParams& p, const uint32_t* __restrict__ Pk,
-                                          const int64_t* __restrict__ zS, int64_t b, int64_t nblk,
+                                          const int64_t* __restrict__ zS,
+                                          const uint32_t* __restrict__ zc, int64_t b, int64_t nblk,
                                           SpanRegs& g) {
   int64_t len = 0, base = 0;
   if (b < nblk) {
@@ -405,7 +438,7 @@ __device__ __forceinline__ void span_load(const SegParams& p, const uint32_t* __
     const int64_t q = int64_t(u) * kUThreads + threadIdx.x;
     const int64_t at = base + (q < len ? q : 0);
     g.j[u] = Pk[at];
-    g.z[u] = zS[at];
+    g.z[u] = kWide ? zS[at] : int64_t(zc[at]);
   }
 }
 
@@ -420,15 +453,21 @@ __device__ __forceinline__ void span_load(const SegParams& p, const uint32_t* __
 // the LDS a CU has for one workgroup, so each workgroup walks spans b,
 // b + gridDim.x, ... and loads the next span's entries before it scans the
 // current one.
+// kWide: the sizes are 8-byte values in zS (and S overwrites them in place);
+// otherwise 4-byte values in zc. Both forms are launched; the one that does
+// not match *wide returns at once.
+template <bool kWide>
 __global__ void __launch_bounds__(kUThreads)
-st_unpart(SegParams p, const uint32_t* __restrict__ Pk, int64_t* __restrict__ zS,
-          int64_t* __restrict__ ctot, int64_t nblk) {
+st_unpart(SegParams p, const uint32_t* __restrict__ Pk, const uint32_t* __restrict__ wide,
+          const uint32_t* __restrict__ zc, int64_t* __restrict__ zS, int64_t* __restrict__ ctot,
+          int64_t nblk) {
   __shared__ int64_t sv[kSC];
   __shared__ uint64_t wtot[kUWaves];
   const uint32_t lane = __lane_id(), wave = threadIdx.x >> 6;
   const int64_t q0 = int64_t(wave) * (kURows * 64) + lane;
+  if ((*wide != 0u) != kWide) return;  // uniform
   SpanRegs g;
-  span_load(p, Pk, zS, blockIdx.x, nblk, g);
+  span_load<kWide>(p, Pk, zS, zc, blockIdx.x, nblk, g);
   for (int64_t b = blockIdx.x; b < nblk; b += gridDim.x) {
     const int64_t i = b / p.nsc, c = b - i * p.nsc;
     const int64_t len = span_len(p, i, c);
@@ -437,7 +476,7 @@ st_unpart(SegParams p, const uint32_t* __restrict__ Pk, int64_t* __restrict__ zS
       if (int64_t(u) * kUThreads + threadIdx.x < len) sv[g.j[u] & kJMask] = g.z[u];
     __syncthreads();
     // the next span's entries are in flight while this one is scanned
-    span_load(p, Pk, zS, b + gridDim.x, nblk, g);
+    span_load<kWide>(p, Pk, zS, zc, b + gridDim.x, nblk, g);
     // the wave's total first, so that each row is written as soon as it is scanned
     uint64_t lsum = 0;
 #pragma unroll 4
@@ -717,7 +756,9 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
   if (d0 < 0) return fail(NOPFS_EINVAL, "d0 must be >= 0");
   if (s.M_max == 0) return NOPFS_OK;
   // one segment per row: the E epochs folded together, cut into spans
-  SegParams p = seg_params(s, gather_ws());
+  // windows of 2^15 samples: one LDS pass of 4-byte sizes, two of 8-byte
+  // ones (at most 2^18: the packed partition entries hold 18 bits of offset)
+  SegParams p = seg_params(s, gather_ws() + 1 < 18 ? gather_ws() + 1 : 18);
   const uint32_t nch = uint32_t(ceil_div(s.M_max, kSC));  // spans per row
   p.emul = int32_t(s.E);
   p.E = 1;
@@ -729,21 +770,30 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
   if (nparts >= (int64_t(1) << 31) || ntiles >= (int64_t(1) << 31))
     return fail(NOPFS_ERANGE, "job too large for one launch");
   Scratch scr(st);
-  uint32_t* Pk;
+  uint32_t *Pk, *zc, *wide;
   uint16_t* OT;
   int64_t *S, *ctot;
   int4* bnd;
+  if ((rc = scr.alloc_n(&wide, 1))) return rc;
+  if ((rc = launch("st_flag", st_flag, dim3(1), dim3(1), 0, st, wide))) return rc;
+  if ((rc = launch("st_range", st_range, dim3(uint32_t(ceil_div(s.F, 1024))), dim3(256), 0, st, s.F,
+                   sizes, wide)))
+    return rc;
   if ((rc = run_partition(p, R, scr, &Pk, &OT, st))) return rc;
   if ((rc = scr.alloc_n(&S, size_t(s.N * s.M_max)))) return rc;
+  if ((rc = scr.alloc_n(&zc, size_t(s.N * s.M_max)))) return rc;
   if ((rc = scr.alloc_n(&ctot, size_t(nblk)))) return rc;
   if ((rc = scr.alloc_n(&bnd, size_t(nparts)))) return rc;
   if ((rc = launch("st_gather", st_gather, dim3(xcd_padded(uint32_t(ntiles))), dim3(kGThreads), 0,
-                   st, p, (const uint32_t*)Pk, (const uint16_t*)OT, sizes, S, ngroups,
-                   uint32_t(ntiles))))
+                   st, p, (const uint32_t*)Pk, (const uint16_t*)OT, sizes, (const uint32_t*)wide, zc,
+                   S, ngroups, uint32_t(ntiles))))
     return rc;
   const int64_t ugrid = nblk < 1024 ? nblk : 1024;
-  if ((rc = launch("st_unpart", st_unpart, dim3(uint32_t(ugrid)), dim3(kUThreads), 0, st, p,
-                   (const uint32_t*)Pk, S, ctot, nblk)))
+  if ((rc = launch("st_unpart", st_unpart<false>, dim3(uint32_t(ugrid)), dim3(kUThreads), 0, st, p,
+                   (const uint32_t*)Pk, (const uint32_t*)wide, (const uint32_t*)zc, S, ctot, nblk)))
+    return rc;
+  if ((rc = launch("st_unpart8", st_unpart<true>, dim3(uint32_t(ugrid)), dim3(kUThreads), 0, st, p,
+                   (const uint32_t*)Pk, (const uint32_t*)wide, (const uint32_t*)zc, S, ctot, nblk)))
     return rc;
   if ((rc = launch("st_base", st_base, dim3(uint32_t(s.N)), dim3(1024), 0, st, nch, ctot))) return rc;
   if ((rc = launch("st_bounds", st_bounds, dim3(uint32_t(ceil_div(nparts, 256))), dim3(256), 0, st,

@@ -159,6 +159,25 @@ def test_staging_heavy_tailed_sizes(oracle):
         _equal(f"fill d0={d0}", fill, oracle.staging_schedule(rjob, R, sizes, d0))
 
 
+@pytest.mark.parametrize("frac", [0.0005, 1.0])
+def test_staging_sizes_beyond_32_bits(oracle, frac):
+    """Sizes of 2^32 bytes and more (a share `frac` of the samples, the rest
+    as usual) make the staging passes carry 8-byte sizes instead of 4-byte
+    ones; the schedule must not depend on which."""
+    F, E, N, B, d, seed = 60_000, 4, 3, 16, 0, 23
+    rng = np.random.default_rng(7)
+    sizes = wl.random_sizes(F, seed, 1_000, 2_000_000)
+    big = rng.random(F) < frac
+    sizes = np.where(big, (1 << 32) + rng.integers(0, 1 << 34, F), sizes).astype(np.int64)
+    rjob = oracle.make_job(F, E, N, B, d, seed)
+    R = oracle.access_streams(rjob)
+    job = nopfs.Job(F, E, N, B, d, seed)
+    for d0 in _d0s(sizes, R, N) + [(1 << 32) - 1, 1 << 32, 5 << 32]:
+        fill = nopfs.staging_schedule(job, _dev(R), _dev(sizes), d0)
+        torch.cuda.synchronize()
+        _equal(f"fill d0={d0}", fill, oracle.staging_schedule(rjob, R, sizes, d0))
+
+
 def test_equal_sizes_closed_form(oracle):
     """Equal sizes s and a buffer of m*s bytes: fill(h) = max(0, h - m + 1)."""
     F, E, N, B = 50_000, 3, 4, 8
