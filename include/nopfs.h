@@ -233,8 +233,8 @@ int nopfs_prefetch_order(const nopfs_job* job, const int32_t* R, const int8_t* t
  *          values give unspecified but in-bounds results).
  *   d0:    staging buffer capacity in bytes, >= 0.
  *   fill:  int32 [N][M_max], output.
- * Scratch: about 12 bytes per stream position, plus 4 bytes per (span of
- * 16384 positions of a row, window of 16384 samples). Errors: EINVAL (also d0 < 0),
+ * Scratch: about 16 bytes per stream position, plus 4 bytes per (span of
+ * 16384 positions of a row, window of 32768 samples). Errors: EINVAL (also d0 < 0),
  * ERANGE, ENOMEM, EDEVICE. */
 int nopfs_staging_schedule(const nopfs_job* job, const int32_t* R, const int64_t* sizes,
                            int64_t d0, int32_t* fill, void* hip_stream);
