@@ -193,31 +193,53 @@ __device__ __forceinline__ double wave_incl_max(double v) {
   return v;
 }
 
-// Exclusive prefix (sum, or max with -inf as identity) of v over the
-// workgroup; *total gets the sum / maximum of all. tmp holds 65 doubles.
-template <bool kMax>
-__device__ __forceinline__ double block_excl(double v, double* tmp, double* total) {
+// Exclusive prefix scans over the workgroup (blockDim.x a multiple of 64):
+// two sums at once, or a maximum with -inf as identity; the totals go to
+// *tot*. No closing barrier: the caller's next use of tmp comes after later
+// barriers. tmp holds 65 entries.
+__device__ __forceinline__ void block_excl_sum2(double a, double u, double2* tmp, double* exa,
+                                                double* exu, double* tota, double* totu) {
   const int lane = __lane_id();
   const int wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
-  const double id = kMax ? -INFINITY : 0.0;
-  const double inc = kMax ? wave_incl_max(v) : wave_incl_sum(v);
+  const double ia = wave_incl_sum(a), iu = wave_incl_sum(u);
+  if (lane == 63) tmp[wave] = make_double2(ia, iu);
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const double2 w = threadIdx.x < unsigned(nwaves) ? tmp[threadIdx.x] : make_double2(0.0, 0.0);
+    const double wa = wave_incl_sum(w.x), wu = wave_incl_sum(w.y);
+    const double pa = __shfl_up(wa, 1, 64), pu = __shfl_up(wu, 1, 64);
+    if (threadIdx.x < unsigned(nwaves))
+      tmp[threadIdx.x] = threadIdx.x == 0 ? make_double2(0.0, 0.0) : make_double2(pa, pu);
+    if (threadIdx.x == 63) tmp[64] = make_double2(wa, wu);
+  }
+  __syncthreads();
+  const double ba = __shfl_up(ia, 1, 64), bu = __shfl_up(iu, 1, 64);
+  const double2 tw = tmp[wave];
+  *exa = tw.x + (lane == 0 ? 0.0 : ba);
+  *exu = tw.y + (lane == 0 ? 0.0 : bu);
+  *tota = tmp[64].x;
+  *totu = tmp[64].y;
+}
+
+__device__ __forceinline__ double block_excl_max(double v, double* tmp, double* total) {
+  const int lane = __lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  const double inc = wave_incl_max(v);
   if (lane == 63) tmp[wave] = inc;
   __syncthreads();
   if (threadIdx.x < 64) {
-    const double w = threadIdx.x < unsigned(nwaves) ? tmp[threadIdx.x] : id;
-    const double wi = kMax ? wave_incl_max(w) : wave_incl_sum(w);
+    const double w = threadIdx.x < unsigned(nwaves) ? tmp[threadIdx.x] : -INFINITY;
+    const double wi = wave_incl_max(w);
     const double prev = __shfl_up(wi, 1, 64);
-    if (threadIdx.x < unsigned(nwaves)) tmp[threadIdx.x] = threadIdx.x == 0 ? id : prev;
+    if (threadIdx.x < unsigned(nwaves)) tmp[threadIdx.x] = threadIdx.x == 0 ? -INFINITY : prev;
     if (threadIdx.x == 63) tmp[64] = wi;
   }
   __syncthreads();
   const double before_lane = __shfl_up(inc, 1, 64);
-  const double in_wave = lane == 0 ? id : before_lane;
-  const double r = kMax ? fmax(tmp[wave], in_wave) : tmp[wave] + in_wave;
   *total = tmp[64];
-  __syncthreads();
-  return r;
+  return fmax(tmp[wave], lane == 0 ? -INFINITY : before_lane);
 }
 
 // LDS slot of position p: one pad per 32 positions, so the four
@@ -226,8 +248,10 @@ __device__ __forceinline__ double block_excl(double v, double* tmp, double* tota
 __device__ __forceinline__ int fm_slot(int p) { return p + (p >> 5); }
 
 struct FmLds {
-  uint64_t sv[kSC + kSC / 32];  // the sub-chunk's entries by position, then results
-  double tmp[65];
+  uint64_t sv[kSC + kSC / 32];  // the span's entries by position, then results
+  double2 tmp2[65];             // the two sum scans
+  double tmpm[65];              // the maximum scan
+  uint16_t code[kFmPart + kFmPart / 32];  // a part's source codes for the transpose
   SharedRates sr;
 };
 
@@ -239,27 +263,42 @@ struct Enter {
 
 // One sub-chunk in stream order: per position, its code and the scans.
 // kFinal: also the consumption times t and source codes, written out.
-template <bool kFinal>
-__device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* __restrict__ Pk,
-                         const uint64_t* __restrict__ zP, const Rates& rt, FmLds& L, Enter in,
-                         Enter* sum_out, int16_t* __restrict__ src, double* __restrict__ tout) {
-  // every entry of the sub-chunk, loaded once and coalesced, into the LDS
-  // slot of its stream position
-  {
-    // all of the thread's loads at once (clamped), then the LDS stores
-    uint32_t j[kFmEnt];
-    uint64_t v[kFmEnt];
+// A span's entries as loaded by one thread: entries t, t + kFmThreads, ...
+// of its partitioned order (packed position, size and source). The loads
+// are unconditional (past the span's end they read its first entry and are
+// dropped when stored), so they are in flight together.
+struct FmRegs {
+  uint32_t j[kFmEnt];
+  uint64_t v[kFmEnt];
+};
+
+__device__ __forceinline__ void fm_load(const SubChunk& s, const uint32_t* __restrict__ Pk,
+                                        const uint64_t* __restrict__ zP, bool valid, FmRegs& g) {
+  const int64_t base = valid ? s.base : 0, len = valid ? s.len : 0;
 #pragma unroll
-    for (int u = 0; u < kFmEnt; ++u) {
-      const int64_t q = int64_t(u) * kFmThreads + threadIdx.x;
-      j[u] = Pk[s.base + (q < s.len ? q : 0)];
-      v[u] = zP[s.base + (q < s.len ? q : 0)];
-    }
-#pragma unroll
-    for (int u = 0; u < kFmEnt; ++u)
-      if (int64_t(u) * kFmThreads + threadIdx.x < s.len) L.sv[fm_slot(int(j[u] & kJMask))] = v[u];
+  for (int u = 0; u < kFmEnt; ++u) {
+    const int64_t q = int64_t(u) * kFmThreads + threadIdx.x;
+    g.j[u] = Pk[base + (q < len ? q : 0)];
+    g.v[u] = zP[base + (q < len ? q : 0)];
   }
+}
+
+// Every entry of the span into the LDS slot of its stream position. Ends
+// with a barrier.
+__device__ __forceinline__ void fm_place(const SubChunk& s, const FmRegs& g, FmLds& L) {
+#pragma unroll
+  for (int u = 0; u < kFmEnt; ++u)
+    if (int64_t(u) * kFmThreads + threadIdx.x < s.len) L.sv[fm_slot(int(g.j[u] & kJMask))] = g.v[u];
   __syncthreads();
+}
+
+// One span in stream order, its entries in L.sv: per position, its code
+// and the scans. kFinal: also the consumption times t and source codes,
+// written out. Ends with a barrier.
+template <bool kFinal>
+__device__ void fm_chunk(const SegParams& p, const SubChunk& s, const Rates& rt, FmLds& L,
+                         Enter in, Enter* sum_out, int16_t* __restrict__ src,
+                         double* __restrict__ tout) {
   const double inv_p0 = 1.0 / rt.p0;
   double ca = 0, cu = 0, cm = -INFINITY;  // running over the parts, relative to the chunk
   const double base_mu = in.a * inv_p0 - in.u;
@@ -285,9 +324,8 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
       ta += rd[u];
       tu += uu[u];
     }
-    double tota, totu;
-    const double exa = block_excl<false>(ta, L.tmp, &tota);
-    const double exu = block_excl<false>(tu, L.tmp, &totu);
+    double tota, totu, exa, exu;
+    block_excl_sum2(ta, tu, L.tmp2, &exa, &exu, &tota, &totu);
     // avail - U at each position, relative to the chunk start
     double mv[kFmPer];
     double ra = ca + exa, ru = cu + exu, tm = -INFINITY;
@@ -300,7 +338,7 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
       tm = fmax(tm, mv[u]);
     }
     double totm;
-    const double exm = block_excl<true>(tm, L.tmp, &totm);
+    const double exm = block_excl_max(tm, L.tmpm, &totm);
     if (kFinal) {
       // t at each position: U(f) + max(what entered, base + best so far)
       double tv[kFmPer];
@@ -312,30 +350,25 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
         tv[u] = (in.u + uf) + fmax(in.m, base_mu + run);
         uf += uu[u];
       }
-      __syncthreads();  // every entry is read
+      // t into the slots this thread read its entries from, codes into their
+      // own table; one barrier, then both go out in stream order
 #pragma unroll
-      for (int u = 0; u < kFmPer; ++u)
-        L.sv[fm_slot(jb + int(threadIdx.x) * kFmPer + u)] = __double_as_longlong(tv[u]);
+      for (int u = 0; u < kFmPer; ++u) {
+        const int x = int(threadIdx.x) * kFmPer + u;
+        L.sv[fm_slot(jb + x)] = __double_as_longlong(tv[u]);
+        const uint32_t c = cd[u];
+        L.code[fm_slot(x)] = uint16_t(c == 0 ? 0u : (c < kOwn0 ? 128u + (c - 1) : 256u + (c - kOwn0)));
+      }
       __syncthreads();
       double* td = tout + s.base + j0;
-#pragma unroll
-      for (int u = 0; u < kFmPer; ++u) {
-        const int x = u * kFmThreads + int(threadIdx.x);
-        if (x < int(hl)) stream_store(td + x, __longlong_as_double(L.sv[fm_slot(jb + x)]));
-      }
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < kFmPer; ++u) {
-        const uint32_t c = cd[u];
-        const uint64_t out = c == 0 ? 0u : (c < kOwn0 ? 128u + (c - 1) : 256u + (c - kOwn0));
-        L.sv[fm_slot(jb + int(threadIdx.x) * kFmPer + u)] = out;
-      }
-      __syncthreads();
       int16_t* sd = src + s.base + j0;
 #pragma unroll
       for (int u = 0; u < kFmPer; ++u) {
         const int x = u * kFmThreads + int(threadIdx.x);
-        if (x < int(hl)) stream_store(sd + x, int16_t(L.sv[fm_slot(jb + x)]));
+        if (x < int(hl)) {
+          stream_store(td + x, __longlong_as_double(L.sv[fm_slot(jb + x)]));
+          stream_store(sd + x, int16_t(L.code[fm_slot(x)]));
+        }
       }
     }
     ca += tota;
@@ -346,15 +379,20 @@ __device__ void fm_chunk(const SegParams& p, const SubChunk& s, const uint32_t* 
   if (!kFinal && threadIdx.x == 0) *sum_out = Enter{ca, cu, cm};
 }
 
-// two workgroups per CU
+// One workgroup per span and per CU (the span takes 135 KB of LDS).
+// Walking several spans per workgroup with the next span's entries requested
+// during the scan needs 48 more registers than the scan leaves: the spills
+// made it slower (3.0 and 5.2 ms against 2.8 and 3.7).
 __global__ void __launch_bounds__(kFmThreads)
 fm_sum(SegParams p, const uint32_t* __restrict__ Pk, const uint64_t* __restrict__ zP, Rates rt,
        uint32_t nch, Enter* __restrict__ sums) {
   __shared__ FmLds L;
   load_rates(rt, L.sr);
   const SubChunk s = sub_chunk(p, nch, blockIdx.x);
-  __syncthreads();
-  fm_chunk<false>(p, s, Pk, zP, rt, L, Enter{0, 0, 0}, &sums[s.i * nch + s.c], nullptr, nullptr);
+  FmRegs g;
+  fm_load(s, Pk, zP, true, g);
+  fm_place(s, g, L);  // its barrier also publishes the rates
+  fm_chunk<false>(p, s, rt, L, Enter{0, 0, 0}, &sums[s.i * nch + s.c], nullptr, nullptr);
 }
 
 // In place: sums[i][c] becomes what enters sub-chunk c.
@@ -381,6 +419,8 @@ fm_final(SegParams p, const uint32_t* __restrict__ Pk, const uint64_t* __restric
   __shared__ FmLds L;
   load_rates(rt, L.sr);
   const SubChunk s = sub_chunk(p, nch, blockIdx.x);
+  FmRegs g;
+  fm_load(s, Pk, zP, true, g);
   if (s.c == int64_t(nch) - 1) {
     // the row's padding past its last read
     for (int64_t f = int64_t(p.E) * s.Li + threadIdx.x; f < p.M_max; f += kFmThreads) {
@@ -388,8 +428,8 @@ fm_final(SegParams p, const uint32_t* __restrict__ Pk, const uint64_t* __restric
       t[s.i * p.M_max + f] = -1.0;
     }
   }
-  __syncthreads();
-  fm_chunk<true>(p, s, Pk, zP, rt, L, ins[s.i * nch + s.c], nullptr, src, t);
+  fm_place(s, g, L);
+  fm_chunk<true>(p, s, rt, L, ins[s.i * nch + s.c], nullptr, src, t);
 }
 
 Rates make_rates(const nopfs_model* m) {
