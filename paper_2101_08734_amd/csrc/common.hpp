@@ -191,7 +191,10 @@ __device__ __forceinline__ uint64_t read_lane64(uint64_t v, int lane) {
 
 // Exclusive scan over the whole workgroup (blockDim.x a multiple of 64, at
 // most 1024). `tmp` holds one slot per wave plus one. Returns the exclusive
-// prefix of v; *total receives the sum over the block.
+// prefix of v; *total receives the sum over the block. kClose = false leaves
+// out the closing barrier, for callers that pass another barrier before tmp
+// is written again.
+template <bool kClose = true>
 __device__ inline uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp,
                                                 uint32_t* total) {
   const int lane = __lane_id();
@@ -209,7 +212,7 @@ __device__ inline uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp,
   __syncthreads();
   uint32_t r = tmp[wave] + inc - v;
   *total = tmp[64];
-  __syncthreads();
+  if (kClose) __syncthreads();
   return r;
 }
 
@@ -245,7 +248,7 @@ __device__ inline uint32_t block_scan_array(uint32_t* a, uint32_t n, uint32_t* t
   uint32_t sum = 0;
   for (uint32_t b = b0; b < b1; ++b) sum += a[b];
   uint32_t total;
-  uint32_t run = block_exclusive_scan(sum, tmp, &total);
+  uint32_t run = block_exclusive_scan<false>(sum, tmp, &total);  // the barrier below closes it
   for (uint32_t b = b0; b < b1; ++b) {
     const uint32_t v = a[b];
     a[b] = run;

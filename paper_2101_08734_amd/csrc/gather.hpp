@@ -105,7 +105,7 @@ __device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* 
         sum += len[m];
       }
       uint32_t total;
-      uint32_t run = block_exclusive_scan(sum, L.tmp, &total);
+      uint32_t run = block_exclusive_scan<false>(sum, L.tmp, &total);  // closed below
 #pragma unroll
       for (int m = 0; m < kGRuns / kGThreads; ++m) {
         L.pref[threadIdx.x * (kGRuns / kGThreads) + m] = run;

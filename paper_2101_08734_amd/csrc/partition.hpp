@@ -71,7 +71,7 @@ __device__ __forceinline__ uint32_t load_runs(const SegParams& p, int64_t i, uin
     rt.start[threadIdx.x] = int32_t(e * Li + sc * kSC + a);
   }
   uint32_t total;
-  const uint32_t ex = block_exclusive_scan(len, rt.tmp, &total);
+  const uint32_t ex = block_exclusive_scan<false>(len, rt.tmp, &total);  // closed below
   rt.pref[threadIdx.x] = ex;
   if (total <= kRunMap)
     for (uint32_t q = 0; q < len; ++q) rt.run_of[ex + q] = uint16_t(threadIdx.x);

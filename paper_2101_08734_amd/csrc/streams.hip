@@ -261,7 +261,7 @@ stream_scatter(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t*
       const uint32_t w0 = 2 * threadIdx.x, w1 = w0 + 1;
       const uint32_t v0 = w0 < nw ? cntw[w0] : 0u, v1 = w1 < nw ? cntw[w1] : 0u;
       const uint32_t s = (v0 & 0xFFFFu) + (v0 >> 16) + (v1 & 0xFFFFu) + (v1 >> 16);
-      uint32_t ex = block_exclusive_scan(s, tmp, &total);
+      uint32_t ex = block_exclusive_scan<false>(s, tmp, &total);  // closed below
       if (w0 < nw) {
         const uint32_t a = ex, b = a + (v0 & 0xFFFFu);
         cntw[w0] = a | (b << 16);
@@ -472,7 +472,7 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
       sum += (v[j] & 0xFFFFu) + (v[j] >> 16);
     }
     uint32_t total;
-    uint32_t ex = block_exclusive_scan(sum, reinterpret_cast<uint32_t*>(kv), &total);
+    uint32_t ex = block_exclusive_scan<false>(sum, reinterpret_cast<uint32_t*>(kv), &total);  // closed below
 #pragma unroll
     for (int j = 0; j < kPerW; ++j) {
       const uint32_t lo16 = ex;
