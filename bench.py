@@ -59,9 +59,8 @@ STAGES = {
 
 
 def stage_bytes(job, M_w):
-    """Algorithmic bytes of each stage per step, as the measurement section
-    of the survey defines them for the C ABI's dense layouts (A reads, N*F
-    cells): streams write R (4A; the key/id exchange allowance 16*E*F is
+    """Algorithmic bytes of each stage per step for the C ABI's dense layouts
+    (A reads, N*F cells): streams write R (4A; the key/id exchange allowance 16*E*F is
     reported beside it), stats read R and write count + first (4A + 5NF),
     next reads R and writes next (8A), the plan reads count, first and sizes
     and writes tier (6NF + 8F)."""

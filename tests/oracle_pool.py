@@ -25,7 +25,7 @@ OUTPUTS = ("R", "count", "first", "next", "tier", "used")
 
 def pool_threads() -> int:
     """Worker threads: the host's cores, at most 16 (the CPU share of a
-    one-GPU machine)."""
+    one-GPU host)."""
     return max(1, min(16, os.cpu_count() or 1))
 
 
