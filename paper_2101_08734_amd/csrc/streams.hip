@@ -383,6 +383,11 @@ __device__ void sort_in_global(const StreamParams& p, const uint32_t* ob, uint32
 constexpr int kSortDigitBits = 13;
 constexpr int kSortDigits = 1 << kSortDigitBits;
 constexpr int kCountWords = kSortDigits / 2;
+constexpr uint32_t kSlotBits = 13;  // bits of a counting-sort slot
+static_assert(kSortCap <= (1 << kSlotBits), "slots fit kSlotBits");
+// kb has 32 - cbits bits and C >= kRound, so cbits >= kSlotBits and
+// kb << kSlotBits | slot fits 32 bits
+static_assert((1 << kSlotBits) <= kRound, "kb and slot fit one word");
 static_assert(kMaxChunks + 1 + (kSortCap >> kBlkShift) / 2 <= kCountWords,
               "the run table fits the digit counts' space");
 
@@ -482,23 +487,28 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
     }
   }
   __syncthreads();
-  uint32_t* kbs = reinterpret_cast<uint32_t*>(kv);  // [kSortCap] kb by counting-sort slot
+  // Each counting-sort slot holds kb << kSlotBits | slot: one comparison
+  // orders two entries by (kb, slot), and an entry of a later digit group
+  // compares above every entry of an earlier one.
+  constexpr uint32_t kGroupLoads = 4;
+  uint32_t* kbs = reinterpret_cast<uint32_t*>(kv);  // [kSortCap + kGroupLoads] by slot
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
     if (q < n) {
       pos[r] += h16[kb[r] >> dshift];
-      kbs[pos[r]] = kb[r];
+      kbs[pos[r]] = (kb[r] << kSlotBits) | pos[r];
     }
   }
+  if (threadIdx.x < kGroupLoads) kbs[n + threadIdx.x] = 0xFFFFFFFFu;  // above every entry
   __syncthreads();
   // Inside its digit group (about two entries), an entry's place in kb
-  // order is the group start plus the group entries below it, entries of
-  // equal kb taking their slot order (their runs are re-sorted by full key
-  // and id below). The first kGroupLoads members are loaded unconditionally
-  // (the loads do not depend on each other and no lane waits for another's
-  // group size); a larger group walks the rest.
-  constexpr uint32_t kGroupLoads = 4;
+  // order is the group start plus the group entries below it in (kb, slot)
+  // order (runs of equal kb are re-sorted by full key and id below). The
+  // first kGroupLoads slots from the group start are compared
+  // unconditionally: slots past the group belong to later groups or are
+  // the guards past the end, and compare above. A larger group walks the
+  // rest.
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
@@ -506,21 +516,11 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
       const uint32_t d = kb[r] >> dshift;
       const uint32_t a0 = h16[d];
       const uint32_t a1 = d + 1 < ndig ? h16[d + 1] : n;
-      const uint32_t me = pos[r], k = kb[r];
-      uint32_t o[kGroupLoads];
-#pragma unroll
-      for (uint32_t j = 0; j < kGroupLoads; ++j) {
-        const uint32_t v = a0 + j;
-        o[j] = kbs[v < uint32_t(kSortCap) ? v : uint32_t(kSortCap) - 1];
-      }
+      const uint32_t me = (kb[r] << kSlotBits) | pos[r];
       uint32_t below = 0;
 #pragma unroll
-      for (uint32_t j = 0; j < kGroupLoads; ++j)
-        below += (a0 + j < a1) & ((o[j] < k) | ((o[j] == k) & (a0 + j < me)));
-      for (uint32_t v = a0 + kGroupLoads; v < a1; ++v) {
-        const uint32_t x = kbs[v];
-        below += (x < k) | ((x == k) & (v < me));
-      }
+      for (uint32_t j = 0; j < kGroupLoads; ++j) below += kbs[a0 + j] < me;
+      for (uint32_t v = a0 + kGroupLoads; v < a1; ++v) below += kbs[v] < me;
       pos[r] = a0 + below;
     }
   }
