@@ -640,56 +640,70 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
     const int64_t sA = (glo > 0 ? glo : 0) >> kScShift;
     const int64_t bA = brow[sA];
     const int64_t bB = brow[sA + 1 < int64_t(nch) ? sA + 1 : sA];
+    // positions and g values fit 32 bits (rows are int32-indexed)
+    const int32_t g0 = int32_t(glo), lg = int32_t(Lg);
     int64_t gv[kGPerT];
 #pragma unroll
     for (int u = 0; u < kGPerT; ++u) {
-      const int64_t x = u * kStThreads + threadIdx.x;
-      gv[u] = Srow[x < Lg && glo + x > 0 ? glo + x : 0];
+      const int32_t x = u * kStThreads + int32_t(threadIdx.x);
+      gv[u] = Srow[x < lg && g0 + x > 0 ? g0 + x : 0];
     }
 #pragma unroll
     for (int u = 0; u < kGPerT; ++u) {
-      const int64_t x = u * kStThreads + threadIdx.x;
-      const int64_t g = glo + x;
-      if (x < Lg)
+      const int32_t x = u * kStThreads + int32_t(threadIdx.x);
+      const int32_t g = g0 + x;
+      if (x < lg)
         gS[x] = g >= 0 ? int64_t(uint64_t((g >> kScShift) == sA ? bA : bB) + uint64_t(gv[u])) : 0;
     }
   }
   __syncthreads();
-  const Prefix P = row_prefix(p, f.i, nch, S, base);
   int32_t res[kStPer];
-  int64_t x = 0;
-  bool started = false;
+  if (staged) {
+    // 32-bit indices into the staged range; only the sums are 64-bit
+    const int32_t g0 = int32_t(glo), lg = int32_t(Lg);
+    const int32_t hb = int32_t(f.h0 + ht0);
+    int32_t x = 0;
+    bool started = false;
 #pragma unroll
-  for (int u = 0; u < kStPer; ++u) {
-    const int64_t h = f.h0 + ht0 + u;
-    res[u] = -1;
-    if (ht0 + u < f.hl) {
-      const int64_t target = sub_sat(int64_t(uint64_t(hbase) + uint64_t(sh[u])), d0);
-      int64_t g;
-      if (staged) {
+    for (int u = 0; u < kStPer; ++u) {
+      res[u] = -1;
+      if (ht0 + u < f.hl) {
+        const int64_t target = sub_sat(int64_t(uint64_t(hbase) + uint64_t(sh[u])), d0);
         if (!started) {
-          int64_t lo = 0, hi = Lg;
+          int32_t lo = 0, hi = lg;
           while (lo < hi) {
-            const int64_t mid = (lo + hi) >> 1;
+            const int32_t mid = (lo + hi) >> 1;
             if (gS[mid] >= target) hi = mid;
             else lo = mid + 1;
           }
-          x = lo < Lg ? lo : Lg - 1;
+          x = lo < lg ? lo : lg - 1;
           started = true;
         }
-        while (x < Lg - 1 && gS[x] < target) ++x;
-        g = glo + x;
-      } else {
-        // g range too wide for LDS (or not monotone): search the row itself
+        while (x < lg - 1 && gS[x] < target) ++x;
+        const int32_t g = g0 + x, h = hb + u;
+        const int32_t fv = g + 1 < h ? g + 1 : h;
+        res[u] = fv > 0 ? fv : 0;
+      }
+    }
+  } else {
+    // g range too wide for LDS (or not monotone): search the row itself
+    const Prefix P = row_prefix(p, f.i, nch, S, base);
+    int64_t x = 0;
+    bool started = false;
+#pragma unroll
+    for (int u = 0; u < kStPer; ++u) {
+      const int64_t h = f.h0 + ht0 + u;
+      res[u] = -1;
+      if (ht0 + u < f.hl) {
+        const int64_t target = sub_sat(int64_t(uint64_t(hbase) + uint64_t(sh[u])), d0);
         if (!started) {
           x = P.lower_bound(h, target);
           started = true;
         }
         while (x < h && P.at(x) < target) ++x;
-        g = x;
+        const int64_t fv = x + 1 < h ? x + 1 : h;
+        res[u] = int32_t(fv > 0 ? fv : 0);
       }
-      const int64_t fv = g + 1 < h ? g + 1 : h;
-      res[u] = int32_t(fv > 0 ? fv : 0);
     }
   }
   __syncthreads();
