@@ -626,11 +626,16 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
   const int4 bb = bnd[b];
   const int64_t hbase = brow[f.c];  // every position of the part is in span c
   // this thread's positions: prefix sums within span c
-  const int64_t ht0 = int64_t(threadIdx.x) * kStPer;  // offset in the part
+  const int32_t ht0 = int32_t(threadIdx.x) * kStPer;  // offset in the part
+  const int32_t hl = int32_t(f.hl);
+  const int64_t* Spart = Srow + f.h0;
   int64_t sh[kStPer];
 #pragma unroll
   for (int u = 0; u < kStPer; ++u)  // unconditional: past the part's end, its last position
-    sh[u] = Srow[f.h0 + (ht0 + u < f.hl ? ht0 + u : f.hl - 1)];
+    sh[u] = Spart[ht0 + u < hl ? ht0 + u : hl - 1];
+  // S(h) - d0 = (hbase - d0) + sh: sizes are >= 1, so no term saturates
+  // (other sizes only need in-bounds results, which the index bounds give)
+  const uint64_t hd = uint64_t(hbase) - uint64_t(d0);
   const int64_t glo = bb.x, ghi = bb.y;
   const int64_t Lg = ghi - glo + 1;
   const bool staged = Lg >= 1 && Lg <= gcap;  // uniform over the workgroup
@@ -661,14 +666,14 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
   if (staged) {
     // 32-bit indices into the staged range; only the sums are 64-bit
     const int32_t g0 = int32_t(glo), lg = int32_t(Lg);
-    const int32_t hb = int32_t(f.h0 + ht0);
+    const int32_t hb = int32_t(f.h0) + ht0;
     int32_t x = 0;
     bool started = false;
 #pragma unroll
     for (int u = 0; u < kStPer; ++u) {
       res[u] = -1;
-      if (ht0 + u < f.hl) {
-        const int64_t target = sub_sat(int64_t(uint64_t(hbase) + uint64_t(sh[u])), d0);
+      if (ht0 + u < hl) {
+        const int64_t target = int64_t(hd + uint64_t(sh[u]));
         if (!started) {
           int32_t lo = 0, hi = lg;
           while (lo < hi) {
