@@ -22,11 +22,13 @@ constexpr int kGatherWin = 1 << kGatherWs;    // 8-byte values held in LDS (128 
 constexpr int kGThreads = 1024;
 constexpr int kGRows = 32;                    // rows per tile
 constexpr int kGRuns = 1024;                  // runs per pass of a tile
-constexpr int kGChunk = 4096;                 // reads per inner pass (run index map)
-constexpr int kGPer = kGChunk / kGThreads;    // reads per thread and inner pass
-static_assert(kGRuns % kGThreads == 0 && kGChunk % kGThreads == 0, "gather tile shape");
+static_assert(kGRuns % kGThreads == 0, "gather tile shape");
 
+// kChunk: reads per inner pass (the run index map); each thread requests
+// kChunk / kGThreads reads of the pass at once.
+template <int kChunk>
 struct GatherLds {
+  static_assert(kChunk % kGThreads == 0, "gather tile shape");
   union {
     uint64_t win[kGatherWin];        // the window's 8-byte values
     uint32_t win4[2 * kGatherWin];   // or 4-byte values, twice as many
@@ -34,7 +36,7 @@ struct GatherLds {
   uint32_t pref[kGRuns + 1];  // reads before each run of the pass
   int32_t rpos[kGRuns];       // span start + run start, in the row
   uint8_t rrow[kGRuns];       // row - first row of the tile
-  uint16_t run_of[kGChunk];   // run of each read of the inner pass
+  uint16_t run_of[kChunk];    // run of each read of the inner pass
   uint32_t tmp[65];
 };
 
@@ -50,15 +52,16 @@ inline int gather_ws() {
 
 // Tile `tile` of the pass. value(k) gives sample k's value of type V (8 or
 // 4 bytes; it is called for k in [0, F) only); emit(pos, row, x, w0, wl)
-// receives kGPer reads of this thread at once: pos[u] the read's index in the
+// receives kChunk / kGThreads reads of this thread at once: pos[u] the read's index in the
 // row table ([N][M_max], -1 for none), row[u] its row, x[u] its sample's
 // offset in the window pass starting at sample w0 (valid when x[u] < wl),
 // with the window's values in L.win (V = uint64_t) or L.win4 (uint32_t).
-template <typename V, typename Value, typename Emit>
+template <typename V, int kChunk, typename Value, typename Emit>
 __device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* __restrict__ Pk,
                                             const uint16_t* __restrict__ OT, uint32_t tile,
-                                            uint32_t ngroups, GatherLds& L, Value value,
+                                            uint32_t ngroups, GatherLds<kChunk>& L, Value value,
                                             Emit emit) {
+  constexpr int kPer = kChunk / kGThreads;
   const uint32_t kb = tile / ngroups;
   const int64_t i0 = int64_t(tile - kb * ngroups) * kGRows;
   const int64_t rows = p.N - i0 < kGRows ? p.N - i0 : kGRows;
@@ -113,8 +116,8 @@ __device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* 
       }
       if (threadIdx.x == 0) L.pref[nr] = total;
       __syncthreads();
-      for (uint32_t x0 = 0; x0 < total; x0 += kGChunk) {
-        const uint32_t xl = total - x0 < kGChunk ? total - x0 : kGChunk;
+      for (uint32_t x0 = 0; x0 < total; x0 += kChunk) {
+        const uint32_t xl = total - x0 < kChunk ? total - x0 : kChunk;
         // run index of every read of the inner pass, written by the runs' owners
 #pragma unroll
         for (int m = 0; m < kGRuns / kGThreads; ++m) {
@@ -126,10 +129,10 @@ __device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* 
           }
         }
         __syncthreads();
-        int64_t pos[kGPer], row[kGPer];
-        uint32_t x[kGPer];
+        int64_t pos[kPer], row[kPer];
+        uint32_t x[kPer];
 #pragma unroll
-        for (int u = 0; u < kGPer; ++u) {
+        for (int u = 0; u < kPer; ++u) {
           const uint32_t t = u * kGThreads + threadIdx.x;
           pos[u] = -1;
           row[u] = i0;
@@ -140,9 +143,9 @@ __device__ __forceinline__ void gather_tile(const SegParams& p, const uint32_t* 
           }
         }
 #pragma unroll
-        for (int u = 0; u < kGPer; ++u) x[u] = Pk[pos[u] >= 0 ? pos[u] : 0];  // unconditional
+        for (int u = 0; u < kPer; ++u) x[u] = Pk[pos[u] >= 0 ? pos[u] : 0];  // unconditional
 #pragma unroll
-        for (int u = 0; u < kGPer; ++u) x[u] = pos[u] >= 0 ? (x[u] >> kScShift) - xoff : 0xFFFFFFFFu;
+        for (int u = 0; u < kPer; ++u) x[u] = pos[u] >= 0 ? (x[u] >> kScShift) - xoff : 0xFFFFFFFFu;
         emit(pos, row, x, w0, wl);
         __syncthreads();
       }

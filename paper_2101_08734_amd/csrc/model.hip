@@ -143,27 +143,30 @@ __device__ __forceinline__ uint32_t choose(const Rates& rt, const SharedRates& s
 }
 
 // Each read of the tile's window and rows gets its source (choose) and its
-// size, packed, at its place in the partitioned row.
+// size, packed, at its place in the partitioned row. Four reads per thread
+// and inner pass (eight, as in the staging gather, were no faster here).
+constexpr int kFmGChunk = 4 * kGThreads;
+constexpr int kFmGPer = kFmGChunk / kGThreads;
 __global__ void __launch_bounds__(kGThreads)
 fm_gather(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
           const int8_t* __restrict__ tier, const uint64_t* __restrict__ szb, Rates rt,
           uint64_t* __restrict__ zP, uint32_t ngroups, uint32_t ntiles) {
-  __shared__ GatherLds L;
+  __shared__ GatherLds<kFmGChunk> L;
   __shared__ SharedRates sr;
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
   load_rates(rt, sr);  // visible after the tile's first barrier
-  gather_tile<uint64_t>(
+  gather_tile<uint64_t, kFmGChunk>(
       p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return szb[k]; },
-      [&](const int64_t (&pos)[kGPer], const int64_t (&row)[kGPer], const uint32_t (&x)[kGPer],
+      [&](const int64_t (&pos)[kFmGPer], const int64_t (&row)[kFmGPer], const uint32_t (&x)[kFmGPer],
           int64_t w0, uint32_t wl) {
         // each read's own tier: a byte of its row's window slice (cached),
         // loads first, unconditional
-        int32_t own[kGPer];
+        int32_t own[kFmGPer];
 #pragma unroll
-        for (int u = 0; u < kGPer; ++u) own[u] = tier[row[u] * p.F + w0 + (x[u] < wl ? x[u] : 0u)];
+        for (int u = 0; u < kFmGPer; ++u) own[u] = tier[row[u] * p.F + w0 + (x[u] < wl ? x[u] : 0u)];
 #pragma unroll
-        for (int u = 0; u < kGPer; ++u)
+        for (int u = 0; u < kFmGPer; ++u)
           if (pos[u] >= 0 && x[u] < wl) {
             const uint64_t sb = L.win[x[u]];
             const uint32_t code = choose(rt, sr, own[u], uint32_t(sb >> kSizeBits));

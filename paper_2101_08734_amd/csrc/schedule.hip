@@ -359,30 +359,35 @@ pf_write(SegParams p, int32_t J, const uint32_t* __restrict__ Pk, const uint8_t*
 // read's place in the partitioned row (so zP holds the sizes in partitioned
 // order).
 // With every size in [0, 2^32) (*wide == 0, found by st_range) the sizes go
-// out as 4-byte values into zc, else as 8-byte values into zP.
+// out as 4-byte values into zc, else as 8-byte values into zP. Eight reads
+// per thread and inner pass (the run map then fills the LDS the window
+// leaves): half the dependent load rounds of four, 2.09 -> 1.94 ms at
+// ImageNet-22k.
+constexpr int kStGChunk = 8 * kGThreads;
+constexpr int kStGPer = kStGChunk / kGThreads;
 __global__ void __launch_bounds__(kGThreads)
 st_gather(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
           const int64_t* __restrict__ sizes, const uint32_t* __restrict__ wide,
           uint32_t* __restrict__ zc, int64_t* __restrict__ zP, uint32_t ngroups, uint32_t ntiles) {
-  __shared__ GatherLds L;
+  __shared__ GatherLds<kStGChunk> L;
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
   if (*wide != 0u) {  // uniform
-    gather_tile<uint64_t>(
+    gather_tile<uint64_t, kStGChunk>(
         p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return uint64_t(sizes[k]); },
-        [&](const int64_t (&pos)[kGPer], const int64_t (&)[kGPer], const uint32_t (&x)[kGPer],
+        [&](const int64_t (&pos)[kStGPer], const int64_t (&)[kStGPer], const uint32_t (&x)[kStGPer],
             int64_t, uint32_t wl) {
 #pragma unroll
-          for (int u = 0; u < kGPer; ++u)
+          for (int u = 0; u < kStGPer; ++u)
             if (pos[u] >= 0 && x[u] < wl) zP[pos[u]] = int64_t(L.win[x[u]]);
         });
   } else {
-    gather_tile<uint32_t>(
+    gather_tile<uint32_t, kStGChunk>(
         p, Pk, OT, tile, ngroups, L, [&](int64_t k) { return uint32_t(sizes[k]); },
-        [&](const int64_t (&pos)[kGPer], const int64_t (&)[kGPer], const uint32_t (&x)[kGPer],
+        [&](const int64_t (&pos)[kStGPer], const int64_t (&)[kStGPer], const uint32_t (&x)[kStGPer],
             int64_t, uint32_t wl) {
 #pragma unroll
-          for (int u = 0; u < kGPer; ++u)
+          for (int u = 0; u < kStGPer; ++u)
             if (pos[u] >= 0 && x[u] < wl) zc[pos[u]] = L.win4[x[u]];
         });
   }
