@@ -67,24 +67,30 @@ namespace {
 
 constexpr int kSchedWs = 13;             // partition windows: 2^13 samples
 constexpr int kWin = 1 << kSchedWs;      // samples per LDS pass of a tile
-constexpr int kTileThreads = 256;
+constexpr int kTileThreads = 512;
 constexpr int kPfMaxJ = 128;
 
 // ------------------------------------------------------------- prefetch --
-constexpr int kPfKeep = 8;  // reads per thread kept in registers between the passes
+constexpr int kPfKeep = 4;  // reads per thread kept in registers between the passes
+// 4-byte words of a window's tiers per thread (the aligned cover of kWin
+// bytes spans at most kWin / 4 + 1 words)
+constexpr int kPfTierWords = (kWin / 4 + 1 + kTileThreads - 1) / kTileThreads;
 
 // Per read of the tile: first-read candidate for its sample (pass 1), then
 // its code (pass 2). When the tile's runs fit one run table and its reads fit
 // kPfKeep per thread, the reads are spread evenly over the threads through
-// the run table and kept in registers between the passes (two dependent
-// global loads per tile); otherwise each thread walks whole runs twice.
+// the run table and kept in registers between the passes. The window's tiers
+// and the run bounds are requested together, the reads before the tables
+// are initialised: two dependent rounds of global loads per tile. Otherwise
+// each thread walks whole runs twice.
 __global__ void __launch_bounds__(kTileThreads)
 pf_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict__ OT,
         const int8_t* __restrict__ tier, int32_t J, uint8_t* __restrict__ code,
         uint32_t ntiles) {
-  __shared__ int32_t fi[kWin];  // first read of each sample of the pass
-  __shared__ int8_t tw[kWin];   // its tier
+  __shared__ int32_t fi[kWin];        // first read of each sample of the pass
+  __shared__ uint32_t tw4[kWin / 4 + 1];  // its tier: byte x + tsh (fast path), x (walk)
   __shared__ RunTable<kTileThreads> rt;
+  int8_t* tw = reinterpret_cast<int8_t*>(tw4);
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
   const int64_t i = tile / p.nbk;
@@ -98,22 +104,37 @@ pf_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict
   const bool one_table = runs <= kTileThreads && kend - k0 <= kWin;  // uniform
   if (one_table) {
     const uint32_t wl = uint32_t(kend - k0);
-    constexpr int kTb = kWin / kTileThreads;  // tier bytes per thread
-    int8_t tv[kTb];
+    // the window's tiers as the 4-byte words covering it, when the cover lies
+    // inside the tier table (not at an unaligned table start or end: then
+    // one byte per load)
+    const int8_t* wbeg = trow + k0;
+    const uint32_t tsh = uint32_t(reinterpret_cast<uintptr_t>(wbeg) & 3u);
+    const int8_t* cbeg = wbeg - tsh;
+    const uint32_t nw = (tsh + wl + 3) / 4;
+    const bool words = cbeg >= tier && cbeg + 4 * int64_t(nw) <= tier + p.N * p.F;  // uniform
+    const uint32_t* w4 = reinterpret_cast<const uint32_t*>(cbeg);
+    uint32_t tv[kPfTierWords];
+    if (words) {
 #pragma unroll
-    for (int u = 0; u < kTb; ++u) {
-      const uint32_t x = threadIdx.x + u * kTileThreads;
-      tv[u] = x < wl ? trow[k0 + x] : int8_t(-1);
-    }
+      for (int u = 0; u < kPfTierWords; ++u) {
+        const uint32_t x = threadIdx.x + u * kTileThreads;
+        tv[u] = w4[x < nw ? x : 0u];  // unconditional
+      }
+    } else {
 #pragma unroll
-    for (int u = 0; u < kTb; ++u) {
-      const uint32_t x = threadIdx.x + u * kTileThreads;
-      if (x < wl) {
-        fi[x] = INT_MAX;
-        tw[x] = tv[u];
+      for (int u = 0; u < kPfTierWords; ++u) {
+        const uint32_t x = threadIdx.x + u * kTileThreads;
+        uint32_t w = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {  // bytes of word x, laid out from the window start
+          const uint32_t y = 4 * x + c;
+          w |= uint32_t(uint8_t(wbeg[y < wl ? y : 0u])) << (8 * c);
+        }
+        tv[u] = w;
       }
     }
-    // run table (its scan's barriers also publish fi and tw)
+    const uint32_t tshl = words ? tsh : 0u;
+    // run table
     const uint32_t total = load_runs(p, i, kb, OT, rt, 0, runs, 0);
     if (total <= uint32_t(kPfKeep * kTileThreads)) {
       uint32_t v[kPfKeep];
@@ -140,7 +161,16 @@ pf_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict
         }
       }
 #pragma unroll
-      for (int u = 0; u < kPfKeep; ++u) v[u] = pos[u] >= 0 ? prow[pos[u]] : 0u;
+      for (int u = 0; u < kPfKeep; ++u) v[u] = prow[pos[u] >= 0 ? pos[u] : 0];  // unconditional
+      // the tables, while the reads are in flight
+      for (uint32_t x = threadIdx.x; x < kWin / 4; x += kTileThreads)
+        reinterpret_cast<int4*>(fi)[x] = make_int4(INT_MAX, INT_MAX, INT_MAX, INT_MAX);
+#pragma unroll
+      for (int u = 0; u < kPfTierWords; ++u) {
+        const uint32_t x = threadIdx.x + u * kTileThreads;
+        if (x < kWin / 4 + 1) tw4[x] = tv[u];
+      }
+      __syncthreads();
 #pragma unroll
       for (int u = 0; u < kPfKeep; ++u)
         if (pos[u] >= 0) {
@@ -153,14 +183,14 @@ pf_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restrict
         if (pos[u] >= 0) {
           const uint32_t x = v[u] >> kScShift;
           if (x < wl) {
-            const int32_t t = tw[x];
+            const int32_t t = tw[x + tshl];
             const bool queued = fi[x] == fb[u] + int32_t(v[u] & kJMask) && t >= 0 && t < J;
             crow[pos[u]] = queued ? uint8_t(t + 1) : uint8_t(0);
           }
         }
       return;
     }
-    __syncthreads();  // the table is no longer read
+    __syncthreads();  // the run table is no longer read
   }
   for (int64_t w0 = k0; w0 < kend; w0 += kWin) {
     const uint32_t wl = uint32_t(kend - w0 < kWin ? kend - w0 : kWin);
