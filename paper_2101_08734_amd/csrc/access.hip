@@ -521,8 +521,6 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
     return;
   }
   NextSmem& s = *reinterpret_cast<NextSmem*>(sm);
-  for (int d = threadIdx.x; d < kNextSlots; d += kNextThreads) s.head[d] = kNoLink;
-  __syncthreads();
   auto gather = [&](int64_t, int64_t fbase, uint32_t v, uint32_t idx) {
     const uint32_t x = v >> kScShift;
     s.kl[idx] = uint16_t(x);
@@ -532,7 +530,8 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
   // With at most kNextThreads runs, read idx = threadIdx.x + q * kNextThreads
   // is this thread's in the gather and in the output: its position in the
   // partitioned row, found once through the run table, stays in a register,
-  // and all of the thread's reads are requested at once.
+  // and all of the thread's reads are requested at once, before the chain
+  // heads are cleared (the clearing and its barrier overlap the loads).
   constexpr int kPerThread = (kNextEnt + kNextThreads - 1) / kNextThreads;
   static_assert(kNextEnt <= int(kRunMap), "the run table maps every read of a fast-path window");
   int32_t posq[kPerThread];
@@ -551,11 +550,15 @@ next_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restri
       }
     }
 #pragma unroll
-    for (int q = 0; q < kPerThread; ++q) vq[q] = posq[q] >= 0 ? prow[posq[q]] : 0u;
+    for (int q = 0; q < kPerThread; ++q) vq[q] = prow[posq[q] >= 0 ? posq[q] : 0];  // unconditional
+    for (int d = threadIdx.x; d < kNextSlots; d += kNextThreads) s.head[d] = kNoLink;
+    __syncthreads();
 #pragma unroll
     for (int q = 0; q < kPerThread; ++q)
       if (posq[q] >= 0) gather(posq[q], fbq[q], vq[q], threadIdx.x + q * kNextThreads);
   } else {
+    for (int d = threadIdx.x; d < kNextSlots; d += kNextThreads) s.head[d] = kNoLink;
+    __syncthreads();
     for_each_read(p, i, kb, OT, prow, rt, 0, p.E, gather);
   }
   __syncthreads();
