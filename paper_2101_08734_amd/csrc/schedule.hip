@@ -224,7 +224,9 @@ __device__ __forceinline__ uint32_t clamp_code(uint32_t m, int32_t J) {
 }
 
 // cnt layout: [N][nch][J]. Order of positions does not matter for counting,
-// so the codes are read in partitioned order.
+// so the codes are read in partitioned order. Up to kPfWordJ tiers the codes
+// are read and counted four to a word; more tiers take one code per lane.
+constexpr int kPfWordJ = 8;
 __global__ void __launch_bounds__(256)
 pf_count(SegParams p, int32_t J, const uint8_t* __restrict__ code, uint32_t nch,
          int32_t* __restrict__ cnt) {
@@ -234,6 +236,57 @@ pf_count(SegParams p, int32_t J, const uint8_t* __restrict__ code, uint32_t nch,
   for (int x = threadIdx.x; x < J; x += 256) s_cnt[x] = 0;
   __syncthreads();
   const uint8_t* src = code + s.base;
+  if (J <= kPfWordJ) {
+    // four codes per load: the 4-byte words covering the sub-chunk (the code
+    // table is the library's own, 256-byte aligned and sized, so the cover
+    // stays inside it), bytes outside the sub-chunk masked to code 0; per
+    // tier, the bytes equal to t + 1 counted within the word
+    const uint32_t sh = uint32_t(reinterpret_cast<uintptr_t>(src) & 3u);
+    const uint32_t* w4 = reinterpret_cast<const uint32_t*>(src - sh);
+    const uint32_t len = uint32_t(s.len);
+    const uint32_t nw = (sh + len + 3) / 4;
+    uint32_t c[kPfWordJ];
+#pragma unroll
+    for (int t = 0; t < kPfWordJ; ++t) c[t] = 0;
+    constexpr int kBatch = 8;
+    for (uint32_t x0 = threadIdx.x; x0 < nw; x0 += 256 * kBatch) {
+      uint32_t m[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {  // unconditional loads, all in flight together
+        const uint32_t x = x0 + u * 256;
+        m[u] = w4[x < nw ? x : 0u];
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const uint32_t x = x0 + u * 256;
+        // byte b of word x is position 4x + b - sh of the sub-chunk
+        uint32_t keep = 0xFFFFFFFFu;
+        if (x == 0) keep &= 0xFFFFFFFFu << (8 * sh);
+        const uint32_t end = 4 * x + 4;  // one past the word's last byte, in cover bytes
+        if (end > sh + len) keep &= 0xFFFFFFFFu >> (8 * (end - sh - len) < 32 ? 8 * (end - sh - len) : 31);
+        if (x >= nw || end - 4 >= sh + len) keep = 0;
+        m[u] &= keep;
+#pragma unroll
+        for (int t = 0; t < kPfWordJ; ++t) {
+          if (t < J) {
+            const uint32_t d = m[u] ^ (uint32_t(t + 1) * 0x01010101u);  // zero bytes: code t + 1
+            const uint32_t nz = ((d & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | d;   // high bit: byte nonzero
+            c[t] += 4u - uint32_t(__popc(nz & 0x80808080u));
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < kPfWordJ; ++t)
+      if (t < J) {
+        const uint32_t tot = __builtin_amdgcn_readlane(wave_inclusive_scan(c[t]), 63);
+        if (lane == 0 && tot) atomicAdd(&s_cnt[t], tot);
+      }
+    __syncthreads();
+    int32_t* out = cnt + (s.i * nch + s.c) * J;
+    for (int x = threadIdx.x; x < J; x += 256) out[x] = int32_t(s_cnt[x]);
+    return;
+  }
   constexpr int kBatch = 8;
   for (int64_t j0 = int64_t(w) * 64 * kBatch; j0 < s.len; j0 += 256 * kBatch) {
     uint32_t m[kBatch];
