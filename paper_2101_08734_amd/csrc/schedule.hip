@@ -404,8 +404,12 @@ pf_write(SegParams p, int32_t J, const uint32_t* __restrict__ Pk, const uint8_t*
     for (int u = 0; u < kPfBatch; ++u) {
       const int64_t j = j0 + (u0 + u) * 64 + lane;
       m[u] = j < s.len ? clamp_code(s_code[j], J) : 0u;
-      k[u] = m[u] ? Rsub[j] : 0;
+      k[u] = Rsub[j < s.len ? j : 0];  // unconditional
     }
+    // every sample id is in a register before the first store: a wait for
+    // a load inside the store loop would also wait for the stores before it
+#pragma unroll
+    for (int u = 0; u < kPfBatch; ++u) asm volatile("" : "+v"(k[u]));
 #pragma unroll
     for (int u = 0; u < kPfBatch; ++u) {
       uint64_t act = __ballot(m[u] != 0);
