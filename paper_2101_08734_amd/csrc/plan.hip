@@ -844,6 +844,14 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
     btw[h] = make_uint4(0, 0, 0, 0);
     if (w < nb1w) btw[h] = *reinterpret_cast<const uint4*>(bt + 16 * w);  // inside the padded row
   }
+  // class-0 tiers of the first window pass (clamped index: unconditional)
+  auto zbins = [&](int64_t w0) {
+    const int64_t wl = kend - w0 < kWriteWin ? kend - w0 : kWriteWin;
+    return uint32_t((w0 + wl - 1) >> kClass0Shift) - uint32_t(w0 >> kClass0Shift) + 1;
+  };
+  const uint32_t nzb_first = zbins(k0);
+  const int8_t zt_first =
+      bt[a.nbin1 + uint32_t(k0 >> kClass0Shift) + (threadIdx.x < nzb_first ? threadIdx.x : 0u)];
   const uint32_t n = c.num[tix];
   const uint32_t* ent = c.ent + i * a.M_max + c.base[tix];
   // round two: the list entries
@@ -886,8 +894,8 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
     const uint32_t nzb = uint32_t((w0 + wlen - 1) >> kClass0Shift) - zb0 + 1;
     const uint32_t sh = kVec ? uint32_t((i * a.F + w0) & 15) : 0u;
     if (threadIdx.x == 0) s_c0cand = 0;
-    int8_t zt = 0;
-    if (threadIdx.x < nzb) zt = bt[a.nbin1 + zb0 + threadIdx.x];
+    int8_t zt = zt_first;
+    if (w0 != k0 && threadIdx.x < nzb) zt = bt[a.nbin1 + zb0 + threadIdx.x];
     __syncthreads();
     if (threadIdx.x < nzb) {
       t0[threadIdx.x] = zt;
