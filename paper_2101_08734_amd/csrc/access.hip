@@ -358,6 +358,10 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
       pass_all = all;
       listed += all;
     }
+    // kCompact: the class records arrive before the row stores go out: a
+    // wait for them behind the stores would wait for the stores too (one
+    // counter covers loads and stores, in order)
+    if (kCompact && kVec) asm volatile("" ::"v"(rec_s), "v"(rec_b));
     if (kVec) {
       if (threadIdx.x < head) {
         crow[threadIdx.x] = uint8_t(c1);
@@ -399,8 +403,13 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      // the list addresses are formed here: an address held from the
+      // kernel's start was spilled, and its reload's wait would also have
+      // waited for the row stores above
+      uint32_t ltid = threadIdx.x;
+      asm volatile("" : "+v"(ltid));
       for (uint32_t t0 = 0; t0 < pass_all; t0 += kStatsThreads) {  // uniform trip count
-        const uint32_t t = t0 + threadIdx.x;
+        const uint32_t t = t0 + ltid;
         const uint2 e = stg[t < pass_all ? t : 0u];
         const uint32_t c = e.x & 0xFFu;
         uint32_t b = bin_lane(c & 63u, int32_t(e.y));
