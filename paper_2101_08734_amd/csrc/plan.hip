@@ -823,7 +823,7 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
              const int8_t* __restrict__ btier, int8_t* __restrict__ tier,
              CandRec* __restrict__ cand, int32_t* __restrict__ ccount, uint32_t ntiles) {
   __shared__ __align__(16) int8_t bt1[kBt1Max];
-  __shared__ __align__(16) uint32_t tbw[kWriteWin / 4 + 4];  // the row's tiers, shifted by sh
+  __shared__ __align__(16) uint32_t tbw[kWriteWin / 4 + 8];  // the row's tiers, shifted by sh
   __shared__ int8_t t0[kWriteWin / (1 << kClass0Shift) + 1];
   int8_t* tb = reinterpret_cast<int8_t*>(tbw);
   __shared__ int s_c0cand;
@@ -911,14 +911,31 @@ plan_write_c(PlanArgs a, CompactArgs c, const int32_t* __restrict__ first,
         return (lo8 + uint32_t(x)) >> kClass0Shift;
       };
       const uint32_t nw = (wlen + sh + 3) / 4;
-      for (uint32_t wd = threadIdx.x; wd < nw; wd += kWriteThreads) {
-        const int32_t xa = int32_t(4 * wd) - int32_t(sh);
-        const uint32_t za = zbin(xa), zd = zbin(xa + 3);
-        uint32_t word = uint32_t(uint8_t(t0[za])) * 0x01010101u;
-        if (za != zd)  // the word spans two class-0 bins
-          word = uint32_t(uint8_t(t0[za])) | (uint32_t(uint8_t(t0[zbin(xa + 1)])) << 8) |
-                 (uint32_t(uint8_t(t0[zbin(xa + 2)])) << 16) | (uint32_t(uint8_t(t0[zd])) << 24);
-        tbw[wd] = word;
+      // eight consecutive words (32 cells) per thread: almost always inside
+      // one class-0 bin (256 cells), then one lookup and two 16-byte stores
+      // (words past nw fall in the table's slack and are never read)
+      for (uint32_t wd0 = 8 * threadIdx.x; wd0 < nw; wd0 += 8 * kWriteThreads) {
+        const int32_t xa = int32_t(4 * wd0) - int32_t(sh);
+        const uint32_t za = zbin(xa), zd = zbin(xa + 31);
+        uint4* dst = reinterpret_cast<uint4*>(tbw + wd0);
+        if (za == zd) {
+          const uint32_t word = uint32_t(uint8_t(t0[za])) * 0x01010101u;
+          dst[0] = make_uint4(word, word, word, word);
+          dst[1] = make_uint4(word, word, word, word);
+        } else {
+          uint32_t wv[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const int32_t xq = xa + 4 * q;
+            const uint32_t a = zbin(xq), d = zbin(xq + 3);
+            wv[q] = uint32_t(uint8_t(t0[a])) * 0x01010101u;
+            if (a != d)  // the word spans two class-0 bins
+              wv[q] = uint32_t(uint8_t(t0[a])) | (uint32_t(uint8_t(t0[zbin(xq + 1)])) << 8) |
+                      (uint32_t(uint8_t(t0[zbin(xq + 2)])) << 16) | (uint32_t(uint8_t(t0[d])) << 24);
+          }
+          dst[0] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+          dst[1] = make_uint4(wv[4], wv[5], wv[6], wv[7]);
+        }
       }
     }
     __syncthreads();
