@@ -85,16 +85,21 @@ seg_partition(SegParams p, const int32_t* __restrict__ R, uint32_t* __restrict__
   const uint32_t W = 1u << p.ws;
   const uint32_t F = uint32_t(p.F);
 
-  for (uint32_t b = threadIdx.x; b <= nbk; b += kPartThreads) hist[b] = 0;
-  __syncthreads();
+  // the sub-chunk's reads are requested before the histogram is cleared
+  // (unconditional loads; past the end they read the first entry)
   constexpr int kPer = kSC / kPartThreads;
   uint32_t kk[kPer];
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
     const uint32_t q = uint32_t(r * kPartThreads) + threadIdx.x;
-    // entries outside [0, F) break the precondition; keep them in bounds
-    uint32_t k = q < len ? uint32_t(R[base + q]) : 0u;
-    kk[r] = k < F ? k : 0u;
+    kk[r] = uint32_t(R[base + (q < len ? q : 0u)]);
+  }
+  for (uint32_t b = threadIdx.x; b <= nbk; b += kPartThreads) hist[b] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    const uint32_t k = kk[r];
+    kk[r] = k < F ? k : 0u;  // entries outside [0, F) break the precondition; keep them in bounds
   }
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
