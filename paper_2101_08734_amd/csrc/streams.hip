@@ -227,7 +227,17 @@ stream_scatter(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t*
   const uint32_t* st = wst + int64_t(blockIdx.y) * (nbw + 1);
   const uint32_t* oc = offc + (int64_t(blockIdx.y) * p.nchunks + chunk) * nbw;
   uint32_t* out = words + int64_t(blockIdx.y) * p.F;
-  for (uint32_t b = threadIdx.x; b < nbw; b += kThreads) dl[b] = int32_t(st[b] + oc[b]);
+  // the chunk's run positions per bucket: requested here (unconditionally),
+  // stored to LDS once the first round's keys are counted
+  constexpr int kDl = kMaxWin / kThreads;
+  static_assert(kMaxWin % kThreads == 0, "run positions per thread");
+  int32_t dlv[kDl];
+#pragma unroll
+  for (int m = 0; m < kDl; ++m) {
+    const uint32_t b = threadIdx.x + uint32_t(m) * kThreads;
+    const uint32_t bc = b < nbw ? b : 0u;
+    dlv[m] = int32_t(st[bc] + oc[bc]);
+  }
   const int64_t id_chunk = int64_t(chunk) * p.C;
   for (int64_t r0 = id_chunk; r0 < id_chunk + p.C && r0 < p.F; r0 += kRound) {
     for (uint32_t x = threadIdx.x; x < (nbw + 2) / 2; x += kThreads) cntw[x] = 0;
@@ -250,6 +260,13 @@ stream_scatter(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t*
           const uint32_t half = (b & 1u) * 16u;
           bs[it][c] = (b << 16) | ((atomicAdd(&cntw[b >> 1], 1u << half) >> half) & 0xFFFFu);
         }
+      }
+    }
+    if (r0 == id_chunk) {  // uniform
+#pragma unroll
+      for (int m = 0; m < kDl; ++m) {
+        const uint32_t b = threadIdx.x + uint32_t(m) * kThreads;
+        if (b < nbw) dl[b] = dlv[m];
       }
     }
     __syncthreads();
