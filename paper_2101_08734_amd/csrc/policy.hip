@@ -26,7 +26,8 @@
 // maxima are taken with fmax: every operand is finite and non-negative and
 // never -0, where fmax and "the larger of the two" agree bit for bit.)
 //
-//   ps_sim -- one wave per worker, 64 reads per batch, one per lane. The
+//   ps_sim -- one wave per worker (two but for Perfect, the second summing
+//             the fetch times by class), 64 reads per batch, one per lane. The
 //             per-read terms (u, fetch, read) and the wait p0 t(g) of every
 //             lane whose g = fill(f) - 1 lies before the batch are computed
 //             lane-parallel. A batch whose waits are all known runs the Q
@@ -86,8 +87,17 @@ __device__ __forceinline__ int ps_class(int32_t policy, int32_t code, int32_t J)
   return 0;
 }
 
+// Every policy but Perfect takes a second wave per worker for the fetch-time
+// sums by source class (Naive and StagingBuffer: the PFS only): they depend
+// on no t, so their sequential chains (stream order within each class) run
+// beside the t chain instead of inside or after each batch of it.
 template <int32_t kPolicy>
-__global__ void __launch_bounds__(64)
+constexpr int ps_threads() {
+  return kPolicy == kPerfect ? 64 : 128;
+}
+
+template <int32_t kPolicy>
+__global__ void __launch_bounds__(ps_threads<kPolicy>())
 ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ sizes,
        const int16_t* __restrict__ src, const int32_t* __restrict__ fill, PsRates rt,
        double* __restrict__ t, double* __restrict__ finish, double* __restrict__ io) {
@@ -96,15 +106,63 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
   __shared__ double ring[kPsRing];
   __shared__ double thr[kPsClasses];
   const int64_t i = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   const int64_t Mi = ps_row_len(r, i);
   const int64_t M = r.M_max;
   const int32_t* Rr = R + i * M;
   const int16_t* Sr = src ? src + i * M : nullptr;
   const int32_t* Fr = fill ? fill + i * M : nullptr;
   double* tr = t + i * M;
-  for (int c = lane; c < kPsClasses; c += 64) thr[c] = rt.thr[c];
+  for (int c = threadIdx.x; c < kPsClasses; c += ps_threads<kPolicy>()) thr[c] = rt.thr[c];
   __syncthreads();
+  if (kPolicy != kPerfect && threadIdx.x >= 64) {
+    // the second wave: fetch time by class, each class's reads in stream
+    // order (ids and sources one batch ahead, sizes when they arrive)
+    double a0 = 0.0, a1 = 0.0;  // class lane, class 64 + lane
+    auto ids = [&](int64_t f0, int32_t& k, int32_t& code) {
+      const int64_t f = f0 + lane;
+      const int64_t fc = f < Mi ? f : 0;  // unconditional (Mi >= 1 inside the loop)
+      k = Rr[fc];
+      code = kPolicy == kNoPFS ? int32_t(Sr[fc]) : 0;
+      if (f >= Mi) k = -1;
+    };
+    int32_t kN = -1, cN = 0;
+    if (Mi > 0) ids(0, kN, cN);
+    for (int64_t f0 = 0; f0 < Mi; f0 += 64) {
+      const int32_t k = kN, code = cN;
+      if (f0 + 64 < Mi) ids(f0 + 64, kN, cN);
+      const double s = double((k >= 0 && k < r.F) ? sizes[k] : int64_t(0));
+      const int cls = ps_class(kPolicy, code, rt.J);
+      const double fetch = s / thr[cls];
+      const int nb = Mi - f0 < 64 ? int(Mi - f0) : 64;
+      if (kPolicy != kNoPFS && nb == 64) {
+        // one class (the PFS) and a full batch: straight-line adds
+        double a = rl_d(a0, 0);
+#pragma unroll
+        for (int q = 0; q < 64; ++q) a = a + rl_d(fetch, q);
+        a0 = lane == 0 ? a : a0;
+        continue;
+      }
+      uint64_t rem = nb == 64 ? ~uint64_t(0) : (uint64_t(1) << nb) - 1;
+      while (rem) {
+        const int c = __builtin_amdgcn_readlane(cls, __builtin_ctzll(rem));
+        const uint64_t m = __ballot(cls == c) & rem;
+        rem &= ~m;
+        double a = c < 64 ? rl_d(a0, c) : rl_d(a1, c - 64);
+        for (uint64_t mm = m; mm; mm &= mm - 1) a = a + rl_d(fetch, __builtin_ctzll(mm));
+        if (c < 64) {
+          a0 = lane == c ? a : a0;
+        } else {
+          a1 = lane == c - 64 ? a : a1;
+        }
+      }
+    }
+    const int K = 1 + 2 * rt.J;
+    double* ior = io + i * K;
+    if (lane < K) ior[lane] = a0;
+    if (64 + lane < K) ior[64 + lane] = a1;
+    return;
+  }
 
   // per-lane raw inputs of a batch: id, source code, window start (only
   // loads here, so nothing waits for them until they are used)
@@ -135,8 +193,6 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
     return (g >= 0 && g < f0 - kPsRing) ? tr[g] : 0.0;
   };
 
-  double acc0 = 0.0, acc1 = 0.0;  // NoPFS: fetch time of class lane, and of class 64 + lane
-  double pfs_acc = 0.0;           // Naive and StagingBuffer: fetch time from the PFS
   double Q = 0.0, tprev = 0.0, uprev = 0.0;
 
   // pipeline: ids two batches ahead, sizes and far lookbacks one
@@ -198,7 +254,6 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
       tb = lane == q ? tf : tb;
       tprev = tf;
       uprev = uq;
-      if (kPolicy == kNaive || kPolicy == kStaging) pfs_acc = pfs_acc + rl_d(fetch, q);
     };
     if (kStaged && inb_mask == 0) {
       // every wait is known: Q does not depend on this batch's t, so its
@@ -231,7 +286,6 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
         tb = lane == q ? tf : tb;
         tprev = tf;
         uprev = rl_d(u, q);
-        if (kPolicy == kStaging) pfs_acc = pfs_acc + rl_d(fetch, q);
       };
       if (nb == 64) {
 #pragma unroll
@@ -263,29 +317,14 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
       tr[f] = tb;
       if (kStaged) ring[f & (kPsRing - 1)] = tb;
     }
-    if (kPolicy == kNoPFS) {
-      // fetch time by class: each class's reads of the batch in stream order
-      uint64_t rem = nb == 64 ? ~uint64_t(0) : (uint64_t(1) << nb) - 1;
-      while (rem) {
-        const int c = __builtin_amdgcn_readlane(cls, __builtin_ctzll(rem));
-        const uint64_t m = __ballot(cls == c) & rem;
-        rem &= ~m;
-        double a = c < 64 ? rl_d(acc0, c) : rl_d(acc1, c - 64);
-        for (uint64_t mm = m; mm; mm &= mm - 1) a = a + rl_d(fetch, __builtin_ctzll(mm));
-        if (c < 64) {
-          acc0 = lane == c ? a : acc0;
-        } else {
-          acc1 = lane == c - 64 ? a : acc1;
-        }
-      }
-    }
   }
   for (int64_t f = Mi + lane; f < M; f += 64) tr[f] = -1.0;
-  const int K = 1 + 2 * rt.J;
-  double* ior = io + i * K;
-  if (kPolicy == kNaive || kPolicy == kStaging) acc0 = lane == 0 ? pfs_acc : 0.0;
-  if (lane < K) ior[lane] = acc0;
-  if (64 + lane < K) ior[64 + lane] = acc1;
+  if (kPolicy == kPerfect) {  // no fetches (the other policies' second wave writes io)
+    const int K = 1 + 2 * rt.J;
+    double* ior = io + i * K;
+    if (lane < K) ior[lane] = 0.0;
+    if (64 + lane < K) ior[64 + lane] = 0.0;
+  }
   if (lane == 0) finish[i] = Mi > 0 ? tprev + uprev : 0.0;
 }
 
@@ -318,19 +357,19 @@ int policy_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, co
   rt.wthr = model->beta < wb ? model->beta : wb;
   rt.c = model->c;
   rt.p0 = model->p0;
-  const dim3 grid(uint32_t(s.N)), block(64);
+  const dim3 grid(uint32_t(s.N));
   switch (policy) {
     case kPerfect:
-      return launch("ps_sim_perfect", ps_sim<kPerfect>, grid, block, 0, st, r, R, sizes, src, fill, rt, t,
+      return launch("ps_sim_perfect", ps_sim<kPerfect>, grid, dim3(ps_threads<kPerfect>()), 0, st, r, R, sizes, src, fill, rt, t,
                     finish, io);
     case kNaive:
-      return launch("ps_sim_naive", ps_sim<kNaive>, grid, block, 0, st, r, R, sizes, src, fill, rt, t,
+      return launch("ps_sim_naive", ps_sim<kNaive>, grid, dim3(ps_threads<kNaive>()), 0, st, r, R, sizes, src, fill, rt, t,
                     finish, io);
     case kStaging:
-      return launch("ps_sim_staging", ps_sim<kStaging>, grid, block, 0, st, r, R, sizes, src, fill, rt, t,
+      return launch("ps_sim_staging", ps_sim<kStaging>, grid, dim3(ps_threads<kStaging>()), 0, st, r, R, sizes, src, fill, rt, t,
                     finish, io);
     default:
-      return launch("ps_sim_nopfs", ps_sim<kNoPFS>, grid, block, 0, st, r, R, sizes, src, fill, rt, t,
+      return launch("ps_sim_nopfs", ps_sim<kNoPFS>, grid, dim3(ps_threads<kNoPFS>()), 0, st, r, R, sizes, src, fill, rt, t,
                     finish, io);
   }
 }
