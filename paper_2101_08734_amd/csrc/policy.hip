@@ -20,25 +20,29 @@
 // finish = t(last) + u(last); io sums fetch times by source class.
 //
 // The recurrence is sequential within a worker (a read may wait for the
-// consumption of any earlier read), so each worker is one wave, and the
-// arithmetic is the same IEEE operations in the same order as the
-// definition: results are bit-identical to a read-by-read evaluation. (The
-// maxima are taken with fmax: every operand is finite and non-negative and
-// never -0, where fmax and "the larger of the two" agree bit for bit.)
+// consumption of any earlier read), so each worker is one workgroup on one
+// CU, and the arithmetic is the same IEEE operations in the same order as
+// the definition: results are bit-identical to a read-by-read evaluation.
+// (The maxima are taken with fmax: every operand is finite and non-negative
+// and never -0, where fmax and "the larger of the two" agree bit for bit.)
+// Reads go in batches of 64, one per lane: the per-read terms (u, fetch,
+// read) are lane-parallel, the chains step through the batch with lane reads
+// (full batches unrolled, so later steps' operands are formed while earlier
+// steps finish). The fetch-time sums by class depend on no t and run in a
+// wave of their own.
 //
-//   ps_sim -- one wave per worker (two but for Perfect, the second summing
-//             the fetch times by class), 64 reads per batch, one per lane. The
-//             per-read terms (u, fetch, read) and the wait p0 t(g) of every
-//             lane whose g = fill(f) - 1 lies before the batch are computed
-//             lane-parallel. A batch whose waits are all known runs the Q
-//             chain over its 64 steps, one division Q / p0 across the lanes,
-//             then the t chain; a batch with a wait inside itself steps read
-//             by read, taking that wait from the batch's t register. Full
-//             batches are unrolled, so later steps' operands are fetched
-//             while earlier steps finish. The batch's t goes to global memory
-//             and to an LDS ring of the last 8,192 positions; waits older
-//             than the ring are loaded from global memory a batch ahead. Ids,
-//             sources and windows are loaded two batches ahead, sizes one.
+//   ps_sim    -- Perfect and Naive: one wave for the t chain (Naive: a
+//                second for the PFS sum). Ids two batches ahead, sizes one.
+//   ps_staged -- StagingBuffer and NoPFS: a Q wave, a T wave and a sums wave.
+//                In iteration k the Q wave forms batch k's terms and its Q
+//                chain (waits p0 t(g) from an LDS ring of the last 8,192
+//                positions, older ones loaded from global memory a batch
+//                ahead), while the T wave runs batch k - 1's t chain from the
+//                Q values left in LDS (one division Q / p0 across the lanes).
+//                A batch waiting on batch k - 1 gets its Q chain after the
+//                iteration's first barrier; one waiting inside itself is
+//                stepped read by read, Q and t, by the T wave in the next
+//                iteration. The sums wave gives each class a lane.
 
 #include <new>
 
@@ -87,10 +91,9 @@ __device__ __forceinline__ int ps_class(int32_t policy, int32_t code, int32_t J)
   return 0;
 }
 
-// Every policy but Perfect takes a second wave per worker for the fetch-time
-// sums by source class (Naive and StagingBuffer: the PFS only): they depend
-// on no t, so their sequential chains (stream order within each class) run
-// beside the t chain instead of inside or after each batch of it.
+// Perfect and Naive. Naive takes a second wave per worker for its PFS
+// fetch-time sum: it depends on no t, so its sequential chain (stream order)
+// runs beside the t chain instead of inside it.
 template <int32_t kPolicy>
 constexpr int ps_threads() {
   return kPolicy == kPerfect ? 64 : 128;
@@ -102,28 +105,25 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
        const int16_t* __restrict__ src, const int32_t* __restrict__ fill, PsRates rt,
        double* __restrict__ t, double* __restrict__ finish, double* __restrict__ io) {
 #pragma clang fp contract(off)
-  constexpr bool kStaged = kPolicy >= kStaging;
-  __shared__ double ring[kPsRing];
+  static_assert(kPolicy == kPerfect || kPolicy == kNaive, "the staging policies: ps_staged");
   __shared__ double thr[kPsClasses];
   const int64_t i = blockIdx.x;
   const int lane = threadIdx.x & 63;
   const int64_t Mi = ps_row_len(r, i);
   const int64_t M = r.M_max;
   const int32_t* Rr = R + i * M;
-  const int16_t* Sr = src ? src + i * M : nullptr;
-  const int32_t* Fr = fill ? fill + i * M : nullptr;
   double* tr = t + i * M;
   for (int c = threadIdx.x; c < kPsClasses; c += ps_threads<kPolicy>()) thr[c] = rt.thr[c];
   __syncthreads();
   if (kPolicy != kPerfect && threadIdx.x >= 64) {
-    // the second wave: fetch time by class, each class's reads in stream
-    // order (ids and sources one batch ahead, sizes when they arrive)
+    // the second wave: the PFS fetch time (class 0), reads in stream order
+    // (ids one batch ahead, sizes when they arrive)
     double a0 = 0.0, a1 = 0.0;  // class lane, class 64 + lane
     auto ids = [&](int64_t f0, int32_t& k, int32_t& code) {
       const int64_t f = f0 + lane;
       const int64_t fc = f < Mi ? f : 0;  // unconditional (Mi >= 1 inside the loop)
       k = Rr[fc];
-      code = kPolicy == kNoPFS ? int32_t(Sr[fc]) : 0;
+      code = 0;
       if (f >= Mi) k = -1;
     };
     int32_t kN = -1, cN = 0;
@@ -135,7 +135,7 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
       const int cls = ps_class(kPolicy, code, rt.J);
       const double fetch = s / thr[cls];
       const int nb = Mi - f0 < 64 ? int(Mi - f0) : 64;
-      if (kPolicy != kNoPFS && nb == 64) {
+      if (nb == 64) {
         // one class (the PFS) and a full batch: straight-line adds
         double a = rl_d(a0, 0);
 #pragma unroll
@@ -164,8 +164,122 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
     return;
   }
 
-  // per-lane raw inputs of a batch: id, source code, window start (only
-  // loads here, so nothing waits for them until they are used)
+  // per-lane raw inputs of a batch: the id (only a load here, so nothing
+  // waits for it until it is used)
+  auto load_ids = [&](int64_t f0, int32_t& k, int32_t& code, int32_t& fl) {
+    const int64_t f = f0 + lane;
+    k = -1;
+    code = 0;
+    fl = 0;
+    if (f < Mi) k = Rr[f];
+  };
+  auto size_of = [&](int32_t k) -> int64_t {
+    return (k >= 0 && k < r.F) ? sizes[k] : int64_t(0);
+  };
+
+  double tprev = 0.0, uprev = 0.0;
+
+  // pipeline: ids two batches ahead, sizes one
+  int32_t kA, cA, fA, kB, cB, fB;
+  load_ids(0, kB, cB, fB);
+  int64_t sB = size_of(kB);
+  load_ids(64, kA, cA, fA);
+  for (int64_t f0 = 0; f0 < Mi; f0 += 64) {
+    // this batch's inputs
+    const double s = double(sB);
+    const int cls = ps_class(kPolicy, cB, rt.J);
+    // per-read terms, lane-parallel, in the definition's expressions
+    const double u = s / rt.c;
+    const double fetch = s / thr[cls];
+    const double rd = fetch + s / rt.wthr;
+    // the next batch's sizes, the one after's ids
+    sB = size_of(kA);
+    cB = cA;
+    fB = fA;
+    load_ids(f0 + 128, kA, cA, fA);
+
+    const int nb = Mi - f0 < 64 ? int(Mi - f0) : 64;
+    double tb = -1.0;  // lane q: t of read f0 + q
+    // one read's step
+    auto step = [&](int q) {
+      const int64_t f = f0 + q;
+      const double uq = rl_d(u, q);
+      const double rq = rl_d(rd, q);
+      double tf;
+      if (kPolicy == kPerfect) {
+        tf = f == 0 ? 0.0 : tprev + uprev;
+      } else {
+        tf = f == 0 ? rq : (tprev + uprev) + rq;
+      }
+      tb = lane == q ? tf : tb;
+      tprev = tf;
+      uprev = uq;
+    };
+    if (nb == 64) {
+      // a full batch: straight-line steps, so the terms of later steps can
+      // be formed while earlier ones finish
+#pragma unroll
+      for (int q = 0; q < 64; ++q) step(q);
+    } else {
+      for (int q = 0; q < nb; ++q) step(q);
+    }
+    const int64_t f = f0 + lane;
+    if (f < Mi) tr[f] = tb;
+  }
+  for (int64_t f = Mi + lane; f < M; f += 64) tr[f] = -1.0;
+  if (kPolicy == kPerfect) {  // no fetches (the other policies' second wave writes io)
+    const int K = 1 + 2 * rt.J;
+    double* ior = io + i * K;
+    if (lane < K) ior[lane] = 0.0;
+    if (64 + lane < K) ior[64 + lane] = 0.0;
+  }
+  if (lane == 0) finish[i] = Mi > 0 ? tprev + uprev : 0.0;
+}
+
+// The staging policies with the Q and t chains in two waves of the worker's
+// workgroup (and the fetch-time sums in a third). Iteration k: the Q wave
+// forms batch k's per-read terms and, when every lookback of the batch is
+// already known, its Q chain; the T wave runs batch k - 1's t chain from the
+// Q values the Q wave left in LDS. Waits of batch k on batch k - 1 are known
+// only once the T wave has finished it, so such a batch's Q chain runs after
+// the iteration's first barrier; a batch with a lookback inside itself is
+// stepped read by read (Q and t) by the T wave in the next iteration. Every
+// wave passes the same two barriers per iteration, and the operations are
+// those of the single-wave evaluation, in the same order.
+struct PsSlot {
+  double Qb[64];   // Q(f0 + q)
+  double u[64];    // compute time of read f0 + q
+  double rd[64];   // its staging time
+  double W[64];    // its wait p0 t(g), lookbacks before the batch (stepped batches)
+  int32_t gq[64];  // its lookback g - f0 (lookbacks inside the batch)
+  uint64_t inb;    // lanes whose lookback is inside the batch
+  int32_t near;    // the T wave steps the batch read by read
+};
+
+template <int32_t kPolicy>
+__global__ void __launch_bounds__(192)
+ps_staged(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ sizes,
+          const int16_t* __restrict__ src, const int32_t* __restrict__ fill, PsRates rt,
+          double* __restrict__ t, double* __restrict__ finish, double* __restrict__ io) {
+#pragma clang fp contract(off)
+  __shared__ double ring[kPsRing];
+  __shared__ double thr[kPsClasses];
+  __shared__ PsSlot slot[2];
+  __shared__ double s_Qend;  // Q after the last batch the T wave stepped
+  const int64_t i = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t Mi = ps_row_len(r, i);
+  const int64_t M = r.M_max;
+  const int32_t* Rr = R + i * M;
+  const int16_t* Sr = kPolicy == kNoPFS ? src + i * M : nullptr;
+  const int32_t* Fr = fill + i * M;
+  double* tr = t + i * M;
+  for (int c = threadIdx.x; c < kPsClasses; c += 192) thr[c] = rt.thr[c];
+  if (threadIdx.x == 0) s_Qend = 0.0;
+  __syncthreads();
+  const int64_t nbat = (Mi + 63) / 64;
+
+  // -- Q wave: inputs two batches ahead (ids), one ahead (sizes, far lookbacks)
   auto load_ids = [&](int64_t f0, int32_t& k, int32_t& code, int32_t& fl) {
     const int64_t f = f0 + lane;
     k = -1;
@@ -174,10 +288,9 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
     if (f < Mi) {
       k = Rr[f];
       if (kPolicy == kNoPFS) code = Sr[f];
-      if (kStaged) fl = Fr[f];
+      fl = Fr[f];
     }
   };
-  // the lookback position g = fill - 1 of read f, clamped to [-1, f - 1]
   auto look = [&](int64_t f0, int32_t fl) -> int64_t {
     const int64_t f = f0 + lane;
     int64_t g = int64_t(fl) - 1;
@@ -188,144 +301,198 @@ ps_sim(PsShape r, const int32_t* __restrict__ R, const int64_t* __restrict__ siz
   auto size_of = [&](int32_t k) -> int64_t {
     return (k >= 0 && k < r.F) ? sizes[k] : int64_t(0);
   };
-  // a lookback older than the ring, loaded from global memory a batch ahead
   auto far_wait = [&](int64_t f0, int64_t g) -> double {
     return (g >= 0 && g < f0 - kPsRing) ? tr[g] : 0.0;
   };
+  double Q = 0.0;
+  int32_t kA = -1, cA = 0, fA = 0, kB = -1, cB = 0, fB = 0;
+  int64_t sB = 0;
+  double farB = 0.0;
+  if (wave == 0) {
+    load_ids(0, kB, cB, fB);
+    sB = size_of(kB);
+    load_ids(64, kA, cA, fA);
+  }
+  // -- T wave
+  double tprev = 0.0, uprev = 0.0;
+  // -- io wave: fetch time by class, ids and sources one batch ahead
+  double a0 = 0.0, a1 = 0.0;
+  const int K = 1 + 2 * rt.J;  // source classes
+  int32_t kN = -1, cN = 0;
+  auto io_ids = [&](int64_t f0, int32_t& k, int32_t& code) {
+    const int64_t f = f0 + lane;
+    const int64_t fc = f < Mi ? f : 0;
+    k = Rr[fc];
+    code = kPolicy == kNoPFS ? int32_t(Sr[fc]) : 0;
+    if (f >= Mi) k = -1;
+  };
+  if (wave == 2 && Mi > 0) io_ids(0, kN, cN);
 
-  double Q = 0.0, tprev = 0.0, uprev = 0.0;
-
-  // pipeline: ids two batches ahead, sizes and far lookbacks one
-  int32_t kA, cA, fA, kB, cB, fB;
-  load_ids(0, kB, cB, fB);
-  int64_t sB = size_of(kB);
-  double farB = 0.0;  // nothing is older than the ring in the first batch
-  load_ids(64, kA, cA, fA);
-  for (int64_t f0 = 0; f0 < Mi; f0 += 64) {
-    // this batch's inputs
-    const double s = double(sB);
-    const int cls = ps_class(kPolicy, cB, rt.J);
-    const int64_t g = kStaged ? look(f0, fB) : -1;
-    const double far = farB;
-    // per-read terms, lane-parallel, in the definition's expressions
-    const double u = s / rt.c;
-    const double fetch = s / thr[cls];
-    const double rd = fetch + s / rt.wthr;
-    // waits resolvable now: before the batch (ring or the far load)
-    double W = 0.0;
-    bool inb = false;
-    if (kStaged) {
-      if (g >= f0) {
-        inb = true;
-      } else if (g >= 0) {
-        const double tg = g >= f0 - kPsRing ? ring[g & (kPsRing - 1)] : far;
-        W = rt.p0 * tg;
-      }
-    }
-    // the next batch's sizes and far lookbacks, the one after's ids
-    sB = size_of(kA);
-    cB = cA;
-    fB = fA;
-    farB = kStaged ? far_wait(f0 + 64, look(f0 + 64, fA)) : 0.0;
-    load_ids(f0 + 128, kA, cA, fA);
-
-    const int nb = Mi - f0 < 64 ? int(Mi - f0) : 64;
-    double tb = -1.0;  // lane q: t of read f0 + q
-    const uint64_t inb_mask = __ballot(inb);
-    // one read's step; Wq is its wait (staging policies)
-    auto step = [&](int q, double Wq) {
-      const int64_t f = f0 + q;
-      const double uq = rl_d(u, q);
-      const double rq = rl_d(rd, q);
-      double tf;
-      if (kPolicy == kPerfect) {
-        tf = f == 0 ? 0.0 : tprev + uprev;
-      } else if (kPolicy == kNaive) {
-        tf = f == 0 ? rq : (tprev + uprev) + rq;
-      } else {
-        Q = __builtin_fmax(Q, Wq);
-        Q = Q + rq;
-        tf = Q / rt.p0;
-        if (f > 0) {
-          const double a = tprev + uprev;
-          tf = __builtin_fmax(tf, a);
-        }
-      }
-      tb = lane == q ? tf : tb;
-      tprev = tf;
-      uprev = uq;
-    };
-    if (kStaged && inb_mask == 0) {
-      // every wait is known: Q does not depend on this batch's t, so its
-      // chain runs first, the divisions Q(f) / p0 run once across the lanes,
-      // and then the t chain (the same operations as step by step)
-      double Qb = 0.0;  // lane q: Q(f0 + q)
-      if (nb == 64) {
+  for (int64_t k = 0; k <= nbat; ++k) {
+    const int64_t f0 = k * 64;
+    // Q wave registers kept across the iteration's first barrier
+    double rd = 0.0, far = 0.0;
+    int64_t g = -1;
+    bool q_done = false;
+    // ------------------------------------------------------------ phase 1
+    if (wave == 0 && k < nbat) {
+      const double s = double(sB);
+      const int cls = ps_class(kPolicy, cB, rt.J);
+      g = look(f0, fB);
+      far = farB;
+      const double u = s / rt.c;
+      const double fetch = s / thr[cls];
+      rd = fetch + s / rt.wthr;
+      sB = size_of(kA);
+      cB = cA;
+      fB = fA;
+      farB = far_wait(f0 + 64, look(f0 + 64, fA));
+      load_ids(f0 + 128, kA, cA, fA);
+      PsSlot& sl = slot[k & 1];
+      sl.u[lane] = u;
+      sl.rd[lane] = rd;
+      const bool prev_near = k > 0 && slot[(k - 1) & 1].near != 0;
+      // every lookback in a batch the T wave has finished (k - 2 or before)
+      if (!prev_near && __ballot(g >= f0 - 64) == 0) {
+        const double tg = g >= 0 ? (g >= f0 - kPsRing ? ring[g & (kPsRing - 1)] : far) : 0.0;
+        const double W = g >= 0 ? rt.p0 * tg : 0.0;
+        const int nb = Mi - f0 < 64 ? int(Mi - f0) : 64;
+        double Qb = 0.0;
+        if (nb == 64) {
 #pragma unroll
-        for (int q = 0; q < 64; ++q) {
-          const double Wq = rl_d(W, q);
-          Q = __builtin_fmax(Q, Wq);
-          Q = Q + rl_d(rd, q);
-          Qb = lane == q ? Q : Qb;
-        }
-      } else {
-        for (int q = 0; q < nb; ++q) {
-          const double Wq = rl_d(W, q);
-          Q = __builtin_fmax(Q, Wq);
-          Q = Q + rl_d(rd, q);
-          Qb = lane == q ? Q : Qb;
-        }
-      }
-      const double av = Qb / rt.p0;
-      auto tstep = [&](int q) {
-        double tf = rl_d(av, q);
-        if (f0 + q > 0) {
-          const double a = tprev + uprev;
-          tf = __builtin_fmax(tf, a);
-        }
-        tb = lane == q ? tf : tb;
-        tprev = tf;
-        uprev = rl_d(u, q);
-      };
-      if (nb == 64) {
-#pragma unroll
-        for (int q = 0; q < 64; ++q) tstep(q);
-      } else {
-        for (int q = 0; q < nb; ++q) tstep(q);
-      }
-    } else if (!kStaged && nb == 64) {
-      // a full batch: straight-line steps, so the terms of later steps can
-      // be formed while earlier ones finish
-#pragma unroll
-      for (int q = 0; q < 64; ++q) step(q, 0.0);
-    } else {
-      for (int q = 0; q < nb; ++q) {
-        double Wq = 0.0;
-        if (kStaged) {
-          if ((inb_mask >> q) & 1) {
-            const int gq = __builtin_amdgcn_readlane(int(g - f0), q);
-            Wq = rt.p0 * rl_d(tb, gq);
-          } else {
-            Wq = rl_d(W, q);
+          for (int q = 0; q < 64; ++q) {
+            Q = __builtin_fmax(Q, rl_d(W, q));
+            Q = Q + rl_d(rd, q);
+            Qb = lane == q ? Q : Qb;
+          }
+        } else {
+          for (int q = 0; q < nb; ++q) {
+            Q = __builtin_fmax(Q, rl_d(W, q));
+            Q = Q + rl_d(rd, q);
+            Qb = lane == q ? Q : Qb;
           }
         }
-        step(q, Wq);
+        sl.Qb[lane] = Qb;
+        if (lane == 0) sl.near = 0;
+        q_done = true;
       }
     }
-    const int64_t f = f0 + lane;
-    if (f < Mi) {
-      tr[f] = tb;
-      if (kStaged) ring[f & (kPsRing - 1)] = tb;
+    if (wave == 1 && k >= 1) {
+      const int64_t fb = f0 - 64;
+      const PsSlot& sl = slot[(k - 1) & 1];
+      const int nb = Mi - fb < 64 ? int(Mi - fb) : 64;
+      const double u = sl.u[lane];
+      double tb = -1.0;
+      if (sl.near) {
+        // read by read, from the Q after the batch before
+        double Qs = s_Qend;
+        const double rd_l = sl.rd[lane], W_l = sl.W[lane];
+        const int32_t gq_l = sl.gq[lane];
+        const uint64_t inb = sl.inb;
+        for (int q = 0; q < nb; ++q) {
+          const double Wq = ((inb >> q) & 1) ? rt.p0 * rl_d(tb, __builtin_amdgcn_readlane(gq_l, q) & 63)
+                                             : rl_d(W_l, q);
+          Qs = __builtin_fmax(Qs, Wq);
+          Qs = Qs + rl_d(rd_l, q);
+          double tf = Qs / rt.p0;
+          if (fb + q > 0) tf = __builtin_fmax(tf, tprev + uprev);
+          tb = lane == q ? tf : tb;
+          tprev = tf;
+          uprev = rl_d(u, q);
+        }
+        if (lane == 0) s_Qend = Qs;
+      } else {
+        const double av = sl.Qb[lane] / rt.p0;
+        auto tstep = [&](int q) {
+          double tf = rl_d(av, q);
+          if (fb + q > 0) tf = __builtin_fmax(tf, tprev + uprev);
+          tb = lane == q ? tf : tb;
+          tprev = tf;
+          uprev = rl_d(u, q);
+        };
+        if (nb == 64) {
+#pragma unroll
+          for (int q = 0; q < 64; ++q) tstep(q);
+        } else {
+          for (int q = 0; q < nb; ++q) tstep(q);
+        }
+      }
+      const int64_t f = fb + lane;
+      if (f < Mi) {
+        tr[f] = tb;
+        ring[f & (kPsRing - 1)] = tb;
+      }
     }
+    if (wave == 2 && k < nbat) {
+      const int32_t kk = kN, code = cN;
+      if (f0 + 64 < Mi) io_ids(f0 + 64, kN, cN);
+      const double s = double((kk >= 0 && kk < r.F) ? sizes[kk] : int64_t(0));
+      const int cls = ps_class(kPolicy, code, rt.J);
+      const double fetch = s / thr[cls];
+      const int nb = Mi - f0 < 64 ? int(Mi - f0) : 64;
+      if (kPolicy != kNoPFS && nb == 64) {
+        double a = rl_d(a0, 0);
+#pragma unroll
+        for (int q = 0; q < 64; ++q) a = a + rl_d(fetch, q);
+        a0 = lane == 0 ? a : a0;
+      } else {
+        // lane c carries class c's sum (and class 64 + c's): every step adds
+        // the read's fetch time in its class's lane and 0.0 in the others,
+        // so each class's sum takes its reads in stream order (the sums are
+        // never -0, so adding +0.0 leaves them bit for bit)
+        auto cstep = [&](int q) {
+          const int cq = __builtin_amdgcn_readlane(cls, q);
+          const double fq = rl_d(fetch, q);
+          a0 = a0 + (cq == lane ? fq : 0.0);
+          if (K > 64) a1 = a1 + (cq == lane + 64 ? fq : 0.0);
+        };
+        if (nb == 64) {
+#pragma unroll
+          for (int q = 0; q < 64; ++q) cstep(q);
+        } else {
+          for (int q = 0; q < nb; ++q) cstep(q);
+        }
+      }
+    }
+    __syncthreads();  // A: batch k - 1's t, and a stepped batch's Q, are in
+    // ------------------------------------------------------------ phase 2
+    if (wave == 0 && k < nbat && !q_done) {
+      PsSlot& sl = slot[k & 1];
+      if (k > 0 && slot[(k - 1) & 1].near != 0) Q = s_Qend;
+      const bool inb = g >= f0;
+      const double tg = (g >= 0 && !inb) ? (g >= f0 - kPsRing ? ring[g & (kPsRing - 1)] : far) : 0.0;
+      const double W = (g >= 0 && !inb) ? rt.p0 * tg : 0.0;
+      const uint64_t inb_mask = __ballot(inb);
+      if (inb_mask == 0) {
+        const int nb = Mi - f0 < 64 ? int(Mi - f0) : 64;
+        double Qb = 0.0;
+        for (int q = 0; q < nb; ++q) {
+          Q = __builtin_fmax(Q, rl_d(W, q));
+          Q = Q + rl_d(rd, q);
+          Qb = lane == q ? Q : Qb;
+        }
+        sl.Qb[lane] = Qb;
+        if (lane == 0) sl.near = 0;
+      } else {
+        sl.W[lane] = W;
+        sl.gq[lane] = int32_t(g - f0);
+        if (lane == 0) {
+          sl.inb = inb_mask;
+          sl.near = 1;
+        }
+      }
+    }
+    __syncthreads();  // B: batch k's Q values or its stepping data are in
   }
-  for (int64_t f = Mi + lane; f < M; f += 64) tr[f] = -1.0;
-  if (kPolicy == kPerfect) {  // no fetches (the other policies' second wave writes io)
-    const int K = 1 + 2 * rt.J;
+  if (wave == 1) {
+    for (int64_t f = Mi + lane; f < M; f += 64) tr[f] = -1.0;
+    if (lane == 0) finish[i] = Mi > 0 ? tprev + uprev : 0.0;
+  }
+  if (wave == 2) {
     double* ior = io + i * K;
-    if (lane < K) ior[lane] = 0.0;
-    if (64 + lane < K) ior[64 + lane] = 0.0;
+    if (lane < K) ior[lane] = a0;
+    if (64 + lane < K) ior[64 + lane] = a1;
   }
-  if (lane == 0) finish[i] = Mi > 0 ? tprev + uprev : 0.0;
 }
 
 int policy_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, const int16_t* src,
@@ -366,11 +533,11 @@ int policy_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, co
       return launch("ps_sim_naive", ps_sim<kNaive>, grid, dim3(ps_threads<kNaive>()), 0, st, r, R, sizes, src, fill, rt, t,
                     finish, io);
     case kStaging:
-      return launch("ps_sim_staging", ps_sim<kStaging>, grid, dim3(ps_threads<kStaging>()), 0, st, r, R, sizes, src, fill, rt, t,
-                    finish, io);
+      return launch("ps_sim_staging", ps_staged<kStaging>, grid, dim3(192), 0, st, r, R, sizes, src, fill,
+                    rt, t, finish, io);
     default:
-      return launch("ps_sim_nopfs", ps_sim<kNoPFS>, grid, dim3(ps_threads<kNoPFS>()), 0, st, r, R, sizes, src, fill, rt, t,
-                    finish, io);
+      return launch("ps_sim_nopfs", ps_staged<kNoPFS>, grid, dim3(192), 0, st, r, R, sizes, src, fill,
+                    rt, t, finish, io);
   }
 }
 
