@@ -131,9 +131,10 @@ def committed_traffic(workload, kernel):
 
 
 POLICY_NAMES = ("perfect", "naive", "staging", "nopfs")
-SEQUENTIAL_NOTE = ("sequential per worker (each read depends on every earlier one), one wave "
-                   "per worker: bound by the wave's instruction issue and latency, not by HBM; "
-                   "frac is the HBM fraction for reference")
+SEQUENTIAL_NOTE = ("sequential per worker (each read depends on every earlier one), one "
+                   "workgroup per worker whose waves split the chains: bound by instruction "
+                   "issue and latency on the chain, not by HBM; frac is the HBM fraction for "
+                   "reference")
 
 
 def _kernel_short_name(full):
