@@ -153,7 +153,11 @@ offsets_transpose(SegParams p, const uint16_t* __restrict__ O, uint16_t* __restr
 // sub-chunk, a few reads for uniform shuffles): it loads the run's bounds and
 // then up to kRunLoads of its reads at once, so a tile needs one dependent
 // pair of loads and no workgroup-wide scan before the LDS updates.
-constexpr int kRunLoads = 8;
+#ifndef NOPFS_RUN_LOADS
+#define NOPFS_RUN_LOADS 8
+#endif
+constexpr int kRunLoads = NOPFS_RUN_LOADS;
+static_assert(kRunLoads % 4 == 0, "whole 16-byte loads");
 
 // kCompact (fused planning call): the tile also lists its read cells for the
 // tier plan, entry = the cell's rank-ordered bin << kListOffBits | offset in
@@ -195,6 +199,7 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
   const int64_t k0 = int64_t(kb) * W;
   const int64_t kend = k0 + W < p.F ? k0 + W : p.F;
   const uint32_t* prow = Pk + i * p.M_max;
+  const uint32_t* pk_end = Pk + p.N * p.M_max;
   const int64_t Li = seg_len(p, i);
   const int64_t runs = int64_t(p.E) * p.nsc;
   const uint16_t* oa = OT + (i * (p.nbk + 1) + kb) * runs;  // run starts in window kb
@@ -251,8 +256,22 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
       const uint32_t* src = prow + fb;
       for (uint32_t q = ra; q < rb; q += kRunLoads) {
         uint32_t v[kRunLoads];
+        if (src + q + kRunLoads <= pk_end) {
+          // 16-byte loads (4-byte aligned); the words past the run are
+          // other windows' reads, in bounds, and not used
 #pragma unroll
-        for (int u = 0; u < kRunLoads; ++u) v[u] = q + u < rb ? src[q + u] : 0u;
+          for (int u = 0; u < kRunLoads; u += 4) {
+            uint4 a;
+            __builtin_memcpy(&a, src + q + u, 16);
+            v[u] = a.x;
+            v[u + 1] = a.y;
+            v[u + 2] = a.z;
+            v[u + 3] = a.w;
+          }
+        } else {
+#pragma unroll
+          for (int u = 0; u < kRunLoads; ++u) v[u] = q + u < rb ? src[q + u] : 0u;
+        }
 #pragma unroll
         for (int u = 0; u < kRunLoads; ++u) {
           const uint32_t x = (v[u] >> kScShift) - xoff;
