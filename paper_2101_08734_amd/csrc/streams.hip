@@ -63,6 +63,7 @@ constexpr int kBlkShift = 3;                               // run-table lookup g
 constexpr int kSortCap = NOPFS_SORT_CAP;  // largest bucket sorted in LDS
 constexpr int kItems = kSortCap / kThreads;
 static_assert(kSortCap % kThreads == 0 && kSortCap < 65536, "16-bit digit counts");
+static_assert(kItems % 4 == 0, "the sort loads its words in quads");
 
 struct StreamParams {
   int64_t F, N, B, P, L, M_max;
@@ -431,13 +432,30 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
   const uint32_t lmask = (1u << p.cbits) - 1u;
   const uint32_t* obg = offb + (int64_t(blockIdx.y) * nbw + b) * (nch + 1);
   const bool fast = n <= uint32_t(p.cap);
-  // the words are requested before the run table, so both round trips overlap
+  // Item r of a thread is position item_pos(r): four consecutive positions
+  // per quad, quads kQuad positions apart. The words are requested before
+  // the run table, so both round trips overlap: each quad as one 16-byte
+  // load (4-byte aligned; words past the bucket are not used) where it
+  // stays inside the words of the launch, else word by word.
+  constexpr uint32_t kQuad = 4 * kThreads;
+  auto item_pos = [](int r) { return uint32_t(r >> 2) * kQuad + 4 * threadIdx.x + uint32_t(r & 3); };
   uint32_t kb[kItems], id[kItems];
   if (fast) {
+    const int64_t room = int64_t(gridDim.y - blockIdx.y) * p.F - lo;  // words from gw to the end
 #pragma unroll
-    for (int r = 0; r < kItems; ++r) {
-      const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
-      kb[r] = q < n ? gw[q] : 0u;
+    for (int h = 0; h < kItems / 4; ++h) {
+      const uint32_t q0 = item_pos(4 * h);
+      if (int64_t(q0) + 4 <= room) {
+        uint4 w;
+        __builtin_memcpy(&w, gw + q0, 16);
+        kb[4 * h] = w.x;
+        kb[4 * h + 1] = w.y;
+        kb[4 * h + 2] = w.z;
+        kb[4 * h + 3] = w.w;
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) kb[4 * h + u] = q0 + u < n ? gw[q0 + u] : 0u;
+      }
     }
   }
   for (uint32_t c = threadIdx.x; c <= nch; c += kThreads) ob[c] = obg[c];
@@ -454,16 +472,20 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
       blk[k] = uint16_t(c);
   }
   __syncthreads();
+  // a quad's first position finds its run from the table, the next three
+  // step on from there
 #pragma unroll
-  for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
-    if (q < n) {
-      uint32_t c = blk[q >> kBlkShift];
-      c += ob[c + 1] <= q;  // most positions are at most two runs on
-      c += ob[c + 1] <= q;
-      while (ob[c + 1] <= q) ++c;
-      id[r] = c * p.C + (kb[r] & lmask);
-      kb[r] >>= p.cbits;
+  for (int h = 0; h < kItems / 4; ++h) {
+    const uint32_t q0 = item_pos(4 * h);
+    uint32_t c = q0 < n ? blk[q0 >> kBlkShift] : 0u;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t q = q0 + u;
+      if (q < n) {
+        while (ob[c + 1] <= q) ++c;
+        id[4 * h + u] = c * p.C + (kb[4 * h + u] & lmask);
+        kb[4 * h + u] >>= p.cbits;
+      }
     }
   }
   __syncthreads();  // the run table is no longer needed: its space holds the digit counts
@@ -476,7 +498,7 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
   uint32_t pos[kItems];
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
+    const uint32_t q = item_pos(r);
     if (q < n) {
       const uint32_t d = kb[r] >> dshift;
       const uint32_t half = (d & 1u) * 16u;
@@ -511,7 +533,7 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
   uint32_t* kbs = reinterpret_cast<uint32_t*>(kv);  // [kSortCap + kGroupLoads] by slot
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
+    const uint32_t q = item_pos(r);
     if (q < n) {
       pos[r] += h16[kb[r] >> dshift];
       kbs[pos[r]] = (kb[r] << kSlotBits) | pos[r];
@@ -528,7 +550,7 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
   // rest.
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
+    const uint32_t q = item_pos(r);
     if (q < n) {
       const uint32_t d = kb[r] >> dshift;
       const uint32_t a0 = h16[d];
@@ -551,7 +573,7 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
   if (threadIdx.x == 0) *nruns = 0;
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
-    const uint32_t q = uint32_t(r * kThreads) + threadIdx.x;
+    const uint32_t q = item_pos(r);
     if (q < n) {
       kbp[pos[r]] = kb[r];
       sorted[pos[r]] = id[r];
