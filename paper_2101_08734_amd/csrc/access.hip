@@ -157,6 +157,11 @@ offsets_transpose(SegParams p, const uint16_t* __restrict__ O, uint16_t* __restr
 #define NOPFS_RUN_LOADS 8
 #endif
 constexpr int kRunLoads = NOPFS_RUN_LOADS;
+#ifndef NOPFS_STATS_SPLIT
+#define NOPFS_STATS_SPLIT 4
+#endif
+constexpr int kStatsSplit = NOPFS_STATS_SPLIT;  // most threads per run
+static_assert(kStatsSplit >= 1, "at least one thread per run");
 static_assert(kRunLoads % 4 == 0, "whole 16-byte loads");
 
 // kCompact (fused planning call): the tile also lists its read cells for the
@@ -233,11 +238,20 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     // the compiler from holding them in registers across the pass)
     uint32_t tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
+    // With fewer runs than threads, ns = min(threads / runs, kStatsSplit)
+    // threads share a run, taking turns at groups of kRunLoads reads (a run
+    // of up to ns * kRunLoads reads then needs one round of loads).
+    uint32_t ns = runs < kStatsThreads ? uint32_t(kStatsThreads / runs) : 1u;  // uniform
+    ns = ns < uint32_t(kStatsSplit) ? ns : uint32_t(kStatsSplit);
+    const uint32_t r_first = tid / ns;
+    const uint32_t r_step = kStatsThreads / ns;
+    const uint32_t q_off = (tid - r_first * ns) * kRunLoads;
+    const uint32_t q_step = ns * kRunLoads;
     // bounds of this thread's first run, requested before the LDS is cleared
     uint32_t ra = 0, rb = 0;
-    if (tid < runs) {
-      ra = oa[tid];
-      rb = ob[tid];
+    if (r_first < runs) {
+      ra = oa[r_first];
+      rb = ob[r_first];
     }
     const uint32_t ncl = wlen + sh < uint32_t(kStatsWin) ? wlen + sh : uint32_t(kStatsWin);
     for (uint32_t x = threadIdx.x; x < (ncl + 3) / 4; x += kStatsThreads) cw[x] = 0;
@@ -246,15 +260,15 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     // value returned) before this barrier; every claim comes after it
     if (kCompact && !kVec && w0 == k0) asm volatile("" ::"v"(zold));
     __syncthreads();
-    for (int64_t r = threadIdx.x; r < runs; r += kStatsThreads) {
-      if (r != threadIdx.x) {
+    for (int64_t r = r_first; r < runs; r += r_step) {
+      if (r != r_first) {
         ra = oa[r];
         rb = ob[r];
       }
       const uint32_t e = uint32_t(r) / nsc, sc = uint32_t(r) - e * nsc;
       const int64_t fb = int64_t(e) * Li + int64_t(sc) * kSC;
       const uint32_t* src = prow + fb;
-      for (uint32_t q = ra; q < rb; q += kRunLoads) {
+      for (uint32_t q = ra + q_off; q < rb; q += q_step) {
         uint32_t v[kRunLoads];
         if (src + q + kRunLoads <= pk_end) {
           // 16-byte loads (4-byte aligned); the words past the run are
