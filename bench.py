@@ -139,14 +139,15 @@ SEQUENTIAL_NOTE = ("sequential per worker (each read depends on every earlier on
 
 def _kernel_short_name(full):
     """'ns::(anonymous namespace)::plan_hist<true>(args...)' -> 'plan_hist';
-    the policy kernel keeps its policy: 'ps_sim<2>(...)' -> 'ps_sim_staging', and
+    the policy kernels keep their policy: 'ps_sim<1>(...)' -> 'ps_sim_naive',
+    'ps_staged<2>(...)' -> 'ps_sim_staging' (the names the library launches them by), and
     the staging schedule's 8-byte-size unpartition its launch name 'st_unpart8'."""
     import re
     m = re.findall(r"(\w+)(?:<([^>()]*)>)?\(", full)
     if not m:
         return full
     name, targ = m[-1]
-    if name == "ps_sim" and targ.strip().isdigit() and int(targ) < len(POLICY_NAMES):
+    if name in ("ps_sim", "ps_staged") and targ.strip().isdigit() and int(targ) < len(POLICY_NAMES):
         return f"ps_sim_{POLICY_NAMES[int(targ)]}"
     if name == "st_unpart" and targ.strip() == "true":  # the 8-byte-size form, launched as such
         return "st_unpart8"
