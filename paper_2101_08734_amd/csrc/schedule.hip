@@ -516,9 +516,8 @@ __device__ __forceinline__ int64_t span_len(const SegParams& p, int64_t i, int64
 
 template <bool kWide>
 __device__ __forceinline__ void span_load(const SegParams& p, const uint32_t* __restrict__ Pk,
-                                          const int64_t* __restrict__ zS,
-                                          const uint32_t* __restrict__ zc, int64_t b, int64_t nblk,
-                                          SpanRegs& g) {
+                                          const int64_t* zS, const uint32_t* zc, int64_t b,
+                                          int64_t nblk, SpanRegs& g) {
   int64_t len = 0, base = 0;
   if (b < nblk) {
     const int64_t i = b / p.nsc, c = b - i * p.nsc;
@@ -534,9 +533,13 @@ __device__ __forceinline__ void span_load(const SegParams& p, const uint32_t* __
   }
 }
 
-// In place, per span c of row i: zS holds the span's sizes in partitioned
-// order on entry and S on exit, S[h] = sum of the sizes at positions
-// (h >> 14 << 14) .. h; ctot[i][c] = the span's total. The sizes go back to
+// Per span c of row i: S[h] = sum of the sizes at positions
+// (h >> 14 << 14) .. h, and ctot[i][c] = the span's total. The sizes come
+// in partitioned order (zS, 8-byte, or zc, 4-byte); with 4-byte sizes, a
+// span whose total is below 2^32 writes S as 4-byte values into zc (in
+// place of its sizes, which the workgroup holds in registers by then) and
+// marks sw[b] = 0; any other span writes S as 8-byte values into zS (in
+// place for 8-byte sizes) and marks sw[b] = 1. The sizes go back to
 // stream order in LDS (each read's partitioned entry carries its position),
 // then wave w sums its 1024 consecutive positions, takes the totals of the
 // waves before it as its carry and scans them as 16 rows of 64 lanes in
@@ -551,7 +554,7 @@ __device__ __forceinline__ void span_load(const SegParams& p, const uint32_t* __
 template <bool kWide>
 __global__ void __launch_bounds__(kUThreads)
 st_unpart(SegParams p, const uint32_t* __restrict__ Pk, const uint32_t* __restrict__ wide,
-          const uint32_t* __restrict__ zc, int64_t* __restrict__ zS, int64_t* __restrict__ ctot,
+          uint32_t* zc, int64_t* zS, int64_t* __restrict__ ctot, uint8_t* __restrict__ sw,
           int64_t nblk) {
   __shared__ int64_t sv[kSC];
   __shared__ uint64_t wtot[kUWaves];
@@ -579,18 +582,28 @@ st_unpart(SegParams p, const uint32_t* __restrict__ Pk, const uint32_t* __restri
     __syncthreads();
     uint64_t carry = 0;
     for (uint32_t w = 0; w < wave; ++w) carry += wtot[w];
+    auto span_total = [&]() {
+      uint64_t t = 0;
+      for (int w = 0; w < kUWaves; ++w) t += wtot[w];
+      return read_lane64(t, 0);  // the same in every lane: held once per wave
+    };
+    bool s64 = true;  // uniform
+    if constexpr (!kWide) s64 = span_total() >= (uint64_t(1) << 32);
     int64_t* row = zS + i * p.M_max + (c << kScShift);
+    uint32_t* row32 = zc + i * p.M_max + (c << kScShift);
 #pragma unroll 4
     for (int u = 0; u < kURows; ++u) {
       const bool in = q0 + u * 64 < len;
       const uint64_t v = wave_inclusive_scan64(in ? uint64_t(sv[q0 + u * 64]) : 0ull) + carry;
-      if (in) stream_store(row + q0 + u * 64, int64_t(v));
+      if (in) {
+        if (s64) stream_store(row + q0 + u * 64, int64_t(v));
+        else stream_store(row32 + q0 + u * 64, uint32_t(v));
+      }
       carry = read_lane64(v, 63);
     }
     if (threadIdx.x == 0) {
-      uint64_t t = 0;
-      for (int w = 0; w < kUWaves; ++w) t += wtot[w];
-      ctot[b] = int64_t(t);
+      ctot[b] = int64_t(span_total());
+      sw[b] = s64 ? 1 : 0;
     }
     __syncthreads();  // sv and wtot are rewritten for the next span
   }
@@ -612,13 +625,26 @@ st_base(uint32_t nch, int64_t* __restrict__ ctot) {
   }
 }
 
+// The span prefix sums (4-byte S32 or 8-byte S by span, as st_unpart
+// marked them in sw).
+struct SpanSums {
+  const int64_t* S;
+  const uint32_t* S32;
+  const uint8_t* sw;  // per span of a row
+};
+
 // Prefix sums along row i of R: at(x) = sum of the sizes at positions 0..x.
 struct Prefix {
   const int64_t* S;     // row i of S (prefix sums local to each span)
+  const uint32_t* S32;  // row i of S32
+  const uint8_t* sw;    // row i of the span marks
   const int64_t* base;  // row i of the span bases
   __device__ __forceinline__ int64_t at(int64_t x) const {
     if (x < 0) return 0;
-    return int64_t(uint64_t(base[x >> kScShift]) + uint64_t(S[x]));
+    const int64_t c = x >> kScShift;
+    const uint32_t lo = S32[x];  // requested with the mark; the 8-byte value only if marked
+    const uint64_t v = sw[c] ? uint64_t(S[x]) : uint64_t(lo);
+    return int64_t(uint64_t(base[c]) + v);
   }
   // smallest g in [-1, h] with at(g) >= target (h qualifies when target <= at(h))
   __device__ int64_t lower_bound(int64_t h, int64_t target) const {
@@ -633,9 +659,11 @@ struct Prefix {
 };
 
 __device__ __forceinline__ Prefix row_prefix(const SegParams& p, int64_t i, uint32_t nch,
-                                             const int64_t* S, const int64_t* base) {
+                                             const SpanSums& ss, const int64_t* base) {
   Prefix P;
-  P.S = S + i * p.M_max;
+  P.S = ss.S + i * p.M_max;
+  P.S32 = ss.S32 + i * p.M_max;
+  P.sw = ss.sw + i * int64_t(nch);
   P.base = base + i * int64_t(nch);
   return P;
 }
@@ -678,7 +706,7 @@ __device__ __forceinline__ FillPart fill_part(const SegParams& p, uint32_t nch, 
 
 // bnd[b] = (g of the part's first position, g of its last position, 0, 0).
 __global__ void __launch_bounds__(256)
-st_bounds(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __restrict__ S,
+st_bounds(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, SpanSums S,
           const int64_t* __restrict__ base, int4* __restrict__ bnd) {
   const int64_t b = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (b >= nparts) return;
@@ -695,7 +723,7 @@ st_bounds(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* 
 }
 
 __global__ void __launch_bounds__(kStThreads) __attribute__((amdgpu_waves_per_eu(8)))
-st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __restrict__ S,
+st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, SpanSums S,
         const int64_t* __restrict__ base, const int4* __restrict__ bnd, int32_t gcap,
         int32_t* __restrict__ fill) {
   // the staged g values, then (after a barrier) the results for the transpose
@@ -712,19 +740,39 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
       out[h] = -1;
   }
   if (f.hl == 0) return;
-  const int64_t* Srow = S + f.i * p.M_max;
+  const int64_t* Srow = S.S + f.i * p.M_max;
+  const uint32_t* S32row = S.S32 + f.i * p.M_max;
+  const uint8_t* swrow = S.sw + f.i * int64_t(nch);
   const int64_t* brow = base + f.i * int64_t(nch);
   // the part's g range first: the staging loads below wait for it
   const int4 bb = bnd[b];
   const int64_t hbase = brow[f.c];  // every position of the part is in span c
-  // this thread's positions: prefix sums within span c
+  const bool wc = swrow[f.c] != 0;  // uniform
+  // this thread's positions: prefix sums within span c (the 4-byte values
+  // requested with the span's mark; the 8-byte ones only for a marked span)
   const int32_t ht0 = int32_t(threadIdx.x) * kStPer;  // offset in the part
   const int32_t hl = int32_t(f.hl);
-  const int64_t* Spart = Srow + f.h0;
   int64_t sh[kStPer];
+  static_assert(kStPer % 4 == 0, "whole 16-byte loads");
+  if (ht0 + kStPer <= hl) {  // 16-byte loads (4-byte aligned)
 #pragma unroll
-  for (int u = 0; u < kStPer; ++u)  // unconditional: past the part's end, its last position
-    sh[u] = Spart[ht0 + u < hl ? ht0 + u : hl - 1];
+    for (int u = 0; u < kStPer; u += 4) {
+      uint4 w;
+      __builtin_memcpy(&w, S32row + f.h0 + ht0 + u, 16);
+      sh[u] = w.x;
+      sh[u + 1] = w.y;
+      sh[u + 2] = w.z;
+      sh[u + 3] = w.w;
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < kStPer; ++u)  // unconditional: past the part's end, its last position
+      sh[u] = int64_t(S32row[f.h0 + (ht0 + u < hl ? ht0 + u : hl - 1)]);
+  }
+  if (wc) {
+#pragma unroll
+    for (int u = 0; u < kStPer; ++u) sh[u] = Srow[f.h0 + (ht0 + u < hl ? ht0 + u : hl - 1)];
+  }
   // S(h) - d0 = (hbase - d0) + sh: sizes are >= 1, so no term saturates
   // (other sizes only need in-bounds results, which the index bounds give)
   const uint64_t hd = uint64_t(hbase) - uint64_t(d0);
@@ -735,15 +783,17 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
     // every load of the range at once (clamped to g >= 0); the range spans
     // at most two spans, whose bases are loaded once
     const int64_t sA = (glo > 0 ? glo : 0) >> kScShift;
+    const int64_t sB = sA + 1 < int64_t(nch) ? sA + 1 : sA;
     const int64_t bA = brow[sA];
-    const int64_t bB = brow[sA + 1 < int64_t(nch) ? sA + 1 : sA];
+    const int64_t bB = brow[sB];
+    const bool wA = swrow[sA] != 0, wB = swrow[sB] != 0;
     // positions and g values fit 32 bits (rows are int32-indexed)
     const int32_t g0 = int32_t(glo), lg = int32_t(Lg);
-    int64_t gv[kGPerT];
+    uint32_t gv[kGPerT];
 #pragma unroll
     for (int u = 0; u < kGPerT; ++u) {
       const int32_t x = u * kStThreads + int32_t(threadIdx.x);
-      gv[u] = Srow[x < lg && g0 + x > 0 ? g0 + x : 0];
+      gv[u] = S32row[x < lg && g0 + x > 0 ? g0 + x : 0];
     }
 #pragma unroll
     for (int u = 0; u < kGPerT; ++u) {
@@ -752,10 +802,22 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
       if (x < lg)
         gS[x] = g >= 0 ? int64_t(uint64_t((g >> kScShift) == sA ? bA : bB) + uint64_t(gv[u])) : 0;
     }
+    if (wA || wB) {  // a span marked 8-byte (uniform; not at the workloads here)
+#pragma unroll 1
+      for (int u = 0; u < kGPerT; ++u) {
+        const int32_t x = u * kStThreads + int32_t(threadIdx.x);
+        const int32_t g = g0 + x;
+        const bool inA = (g >> kScShift) == sA;
+        if (x < lg && g >= 0 && (inA ? wA : wB))
+          gS[x] = int64_t(uint64_t(inA ? bA : bB) + uint64_t(Srow[g]));
+      }
+    }
   }
   __syncthreads();
   int32_t res[kStPer];
   if (staged) {
+    // the staged range is read by every thread: the results wait for the
+    // barrier below before they overwrite it
     // 32-bit indices into the staged range; only the sums are 64-bit
     const int32_t g0 = int32_t(glo), lg = int32_t(Lg);
     const int32_t hb = int32_t(f.h0) + ht0;
@@ -783,29 +845,30 @@ st_fill(SegParams p, int64_t d0, uint32_t nch, int64_t nparts, const int64_t* __
       }
     }
   } else {
-    // g range too wide for LDS (or not monotone): search the row itself
+    // g range too wide for LDS (or not monotone): search the row itself,
+    // one position at a time (rare: a loop, not unrolled), the results
+    // straight into the transpose (nothing reads the staged range here)
     const Prefix P = row_prefix(p, f.i, nch, S, base);
     int64_t x = 0;
-    bool started = false;
-#pragma unroll
+#pragma unroll 1
     for (int u = 0; u < kStPer; ++u) {
       const int64_t h = f.h0 + ht0 + u;
-      res[u] = -1;
+      int32_t r = -1;
       if (ht0 + u < f.hl) {
-        const int64_t target = sub_sat(int64_t(uint64_t(hbase) + uint64_t(sh[u])), d0);
-        if (!started) {
-          x = P.lower_bound(h, target);
-          started = true;
-        }
+        const int64_t target = sub_sat(P.at(h), d0);
+        if (u == 0) x = P.lower_bound(h, target);
         while (x < h && P.at(x) < target) ++x;
         const int64_t fv = x + 1 < h ? x + 1 : h;
-        res[u] = int32_t(fv > 0 ? fv : 0);
+        r = int32_t(fv > 0 ? fv : 0);
       }
+      fo[lds_slot(threadIdx.x * kStPer + u)] = r;
     }
   }
   __syncthreads();
+  if (staged) {
 #pragma unroll
-  for (int u = 0; u < kStPer; ++u) fo[lds_slot(threadIdx.x * kStPer + u)] = res[u];
+    for (int u = 0; u < kStPer; ++u) fo[lds_slot(threadIdx.x * kStPer + u)] = res[u];
+  }
   __syncthreads();
 #pragma unroll
   for (int u = 0; u < kStPer; ++u) {
@@ -884,6 +947,7 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
   uint32_t *Pk, *zc, *wide;
   uint16_t* OT;
   int64_t *S, *ctot;
+  uint8_t* sw;
   int4* bnd;
   if ((rc = scr.alloc_n(&wide, 1))) return rc;
   if ((rc = launch("st_flag", st_flag, dim3(1), dim3(1), 0, st, wide))) return rc;
@@ -894,6 +958,7 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
   if ((rc = scr.alloc_n(&S, size_t(s.N * s.M_max)))) return rc;
   if ((rc = scr.alloc_n(&zc, size_t(s.N * s.M_max)))) return rc;
   if ((rc = scr.alloc_n(&ctot, size_t(nblk)))) return rc;
+  if ((rc = scr.alloc_n(&sw, size_t(nblk)))) return rc;
   if ((rc = scr.alloc_n(&bnd, size_t(nparts)))) return rc;
   if ((rc = launch("st_gather", st_gather, dim3(xcd_padded(uint32_t(ntiles))), dim3(kGThreads), 0,
                    st, p, (const uint32_t*)Pk, (const uint16_t*)OT, sizes, (const uint32_t*)wide, zc,
@@ -901,19 +966,19 @@ int staging_impl(const nopfs_job* job, const int32_t* R, const int64_t* sizes, i
     return rc;
   const int64_t ugrid = nblk < 1024 ? nblk : 1024;
   if ((rc = launch("st_unpart", st_unpart<false>, dim3(uint32_t(ugrid)), dim3(kUThreads), 0, st, p,
-                   (const uint32_t*)Pk, (const uint32_t*)wide, (const uint32_t*)zc, S, ctot, nblk)))
+                   (const uint32_t*)Pk, (const uint32_t*)wide, zc, S, ctot, sw, nblk)))
     return rc;
   if ((rc = launch("st_unpart8", st_unpart<true>, dim3(uint32_t(ugrid)), dim3(kUThreads), 0, st, p,
-                   (const uint32_t*)Pk, (const uint32_t*)wide, (const uint32_t*)zc, S, ctot, nblk)))
+                   (const uint32_t*)Pk, (const uint32_t*)wide, zc, S, ctot, sw, nblk)))
     return rc;
   if ((rc = launch("st_base", st_base, dim3(uint32_t(s.N)), dim3(1024), 0, st, nch, ctot))) return rc;
+  const SpanSums ss{S, zc, sw};
   if ((rc = launch("st_bounds", st_bounds, dim3(uint32_t(ceil_div(nparts, 256))), dim3(256), 0, st,
-                   p, d0, nch, nparts, (const int64_t*)S, (const int64_t*)ctot, bnd)))
+                   p, d0, nch, nparts, ss, (const int64_t*)ctot, bnd)))
     return rc;
   const int32_t gcap = (debug_value(4) > 0 && debug_value(4) < kGCap) ? int32_t(debug_value(4)) : kGCap;
   return launch("st_fill", st_fill, dim3(xcd_padded(uint32_t(nparts))), dim3(kStThreads), 0, st, p,
-                d0, nch, nparts, (const int64_t*)S, (const int64_t*)ctot, (const int4*)bnd, gcap,
-                fill);
+                d0, nch, nparts, ss, (const int64_t*)ctot, (const int4*)bnd, gcap, fill);
 }
 
 }  // namespace

@@ -178,6 +178,35 @@ def test_staging_sizes_beyond_32_bits(oracle, frac):
         _equal(f"fill d0={d0}", fill, oracle.staging_schedule(rjob, R, sizes, d0))
 
 
+def test_staging_span_sums_of_both_widths(oracle):
+    """Sizes around 2^32 / 2^14 bytes: within one row, some spans of 16,384
+    positions hold 2^32 bytes or more (their prefix sums are kept as 8-byte
+    values) and others less (4-byte values). Buffers larger than a span's
+    bytes make windows that reach across spans of both kinds; the staged
+    search and the global-memory search must both agree with the oracle."""
+    F, E, N, B, d, seed = 30_000, 10, 4, 8, 0, 27
+    rng = np.random.default_rng(11)
+    sizes = rng.integers(229_500, 294_500, F).astype(np.int64)
+    rjob = oracle.make_job(F, E, N, B, d, seed)
+    R = oracle.access_streams(rjob)
+    job = nopfs.Job(F, E, N, B, d, seed)
+    _, M, Mw = nopfs.stream_shape(job)
+    kinds = set()
+    for i in range(N):
+        for c in range(Mw[i] // 16384):
+            kinds.add(int(sizes[R[i, c * 16384:(c + 1) * 16384]].sum()) >= 1 << 32)
+    assert kinds == {False, True}, "the sizes must give spans of both widths"
+    try:
+        for gcap in (0, 64):
+            nopfs.debug_set(4, gcap)
+            for d0 in (0, 1_000_000_000, 5_000_000_000, 1 << 32, 12_000_000_000):
+                fill = nopfs.staging_schedule(job, _dev(R), _dev(sizes), d0)
+                torch.cuda.synchronize()
+                _equal(f"fill gcap={gcap} d0={d0}", fill, oracle.staging_schedule(rjob, R, sizes, d0))
+    finally:
+        nopfs.debug_set(4, 0)
+
+
 def test_equal_sizes_closed_form(oracle):
     """Equal sizes s and a buffer of m*s bytes: fill(h) = max(0, h - m + 1)."""
     F, E, N, B = 50_000, 3, 4, 8
