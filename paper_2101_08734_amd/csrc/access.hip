@@ -195,7 +195,10 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
            const ClassTable* __restrict__ classes) {
   extern __shared__ uint32_t sm[];
   uint32_t* cw = sm;                                             // byte counters
-  int32_t* fi = reinterpret_cast<int32_t*>(sm + kStatsCwWords);  // first reads
+  // first reads, kept as unsigned values from an initial 0xFFFFFFFF: the
+  // unsigned minimum of a cell's reads (positions below 2^31), and -1 as an
+  // int32 for a cell nobody reads, which is the table's own value for it
+  uint32_t* fi = sm + kStatsCwWords;
   const uint32_t tile = xcd_logical(blockIdx.x, gridDim.x);
   if (tile >= ntiles) return;
   const int64_t i = tile / p.nbk;
@@ -255,7 +258,7 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     }
     const uint32_t ncl = wlen + sh < uint32_t(kStatsWin) ? wlen + sh : uint32_t(kStatsWin);
     for (uint32_t x = threadIdx.x; x < (ncl + 3) / 4; x += kStatsThreads) cw[x] = 0;
-    for (uint32_t x = threadIdx.x; x < ncl; x += kStatsThreads) fi[x] = INT_MAX;
+    for (uint32_t x = threadIdx.x; x < ncl; x += kStatsThreads) fi[x] = 0xFFFFFFFFu;
     // kCompact: the zeroing of the entry count has been performed (its old
     // value returned) before this barrier; every claim comes after it
     if (kCompact && !kVec && w0 == k0) asm volatile("" ::"v"(zold));
@@ -292,7 +295,7 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
           if (q + u < rb && x < wlen) {
             const uint32_t px = (x + sh) & kStatsPosMask;
             atomicAdd(&cw[px >> 2], 1u << ((px & 3u) * 8u));
-            atomicMin(&fi[px], int32_t(fb + (v[u] & kJMask)));
+            atomicMin(&fi[px], uint32_t(fb + (v[u] & kJMask)));
           }
         }
       }
@@ -325,7 +328,7 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
     auto cell = [&](uint32_t x, uint32_t& c, int32_t& f) {
       const uint32_t px = (x + sh) & kStatsPosMask;
       c = (cw[px >> 2] >> ((px & 3u) * 8u)) & 0xFFu;
-      f = c ? fi[px] : -1;
+      f = int32_t(fi[px]);  // -1 exactly when c == 0
     };
     uint32_t c1 = 0, c2 = 0;
     int32_t f1 = -1, f2 = -1;
@@ -359,12 +362,12 @@ stats_tile(SegParams p, const uint32_t* __restrict__ Pk, const uint16_t* __restr
       if (u < nunits) {
         const uint32_t px = (x + sh) & kStatsPosMask;  // no group wraps
         const uint32_t word = cw[px >> 2];
-        const int4 fq = *reinterpret_cast<const int4*>(&fi[px]);
         cwr[m] = word;
-        frr[m] = make_int4((word & 0xFFu) ? fq.x : -1, (word & 0xFF00u) ? fq.y : -1,
-                           (word & 0xFF0000u) ? fq.z : -1, (word >> 24) ? fq.w : -1);
-        nmine += ((word & 0xFFu) != 0) + ((word & 0xFF00u) != 0) + ((word & 0xFF0000u) != 0) +
-                 ((word >> 24) != 0);
+        frr[m] = *reinterpret_cast<const int4*>(&fi[px]);  // -1 for unread cells already
+        // nonzero counts among the word's four bytes: a byte's high bit in
+        // ((w & 0x7F..) + 0x7F..) | w is set exactly when the byte is nonzero
+        const uint32_t nz = ((word & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | word;
+        nmine += __popc(nz & 0x80808080u);
       }
     }
     // list: the waves' read cells go in wave order, each wave's as one run
