@@ -673,7 +673,7 @@ struct CompactArgs {
   uint32_t wps;  // windows per slice of kSliceCells samples
 };
 #ifndef NOPFS_HIST_CU
-#define NOPFS_HIST_CU 4
+#define NOPFS_HIST_CU 6
 #endif
 constexpr int kHistCU = NOPFS_HIST_CU;  // list entries per lane in flight
 

@@ -529,7 +529,10 @@ stream_sort(StreamParams p, const uint32_t* __restrict__ wst, const uint32_t* __
   // Each counting-sort slot holds kb << kSlotBits | slot: one comparison
   // orders two entries by (kb, slot), and an entry of a later digit group
   // compares above every entry of an earlier one.
-  constexpr uint32_t kGroupLoads = 4;
+#ifndef NOPFS_SORT_GROUP_LOADS
+#define NOPFS_SORT_GROUP_LOADS 4
+#endif
+  constexpr uint32_t kGroupLoads = NOPFS_SORT_GROUP_LOADS;
   uint32_t* kbs = reinterpret_cast<uint32_t*>(kv);  // [kSortCap + kGroupLoads] by slot
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
